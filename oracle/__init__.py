@@ -1,0 +1,93 @@
+"""CPU oracle for integer GEMM C += A.B -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package. The GPU library does not depend on it
+and must never fall back to it.
+
+The arithmetic lives in ``igemm_oracle.c`` (plain int64 triple loop, reduced
+modulo 2^32 at the end; Sec. 4.1 definition of C += A B). This module only
+marshals numpy arrays into that library with ctypes.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_build.LIB):
+        _build.build()
+    lib = ctypes.CDLL(_build.LIB)
+    i64 = ctypes.c_int64
+    vp = ctypes.c_void_p
+    for name in ("oracle_igemm_i16", "oracle_igemm_i8"):
+        fn = getattr(lib, name)
+        fn.argtypes = [i64, i64, i64, vp, i64, vp, i64, vp, i64]
+        fn.restype = ctypes.c_int
+    lib.oracle_num_threads.argtypes = []
+    lib.oracle_num_threads.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def num_threads() -> int:
+    """Threads the oracle's OpenMP loop uses."""
+    return int(_load().oracle_num_threads())
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _ld(a: np.ndarray, what: str) -> int:
+    if a.ndim != 2:
+        raise ValueError(f"{what} must be 2-D")
+    if a.size == 0:
+        return max(a.shape[1], 1)
+    if a.shape[1] > 1 and a.strides[1] != a.itemsize:
+        raise ValueError(f"{what} must have unit stride along its rows")
+    if a.shape[0] == 1:
+        return max(a.shape[1], 1)
+    return a.strides[0] // a.itemsize
+
+
+def igemm_raw(dtype: str, m: int, n: int, k: int, A, lda: int, B, ldb: int,
+              C, ldc: int) -> int:
+    """Call the oracle on raw buffers (numpy arrays used for their memory).
+
+    ``C`` is updated in place. Returns the oracle's status (0 = OK).
+    """
+    lib = _load()
+    fn = lib.oracle_igemm_i16 if dtype == "i16" else lib.oracle_igemm_i8
+    return int(fn(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc))
+
+
+def igemm(A: np.ndarray, B: np.ndarray, C: np.ndarray) -> np.ndarray:
+    """C += A.B (mod 2^32) in place on numpy views; returns C.
+
+    A (m x k) and B (k x n) are int16 or int8 (same type); C is int32 m x n.
+    Views with a row stride larger than their width are allowed; elements
+    outside the views are not touched.
+    """
+    if A.dtype != B.dtype or A.dtype not in (np.int16, np.int8):
+        raise TypeError("A and B must both be int16 or both int8")
+    if C.dtype != np.int32:
+        raise TypeError("C must be int32")
+    m, k = A.shape
+    k2, n = B.shape
+    if k2 != k or C.shape != (m, n):
+        raise ValueError("shape mismatch")
+    dtype = "i16" if A.dtype == np.int16 else "i8"
+    st = igemm_raw(dtype, m, n, k, A, _ld(A, "A"), B, _ld(B, "B"), C, _ld(C, "C"))
+    if st != 0:
+        raise RuntimeError(f"oracle returned {st}")
+    return C

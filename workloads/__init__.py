@@ -1,0 +1,203 @@
+"""Seeded synthetic inputs for integer GEMM C += A.B.
+
+This module only draws numbers. It holds none of the GEMM arithmetic, so the
+CPU oracle (under ``oracle/``) and the GPU path can both take their inputs
+from here without sharing any of the method.
+
+Workloads (all row-major, C is int32):
+
+* ``i16_256``      int16 m=n=k=256, A,B uniform over the full int16 range,
+                   C zero, seed 0.
+* ``i16_4096``     int16 m=n=k=4096, A,B uniform over the full range,
+                   C uniform in [-2^20, 2^20], seed 1.
+* ``i8_8192``      int8 m=n=k=8192, A,B uniform in [-128,127], C zero, seed 2.
+* ``i16_conv``     six int16 GEMMs shaped like the im2row lowering of the
+                   convolutions of a 50-layer residual CNN at batch 1 on a
+                   224x224 input (m = output pixels, n = output channels,
+                   k = input channels x kernel window; the lowering of a
+                   convolution to one GEMM is Sec. 4.2). A uniform in [0,255]
+                   (activations), B = rint(normal(0,32)) clipped to int16
+                   (weights), C zero; layer i uses seed 40+i.
+* ``i8_skinny``    six int8 GEMMs shaped like the projections of a 7B-class
+                   decoder at small batch (one large dimension and two small
+                   ones, Sec. 2 and Sec. 4.2): m in {1,8,32} with (n,k) in
+                   {(4096,4096), (11008,4096)}; A uniform in [-128,127],
+                   B = rint(normal(0,20)) clipped to [-128,127], C zero;
+                   shape i uses seed 50+i.
+
+Conventions: numpy ``default_rng(seed)`` (PCG64); draws in the order A, B, C;
+uniform integer ranges include both ends; "normal clipped" rounds with
+``rint`` (ties to even) and then clips. No dataset, image or trained weight
+is involved: every tensor is i.i.d. synthetic with the stated distribution.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Optional, Tuple
+
+import numpy as np
+
+I16_MIN, I16_MAX = -32768, 32767
+I8_MIN, I8_MAX = -128, 127
+
+
+@dataclass(frozen=True)
+class Dist:
+    """A value distribution for one operand."""
+
+    kind: str  # "uniform" | "normal_clip" | "zero"
+    lo: int = 0
+    hi: int = 0
+    sigma: float = 0.0
+
+
+@dataclass(frozen=True)
+class Case:
+    """One GEMM problem: shape, operand type and value distributions."""
+
+    name: str
+    dtype: str  # "i16" | "i8"
+    m: int
+    n: int
+    k: int
+    a: Dist
+    b: Dist
+    c: Dist
+    seed: int
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    cases: Tuple[Case, ...]
+    description: str = ""
+
+
+def _np_dtype(dtype: str):
+    if dtype == "i16":
+        return np.int16
+    if dtype == "i8":
+        return np.int8
+    raise ValueError(f"unknown operand dtype {dtype!r}")
+
+
+def draw(rng: np.random.Generator, dist: Dist, shape, dtype) -> np.ndarray:
+    """Draw one operand. ``dtype`` is the numpy storage type."""
+    if dist.kind == "zero":
+        return np.zeros(shape, dtype=dtype)
+    if dist.kind == "uniform":
+        return rng.integers(dist.lo, dist.hi, size=shape, dtype=dtype, endpoint=True)
+    if dist.kind == "normal_clip":
+        x = np.rint(rng.normal(0.0, dist.sigma, size=shape))
+        return np.clip(x, dist.lo, dist.hi).astype(dtype)
+    raise ValueError(f"unknown distribution {dist.kind!r}")
+
+
+def generate(case: Case, seed: Optional[int] = None):
+    """Return (A, B, C0) as C-contiguous numpy arrays for ``case``.
+
+    A is m x k and B is k x n in the case's operand type; C0 is m x n int32.
+    """
+    rng = np.random.default_rng(case.seed if seed is None else seed)
+    et = _np_dtype(case.dtype)
+    A = draw(rng, case.a, (case.m, case.k), et)
+    B = draw(rng, case.b, (case.k, case.n), et)
+    C = draw(rng, case.c, (case.m, case.n), np.int32)
+    return A, B, C
+
+
+def random_operands(dtype: str, m: int, n: int, k: int, seed: int,
+                    c_range: int = 1 << 20, lda: Optional[int] = None,
+                    ldb: Optional[int] = None, ldc: Optional[int] = None):
+    """Full-range random operands with optional padded leading dimensions.
+
+    Returns (A, B, C) where each is a 2-D array whose row length is the
+    leading dimension (>= the logical width); padding is filled with values
+    from the same distribution so an out-of-bounds read changes the result
+    and an out-of-bounds write is visible.
+    """
+    et = _np_dtype(dtype)
+    lo, hi = (I16_MIN, I16_MAX) if dtype == "i16" else (I8_MIN, I8_MAX)
+    lda = k if lda is None else lda
+    ldb = n if ldb is None else ldb
+    ldc = n if ldc is None else ldc
+    rng = np.random.default_rng(seed)
+    A = rng.integers(lo, hi, size=(m, max(lda, 1)), dtype=et, endpoint=True)
+    B = rng.integers(lo, hi, size=(k, max(ldb, 1)), dtype=et, endpoint=True)
+    C = rng.integers(-c_range, c_range, size=(m, max(ldc, 1)), dtype=np.int32,
+                     endpoint=True)
+    return A, B, C
+
+
+_U16 = Dist("uniform", I16_MIN, I16_MAX)
+_U8 = Dist("uniform", I8_MIN, I8_MAX)
+_ZERO = Dist("zero")
+
+CONV_SHAPES = (
+    (12544, 64, 147),
+    (3136, 64, 576),
+    (3136, 256, 64),
+    (784, 128, 1152),
+    (196, 256, 2304),
+    (49, 512, 4608),
+)
+
+SKINNY_SHAPES = (
+    (1, 4096, 4096),
+    (8, 4096, 4096),
+    (32, 4096, 4096),
+    (1, 11008, 4096),
+    (8, 11008, 4096),
+    (32, 11008, 4096),
+)
+
+WORKLOADS = {
+    "i16_256": Workload(
+        "i16_256",
+        (Case("i16_256", "i16", 256, 256, 256, _U16, _U16, _ZERO, 0),),
+        "int16 C+=A.B, m=n=k=256, full-range operands, C zero",
+    ),
+    "i16_4096": Workload(
+        "i16_4096",
+        (Case("i16_4096", "i16", 4096, 4096, 4096, _U16, _U16,
+              Dist("uniform", -(1 << 20), 1 << 20), 1),),
+        "int16 C+=A.B, m=n=k=4096, full-range operands, C uniform in +-2^20",
+    ),
+    "i8_8192": Workload(
+        "i8_8192",
+        (Case("i8_8192", "i8", 8192, 8192, 8192, _U8, _U8, _ZERO, 2),),
+        "int8 C+=A.B, m=n=k=8192, full-range operands, C zero",
+    ),
+    "i16_conv": Workload(
+        "i16_conv",
+        tuple(
+            Case(f"i16_conv_{i}_{m}x{n}x{k}", "i16", m, n, k,
+                 Dist("uniform", 0, 255),
+                 Dist("normal_clip", I16_MIN, I16_MAX, 32.0), _ZERO, 40 + i)
+            for i, (m, n, k) in enumerate(CONV_SHAPES)
+        ),
+        "int16 GEMMs shaped like a 50-layer residual CNN's im2row convolutions",
+    ),
+    "i8_skinny": Workload(
+        "i8_skinny",
+        tuple(
+            Case(f"i8_skinny_{i}_{m}x{n}x{k}", "i8", m, n, k, _U8,
+                 Dist("normal_clip", I8_MIN, I8_MAX, 20.0), _ZERO, 50 + i)
+            for i, (m, n, k) in enumerate(SKINNY_SHAPES)
+        ),
+        "int8 skinny GEMMs shaped like 7B-class decoder projections",
+    ),
+}
+
+ORDER: List[str] = ["i16_256", "i16_4096", "i8_8192", "i16_conv", "i8_skinny"]
+
+
+def ops(case: Case) -> int:
+    """Arithmetic operations of one GEMM, counting a multiply-add as two."""
+    return 2 * case.m * case.n * case.k
+
+
+def algorithmic_bytes(case: Case) -> int:
+    """A and B read once, C read and written once as int32."""
+    e = 2 if case.dtype == "i16" else 1
+    return case.m * case.k * e + case.k * case.n * e + 8 * case.m * case.n
