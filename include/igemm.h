@@ -1,0 +1,141 @@
+/*
+ * igemm.h -- integer GEMM  C += A * B  on AMD Instinct MI355X (gfx950).
+ *
+ * Operation (Sec. 4.1, "GEMM in conventional processor architectures"):
+ * A is m x k, B is k x n, C is m x n, and C is updated in place with the
+ * product A B. Operands are signed two's-complement int16 (igemm_i16) or
+ * int8 (igemm_i8); C is int32. Every product and sum is formed exactly and
+ * the updated C[i,j] is the exact value C[i,j] + sum_p A[i,p] B[p,j]
+ * reduced modulo 2^32 (two's-complement wraparound). Integer addition modulo
+ * 2^32 is associative, so the result is unique and bit-reproducible whatever
+ * the blocking, the order of the k loop or the number of workgroups that
+ * contribute to one element.
+ *
+ * Storage: ROW-MAJOR, leading dimensions counted in ELEMENTS:
+ *   A[i,p] = A[i*lda + p]   (lda >= max(1,k))
+ *   B[p,j] = B[p*ldb + j]   (ldb >= max(1,n))
+ *   C[i,j] = C[i*ldc + j]   (ldc >= max(1,n))
+ * Elements outside these windows are neither read nor written. A
+ * column-major caller uses the identity C^T += B^T A^T: pass
+ * (n, m, k, B, ldb, A, lda, C, ldc).
+ *
+ * Ownership and memory: A, B and C are DEVICE pointers owned by the caller
+ * (allocated by any HIP allocator; the library never frees them). The
+ * library allocates no device memory and keeps no per-call state; C itself
+ * is the only output buffer. C must not overlap A or B (not checked).
+ * Pointers and leading dimensions of any alignment are accepted; 16-byte
+ * aligned rows take the vector-load path, others a slower element path.
+ *
+ * Asynchrony and errors: every entry point validates its arguments on the
+ * host and returns IGEMM_EINVAL before making any HIP call if they are
+ * invalid. Otherwise it enqueues kernels on `stream` (a hipStream_t; NULL is
+ * the default stream) and returns IGEMM_OK, or IGEMM_EHIP if a launch was
+ * refused. The update of C is complete when the stream is. Faults inside a
+ * kernel surface at the caller's next synchronisation. Calls on different
+ * streams may run concurrently as long as their C windows do not overlap.
+ */
+#ifndef IGEMM_H
+#define IGEMM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum igemm_status {
+    IGEMM_OK = 0,
+    IGEMM_EINVAL = -1,  /* invalid argument; nothing was enqueued          */
+    IGEMM_EHIP = -2,    /* a HIP runtime call or kernel launch failed      */
+    IGEMM_ENOTSUP = -3  /* valid but unsupported (a size beyond 2^31 - 1)  */
+} igemm_status;
+
+/*
+ * C += A B with int16 operands and int32 wraparound output (Sec. 4.1; the
+ * paper's baseline datatype is int16, Sec. 6.1).
+ *   m, n, k  >= 0. m == 0 or n == 0: no-op. k == 0: C unchanged.
+ *   A        device, m x k int16, row-major, leading dimension lda.
+ *   B        device, k x n int16, row-major, leading dimension ldb.
+ *   C        device, m x n int32, row-major, leading dimension ldc; read
+ *            and written.
+ *   stream   hipStream_t or NULL.
+ * Returns an igemm_status.
+ */
+int igemm_i16(int64_t m, int64_t n, int64_t k,
+              const int16_t *A, int64_t lda,
+              const int16_t *B, int64_t ldb,
+              int32_t *C, int64_t ldc, void *stream);
+
+/* Same operation with int8 operands (the lower-precision variant that
+ * Sec. 6.1 lists as future work; int8 inputs in [-128, 127]). */
+int igemm_i8(int64_t m, int64_t n, int64_t k,
+             const int8_t *A, int64_t lda,
+             const int8_t *B, int64_t ldb,
+             int32_t *C, int64_t ldc, void *stream);
+
+/*
+ * Expert variants of the two calls above with an explicit kernel choice, for
+ * tuning sweeps and for tests that must reach every kernel:
+ *   kernel   -1 = automatic (same as igemm_i16 / igemm_i8), otherwise an
+ *            index 0 .. igemm_num_kernels()-1 whose operand type matches the
+ *            call (IGEMM_EINVAL otherwise).
+ *   split    -1 = automatic, otherwise the number of slices the k range is
+ *            cut into (>= 1); slices add their partial results into C with
+ *            32-bit atomic adds, which are exact modulo 2^32 in any order.
+ *            Values above ceil(k/64) are reduced to it.
+ * Semantics, memory and errors are those of igemm_i16 / igemm_i8.
+ */
+int igemm_i16_ex(int64_t m, int64_t n, int64_t k,
+                 const int16_t *A, int64_t lda,
+                 const int16_t *B, int64_t ldb,
+                 int32_t *C, int64_t ldc, void *stream,
+                 int kernel, int split);
+int igemm_i8_ex(int64_t m, int64_t n, int64_t k,
+                const int8_t *A, int64_t lda,
+                const int8_t *B, int64_t ldb,
+                int32_t *C, int64_t ldc, void *stream,
+                int kernel, int split);
+
+/* The launch the library would make for a call (host only, no HIP call).
+ * Filled by igemm_query_plan. */
+typedef struct igemm_plan {
+    int kernel;        /* kernel index                                     */
+    int elem_bytes;    /* 2 = int16 operands, 1 = int8                     */
+    int bm, bn, bk;    /* workgroup tile of C and k-tile depth (elements)  */
+    int split;         /* number of k slices                               */
+    int64_t k_chunk;   /* k elements per slice (multiple of bk)            */
+    int64_t tiles;     /* C tiles = ceil(m/bm) * ceil(n/bn)                */
+    int64_t grid;      /* workgroups launched = tiles * split              */
+    int threads;       /* threads per workgroup                            */
+    int vec_a, vec_b;  /* 1 if A / B rows take 16-byte vector loads        */
+    int limb_products; /* int8 MFMA products per operand pair: 4 or 1      */
+} igemm_plan;
+
+/*
+ * Fill *out with the plan for a call with these arguments (pointers are only
+ * inspected for alignment, never dereferenced). elem_bytes is 2 for int16,
+ * 1 for int8. num_cu is the compute-unit count to plan for (0 = 256, one
+ * MI355X). kernel/split as in the _ex calls. Returns IGEMM_OK, IGEMM_EINVAL
+ * for invalid arguments, or IGEMM_OK with out->grid == 0 for a no-op call.
+ */
+int igemm_query_plan(int elem_bytes, int64_t m, int64_t n, int64_t k,
+                     const void *A, int64_t lda, const void *B, int64_t ldb,
+                     const void *C, int64_t ldc, int num_cu,
+                     int kernel, int split, igemm_plan *out);
+
+/* Number of kernels, and a static name for index `kernel` (NULL if out of
+ * range). */
+int igemm_num_kernels(void);
+const char *igemm_kernel_name(int kernel);
+
+/* Static, human-readable text for a status code. */
+const char *igemm_strerror(int status);
+
+/* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
+int igemm_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* IGEMM_H */

@@ -1,0 +1,230 @@
+"""Python binding for libigemm (integer GEMM C += A.B on MI355X / gfx950).
+
+The functions here marshal arguments into the C ABI of ``include/igemm.h``
+with ctypes; every step of the computation runs in the HIP library. PyTorch
+is used only to hand over device pointers and the current HIP stream. There
+is no CPU fallback: if the library is missing, importing this package raises.
+
+Same names as the C ABI:
+    igemm_i16(m, n, k, A, lda, B, ldb, C, ldc, stream=None)
+    igemm_i8 (m, n, k, A, lda, B, ldb, C, ldc, stream=None)
+    igemm_i16_ex / igemm_i8_ex(..., kernel=-1, split=-1)
+    igemm_query_plan(elem_bytes, m, n, k, A, lda, B, ldb, C, ldc, num_cu=0,
+                     kernel=-1, split=-1) -> dict
+    igemm_strerror(status), igemm_kernel_name(i), igemm_num_kernels(),
+    igemm_version()
+A, B, C may be integer device addresses or torch tensors (their data_ptr()).
+Tensor conveniences: gemm_i16(A, B, C) and gemm_i8(A, B, C) take 2-D CUDA
+tensors with unit stride along rows and update C in place.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libigemm.so")
+
+IGEMM_OK = 0
+IGEMM_EINVAL = -1
+IGEMM_EHIP = -2
+IGEMM_ENOTSUP = -3
+
+
+class IgemmError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {igemm_strerror(status)} (status {status})")
+        self.status = status
+
+
+class _Plan(ctypes.Structure):
+    _fields_ = [("kernel", ctypes.c_int), ("elem_bytes", ctypes.c_int),
+                ("bm", ctypes.c_int), ("bn", ctypes.c_int), ("bk", ctypes.c_int),
+                ("split", ctypes.c_int), ("k_chunk", ctypes.c_int64),
+                ("tiles", ctypes.c_int64), ("grid", ctypes.c_int64),
+                ("threads", ctypes.c_int), ("vec_a", ctypes.c_int), ("vec_b", ctypes.c_int),
+                ("limb_products", ctypes.c_int)]
+
+
+def _load():
+    # torch ships its own HIP runtime whose DT_NEEDED name differs from the
+    # soname this library links against; loading torch first lets the dynamic
+    # linker bind both to that one runtime, so torch's streams and allocations
+    # are valid handles for this library's launches.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is not built; run `python -c 'import __graft_entry__ as g; g.build()'` "
+            "or `python -m paper_2302_07594_amd.build` (the HIP library has no fallback)")
+    lib = ctypes.CDLL(LIB_PATH)
+    i64, vp, ci = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
+    gemm_args = [i64, i64, i64, vp, i64, vp, i64, vp, i64, vp]
+    for name in ("igemm_i16", "igemm_i8"):
+        getattr(lib, name).argtypes = gemm_args
+        getattr(lib, name).restype = ci
+        getattr(lib, name + "_ex").argtypes = gemm_args + [ci, ci]
+        getattr(lib, name + "_ex").restype = ci
+    lib.igemm_query_plan.argtypes = [ci, i64, i64, i64, vp, i64, vp, i64, vp, i64, ci, ci, ci,
+                                     ctypes.POINTER(_Plan)]
+    lib.igemm_query_plan.restype = ci
+    lib.igemm_strerror.argtypes = [ci]
+    lib.igemm_strerror.restype = ctypes.c_char_p
+    lib.igemm_kernel_name.argtypes = [ci]
+    lib.igemm_kernel_name.restype = ctypes.c_char_p
+    lib.igemm_num_kernels.argtypes = []
+    lib.igemm_num_kernels.restype = ci
+    lib.igemm_version.argtypes = []
+    lib.igemm_version.restype = ci
+    return lib
+
+
+_lib = _load()
+
+
+def library_path() -> str:
+    return LIB_PATH
+
+
+def _addr(x) -> int:
+    if x is None:
+        return 0
+    if isinstance(x, int):
+        return x
+    if hasattr(x, "data_ptr"):
+        return int(x.data_ptr())
+    raise TypeError(f"expected a device address or a tensor, got {type(x).__name__}")
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        import torch
+        return int(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return stream
+    if hasattr(stream, "cuda_stream"):
+        return int(stream.cuda_stream)
+    raise TypeError("stream must be None, an int handle or a torch stream")
+
+
+def _call(name, m, n, k, A, lda, B, ldb, C, ldc, stream, *extra) -> int:
+    fn = getattr(_lib, name)
+    st = fn(int(m), int(n), int(k), _addr(A), int(lda), _addr(B), int(ldb), _addr(C), int(ldc),
+            _stream(stream), *extra)
+    return int(st)
+
+
+def igemm_i16(m, n, k, A, lda, B, ldb, C, ldc, stream=None) -> int:
+    """C += A.B, int16 operands, int32 wraparound C. Returns the status."""
+    return _call("igemm_i16", m, n, k, A, lda, B, ldb, C, ldc, stream)
+
+
+def igemm_i8(m, n, k, A, lda, B, ldb, C, ldc, stream=None) -> int:
+    """C += A.B, int8 operands, int32 wraparound C. Returns the status."""
+    return _call("igemm_i8", m, n, k, A, lda, B, ldb, C, ldc, stream)
+
+
+def igemm_i16_ex(m, n, k, A, lda, B, ldb, C, ldc, stream=None, kernel=-1, split=-1) -> int:
+    return _call("igemm_i16_ex", m, n, k, A, lda, B, ldb, C, ldc, stream, int(kernel), int(split))
+
+
+def igemm_i8_ex(m, n, k, A, lda, B, ldb, C, ldc, stream=None, kernel=-1, split=-1) -> int:
+    return _call("igemm_i8_ex", m, n, k, A, lda, B, ldb, C, ldc, stream, int(kernel), int(split))
+
+
+_PLACEHOLDER = 1 << 12  # aligned, non-NULL; the planner never dereferences it
+
+
+def igemm_query_plan(elem_bytes, m, n, k, A=None, lda=None, B=None, ldb=None, C=None,
+                     ldc=None, num_cu=0, kernel=-1, split=-1):
+    """The launch the library would make (host-only). Returns a dict, or
+    raises IgemmError for invalid arguments. Omitted pointers stand for
+    16-byte aligned buffers."""
+    A = _PLACEHOLDER if A is None else A
+    B = _PLACEHOLDER if B is None else B
+    C = _PLACEHOLDER if C is None else C
+    lda = k if lda is None else lda
+    ldb = n if ldb is None else ldb
+    ldc = n if ldc is None else ldc
+    p = _Plan()
+    st = _lib.igemm_query_plan(int(elem_bytes), int(m), int(n), int(k), _addr(A), int(lda),
+                               _addr(B), int(ldb), _addr(C), int(ldc), int(num_cu), int(kernel),
+                               int(split), ctypes.byref(p))
+    if st != IGEMM_OK:
+        raise IgemmError(st, "igemm_query_plan")
+    d = {f: getattr(p, f) for f, _ in _Plan._fields_}
+    d["kernel_name"] = igemm_kernel_name(p.kernel) if p.kernel >= 0 else None
+    return d
+
+
+def igemm_strerror(status: int) -> str:
+    return _lib.igemm_strerror(int(status)).decode()
+
+
+def igemm_kernel_name(kernel: int):
+    r = _lib.igemm_kernel_name(int(kernel))
+    return r.decode() if r is not None else None
+
+
+def igemm_num_kernels() -> int:
+    return int(_lib.igemm_num_kernels())
+
+
+def igemm_version() -> int:
+    return int(_lib.igemm_version())
+
+
+def kernels_for(elem_bytes: int):
+    """Indices of the kernels that take operands of ``elem_bytes`` bytes."""
+    out = []
+    for i in range(igemm_num_kernels()):
+        nm = igemm_kernel_name(i)
+        if (elem_bytes == 2) == nm.startswith("i16"):
+            out.append(i)
+    return out
+
+
+def _check_tensors(A, B, C, torch_dtype, name):
+    import torch
+    if A.dtype != torch_dtype or B.dtype != torch_dtype:
+        raise TypeError(f"{name}: A and B must be {torch_dtype}")
+    if C.dtype != torch.int32:
+        raise TypeError(f"{name}: C must be torch.int32")
+    if A.dim() != 2 or B.dim() != 2 or C.dim() != 2:
+        raise ValueError(f"{name}: A, B and C must be 2-D")
+    m, k = A.shape
+    k2, n = B.shape
+    if k2 != k or tuple(C.shape) != (m, n):
+        raise ValueError(f"{name}: shapes {tuple(A.shape)} x {tuple(B.shape)} -> {tuple(C.shape)}")
+    for t, nm in ((A, "A"), (B, "B"), (C, "C")):
+        if not t.is_cuda:
+            raise ValueError(f"{name}: {nm} must be a CUDA (HIP) tensor")
+        if t.shape[1] > 1 and t.stride(1) != 1:
+            raise ValueError(f"{name}: {nm} must have unit stride along rows")
+
+    def ld(t):
+        return t.stride(0) if t.shape[0] > 1 else max(t.shape[1], 1)
+    return m, n, k, ld(A), ld(B), ld(C)
+
+
+def gemm_i16(A, B, C, stream=None, kernel=-1, split=-1):
+    """C += A.B for 2-D torch.int16 CUDA tensors A (m x k), B (k x n) and a
+    torch.int32 C (m x n). Returns C. Raises IgemmError on a bad status."""
+    import torch
+    m, n, k, lda, ldb, ldc = _check_tensors(A, B, C, torch.int16, "gemm_i16")
+    st = igemm_i16_ex(m, n, k, A, lda, B, ldb, C, ldc, stream, kernel, split)
+    if st != IGEMM_OK:
+        raise IgemmError(st, "igemm_i16")
+    return C
+
+
+def gemm_i8(A, B, C, stream=None, kernel=-1, split=-1):
+    """C += A.B for 2-D torch.int8 CUDA tensors; see gemm_i16."""
+    import torch
+    m, n, k, lda, ldb, ldc = _check_tensors(A, B, C, torch.int8, "gemm_i8")
+    st = igemm_i8_ex(m, n, k, A, lda, B, ldb, C, ldc, stream, kernel, split)
+    if st != IGEMM_OK:
+        raise IgemmError(st, "igemm_i8")
+    return C

@@ -1,0 +1,164 @@
+// Host-side argument validation and launch planning (no HIP calls).
+//
+// The planner plays the role of the paper's choice of cache configuration
+// parameters (Sec. 4.1: mc, nc, kc around a fixed micro-kernel; Sec. 6.3 and
+// 6.4 pick kc and mc from the sizes of the memory levels). On the GPU the
+// workgroup tile (bm x bn) takes the place of mc x nc, the k-tile of 64
+// elements the place of kc, and the number of k slices is chosen so that
+// small-output shapes -- the deep-learning shapes with one large and two
+// small dimensions (Sec. 2, Sec. 4.2) -- still occupy every compute unit.
+#include <limits.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "igemm_internal.h"
+
+namespace igemm {
+
+const KernelDesc kKernels[K_COUNT] = {
+    {"i8_256x256", 1, 256, 256, 128, 128},
+    {"i8_128x128", 1, 128, 128, 64, 64},
+    {"i8_32x256", 1, 32, 256, 32, 64},
+    {"i8_16x256", 1, 16, 256, 16, 64},
+    {"i16_128x128", 2, 128, 128, 64, 64},
+    {"i16_64x64", 2, 64, 64, 32, 32},
+    {"i16_32x128", 2, 32, 128, 32, 32},
+    {"i16_16x128", 2, 16, 128, 16, 32},
+};
+
+static bool mul_ok(int64_t a, int64_t b, int64_t *out) {
+    return !__builtin_mul_overflow(a, b, out);
+}
+
+// Byte extent of a rows x cols window with leading dimension ld; false on
+// int64 overflow.
+static bool extent_ok(int64_t rows, int64_t cols, int64_t ld, int64_t es) {
+    int64_t t;
+    if (!mul_ok(rows - 1, ld, &t)) return false;
+    if (__builtin_add_overflow(t, cols, &t)) return false;
+    return mul_ok(t, es, &t);
+}
+
+int validate(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
+             const void *B, int64_t ldb, const void *C, int64_t ldc) {
+    if (es != 1 && es != 2) return IGEMM_EINVAL;
+    if (m < 0 || n < 0 || k < 0) return IGEMM_EINVAL;
+    if (m == 0 || n == 0) return IGEMM_OK;
+    if (C == NULL || ldc < n) return IGEMM_EINVAL;
+    if (!extent_ok(m, n, ldc, 4)) return IGEMM_EINVAL;
+    if (k > 0) {
+        if (A == NULL || B == NULL) return IGEMM_EINVAL;
+        if (lda < k || ldb < n) return IGEMM_EINVAL;
+        if (!extent_ok(m, k, lda, es) || !extent_ok(k, n, ldb, es)) return IGEMM_EINVAL;
+    }
+    // k leaves headroom so that k-tile offsets computed in int never overflow.
+    if (m > INT_MAX || n > INT_MAX || k > INT_MAX - 65536) return IGEMM_ENOTSUP;
+    return IGEMM_OK;
+}
+
+static int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+static int64_t tiles_of(int id, int64_t m, int64_t n) {
+    return cdiv(m, kKernels[id].bm) * cdiv(n, kKernels[id].bn);
+}
+
+static int auto_kernel(int es, int64_t m, int64_t n, int num_cu) {
+    if (es == 1) {
+        if (m <= 16) return K_I8_16x256;
+        if (m <= 32) return K_I8_32x256;
+        if (tiles_of(K_I8_256x256, m, n) >= num_cu) return K_I8_256x256;
+        return K_I8_128x128;
+    }
+    if (m <= 16) return K_I16_16x128;
+    if (m <= 32) return K_I16_32x128;
+    if (tiles_of(K_I16_128x128, m, n) >= num_cu) return K_I16_128x128;
+    return K_I16_64x64;
+}
+
+int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
+              const void *B, int64_t ldb, int num_cu, int kernel, int split,
+              igemm_plan *out) {
+    if (out == NULL) return IGEMM_EINVAL;
+    if (num_cu <= 0) num_cu = 256;
+    *out = igemm_plan{};
+    out->elem_bytes = es;
+    out->bk = kBK;
+    out->threads = kThreads;
+    out->limb_products = es == 2 ? 4 : 1;
+    if (m == 0 || n == 0 || k == 0) {
+        out->kernel = -1;
+        return IGEMM_OK;  // no-op: nothing is launched
+    }
+    if (kernel < -1 || kernel >= K_COUNT || split < -1 || split == 0) return IGEMM_EINVAL;
+    int id = kernel >= 0 ? kernel : auto_kernel(es, m, n, num_cu);
+    if (kKernels[id].es != es) return IGEMM_EINVAL;
+    const KernelDesc &d = kKernels[id];
+    const int64_t tiles = tiles_of(id, m, n);
+    const int64_t ktiles = cdiv(k, kBK);
+    const int64_t min_split = cdiv(k, kMaxKChunk);
+    int64_t s;
+    if (split > 0) {
+        s = split;
+    } else if (tiles >= num_cu) {
+        s = 1;
+    } else {
+        // Aim for two workgroups per compute unit, but keep at least two
+        // k-tiles per slice so each slice still pipelines its loads.
+        s = cdiv(2 * (int64_t)num_cu, tiles);
+        int64_t cap = ktiles / 2 > 1 ? ktiles / 2 : 1;
+        if (s > cap) s = cap;
+    }
+    if (s < min_split) s = min_split;
+    if (s > ktiles) s = ktiles;
+    if (s < 1) s = 1;
+    const int64_t kchunk = cdiv(ktiles, s) * kBK;
+    s = cdiv(k, kchunk);
+    const int64_t grid = tiles * s;
+    if (grid > INT_MAX || cdiv(m, d.bm) > INT_MAX || cdiv(n, d.bn) > INT_MAX)
+        return IGEMM_ENOTSUP;
+    out->kernel = id;
+    out->bm = d.bm;
+    out->bn = d.bn;
+    out->split = (int)s;
+    out->k_chunk = kchunk;
+    out->tiles = tiles;
+    out->grid = grid;
+    const uintptr_t a = (uintptr_t)A, b = (uintptr_t)B;
+    out->vec_a = (a % 16 == 0) && ((lda * es) % 16 == 0);
+    out->vec_b = (b % 16 == 0) && ((ldb * es) % 16 == 0);
+    return IGEMM_OK;
+}
+
+}  // namespace igemm
+
+extern "C" {
+
+int igemm_query_plan(int elem_bytes, int64_t m, int64_t n, int64_t k, const void *A,
+                     int64_t lda, const void *B, int64_t ldb, const void *C, int64_t ldc,
+                     int num_cu, int kernel, int split, igemm_plan *out) {
+    if (out == NULL) return IGEMM_EINVAL;
+    int st = igemm::validate(elem_bytes, m, n, k, A, lda, B, ldb, C, ldc);
+    if (st != IGEMM_OK) return st;
+    return igemm::make_plan(elem_bytes, m, n, k, A, lda, B, ldb, num_cu, kernel, split, out);
+}
+
+int igemm_num_kernels(void) { return igemm::K_COUNT; }
+
+const char *igemm_kernel_name(int kernel) {
+    if (kernel < 0 || kernel >= igemm::K_COUNT) return NULL;
+    return igemm::kKernels[kernel].name;
+}
+
+const char *igemm_strerror(int status) {
+    switch (status) {
+        case IGEMM_OK: return "success";
+        case IGEMM_EINVAL: return "invalid argument (nothing was enqueued)";
+        case IGEMM_EHIP: return "HIP runtime call or kernel launch failed";
+        case IGEMM_ENOTSUP: return "unsupported size (a dimension or the grid exceeds 2^31 - 1)";
+        default: return "unknown status";
+    }
+}
+
+int igemm_version(void) { return 100; }
+
+}  // extern "C"

@@ -1,0 +1,135 @@
+"""Host-side checks of the C ABI (no GPU): the library loads, exports every
+function include/igemm.h declares, rejects invalid arguments before any HIP
+call, and plans launches as documented."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2302_07594_amd as ig
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "igemm.h")
+
+FAKE_A = 0x10000   # never dereferenced: every call below fails validation or is a no-op
+FAKE_B = 0x20000
+FAKE_C = 0x30000
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(igemm_\w+)\s*\(", text, re.M)))
+
+
+def test_header_declares_entry_points():
+    fns = declared_functions()
+    for name in ("igemm_i16", "igemm_i8", "igemm_strerror", "igemm_i16_ex", "igemm_i8_ex",
+                 "igemm_query_plan", "igemm_num_kernels", "igemm_kernel_name",
+                 "igemm_version"):
+        assert name in fns
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(ig.library_path())
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_oracle_not_linked_into_library():
+    lib = ctypes.CDLL(ig.library_path())
+    assert not hasattr(lib, "oracle_igemm_i16")
+
+
+@pytest.mark.parametrize("fn", [ig.igemm_i16, ig.igemm_i8])
+def test_invalid_arguments(fn):
+    E = ig.IGEMM_EINVAL
+    s = 0
+    assert fn(-1, 4, 4, FAKE_A, 4, FAKE_B, 4, FAKE_C, 4, s) == E
+    assert fn(4, -1, 4, FAKE_A, 4, FAKE_B, 4, FAKE_C, 4, s) == E
+    assert fn(4, 4, -1, FAKE_A, 4, FAKE_B, 4, FAKE_C, 4, s) == E
+    assert fn(4, 4, 4, FAKE_A, 3, FAKE_B, 4, FAKE_C, 4, s) == E   # lda < k
+    assert fn(4, 4, 4, FAKE_A, 4, FAKE_B, 3, FAKE_C, 4, s) == E   # ldb < n
+    assert fn(4, 4, 4, FAKE_A, 4, FAKE_B, 4, FAKE_C, 3, s) == E   # ldc < n
+    assert fn(4, 4, 4, 0, 4, FAKE_B, 4, FAKE_C, 4, s) == E        # A NULL
+    assert fn(4, 4, 4, FAKE_A, 4, 0, 4, FAKE_C, 4, s) == E        # B NULL
+    assert fn(4, 4, 4, FAKE_A, 4, FAKE_B, 4, 0, 4, s) == E        # C NULL
+    big = 1 << 62
+    assert fn(big, 4, 4, FAKE_A, 4, FAKE_B, 4, FAKE_C, big, s) == E  # extent overflow
+
+
+@pytest.mark.parametrize("fn", [ig.igemm_i16, ig.igemm_i8])
+def test_noop_calls_return_ok_without_device(fn):
+    s = 0
+    assert fn(0, 4, 4, 0, 4, 0, 4, 0, 4, s) == ig.IGEMM_OK         # m = 0
+    assert fn(4, 0, 4, 0, 4, 0, 4, 0, 4, s) == ig.IGEMM_OK         # n = 0
+    assert fn(4, 4, 0, 0, 1, 0, 4, FAKE_C, 4, s) == ig.IGEMM_OK    # k = 0: C unchanged
+
+
+def test_ex_rejects_mismatched_kernel():
+    s = 0
+    i8_kernel = ig.kernels_for(1)[0]
+    i16_kernel = ig.kernels_for(2)[0]
+    assert ig.igemm_i16_ex(4, 4, 4, FAKE_A, 4, FAKE_B, 4, FAKE_C, 4, s,
+                           i8_kernel, -1) == ig.IGEMM_EINVAL
+    assert ig.igemm_i8_ex(4, 4, 4, FAKE_A, 4, FAKE_B, 4, FAKE_C, 4, s,
+                          i16_kernel, -1) == ig.IGEMM_EINVAL
+    assert ig.igemm_i8_ex(4, 4, 4, FAKE_A, 4, FAKE_B, 4, FAKE_C, 4, s,
+                          ig.igemm_num_kernels(), -1) == ig.IGEMM_EINVAL
+    assert ig.igemm_i8_ex(4, 4, 4, FAKE_A, 4, FAKE_B, 4, FAKE_C, 4, s, -1, 0) == ig.IGEMM_EINVAL
+
+
+def test_too_large_is_unsupported():
+    s = 0
+    n = (1 << 31) + 64
+    assert ig.igemm_i8(1, n, 1, FAKE_A, 1, FAKE_B, n, FAKE_C, n, s) == ig.IGEMM_ENOTSUP
+
+
+def test_strerror_and_names():
+    assert ig.igemm_strerror(0) == "success"
+    assert "invalid" in ig.igemm_strerror(-1)
+    assert ig.igemm_strerror(12345) == "unknown status"
+    names = [ig.igemm_kernel_name(i) for i in range(ig.igemm_num_kernels())]
+    assert all(names) and len(set(names)) == len(names)
+    assert ig.igemm_kernel_name(-1) is None
+    assert ig.igemm_version() >= 100
+
+
+def test_plans_for_workloads():
+    import workloads
+    for wname in workloads.ORDER:
+        for case in workloads.WORKLOADS[wname].cases:
+            es = 2 if case.dtype == "i16" else 1
+            p = ig.igemm_query_plan(es, case.m, case.n, case.k, FAKE_A, case.k, FAKE_B, case.n,
+                                    FAKE_C, case.n)
+            assert p["elem_bytes"] == es
+            assert p["kernel_name"].startswith("i16" if es == 2 else "i8")
+            assert p["split"] >= 1 and p["k_chunk"] % 64 == 0
+            assert p["split"] * p["k_chunk"] >= case.k > (p["split"] - 1) * p["k_chunk"]
+            assert p["k_chunk"] <= 32768
+            assert p["grid"] == p["tiles"] * p["split"]
+            assert p["limb_products"] == (4 if es == 2 else 1)
+    big = ig.igemm_query_plan(2, 4096, 4096, 4096, FAKE_A, 4096, FAKE_B, 4096, FAKE_C, 4096)
+    assert big["kernel_name"] == "i16_128x128" and big["split"] == 1 and big["vec_a"] == 1
+    big8 = ig.igemm_query_plan(1, 8192, 8192, 8192, FAKE_A, 8192, FAKE_B, 8192, FAKE_C, 8192)
+    assert big8["kernel_name"] == "i8_256x256" and big8["split"] == 1
+
+
+def test_plan_alignment_and_split_rules():
+    # odd leading dimension or base -> element path
+    p = ig.igemm_query_plan(2, 100, 64, 147, FAKE_A, 147, FAKE_B, 64, FAKE_C, 64)
+    assert p["vec_a"] == 0 and p["vec_b"] == 1
+    p = ig.igemm_query_plan(1, 100, 64, 128, FAKE_A + 1, 128, FAKE_B, 64, FAKE_C, 64)
+    assert p["vec_a"] == 0
+    # k beyond the per-workgroup cap forces slices
+    p = ig.igemm_query_plan(1, 4096, 4096, 100000, FAKE_A, 100000, FAKE_B, 4096, FAKE_C, 4096)
+    assert p["split"] >= 4 and p["k_chunk"] <= 32768
+    # explicit split is honoured, clamped to the number of k-tiles
+    p = ig.igemm_query_plan(1, 64, 64, 640, FAKE_A, 640, FAKE_B, 64, FAKE_C, 64, split=3)
+    assert p["split"] == 3
+    p = ig.igemm_query_plan(1, 64, 64, 100, FAKE_A, 100, FAKE_B, 64, FAKE_C, 64, split=50)
+    assert p["split"] == 2
+    # no-op
+    p = ig.igemm_query_plan(1, 64, 64, 0, FAKE_A, 1, FAKE_B, 64, FAKE_C, 64)
+    assert p["grid"] == 0 and p["kernel"] == -1
