@@ -1,0 +1,244 @@
+#!/usr/bin/env python3
+"""Benchmark for integer GEMM C += A.B on one MI355X.
+
+A step is one call of igemm_i16 on the int16 workload m = n = k = 4096
+(A, B uniform over the full int16 range, C uniform in [-2^20, 2^20], seed 1):
+host validation and planning, then one kernel that stages and splits the
+operands, runs the int8 matrix-core products, applies the limb corrections
+and adds into C with int32 wraparound. Inputs are resident in HBM before the
+timed region starts.
+
+Prints ONE JSON line. Besides the headline value it carries:
+  roofline      the kernel's achieved rate against its ceiling, timed with HIP
+                events on the stream the kernel is launched on;
+  cpu_baseline  the CPU oracle timed on the host cores over a bounded sample
+                of the same workload;
+  per_config    every other workload, each timed the same way (memory-bound
+                ones rotate through enough buffer sets to defeat the 256 MB
+                last-level cache), with its own roofline fraction.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-extra]
+                       [--no-cpu-baseline] [--cpu-seconds S]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+# MI355X published dense peaks and bandwidth.
+PEAK_INT8_TOPS = 5000.0      # int8 MFMA, dense
+HBM_GBS = 8000.0             # HBM3E
+LIMB_PRODUCTS_I16 = 4        # int8 products per int16 multiply-add
+PEAK_I16_TOPS = PEAK_INT8_TOPS / LIMB_PRODUCTS_I16
+MALL_BYTES = 256 << 20
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_i16_128x128_4096cube.json")
+KERNEL_SRC = os.path.join(ROOT, "paper_2302_07594_amd", "csrc", "igemm_kernels.hip")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if
+    it was taken on the current kernel source; otherwise None."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    return t.get("traffic_bytes_per_launch")
+
+
+def roofline_for(dtype, m, n, k, seconds):
+    """(bound, achieved, peak, unit) for one GEMM of this shape."""
+    es = 2 if dtype == "i16" else 1
+    ops = 2.0 * m * n * k
+    nbytes = m * k * es + k * n * es + 8.0 * m * n
+    peak_ops = (PEAK_I16_TOPS if es == 2 else PEAK_INT8_TOPS) * 1e12
+    if ops / nbytes >= peak_ops / (HBM_GBS * 1e9):
+        return "mfma", ops / seconds / 1e12, peak_ops / 1e12, "TOPS"
+    return "hbm", nbytes / seconds / 1e9, HBM_GBS, "GB/s"
+
+
+def time_launches(fn, iters):
+    """Average device time per launch (HIP events on the current stream)."""
+    import torch
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(iters):
+        fn(i)
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e-3 / iters
+
+
+def bench_case(case, min_sets=1, iters=50, warmup=5):
+    """Time one workload case on rotating device copies of its operands."""
+    import torch
+
+    import paper_2302_07594_amd as ig
+    import workloads
+    A, B, C = workloads.generate(case)
+    es = 2 if case.dtype == "i16" else 1
+    set_bytes = A.nbytes + B.nbytes + C.nbytes
+    nsets = max(min_sets, -(-2 * MALL_BYTES // set_bytes))
+    nsets = min(nsets, 64)
+    Ad0, Bd0, Cd0 = (torch.from_numpy(x).cuda() for x in (A, B, C))
+    sets = [(Ad0, Bd0, Cd0)] + [(Ad0.clone(), Bd0.clone(), Cd0.clone()) for _ in range(nsets - 1)]
+    f = ig.gemm_i16 if es == 2 else ig.gemm_i8
+    for i in range(warmup):
+        f(*sets[i % nsets])
+    torch.cuda.synchronize()
+    t = time_launches(lambda i: f(*sets[i % nsets]), iters)
+    plan = ig.igemm_query_plan(es, case.m, case.n, case.k)
+    bound, ach, peak, unit = roofline_for(case.dtype, case.m, case.n, case.k, t)
+    return {
+        "name": case.name, "dtype": case.dtype, "m": case.m, "n": case.n, "k": case.k,
+        "kernel": plan["kernel_name"], "split": plan["split"], "grid": plan["grid"],
+        "us": round(t * 1e6, 2), "TOPS": round(2.0 * case.m * case.n * case.k / t / 1e12, 2),
+        "bound": bound, "achieved": round(ach, 1), "peak": peak, "unit": unit,
+        "frac": round(ach / peak, 4), "buffer_sets": nsets,
+    }
+
+
+def cpu_baseline(A, B, C_gpu_first, C0, seconds):
+    """Time the CPU oracle on whole rows of the same workload, for at most
+    about `seconds`; also confirm those rows match the GPU's first result."""
+    import numpy as np
+
+    import oracle
+    m, k = A.shape
+    n = B.shape[1]
+    block = 64
+    done = 0
+    elapsed = 0.0
+    mismatched = 0
+    while done < m and elapsed < seconds:
+        rows = slice(done, min(m, done + block))
+        Cr = np.ascontiguousarray(C0[rows])
+        t0 = time.perf_counter()
+        oracle.igemm(np.ascontiguousarray(A[rows]), B, Cr)
+        elapsed += time.perf_counter() - t0
+        mismatched += int((Cr != C_gpu_first[rows]).sum())
+        done = rows.stop
+    ops = 2.0 * done * n * k
+    return {
+        "value": round(ops / elapsed / 1e12, 6), "unit": "TOPS",
+        "cores": oracle.num_threads(), "kind": "oracle",
+        "sample": f"rows 0..{done - 1} of the {m}x{n}x{k} int16 workload "
+                  f"({done * n * k:.3g} multiply-adds, {elapsed:.1f} s)",
+        "rows_bit_exact_vs_gpu": mismatched == 0, "rows_checked": done,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-extra", action="store_true", help="skip the per-config table")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: --gpus {args.gpus} is not supported: this build measures one GPU "
+              "(the kernel at one GPU's share); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2302_07594_amd as ig
+    import workloads
+
+    case = workloads.WORKLOADS["i16_4096"].cases[0]
+    m, n, k = case.m, case.n, case.k
+    log(f"bench: generating {case.name}")
+    A, B, C0 = workloads.generate(case)
+    Ad = torch.from_numpy(A).cuda()
+    Bd = torch.from_numpy(B).cuda()
+    Cd = torch.from_numpy(C0).cuda()
+    # First launch on the pristine C; its result is compared with the oracle
+    # rows in the CPU-baseline leg.
+    ig.gemm_i16(Ad, Bd, Cd)
+    torch.cuda.synchronize()
+    C_first = Cd.cpu().numpy()
+    plan = ig.igemm_query_plan(2, m, n, k, Ad, k, Bd, n, Cd, n)
+
+    log(f"bench: warmup {args.warmup}, timed steps {args.steps}")
+    for _ in range(args.warmup):
+        ig.gemm_i16(Ad, Bd, Cd)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        ig.gemm_i16(Ad, Bd, Cd)
+    e1.record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    wall = (t1 - t0) / args.steps
+    kern = e0.elapsed_time(e1) * 1e-3 / args.steps
+    ops = 2.0 * m * n * k
+    value = ops / wall / 1e12
+    ach = ops / kern / 1e12
+
+    out = {
+        "metric": "int16 GEMM C+=A.B throughput on 1 MI355X (int8 MFMA limb split), TOPS",
+        "value": round(value, 2), "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(wall * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int16", "data": "synthetic",
+        "config": {
+            "workload": "int16 GEMM C += A.B, m=n=k=4096, row-major, A,B uniform over the full "
+                        "int16 range, C uniform in [-2^20,2^20], int32 wraparound, seed 1",
+            "m": m, "n": n, "k": k, "accumulate": "int32 modulo 2^32",
+            "kernel": plan["kernel_name"], "split": plan["split"], "grid": plan["grid"],
+        },
+        "roofline": {
+            "bound": "mfma", "achieved": round(ach, 1), "peak": PEAK_I16_TOPS, "unit": "TOPS",
+            "frac": round(ach / PEAK_I16_TOPS, 4), "traffic": measured_traffic(),
+            "kernel": "igemm_tiled<int16, 128x128>",
+            "peak_basis": "int8 MFMA dense peak 5000 TOPS / 4 int8 limb products per int16 "
+                          "multiply-add",
+            "int8_mfma_frac": round(ach * LIMB_PRODUCTS_I16 / PEAK_INT8_TOPS, 4),
+            "kernel_us": round(kern * 1e6, 2),
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("bench: CPU oracle baseline")
+        out["cpu_baseline"] = cpu_baseline(A, B, C_first, C0, args.cpu_seconds)
+    del Ad, Bd, Cd
+    torch.cuda.empty_cache()
+    if not args.no_extra:
+        per = []
+        for wname in ("i16_256", "i8_8192", "i16_conv", "i8_skinny"):
+            for c in workloads.WORKLOADS[wname].cases:
+                log(f"bench: per-config {c.name}")
+                per.append(bench_case(c))
+                torch.cuda.empty_cache()
+        out["per_config"] = per
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -11,9 +11,10 @@
 //     the operand layout of the MFMA instructions; LDS rows are XOR-swizzled
 //     in 16-byte chunks so that the staging writes and the fragment reads are
 //     free of bank conflicts;
-//   * each wave keeps its C tile in accumulator registers and runs
-//     v_mfma_i32_16x16x64_i8 over the k-tile (loop L6: rank-64 updates
-//     instead of rank-1);
+//   * each wave keeps its C tile in accumulator registers and runs int8
+//     matrix-core instructions (v_mfma_i32_32x32x32_i8, or
+//     v_mfma_i32_16x16x64_i8 for 16-row tiles) over the k-tile (loop L6:
+//     rank-64 updates instead of rank-1);
 //   * the epilogue adds the accumulators into C with int32 wraparound (the
 //     C_r load / update / store of Sec. 5.2), by plain read-add-write, or by
 //     32-bit atomic adds when the k range is sliced across workgroups.
@@ -32,6 +33,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "igemm.h"
 #include "igemm_internal.h"
 
@@ -39,23 +42,56 @@ namespace igemm {
 namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
 typedef unsigned int u32;
+
+// The two gfx950 int8 matrix-core instructions, described by their tile
+// shape. Both take 16 bytes of A and 16 bytes of B per lane (one row of A /
+// one column of B, k-contiguous); the k range a lane holds is chunk
+// `2*ks + lane/32` (32x32x32) or `lane/16` (16x16x64) of the 64-byte k-tile.
+// 32x32x32 is the default: the compiler accumulates it in place, whereas it
+// rotates the 16x16x64 accumulators through copies, so 16x16x64 is kept for
+// 16-row tiles only.
+template <int MF>
+struct Mfma;
+template <>
+struct Mfma<16> {
+    typedef v4i acc_t;
+    static constexpr int REGS = 4, KSTEPS = 1;
+    static __device__ __forceinline__ acc_t mma(v4i a, v4i b, acc_t c) {
+        return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+    }
+    static __device__ __forceinline__ int frag_row(int lane) { return lane & 15; }
+    static __device__ __forceinline__ int frag_chunk(int lane, int ks) { return lane >> 4; }
+    // output register r of `lane` holds C[row][col] of the 16x16 tile
+    static __device__ __forceinline__ int out_row(int lane, int r) { return 4 * (lane >> 4) + r; }
+    static __device__ __forceinline__ int out_col(int lane) { return lane & 15; }
+};
+template <>
+struct Mfma<32> {
+    typedef v16i acc_t;
+    static constexpr int REGS = 16, KSTEPS = 2;
+    static __device__ __forceinline__ acc_t mma(v4i a, v4i b, acc_t c) {
+        return __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0);
+    }
+    static __device__ __forceinline__ int frag_row(int lane) { return lane & 31; }
+    static __device__ __forceinline__ int frag_chunk(int lane, int ks) { return 2 * ks + (lane >> 5); }
+    static __device__ __forceinline__ int out_row(int lane, int r) {
+        return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+    }
+    static __device__ __forceinline__ int out_col(int lane) { return lane & 31; }
+};
 
 // ---------------------------------------------------------------------------
 // LDS layout. Every operand plane is stored as rows of 64 bytes (the 64
 // k-elements of one row of A or one column of B), split into four 16-byte
-// chunks. The chunk index is XORed with bits 1-2 of the row, and for B the
-// row parity is flipped by bit 4 of the row, so that (i) eight consecutive
-// rows read at the same chunk -- one MFMA fragment load phase -- hit distinct
-// banks, and (ii) the B staging writes of one wave spread over both halves of
-// the banks.
-__device__ __forceinline__ int lds_off_a(int row, int q) {
-    return row * 64 + ((q ^ ((row >> 1) & 3)) << 4);
-}
-__device__ __forceinline__ int lds_off_b(int row, int q) {
-    const int r = row ^ ((row >> 4) & 1);
-    return r * 64 + ((q ^ ((r >> 1) & 3)) << 4);
-}
+// chunks; chunk q of row r sits at position q ^ swz(r). With
+// swz(r) = ((r >> 1) ^ (r >> 2)) & 3 the fragment reads of both MFMA shapes
+// (16 or 32 consecutive rows at one chunk) are free of bank conflicts on
+// gfx950's 64-bank LDS (measured: ~200 B/clk/CU, against ~110 for the
+// 2-way-conflicted (r >> 1) & 3).
+__device__ __forceinline__ int swz(int row) { return ((row >> 1) ^ (row >> 2)) & 3; }
+__device__ __forceinline__ int lds_off(int row, int q) { return row * 64 + ((q ^ swz(row)) << 4); }
 
 __device__ __forceinline__ u32 perm(u32 hi, u32 lo, u32 sel) {
     return __builtin_amdgcn_perm(hi, lo, sel);
@@ -89,7 +125,7 @@ __device__ __forceinline__ u32 byte_mask(int v) {
 template <int ES>
 __device__ __forceinline__ v4i load_elems(const void *rowp, int e0, int len) {
     u32 w[4] = {0u, 0u, 0u, 0u};
-    if (ES == 1) {
+    if constexpr (ES == 1) {
         const uint8_t *p = (const uint8_t *)rowp;
 #pragma unroll
         for (int i = 0; i < 16; ++i)
@@ -117,14 +153,20 @@ __device__ __forceinline__ v4i load16(const void *rowp, int e0, int len) {
 }
 
 // ---------------------------------------------------------------------------
-template <int ES, int BM, int BN, int WM, int WN, bool VA, bool VB, bool SPLIT>
+template <int V>
+using ic = std::integral_constant<int, V>;
+
+template <int ES, int BM, int BN, int WM, int WN, int MF, bool VA, bool VB, bool SPLIT>
 __global__ void __launch_bounds__(256, 1)
 igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ Bp,
             int64_t ldb, int32_t *__restrict__ C, int64_t ldc, int m, int n, int k,
             int kchunk, int tiles_m, int tiles_n) {
-    constexpr int P = ES;                // limb planes per operand
+    constexpr int P = ES;                  // limb planes per operand
     constexpr int NACC = ES == 2 ? 3 : 1;  // accumulator sets
-    constexpr int TM = WM / 16, TN = WN / 16;
+    typedef Mfma<MF> M;
+    typedef typename M::acc_t acc_t;
+    constexpr int TM = WM / MF, TN = WN / MF;
+    static_assert(WM % MF == 0 && WN % MF == 0, "wave tile is a whole number of MFMA tiles");
     constexpr int WGN = BN / WN;
     static_assert((BM / WM) * WGN == 4, "four waves per workgroup");
     constexpr int APL = BM * 64, BPL = BN * 64;  // bytes per LDS plane
@@ -134,9 +176,12 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     constexpr int BUN = BN * ES;  // B units (4 rows x 16 bytes) per k-tile
     constexpr int BUT = (BUN + 255) / 256;
     constexpr int CPU = 16 / ES;  // columns per B unit
-    static_assert(2 * STAGE >= 4 * 2 * (BM + BN), "LDS reuse for the limb sums");
+    static_assert((ACH & (ACH - 1)) == 0 && (BUN & (BUN - 1)) == 0, "power-of-two staging");
+    constexpr int NST = 4;  // LDS stages of the pipeline
+    static_assert(NST * STAGE >= 4 * 2 * (BM + BN), "LDS reuse for the limb sums");
+    static_assert(NST * STAGE <= 160 * 1024, "gfx950 LDS");
 
-    __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
+    __shared__ __attribute__((aligned(16))) char smem[NST * STAGE];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -164,13 +209,63 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     const int kbeg = z * kchunk;
     const int kend = min(k, kbeg + kchunk);
     if (kbeg >= kend) return;  // uniform over the workgroup
-    const int ktiles = (kend - kbeg + 63) >> 6;
 
     const int8_t *A8 = (const int8_t *)Ap;
     const int8_t *B8 = (const int8_t *)Bp;
 
-    v4i ra[ACT];
-    v4i rb[BUT][4];
+    // ---- per-thread staging geometry (fixed over the k loop) ---------------
+    // Slots beyond the tile (fewer chunks than threads) repeat a real chunk;
+    // they write the same bytes to the same LDS address and are left out of
+    // the limb sums.
+    int a_row[ACT], a_q[ACT], a_woff[ACT];
+    bool a_dup[ACT];
+#pragma unroll
+    for (int s = 0; s < ACT; ++s) {
+        const int c = tid + 256 * s;
+        a_dup[s] = c >= ACH;
+        const int ce = c & (ACH - 1);
+        a_row[s] = ce / (4 * ES);
+        a_q[s] = ce % (4 * ES);
+        a_woff[s] = ES == 1 ? lds_off(a_row[s], a_q[s])
+                            : lds_off(a_row[s], a_q[s] >> 1) + ((a_q[s] & 1) << 3);
+    }
+    int b_rg[BUT], b_cc[BUT];
+    bool b_dup[BUT];
+    int b_wbase[BUT][4];  // [slot][compile-time swizzle class of the column]
+#pragma unroll
+    for (int s = 0; s < BUT; ++s) {
+        const int u = tid + 256 * s;
+        b_dup[s] = u >= BUN;
+        const int ue = u & (BUN - 1);
+        // Consecutive lanes take consecutive row groups: their transposed LDS
+        // writes then spread over all banks. (Taking consecutive column chunks
+        // instead reads whole cache lines per load, but puts sixteen lanes of
+        // one LDS write on the same banks, which measured slower.)
+        b_rg[s] = ue & 15;
+        b_cc[s] = ue >> 4;
+        // Column col = cc*CPU + c' of the unit goes to LDS row col, chunk
+        // q ^ swz(col). For CPU = 16, swz(col) = g(c'); for CPU = 8,
+        // swz(col) = g(c') ^ 2*(cc & 1), with g(c') = ((c' >> 1) ^ (c' >> 2)) & 3.
+        // So the offset is a per-thread base for each g plus c' * 64.
+        const int q = (b_rg[s] >> 2) ^ (CPU == 8 ? ((b_cc[s] & 1) << 1) : 0);
+        const int base = b_cc[s] * CPU * 64 + ((b_rg[s] & 3) << 2);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) b_wbase[s][g] = base + ((q ^ g) << 4);
+    }
+    // Fragment read bases (LDS byte offsets within a stage).
+    // Fragment read bases: the MFMA tile rows start at multiples of 16, so
+    // swz(row) depends only on the lane's row within the tile.
+    const int fr = M::frag_row(lane);
+    int a_rbase[M::KSTEPS], b_rbase[M::KSTEPS];
+#pragma unroll
+    for (int ks = 0; ks < M::KSTEPS; ++ks) {
+        const int cq = (M::frag_chunk(lane, ks) ^ swz(fr)) << 4;
+        a_rbase[ks] = (wm0 + fr) * 64 + cq;
+        b_rbase[ks] = (wn0 + fr) * 64 + cq;
+    }
+
+    v4i ra[2][ACT];
+    v4i rb[2][BUT][4];
     int sah[ACT], sal[ACT];
     int sbh[BUT][8], sbl[BUT][8];
 #pragma unroll
@@ -180,113 +275,127 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
 #pragma unroll
         for (int c = 0; c < 8; ++c) sbh[s][c] = sbl[s][c] = 0;
 
-    v4i acc[NACC][TM][TN];
+    acc_t acc[NACC][TM][TN];
 #pragma unroll
     for (int a = 0; a < NACC; ++a)
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int j = 0; j < TN; ++j) acc[a][i][j] = v4i{0, 0, 0, 0};
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int r = 0; r < M::REGS; ++r) acc[a][i][j][r] = 0;
 
-    // ---- global -> registers ------------------------------------------------
-    auto load_tile = [&](int k0) {
+    // ---- global -> registers, interior tiles: no bounds checks --------------
+    // Row offsets fit in 32 bits (checked on the host), so each load is a
+    // uniform 64-bit base plus a 32-bit per-lane offset.
+    uint32_t a_goff[ACT], b_goff[BUT];
+#pragma unroll
+    for (int s = 0; s < ACT; ++s)
+        a_goff[s] = (uint32_t)(((int64_t)a_row[s] * lda + a_q[s] * (16 / ES)) * ES);
+#pragma unroll
+    for (int s = 0; s < BUT; ++s)
+        b_goff[s] = (uint32_t)(((int64_t)(4 * b_rg[s]) * ldb + b_cc[s] * CPU) * ES);
+    const int64_t ldb_bytes = ldb * ES;
+    const int8_t *a_tile0 = A8 + (int64_t)m0 * lda * ES;
+    const int8_t *b_tile0 = B8 + (int64_t)n0 * ES;
+
+    auto load_fast = [&](auto par, int k0) {
+        constexpr int R = decltype(par)::value;
+        const int8_t *ab = a_tile0 + (int64_t)k0 * ES;
+#pragma unroll
+        for (int s = 0; s < ACT; ++s) ra[R][s] = *(const v4i *)(ab + a_goff[s]);
+        const int8_t *bb = b_tile0 + (int64_t)k0 * ldb_bytes;
+#pragma unroll
+        for (int s = 0; s < BUT; ++s)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                rb[R][s][r] = *(const v4i *)(bb + r * ldb_bytes + b_goff[s]);
+    };
+
+    // ---- global -> registers, any tile: per-element bounds -------------------
+    auto load_safe = [&](auto par, int k0) {
+        constexpr int R = decltype(par)::value;
         const int klen = kend - k0;
 #pragma unroll
         for (int s = 0; s < ACT; ++s) {
-            const int c = tid + 256 * s;
-            if (ACH % 256 == 0 || c < ACH) {
-                const int row = c / (4 * ES), q = c % (4 * ES);
-                const int gi = m0 + row;
-                const int len = gi < m ? klen : 0;
-                const int gic = gi < m ? gi : m - 1;
-                const void *rowp = A8 + ((int64_t)gic * lda + k0) * ES;
-                ra[s] = load16<ES, VA>(rowp, q * (16 / ES), len);
-            }
+            const int gi = m0 + a_row[s];
+            const int len = gi < m ? klen : 0;
+            const int gic = gi < m ? gi : m - 1;
+            const void *rowp = A8 + ((int64_t)gic * lda + k0) * ES;
+            ra[R][s] = load16<ES, VA>(rowp, a_q[s] * (16 / ES), len);
         }
         const int nlen = n - n0;
 #pragma unroll
         for (int s = 0; s < BUT; ++s) {
-            const int u = tid + 256 * s;
-            if (BUN % 256 == 0 || u < BUN) {
-                const int rg = u & 15, cc = u >> 4;
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int p = k0 + 4 * rg + r;
-                    const int len = p < kend ? nlen : 0;
-                    const int pc = p < kend ? p : kend - 1;
-                    const void *rowp = B8 + ((int64_t)pc * ldb + n0) * ES;
-                    rb[s][r] = load16<ES, VB>(rowp, cc * CPU, len);
-                }
+            for (int r = 0; r < 4; ++r) {
+                const int p = k0 + 4 * b_rg[s] + r;
+                const int len = p < kend ? nlen : 0;
+                const int pc = p < kend ? p : kend - 1;
+                const void *rowp = B8 + ((int64_t)pc * ldb + n0) * ES;
+                rb[R][s][r] = load16<ES, VB>(rowp, b_cc[s] * CPU, len);
             }
         }
     };
 
-    // ---- registers -> LDS (limb split, B transpose, limb sums) ------------
-    auto store_tile = [&](int buf, int k0) {
-        char *As = smem + buf * STAGE;
+    // ---- registers -> LDS (limb split, B transpose, limb sums) --------------
+    // MASK: zero the limbs of elements at or beyond kend (last k-tile only).
+    auto store_tile = [&](auto par, auto buf, auto mask, int k0) {
+        constexpr int R = decltype(par)::value;
+        constexpr int BUF = decltype(buf)::value;
+        constexpr bool MASK = decltype(mask)::value != 0;
+        char *As = smem + BUF * STAGE;
         char *Bs = As + P * APL;
-        const bool ktail = k0 + 64 > kend;
 #pragma unroll
         for (int s = 0; s < ACT; ++s) {
-            const int c = tid + 256 * s;
-            if (ACH % 256 == 0 || c < ACH) {
-                const int row = c / (4 * ES), q = c % (4 * ES);
-                if (ES == 1) {
-                    *(v4i *)(As + lds_off_a(row, q)) = ra[s];
-                } else {
-                    const u32 y0 = ra[s].x, y1 = ra[s].y, y2 = ra[s].z, y3 = ra[s].w;
-                    u32 h0 = perm(y1, y0, 0x07050301u), h1 = perm(y3, y2, 0x07050301u);
-                    u32 l0 = perm(y1, y0, 0x06040200u) ^ 0x80808080u;
-                    u32 l1 = perm(y3, y2, 0x06040200u) ^ 0x80808080u;
-                    if (ktail) {
-                        const int v = kend - k0 - q * 8;
-                        const u32 m0k = byte_mask(v), m1k = byte_mask(v - 4);
-                        h0 &= m0k;
-                        l0 &= m0k;
-                        h1 &= m1k;
-                        l1 &= m1k;
-                    }
-                    sah[s] = sum4(h1, sum4(h0, sah[s]));
-                    sal[s] = sum4(l1, sum4(l0, sal[s]));
-                    const int off = lds_off_a(row, q >> 1) + ((q & 1) << 3);
-                    *(uint2 *)(As + off) = make_uint2(h0, h1);
-                    *(uint2 *)(As + APL + off) = make_uint2(l0, l1);
+            if constexpr (ES == 1) {
+                *(v4i *)(As + a_woff[s]) = ra[R][s];
+            } else {
+                const u32 y0 = ra[R][s].x, y1 = ra[R][s].y, y2 = ra[R][s].z, y3 = ra[R][s].w;
+                u32 h0 = perm(y1, y0, 0x07050301u), h1 = perm(y3, y2, 0x07050301u);
+                u32 l0 = perm(y1, y0, 0x06040200u) ^ 0x80808080u;
+                u32 l1 = perm(y3, y2, 0x06040200u) ^ 0x80808080u;
+                if constexpr (MASK) {
+                    const int v = kend - k0 - a_q[s] * 8;
+                    const u32 m0k = byte_mask(v), m1k = byte_mask(v - 4);
+                    h0 &= m0k;
+                    l0 &= m0k;
+                    h1 &= m1k;
+                    l1 &= m1k;
                 }
+                sah[s] = sum4(h1, sum4(h0, sah[s]));
+                sal[s] = sum4(l1, sum4(l0, sal[s]));
+                *(uint2 *)(As + a_woff[s]) = make_uint2(h0, h1);
+                *(uint2 *)(As + APL + a_woff[s]) = make_uint2(l0, l1);
             }
         }
 #pragma unroll
         for (int s = 0; s < BUT; ++s) {
-            const int u = tid + 256 * s;
-            if (BUN % 256 == 0 || u < BUN) {
-                const int rg = u & 15, cc = u >> 4;
-                const int q = rg >> 2, sub = (rg & 3) << 2;
-                u32 rmask = 0xffffffffu;
-                if (ES == 2 && ktail) rmask = byte_mask(kend - (k0 + 4 * rg));
+            u32 rmask = 0xffffffffu;
+            if constexpr (ES == 2 && MASK) rmask = byte_mask(kend - (k0 + 4 * b_rg[s]));
 #pragma unroll
-                for (int d = 0; d < 4; ++d) {
-                    u32 y0, y1, y2, y3;
-                    transpose4x4((u32)rb[s][0][d], (u32)rb[s][1][d], (u32)rb[s][2][d],
-                                 (u32)rb[s][3][d], y0, y1, y2, y3);
-                    if (ES == 1) {
-                        const int col = cc * 16 + 4 * d;
-                        *(u32 *)(Bs + lds_off_b(col + 0, q) + sub) = y0;
-                        *(u32 *)(Bs + lds_off_b(col + 1, q) + sub) = y1;
-                        *(u32 *)(Bs + lds_off_b(col + 2, q) + sub) = y2;
-                        *(u32 *)(Bs + lds_off_b(col + 3, q) + sub) = y3;
-                    } else {
-                        // y0/y2: low bytes of columns 2d, 2d+1; y1/y3: high bytes.
-                        const u32 la = (y0 ^ 0x80808080u) & rmask, ha = y1 & rmask;
-                        const u32 lb = (y2 ^ 0x80808080u) & rmask, hb = y3 & rmask;
-                        sbh[s][2 * d] = sum4(ha, sbh[s][2 * d]);
-                        sbl[s][2 * d] = sum4(la, sbl[s][2 * d]);
-                        sbh[s][2 * d + 1] = sum4(hb, sbh[s][2 * d + 1]);
-                        sbl[s][2 * d + 1] = sum4(lb, sbl[s][2 * d + 1]);
-                        const int col = cc * 8 + 2 * d;
-                        const int oa = lds_off_b(col, q) + sub, ob = lds_off_b(col + 1, q) + sub;
-                        *(u32 *)(Bs + oa) = ha;
-                        *(u32 *)(Bs + BPL + oa) = la;
-                        *(u32 *)(Bs + ob) = hb;
-                        *(u32 *)(Bs + BPL + ob) = lb;
+            for (int d = 0; d < 4; ++d) {
+                u32 y[4];
+                transpose4x4((u32)rb[R][s][0][d], (u32)rb[R][s][1][d], (u32)rb[R][s][2][d],
+                             (u32)rb[R][s][3][d], y[0], y[1], y[2], y[3]);
+                if constexpr (ES == 1) {
+#pragma unroll
+                    for (int t4 = 0; t4 < 4; ++t4) {
+                        const int cp = 4 * d + t4;  // column within the unit
+                        *(u32 *)(Bs + b_wbase[s][((cp >> 1) ^ (cp >> 2)) & 3] + cp * 64) = y[t4];
+                    }
+                } else {
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        // y[2h]: low bytes of column 2d+h, y[2h+1]: high bytes.
+                        const u32 lo = (y[2 * h] ^ 0x80808080u) & rmask;
+                        const u32 hi = y[2 * h + 1] & rmask;
+                        const int cp = 2 * d + h;
+                        sbh[s][cp] = sum4(hi, sbh[s][cp]);
+                        sbl[s][cp] = sum4(lo, sbl[s][cp]);
+                        const int off = b_wbase[s][((cp >> 1) ^ (cp >> 2)) & 3] + cp * 64;
+                        *(u32 *)(Bs + off) = hi;
+                        *(u32 *)(Bs + BPL + off) = lo;
                     }
                 }
             }
@@ -294,95 +403,162 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     };
 
     // ---- MFMA over one k-tile ----------------------------------------------
-    auto compute = [&](int buf) {
-        const char *As = smem + buf * STAGE;
+    // ---- LDS -> fragment registers, and the MFMAs of one k sub-step ---------
+    // Two fragment slots: the MFMAs of one sub-step run on one slot while the
+    // next sub-step's fragments load into the other.
+    v4i fa[2][P][TM], fb[2][P][TN];
+    auto read_frags = [&](auto slot, auto buf, auto ks) {
+        constexpr int SL = decltype(slot)::value;
+        constexpr int BUF = decltype(buf)::value;
+        constexpr int KS = decltype(ks)::value;
+        const char *As = smem + BUF * STAGE;
         const char *Bs = As + P * APL;
-        const int fr = lane & 15, fq = lane >> 4;
-        v4i af[P][TM], bf[P][TN];
 #pragma unroll
         for (int p = 0; p < P; ++p) {
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-                af[p][i] = *(const v4i *)(As + p * APL + lds_off_a(wm0 + 16 * i + fr, fq));
-#pragma unroll
             for (int j = 0; j < TN; ++j)
-                bf[p][j] = *(const v4i *)(Bs + p * BPL + lds_off_b(wn0 + 16 * j + fr, fq));
+                fb[SL][p][j] = *(const v4i *)(Bs + p * BPL + b_rbase[KS] + j * MF * 64);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                fa[SL][p][i] = *(const v4i *)(As + p * APL + a_rbase[KS] + i * MF * 64);
         }
-        if (ES == 1) {
+    };
+    auto mfmas = [&](auto slot) {
+        constexpr int SL = decltype(slot)::value;
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j)
-                    acc[0][i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[0][i], bf[0][j],
-                                                                         acc[0][i][j], 0, 0, 0);
-        } else {
-            // plane 0 = high limbs, plane 1 = offset low limbs
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
+        for (int i = 0; i < TM; ++i) {
+            if constexpr (ES == 1) {
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[0][i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[0][i], bf[0][j],
-                                                                         acc[0][i][j], 0, 0, 0);
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j)
-                    acc[1][i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[0][i], bf[1][j],
-                                                                         acc[1][i][j], 0, 0, 0);
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
+                    acc[0][i][j] = M::mma(fa[SL][0][i], fb[SL][0][j], acc[0][i][j]);
+            } else {
+                // plane 0 = high limbs, plane 1 = offset low limbs
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[2][i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[1][i], bf[1][j],
-                                                                         acc[2][i][j], 0, 0, 0);
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
+                    acc[0][i][j] = M::mma(fa[SL][0][i], fb[SL][0][j], acc[0][i][j]);
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[1][i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[1][i], bf[0][j],
-                                                                         acc[1][i][j], 0, 0, 0);
+                    acc[1][i][j] = M::mma(fa[SL][0][i], fb[SL][1][j], acc[1][i][j]);
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[2][i][j] = M::mma(fa[SL][1][i], fb[SL][1][j], acc[2][i][j]);
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[1][i][j] = M::mma(fa[SL][1][i], fb[SL][0][j], acc[1][i][j]);
+            }
         }
     };
 
-    // ---- main loop: double-buffered LDS, next tile's loads in flight -------
-    load_tile(kbeg);
-    store_tile(0, kbeg);
-    __syncthreads();
-    for (int kt = 0; kt < ktiles; ++kt) {
-        const bool more = kt + 1 < ktiles;
-        const int knext = kbeg + (kt + 1) * 64;
-        if (more) load_tile(knext);
-        compute(kt & 1);
-        if (more) store_tile((kt + 1) & 1, knext);
+    // One pipelined k-tile kt with S = kt mod 4. On entry LDS stages S and
+    // S+1 hold tiles kt and kt+1, register set S&1 holds (or is receiving)
+    // tile kt+2, and fragment slot 0 holds sub-step 0 of tile kt. The step
+    // starts loading tile kt+3 into register set (S+1)&1, runs the MFMAs of
+    // tile kt while reading the next sub-step's fragments (the last one from
+    // stage S+1, already complete), writes tile kt+2 into stage S+2, and ends
+    // with one barrier.
+    auto step = [&](auto phase, auto do_load, auto do_store, auto do_pref, int kt) {
+        constexpr int S = decltype(phase)::value;
+        if (decltype(do_load)::value) load_fast(ic<(S + 1) & 1>{}, kbeg + (kt + 3) * 64);
+        if constexpr (M::KSTEPS == 2) {
+            // sub-step 0 on slot 0 while sub-step 1 loads into slot 1
+            read_frags(ic<1>{}, ic<S>{}, ic<1>{});
+            mfmas(ic<0>{});
+            // sub-step 1 on slot 1 while tile kt+2 is staged and the next
+            // tile's sub-step 0 loads into slot 0
+            if (decltype(do_store)::value)
+                store_tile(ic<S & 1>{}, ic<(S + 2) & 3>{}, ic<0>{}, kbeg + (kt + 2) * 64);
+            if (decltype(do_pref)::value) read_frags(ic<0>{}, ic<(S + 1) & 3>{}, ic<0>{});
+            mfmas(ic<1>{});
+        } else {
+            // one sub-step per tile; tiles alternate between the slots
+            constexpr int SL = S & 1;
+            if (decltype(do_store)::value)
+                store_tile(ic<S & 1>{}, ic<(S + 2) & 3>{}, ic<0>{}, kbeg + (kt + 2) * 64);
+            if (decltype(do_pref)::value) read_frags(ic<1 - SL>{}, ic<(S + 1) & 3>{}, ic<0>{});
+            mfmas(ic<SL>{});
+        }
         __syncthreads();
+    };
+
+    // One unpipelined k-tile through LDS stage 0 with bounds checks.
+    auto safe_tile = [&](int k0) {
+        load_safe(ic<0>{}, k0);
+        if (k0 + 64 > kend)
+            store_tile(ic<0>{}, ic<0>{}, ic<1>{}, k0);
+        else
+            store_tile(ic<0>{}, ic<0>{}, ic<0>{}, k0);
+        __syncthreads();
+        read_frags(ic<0>{}, ic<0>{}, ic<0>{});
+        mfmas(ic<0>{});
+        if constexpr (M::KSTEPS == 2) {
+            read_frags(ic<0>{}, ic<0>{}, ic<1>{});
+            mfmas(ic<0>{});
+        }
+        __syncthreads();
+    };
+
+    // ---- main loop ------------------------------------------------------------
+    // Interior workgroups run a multiple of four full k-tiles through the
+    // pipeline; the leading remainder of full tiles, the partial last tile and
+    // every edge workgroup take the bounds-checked single-tile path.
+    const int nfull = (kend - kbeg) >> 6;  // k-tiles with all 64 elements inside
+    const bool interior = VA && VB && (m0 + BM <= m) && (n0 + BN <= n);
+    const int npipe = interior ? (nfull & ~3) : 0;
+    const int klead = kbeg + (nfull - npipe) * 64 * (npipe > 0);
+    if (npipe > 0)
+        for (int k0 = kbeg; k0 < klead; k0 += 64) safe_tile(k0);
+    if constexpr (VA && VB) {
+        if (npipe > 0) {
+            const int kb = klead;  // first pipelined k-tile
+            // Prologue: tiles 0, 1 into stages 0, 1; tile 2 into register
+            // set 0; fragments of tile 0, sub-step 0 into slot 0.
+            load_fast(ic<0>{}, kb);
+            load_fast(ic<1>{}, kb + 64);
+            store_tile(ic<0>{}, ic<0>{}, ic<0>{}, kb);
+            store_tile(ic<1>{}, ic<1>{}, ic<0>{}, kb + 64);
+            load_fast(ic<0>{}, kb + 128);
+            __syncthreads();
+            read_frags(ic<0>{}, ic<0>{}, ic<0>{});
+            // The steps address tiles relative to kbeg; shift by the lead.
+            const int t0 = (kb - kbeg) >> 6;
+            int kt = 0;
+            for (; kt < npipe - 4; kt += 4) {
+                step(ic<0>{}, ic<1>{}, ic<1>{}, ic<1>{}, t0 + kt);
+                step(ic<1>{}, ic<1>{}, ic<1>{}, ic<1>{}, t0 + kt + 1);
+                step(ic<2>{}, ic<1>{}, ic<1>{}, ic<1>{}, t0 + kt + 2);
+                step(ic<3>{}, ic<1>{}, ic<1>{}, ic<1>{}, t0 + kt + 3);
+            }
+            step(ic<0>{}, ic<1>{}, ic<1>{}, ic<1>{}, t0 + kt);
+            step(ic<1>{}, ic<0>{}, ic<1>{}, ic<1>{}, t0 + kt + 1);
+            step(ic<2>{}, ic<0>{}, ic<0>{}, ic<1>{}, t0 + kt + 2);
+            step(ic<3>{}, ic<0>{}, ic<0>{}, ic<0>{}, t0 + kt + 3);
+        }
     }
+    const int ktail = npipe > 0 ? klead + npipe * 64 : kbeg;
+    for (int k0 = ktail; k0 < kend; k0 += 64) safe_tile(k0);
 
     // ---- epilogue -------------------------------------------------------------
     int *sRH = (int *)smem;
     int *sRL = sRH + BM;
     int *sKH = sRL + BM;
     int *sKL = sKH + BN;
-    if (ES == 2) {
+    if constexpr (ES == 2) {
         for (int i = tid; i < 2 * (BM + BN); i += 256) sRH[i] = 0;
         __syncthreads();
 #pragma unroll
         for (int s = 0; s < ACT; ++s) {
-            const int c = tid + 256 * s;
-            if (ACH % 256 == 0 || c < ACH) {
-                const int row = c / 8;
-                atomicAdd(&sRH[row], sah[s]);
-                atomicAdd(&sRL[row], sal[s]);
+            if (!a_dup[s]) {
+                atomicAdd(&sRH[a_row[s]], sah[s]);
+                atomicAdd(&sRL[a_row[s]], sal[s]);
             }
         }
 #pragma unroll
         for (int s = 0; s < BUT; ++s) {
-            const int u = tid + 256 * s;
-            if (BUN % 256 == 0 || u < BUN) {
-                const int cc = u >> 4;
+            if (!b_dup[s]) {
 #pragma unroll
                 for (int c = 0; c < 8; ++c) {
-                    atomicAdd(&sKH[cc * 8 + c], sbh[s][c]);
-                    atomicAdd(&sKL[cc * 8 + c], sbl[s][c]);
+                    atomicAdd(&sKH[b_cc[s] * 8 + c], sbh[s][c]);
+                    atomicAdd(&sKL[b_cc[s] * 8 + c], sbl[s][c]);
                 }
             }
         }
@@ -393,16 +569,16 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-            const int lc = wn0 + 16 * j + (lane & 15);
+            const int lc = wn0 + MF * j + M::out_col(lane);
             const int gc = n0 + lc;
             u32 colterm = 0;
-            if (ES == 2) colterm = 32768u * (u32)sKH[lc] + 128u * (u32)sKL[lc] + kconst;
+            if constexpr (ES == 2) colterm = 32768u * (u32)sKH[lc] + 128u * (u32)sKL[lc] + kconst;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int lr = wm0 + 16 * i + 4 * (lane >> 4) + r;
+            for (int r = 0; r < M::REGS; ++r) {
+                const int lr = wm0 + MF * i + M::out_row(lane, r);
                 const int gr = m0 + lr;
                 u32 v;
-                if (ES == 1) {
+                if constexpr (ES == 1) {
                     v = (u32)acc[0][i][j][r];
                 } else {
                     v = 65536u * (u32)acc[0][i][j][r] + 256u * (u32)acc[1][i][j][r] +
@@ -418,13 +594,15 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
                 }
             }
         }
+        // Keep the scheduler from hoisting every C load of the tile at once.
+        __builtin_amdgcn_sched_barrier(0);
     }
 }
 
 // ---------------------------------------------------------------------------
-template <int ES, int BM, int BN, int WM, int WN>
+template <int ES, int BM, int BN, int WM, int WN, int MF>
 const void *pick(bool va, bool vb, bool split) {
-#define IGEMM_K(a, b, s) (const void *)&igemm_tiled<ES, BM, BN, WM, WN, a, b, s>
+#define IGEMM_K(a, b, s) (const void *)&igemm_tiled<ES, BM, BN, WM, WN, MF, a, b, s>
     if (split) {
         if (va) return vb ? IGEMM_K(true, true, true) : IGEMM_K(true, false, true);
         return vb ? IGEMM_K(false, true, true) : IGEMM_K(false, false, true);
@@ -436,14 +614,14 @@ const void *pick(bool va, bool vb, bool split) {
 
 const void *kernel_fn(int id, bool va, bool vb, bool split) {
     switch (id) {
-        case K_I8_256x256: return pick<1, 256, 256, 128, 128>(va, vb, split);
-        case K_I8_128x128: return pick<1, 128, 128, 64, 64>(va, vb, split);
-        case K_I8_32x256: return pick<1, 32, 256, 32, 64>(va, vb, split);
-        case K_I8_16x256: return pick<1, 16, 256, 16, 64>(va, vb, split);
-        case K_I16_128x128: return pick<2, 128, 128, 64, 64>(va, vb, split);
-        case K_I16_64x64: return pick<2, 64, 64, 32, 32>(va, vb, split);
-        case K_I16_32x128: return pick<2, 32, 128, 32, 32>(va, vb, split);
-        case K_I16_16x128: return pick<2, 16, 128, 16, 32>(va, vb, split);
+        case K_I8_256x256: return pick<1, 256, 256, 128, 128, 32>(va, vb, split);
+        case K_I8_128x128: return pick<1, 128, 128, 64, 64, 32>(va, vb, split);
+        case K_I8_32x256: return pick<1, 32, 256, 32, 64, 32>(va, vb, split);
+        case K_I8_16x256: return pick<1, 16, 256, 16, 64, 16>(va, vb, split);
+        case K_I16_128x128: return pick<2, 128, 128, 64, 64, 32>(va, vb, split);
+        case K_I16_64x64: return pick<2, 64, 64, 32, 32, 32>(va, vb, split);
+        case K_I16_32x128: return pick<2, 32, 128, 32, 32, 32>(va, vb, split);
+        case K_I16_16x128: return pick<2, 16, 128, 16, 32, 16>(va, vb, split);
         default: return nullptr;
     }
 }

@@ -124,8 +124,10 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
     out->tiles = tiles;
     out->grid = grid;
     const uintptr_t a = (uintptr_t)A, b = (uintptr_t)B;
-    out->vec_a = (a % 16 == 0) && ((lda * es) % 16 == 0);
-    out->vec_b = (b % 16 == 0) && ((ldb * es) % 16 == 0);
+    // Vector path: 16-byte aligned rows, and per-lane row offsets within one
+    // workgroup tile that fit in 32 bits (bm rows of A, 64 rows of B).
+    out->vec_a = (a % 16 == 0) && ((lda * es) % 16 == 0) && ((int64_t)d.bm * lda * es < INT_MAX);
+    out->vec_b = (b % 16 == 0) && ((ldb * es) % 16 == 0) && ((int64_t)kBK * ldb * es < INT_MAX);
     return IGEMM_OK;
 }
 
