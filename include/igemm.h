@@ -20,11 +20,23 @@
  * (n, m, k, B, ldb, A, lda, C, ldc).
  *
  * Ownership and memory: A, B and C are DEVICE pointers owned by the caller
- * (allocated by any HIP allocator; the library never frees them). The
- * library allocates no device memory and keeps no per-call state; C itself
+ * (allocated by any HIP allocator; the library never frees them). C itself
  * is the only output buffer. C must not overlap A or B (not checked).
  * Pointers and leading dimensions of any alignment are accepted; 16-byte
  * aligned rows take the vector-load path, others a slower element path.
+ *
+ * Workspace: large products take the packed path (Sec. 4.1's packing of the
+ * A and B panels into contiguous buffers, done once per call for the whole
+ * operands): pack kernels rearrange A and B into a device workspace, then
+ * the main kernel multiplies the packed copies. igemm_query_plan reports
+ * the workspace a call needs (plan.workspace_bytes, 0 for the fused
+ * kernels). The _ws calls take a caller-owned workspace; the other calls
+ * draw it from a stream-ordered memory pool that the library owns, one per
+ * device, allocated and released on `stream` around the launches (the pool
+ * keeps freed memory for reuse until igemm_trim_workspace). While `stream`
+ * is being captured into a graph those calls never use the pool: automatic
+ * kernel choice then takes a fused kernel, and an explicit packed kernel
+ * returns IGEMM_EINVAL.
  *
  * Asynchrony and errors: every entry point validates its arguments on the
  * host and returns IGEMM_EINVAL before making any HIP call if they are
@@ -47,7 +59,10 @@ typedef enum igemm_status {
     IGEMM_OK = 0,
     IGEMM_EINVAL = -1,  /* invalid argument; nothing was enqueued          */
     IGEMM_EHIP = -2,    /* a HIP runtime call or kernel launch failed      */
-    IGEMM_ENOTSUP = -3  /* valid but unsupported (a size beyond 2^31 - 1)  */
+    IGEMM_ENOTSUP = -3, /* valid but unsupported (a size beyond 2^31 - 1,  */
+                        /* or a grid beyond 2^24 workgroups)              */
+    IGEMM_ENOMEM = -4   /* workspace allocation failed, or the caller's    */
+                        /* workspace is smaller than the plan needs        */
 } igemm_status;
 
 /*
@@ -82,7 +97,8 @@ int igemm_i8(int64_t m, int64_t n, int64_t k,
  *   split    -1 = automatic, otherwise the number of slices the k range is
  *            cut into (>= 1); slices add their partial results into C with
  *            32-bit atomic adds, which are exact modulo 2^32 in any order.
- *            Values above ceil(k/64) are reduced to it.
+ *            Values above ceil(k/64) are reduced to it. Packed kernels
+ *            ignore it: they always run one launch per 32768 k elements.
  * Semantics, memory and errors are those of igemm_i16 / igemm_i8.
  */
 int igemm_i16_ex(int64_t m, int64_t n, int64_t k,
@@ -97,7 +113,9 @@ int igemm_i8_ex(int64_t m, int64_t n, int64_t k,
                 int kernel, int split);
 
 /* The launch the library would make for a call (host only, no HIP call).
- * Filled by igemm_query_plan. */
+ * Filled by igemm_query_plan. For packed kernels split is the number of
+ * main-kernel launches (one per k chunk of k_chunk elements) and grid the
+ * workgroups of each. */
 typedef struct igemm_plan {
     int kernel;        /* kernel index                                     */
     int elem_bytes;    /* 2 = int16 operands, 1 = int8                     */
@@ -109,6 +127,8 @@ typedef struct igemm_plan {
     int threads;       /* threads per workgroup                            */
     int vec_a, vec_b;  /* 1 if A / B rows take 16-byte vector loads        */
     int limb_products; /* int8 MFMA products per operand pair: 4 or 1      */
+    int packed;        /* 1 if operands are packed into a workspace first  */
+    int64_t workspace_bytes; /* device workspace the call needs (0: none)  */
 } igemm_plan;
 
 /*
@@ -122,6 +142,35 @@ int igemm_query_plan(int elem_bytes, int64_t m, int64_t n, int64_t k,
                      const void *A, int64_t lda, const void *B, int64_t ldb,
                      const void *C, int64_t ldc, int num_cu,
                      int kernel, int split, igemm_plan *out);
+
+/*
+ * The expert calls with a caller-owned workspace (for callers that manage
+ * device memory themselves, e.g. a framework's caching allocator, or that
+ * capture the call into a graph):
+ *   workspace        device pointer, 256-byte aligned (IGEMM_EINVAL
+ *                    otherwise), at least workspace_bytes long, or NULL to
+ *                    use the library's pool as the calls above do.
+ *   workspace_bytes  its size; IGEMM_ENOMEM (nothing enqueued) if it is
+ *                    smaller than the plan's workspace_bytes.
+ * The workspace is read and written by the kernels enqueued on `stream`; it
+ * must not be reused by other work until they have finished. A call whose
+ * plan needs no workspace ignores both arguments.
+ */
+int igemm_i16_ws(int64_t m, int64_t n, int64_t k,
+                 const int16_t *A, int64_t lda,
+                 const int16_t *B, int64_t ldb,
+                 int32_t *C, int64_t ldc, void *stream,
+                 int kernel, int split, void *workspace, int64_t workspace_bytes);
+int igemm_i8_ws(int64_t m, int64_t n, int64_t k,
+                const int8_t *A, int64_t lda,
+                const int8_t *B, int64_t ldb,
+                int32_t *C, int64_t ldc, void *stream,
+                int kernel, int split, void *workspace, int64_t workspace_bytes);
+
+/* Release the memory the library's workspace pool for the current device
+ * holds beyond what in-flight calls use (hipMemPoolTrimTo). Returns
+ * IGEMM_OK, or IGEMM_EHIP. */
+int igemm_trim_workspace(void);
 
 /* Number of kernels, and a static name for index `kernel` (NULL if out of
  * range). */

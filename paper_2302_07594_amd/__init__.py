@@ -3,19 +3,26 @@
 The functions here marshal arguments into the C ABI of ``include/igemm.h``
 with ctypes; every step of the computation runs in the HIP library. PyTorch
 is used only to hand over device pointers and the current HIP stream. There
-is no CPU fallback: if the library is missing, importing this package raises.
+is no CPU fallback: the library is loaded at the first call, and that call
+raises ImportError if it is not built (``build`` is importable without it).
 
 Same names as the C ABI:
     igemm_i16(m, n, k, A, lda, B, ldb, C, ldc, stream=None)
     igemm_i8 (m, n, k, A, lda, B, ldb, C, ldc, stream=None)
     igemm_i16_ex / igemm_i8_ex(..., kernel=-1, split=-1)
+    igemm_i16_ws / igemm_i8_ws(..., kernel=-1, split=-1, workspace=None,
+                               workspace_bytes=0)
+    igemm_trim_workspace()
     igemm_query_plan(elem_bytes, m, n, k, A, lda, B, ldb, C, ldc, num_cu=0,
                      kernel=-1, split=-1) -> dict
     igemm_strerror(status), igemm_kernel_name(i), igemm_num_kernels(),
     igemm_version()
 A, B, C may be integer device addresses or torch tensors (their data_ptr()).
 Tensor conveniences: gemm_i16(A, B, C) and gemm_i8(A, B, C) take 2-D CUDA
-tensors with unit stride along rows and update C in place.
+tensors with unit stride along rows and update C in place; a workspace the
+call needs is taken from torch's caching allocator (so the calls can be
+captured into a torch CUDA graph) unless workspace="library" asks for the
+library's own stream-ordered pool.
 """
 from __future__ import annotations
 
@@ -29,6 +36,7 @@ IGEMM_OK = 0
 IGEMM_EINVAL = -1
 IGEMM_EHIP = -2
 IGEMM_ENOTSUP = -3
+IGEMM_ENOMEM = -4
 
 
 class IgemmError(RuntimeError):
@@ -43,7 +51,8 @@ class _Plan(ctypes.Structure):
                 ("split", ctypes.c_int), ("k_chunk", ctypes.c_int64),
                 ("tiles", ctypes.c_int64), ("grid", ctypes.c_int64),
                 ("threads", ctypes.c_int), ("vec_a", ctypes.c_int), ("vec_b", ctypes.c_int),
-                ("limb_products", ctypes.c_int)]
+                ("limb_products", ctypes.c_int), ("packed", ctypes.c_int),
+                ("workspace_bytes", ctypes.c_int64)]
 
 
 def _load():
@@ -67,6 +76,10 @@ def _load():
         getattr(lib, name).restype = ci
         getattr(lib, name + "_ex").argtypes = gemm_args + [ci, ci]
         getattr(lib, name + "_ex").restype = ci
+        getattr(lib, name + "_ws").argtypes = gemm_args + [ci, ci, vp, i64]
+        getattr(lib, name + "_ws").restype = ci
+    lib.igemm_trim_workspace.argtypes = []
+    lib.igemm_trim_workspace.restype = ci
     lib.igemm_query_plan.argtypes = [ci, i64, i64, i64, vp, i64, vp, i64, vp, i64, ci, ci, ci,
                                      ctypes.POINTER(_Plan)]
     lib.igemm_query_plan.restype = ci
@@ -81,7 +94,23 @@ def _load():
     return lib
 
 
-_lib = _load()
+class _Lazy:
+    """Loads libigemm.so on first attribute access."""
+    _handle = None
+
+    def __getattr__(self, name):
+        if _Lazy._handle is None:
+            _Lazy._handle = _load()
+        return getattr(_Lazy._handle, name)
+
+
+_lib = _Lazy()
+
+
+def load() -> None:
+    """Load the HIP library now (raises ImportError if it is not built)."""
+    if _Lazy._handle is None:
+        _Lazy._handle = _load()
 
 
 def library_path() -> str:
@@ -132,6 +161,22 @@ def igemm_i16_ex(m, n, k, A, lda, B, ldb, C, ldc, stream=None, kernel=-1, split=
 
 def igemm_i8_ex(m, n, k, A, lda, B, ldb, C, ldc, stream=None, kernel=-1, split=-1) -> int:
     return _call("igemm_i8_ex", m, n, k, A, lda, B, ldb, C, ldc, stream, int(kernel), int(split))
+
+
+def igemm_i16_ws(m, n, k, A, lda, B, ldb, C, ldc, stream=None, kernel=-1, split=-1,
+                 workspace=None, workspace_bytes=0) -> int:
+    return _call("igemm_i16_ws", m, n, k, A, lda, B, ldb, C, ldc, stream, int(kernel),
+                 int(split), _addr(workspace), int(workspace_bytes))
+
+
+def igemm_i8_ws(m, n, k, A, lda, B, ldb, C, ldc, stream=None, kernel=-1, split=-1,
+                workspace=None, workspace_bytes=0) -> int:
+    return _call("igemm_i8_ws", m, n, k, A, lda, B, ldb, C, ldc, stream, int(kernel),
+                 int(split), _addr(workspace), int(workspace_bytes))
+
+
+def igemm_trim_workspace() -> int:
+    return int(_lib.igemm_trim_workspace())
 
 
 _PLACEHOLDER = 1 << 12  # aligned, non-NULL; the planner never dereferences it
@@ -209,22 +254,55 @@ def _check_tensors(A, B, C, torch_dtype, name):
     return m, n, k, ld(A), ld(B), ld(C)
 
 
-def gemm_i16(A, B, C, stream=None, kernel=-1, split=-1):
+_num_cu_cache = {}
+
+
+def _num_cu(device) -> int:
+    import torch
+    idx = device.index if device.index is not None else torch.cuda.current_device()
+    if idx not in _num_cu_cache:
+        _num_cu_cache[idx] = torch.cuda.get_device_properties(idx).multi_processor_count
+    return _num_cu_cache[idx]
+
+
+def _gemm(es, A, B, C, stream, kernel, split, workspace, name):
+    import torch
+    m, n, k, lda, ldb, ldc = _check_tensors(A, B, C, torch.int16 if es == 2 else torch.int8, name)
+    fn = igemm_i16_ws if es == 2 else igemm_i8_ws
+    ws, ws_bytes = None, 0
+    if workspace is None or workspace == "torch":
+        if m and n and k:
+            plan = igemm_query_plan(es, m, n, k, A, lda, B, ldb, C, ldc, _num_cu(C.device),
+                                    kernel, split)
+            if plan["workspace_bytes"] > 0:
+                ws_bytes = plan["workspace_bytes"]
+                ws = torch.empty(ws_bytes + 256, dtype=torch.uint8, device=C.device)
+                if stream is not None and hasattr(stream, "cuda_stream"):
+                    ws.record_stream(stream)
+                # the caching allocator hands out 512-byte aligned blocks
+                if ws.data_ptr() % 256:
+                    off = 256 - ws.data_ptr() % 256
+                    ws = ws[off:]
+    elif workspace == "library":
+        pass
+    elif hasattr(workspace, "data_ptr"):
+        ws, ws_bytes = workspace, workspace.numel() * workspace.element_size()
+    else:
+        raise ValueError(f"{name}: workspace must be None, 'torch', 'library' or a tensor")
+    st = fn(m, n, k, A, lda, B, ldb, C, ldc, stream, kernel, split, ws, ws_bytes)
+    if st != IGEMM_OK:
+        raise IgemmError(st, name)
+    return C
+
+
+def gemm_i16(A, B, C, stream=None, kernel=-1, split=-1, workspace=None):
     """C += A.B for 2-D torch.int16 CUDA tensors A (m x k), B (k x n) and a
-    torch.int32 C (m x n). Returns C. Raises IgemmError on a bad status."""
-    import torch
-    m, n, k, lda, ldb, ldc = _check_tensors(A, B, C, torch.int16, "gemm_i16")
-    st = igemm_i16_ex(m, n, k, A, lda, B, ldb, C, ldc, stream, kernel, split)
-    if st != IGEMM_OK:
-        raise IgemmError(st, "igemm_i16")
-    return C
+    torch.int32 C (m x n). Returns C. Raises IgemmError on a bad status.
+    workspace: None / "torch" (torch's allocator), "library" (the library's
+    pool) or a uint8 CUDA tensor (256-byte aligned) to use as is."""
+    return _gemm(2, A, B, C, stream, kernel, split, workspace, "gemm_i16")
 
 
-def gemm_i8(A, B, C, stream=None, kernel=-1, split=-1):
+def gemm_i8(A, B, C, stream=None, kernel=-1, split=-1, workspace=None):
     """C += A.B for 2-D torch.int8 CUDA tensors; see gemm_i16."""
-    import torch
-    m, n, k, lda, ldb, ldc = _check_tensors(A, B, C, torch.int8, "gemm_i8")
-    st = igemm_i8_ex(m, n, k, A, lda, B, ldb, C, ldc, stream, kernel, split)
-    if st != IGEMM_OK:
-        raise IgemmError(st, "igemm_i8")
-    return C
+    return _gemm(1, A, B, C, stream, kernel, split, workspace, "gemm_i8")

@@ -1,0 +1,151 @@
+// The C entry points: validation, planning, workspace and dispatch to the
+// fused tiled kernels or to the pack-then-multiply path.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <mutex>
+
+#include "igemm.h"
+#include "igemm_internal.h"
+
+namespace igemm {
+namespace {
+
+constexpr int kMaxDevices = 64;
+
+int num_cu_of_current_device() {
+    static int cached[kMaxDevices] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 256;
+    if (dev >= 0 && dev < kMaxDevices && cached[dev] > 0) return cached[dev];
+    int cu = 0;
+    if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cu <= 0)
+        cu = 256;
+    if (dev >= 0 && dev < kMaxDevices) cached[dev] = cu;
+    return cu;
+}
+
+// One stream-ordered memory pool per device for the packed path's workspace.
+// Its release threshold is unlimited, so after the first call of a given
+// size the allocations are served from memory the pool already holds.
+std::mutex g_pool_mu;
+hipMemPool_t g_pools[kMaxDevices] = {};
+
+int pool_of_current_device(hipMemPool_t *out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return IGEMM_EHIP;
+    std::lock_guard<std::mutex> lock(g_pool_mu);
+    if (g_pools[dev] == nullptr) {
+        hipMemPoolProps props = {};
+        props.allocType = hipMemAllocationTypePinned;
+        props.handleTypes = hipMemHandleTypeNone;
+        props.location.type = hipMemLocationTypeDevice;
+        props.location.id = dev;
+        hipMemPool_t pool = nullptr;
+        if (hipMemPoolCreate(&pool, &props) != hipSuccess) return IGEMM_EHIP;
+        uint64_t threshold = UINT64_MAX;
+        if (hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &threshold) !=
+            hipSuccess) {
+            (void)hipMemPoolDestroy(pool);
+            return IGEMM_EHIP;
+        }
+        g_pools[dev] = pool;
+    }
+    *out = g_pools[dev];
+    return IGEMM_OK;
+}
+
+bool stream_is_capturing(hipStream_t s) {
+    hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &st) != hipSuccess) return false;
+    return st != hipStreamCaptureStatusNone;
+}
+
+int run(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, const void *B,
+        int64_t ldb, int32_t *C, int64_t ldc, void *stream, int kernel, int split,
+        void *workspace, int64_t workspace_bytes) {
+    int st = validate(es, m, n, k, A, lda, B, ldb, C, ldc);
+    if (st != IGEMM_OK) return st;
+    if (m == 0 || n == 0 || k == 0) return IGEMM_OK;
+    if (kernel < -1 || kernel >= K_COUNT || split < -1 || split == 0) return IGEMM_EINVAL;
+    if (kernel >= 0 && kKernels[kernel].es != es) return IGEMM_EINVAL;
+    if (workspace != nullptr && ((uintptr_t)workspace % 256 != 0 || workspace_bytes < 0))
+        return IGEMM_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    // Without a caller workspace the pool is the only source, and it is not
+    // used while the stream is being captured.
+    const bool pool_ok = workspace != nullptr || !stream_is_capturing(s);
+    if (kernel >= 0 && kKernels[kernel].packed && !pool_ok) return IGEMM_EINVAL;
+    igemm_plan p;
+    st = make_plan(es, m, n, k, A, lda, B, ldb, ldc, num_cu_of_current_device(), kernel, split,
+                   pool_ok, &p);
+    if (st != IGEMM_OK) return st;
+    if (!p.packed) return launch_tiled(es, p, m, n, k, A, lda, B, ldb, C, ldc, stream);
+    if (workspace != nullptr) {
+        if (workspace_bytes < p.workspace_bytes) return IGEMM_ENOMEM;
+        return launch_packed(es, p, m, n, k, A, lda, B, ldb, C, ldc, workspace, stream);
+    }
+    hipMemPool_t pool = nullptr;
+    st = pool_of_current_device(&pool);
+    if (st != IGEMM_OK) return st;
+    void *ws = nullptr;
+    if (hipMallocFromPoolAsync(&ws, (size_t)p.workspace_bytes, pool, s) != hipSuccess ||
+        ws == nullptr) {
+        (void)hipGetLastError();
+        return IGEMM_ENOMEM;
+    }
+    st = launch_packed(es, p, m, n, k, A, lda, B, ldb, C, ldc, ws, stream);
+    if (hipFreeAsync(ws, s) != hipSuccess && st == IGEMM_OK) st = IGEMM_EHIP;
+    return st;
+}
+
+}  // namespace
+}  // namespace igemm
+
+extern "C" {
+
+int igemm_i16(int64_t m, int64_t n, int64_t k, const int16_t *A, int64_t lda,
+              const int16_t *B, int64_t ldb, int32_t *C, int64_t ldc, void *stream) {
+    return igemm::run(2, m, n, k, A, lda, B, ldb, C, ldc, stream, -1, -1, nullptr, 0);
+}
+
+int igemm_i8(int64_t m, int64_t n, int64_t k, const int8_t *A, int64_t lda, const int8_t *B,
+             int64_t ldb, int32_t *C, int64_t ldc, void *stream) {
+    return igemm::run(1, m, n, k, A, lda, B, ldb, C, ldc, stream, -1, -1, nullptr, 0);
+}
+
+int igemm_i16_ex(int64_t m, int64_t n, int64_t k, const int16_t *A, int64_t lda,
+                 const int16_t *B, int64_t ldb, int32_t *C, int64_t ldc, void *stream,
+                 int kernel, int split) {
+    return igemm::run(2, m, n, k, A, lda, B, ldb, C, ldc, stream, kernel, split, nullptr, 0);
+}
+
+int igemm_i8_ex(int64_t m, int64_t n, int64_t k, const int8_t *A, int64_t lda,
+                const int8_t *B, int64_t ldb, int32_t *C, int64_t ldc, void *stream,
+                int kernel, int split) {
+    return igemm::run(1, m, n, k, A, lda, B, ldb, C, ldc, stream, kernel, split, nullptr, 0);
+}
+
+int igemm_i16_ws(int64_t m, int64_t n, int64_t k, const int16_t *A, int64_t lda,
+                 const int16_t *B, int64_t ldb, int32_t *C, int64_t ldc, void *stream,
+                 int kernel, int split, void *workspace, int64_t workspace_bytes) {
+    return igemm::run(2, m, n, k, A, lda, B, ldb, C, ldc, stream, kernel, split, workspace,
+                      workspace_bytes);
+}
+
+int igemm_i8_ws(int64_t m, int64_t n, int64_t k, const int8_t *A, int64_t lda,
+                const int8_t *B, int64_t ldb, int32_t *C, int64_t ldc, void *stream,
+                int kernel, int split, void *workspace, int64_t workspace_bytes) {
+    return igemm::run(1, m, n, k, A, lda, B, ldb, C, ldc, stream, kernel, split, workspace,
+                      workspace_bytes);
+}
+
+int igemm_trim_workspace(void) {
+    hipMemPool_t pool = nullptr;
+    int st = igemm::pool_of_current_device(&pool);
+    if (st != IGEMM_OK) return st;
+    return hipMemPoolTrimTo(pool, 0) == hipSuccess ? IGEMM_OK : IGEMM_EHIP;
+}
+
+}  // extern "C"

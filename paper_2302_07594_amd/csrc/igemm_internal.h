@@ -7,13 +7,15 @@
 
 namespace igemm {
 
-// One tiled kernel family: operand size, workgroup tile of C and the tile of
-// C each of the four waves owns.
+// One kernel family: operand size, workgroup tile of C and the tile of C
+// each of the four waves owns. Packed kernels multiply operands that a pack
+// step has first rearranged into a workspace.
 struct KernelDesc {
     const char *name;
     int es;      // operand bytes: 2 = int16 (two int8 limb planes), 1 = int8
     int bm, bn;  // workgroup tile of C
     int wm, wn;  // wave tile of C
+    bool packed;
 };
 
 enum KernelId {
@@ -25,6 +27,8 @@ enum KernelId {
     K_I16_64x64,
     K_I16_32x128,
     K_I16_16x128,
+    K_I8_PACKED_256x256,
+    K_I16_PACKED_128x128,
     K_COUNT
 };
 
@@ -37,11 +41,39 @@ constexpr int64_t kMaxKChunk = 32768;
 
 extern const KernelDesc kKernels[K_COUNT];
 
+// Workspace of the packed path (byte offsets from a 256-byte aligned base).
+// Planes are k-contiguous int8 rows of k_pad bytes, zero beyond k:
+//   A: es planes of m_pad rows (int16: high limb, then offset low limb),
+//      absent for int8 A that is already aligned and tile-shaped;
+//   B: es planes of n_pad rows (the columns of B);
+//   corr_a: m_pad row corrections, corr_b: b_slices x n_pad partial column
+//   corrections (int16 only).
+struct PackedLayout {
+    int64_t m_pad, n_pad, k_pad;
+    int64_t kspan;     // k rows per pack_b workgroup
+    int b_slices;      // k slices of pack_b
+    bool pack_a;
+    int64_t off_a, off_b, off_corr_a, off_corr_b, bytes;
+};
+
 // Validation and planning; pure host code, no HIP calls.
 int validate(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
              const void *B, int64_t ldb, const void *C, int64_t ldc);
+// allow_packed = false restricts automatic choice to the fused kernels (used
+// when no workspace can be obtained, e.g. under stream capture).
 int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
-              const void *B, int64_t ldb, int num_cu, int kernel, int split,
-              igemm_plan *out);
+              const void *B, int64_t ldb, int64_t ldc, int num_cu, int kernel, int split,
+              bool allow_packed, igemm_plan *out);
+void packed_layout(int es, int64_t m, int64_t n, int64_t k, int kernel, const void *A,
+                   int64_t lda, PackedLayout *L);
+
+// Kernel launches for a validated plan (stream is a hipStream_t). The packed
+// launch needs a workspace of at least plan.workspace_bytes, 256-byte aligned.
+int launch_tiled(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                 int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
+                 void *stream);
+int launch_packed(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                  int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
+                  void *workspace, void *stream);
 
 }  // namespace igemm

@@ -36,126 +36,13 @@
 #include <type_traits>
 
 #include "igemm.h"
+#include "igemm_device.h"
 #include "igemm_internal.h"
 
 namespace igemm {
 namespace {
 
-typedef int v4i __attribute__((ext_vector_type(4)));
-typedef int v16i __attribute__((ext_vector_type(16)));
-typedef unsigned int u32;
-
-// The two gfx950 int8 matrix-core instructions, described by their tile
-// shape. Both take 16 bytes of A and 16 bytes of B per lane (one row of A /
-// one column of B, k-contiguous); the k range a lane holds is chunk
-// `2*ks + lane/32` (32x32x32) or `lane/16` (16x16x64) of the 64-byte k-tile.
-// 32x32x32 is the default: the compiler accumulates it in place, whereas it
-// rotates the 16x16x64 accumulators through copies, so 16x16x64 is kept for
-// 16-row tiles only.
-template <int MF>
-struct Mfma;
-template <>
-struct Mfma<16> {
-    typedef v4i acc_t;
-    static constexpr int REGS = 4, KSTEPS = 1;
-    static __device__ __forceinline__ acc_t mma(v4i a, v4i b, acc_t c) {
-        return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
-    }
-    static __device__ __forceinline__ int frag_row(int lane) { return lane & 15; }
-    static __device__ __forceinline__ int frag_chunk(int lane, int ks) { return lane >> 4; }
-    // output register r of `lane` holds C[row][col] of the 16x16 tile
-    static __device__ __forceinline__ int out_row(int lane, int r) { return 4 * (lane >> 4) + r; }
-    static __device__ __forceinline__ int out_col(int lane) { return lane & 15; }
-};
-template <>
-struct Mfma<32> {
-    typedef v16i acc_t;
-    static constexpr int REGS = 16, KSTEPS = 2;
-    static __device__ __forceinline__ acc_t mma(v4i a, v4i b, acc_t c) {
-        return __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0);
-    }
-    static __device__ __forceinline__ int frag_row(int lane) { return lane & 31; }
-    static __device__ __forceinline__ int frag_chunk(int lane, int ks) { return 2 * ks + (lane >> 5); }
-    static __device__ __forceinline__ int out_row(int lane, int r) {
-        return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-    }
-    static __device__ __forceinline__ int out_col(int lane) { return lane & 31; }
-};
-
 // ---------------------------------------------------------------------------
-// LDS layout. Every operand plane is stored as rows of 64 bytes (the 64
-// k-elements of one row of A or one column of B), split into four 16-byte
-// chunks; chunk q of row r sits at position q ^ swz(r). With
-// swz(r) = ((r >> 1) ^ (r >> 2)) & 3 the fragment reads of both MFMA shapes
-// (16 or 32 consecutive rows at one chunk) are free of bank conflicts on
-// gfx950's 64-bank LDS (measured: ~200 B/clk/CU, against ~110 for the
-// 2-way-conflicted (r >> 1) & 3).
-__device__ __forceinline__ int swz(int row) { return ((row >> 1) ^ (row >> 2)) & 3; }
-__device__ __forceinline__ int lds_off(int row, int q) { return row * 64 + ((q ^ swz(row)) << 4); }
-
-__device__ __forceinline__ u32 perm(u32 hi, u32 lo, u32 sel) {
-    return __builtin_amdgcn_perm(hi, lo, sel);
-}
-
-// 4x4 byte transpose: x_r holds bytes (r, c = 0..3); y_c receives bytes
-// (r = 0..3, c).
-__device__ __forceinline__ void transpose4x4(u32 x0, u32 x1, u32 x2, u32 x3, u32 &y0,
-                                             u32 &y1, u32 &y2, u32 &y3) {
-    const u32 t0 = perm(x1, x0, 0x05010400u);
-    const u32 t1 = perm(x1, x0, 0x07030602u);
-    const u32 t2 = perm(x3, x2, 0x05010400u);
-    const u32 t3 = perm(x3, x2, 0x07030602u);
-    y0 = perm(t2, t0, 0x05040100u);
-    y1 = perm(t2, t0, 0x07060302u);
-    y2 = perm(t3, t1, 0x05040100u);
-    y3 = perm(t3, t1, 0x07060302u);
-}
-
-__device__ __forceinline__ int sum4(u32 x, int acc) {
-    return __builtin_amdgcn_sdot4((int)x, 0x01010101, acc, false);
-}
-
-// Byte mask keeping the first `v` bytes of a dword (v clamped to 0..4).
-__device__ __forceinline__ u32 byte_mask(int v) {
-    return v >= 4 ? 0xffffffffu : (v <= 0 ? 0u : ((1u << (8 * v)) - 1u));
-}
-
-// Element-wise load of 16 bytes (16 int8 or 8 int16 elements) starting at
-// element e0 of a row with `len` valid elements; invalid elements are zero.
-template <int ES>
-__device__ __forceinline__ v4i load_elems(const void *rowp, int e0, int len) {
-    u32 w[4] = {0u, 0u, 0u, 0u};
-    if constexpr (ES == 1) {
-        const uint8_t *p = (const uint8_t *)rowp;
-#pragma unroll
-        for (int i = 0; i < 16; ++i)
-            if (e0 + i < len) w[i >> 2] |= (u32)p[e0 + i] << (8 * (i & 3));
-    } else {
-        const uint16_t *p = (const uint16_t *)rowp;
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-            if (e0 + i < len) w[i >> 1] |= (u32)p[e0 + i] << (16 * (i & 1));
-    }
-    v4i r;
-    r.x = (int)w[0];
-    r.y = (int)w[1];
-    r.z = (int)w[2];
-    r.w = (int)w[3];
-    return r;
-}
-
-template <int ES, bool VEC>
-__device__ __forceinline__ v4i load16(const void *rowp, int e0, int len) {
-    constexpr int E = 16 / ES;
-    if (VEC && e0 + E <= len)
-        return *(const v4i *)((const char *)rowp + (size_t)e0 * ES);
-    return load_elems<ES>(rowp, e0, len);
-}
-
-// ---------------------------------------------------------------------------
-template <int V>
-using ic = std::integral_constant<int, V>;
-
 template <int ES, int BM, int BN, int WM, int WN, int MF, bool VA, bool VB, bool SPLIT>
 __global__ void __launch_bounds__(256, 1)
 igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ Bp,
@@ -458,18 +345,32 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     // with one barrier.
     auto step = [&](auto phase, auto do_load, auto do_store, auto do_pref, int kt) {
         constexpr int S = decltype(phase)::value;
-        if (decltype(do_load)::value) load_fast(ic<(S + 1) & 1>{}, kbeg + (kt + 3) * 64);
         if constexpr (M::KSTEPS == 2) {
-            // sub-step 0 on slot 0 while sub-step 1 loads into slot 1
+            constexpr int NM = TM * TN * (ES == 2 ? 4 : 1);  // MFMAs per sub-step
+            constexpr int NR = P * (TM + TN);                // fragment reads
+            constexpr int NV = ACT + 4 * BUT;                 // global loads
+            // staging work of one tile: perms, xors, limb sums, LDS writes
+            constexpr int VALU = ES == 2 ? (10 * ACT + 56 * BUT) : (36 * BUT);
+            constexpr int DSW = ES == 2 ? (2 * ACT + 16 * BUT) : (ACT + 16 * BUT);
+            // sub-step 0 on slot 0 while sub-step 1 loads into slot 1 and the
+            // global loads of tile kt+3 go out
+            if (decltype(do_load)::value) load_fast(ic<(S + 1) & 1>{}, kbeg + (kt + 3) * 64);
             read_frags(ic<1>{}, ic<S>{}, ic<1>{});
             mfmas(ic<0>{});
-            // sub-step 1 on slot 1 while tile kt+2 is staged and the next
-            // tile's sub-step 0 loads into slot 0
+            interleave<NM, NR, decltype(do_load)::value ? NV : 0, 0, 0>();
+            __builtin_amdgcn_sched_barrier(0);
+            // sub-step 1 on slot 1 while the next tile's sub-step 0 loads into
+            // slot 0 and tile kt+2 is staged into LDS
+            if (decltype(do_pref)::value) read_frags(ic<0>{}, ic<(S + 1) & 3>{}, ic<0>{});
             if (decltype(do_store)::value)
                 store_tile(ic<S & 1>{}, ic<(S + 2) & 3>{}, ic<0>{}, kbeg + (kt + 2) * 64);
-            if (decltype(do_pref)::value) read_frags(ic<0>{}, ic<(S + 1) & 3>{}, ic<0>{});
             mfmas(ic<1>{});
+            interleave<NM, decltype(do_pref)::value ? NR : 0, 0,
+                       decltype(do_store)::value ? (VALU + NM - 1) / NM : 0,
+                       decltype(do_store)::value ? (DSW + NM - 1) / NM : 0>();
+            __builtin_amdgcn_sched_barrier(0);
         } else {
+            if (decltype(do_load)::value) load_fast(ic<(S + 1) & 1>{}, kbeg + (kt + 3) * 64);
             // one sub-step per tile; tiles alternate between the slots
             constexpr int SL = S & 1;
             if (decltype(do_store)::value)
@@ -626,29 +527,12 @@ const void *kernel_fn(int id, bool va, bool vb, bool split) {
     }
 }
 
-int num_cu_of_current_device() {
-    static int cached[64] = {0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return 256;
-    if (dev >= 0 && dev < 64 && cached[dev] > 0) return cached[dev];
-    int cu = 0;
-    if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        cu <= 0)
-        cu = 256;
-    if (dev >= 0 && dev < 64) cached[dev] = cu;
-    return cu;
-}
+}  // namespace
 
-int run(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, const void *B,
-        int64_t ldb, int32_t *C, int64_t ldc, void *stream, int kernel, int split) {
-    int st = validate(es, m, n, k, A, lda, B, ldb, C, ldc);
-    if (st != IGEMM_OK) return st;
-    if (m == 0 || n == 0 || k == 0) return IGEMM_OK;
-    if (kernel < -1 || kernel >= K_COUNT || split < -1 || split == 0) return IGEMM_EINVAL;
-    if (kernel >= 0 && kKernels[kernel].es != es) return IGEMM_EINVAL;
-    igemm_plan p;
-    st = make_plan(es, m, n, k, A, lda, B, ldb, num_cu_of_current_device(), kernel, split, &p);
-    if (st != IGEMM_OK) return st;
+int launch_tiled(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                 int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
+                 void *stream) {
+    (void)es;
     const void *fn = kernel_fn(p.kernel, p.vec_a != 0, p.vec_b != 0, p.split > 1);
     if (fn == nullptr) return IGEMM_EINVAL;
     int mi = (int)m, ni = (int)n, ki = (int)k, kc = (int)p.k_chunk;
@@ -661,31 +545,4 @@ int run(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, con
     return e == hipSuccess ? IGEMM_OK : IGEMM_EHIP;
 }
 
-}  // namespace
 }  // namespace igemm
-
-extern "C" {
-
-int igemm_i16(int64_t m, int64_t n, int64_t k, const int16_t *A, int64_t lda,
-              const int16_t *B, int64_t ldb, int32_t *C, int64_t ldc, void *stream) {
-    return igemm::run(2, m, n, k, A, lda, B, ldb, C, ldc, stream, -1, -1);
-}
-
-int igemm_i8(int64_t m, int64_t n, int64_t k, const int8_t *A, int64_t lda, const int8_t *B,
-             int64_t ldb, int32_t *C, int64_t ldc, void *stream) {
-    return igemm::run(1, m, n, k, A, lda, B, ldb, C, ldc, stream, -1, -1);
-}
-
-int igemm_i16_ex(int64_t m, int64_t n, int64_t k, const int16_t *A, int64_t lda,
-                 const int16_t *B, int64_t ldb, int32_t *C, int64_t ldc, void *stream,
-                 int kernel, int split) {
-    return igemm::run(2, m, n, k, A, lda, B, ldb, C, ldc, stream, kernel, split);
-}
-
-int igemm_i8_ex(int64_t m, int64_t n, int64_t k, const int8_t *A, int64_t lda,
-                const int8_t *B, int64_t ldb, int32_t *C, int64_t ldc, void *stream,
-                int kernel, int split) {
-    return igemm::run(1, m, n, k, A, lda, B, ldb, C, ldc, stream, kernel, split);
-}
-
-}  // extern "C"

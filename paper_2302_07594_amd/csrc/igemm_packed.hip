@@ -1,0 +1,533 @@
+// Pack-then-multiply path for large GEMMs.
+//
+// The paper's GEMM packs panels of A and B into buffers whose layout lets the
+// micro-kernel stream them with unit stride (Sec. 4.1, the packing routines
+// around the micro-kernel; Sec. 5.1 pre-packs A_c once for DL inference). On
+// the GPU this is done for the whole operands, once per call, by two small
+// memory-bound kernels:
+//   * pack A: int16 rows are split into a high and an offset-low int8 limb
+//     plane (k-contiguous, zero-padded to m_pad x k_pad) and the row limb sums
+//     are reduced into one 32-bit correction per row; int8 A is only copied
+//     when its rows are not 16-byte aligned or not tile multiples;
+//   * pack B: B is transposed to k-contiguous columns (and split into limb
+//     planes for int16), zero-padded to n_pad x k_pad, with per-column limb
+//     sums reduced per k slice.
+// The main kernel then reads both operands with global-to-LDS DMA loads
+// (global_load_lds_dwordx4: no VGPRs, no staging instructions) into a
+// four-stage LDS ring, three k-tiles ahead of the matrix cores, and runs the
+// same MFMA micro-tiles as the fused kernels. All padding is zero, so the
+// main loop has no bounds checks and every partial limb product of padding is
+// zero; only the C update is bounded.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "igemm.h"
+#include "igemm_device.h"
+#include "igemm_internal.h"
+
+namespace igemm {
+namespace packed {
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// 16 bytes per lane from global memory straight into LDS: lane i writes
+// [lds + 16 i, lds + 16 i + 16) (global_load_lds_dwordx4; lds must be wave
+// uniform). Kept out of the kernel templates: the builtin exists only for
+// the device, and inside a template it would suppress the host launch stub.
+__device__ __forceinline__ void dma16(const void *g, lds_void *lds) {
+    __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
+}
+
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+// ---- pack A, int16: one workgroup per padded row ---------------------------
+// Writes Ah/Al[i][0, k_pad) and corrA[i] = 32768*sum(h) + 128*sum(l) mod 2^32.
+template <bool VEC>
+__global__ void __launch_bounds__(256)
+pack_a_i16(const int16_t *__restrict__ A, int64_t lda, int m, int k, int k_pad,
+           int8_t *__restrict__ Ah, int8_t *__restrict__ Al, uint32_t *__restrict__ corrA) {
+    const int i = blockIdx.x, tid = threadIdx.x;
+    const int len = i < m ? k : 0;
+    const int16_t *arow = A + (int64_t)(i < m ? i : 0) * lda;
+    int8_t *hrow = Ah + (int64_t)i * k_pad;
+    int8_t *lrow = Al + (int64_t)i * k_pad;
+    int sh = 0, sl = 0;
+    for (int e0 = tid * 8; e0 < k_pad; e0 += 256 * 8) {
+        const v4i raw = load16<2, VEC>(arow, e0, len);
+        const u32 y0 = raw.x, y1 = raw.y, y2 = raw.z, y3 = raw.w;
+        const int v = len - e0;
+        const u32 m0 = byte_mask(v), m1 = byte_mask(v - 4);
+        const u32 h0 = perm(y1, y0, 0x07050301u) & m0, h1 = perm(y3, y2, 0x07050301u) & m1;
+        const u32 l0 = (perm(y1, y0, 0x06040200u) ^ 0x80808080u) & m0;
+        const u32 l1 = (perm(y3, y2, 0x06040200u) ^ 0x80808080u) & m1;
+        sh = sum4(h1, sum4(h0, sh));
+        sl = sum4(l1, sum4(l0, sl));
+        *(uint2 *)(hrow + e0) = make_uint2(h0, h1);
+        *(uint2 *)(lrow + e0) = make_uint2(l0, l1);
+    }
+    __shared__ int red[2][4];
+    sh = wave_sum(sh);
+    sl = wave_sum(sl);
+    if ((tid & 63) == 0) {
+        red[0][tid >> 6] = sh;
+        red[1][tid >> 6] = sl;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        const u32 h = (u32)red[0][0] + (u32)red[0][1] + (u32)red[0][2] + (u32)red[0][3];
+        const u32 l = (u32)red[1][0] + (u32)red[1][1] + (u32)red[1][2] + (u32)red[1][3];
+        corrA[i] = 32768u * h + 128u * l;
+    }
+}
+
+// ---- pack A, int8: copy into a zero-padded m_pad x k_pad buffer ------------
+template <bool VEC>
+__global__ void __launch_bounds__(256)
+pack_a_i8(const int8_t *__restrict__ A, int64_t lda, int m, int k, int k_pad,
+          int8_t *__restrict__ Ap) {
+    const int i = blockIdx.x, tid = threadIdx.x;
+    const int len = i < m ? k : 0;
+    const int8_t *arow = A + (int64_t)(i < m ? i : 0) * lda;
+    int8_t *prow = Ap + (int64_t)i * k_pad;
+    for (int e0 = tid * 16; e0 < k_pad; e0 += 256 * 16)
+        *(v4i *)(prow + e0) = load16<1, VEC>(arow, e0, len);
+}
+
+// ---- pack B: transpose to k-contiguous columns ----------------------------
+// Workgroup (blockIdx.x, blockIdx.y) covers columns [64x, 64x + 64) and the
+// k slice [kspan*y, kspan*(y+1)). Per pass, thread (rg, cc) loads 4 rows x 16
+// bytes, transposes 4x4 byte blocks in registers (and for int16 separates the
+// limb planes), parks the per-column dwords in LDS, and the workgroup writes
+// each column's k run out contiguously. For int16 the per-column limb sums of
+// the slice go to corr_part[y][col].
+template <int ES, bool VEC>
+__global__ void __launch_bounds__(256)
+pack_b(const void *__restrict__ Bv, int64_t ldb, int k, int n, int k_pad, int kspan, int n_pad,
+       int8_t *__restrict__ Bp0, int8_t *__restrict__ Bp1, uint32_t *__restrict__ corr_part) {
+    constexpr int P = ES;                 // output planes
+    constexpr int CC = ES == 2 ? 8 : 4;   // 16-byte column chunks per workgroup (64 columns)
+    constexpr int RG = 256 / CC;          // row groups of 4 rows
+    constexpr int ROWS = 4 * RG;          // k rows per pass
+    constexpr int DW = ROWS / 4;          // dwords per column per pass
+    constexpr int CPU = 16 / ES;          // columns per chunk
+    __shared__ u32 T[P][64][DW + 1];
+    __shared__ int cs[64];
+    const int8_t *B8 = (const int8_t *)Bv;
+    const int tid = threadIdx.x, cc = tid % CC, rg = tid / CC;
+    const int j0 = blockIdx.x * 64;
+    const int kb = blockIdx.y * kspan, ke = min(k_pad, kb + kspan);
+    const int nlen = n - j0;
+    int shh[8] = {0, 0, 0, 0, 0, 0, 0, 0}, sll[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (tid < 64) cs[tid] = 0;
+    for (int p0 = kb; p0 < ke; p0 += ROWS) {
+        v4i x[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int p = p0 + 4 * rg + r;
+            const int len = p < k ? nlen : 0;
+            const void *rowp = B8 + ((int64_t)(p < k ? p : 0) * ldb + j0) * ES;
+            x[r] = load16<ES, VEC>(rowp, cc * CPU, len);
+        }
+        const u32 rmask = ES == 2 ? byte_mask(k - (p0 + 4 * rg)) : 0xffffffffu;
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+            u32 y[4];
+            transpose4x4((u32)x[0][d], (u32)x[1][d], (u32)x[2][d], (u32)x[3][d], y[0], y[1],
+                         y[2], y[3]);
+            if constexpr (ES == 1) {
+#pragma unroll
+                for (int t = 0; t < 4; ++t) T[0][cc * 16 + 4 * d + t][rg] = y[t];
+            } else {
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const u32 lo = (y[2 * h] ^ 0x80808080u) & rmask;
+                    const u32 hi = y[2 * h + 1] & rmask;
+                    const int c = 2 * d + h;
+                    shh[c] = sum4(hi, shh[c]);
+                    sll[c] = sum4(lo, sll[c]);
+                    T[0][cc * 8 + c][rg] = hi;
+                    T[1][cc * 8 + c][rg] = lo;
+                }
+            }
+        }
+        __syncthreads();
+        // P planes x 64 columns x ROWS bytes, in 16-byte chunks.
+        constexpr int CH = ROWS / 16;
+        for (int idx = tid; idx < P * 64 * CH; idx += 256) {
+            const int plane = idx / (64 * CH), rem = idx % (64 * CH);
+            const int col = rem / CH, ch = rem % CH;
+            const u32 *src = &T[plane][col][4 * ch];
+            v4i v;
+            v.x = (int)src[0];
+            v.y = (int)src[1];
+            v.z = (int)src[2];
+            v.w = (int)src[3];
+            int8_t *dst = (plane ? Bp1 : Bp0) + (int64_t)(j0 + col) * k_pad + p0 + ch * 16;
+            *(v4i *)dst = v;
+        }
+        __syncthreads();
+    }
+    if constexpr (ES == 2) {
+#pragma unroll
+        for (int c = 0; c < 8; ++c) atomicAdd(&cs[cc * 8 + c], (int)(32768u * (u32)shh[c] + 128u * (u32)sll[c]));
+        __syncthreads();
+        if (tid < 64) corr_part[(int64_t)blockIdx.y * n_pad + j0 + tid] = (u32)cs[tid];
+    }
+}
+
+// ---- the packed-operand GEMM ---------------------------------------------
+// A planes: P x m_pad x k_pad (row stride lda_p, plane stride a_plane), B
+// planes: P x n_pad x k_pad. ktiles = k_pad / 64 is a multiple of 4.
+template <int ES, int BM, int BN, int WM, int WN>
+__global__ void __launch_bounds__(256, 1)
+igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
+             const int8_t *__restrict__ Bp, int64_t ldb_p, int64_t b_plane,
+             const uint32_t *__restrict__ corrA, const uint32_t *__restrict__ corr_part,
+             int corr_splits, int n_pad, uint32_t kconst, int32_t *__restrict__ C, int64_t ldc,
+             int m, int n, int ktiles, int tiles_m, int tiles_n) {
+    constexpr int MF = 32;
+    typedef Mfma<MF> M;
+    typedef typename M::acc_t acc_t;
+    constexpr int P = ES;
+    constexpr int NACC = ES == 2 ? 3 : 1;
+    constexpr int TM = WM / MF, TN = WN / MF;
+    constexpr int WGN = BN / WN;
+    static_assert((BM / WM) * WGN == 4, "four waves per workgroup");
+    constexpr int APL = BM * 64, BPL = BN * 64;
+    constexpr int STAGE = P * (APL + BPL);
+    constexpr int NBLK = STAGE / 1024;  // 1 KB DMA blocks per stage
+    static_assert(NBLK % 4 == 0 && NBLK / 4 <= 16, "DMA blocks per wave");
+    constexpr int DPW = NBLK / 4;       // DMA instructions per wave per k-tile
+    constexpr int NBA = P * BM / 16;    // blocks holding A planes
+
+    // Four LDS stages as separate objects, so that the compiler can tell the
+    // DMA writes of one stage from the fragment reads of another.
+    __shared__ __attribute__((aligned(16))) char st0[STAGE];
+    __shared__ __attribute__((aligned(16))) char st1[STAGE];
+    __shared__ __attribute__((aligned(16))) char st2[STAGE];
+    __shared__ __attribute__((aligned(16))) char st3[STAGE];
+    auto stage = [&](auto s) -> char * {
+        constexpr int S = decltype(s)::value;
+        if constexpr (S == 0) return st0;
+        else if constexpr (S == 1) return st1;
+        else if constexpr (S == 2) return st2;
+        else return st3;
+    };
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    // wave-uniform, so that DMA destinations (m0) are scalar arithmetic
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm0 = (wave / WGN) * WM, wn0 = (wave % WGN) * WN;
+
+    int bid = blockIdx.x;
+    const int G = gridDim.x;
+    if ((G & 7) == 0) bid = (bid & 7) * (G >> 3) + (bid >> 3);
+    constexpr int GROUP = 8;
+    const int span = GROUP * tiles_n;
+    const int first_m = (bid / span) * GROUP;
+    const int gsize = min(tiles_m - first_m, GROUP);
+    const int tm = first_m + (bid % span) % gsize;
+    const int tn = (bid % span) / gsize;
+    const int m0 = tm * BM, n0 = tn * BN;
+
+    // DMA sources: wave w moves blocks w*DPW .. w*DPW+DPW-1 of every stage.
+    // Lane i of a block writes LDS bytes [16i, 16i+16) of that block, i.e. row
+    // r0 + i/4, physical chunk i%4, which holds logical chunk (i%4) ^ swz(row).
+    const int8_t *src[DPW];
+#pragma unroll
+    for (int d = 0; d < DPW; ++d) {
+        const int b = wave * DPW + d;
+        const int row_in_blocks = (b < NBA ? b % (BM / 16) : (b - NBA) % (BN / 16)) * 16 + (lane >> 2);
+        const int plane = b < NBA ? b / (BM / 16) : (b - NBA) / (BN / 16);
+        const int q = (lane & 3) ^ swz(row_in_blocks);
+        if (b < NBA)
+            src[d] = Ap + plane * a_plane + (int64_t)(m0 + row_in_blocks) * lda_p + 16 * q;
+        else
+            src[d] = Bp + plane * b_plane + (int64_t)(n0 + row_in_blocks) * ldb_p + 16 * q;
+    }
+    auto dma = [&](auto s, int kt) {
+        char *dst = stage(s) + wave * DPW * 1024;
+        const int64_t koff = (int64_t)kt * 64;
+#pragma unroll
+        for (int d = 0; d < DPW; ++d)
+            dma16(src[d] + koff, (lds_void *)(dst + d * 1024));
+    };
+
+    // Fragment reads (same LDS layout as the fused kernels).
+    const int fr = M::frag_row(lane);
+    int a_rbase[2], b_rbase[2];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+        const int cq = (M::frag_chunk(lane, ks) ^ swz(fr)) << 4;
+        a_rbase[ks] = (wm0 + fr) * 64 + cq;
+        b_rbase[ks] = (wn0 + fr) * 64 + cq;
+    }
+    v4i fa[2][P][TM], fb[2][P][TN];
+    auto read_frags = [&](auto slot, auto s, auto ks) {
+        constexpr int SL = decltype(slot)::value;
+        constexpr int KS = decltype(ks)::value;
+        const char *As = stage(s);
+        const char *Bs = As + P * APL;
+#pragma unroll
+        for (int p = 0; p < P; ++p) {
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                fb[SL][p][j] = *(const v4i *)(Bs + p * BPL + b_rbase[KS] + j * MF * 64);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                fa[SL][p][i] = *(const v4i *)(As + p * APL + a_rbase[KS] + i * MF * 64);
+        }
+    };
+
+    acc_t acc[NACC][TM][TN];
+#pragma unroll
+    for (int a = 0; a < NACC; ++a)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int r = 0; r < M::REGS; ++r) acc[a][i][j][r] = 0;
+    auto mfmas = [&](auto slot) {
+        constexpr int SL = decltype(slot)::value;
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            if constexpr (ES == 1) {
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[0][i][j] = M::mma(fa[SL][0][i], fb[SL][0][j], acc[0][i][j]);
+            } else {
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[0][i][j] = M::mma(fa[SL][0][i], fb[SL][0][j], acc[0][i][j]);
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[1][i][j] = M::mma(fa[SL][0][i], fb[SL][1][j], acc[1][i][j]);
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[2][i][j] = M::mma(fa[SL][1][i], fb[SL][1][j], acc[2][i][j]);
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[1][i][j] = M::mma(fa[SL][1][i], fb[SL][0][j], acc[1][i][j]);
+            }
+        }
+    };
+
+    // Wait until at most DPW DMA instructions of this wave are outstanding
+    // (the newest k-tile), then synchronise the workgroup. Encoding of
+    // s_waitcnt: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] << 14.
+    constexpr int WAIT_NEWEST =
+        (DPW & 0xf) | (0x7 << 4) | (0xf << 8) | (((DPW >> 4) & 3) << 14);
+    auto sync_stage = [&]() {
+        __builtin_amdgcn_s_waitcnt(WAIT_NEWEST);
+        __builtin_amdgcn_s_barrier();
+    };
+
+    constexpr int NM = TM * TN * (ES == 2 ? 4 : 1);
+    constexpr int NR = P * (TM + TN);
+    // Step kt (S = kt mod 4): stages S and S+1 hold tiles kt and kt+1, stage
+    // S+2 is receiving tile kt+2, slot 0 holds sub-step 0 of tile kt. Start the
+    // DMA of tile kt+3 (clamped to the last tile; a clamped copy is never
+    // read), run both sub-steps while reading the next fragments, then wait for
+    // tile kt+2 and synchronise.
+    // Each sub-step opens with an MFMA, and its fragment reads follow MFMAs:
+    // the compiler cannot tell the DMA loads' LDS writes apart from other LDS
+    // traffic, so any wait for a fragment is a full lgkmcnt(0), and this
+    // order makes that wait cover only reads issued a sub-step earlier.
+    auto step = [&](auto s, int kt) {
+        constexpr int S = decltype(s)::value;
+        dma(ic<(S + 3) & 3>{}, min(kt + 3, ktiles - 1));
+        read_frags(ic<1>{}, ic<S>{}, ic<1>{});
+        mfmas(ic<0>{});
+#pragma unroll
+        for (int i = 0; i < NM; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            if (i < NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            if (i < DPW) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        read_frags(ic<0>{}, ic<(S + 1) & 3>{}, ic<0>{});
+        mfmas(ic<1>{});
+#pragma unroll
+        for (int i = 0; i < NM; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            if (i < NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        sync_stage();
+    };
+
+    dma(ic<0>{}, 0);
+    dma(ic<1>{}, min(1, ktiles - 1));
+    dma(ic<2>{}, min(2, ktiles - 1));
+    // tiles 0 and 1 complete (tile 2 may be outstanding)
+    sync_stage();
+    read_frags(ic<0>{}, ic<0>{}, ic<0>{});
+    for (int kt = 0; kt < ktiles; kt += 4) {
+        step(ic<0>{}, kt);
+        step(ic<1>{}, kt + 1);
+        step(ic<2>{}, kt + 2);
+        step(ic<3>{}, kt + 3);
+    }
+    // Drain the clamped copies before the workgroup's LDS is released.
+    __builtin_amdgcn_s_waitcnt(0);
+
+    // ---- epilogue -----------------------------------------------------------
+    // int16 corrections first (small, cache-resident): the column term per
+    // output column and the row term per output row of this lane.
+    u32 colt[TN], rowt[TM][M::REGS];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) colt[j] = 0;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int r = 0; r < M::REGS; ++r) rowt[i][r] = 0;
+    if constexpr (ES == 2) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int gc = n0 + wn0 + MF * j + M::out_col(lane);
+            u32 t = kconst;
+            for (int z = 0; z < corr_splits; ++z) t += corr_part[(int64_t)z * n_pad + gc];
+            colt[j] = t;
+        }
+        if (corrA != nullptr) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int r = 0; r < M::REGS; ++r)
+                    rowt[i][r] = corrA[m0 + wm0 + MF * i + M::out_row(lane, r)];
+        }
+    }
+    // C addresses: a wave-uniform tile base plus 32-bit lane offsets (the
+    // planner keeps bm * ldc * 4 below 2^31).
+    char *Ctile = (char *)(C + (int64_t)m0 * ldc + n0);
+    const int ldc32 = (int)ldc;
+    // C is read, added to and written back in batches of NB output blocks:
+    // every load of a batch is issued before the first add, so a wave keeps
+    // NB * REGS loads in flight instead of waiting out one round trip per
+    // block (all workgroups of a round reach this point together).
+    constexpr int NOUT = TM * TN;
+    constexpr int NB = NOUT < 4 ? NOUT : 4;
+#pragma unroll
+    for (int b0 = 0; b0 < NOUT; b0 += NB) {
+        int32_t cv[NB][M::REGS];
+#pragma unroll
+        for (int bb = 0; bb < NB; ++bb) {
+            const int i = (b0 + bb) / TN, j = (b0 + bb) % TN;
+            const int lc = wn0 + MF * j + M::out_col(lane);
+#pragma unroll
+            for (int r = 0; r < M::REGS; ++r) {
+                const int lr = wm0 + MF * i + M::out_row(lane, r);
+                cv[bb][r] = (m0 + lr < m && n0 + lc < n)
+                                ? *(const int32_t *)(Ctile + (u32)(lr * ldc32 + lc) * 4u)
+                                : 0;
+            }
+        }
+#pragma unroll
+        for (int bb = 0; bb < NB; ++bb) {
+            const int i = (b0 + bb) / TN, j = (b0 + bb) % TN;
+            const int lc = wn0 + MF * j + M::out_col(lane);
+#pragma unroll
+            for (int r = 0; r < M::REGS; ++r) {
+                const int lr = wm0 + MF * i + M::out_row(lane, r);
+                u32 v;
+                if constexpr (ES == 1) {
+                    v = (u32)acc[0][i][j][r];
+                } else {
+                    v = 65536u * (u32)acc[0][i][j][r] + 256u * (u32)acc[1][i][j][r] +
+                        (u32)acc[2][i][j][r] + colt[j] + rowt[i][r];
+                }
+                if (m0 + lr < m && n0 + lc < n)
+                    *(int32_t *)(Ctile + (u32)(lr * ldc32 + lc) * 4u) = (int32_t)((u32)cv[bb][r] + v);
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+}  // namespace packed
+
+using namespace packed;
+
+// ---------------------------------------------------------------------------
+// Host side of the packed path.
+
+int launch_packed(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                  int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
+                  void *workspace, void *stream_) {
+    hipStream_t stream = (hipStream_t)stream_;
+    PackedLayout L;
+    packed_layout(es, m, n, k, p.kernel, A, lda, &L);
+    int8_t *ws = (int8_t *)workspace;
+    const bool va = p.vec_a != 0, vb = p.vec_b != 0;
+    const int mi = (int)m, ni = (int)n, ki = (int)k, kp = (int)L.k_pad, np = (int)L.n_pad;
+    int8_t *Apk = ws + L.off_a, *Bpk = ws + L.off_b;
+    uint32_t *corrA = (uint32_t *)(ws + L.off_corr_a);
+    uint32_t *corrB = (uint32_t *)(ws + L.off_corr_b);
+    const int64_t a_plane = L.m_pad * L.k_pad, b_plane = L.n_pad * L.k_pad;
+
+    if (L.pack_a) {
+        const dim3 g((unsigned)L.m_pad);
+        if (es == 2) {
+            int8_t *Al = Apk + a_plane;
+            const int16_t *A16 = (const int16_t *)A;
+            if (va)
+                pack_a_i16<true><<<g, 256, 0, stream>>>(A16, lda, mi, ki, kp, Apk, Al, corrA);
+            else
+                pack_a_i16<false><<<g, 256, 0, stream>>>(A16, lda, mi, ki, kp, Apk, Al, corrA);
+        } else {
+            const int8_t *A8 = (const int8_t *)A;
+            if (va)
+                pack_a_i8<true><<<g, 256, 0, stream>>>(A8, lda, mi, ki, kp, Apk);
+            else
+                pack_a_i8<false><<<g, 256, 0, stream>>>(A8, lda, mi, ki, kp, Apk);
+        }
+        if (hipGetLastError() != hipSuccess) return IGEMM_EHIP;
+    }
+    {
+        const dim3 g((unsigned)(L.n_pad / 64), (unsigned)L.b_slices);
+        const int ks = (int)L.kspan;
+        if (es == 2) {
+            int8_t *Bl = Bpk + b_plane;
+            if (vb)
+                pack_b<2, true><<<g, 256, 0, stream>>>(B, ldb, ki, ni, kp, ks, np, Bpk, Bl, corrB);
+            else
+                pack_b<2, false><<<g, 256, 0, stream>>>(B, ldb, ki, ni, kp, ks, np, Bpk, Bl, corrB);
+        } else {
+            if (vb)
+                pack_b<1, true><<<g, 256, 0, stream>>>(B, ldb, ki, ni, kp, ks, np, Bpk, Bpk, corrB);
+            else
+                pack_b<1, false><<<g, 256, 0, stream>>>(B, ldb, ki, ni, kp, ks, np, Bpk, Bpk, corrB);
+        }
+        if (hipGetLastError() != hipSuccess) return IGEMM_EHIP;
+    }
+    const KernelDesc &d = kKernels[p.kernel];
+    const int tm = (int)(L.m_pad / d.bm), tn = (int)(L.n_pad / d.bn);
+    const int8_t *Asrc = L.pack_a ? Apk : (const int8_t *)A;
+    const int64_t lda_p = L.pack_a ? L.k_pad : lda;
+    const dim3 grid((unsigned)p.grid);
+    // One launch per k chunk; the row and column corrections and the
+    // 16384 k constant are added by the first launch only.
+    for (int64_t k0 = 0; k0 < L.k_pad; k0 += p.k_chunk) {
+        const int64_t kc = L.k_pad - k0 < p.k_chunk ? L.k_pad - k0 : p.k_chunk;
+        const int ktiles = (int)(kc / 64);
+        const bool first = k0 == 0;
+        if (es == 2)
+            igemm_packed<2, 128, 128, 64, 64><<<grid, 256, 0, stream>>>(
+                Asrc + k0, lda_p, a_plane, Bpk + k0, L.k_pad, b_plane, first ? corrA : nullptr,
+                corrB, first ? L.b_slices : 0, np, first ? 16384u * (uint32_t)k : 0u, C, ldc, mi,
+                ni, ktiles, tm, tn);
+        else
+            igemm_packed<1, 256, 256, 128, 128><<<grid, 256, 0, stream>>>(
+                Asrc + k0, lda_p, 0, Bpk + k0, L.k_pad, 0, nullptr, nullptr, 0, np, 0u, C, ldc,
+                mi, ni, ktiles, tm, tn);
+        if (hipGetLastError() != hipSuccess) return IGEMM_EHIP;
+    }
+    return IGEMM_OK;
+}
+
+}  // namespace igemm

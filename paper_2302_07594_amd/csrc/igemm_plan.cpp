@@ -16,15 +16,21 @@
 namespace igemm {
 
 const KernelDesc kKernels[K_COUNT] = {
-    {"i8_256x256", 1, 256, 256, 128, 128},
-    {"i8_128x128", 1, 128, 128, 64, 64},
-    {"i8_32x256", 1, 32, 256, 32, 64},
-    {"i8_16x256", 1, 16, 256, 16, 64},
-    {"i16_128x128", 2, 128, 128, 64, 64},
-    {"i16_64x64", 2, 64, 64, 32, 32},
-    {"i16_32x128", 2, 32, 128, 32, 32},
-    {"i16_16x128", 2, 16, 128, 16, 32},
+    {"i8_256x256", 1, 256, 256, 128, 128, false},
+    {"i8_128x128", 1, 128, 128, 64, 64, false},
+    {"i8_32x256", 1, 32, 256, 32, 64, false},
+    {"i8_16x256", 1, 16, 256, 16, 64, false},
+    {"i16_128x128", 2, 128, 128, 64, 64, false},
+    {"i16_64x64", 2, 64, 64, 32, 32, false},
+    {"i16_32x128", 2, 32, 128, 32, 32, false},
+    {"i16_16x128", 2, 16, 128, 16, 32, false},
+    {"i8_packed_256x256", 1, 256, 256, 128, 128, true},
+    {"i16_packed_128x128", 2, 128, 128, 64, 64, true},
 };
+
+// Largest grid (in workgroups) of one launch: the dispatch packet counts
+// work-items in 32 bits.
+static constexpr int64_t kMaxGrid = ((int64_t)1 << 32) / kThreads - 1;
 
 static bool mul_ok(int64_t a, int64_t b, int64_t *out) {
     return !__builtin_mul_overflow(a, b, out);
@@ -62,7 +68,56 @@ static int64_t tiles_of(int id, int64_t m, int64_t n) {
     return cdiv(m, kKernels[id].bm) * cdiv(n, kKernels[id].bn);
 }
 
-static int auto_kernel(int es, int64_t m, int64_t n, int num_cu) {
+static int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
+
+void packed_layout(int es, int64_t m, int64_t n, int64_t k, int kernel, const void *A,
+                   int64_t lda, PackedLayout *L) {
+    const KernelDesc &d = kKernels[kernel];
+    L->m_pad = cdiv(m, d.bm) * d.bm;
+    L->n_pad = cdiv(n, d.bn) * d.bn;
+    // A multiple of four 64-element k-tiles, so the main loop has no remainder.
+    L->k_pad = cdiv(k, 256) * 256;
+    // pack_b: 64 columns per workgroup and k slices of whole passes (a pass
+    // covers 128 int16 or 256 int8 rows), enough slices for ~512 workgroups.
+    const int64_t colblocks = L->n_pad / 64;
+    const int64_t rows_per_pass = es == 2 ? 128 : 256;
+    const int64_t passes = L->k_pad / rows_per_pass;
+    int64_t s = cdiv(512, colblocks);
+    if (s > passes) s = passes;
+    if (s < 1) s = 1;
+    L->kspan = cdiv(passes, s) * rows_per_pass;
+    L->b_slices = (int)cdiv(L->k_pad, L->kspan);
+    const uintptr_t a = (uintptr_t)A;
+    L->pack_a = es == 2 || !(a % 16 == 0 && lda % 16 == 0 && m % d.bm == 0 && k % 256 == 0);
+    int64_t off = 0;
+    L->off_a = off;
+    if (L->pack_a) off = align256(off + es * L->m_pad * L->k_pad);
+    L->off_b = off;
+    off = align256(off + es * L->n_pad * L->k_pad);
+    L->off_corr_a = off;
+    if (es == 2) off = align256(off + 4 * L->m_pad);
+    L->off_corr_b = off;
+    if (es == 2) off = align256(off + 4 * (int64_t)L->b_slices * L->n_pad);
+    L->bytes = off;
+}
+
+// The packed path pays off once the product is large enough for the pack
+// traffic (one read and one write of each operand) to be small next to the
+// matrix-core time and there are enough tiles to fill the chip.
+static bool packed_pays(int es, int64_t m, int64_t n, int64_t k, int num_cu) {
+    const int id = es == 2 ? K_I16_PACKED_128x128 : K_I8_PACKED_256x256;
+    return k >= 1024 && m >= 1024 && n >= 1024 && tiles_of(id, m, n) >= num_cu;
+}
+
+// The packed kernel addresses its C tile with 32-bit byte offsets.
+static bool packed_fits(int id, int64_t ldc) {
+    return (int64_t)kKernels[id].bm * ldc * 4 < INT_MAX;
+}
+
+static int auto_kernel(int es, int64_t m, int64_t n, int64_t k, int64_t ldc, int num_cu,
+                       bool allow_packed) {
+    const int pid = es == 2 ? K_I16_PACKED_128x128 : K_I8_PACKED_256x256;
+    if (allow_packed && packed_pays(es, m, n, k, num_cu) && packed_fits(pid, ldc)) return pid;
     if (es == 1) {
         if (m <= 16) return K_I8_16x256;
         if (m <= 32) return K_I8_32x256;
@@ -76,8 +131,8 @@ static int auto_kernel(int es, int64_t m, int64_t n, int num_cu) {
 }
 
 int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
-              const void *B, int64_t ldb, int num_cu, int kernel, int split,
-              igemm_plan *out) {
+              const void *B, int64_t ldb, int64_t ldc, int num_cu, int kernel, int split,
+              bool allow_packed, igemm_plan *out) {
     if (out == NULL) return IGEMM_EINVAL;
     if (num_cu <= 0) num_cu = 256;
     *out = igemm_plan{};
@@ -90,10 +145,32 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
         return IGEMM_OK;  // no-op: nothing is launched
     }
     if (kernel < -1 || kernel >= K_COUNT || split < -1 || split == 0) return IGEMM_EINVAL;
-    int id = kernel >= 0 ? kernel : auto_kernel(es, m, n, num_cu);
+    int id = kernel >= 0 ? kernel : auto_kernel(es, m, n, k, ldc, num_cu, allow_packed);
     if (kKernels[id].es != es) return IGEMM_EINVAL;
     const KernelDesc &d = kKernels[id];
     const int64_t tiles = tiles_of(id, m, n);
+    const uintptr_t a = (uintptr_t)A, b = (uintptr_t)B;
+    if (d.packed) {
+        // Pack once, then one launch of the main kernel per k chunk of at most
+        // kMaxKChunk elements; the launches add into C in stream order.
+        PackedLayout L;
+        packed_layout(es, m, n, k, id, A, lda, &L);
+        if (tiles > kMaxGrid || L.m_pad > kMaxGrid || L.n_pad / 64 > kMaxGrid ||
+            L.b_slices > 65535 || !packed_fits(id, ldc))
+            return IGEMM_ENOTSUP;
+        out->kernel = id;
+        out->bm = d.bm;
+        out->bn = d.bn;
+        out->k_chunk = L.k_pad < kMaxKChunk ? L.k_pad : kMaxKChunk;
+        out->split = (int)cdiv(L.k_pad, out->k_chunk);
+        out->tiles = tiles;
+        out->grid = tiles;
+        out->vec_a = (a % 16 == 0) && ((lda * es) % 16 == 0);
+        out->vec_b = (b % 16 == 0) && ((ldb * es) % 16 == 0);
+        out->packed = 1;
+        out->workspace_bytes = L.bytes;
+        return IGEMM_OK;
+    }
     const int64_t ktiles = cdiv(k, kBK);
     const int64_t min_split = cdiv(k, kMaxKChunk);
     int64_t s;
@@ -114,8 +191,7 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
     const int64_t kchunk = cdiv(ktiles, s) * kBK;
     s = cdiv(k, kchunk);
     const int64_t grid = tiles * s;
-    if (grid > INT_MAX || cdiv(m, d.bm) > INT_MAX || cdiv(n, d.bn) > INT_MAX)
-        return IGEMM_ENOTSUP;
+    if (grid > kMaxGrid) return IGEMM_ENOTSUP;
     out->kernel = id;
     out->bm = d.bm;
     out->bn = d.bn;
@@ -123,7 +199,6 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
     out->k_chunk = kchunk;
     out->tiles = tiles;
     out->grid = grid;
-    const uintptr_t a = (uintptr_t)A, b = (uintptr_t)B;
     // Vector path: 16-byte aligned rows, and per-lane row offsets within one
     // workgroup tile that fit in 32 bits (bm rows of A, 64 rows of B).
     out->vec_a = (a % 16 == 0) && ((lda * es) % 16 == 0) && ((int64_t)d.bm * lda * es < INT_MAX);
@@ -141,7 +216,8 @@ int igemm_query_plan(int elem_bytes, int64_t m, int64_t n, int64_t k, const void
     if (out == NULL) return IGEMM_EINVAL;
     int st = igemm::validate(elem_bytes, m, n, k, A, lda, B, ldb, C, ldc);
     if (st != IGEMM_OK) return st;
-    return igemm::make_plan(elem_bytes, m, n, k, A, lda, B, ldb, num_cu, kernel, split, out);
+    return igemm::make_plan(elem_bytes, m, n, k, A, lda, B, ldb, ldc, num_cu, kernel, split,
+                            true, out);
 }
 
 int igemm_num_kernels(void) { return igemm::K_COUNT; }
@@ -156,11 +232,13 @@ const char *igemm_strerror(int status) {
         case IGEMM_OK: return "success";
         case IGEMM_EINVAL: return "invalid argument (nothing was enqueued)";
         case IGEMM_EHIP: return "HIP runtime call or kernel launch failed";
-        case IGEMM_ENOTSUP: return "unsupported size (a dimension or the grid exceeds 2^31 - 1)";
+        case IGEMM_ENOTSUP:
+            return "unsupported size (a dimension exceeds 2^31 - 1 or the grid 2^24 workgroups)";
+        case IGEMM_ENOMEM: return "the workspace could not be allocated, or is too small";
         default: return "unknown status";
     }
 }
 
-int igemm_version(void) { return 100; }
+int igemm_version(void) { return 200; }
 
 }  // extern "C"

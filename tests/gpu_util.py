@@ -22,9 +22,11 @@ def to_device(x: np.ndarray, offset_elems: int = 0):
 
 
 def gpu_gemm(A, B, C, m, n, k, kernel=-1, split=-1, offsets=(0, 0, 0), stream=None,
-             check_status=True):
+             check_status=True, workspace=None):
     """Run C += A.B on the GPU. A, B, C are full numpy arrays whose row length
     is the leading dimension; the logical shapes are m x k, k x n, m x n.
+    workspace=None calls the _ex entry point (library pool for packed plans);
+    a device tensor is passed to the _ws entry point as the workspace.
     Returns (status, C after the call as numpy)."""
     import torch
 
@@ -33,11 +35,16 @@ def gpu_gemm(A, B, C, m, n, k, kernel=-1, split=-1, offsets=(0, 0, 0), stream=No
     Ad = to_device(A, offsets[0])
     Bd = to_device(B, offsets[1])
     Cd = to_device(C, offsets[2])
-    fn = ig.igemm_i16_ex if es == 2 else ig.igemm_i8_ex
     lda, ldb, ldc = A.shape[1], B.shape[1], C.shape[1]
-    st = fn(m, n, k, Ad.data_ptr(), lda, Bd.data_ptr(), ldb, Cd.data_ptr(), ldc,
-            stream if stream is not None else torch.cuda.current_stream().cuda_stream,
-            kernel, split)
+    s = stream if stream is not None else torch.cuda.current_stream().cuda_stream
+    if workspace is None:
+        fn = ig.igemm_i16_ex if es == 2 else ig.igemm_i8_ex
+        st = fn(m, n, k, Ad.data_ptr(), lda, Bd.data_ptr(), ldb, Cd.data_ptr(), ldc, s,
+                kernel, split)
+    else:
+        fn = ig.igemm_i16_ws if es == 2 else ig.igemm_i8_ws
+        st = fn(m, n, k, Ad.data_ptr(), lda, Bd.data_ptr(), ldb, Cd.data_ptr(), ldc, s,
+                kernel, split, workspace.data_ptr(), workspace.numel())
     torch.cuda.synchronize()
     if check_status and st != 0:
         raise AssertionError(f"status {st}: {ig.igemm_strerror(st)}")

@@ -27,7 +27,7 @@ def test_header_declares_entry_points():
     fns = declared_functions()
     for name in ("igemm_i16", "igemm_i8", "igemm_strerror", "igemm_i16_ex", "igemm_i8_ex",
                  "igemm_query_plan", "igemm_num_kernels", "igemm_kernel_name",
-                 "igemm_version"):
+                 "igemm_version", "igemm_i16_ws", "igemm_i8_ws", "igemm_trim_workspace"):
         assert name in fns
 
 
@@ -108,12 +108,18 @@ def test_plans_for_workloads():
             assert p["split"] >= 1 and p["k_chunk"] % 64 == 0
             assert p["split"] * p["k_chunk"] >= case.k > (p["split"] - 1) * p["k_chunk"]
             assert p["k_chunk"] <= 32768
-            assert p["grid"] == p["tiles"] * p["split"]
+            if p["packed"]:
+                # one launch of `grid` workgroups per k chunk
+                assert p["grid"] == p["tiles"] and p["workspace_bytes"] > 0
+            else:
+                assert p["grid"] == p["tiles"] * p["split"] and p["workspace_bytes"] == 0
             assert p["limb_products"] == (4 if es == 2 else 1)
     big = ig.igemm_query_plan(2, 4096, 4096, 4096, FAKE_A, 4096, FAKE_B, 4096, FAKE_C, 4096)
-    assert big["kernel_name"] == "i16_128x128" and big["split"] == 1 and big["vec_a"] == 1
+    assert big["kernel_name"] == "i16_packed_128x128" and big["split"] == 1
     big8 = ig.igemm_query_plan(1, 8192, 8192, 8192, FAKE_A, 8192, FAKE_B, 8192, FAKE_C, 8192)
-    assert big8["kernel_name"] == "i8_256x256" and big8["split"] == 1
+    assert big8["kernel_name"] == "i8_packed_256x256" and big8["split"] == 1
+    small = ig.igemm_query_plan(2, 256, 256, 256, FAKE_A, 256, FAKE_B, 256, FAKE_C, 256)
+    assert not small["packed"] and small["workspace_bytes"] == 0
 
 
 def test_plan_alignment_and_split_rules():
@@ -133,3 +139,53 @@ def test_plan_alignment_and_split_rules():
     # no-op
     p = ig.igemm_query_plan(1, 64, 64, 0, FAKE_A, 1, FAKE_B, 64, FAKE_C, 64)
     assert p["grid"] == 0 and p["kernel"] == -1
+
+
+def _kid(name):
+    return [i for i in range(ig.igemm_num_kernels()) if ig.igemm_kernel_name(i) == name][0]
+
+
+def test_packed_workspace_layout():
+    """int16: two limb planes of A and of B (rows padded to the tile, k to a
+    multiple of 256), row corrections and per-slice column corrections; int8
+    skips the copy of an A that is aligned and tile-shaped."""
+    p = ig.igemm_query_plan(2, 4096, 4096, 4096, FAKE_A, 4096, FAKE_B, 4096, FAKE_C, 4096)
+    planes = 2 * 4096 * 4096
+    assert p["workspace_bytes"] >= 2 * planes + 4 * 4096 + 4 * 4096
+    assert p["workspace_bytes"] % 256 == 0
+    kid = _kid("i8_packed_256x256")
+    q = ig.igemm_query_plan(1, 512, 300, 768, FAKE_A, 768, FAKE_B, 300, FAKE_C, 300, kernel=kid)
+    assert q["workspace_bytes"] == 512 * 768           # B only: n_pad = 512, k_pad = 768
+    q = ig.igemm_query_plan(1, 512, 300, 768, FAKE_A + 1, 768, FAKE_B, 300, FAKE_C, 300,
+                            kernel=kid)
+    assert q["workspace_bytes"] == 512 * 768 + 512 * 768   # misaligned A is copied too
+    q = ig.igemm_query_plan(1, 500, 300, 768, FAKE_A, 768, FAKE_B, 300, FAKE_C, 300, kernel=kid)
+    assert q["workspace_bytes"] == 512 * 768 + 512 * 768   # ragged m: A is padded
+    # k beyond 32768: one main-kernel launch per 32768-element chunk
+    q = ig.igemm_query_plan(2, 300, 200, 70000, FAKE_A, 70000, FAKE_B, 200, FAKE_C, 200,
+                            kernel=_kid("i16_packed_128x128"))
+    assert q["split"] == 3 and q["k_chunk"] == 32768 and q["packed"] == 1
+
+
+def test_packed_grid_limits():
+    kid = _kid("i16_packed_128x128")
+    m = 1 << 25   # more padded rows than one launch can cover with pack_a
+    with pytest.raises(ig.IgemmError) as e:
+        ig.igemm_query_plan(2, m, 256, 256, FAKE_A, 256, FAKE_B, 256, FAKE_C, 256, kernel=kid)
+    assert e.value.status == ig.IGEMM_ENOTSUP
+
+
+@pytest.mark.parametrize("fn", [ig.igemm_i16_ws, ig.igemm_i8_ws])
+def test_ws_rejects_bad_workspace(fn):
+    s = 0
+    E = ig.IGEMM_EINVAL
+    # a misaligned or negative-size workspace is refused before any HIP call
+    assert fn(4, 4, 4, FAKE_A, 4, FAKE_B, 4, FAKE_C, 4, s, -1, -1, 0x40001, 1 << 20) == E
+    assert fn(4, 4, 4, FAKE_A, 4, FAKE_B, 4, FAKE_C, 4, s, -1, -1, 0x40000, -5) == E
+    # argument checks come first, as for the other calls
+    assert fn(4, 4, 4, FAKE_A, 3, FAKE_B, 4, FAKE_C, 4, s, -1, -1, 0x40000, 1 << 20) == E
+    assert fn(0, 4, 4, 0, 4, 0, 4, 0, 4, s, -1, -1, 0, 0) == ig.IGEMM_OK
+
+
+def test_strerror_enomem():
+    assert "workspace" in ig.igemm_strerror(ig.IGEMM_ENOMEM)

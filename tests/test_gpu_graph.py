@@ -10,8 +10,12 @@ pytestmark = pytest.mark.gpu
 
 
 @pytest.mark.parametrize("dt,shape,split", [("i16", (130, 260, 300), -1), ("i8", (40, 300, 700), 5),
-                                            ("i16", (256, 256, 256), 1)])
+                                            ("i16", (256, 256, 256), 1),
+                                            ("i16", (1100, 1030, 1200), -1),
+                                            ("i8", (1030, 1100, 1300), -1)])
 def test_graph_replays_match_eager(dt, shape, split):
+    """The last two shapes take the packed path; its workspace comes from
+    torch's caching allocator, which is capture-aware."""
     import torch
     import paper_2302_07594_amd as ig
     m, n, k = shape

@@ -1,0 +1,166 @@
+"""GPU parity of the pack-then-multiply path (pack kernels into a workspace,
+then the DMA-fed matrix-core kernel) against the CPU oracle, bit-exact, and
+its workspace handling: library pool, caller workspace, too-small and
+misaligned workspaces, graph capture."""
+import numpy as np
+import pytest
+
+import workloads
+from gpu_util import describe_mismatch, gpu_gemm, oracle_gemm
+
+pytestmark = pytest.mark.gpu
+
+PACKED = {"i16": "i16_packed_128x128", "i8": "i8_packed_256x256"}
+
+
+def _ig():
+    import paper_2302_07594_amd as ig
+    return ig
+
+
+def _kid(dt):
+    ig = _ig()
+    return [i for i in range(ig.igemm_num_kernels()) if ig.igemm_kernel_name(i) == PACKED[dt]][0]
+
+
+def _workspace(nbytes):
+    import torch
+    return torch.empty(max(nbytes, 1), dtype=torch.uint8, device="cuda")
+
+
+def _check(dt, A, B, C, m, n, k, **kw):
+    _, got = gpu_gemm(A, B, C, m, n, k, kernel=_kid(dt), **kw)
+    want = oracle_gemm(A, B, C, m, n, k)
+    assert np.array_equal(got, want), describe_mismatch(got, want)
+    return got
+
+
+SHAPES = [
+    (1, 1, 1),
+    (7, 300, 5),              # k far below one 256-element pack unit
+    (129, 257, 255),          # one more than a tile in m and n, k just below 256
+    (256, 256, 256),          # exactly one int8 tile
+    (300, 520, 1000),         # several tiles, ragged everywhere
+    (640, 384, 2304),         # tile multiples (int8 A taken unpacked when aligned)
+]
+
+
+@pytest.mark.parametrize("dt", ["i16", "i8"])
+@pytest.mark.parametrize("shape", SHAPES, ids=["x".join(map(str, s)) for s in SHAPES])
+def test_packed_ragged_pool(dt, shape):
+    m, n, k = shape
+    A, B, C = workloads.random_operands(dt, m, n, k, seed=600 + m + 3 * n + 7 * k)
+    _check(dt, A, B, C, m, n, k)
+
+
+@pytest.mark.parametrize("dt", ["i16", "i8"])
+@pytest.mark.parametrize("shape", SHAPES[2:5], ids=["x".join(map(str, s)) for s in SHAPES[2:5]])
+def test_packed_caller_workspace(dt, shape):
+    ig = _ig()
+    m, n, k = shape
+    A, B, C = workloads.random_operands(dt, m, n, k, seed=700 + m + n + k)
+    es = 2 if dt == "i16" else 1
+    need = ig.igemm_query_plan(es, m, n, k, kernel=_kid(dt))["workspace_bytes"]
+    ws = _workspace(need)
+    ws.fill_(0x5A)   # stale contents must not matter
+    _check(dt, A, B, C, m, n, k, workspace=ws)
+
+
+@pytest.mark.parametrize("dt", ["i16", "i8"])
+def test_packed_small_or_misaligned_workspace_rejected(dt):
+    ig = _ig()
+    m, n, k = 200, 300, 500
+    A, B, C = workloads.random_operands(dt, m, n, k, seed=41)
+    es = 2 if dt == "i16" else 1
+    need = ig.igemm_query_plan(es, m, n, k, kernel=_kid(dt))["workspace_bytes"]
+    ws = _workspace(need + 512)
+    st, got = gpu_gemm(A, B, C, m, n, k, kernel=_kid(dt), workspace=ws[: need - 256],
+                       check_status=False)
+    assert st == ig.IGEMM_ENOMEM and np.array_equal(got, C)
+    st, got = gpu_gemm(A, B, C, m, n, k, kernel=_kid(dt), workspace=ws[16:],
+                       check_status=False)
+    assert st == ig.IGEMM_EINVAL and np.array_equal(got, C)
+
+
+@pytest.mark.parametrize("dt", ["i16", "i8"])
+@pytest.mark.parametrize("offsets", [(1, 0, 0), (0, 1, 0), (1, 1, 1)])
+def test_packed_misaligned_operands(dt, offsets):
+    m, n, k = 260, 270, 600
+    A, B, C = workloads.random_operands(dt, m, n, k, seed=43, lda=k + 3, ldb=n + 1, ldc=n + 2)
+    got = _check(dt, A, B, C, m, n, k, offsets=offsets)
+    assert np.array_equal(got[:, n:], C[:, n:])
+
+
+@pytest.mark.parametrize("value", [-32768, 32767])
+def test_packed_int16_extremes_multi_chunk(value):
+    """k = 40000 > 32768: two main-kernel launches over one packing; every
+    limb sum is at its bound."""
+    m, n, k = 40, 70, 40000
+    A = np.full((m, k), value, np.int16)
+    B = np.full((k, n), value, np.int16)
+    C = np.zeros((m, n), np.int32)
+    got = _check("i16", A, B, C, m, n, k)
+    assert np.all(got == got[0, 0])
+
+
+@pytest.mark.parametrize("value", [-128, 127])
+def test_packed_int8_extremes_multi_chunk(value):
+    m, n, k = 33, 65, 70000
+    A = np.full((m, k), value, np.int8)
+    B = np.full((k, n), value, np.int8)
+    C = np.full((m, n), 2 ** 31 - 1000, np.int32)
+    _check("i8", A, B, C, m, n, k)
+
+
+@pytest.mark.parametrize("dt", ["i16", "i8"])
+def test_packed_random_multi_chunk(dt):
+    m, n, k = 130, 200, 33000
+    A, B, C = workloads.random_operands(dt, m, n, k, seed=47)
+    _check(dt, A, B, C, m, n, k)
+
+
+@pytest.mark.parametrize("dt", ["i16", "i8"])
+def test_packed_matches_fused(dt):
+    """Same inputs through the packed kernel and every fused kernel of the type."""
+    ig = _ig()
+    m, n, k = 300, 400, 1500
+    A, B, C = workloads.random_operands(dt, m, n, k, seed=49)
+    _, ref = gpu_gemm(A, B, C, m, n, k, kernel=_kid(dt))
+    for kid in ig.kernels_for(2 if dt == "i16" else 1):
+        _, got = gpu_gemm(A, B, C, m, n, k, kernel=kid)
+        assert np.array_equal(got, ref), ig.igemm_kernel_name(kid)
+
+
+def test_tensor_wrapper_workspace_modes():
+    import torch
+    ig = _ig()
+    m, n, k = 1024, 1100, 1300
+    A, B, C = workloads.random_operands("i16", m, n, k, seed=51)
+    want = oracle_gemm(A, B, C, m, n, k)
+    for mode in (None, "library"):
+        Ad, Bd, Cd = (torch.from_numpy(x).cuda() for x in (A, B, C))
+        ig.gemm_i16(Ad, Bd, Cd, kernel=_kid("i16"), workspace=mode)
+        torch.cuda.synchronize()
+        assert np.array_equal(Cd.cpu().numpy(), want), mode
+    assert ig.igemm_trim_workspace() == ig.IGEMM_OK
+
+
+def test_capture_refuses_pool_for_explicit_packed():
+    """Under stream capture the pool is not used: an explicit packed kernel
+    without a workspace is refused, and nothing is recorded."""
+    import torch
+    ig = _ig()
+    m, n, k = 256, 256, 512
+    A, B, C = workloads.random_operands("i16", m, n, k, seed=53)
+    Ad, Bd, Cd = (torch.from_numpy(x).cuda() for x in (A, B, C))
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            st = ig.igemm_i16_ex(m, n, k, Ad, k, Bd, n, Cd, n, s.cuda_stream, _kid("i16"), -1)
+            Cd.add_(0)   # keep the captured graph non-empty
+    assert st == ig.IGEMM_EINVAL
+    g.replay()
+    torch.cuda.synchronize()
+    assert np.array_equal(Cd.cpu().numpy(), C)

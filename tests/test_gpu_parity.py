@@ -32,7 +32,7 @@ def test_int16_256_cube_full():
 
 
 def _kernel_shapes(name):
-    bm, bn = (int(x) for x in name.split("_")[1].split("x"))
+    bm, bn = (int(x) for x in name.split("_")[-1].split("x"))
     return [
         (bm, bn, 64),                      # exactly one tile, one k-tile
         (bm + 3, bn + 5, 3 * 64 + 17),     # ragged m, n and k tails, several tiles
