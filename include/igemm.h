@@ -167,6 +167,48 @@ int igemm_i8_ws(int64_t m, int64_t n, int64_t k,
                 int32_t *C, int64_t ldc, void *stream,
                 int kernel, int split, void *workspace, int64_t workspace_bytes);
 
+/*
+ * Pack once, multiply many times. In DL inference one operand is fixed
+ * (the weights) and the paper packs it once and reuses it (Sec. 5.1); these
+ * calls split the packed path into its two parts so that a caller can keep
+ * the packed operands and run only the multiply:
+ *   igemm_pack_i16 / igemm_pack_i8  write the packed A and B of the product
+ *            C += A B into `workspace` (A and B as in igemm_i16 / igemm_i8;
+ *            C is not touched).
+ *   igemm_i16_prepacked / igemm_i8_prepacked  run the multiply C += A B on
+ *            a workspace filled by the pack call with the same m, n, k, A,
+ *            lda and kernel (A itself is read only by int8 plans that use it
+ *            in place of a packed copy: 16-byte aligned A, lda a multiple
+ *            of 16, m a multiple of 256 and k of 256).
+ *   kernel   -1 = the packed kernel of the operand type, otherwise a packed
+ *            kernel index of that type (IGEMM_EINVAL for fused kernels).
+ *   workspace, workspace_bytes  device memory owned by the caller,
+ *            256-byte aligned, at least plan.workspace_bytes of
+ *            igemm_query_plan for that kernel (IGEMM_EINVAL for NULL or
+ *            misaligned, IGEMM_ENOMEM if too small; nothing is enqueued).
+ * Both calls are asynchronous on `stream`; the multiply must be ordered
+ * after the pack (same stream, or an event) and the workspace kept intact
+ * between them. Sizes beyond the packed path's limits return IGEMM_ENOTSUP.
+ */
+int igemm_pack_i16(int64_t m, int64_t n, int64_t k,
+                   const int16_t *A, int64_t lda,
+                   const int16_t *B, int64_t ldb,
+                   int kernel, void *workspace, int64_t workspace_bytes, void *stream);
+int igemm_pack_i8(int64_t m, int64_t n, int64_t k,
+                  const int8_t *A, int64_t lda,
+                  const int8_t *B, int64_t ldb,
+                  int kernel, void *workspace, int64_t workspace_bytes, void *stream);
+int igemm_i16_prepacked(int64_t m, int64_t n, int64_t k,
+                        const int16_t *A, int64_t lda,
+                        int32_t *C, int64_t ldc,
+                        int kernel, const void *workspace, int64_t workspace_bytes,
+                        void *stream);
+int igemm_i8_prepacked(int64_t m, int64_t n, int64_t k,
+                       const int8_t *A, int64_t lda,
+                       int32_t *C, int64_t ldc,
+                       int kernel, const void *workspace, int64_t workspace_bytes,
+                       void *stream);
+
 /* Release the memory the library's workspace pool for the current device
  * holds beyond what in-flight calls use (hipMemPoolTrimTo). Returns
  * IGEMM_OK, or IGEMM_EHIP. */

@@ -13,6 +13,10 @@ Same names as the C ABI:
     igemm_i16_ws / igemm_i8_ws(..., kernel=-1, split=-1, workspace=None,
                                workspace_bytes=0)
     igemm_trim_workspace()
+    igemm_pack_i16 / igemm_pack_i8(m, n, k, A, lda, B, ldb, kernel=-1,
+                                   workspace, workspace_bytes, stream=None)
+    igemm_i16_prepacked / igemm_i8_prepacked(m, n, k, A, lda, C, ldc, kernel=-1,
+                                             workspace, workspace_bytes, stream=None)
     igemm_query_plan(elem_bytes, m, n, k, A, lda, B, ldb, C, ldc, num_cu=0,
                      kernel=-1, split=-1) -> dict
     igemm_strerror(status), igemm_kernel_name(i), igemm_num_kernels(),
@@ -78,6 +82,12 @@ def _load():
         getattr(lib, name + "_ex").restype = ci
         getattr(lib, name + "_ws").argtypes = gemm_args + [ci, ci, vp, i64]
         getattr(lib, name + "_ws").restype = ci
+    for name in ("igemm_pack_i16", "igemm_pack_i8"):
+        getattr(lib, name).argtypes = [i64, i64, i64, vp, i64, vp, i64, ci, vp, i64, vp]
+        getattr(lib, name).restype = ci
+    for name in ("igemm_i16_prepacked", "igemm_i8_prepacked"):
+        getattr(lib, name).argtypes = [i64, i64, i64, vp, i64, vp, i64, ci, vp, i64, vp]
+        getattr(lib, name).restype = ci
     lib.igemm_trim_workspace.argtypes = []
     lib.igemm_trim_workspace.restype = ci
     lib.igemm_query_plan.argtypes = [ci, i64, i64, i64, vp, i64, vp, i64, vp, i64, ci, ci, ci,
@@ -175,6 +185,34 @@ def igemm_i8_ws(m, n, k, A, lda, B, ldb, C, ldc, stream=None, kernel=-1, split=-
                  int(split), _addr(workspace), int(workspace_bytes))
 
 
+def igemm_pack_i16(m, n, k, A, lda, B, ldb, kernel=-1, workspace=None, workspace_bytes=0,
+                   stream=None) -> int:
+    return int(_lib.igemm_pack_i16(int(m), int(n), int(k), _addr(A), int(lda), _addr(B),
+                                   int(ldb), int(kernel), _addr(workspace), int(workspace_bytes),
+                                   _stream(stream)))
+
+
+def igemm_pack_i8(m, n, k, A, lda, B, ldb, kernel=-1, workspace=None, workspace_bytes=0,
+                  stream=None) -> int:
+    return int(_lib.igemm_pack_i8(int(m), int(n), int(k), _addr(A), int(lda), _addr(B),
+                                  int(ldb), int(kernel), _addr(workspace), int(workspace_bytes),
+                                  _stream(stream)))
+
+
+def igemm_i16_prepacked(m, n, k, A, lda, C, ldc, kernel=-1, workspace=None, workspace_bytes=0,
+                        stream=None) -> int:
+    return int(_lib.igemm_i16_prepacked(int(m), int(n), int(k), _addr(A), int(lda), _addr(C),
+                                        int(ldc), int(kernel), _addr(workspace),
+                                        int(workspace_bytes), _stream(stream)))
+
+
+def igemm_i8_prepacked(m, n, k, A, lda, C, ldc, kernel=-1, workspace=None, workspace_bytes=0,
+                       stream=None) -> int:
+    return int(_lib.igemm_i8_prepacked(int(m), int(n), int(k), _addr(A), int(lda), _addr(C),
+                                       int(ldc), int(kernel), _addr(workspace),
+                                       int(workspace_bytes), _stream(stream)))
+
+
 def igemm_trim_workspace() -> int:
     return int(_lib.igemm_trim_workspace())
 
@@ -265,6 +303,17 @@ def _num_cu(device) -> int:
     return _num_cu_cache[idx]
 
 
+def _aligned_workspace(nbytes, device, stream=None):
+    """A uint8 device tensor of nbytes from torch's caching allocator,
+    256-byte aligned, recorded on `stream` if that is a torch stream."""
+    import torch
+    ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+    if stream is not None and hasattr(stream, "cuda_stream"):
+        ws.record_stream(stream)
+    off = (-ws.data_ptr()) % 256
+    return ws[off:off + nbytes]
+
+
 def _gemm(es, A, B, C, stream, kernel, split, workspace, name):
     import torch
     m, n, k, lda, ldb, ldc = _check_tensors(A, B, C, torch.int16 if es == 2 else torch.int8, name)
@@ -276,13 +325,7 @@ def _gemm(es, A, B, C, stream, kernel, split, workspace, name):
                                     kernel, split)
             if plan["workspace_bytes"] > 0:
                 ws_bytes = plan["workspace_bytes"]
-                ws = torch.empty(ws_bytes + 256, dtype=torch.uint8, device=C.device)
-                if stream is not None and hasattr(stream, "cuda_stream"):
-                    ws.record_stream(stream)
-                # the caching allocator hands out 512-byte aligned blocks
-                if ws.data_ptr() % 256:
-                    off = 256 - ws.data_ptr() % 256
-                    ws = ws[off:]
+                ws = _aligned_workspace(ws_bytes, C.device, stream)
     elif workspace == "library":
         pass
     elif hasattr(workspace, "data_ptr"):
@@ -292,6 +335,71 @@ def _gemm(es, A, B, C, stream, kernel, split, workspace, name):
     st = fn(m, n, k, A, lda, B, ldb, C, ldc, stream, kernel, split, ws, ws_bytes)
     if st != IGEMM_OK:
         raise IgemmError(st, name)
+    return C
+
+
+class Packed:
+    """Packed operands of C += A.B (pack once, multiply many times).
+
+    Holds the device workspace written by igemm_pack_*, the shape and the A
+    it was packed with (int8 plans may read A in place)."""
+
+    def __init__(self, es, m, n, k, A, lda, kernel, workspace, nbytes):
+        self.es, self.m, self.n, self.k = es, m, n, k
+        self.A, self.lda, self.kernel = A, lda, kernel
+        self.workspace, self.nbytes = workspace, nbytes
+
+
+def _packed_kernel(es):
+    want = "i16_packed_128x128" if es == 2 else "i8_packed_256x256"
+    return [i for i in range(igemm_num_kernels()) if igemm_kernel_name(i) == want][0]
+
+
+def pack(A, B, stream=None):
+    """Pack the operands of C += A.B (2-D torch.int16 or torch.int8 CUDA
+    tensors, unit stride along rows). Returns a Packed object for
+    gemm_prepacked; A must stay alive and unchanged while it is used."""
+    import torch
+    if A.dtype not in (torch.int16, torch.int8) or B.dtype != A.dtype:
+        raise TypeError("pack: A and B must both be torch.int16 or both torch.int8")
+    es = 2 if A.dtype == torch.int16 else 1
+    if A.dim() != 2 or B.dim() != 2 or A.shape[1] != B.shape[0]:
+        raise ValueError(f"pack: shapes {tuple(A.shape)} x {tuple(B.shape)}")
+    for t, nm in ((A, "A"), (B, "B")):
+        if not t.is_cuda:
+            raise ValueError(f"pack: {nm} must be a CUDA (HIP) tensor")
+        if t.shape[1] > 1 and t.stride(1) != 1:
+            raise ValueError(f"pack: {nm} must have unit stride along rows")
+    m, k = A.shape
+    n = B.shape[1]
+    lda = A.stride(0) if m > 1 else max(k, 1)
+    ldb = B.stride(0) if k > 1 else max(n, 1)
+    kid = _packed_kernel(es)
+    nbytes = 0
+    if m and n and k:
+        plan = igemm_query_plan(es, m, n, k, A, lda, B, ldb, None, n, _num_cu(A.device), kid)
+        nbytes = plan["workspace_bytes"]
+    ws = _aligned_workspace(max(nbytes, 1), A.device, stream)
+    fn = igemm_pack_i16 if es == 2 else igemm_pack_i8
+    st = fn(m, n, k, A, lda, B, ldb, kid, ws, nbytes, stream)
+    if st != IGEMM_OK:
+        raise IgemmError(st, "pack")
+    return Packed(es, m, n, k, A, lda, kid, ws, nbytes)
+
+
+def gemm_prepacked(P, C, stream=None):
+    """C += A.B from operands packed by pack(); C is a torch.int32 CUDA
+    tensor of shape (m, n) with unit stride along rows. Returns C."""
+    import torch
+    if C.dtype != torch.int32 or C.dim() != 2 or tuple(C.shape) != (P.m, P.n) or not C.is_cuda:
+        raise ValueError("gemm_prepacked: C must be an int32 CUDA tensor of shape (m, n)")
+    if C.shape[1] > 1 and C.stride(1) != 1:
+        raise ValueError("gemm_prepacked: C must have unit stride along rows")
+    ldc = C.stride(0) if C.shape[0] > 1 else max(C.shape[1], 1)
+    fn = igemm_i16_prepacked if P.es == 2 else igemm_i8_prepacked
+    st = fn(P.m, P.n, P.k, P.A, P.lda, C, ldc, P.kernel, P.workspace, P.nbytes, stream)
+    if st != IGEMM_OK:
+        raise IgemmError(st, "gemm_prepacked")
     return C
 
 

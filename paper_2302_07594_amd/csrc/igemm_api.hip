@@ -84,7 +84,9 @@ int run(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, con
     if (!p.packed) return launch_tiled(es, p, m, n, k, A, lda, B, ldb, C, ldc, stream);
     if (workspace != nullptr) {
         if (workspace_bytes < p.workspace_bytes) return IGEMM_ENOMEM;
-        return launch_packed(es, p, m, n, k, A, lda, B, ldb, C, ldc, workspace, stream);
+        st = launch_pack(es, p, m, n, k, A, lda, B, ldb, workspace, stream);
+        if (st != IGEMM_OK) return st;
+        return launch_multiply(es, p, m, n, k, A, lda, C, ldc, workspace, stream);
     }
     hipMemPool_t pool = nullptr;
     st = pool_of_current_device(&pool);
@@ -95,9 +97,53 @@ int run(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, con
         (void)hipGetLastError();
         return IGEMM_ENOMEM;
     }
-    st = launch_packed(es, p, m, n, k, A, lda, B, ldb, C, ldc, ws, stream);
+    st = launch_pack(es, p, m, n, k, A, lda, B, ldb, ws, stream);
+    if (st == IGEMM_OK) st = launch_multiply(es, p, m, n, k, A, lda, C, ldc, ws, stream);
     if (hipFreeAsync(ws, s) != hipSuccess && st == IGEMM_OK) st = IGEMM_EHIP;
     return st;
+}
+
+// Plan of a pack-once call: the packed kernel of the operand type (kernel -1)
+// or the given packed kernel; the B and C arguments only need to pass the
+// argument checks.
+int packed_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
+                const void *B, int64_t ldb, int64_t ldc, int kernel, const void *workspace,
+                int64_t workspace_bytes, igemm_plan *p) {
+    if (kernel < -1 || kernel >= K_COUNT) return IGEMM_EINVAL;
+    if (kernel == -1) kernel = es == 2 ? K_I16_PACKED_128x128 : K_I8_PACKED_256x256;
+    if (kKernels[kernel].es != es || !kKernels[kernel].packed) return IGEMM_EINVAL;
+    if (workspace == nullptr || (uintptr_t)workspace % 256 != 0 || workspace_bytes < 0)
+        return IGEMM_EINVAL;
+    int st = make_plan(es, m, n, k, A, lda, B, ldb, ldc, 256, kernel, -1, true, p);
+    if (st != IGEMM_OK) return st;
+    return workspace_bytes < p->workspace_bytes ? IGEMM_ENOMEM : IGEMM_OK;
+}
+
+int run_pack(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, const void *B,
+             int64_t ldb, int kernel, void *workspace, int64_t workspace_bytes, void *stream) {
+    // C is not touched by packing: a placeholder passes the checks.
+    const void *fake_c = (const void *)(uintptr_t)4096;
+    int st = validate(es, m, n, k, A, lda, B, ldb, fake_c, n > 0 ? n : 1);
+    if (st != IGEMM_OK) return st;
+    if (m == 0 || n == 0 || k == 0) return IGEMM_OK;
+    igemm_plan p;
+    st = packed_plan(es, m, n, k, A, lda, B, ldb, n, kernel, workspace, workspace_bytes, &p);
+    if (st != IGEMM_OK) return st;
+    return launch_pack(es, p, m, n, k, A, lda, B, ldb, workspace, stream);
+}
+
+int run_prepacked(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
+                  int32_t *C, int64_t ldc, int kernel, const void *workspace,
+                  int64_t workspace_bytes, void *stream) {
+    // B was consumed by the pack call: a placeholder passes the checks.
+    const void *fake_b = (const void *)(uintptr_t)4096;
+    int st = validate(es, m, n, k, A, lda, fake_b, n > 0 ? n : 1, C, ldc);
+    if (st != IGEMM_OK) return st;
+    if (m == 0 || n == 0 || k == 0) return IGEMM_OK;
+    igemm_plan p;
+    st = packed_plan(es, m, n, k, A, lda, fake_b, n, ldc, kernel, workspace, workspace_bytes, &p);
+    if (st != IGEMM_OK) return st;
+    return launch_multiply(es, p, m, n, k, A, lda, C, ldc, workspace, stream);
 }
 
 }  // namespace
@@ -139,6 +185,32 @@ int igemm_i8_ws(int64_t m, int64_t n, int64_t k, const int8_t *A, int64_t lda,
                 int kernel, int split, void *workspace, int64_t workspace_bytes) {
     return igemm::run(1, m, n, k, A, lda, B, ldb, C, ldc, stream, kernel, split, workspace,
                       workspace_bytes);
+}
+
+int igemm_pack_i16(int64_t m, int64_t n, int64_t k, const int16_t *A, int64_t lda,
+                   const int16_t *B, int64_t ldb, int kernel, void *workspace,
+                   int64_t workspace_bytes, void *stream) {
+    return igemm::run_pack(2, m, n, k, A, lda, B, ldb, kernel, workspace, workspace_bytes, stream);
+}
+
+int igemm_pack_i8(int64_t m, int64_t n, int64_t k, const int8_t *A, int64_t lda,
+                  const int8_t *B, int64_t ldb, int kernel, void *workspace,
+                  int64_t workspace_bytes, void *stream) {
+    return igemm::run_pack(1, m, n, k, A, lda, B, ldb, kernel, workspace, workspace_bytes, stream);
+}
+
+int igemm_i16_prepacked(int64_t m, int64_t n, int64_t k, const int16_t *A, int64_t lda,
+                        int32_t *C, int64_t ldc, int kernel, const void *workspace,
+                        int64_t workspace_bytes, void *stream) {
+    return igemm::run_prepacked(2, m, n, k, A, lda, C, ldc, kernel, workspace, workspace_bytes,
+                                stream);
+}
+
+int igemm_i8_prepacked(int64_t m, int64_t n, int64_t k, const int8_t *A, int64_t lda,
+                       int32_t *C, int64_t ldc, int kernel, const void *workspace,
+                       int64_t workspace_bytes, void *stream) {
+    return igemm::run_prepacked(1, m, n, k, A, lda, C, ldc, kernel, workspace, workspace_bytes,
+                                stream);
 }
 
 int igemm_trim_workspace(void) {

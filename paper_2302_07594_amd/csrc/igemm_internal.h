@@ -72,8 +72,11 @@ void packed_layout(int es, int64_t m, int64_t n, int64_t k, int kernel, const vo
 int launch_tiled(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
                  int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
                  void *stream);
-int launch_packed(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
-                  int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
-                  void *workspace, void *stream);
+// The packed path in two parts: pack A and B into the workspace, then run
+// the multiply (one launch per k chunk) on a packed workspace.
+int launch_pack(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                int64_t lda, const void *B, int64_t ldb, void *workspace, void *stream);
+int launch_multiply(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                    int64_t lda, int32_t *C, int64_t ldc, const void *workspace, void *stream);
 
 }  // namespace igemm

@@ -456,9 +456,8 @@ using namespace packed;
 // ---------------------------------------------------------------------------
 // Host side of the packed path.
 
-int launch_packed(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
-                  int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
-                  void *workspace, void *stream_) {
+int launch_pack(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                int64_t lda, const void *B, int64_t ldb, void *workspace, void *stream_) {
     hipStream_t stream = (hipStream_t)stream_;
     PackedLayout L;
     packed_layout(es, m, n, k, p.kernel, A, lda, &L);
@@ -488,23 +487,34 @@ int launch_packed(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, 
         }
         if (hipGetLastError() != hipSuccess) return IGEMM_EHIP;
     }
-    {
-        const dim3 g((unsigned)(L.n_pad / 64), (unsigned)L.b_slices);
-        const int ks = (int)L.kspan;
-        if (es == 2) {
-            int8_t *Bl = Bpk + b_plane;
-            if (vb)
-                pack_b<2, true><<<g, 256, 0, stream>>>(B, ldb, ki, ni, kp, ks, np, Bpk, Bl, corrB);
-            else
-                pack_b<2, false><<<g, 256, 0, stream>>>(B, ldb, ki, ni, kp, ks, np, Bpk, Bl, corrB);
-        } else {
-            if (vb)
-                pack_b<1, true><<<g, 256, 0, stream>>>(B, ldb, ki, ni, kp, ks, np, Bpk, Bpk, corrB);
-            else
-                pack_b<1, false><<<g, 256, 0, stream>>>(B, ldb, ki, ni, kp, ks, np, Bpk, Bpk, corrB);
-        }
-        if (hipGetLastError() != hipSuccess) return IGEMM_EHIP;
+    const dim3 g((unsigned)(L.n_pad / 64), (unsigned)L.b_slices);
+    const int ks = (int)L.kspan;
+    if (es == 2) {
+        int8_t *Bl = Bpk + b_plane;
+        if (vb)
+            pack_b<2, true><<<g, 256, 0, stream>>>(B, ldb, ki, ni, kp, ks, np, Bpk, Bl, corrB);
+        else
+            pack_b<2, false><<<g, 256, 0, stream>>>(B, ldb, ki, ni, kp, ks, np, Bpk, Bl, corrB);
+    } else {
+        if (vb)
+            pack_b<1, true><<<g, 256, 0, stream>>>(B, ldb, ki, ni, kp, ks, np, Bpk, Bpk, corrB);
+        else
+            pack_b<1, false><<<g, 256, 0, stream>>>(B, ldb, ki, ni, kp, ks, np, Bpk, Bpk, corrB);
     }
+    return hipGetLastError() == hipSuccess ? IGEMM_OK : IGEMM_EHIP;
+}
+
+int launch_multiply(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                    int64_t lda, int32_t *C, int64_t ldc, const void *workspace, void *stream_) {
+    hipStream_t stream = (hipStream_t)stream_;
+    PackedLayout L;
+    packed_layout(es, m, n, k, p.kernel, A, lda, &L);
+    const int8_t *ws = (const int8_t *)workspace;
+    const int mi = (int)m, ni = (int)n, np = (int)L.n_pad;
+    const int8_t *Apk = ws + L.off_a, *Bpk = ws + L.off_b;
+    const uint32_t *corrA = (const uint32_t *)(ws + L.off_corr_a);
+    const uint32_t *corrB = (const uint32_t *)(ws + L.off_corr_b);
+    const int64_t a_plane = L.m_pad * L.k_pad, b_plane = L.n_pad * L.k_pad;
     const KernelDesc &d = kKernels[p.kernel];
     const int tm = (int)(L.m_pad / d.bm), tn = (int)(L.n_pad / d.bn);
     const int8_t *Asrc = L.pack_a ? Apk : (const int8_t *)A;

@@ -189,3 +189,27 @@ def test_ws_rejects_bad_workspace(fn):
 
 def test_strerror_enomem():
     assert "workspace" in ig.igemm_strerror(ig.IGEMM_ENOMEM)
+
+
+@pytest.mark.parametrize("es", [2, 1])
+def test_pack_once_calls_reject_bad_arguments(es):
+    """Argument, kernel and workspace checks of the pack-once calls come
+    before any HIP call."""
+    s = 0
+    pk = ig.igemm_pack_i16 if es == 2 else ig.igemm_pack_i8
+    mul = ig.igemm_i16_prepacked if es == 2 else ig.igemm_i8_prepacked
+    W = 0x40000
+    E = ig.IGEMM_EINVAL
+    fused = ig.kernels_for(es)[0]
+    assert pk(64, 64, 64, FAKE_A, 64, FAKE_B, 64, -1, 0, 1 << 20, s) == E        # no workspace
+    assert pk(64, 64, 64, FAKE_A, 64, FAKE_B, 64, -1, W + 16, 1 << 20, s) == E   # misaligned
+    assert pk(64, 64, 64, FAKE_A, 64, FAKE_B, 64, fused, W, 1 << 20, s) == E     # fused kernel
+    assert pk(64, 64, 64, FAKE_A, 63, FAKE_B, 64, -1, W, 1 << 20, s) == E        # lda < k
+    assert pk(64, 64, 64, FAKE_A, 64, FAKE_B, 64, -1, W, 256, s) == ig.IGEMM_ENOMEM
+    assert pk(0, 64, 64, FAKE_A, 64, FAKE_B, 64, -1, W, 0, s) == ig.IGEMM_OK      # no-op
+    assert mul(64, 64, 64, FAKE_A, 64, FAKE_C, 64, -1, 0, 1 << 20, s) == E
+    assert mul(64, 64, 64, FAKE_A, 64, 0, 64, -1, W, 1 << 20, s) == E             # C NULL
+    assert mul(64, 64, 64, FAKE_A, 64, FAKE_C, 63, -1, W, 1 << 20, s) == E        # ldc < n
+    assert mul(64, 64, 64, FAKE_A, 64, FAKE_C, 64, fused, W, 1 << 20, s) == E
+    assert mul(64, 64, 64, FAKE_A, 64, FAKE_C, 64, -1, W, 256, s) == ig.IGEMM_ENOMEM
+    assert mul(64, 64, 0, FAKE_A, 1, FAKE_C, 64, -1, W, 0, s) == ig.IGEMM_OK

@@ -164,3 +164,39 @@ def test_capture_refuses_pool_for_explicit_packed():
     g.replay()
     torch.cuda.synchronize()
     assert np.array_equal(Cd.cpu().numpy(), C)
+
+
+@pytest.mark.parametrize("dt,shape", [("i16", (300, 520, 1000)), ("i8", (300, 520, 1000)),
+                                      ("i8", (512, 384, 768)), ("i16", (130, 200, 33000))])
+def test_pack_once_multiply_twice(dt, shape):
+    """One pack, two multiplies into different C: both match the oracle
+    (int8 512x384x768 reads A in place; int16 k = 33000 runs two chunks)."""
+    import torch
+    ig = _ig()
+    m, n, k = shape
+    A, B, C1 = workloads.random_operands(dt, m, n, k, seed=800 + m)
+    C2 = workloads.random_operands(dt, m, n, 1, seed=900 + m)[2]
+    Ad, Bd = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+    P = ig.pack(Ad, Bd)
+    del Bd   # B is no longer needed once packed
+    torch.cuda.synchronize()
+    for Cn in (C1, C2):
+        Cd = torch.from_numpy(Cn).cuda()
+        ig.gemm_prepacked(P, Cd)
+        torch.cuda.synchronize()
+        want = oracle_gemm(A, B, Cn, m, n, k)
+        got = Cd.cpu().numpy()
+        assert np.array_equal(got, want), describe_mismatch(got, want)
+
+
+def test_prepacked_equals_one_shot_call():
+    import torch
+    ig = _ig()
+    m, n, k = 640, 700, 900
+    A, B, C = workloads.random_operands("i16", m, n, k, seed=61)
+    Ad, Bd = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+    C1, C2 = torch.from_numpy(C).cuda(), torch.from_numpy(C).cuda()
+    ig.gemm_i16(Ad, Bd, C1, kernel=_kid("i16"))
+    ig.gemm_prepacked(ig.pack(Ad, Bd), C2)
+    torch.cuda.synchronize()
+    assert torch.equal(C1, C2)
