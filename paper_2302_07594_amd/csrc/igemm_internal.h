@@ -46,8 +46,8 @@ extern const KernelDesc kKernels[K_COUNT];
 //   A: es planes of m_pad rows (int16: high limb, then offset low limb),
 //      absent for int8 A that is already aligned and tile-shaped;
 //   B: es planes of n_pad rows (the columns of B);
-//   corr_a: m_pad row corrections, corr_b: b_slices x n_pad partial column
-//   corrections (int16 only).
+//   corr_a: m_pad row corrections, corr_b: n_pad column corrections (int16
+//   only; pack_b adds each k slice's column sums into them).
 struct PackedLayout {
     int64_t m_pad, n_pad, k_pad;
     int64_t kspan;     // k rows per pack_b workgroup

@@ -45,12 +45,16 @@ __device__ __forceinline__ int wave_sum(int v) {
 }
 
 // ---- pack A, int16: one workgroup per padded row ---------------------------
-// Writes Ah/Al[i][0, k_pad) and corrA[i] = 32768*sum(h) + 128*sum(l) mod 2^32.
+// Writes Ah/Al[i][0, k_pad) and corrA[i] = 32768*sum(h) + 128*sum(l) mod 2^32,
+// and zeroes corrB[0, n_pad).
 template <bool VEC>
 __global__ void __launch_bounds__(256)
 pack_a_i16(const int16_t *__restrict__ A, int64_t lda, int m, int k, int k_pad,
-           int8_t *__restrict__ Ah, int8_t *__restrict__ Al, uint32_t *__restrict__ corrA) {
+           int8_t *__restrict__ Ah, int8_t *__restrict__ Al, uint32_t *__restrict__ corrA,
+           uint32_t *__restrict__ corrB, int n_pad) {
     const int i = blockIdx.x, tid = threadIdx.x;
+    // Clear the column corrections that pack_b (next on the stream) adds into.
+    for (int j = i * 256 + tid; j < n_pad; j += gridDim.x * 256) corrB[j] = 0u;
     const int len = i < m ? k : 0;
     const int16_t *arow = A + (int64_t)(i < m ? i : 0) * lda;
     int8_t *hrow = Ah + (int64_t)i * k_pad;
@@ -103,11 +107,11 @@ pack_a_i8(const int8_t *__restrict__ A, int64_t lda, int m, int k, int k_pad,
 // bytes, transposes 4x4 byte blocks in registers (and for int16 separates the
 // limb planes), parks the per-column dwords in LDS, and the workgroup writes
 // each column's k run out contiguously. For int16 the per-column limb sums of
-// the slice go to corr_part[y][col].
+// the slice are added into corrB[col] (zeroed by pack_a_i16, which runs first).
 template <int ES, bool VEC>
 __global__ void __launch_bounds__(256)
 pack_b(const void *__restrict__ Bv, int64_t ldb, int k, int n, int k_pad, int kspan, int n_pad,
-       int8_t *__restrict__ Bp0, int8_t *__restrict__ Bp1, uint32_t *__restrict__ corr_part) {
+       int8_t *__restrict__ Bp0, int8_t *__restrict__ Bp1, uint32_t *__restrict__ corrB) {
     constexpr int P = ES;                 // output planes
     constexpr int CC = ES == 2 ? 8 : 4;   // 16-byte column chunks per workgroup (64 columns)
     constexpr int RG = 256 / CC;          // row groups of 4 rows
@@ -175,7 +179,7 @@ pack_b(const void *__restrict__ Bv, int64_t ldb, int k, int n, int k_pad, int ks
 #pragma unroll
         for (int c = 0; c < 8; ++c) atomicAdd(&cs[cc * 8 + c], (int)(32768u * (u32)shh[c] + 128u * (u32)sll[c]));
         __syncthreads();
-        if (tid < 64) corr_part[(int64_t)blockIdx.y * n_pad + j0 + tid] = (u32)cs[tid];
+        if (tid < 64) atomicAdd(&corrB[j0 + tid], (u32)cs[tid]);
     }
 }
 
@@ -186,8 +190,8 @@ template <int ES, int BM, int BN, int WM, int WN>
 __global__ void __launch_bounds__(256, 1)
 igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
              const int8_t *__restrict__ Bp, int64_t ldb_p, int64_t b_plane,
-             const uint32_t *__restrict__ corrA, const uint32_t *__restrict__ corr_part,
-             int corr_splits, int n_pad, uint32_t kconst, int32_t *__restrict__ C, int64_t ldc,
+             const uint32_t *__restrict__ corrA, const uint32_t *__restrict__ corrB,
+             uint32_t kconst, int32_t *__restrict__ C, int64_t ldc,
              int m, int n, int ktiles, int tiles_m, int tiles_n) {
     constexpr int MF = 32;
     typedef Mfma<MF> M;
@@ -317,68 +321,77 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
         }
     };
 
-    // Wait until at most DPW DMA instructions of this wave are outstanding
-    // (the newest k-tile), then synchronise the workgroup. Encoding of
-    // s_waitcnt: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] << 14.
+    // End of a k-step: wait until at most DPW DMA instructions of this wave
+    // are outstanding (the newest k-tile), or none in the last steps, which
+    // start no DMA, then synchronise the workgroup. Encoding of s_waitcnt:
+    // vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] << 14.
     constexpr int WAIT_NEWEST =
         (DPW & 0xf) | (0x7 << 4) | (0xf << 8) | (((DPW >> 4) & 3) << 14);
-    auto sync_stage = [&]() {
-        __builtin_amdgcn_s_waitcnt(WAIT_NEWEST);
-        __builtin_amdgcn_s_barrier();
-    };
+    constexpr int WAIT_ALL = (0x7 << 4) | (0xf << 8);
 
     constexpr int NM = TM * TN * (ES == 2 ? 4 : 1);
     constexpr int NR = P * (TM + TN);
     // Step kt (S = kt mod 4): stages S and S+1 hold tiles kt and kt+1, stage
     // S+2 is receiving tile kt+2, slot 0 holds sub-step 0 of tile kt. Start the
-    // DMA of tile kt+3 (clamped to the last tile; a clamped copy is never
-    // read), run both sub-steps while reading the next fragments, then wait for
-    // tile kt+2 and synchronise.
+    // DMA of tile kt+3 (if there is one), run both sub-steps while reading the
+    // next fragments, then wait for tile kt+2 and synchronise. The last three
+    // steps start no DMA and the last one prefetches nothing, so no copy is in
+    // flight when the epilogue starts (the compiler then tracks the C loads'
+    // completion precisely instead of waiting for every load before a store).
     // Each sub-step opens with an MFMA, and its fragment reads follow MFMAs:
     // the compiler cannot tell the DMA loads' LDS writes apart from other LDS
     // traffic, so any wait for a fragment is a full lgkmcnt(0), and this
     // order makes that wait cover only reads issued a sub-step earlier.
-    auto step = [&](auto s, int kt) {
+    auto step = [&](auto s, int kt, auto do_dma, auto do_pref) {
         constexpr int S = decltype(s)::value;
-        dma(ic<(S + 3) & 3>{}, min(kt + 3, ktiles - 1));
+        constexpr bool DMA = decltype(do_dma)::value != 0;
+        constexpr bool PREF = decltype(do_pref)::value != 0;
+        if constexpr (DMA) dma(ic<(S + 3) & 3>{}, kt + 3);
         read_frags(ic<1>{}, ic<S>{}, ic<1>{});
         mfmas(ic<0>{});
 #pragma unroll
         for (int i = 0; i < NM; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             if (i < NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            if (i < DPW) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            if (DMA && i < DPW) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
         }
         __builtin_amdgcn_sched_barrier(0);
-        read_frags(ic<0>{}, ic<(S + 1) & 3>{}, ic<0>{});
+        if constexpr (PREF) read_frags(ic<0>{}, ic<(S + 1) & 3>{}, ic<0>{});
         mfmas(ic<1>{});
 #pragma unroll
         for (int i = 0; i < NM; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            if (i < NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            if (PREF && i < NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         }
         __builtin_amdgcn_sched_barrier(0);
-        sync_stage();
+        if constexpr (PREF) {
+            __builtin_amdgcn_s_waitcnt(DMA ? WAIT_NEWEST : WAIT_ALL);
+            __builtin_amdgcn_s_barrier();
+        }
     };
 
+    // ktiles is a multiple of 4 and at least 4.
     dma(ic<0>{}, 0);
-    dma(ic<1>{}, min(1, ktiles - 1));
-    dma(ic<2>{}, min(2, ktiles - 1));
+    dma(ic<1>{}, 1);
+    dma(ic<2>{}, 2);
     // tiles 0 and 1 complete (tile 2 may be outstanding)
-    sync_stage();
+    __builtin_amdgcn_s_waitcnt(WAIT_NEWEST);
+    __builtin_amdgcn_s_barrier();
     read_frags(ic<0>{}, ic<0>{}, ic<0>{});
-    for (int kt = 0; kt < ktiles; kt += 4) {
-        step(ic<0>{}, kt);
-        step(ic<1>{}, kt + 1);
-        step(ic<2>{}, kt + 2);
-        step(ic<3>{}, kt + 3);
+    int kt = 0;
+    for (; kt < ktiles - 4; kt += 4) {
+        step(ic<0>{}, kt, ic<1>{}, ic<1>{});
+        step(ic<1>{}, kt + 1, ic<1>{}, ic<1>{});
+        step(ic<2>{}, kt + 2, ic<1>{}, ic<1>{});
+        step(ic<3>{}, kt + 3, ic<1>{}, ic<1>{});
     }
-    // Drain the clamped copies before the workgroup's LDS is released.
-    __builtin_amdgcn_s_waitcnt(0);
-
+    step(ic<0>{}, kt, ic<1>{}, ic<1>{});
+    step(ic<1>{}, kt + 1, ic<0>{}, ic<1>{});
+    step(ic<2>{}, kt + 2, ic<0>{}, ic<1>{});
+    step(ic<3>{}, kt + 3, ic<0>{}, ic<0>{});
     // ---- epilogue -----------------------------------------------------------
-    // int16 corrections first (small, cache-resident): the column term per
-    // output column and the row term per output row of this lane.
+    // int16 corrections (first k chunk only): the column term of each output
+    // column and the row term of each output row of this lane.
     u32 colt[TN], rowt[TM][M::REGS];
 #pragma unroll
     for (int j = 0; j < TN; ++j) colt[j] = 0;
@@ -387,14 +400,10 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
 #pragma unroll
         for (int r = 0; r < M::REGS; ++r) rowt[i][r] = 0;
     if constexpr (ES == 2) {
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int gc = n0 + wn0 + MF * j + M::out_col(lane);
-            u32 t = kconst;
-            for (int z = 0; z < corr_splits; ++z) t += corr_part[(int64_t)z * n_pad + gc];
-            colt[j] = t;
-        }
         if (corrA != nullptr) {
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                colt[j] = kconst + corrB[n0 + wn0 + MF * j + M::out_col(lane)];
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -402,34 +411,48 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
                     rowt[i][r] = corrA[m0 + wm0 + MF * i + M::out_row(lane, r)];
         }
     }
-    // C addresses: a wave-uniform tile base plus 32-bit lane offsets (the
-    // planner keeps bm * ldc * 4 below 2^31).
-    char *Ctile = (char *)(C + (int64_t)m0 * ldc + n0);
+    // C is accessed through a buffer resource based at the tile's corner,
+    // with 32-bit byte offsets (the planner keeps bm * ldc * 4 below 2^31).
+    // Elements outside m x n get an offset beyond the resource's range: the
+    // hardware returns 0 for such loads and drops such stores, so the
+    // epilogue has no branches and the compiler can count the outstanding
+    // loads exactly (with a branch per element it waits for all of them
+    // before every store).
+    const __amdgpu_buffer_rsrc_t Crs =
+        __builtin_amdgcn_make_buffer_rsrc(C + (int64_t)m0 * ldc + n0, 0, 0x7fffffff, 0x00020000);
     const int ldc32 = (int)ldc;
-    // C is read, added to and written back in batches of NB output blocks:
-    // every load of a batch is issued before the first add, so a wave keeps
-    // NB * REGS loads in flight instead of waiting out one round trip per
-    // block (all workgroups of a round reach this point together).
+    auto c_off = [&](int lr, int lc) -> u32 {
+        return (m0 + lr < m && n0 + lc < n) ? (u32)(lr * ldc32 + lc) * 4u : 0x80000000u;
+    };
+    // C is read, added to and written back in batches of NB output blocks,
+    // software-pipelined: the loads of batch b+1 are issued before batch b is
+    // added and stored, so a wave keeps up to 2 * NB * REGS loads in flight.
+    // (All workgroups of a round reach this point together; one round trip
+    // per block would leave the matrix cores idle for many microseconds.)
     constexpr int NOUT = TM * TN;
-    constexpr int NB = NOUT < 4 ? NOUT : 4;
-#pragma unroll
-    for (int b0 = 0; b0 < NOUT; b0 += NB) {
-        int32_t cv[NB][M::REGS];
+    constexpr int NB = NOUT <= 4 ? NOUT : 2;  // 2 x 2 x 16 C values in flight keeps
+                                              // the 256x256 kernel out of scratch
+    constexpr int NBATCH = NOUT / NB;
+    static_assert(NOUT % NB == 0 && NBATCH <= 8, "epilogue batches");
+    int32_t cv[2][NB][M::REGS];
+    auto load_batch = [&](auto buf, auto batch) {
+        constexpr int BF = decltype(buf)::value, B0 = decltype(batch)::value * NB;
 #pragma unroll
         for (int bb = 0; bb < NB; ++bb) {
-            const int i = (b0 + bb) / TN, j = (b0 + bb) % TN;
+            const int i = (B0 + bb) / TN, j = (B0 + bb) % TN;
             const int lc = wn0 + MF * j + M::out_col(lane);
 #pragma unroll
             for (int r = 0; r < M::REGS; ++r) {
                 const int lr = wm0 + MF * i + M::out_row(lane, r);
-                cv[bb][r] = (m0 + lr < m && n0 + lc < n)
-                                ? *(const int32_t *)(Ctile + (u32)(lr * ldc32 + lc) * 4u)
-                                : 0;
+                cv[BF][bb][r] = __builtin_amdgcn_raw_buffer_load_b32(Crs, c_off(lr, lc), 0, 0);
             }
         }
+    };
+    auto finish_batch = [&](auto buf, auto batch) {
+        constexpr int BF = decltype(buf)::value, B0 = decltype(batch)::value * NB;
 #pragma unroll
         for (int bb = 0; bb < NB; ++bb) {
-            const int i = (b0 + bb) / TN, j = (b0 + bb) % TN;
+            const int i = (B0 + bb) / TN, j = (B0 + bb) % TN;
             const int lc = wn0 + MF * j + M::out_col(lane);
 #pragma unroll
             for (int r = 0; r < M::REGS; ++r) {
@@ -441,12 +464,26 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
                     v = 65536u * (u32)acc[0][i][j][r] + 256u * (u32)acc[1][i][j][r] +
                         (u32)acc[2][i][j][r] + colt[j] + rowt[i][r];
                 }
-                if (m0 + lr < m && n0 + lc < n)
-                    *(int32_t *)(Ctile + (u32)(lr * ldc32 + lc) * 4u) = (int32_t)((u32)cv[bb][r] + v);
+                __builtin_amdgcn_raw_buffer_store_b32((int)((u32)cv[BF][bb][r] + v), Crs,
+                                                      c_off(lr, lc), 0, 0);
             }
         }
+    };
+    load_batch(ic<0>{}, ic<0>{});
+    auto epi_step = [&](auto batch) {
+        constexpr int BT = decltype(batch)::value;
+        if constexpr (BT + 1 < NBATCH) load_batch(ic<(BT + 1) & 1>{}, ic<BT + 1>{});
+        finish_batch(ic<BT & 1>{}, ic<BT>{});
         __builtin_amdgcn_sched_barrier(0);
-    }
+    };
+    epi_step(ic<0>{});
+    if constexpr (NBATCH > 1) epi_step(ic<1>{});
+    if constexpr (NBATCH > 2) epi_step(ic<2>{});
+    if constexpr (NBATCH > 3) epi_step(ic<3>{});
+    if constexpr (NBATCH > 4) epi_step(ic<4>{});
+    if constexpr (NBATCH > 5) epi_step(ic<5>{});
+    if constexpr (NBATCH > 6) epi_step(ic<6>{});
+    if constexpr (NBATCH > 7) epi_step(ic<7>{});
 }
 
 }  // namespace packed
@@ -475,9 +512,11 @@ int launch_pack(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, co
             int8_t *Al = Apk + a_plane;
             const int16_t *A16 = (const int16_t *)A;
             if (va)
-                pack_a_i16<true><<<g, 256, 0, stream>>>(A16, lda, mi, ki, kp, Apk, Al, corrA);
+                pack_a_i16<true><<<g, 256, 0, stream>>>(A16, lda, mi, ki, kp, Apk, Al, corrA,
+                                                        corrB, np);
             else
-                pack_a_i16<false><<<g, 256, 0, stream>>>(A16, lda, mi, ki, kp, Apk, Al, corrA);
+                pack_a_i16<false><<<g, 256, 0, stream>>>(A16, lda, mi, ki, kp, Apk, Al, corrA,
+                                                         corrB, np);
         } else {
             const int8_t *A8 = (const int8_t *)A;
             if (va)
@@ -510,7 +549,7 @@ int launch_multiply(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k
     PackedLayout L;
     packed_layout(es, m, n, k, p.kernel, A, lda, &L);
     const int8_t *ws = (const int8_t *)workspace;
-    const int mi = (int)m, ni = (int)n, np = (int)L.n_pad;
+    const int mi = (int)m, ni = (int)n;
     const int8_t *Apk = ws + L.off_a, *Bpk = ws + L.off_b;
     const uint32_t *corrA = (const uint32_t *)(ws + L.off_corr_a);
     const uint32_t *corrB = (const uint32_t *)(ws + L.off_corr_b);
@@ -529,12 +568,11 @@ int launch_multiply(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k
         if (es == 2)
             igemm_packed<2, 128, 128, 64, 64><<<grid, 256, 0, stream>>>(
                 Asrc + k0, lda_p, a_plane, Bpk + k0, L.k_pad, b_plane, first ? corrA : nullptr,
-                corrB, first ? L.b_slices : 0, np, first ? 16384u * (uint32_t)k : 0u, C, ldc, mi,
-                ni, ktiles, tm, tn);
+                corrB, first ? 16384u * (uint32_t)k : 0u, C, ldc, mi, ni, ktiles, tm, tn);
         else
             igemm_packed<1, 256, 256, 128, 128><<<grid, 256, 0, stream>>>(
-                Asrc + k0, lda_p, 0, Bpk + k0, L.k_pad, 0, nullptr, nullptr, 0, np, 0u, C, ldc,
-                mi, ni, ktiles, tm, tn);
+                Asrc + k0, lda_p, 0, Bpk + k0, L.k_pad, 0, nullptr, nullptr, 0u, C, ldc, mi, ni,
+                ktiles, tm, tn);
         if (hipGetLastError() != hipSuccess) return IGEMM_EHIP;
     }
     return IGEMM_OK;

@@ -97,7 +97,7 @@ void packed_layout(int es, int64_t m, int64_t n, int64_t k, int kernel, const vo
     L->off_corr_a = off;
     if (es == 2) off = align256(off + 4 * L->m_pad);
     L->off_corr_b = off;
-    if (es == 2) off = align256(off + 4 * (int64_t)L->b_slices * L->n_pad);
+    if (es == 2) off = align256(off + 4 * L->n_pad);
     L->bytes = off;
 }
 
