@@ -253,6 +253,17 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
         else
             src[d] = Bp + plane * b_plane + (int64_t)(n0 + row_in_blocks) * ldb_p + 16 * q;
     }
+    // Half of a k-tile's DMA blocks; the main loop issues one half per
+    // sub-step, one instruction every few MFMAs, so that the four waves do
+    // not stall together behind a full address queue.
+    auto dmah = [&](auto s, int kt, auto half) {
+        constexpr int H = decltype(half)::value;
+        char *dst = stage(s) + wave * DPW * 1024;
+        const int64_t koff = (int64_t)kt * 64;
+#pragma unroll
+        for (int d = H * DPW / 2; d < (H + 1) * DPW / 2; ++d)
+            dma16(src[d] + koff, (lds_void *)(dst + d * 1024));
+    };
     auto dma = [&](auto s, int kt) {
         char *dst = stage(s) + wave * DPW * 1024;
         const int64_t koff = (int64_t)kt * 64;
@@ -346,22 +357,24 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
         constexpr int S = decltype(s)::value;
         constexpr bool DMA = decltype(do_dma)::value != 0;
         constexpr bool PREF = decltype(do_pref)::value != 0;
-        if constexpr (DMA) dma(ic<(S + 3) & 3>{}, kt + 3);
+        if constexpr (DMA) dmah(ic<(S + 3) & 3>{}, kt + 3, ic<0>{});
         read_frags(ic<1>{}, ic<S>{}, ic<1>{});
         mfmas(ic<0>{});
 #pragma unroll
         for (int i = 0; i < NM; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             if (i < NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            if (DMA && i < DPW) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            if (DMA && (i % (2 * NM / DPW)) == 0) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
         }
         __builtin_amdgcn_sched_barrier(0);
+        if constexpr (DMA) dmah(ic<(S + 3) & 3>{}, kt + 3, ic<1>{});
         if constexpr (PREF) read_frags(ic<0>{}, ic<(S + 1) & 3>{}, ic<0>{});
         mfmas(ic<1>{});
 #pragma unroll
         for (int i = 0; i < NM; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             if (PREF && i < NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            if (DMA && (i % (2 * NM / DPW)) == 0) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
         }
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (PREF) {
