@@ -151,8 +151,12 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
         b_rbase[ks] = (wn0 + fr) * 64 + cq;
     }
 
-    v4i ra[2][ACT];
-    v4i rb[2][BUT][4];
+    // Register sets for staged k-tiles: two for the pipeline; the short path
+    // (a k range of at most NST tiles) loads every tile at once.
+    constexpr bool SHORT = BM * BN <= 32 * 256;
+    constexpr int NPAR = SHORT ? NST : 2;
+    v4i ra[NPAR][ACT];
+    v4i rb[NPAR][BUT][4];
     int sah[ACT], sal[ACT];
     int sbh[BUT][8], sbl[BUT][8];
 #pragma unroll
@@ -186,7 +190,7 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     const int8_t *a_tile0 = A8 + (int64_t)m0 * lda * ES;
     const int8_t *b_tile0 = B8 + (int64_t)n0 * ES;
 
-    auto load_fast = [&](auto par, int k0) {
+    auto load_fast = [&](auto par, int k0) __attribute__((always_inline)) {
         constexpr int R = decltype(par)::value;
         const int8_t *ab = a_tile0 + (int64_t)k0 * ES;
 #pragma unroll
@@ -200,7 +204,7 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     };
 
     // ---- global -> registers, any tile: per-element bounds -------------------
-    auto load_safe = [&](auto par, int k0) {
+    auto load_safe = [&](auto par, int k0) __attribute__((always_inline)) {
         constexpr int R = decltype(par)::value;
         const int klen = kend - k0;
 #pragma unroll
@@ -227,7 +231,7 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
 
     // ---- registers -> LDS (limb split, B transpose, limb sums) --------------
     // MASK: zero the limbs of elements at or beyond kend (last k-tile only).
-    auto store_tile = [&](auto par, auto buf, auto mask, int k0) {
+    auto store_tile = [&](auto par, auto buf, auto mask, int k0) __attribute__((always_inline)) {
         constexpr int R = decltype(par)::value;
         constexpr int BUF = decltype(buf)::value;
         constexpr bool MASK = decltype(mask)::value != 0;
@@ -294,7 +298,7 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     // Two fragment slots: the MFMAs of one sub-step run on one slot while the
     // next sub-step's fragments load into the other.
     v4i fa[2][P][TM], fb[2][P][TN];
-    auto read_frags = [&](auto slot, auto buf, auto ks) {
+    auto read_frags = [&](auto slot, auto buf, auto ks) __attribute__((always_inline)) {
         constexpr int SL = decltype(slot)::value;
         constexpr int BUF = decltype(buf)::value;
         constexpr int KS = decltype(ks)::value;
@@ -310,7 +314,7 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
                 fa[SL][p][i] = *(const v4i *)(As + p * APL + a_rbase[KS] + i * MF * 64);
         }
     };
-    auto mfmas = [&](auto slot) {
+    auto mfmas = [&](auto slot) __attribute__((always_inline)) {
         constexpr int SL = decltype(slot)::value;
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
@@ -343,7 +347,7 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     // tile kt while reading the next sub-step's fragments (the last one from
     // stage S+1, already complete), writes tile kt+2 into stage S+2, and ends
     // with one barrier.
-    auto step = [&](auto phase, auto do_load, auto do_store, auto do_pref, int kt) {
+    auto step = [&](auto phase, auto do_load, auto do_store, auto do_pref, int kt) __attribute__((always_inline)) {
         constexpr int S = decltype(phase)::value;
         if constexpr (M::KSTEPS == 2) {
             constexpr int NM = TM * TN * (ES == 2 ? 4 : 1);  // MFMAs per sub-step
@@ -382,7 +386,7 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     };
 
     // One unpipelined k-tile through LDS stage 0 with bounds checks.
-    auto safe_tile = [&](int k0) {
+    auto safe_tile = [&](int k0) __attribute__((always_inline)) {
         load_safe(ic<0>{}, k0);
         if (k0 + 64 > kend)
             store_tile(ic<0>{}, ic<0>{}, ic<1>{}, k0);
@@ -397,6 +401,222 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
         }
         __syncthreads();
     };
+
+    // ---- epilogue (C += result), as a function of where C comes from ----------
+    // cpre: C values loaded before the k loop (short path), or none.
+    int32_t cpre[SHORT ? TM : 1][SHORT ? TN : 1][SHORT ? M::REGS : 1];
+    auto epilogue = [&](auto pre) __attribute__((always_inline)) {
+        constexpr bool PRE = decltype(pre)::value != 0;
+        int *sRH = (int *)smem;
+        int *sRL = sRH + BM;
+        int *sKH = sRL + BM;
+        int *sKL = sKH + BN;
+        if constexpr (ES == 2) {
+            for (int i = tid; i < 2 * (BM + BN); i += 256) sRH[i] = 0;
+            __syncthreads();
+#pragma unroll
+            for (int s = 0; s < ACT; ++s) {
+                if (!a_dup[s]) {
+                    atomicAdd(&sRH[a_row[s]], sah[s]);
+                    atomicAdd(&sRL[a_row[s]], sal[s]);
+                }
+            }
+#pragma unroll
+            for (int s = 0; s < BUT; ++s) {
+                if (!b_dup[s]) {
+#pragma unroll
+                    for (int c = 0; c < 8; ++c) {
+                        atomicAdd(&sKH[b_cc[s] * 8 + c], sbh[s][c]);
+                        atomicAdd(&sKL[b_cc[s] * 8 + c], sbl[s][c]);
+                    }
+                }
+            }
+            __syncthreads();
+        }
+        const u32 kconst = 16384u * (u32)(kend - kbeg);
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int lc = wn0 + MF * j + M::out_col(lane);
+                const int gc = n0 + lc;
+                u32 colterm = 0;
+                if constexpr (ES == 2)
+                    colterm = 32768u * (u32)sKH[lc] + 128u * (u32)sKL[lc] + kconst;
+#pragma unroll
+                for (int r = 0; r < M::REGS; ++r) {
+                    const int lr = wm0 + MF * i + M::out_row(lane, r);
+                    const int gr = m0 + lr;
+                    u32 v;
+                    if constexpr (ES == 1) {
+                        v = (u32)acc[0][i][j][r];
+                    } else {
+                        v = 65536u * (u32)acc[0][i][j][r] + 256u * (u32)acc[1][i][j][r] +
+                            (u32)acc[2][i][j][r] + 32768u * (u32)sRH[lr] + 128u * (u32)sRL[lr] +
+                            colterm;
+                    }
+                    if (gr < m && gc < n) {
+                        int32_t *cp = C + (int64_t)gr * ldc + gc;
+                        if constexpr (SPLIT)
+                            atomicAdd(cp, (int)v);
+                        else if constexpr (PRE)
+                            *cp = (int32_t)((u32)cpre[i][j][r] + v);
+                        else
+                            *cp = (int32_t)((u32)*cp + v);
+                    }
+                }
+            }
+            // Keep the scheduler from hoisting every C load of the tile at once.
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+
+    // ---- short path: a k range of at most NST k-tiles -------------------------
+    // Small products (skinny, convolution-shaped, small cubes) give each
+    // workgroup only a few k-tiles, too few to fill a pipeline: one global
+    // round trip per tile would dominate. Here every tile of the range is
+    // loaded at once with branch-free range-checked loads (a branch per load
+    // would make the compiler wait for each load before issuing the next), C
+    // is fetched at the same time (addresses clamped into the matrix), and
+    // one barrier precedes all the MFMAs.
+    if constexpr (SHORT) {
+        const int nkt = (kend - kbeg + 63) >> 6;
+        // Buffer resources at the corner of this workgroup's A rows and B
+        // columns (from kbeg), with 32-bit lane offsets (an element offset
+        // past the range also reads zero, so element loads of misaligned
+        // rows follow the same rule). Rows of A beyond m,
+        // k-tiles beyond kend and rows of B beyond kend get an offset past the
+        // resource's range, which the hardware returns as zero (per dword), so
+        // the loads need no branches; the range ends at the matrix's last byte
+        // (rounded up to a dword), so no load reaches past the allocation.
+        const int64_t a_span = (int64_t)BM * lda * ES + 256 * ES;
+        const int64_t b_span = (int64_t)256 * ldb * ES + BN * ES;
+        if (nkt <= NST && a_span < 0x7ffffff0 && b_span < 0x7ffffff0) {
+            const char *a_base = (const char *)Ap + ((int64_t)m0 * lda + kbeg) * ES;
+            const char *b_base = (const char *)Bp + ((int64_t)kbeg * ldb + n0) * ES;
+            const int64_t a_ext = ((int64_t)(m - 1 - m0) * lda + (k - kbeg)) * ES;
+            const int64_t b_ext = ((int64_t)(k - 1 - kbeg) * ldb + (n - n0)) * ES;
+            const int a_rec = (int)min((a_ext + 3) & ~(int64_t)3, (int64_t)0x7ffffff0);
+            const int b_rec = (int)min((b_ext + 3) & ~(int64_t)3, (int64_t)0x7ffffff0);
+            const __amdgpu_buffer_rsrc_t Ars =
+                __builtin_amdgcn_make_buffer_rsrc((void *)a_base, 0, a_rec, 0x00020000);
+            const __amdgpu_buffer_rsrc_t Brs =
+                __builtin_amdgcn_make_buffer_rsrc((void *)b_base, 0, b_rec, 0x00020000);
+            const int klen = kend - kbeg;
+            const int lda_b = (int)(lda * ES), ldb_b = (int)(ldb * ES);
+            // 16 bytes at byte offset `off` of a resource: one vector load when
+            // rows are 16-byte aligned (VEC), else one load per element (rows
+            // of any alignment), every load unconditional.
+            auto load16_rs = [&](auto vec, __amdgpu_buffer_rsrc_t rs, u32 off)
+                                 __attribute__((always_inline)) -> v4i {
+                if constexpr (decltype(vec)::value != 0) {
+                    return __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
+                } else {
+                    u32 w[4];
+#pragma unroll
+                    for (int d = 0; d < 4; ++d) {
+                        if constexpr (ES == 2) {
+                            const u32 lo = __builtin_amdgcn_raw_buffer_load_b16(rs, off + 4 * d, 0, 0);
+                            const u32 hi =
+                                __builtin_amdgcn_raw_buffer_load_b16(rs, off + 4 * d + 2, 0, 0);
+                            w[d] = lo | (hi << 16);
+                        } else {
+                            u32 x = 0;
+#pragma unroll
+                            for (int b = 0; b < 4; ++b)
+                                x |= (u32)__builtin_amdgcn_raw_buffer_load_b8(rs, off + 4 * d + b,
+                                                                             0, 0)
+                                     << (8 * b);
+                            w[d] = x;
+                        }
+                    }
+                    v4i v;
+                    v.x = (int)w[0];
+                    v.y = (int)w[1];
+                    v.z = (int)w[2];
+                    v.w = (int)w[3];
+                    return v;
+                }
+            };
+            // k-tile t of the range into register set R
+            auto load_short = [&](auto par, auto tile) __attribute__((always_inline)) {
+                constexpr int R = decltype(par)::value, T = decltype(tile)::value;
+#pragma unroll
+                for (int s = 0; s < ACT; ++s) {
+                    const int e = T * 64 + a_q[s] * (16 / ES);  // first element, from kbeg
+                    const int valid = klen - e;                 // elements before kend
+                    const u32 off = (m0 + a_row[s] < m && valid > 0)
+                                        ? (u32)(a_row[s] * lda_b + e * ES)
+                                        : 0x80000000u;
+                    ra[R][s] = load16_rs(ic<VA>{}, Ars, off);
+                }
+#pragma unroll
+                for (int s = 0; s < BUT; ++s) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int p = T * 64 + 4 * b_rg[s] + r;  // row of B, from kbeg
+                        const u32 off = p < klen ? (u32)(p * ldb_b + b_cc[s] * CPU * ES)
+                                                 : 0x80000000u;
+                        rb[R][s][r] = load16_rs(ic<VB>{}, Brs, off);
+                    }
+                }
+            };
+            if constexpr (!SPLIT) {
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j) {
+                        const int gc = min(n0 + wn0 + MF * j + M::out_col(lane), n - 1);
+#pragma unroll
+                        for (int r = 0; r < M::REGS; ++r) {
+                            const int gr = min(m0 + wm0 + MF * i + M::out_row(lane, r), m - 1);
+                            cpre[i][j][r] = C[(int64_t)gr * ldc + gc];
+                        }
+                    }
+            }
+            load_short(ic<0>{}, ic<0>{});
+            load_short(ic<1>{}, ic<1>{});
+            load_short(ic<2>{}, ic<2>{});
+            load_short(ic<3>{}, ic<3>{});
+            __builtin_amdgcn_sched_barrier(0);  // every load goes out before the first wait
+            // Elements of A at or beyond kend (the next k slice) count as zero.
+            auto mask_short = [&](auto par, auto tile) __attribute__((always_inline)) {
+                constexpr int R = decltype(par)::value, T = decltype(tile)::value;
+#pragma unroll
+                for (int s = 0; s < ACT; ++s) {
+                    const int vb = (klen - (T * 64 + a_q[s] * (16 / ES))) * ES;
+                    ra[R][s].x &= (int)byte_mask(vb);
+                    ra[R][s].y &= (int)byte_mask(vb - 4);
+                    ra[R][s].z &= (int)byte_mask(vb - 8);
+                    ra[R][s].w &= (int)byte_mask(vb - 12);
+                }
+            };
+            mask_short(ic<0>{}, ic<0>{});
+            mask_short(ic<1>{}, ic<1>{});
+            mask_short(ic<2>{}, ic<2>{});
+            mask_short(ic<3>{}, ic<3>{});
+            store_tile(ic<0>{}, ic<0>{}, ic<1>{}, kbeg);
+            store_tile(ic<1>{}, ic<1>{}, ic<1>{}, kbeg + 64);
+            store_tile(ic<2>{}, ic<2>{}, ic<1>{}, kbeg + 128);
+            store_tile(ic<3>{}, ic<3>{}, ic<1>{}, kbeg + 192);
+            __syncthreads();
+            auto tile_mfmas = [&](auto buf) __attribute__((always_inline)) {
+                read_frags(ic<0>{}, buf, ic<0>{});
+                mfmas(ic<0>{});
+                if constexpr (M::KSTEPS == 2) {
+                    read_frags(ic<1>{}, buf, ic<1>{});
+                    mfmas(ic<1>{});
+                }
+            };
+            tile_mfmas(ic<0>{});
+            if (nkt > 1) tile_mfmas(ic<1>{});
+            if (nkt > 2) tile_mfmas(ic<2>{});
+            if (nkt > 3) tile_mfmas(ic<3>{});
+            __syncthreads();  // the epilogue reuses stage 0 for the limb sums
+            epilogue(ic<1>{});
+            return;
+        }
+    }
 
     // ---- main loop ------------------------------------------------------------
     // Interior workgroups run a multiple of four full k-tiles through the
@@ -438,66 +658,7 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     const int ktail = npipe > 0 ? klead + npipe * 64 : kbeg;
     for (int k0 = ktail; k0 < kend; k0 += 64) safe_tile(k0);
 
-    // ---- epilogue -------------------------------------------------------------
-    int *sRH = (int *)smem;
-    int *sRL = sRH + BM;
-    int *sKH = sRL + BM;
-    int *sKL = sKH + BN;
-    if constexpr (ES == 2) {
-        for (int i = tid; i < 2 * (BM + BN); i += 256) sRH[i] = 0;
-        __syncthreads();
-#pragma unroll
-        for (int s = 0; s < ACT; ++s) {
-            if (!a_dup[s]) {
-                atomicAdd(&sRH[a_row[s]], sah[s]);
-                atomicAdd(&sRL[a_row[s]], sal[s]);
-            }
-        }
-#pragma unroll
-        for (int s = 0; s < BUT; ++s) {
-            if (!b_dup[s]) {
-#pragma unroll
-                for (int c = 0; c < 8; ++c) {
-                    atomicAdd(&sKH[b_cc[s] * 8 + c], sbh[s][c]);
-                    atomicAdd(&sKL[b_cc[s] * 8 + c], sbl[s][c]);
-                }
-            }
-        }
-        __syncthreads();
-    }
-    const u32 kconst = 16384u * (u32)(kend - kbeg);
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int lc = wn0 + MF * j + M::out_col(lane);
-            const int gc = n0 + lc;
-            u32 colterm = 0;
-            if constexpr (ES == 2) colterm = 32768u * (u32)sKH[lc] + 128u * (u32)sKL[lc] + kconst;
-#pragma unroll
-            for (int r = 0; r < M::REGS; ++r) {
-                const int lr = wm0 + MF * i + M::out_row(lane, r);
-                const int gr = m0 + lr;
-                u32 v;
-                if constexpr (ES == 1) {
-                    v = (u32)acc[0][i][j][r];
-                } else {
-                    v = 65536u * (u32)acc[0][i][j][r] + 256u * (u32)acc[1][i][j][r] +
-                        (u32)acc[2][i][j][r] + 32768u * (u32)sRH[lr] + 128u * (u32)sRL[lr] +
-                        colterm;
-                }
-                if (gr < m && gc < n) {
-                    int32_t *cp = C + (int64_t)gr * ldc + gc;
-                    if (SPLIT)
-                        atomicAdd(cp, (int)v);
-                    else
-                        *cp = (int32_t)((u32)*cp + v);
-                }
-            }
-        }
-        // Keep the scheduler from hoisting every C load of the tile at once.
-        __builtin_amdgcn_sched_barrier(0);
-    }
+    epilogue(ic<0>{});
 }
 
 // ---------------------------------------------------------------------------

@@ -185,6 +185,24 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
         int64_t cap = ktiles / 2 > 1 ? ktiles / 2 : 1;
         if (s > cap) s = cap;
     }
+    // Small-tile kernels take a k range of at most four k-tiles in one go
+    // (all loads issued at once); prefer that when the grid stays modest.
+    const bool short_tiles = (int64_t)d.bm * d.bn <= 32 * 256;
+    // Four-tile ranges also beat shorter ones when they still give a
+    // workgroup per CU (fewer slices add into C).
+    if (split <= 0 && short_tiles && cdiv(ktiles, s) > 4 &&
+        tiles * cdiv(ktiles, 4) <= 4 * (int64_t)num_cu)
+        s = cdiv(ktiles, 4);
+    if (split <= 0 && short_tiles && cdiv(ktiles, s) < 4 &&
+        tiles * cdiv(ktiles, 4) >= (int64_t)num_cu)
+        s = cdiv(ktiles, 4);
+    // Every k slice adds its partial tile into C with atomics; their cost
+    // grows with m * n * slices (measured: past ~2^21 element updates it
+    // outweighs the extra parallelism).
+    if (split <= 0) {
+        const int64_t cap = ((int64_t)1 << 21) / (m * n);
+        if (s > cap) s = cap > 1 ? cap : 1;
+    }
     if (s < min_split) s = min_split;
     if (s > ktiles) s = ktiles;
     if (s < 1) s = 1;
