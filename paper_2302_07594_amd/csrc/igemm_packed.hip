@@ -185,8 +185,10 @@ pack_b(const void *__restrict__ Bv, int64_t ldb, int k, int n, int k_pad, int ks
 
 // ---- the packed-operand GEMM ---------------------------------------------
 // A planes: P x m_pad x k_pad (row stride lda_p, plane stride a_plane), B
-// planes: P x n_pad x k_pad. ktiles = k_pad / 64 is a multiple of 4.
-template <int ES, int BM, int BN, int WM, int WN>
+// planes: P x n_pad x k_pad. ktiles = k_pad / 64 is a multiple of 4. NST is
+// the number of LDS stages of the DMA ring (4, or 3 for tiles whose stage
+// is too large for four).
+template <int ES, int BM, int BN, int WM, int WN, int NST>
 __global__ void __launch_bounds__(256, 1)
 igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
              const int8_t *__restrict__ Bp, int64_t ldb_p, int64_t b_plane,
@@ -201,21 +203,26 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     constexpr int TM = WM / MF, TN = WN / MF;
     constexpr int WGN = BN / WN;
     static_assert((BM / WM) * WGN == 4, "four waves per workgroup");
+    static_assert(NST == 3 || NST == 4, "three or four LDS stages");
     constexpr int APL = BM * 64, BPL = BN * 64;
     constexpr int STAGE = P * (APL + BPL);
-    constexpr int NBLK = STAGE / 1024;  // 1 KB DMA blocks per stage
-    static_assert(NBLK % 4 == 0 && NBLK / 4 <= 16, "DMA blocks per wave");
-    constexpr int DPW = NBLK / 4;       // DMA instructions per wave per k-tile
-    constexpr int NBA = P * BM / 16;    // blocks holding A planes
+    static_assert(NST * STAGE <= 160 * 1024, "gfx950 LDS");
+    // 1 KB DMA blocks per stage: NBA hold the A planes, NBB the B planes;
+    // each wave moves DPA of the A blocks and DPB of the B blocks.
+    constexpr int NBA = P * BM / 16, NBB = P * BN / 16;
+    static_assert(NBA % 4 == 0 && NBB % 4 == 0, "DMA blocks per wave");
+    constexpr int DPA = NBA / 4, DPB = NBB / 4, DPW = DPA + DPB;
+    static_assert(DPW <= 15, "outstanding DMA count fits s_waitcnt");
 
-    // Four LDS stages as separate objects, so that the compiler can tell the
+    // The LDS stages as separate objects, so that the compiler can tell the
     // DMA writes of one stage from the fragment reads of another.
     __shared__ __attribute__((aligned(16))) char st0[STAGE];
     __shared__ __attribute__((aligned(16))) char st1[STAGE];
     __shared__ __attribute__((aligned(16))) char st2[STAGE];
-    __shared__ __attribute__((aligned(16))) char st3[STAGE];
+    __shared__ __attribute__((aligned(16))) char st3[NST == 4 ? STAGE : 16];
     auto stage = [&](auto s) -> char * {
         constexpr int S = decltype(s)::value;
+        static_assert(S < NST, "stage index");
         if constexpr (S == 0) return st0;
         else if constexpr (S == 1) return st1;
         else if constexpr (S == 2) return st2;
@@ -223,7 +230,7 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     };
 
     const int tid = threadIdx.x, lane = tid & 63;
-    // wave-uniform, so that DMA destinations (m0) are scalar arithmetic
+    // wave-uniform, so that DMA sources and destinations are scalar values
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm0 = (wave / WGN) * WM, wn0 = (wave % WGN) * WN;
 
@@ -238,38 +245,40 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     const int tn = (bid % span) / gsize;
     const int m0 = tm * BM, n0 = tn * BN;
 
-    // DMA sources: wave w moves blocks w*DPW .. w*DPW+DPW-1 of every stage.
-    // Lane i of a block writes LDS bytes [16i, 16i+16) of that block, i.e. row
-    // r0 + i/4, physical chunk i%4, which holds logical chunk (i%4) ^ swz(row).
+    // DMA: lane i of a 1 KB block writes LDS bytes [16i, 16i+16), i.e. row
+    // r0 + i/4 of the block, physical chunk i%4, which holds logical chunk
+    // (i%4) ^ swz(row); r0 is a multiple of 16, so swz(row) = swz(i/4). The
+    // source is a wave-uniform block base plus a per-lane 32-bit offset that
+    // is the same for every block of an operand (the planner keeps 16 rows
+    // of a plane below 2^32 bytes).
+    const u32 lrow = (u32)(lane >> 2);
+    const u32 lq = (u32)((lane & 3) ^ swz(lane >> 2));
+    const u32 a_loff = lrow * (u32)lda_p + 16u * lq;
+    const u32 b_loff = lrow * (u32)ldb_p + 16u * lq;
     const int8_t *src[DPW];
+    int ldsoff[DPW];
 #pragma unroll
     for (int d = 0; d < DPW; ++d) {
-        const int b = wave * DPW + d;
-        const int row_in_blocks = (b < NBA ? b % (BM / 16) : (b - NBA) % (BN / 16)) * 16 + (lane >> 2);
-        const int plane = b < NBA ? b / (BM / 16) : (b - NBA) / (BN / 16);
-        const int q = (lane & 3) ^ swz(row_in_blocks);
-        if (b < NBA)
-            src[d] = Ap + plane * a_plane + (int64_t)(m0 + row_in_blocks) * lda_p + 16 * q;
-        else
-            src[d] = Bp + plane * b_plane + (int64_t)(n0 + row_in_blocks) * ldb_p + 16 * q;
+        if (d < DPA) {
+            const int b = wave * DPA + d;
+            const int plane = b / (BM / 16), r0 = (b % (BM / 16)) * 16;
+            src[d] = Ap + plane * a_plane + (int64_t)(m0 + r0) * lda_p;
+            ldsoff[d] = b * 1024;
+        } else {
+            const int bb = wave * DPB + (d - DPA);
+            const int plane = bb / (BN / 16), r0 = (bb % (BN / 16)) * 16;
+            src[d] = Bp + plane * b_plane + (int64_t)(n0 + r0) * ldb_p;
+            ldsoff[d] = (NBA + bb) * 1024;
+        }
     }
-    // Half of a k-tile's DMA blocks; the main loop issues one half per
-    // sub-step, one instruction every few MFMAs, so that the four waves do
-    // not stall together behind a full address queue.
-    auto dmah = [&](auto s, int kt, auto half) {
-        constexpr int H = decltype(half)::value;
-        char *dst = stage(s) + wave * DPW * 1024;
+    // DMA blocks [D0, D1) of k-tile kt into stage s.
+    auto dma_range = [&](auto s, int kt, auto d0, auto d1) {
+        constexpr int D0 = decltype(d0)::value, D1 = decltype(d1)::value;
+        char *dst = stage(s);
         const int64_t koff = (int64_t)kt * 64;
 #pragma unroll
-        for (int d = H * DPW / 2; d < (H + 1) * DPW / 2; ++d)
-            dma16(src[d] + koff, (lds_void *)(dst + d * 1024));
-    };
-    auto dma = [&](auto s, int kt) {
-        char *dst = stage(s) + wave * DPW * 1024;
-        const int64_t koff = (int64_t)kt * 64;
-#pragma unroll
-        for (int d = 0; d < DPW; ++d)
-            dma16(src[d] + koff, (lds_void *)(dst + d * 1024));
+        for (int d = D0; d < D1; ++d)
+            dma16(src[d] + koff + (d < DPA ? a_loff : b_loff), (lds_void *)(dst + ldsoff[d]));
     };
 
     // Fragment reads (same LDS layout as the fused kernels).
@@ -332,76 +341,106 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
         }
     };
 
-    // End of a k-step: wait until at most DPW DMA instructions of this wave
-    // are outstanding (the newest k-tile), or none in the last steps, which
-    // start no DMA, then synchronise the workgroup. Encoding of s_waitcnt:
-    // vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] << 14.
-    constexpr int WAIT_NEWEST =
-        (DPW & 0xf) | (0x7 << 4) | (0xf << 8) | (((DPW >> 4) & 3) << 14);
+    // s_waitcnt encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] << 14.
+    constexpr int WAIT_NEWEST = (DPW & 0xf) | (0x7 << 4) | (0xf << 8);
     constexpr int WAIT_ALL = (0x7 << 4) | (0xf << 8);
 
-    constexpr int NM = TM * TN * (ES == 2 ? 4 : 1);
-    constexpr int NR = P * (TM + TN);
-    // Step kt (S = kt mod 4): stages S and S+1 hold tiles kt and kt+1, stage
-    // S+2 is receiving tile kt+2, slot 0 holds sub-step 0 of tile kt. Start the
-    // DMA of tile kt+3 (if there is one), run both sub-steps while reading the
-    // next fragments, then wait for tile kt+2 and synchronise. The last three
-    // steps start no DMA and the last one prefetches nothing, so no copy is in
-    // flight when the epilogue starts (the compiler then tracks the C loads'
-    // completion precisely instead of waiting for every load before a store).
-    // Each sub-step opens with an MFMA, and its fragment reads follow MFMAs:
-    // the compiler cannot tell the DMA loads' LDS writes apart from other LDS
-    // traffic, so any wait for a fragment is a full lgkmcnt(0), and this
-    // order makes that wait cover only reads issued a sub-step earlier.
+    constexpr int NM = TM * TN * (ES == 2 ? 4 : 1);  // MFMAs per sub-step
+    constexpr int NR = P * (TM + TN);                // fragment reads per sub-step
+    // DMA issue: with four stages the next tile's loads are spread over both
+    // sub-steps, with three (less slack) over the first sub-step only.
+    constexpr int D_SUB0 = NST == 4 ? DPW / 2 : DPW;
+    // Step kt (S = kt mod NST): stages S and S+1 hold tiles kt and kt+1, slot
+    // 0 holds sub-step 0 of tile kt. Start the DMA of tile kt+NST-1 (if there
+    // is one) into the stage that held tile kt-1, run both sub-steps while
+    // reading the next fragments, then wait until tile kt+2 has landed (with
+    // four stages tile kt+3 may stay in flight) and synchronise. The last
+    // steps start no DMA and the last one prefetches nothing, so no copy is
+    // in flight when the epilogue starts (the compiler then tracks the C
+    // loads' completion precisely instead of waiting for every load before a
+    // store). Each sub-step opens with an MFMA, and its fragment reads follow
+    // MFMAs: the compiler cannot tell the DMA loads' LDS writes apart from
+    // other LDS traffic, so any wait for a fragment is a full lgkmcnt(0), and
+    // this order makes that wait cover only reads issued a sub-step earlier.
     auto step = [&](auto s, int kt, auto do_dma, auto do_pref) {
         constexpr int S = decltype(s)::value;
+        constexpr int SD = (S + NST - 1) % NST;  // stage receiving the DMA
         constexpr bool DMA = decltype(do_dma)::value != 0;
         constexpr bool PREF = decltype(do_pref)::value != 0;
-        if constexpr (DMA) dmah(ic<(S + 3) & 3>{}, kt + 3, ic<0>{});
+        if constexpr (DMA) dma_range(ic<SD>{}, kt + NST - 1, ic<0>{}, ic<D_SUB0>{});
         read_frags(ic<1>{}, ic<S>{}, ic<1>{});
         mfmas(ic<0>{});
 #pragma unroll
         for (int i = 0; i < NM; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             if (i < NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            if (DMA && (i % (2 * NM / DPW)) == 0) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            if (DMA && (i * D_SUB0) / NM != ((i + 1) * D_SUB0) / NM)
+                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
         }
         __builtin_amdgcn_sched_barrier(0);
-        if constexpr (DMA) dmah(ic<(S + 3) & 3>{}, kt + 3, ic<1>{});
-        if constexpr (PREF) read_frags(ic<0>{}, ic<(S + 1) & 3>{}, ic<0>{});
+        if constexpr (DMA && D_SUB0 < DPW)
+            dma_range(ic<SD>{}, kt + NST - 1, ic<D_SUB0>{}, ic<DPW>{});
+        if constexpr (PREF) read_frags(ic<0>{}, ic<(S + 1) % NST>{}, ic<0>{});
         mfmas(ic<1>{});
 #pragma unroll
         for (int i = 0; i < NM; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             if (PREF && i < NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            if (DMA && (i % (2 * NM / DPW)) == 0) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            if (DMA && D_SUB0 < DPW &&
+                (i * (DPW - D_SUB0)) / NM != ((i + 1) * (DPW - D_SUB0)) / NM)
+                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
         }
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (PREF) {
-            __builtin_amdgcn_s_waitcnt(DMA ? WAIT_NEWEST : WAIT_ALL);
+            __builtin_amdgcn_s_waitcnt(DMA && NST == 4 ? WAIT_NEWEST : WAIT_ALL);
             __builtin_amdgcn_s_barrier();
         }
     };
+    // The last T steps from a stage-0 step at kt0: step j starts a DMA only if
+    // tile j+NST-1 exists and prefetches only if tile j+1 exists.
+    auto tail_step = [&](auto jc, auto tc, int kt0) {
+        constexpr int J = decltype(jc)::value, T = decltype(tc)::value;
+        if constexpr (J < T)
+            step(ic<J % NST>{}, kt0 + J, ic<(J + NST - 1 < T)>{}, ic<(J + 1 < T)>{});
+    };
+    auto tail = [&](auto tc, int kt0) {
+        tail_step(ic<0>{}, tc, kt0);
+        tail_step(ic<1>{}, tc, kt0);
+        tail_step(ic<2>{}, tc, kt0);
+        tail_step(ic<3>{}, tc, kt0);
+        tail_step(ic<4>{}, tc, kt0);
+        tail_step(ic<5>{}, tc, kt0);
+    };
 
-    // ktiles is a multiple of 4 and at least 4.
-    dma(ic<0>{}, 0);
-    dma(ic<1>{}, 1);
-    dma(ic<2>{}, 2);
-    // tiles 0 and 1 complete (tile 2 may be outstanding)
-    __builtin_amdgcn_s_waitcnt(WAIT_NEWEST);
+    // Prologue: tiles 0 .. NST-2 into stages 0 .. NST-2; tiles 0 and 1 must
+    // have landed (with four stages tile 2 may stay in flight).
+    dma_range(ic<0>{}, 0, ic<0>{}, ic<DPW>{});
+    dma_range(ic<1>{}, 1, ic<0>{}, ic<DPW>{});
+    if constexpr (NST == 4) dma_range(ic<2>{}, 2, ic<0>{}, ic<DPW>{});
+    __builtin_amdgcn_s_waitcnt(NST == 4 ? WAIT_NEWEST : WAIT_ALL);
     __builtin_amdgcn_s_barrier();
     read_frags(ic<0>{}, ic<0>{}, ic<0>{});
+    // Groups of NST steps in which every step starts a DMA and prefetches,
+    // then the remaining T = ktiles - kt steps (T in [NST-1, 2*NST-2]; ktiles
+    // is a multiple of 4 and at least 4).
     int kt = 0;
-    for (; kt < ktiles - 4; kt += 4) {
+    for (; kt <= ktiles - 2 * NST + 1; kt += NST) {
         step(ic<0>{}, kt, ic<1>{}, ic<1>{});
         step(ic<1>{}, kt + 1, ic<1>{}, ic<1>{});
         step(ic<2>{}, kt + 2, ic<1>{}, ic<1>{});
-        step(ic<3>{}, kt + 3, ic<1>{}, ic<1>{});
+        if constexpr (NST == 4) step(ic<3>{}, kt + 3, ic<1>{}, ic<1>{});
     }
-    step(ic<0>{}, kt, ic<1>{}, ic<1>{});
-    step(ic<1>{}, kt + 1, ic<0>{}, ic<1>{});
-    step(ic<2>{}, kt + 2, ic<0>{}, ic<1>{});
-    step(ic<3>{}, kt + 3, ic<0>{}, ic<0>{});
+    if constexpr (NST == 4) {
+        tail(ic<4>{}, kt);
+    } else {
+        const int T = ktiles - kt;
+        if (T == 2)
+            tail(ic<2>{}, kt);
+        else if (T == 3)
+            tail(ic<3>{}, kt);
+        else
+            tail(ic<4>{}, kt);
+    }
     // ---- epilogue -----------------------------------------------------------
     // int16 corrections (first k chunk only): the column term of each output
     // column and the row term of each output row of this lane.
@@ -578,12 +617,14 @@ int launch_multiply(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k
         const int64_t kc = L.k_pad - k0 < p.k_chunk ? L.k_pad - k0 : p.k_chunk;
         const int ktiles = (int)(kc / 64);
         const bool first = k0 == 0;
+        const uint32_t *cA = first ? corrA : nullptr;
+        const uint32_t kc16 = first ? 16384u * (uint32_t)k : 0u;
         if (es == 2)
-            igemm_packed<2, 128, 128, 64, 64><<<grid, 256, 0, stream>>>(
-                Asrc + k0, lda_p, a_plane, Bpk + k0, L.k_pad, b_plane, first ? corrA : nullptr,
-                corrB, first ? 16384u * (uint32_t)k : 0u, C, ldc, mi, ni, ktiles, tm, tn);
+            igemm_packed<2, 128, 128, 64, 64, 4><<<grid, 256, 0, stream>>>(
+                Asrc + k0, lda_p, a_plane, Bpk + k0, L.k_pad, b_plane, cA, corrB, kc16, C, ldc,
+                mi, ni, ktiles, tm, tn);
         else
-            igemm_packed<1, 256, 256, 128, 128><<<grid, 256, 0, stream>>>(
+            igemm_packed<1, 256, 256, 128, 128, 4><<<grid, 256, 0, stream>>>(
                 Asrc + k0, lda_p, 0, Bpk + k0, L.k_pad, 0, nullptr, nullptr, 0u, C, ldc, mi, ni,
                 ktiles, tm, tn);
         if (hipGetLastError() != hipSuccess) return IGEMM_EHIP;

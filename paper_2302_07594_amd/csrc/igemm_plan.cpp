@@ -114,10 +114,12 @@ static bool packed_fits(int id, int64_t ldc) {
     return (int64_t)kKernels[id].bm * ldc * 4 < INT_MAX;
 }
 
-static int auto_kernel(int es, int64_t m, int64_t n, int64_t k, int64_t ldc, int num_cu,
-                       bool allow_packed) {
+static int auto_kernel(int es, int64_t m, int64_t n, int64_t k, int64_t lda, int64_t ldc,
+                       int num_cu, bool allow_packed) {
     const int pid = es == 2 ? K_I16_PACKED_128x128 : K_I8_PACKED_256x256;
-    if (allow_packed && packed_pays(es, m, n, k, num_cu) && packed_fits(pid, ldc)) return pid;
+    if (allow_packed && packed_pays(es, m, n, k, num_cu) && packed_fits(pid, ldc) &&
+        16 * (k > lda ? k : lda) < ((int64_t)1 << 31))
+        return pid;
     if (es == 1) {
         if (m <= 16) return K_I8_16x256;
         if (m <= 32) return K_I8_32x256;
@@ -145,7 +147,7 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
         return IGEMM_OK;  // no-op: nothing is launched
     }
     if (kernel < -1 || kernel >= K_COUNT || split < -1 || split == 0) return IGEMM_EINVAL;
-    int id = kernel >= 0 ? kernel : auto_kernel(es, m, n, k, ldc, num_cu, allow_packed);
+    int id = kernel >= 0 ? kernel : auto_kernel(es, m, n, k, lda, ldc, num_cu, allow_packed);
     if (kKernels[id].es != es) return IGEMM_EINVAL;
     const KernelDesc &d = kKernels[id];
     const int64_t tiles = tiles_of(id, m, n);
@@ -155,8 +157,11 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
         // kMaxKChunk elements; the launches add into C in stream order.
         PackedLayout L;
         packed_layout(es, m, n, k, id, A, lda, &L);
+        // The multiply kernel addresses 16 rows of a plane with 32-bit lane
+        // offsets.
+        const int64_t plane_ld = L.pack_a ? L.k_pad : (L.k_pad > lda ? L.k_pad : lda);
         if (tiles > kMaxGrid || L.m_pad > kMaxGrid || L.n_pad / 64 > kMaxGrid ||
-            L.b_slices > 65535 || !packed_fits(id, ldc))
+            L.b_slices > 65535 || !packed_fits(id, ldc) || 16 * plane_ld >= ((int64_t)1 << 32))
             return IGEMM_ENOTSUP;
         out->kernel = id;
         out->bm = d.bm;
