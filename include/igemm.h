@@ -129,6 +129,9 @@ typedef struct igemm_plan {
     int limb_products; /* int8 MFMA products per operand pair: 4 or 1      */
     int packed;        /* 1 if operands are packed into a workspace first  */
     int64_t workspace_bytes; /* device workspace the call needs (0: none)  */
+    int64_t packed_a_bytes;  /* its A part (packed A and row corrections)  */
+    int64_t packed_b_bytes;  /* its B part (packed B, column corrections): */
+                             /* the buffer igemm_pack_b_* fills            */
 } igemm_plan;
 
 /*
@@ -208,6 +211,47 @@ int igemm_i8_prepacked(int64_t m, int64_t n, int64_t k,
                        int32_t *C, int64_t ldc,
                        int kernel, const void *workspace, int64_t workspace_bytes,
                        void *stream);
+
+/*
+ * Pack the fixed operand alone (Sec. 5.1: the weights are packed once, the
+ * activations on every call). The packed B depends only on n, k, B and the
+ * kernel, so one packed B serves products with any m and any A:
+ *   igemm_pack_b_i16 / igemm_pack_b_i8  write the packed k x n matrix B
+ *            (row-major, leading dimension ldb >= n) into `packed_b`.
+ *   igemm_i16_packed_b / igemm_i8_packed_b  C += A B for an m x k A (as in
+ *            igemm_i16 / igemm_i8) and a B packed by the call above with
+ *            the same n, k and kernel: pack A, then multiply. A's packed
+ *            copy goes into `workspace` (caller-owned, 256-byte aligned, at
+ *            least plan.packed_a_bytes of igemm_query_plan for (m, n, k)
+ *            and that kernel; IGEMM_ENOMEM if smaller), or, with workspace
+ *            NULL, into memory from the library's pool (IGEMM_EINVAL while
+ *            `stream` is being captured, when A needs a packed copy).
+ *   kernel   -1 = the packed kernel of the operand type, otherwise a packed
+ *            kernel index of that type (IGEMM_EINVAL for fused kernels).
+ *   packed_b, packed_b_bytes  device memory owned by the caller, 256-byte
+ *            aligned, at least plan.packed_b_bytes (IGEMM_EINVAL for NULL or
+ *            misaligned, IGEMM_ENOMEM if too small; nothing is enqueued).
+ * Asynchronous on `stream`; a multiply must be ordered after the pack and
+ * `packed_b` kept intact between them. Multiplies that share one packed B
+ * may run concurrently (they only read it). Sizes beyond the packed path's
+ * limits return IGEMM_ENOTSUP.
+ */
+int igemm_pack_b_i16(int64_t n, int64_t k, const int16_t *B, int64_t ldb, int kernel,
+                     void *packed_b, int64_t packed_b_bytes, void *stream);
+int igemm_pack_b_i8(int64_t n, int64_t k, const int8_t *B, int64_t ldb, int kernel,
+                    void *packed_b, int64_t packed_b_bytes, void *stream);
+int igemm_i16_packed_b(int64_t m, int64_t n, int64_t k,
+                       const int16_t *A, int64_t lda,
+                       const void *packed_b, int64_t packed_b_bytes,
+                       int32_t *C, int64_t ldc,
+                       int kernel, void *workspace, int64_t workspace_bytes,
+                       void *stream);
+int igemm_i8_packed_b(int64_t m, int64_t n, int64_t k,
+                      const int8_t *A, int64_t lda,
+                      const void *packed_b, int64_t packed_b_bytes,
+                      int32_t *C, int64_t ldc,
+                      int kernel, void *workspace, int64_t workspace_bytes,
+                      void *stream);
 
 /* Release the memory the library's workspace pool for the current device
  * holds beyond what in-flight calls use (hipMemPoolTrimTo). Returns

@@ -17,6 +17,11 @@ Same names as the C ABI:
                                    workspace, workspace_bytes, stream=None)
     igemm_i16_prepacked / igemm_i8_prepacked(m, n, k, A, lda, C, ldc, kernel=-1,
                                              workspace, workspace_bytes, stream=None)
+    igemm_pack_b_i16 / igemm_pack_b_i8(n, k, B, ldb, kernel=-1, packed_b,
+                                       packed_b_bytes, stream=None)
+    igemm_i16_packed_b / igemm_i8_packed_b(m, n, k, A, lda, packed_b, packed_b_bytes,
+                                           C, ldc, kernel=-1, workspace=None,
+                                           workspace_bytes=0, stream=None)
     igemm_query_plan(elem_bytes, m, n, k, A, lda, B, ldb, C, ldc, num_cu=0,
                      kernel=-1, split=-1) -> dict
     igemm_strerror(status), igemm_kernel_name(i), igemm_num_kernels(),
@@ -56,7 +61,8 @@ class _Plan(ctypes.Structure):
                 ("tiles", ctypes.c_int64), ("grid", ctypes.c_int64),
                 ("threads", ctypes.c_int), ("vec_a", ctypes.c_int), ("vec_b", ctypes.c_int),
                 ("limb_products", ctypes.c_int), ("packed", ctypes.c_int),
-                ("workspace_bytes", ctypes.c_int64)]
+                ("workspace_bytes", ctypes.c_int64), ("packed_a_bytes", ctypes.c_int64),
+                ("packed_b_bytes", ctypes.c_int64)]
 
 
 def _load():
@@ -87,6 +93,12 @@ def _load():
         getattr(lib, name).restype = ci
     for name in ("igemm_i16_prepacked", "igemm_i8_prepacked"):
         getattr(lib, name).argtypes = [i64, i64, i64, vp, i64, vp, i64, ci, vp, i64, vp]
+        getattr(lib, name).restype = ci
+    for name in ("igemm_pack_b_i16", "igemm_pack_b_i8"):
+        getattr(lib, name).argtypes = [i64, i64, vp, i64, ci, vp, i64, vp]
+        getattr(lib, name).restype = ci
+    for name in ("igemm_i16_packed_b", "igemm_i8_packed_b"):
+        getattr(lib, name).argtypes = [i64, i64, i64, vp, i64, vp, i64, vp, i64, ci, vp, i64, vp]
         getattr(lib, name).restype = ci
     lib.igemm_trim_workspace.argtypes = []
     lib.igemm_trim_workspace.restype = ci
@@ -211,6 +223,34 @@ def igemm_i8_prepacked(m, n, k, A, lda, C, ldc, kernel=-1, workspace=None, works
     return int(_lib.igemm_i8_prepacked(int(m), int(n), int(k), _addr(A), int(lda), _addr(C),
                                        int(ldc), int(kernel), _addr(workspace),
                                        int(workspace_bytes), _stream(stream)))
+
+
+def igemm_pack_b_i16(n, k, B, ldb, kernel=-1, packed_b=None, packed_b_bytes=0,
+                     stream=None) -> int:
+    return int(_lib.igemm_pack_b_i16(int(n), int(k), _addr(B), int(ldb), int(kernel),
+                                     _addr(packed_b), int(packed_b_bytes), _stream(stream)))
+
+
+def igemm_pack_b_i8(n, k, B, ldb, kernel=-1, packed_b=None, packed_b_bytes=0,
+                    stream=None) -> int:
+    return int(_lib.igemm_pack_b_i8(int(n), int(k), _addr(B), int(ldb), int(kernel),
+                                    _addr(packed_b), int(packed_b_bytes), _stream(stream)))
+
+
+def igemm_i16_packed_b(m, n, k, A, lda, packed_b, packed_b_bytes, C, ldc, kernel=-1,
+                       workspace=None, workspace_bytes=0, stream=None) -> int:
+    return int(_lib.igemm_i16_packed_b(int(m), int(n), int(k), _addr(A), int(lda),
+                                       _addr(packed_b), int(packed_b_bytes), _addr(C), int(ldc),
+                                       int(kernel), _addr(workspace), int(workspace_bytes),
+                                       _stream(stream)))
+
+
+def igemm_i8_packed_b(m, n, k, A, lda, packed_b, packed_b_bytes, C, ldc, kernel=-1,
+                      workspace=None, workspace_bytes=0, stream=None) -> int:
+    return int(_lib.igemm_i8_packed_b(int(m), int(n), int(k), _addr(A), int(lda),
+                                      _addr(packed_b), int(packed_b_bytes), _addr(C), int(ldc),
+                                      int(kernel), _addr(workspace), int(workspace_bytes),
+                                      _stream(stream)))
 
 
 def igemm_trim_workspace() -> int:
@@ -400,6 +440,68 @@ def gemm_prepacked(P, C, stream=None):
     st = fn(P.m, P.n, P.k, P.A, P.lda, C, ldc, P.kernel, P.workspace, P.nbytes, stream)
     if st != IGEMM_OK:
         raise IgemmError(st, "gemm_prepacked")
+    return C
+
+
+class PackedB:
+    """The fixed operand B of C += A.B in packed form (pack once, multiply
+    with any A of k columns). Holds the device buffer igemm_pack_b_* wrote."""
+
+    def __init__(self, es, n, k, kernel, buf, nbytes):
+        self.es, self.n, self.k, self.kernel = es, n, k, kernel
+        self.buf, self.nbytes = buf, nbytes
+
+
+def pack_b(B, stream=None):
+    """Pack a 2-D torch.int16 or torch.int8 CUDA tensor B (k x n, unit stride
+    along rows) for gemm_packed_b. Returns a PackedB."""
+    import torch
+    if B.dtype not in (torch.int16, torch.int8) or B.dim() != 2 or not B.is_cuda:
+        raise TypeError("pack_b: B must be a 2-D torch.int16 or torch.int8 CUDA tensor")
+    if B.shape[1] > 1 and B.stride(1) != 1:
+        raise ValueError("pack_b: B must have unit stride along rows")
+    es = 2 if B.dtype == torch.int16 else 1
+    k, n = B.shape
+    ldb = B.stride(0) if k > 1 else max(n, 1)
+    kid = _packed_kernel(es)
+    nbytes = 0
+    if n and k:
+        nbytes = igemm_query_plan(es, 1, n, k, None, k, B, ldb, None, n, _num_cu(B.device),
+                                  kid)["packed_b_bytes"]
+    buf = _aligned_workspace(max(nbytes, 1), B.device, stream)
+    fn = igemm_pack_b_i16 if es == 2 else igemm_pack_b_i8
+    st = fn(n, k, B, ldb, kid, buf, nbytes, stream)
+    if st != IGEMM_OK:
+        raise IgemmError(st, "pack_b")
+    return PackedB(es, n, k, kid, buf, nbytes)
+
+
+def gemm_packed_b(A, PB, C, stream=None):
+    """C += A.B with B packed by pack_b: A is an m x k CUDA tensor of B's
+    type, C an m x n torch.int32 CUDA tensor (unit stride along rows).
+    A's packed copy takes memory from torch's caching allocator. Returns C."""
+    import torch
+    want = torch.int16 if PB.es == 2 else torch.int8
+    if A.dtype != want or A.dim() != 2 or A.shape[1] != PB.k or not A.is_cuda:
+        raise ValueError(f"gemm_packed_b: A must be a {want} CUDA tensor with {PB.k} columns")
+    m = A.shape[0]
+    if C.dtype != torch.int32 or C.dim() != 2 or tuple(C.shape) != (m, PB.n) or not C.is_cuda:
+        raise ValueError("gemm_packed_b: C must be an int32 CUDA tensor of shape (m, n)")
+    for t, nm in ((A, "A"), (C, "C")):
+        if t.shape[1] > 1 and t.stride(1) != 1:
+            raise ValueError(f"gemm_packed_b: {nm} must have unit stride along rows")
+    lda = A.stride(0) if m > 1 else max(PB.k, 1)
+    ldc = C.stride(0) if m > 1 else max(PB.n, 1)
+    ws, ws_bytes = None, 0
+    if m and PB.n and PB.k:
+        ws_bytes = igemm_query_plan(PB.es, m, PB.n, PB.k, A, lda, None, PB.n, C, ldc,
+                                    _num_cu(C.device), PB.kernel)["packed_a_bytes"]
+        if ws_bytes > 0:
+            ws = _aligned_workspace(ws_bytes, C.device, stream)
+    fn = igemm_i16_packed_b if PB.es == 2 else igemm_i8_packed_b
+    st = fn(m, PB.n, PB.k, A, lda, PB.buf, PB.nbytes, C, ldc, PB.kernel, ws, ws_bytes, stream)
+    if st != IGEMM_OK:
+        raise IgemmError(st, "gemm_packed_b")
     return C
 
 

@@ -62,6 +62,52 @@ bool stream_is_capturing(hipStream_t s) {
     return st != hipStreamCaptureStatusNone;
 }
 
+// The one-call workspace holds the A part, then the B part.
+int pack_both(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+              int64_t lda, const void *B, int64_t ldb, void *ws, void *stream) {
+    char *wb = (char *)ws + p.packed_a_bytes;
+    // int16 always packs A, and that kernel clears B's column corrections
+    // before pack_b adds into them; int8 has no corrections.
+    int st = launch_pack_a(es, p, m, n, k, A, lda, ws, wb, stream);
+    if (st != IGEMM_OK) return st;
+    return launch_pack_b(es, p, m, n, k, A, lda, B, ldb, wb, false, stream);
+}
+int multiply_both(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                  int64_t lda, int32_t *C, int64_t ldc, const void *ws, void *stream) {
+    return launch_multiply(es, p, m, n, k, A, lda, C, ldc, ws,
+                           (const char *)ws + p.packed_a_bytes, stream);
+}
+
+// Device workspace for one call: the caller's, or one from the pool that is
+// released on the stream after the call's kernels.
+struct Scratch {
+    void *ptr = nullptr;
+    bool pooled = false;
+};
+int get_scratch(void *workspace, int64_t workspace_bytes, int64_t need, hipStream_t s,
+                Scratch *out) {
+    if (need <= 0) return IGEMM_OK;
+    if (workspace != nullptr) {
+        if (workspace_bytes < need) return IGEMM_ENOMEM;
+        out->ptr = workspace;
+        return IGEMM_OK;
+    }
+    hipMemPool_t pool = nullptr;
+    int st = pool_of_current_device(&pool);
+    if (st != IGEMM_OK) return st;
+    if (hipMallocFromPoolAsync(&out->ptr, (size_t)need, pool, s) != hipSuccess ||
+        out->ptr == nullptr) {
+        (void)hipGetLastError();
+        return IGEMM_ENOMEM;
+    }
+    out->pooled = true;
+    return IGEMM_OK;
+}
+int put_scratch(const Scratch &sc, hipStream_t s, int st) {
+    if (sc.pooled && hipFreeAsync(sc.ptr, s) != hipSuccess && st == IGEMM_OK) st = IGEMM_EHIP;
+    return st;
+}
+
 int run(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, const void *B,
         int64_t ldb, int32_t *C, int64_t ldc, void *stream, int kernel, int split,
         void *workspace, int64_t workspace_bytes) {
@@ -82,25 +128,12 @@ int run(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, con
                    pool_ok, &p);
     if (st != IGEMM_OK) return st;
     if (!p.packed) return launch_tiled(es, p, m, n, k, A, lda, B, ldb, C, ldc, stream);
-    if (workspace != nullptr) {
-        if (workspace_bytes < p.workspace_bytes) return IGEMM_ENOMEM;
-        st = launch_pack(es, p, m, n, k, A, lda, B, ldb, workspace, stream);
-        if (st != IGEMM_OK) return st;
-        return launch_multiply(es, p, m, n, k, A, lda, C, ldc, workspace, stream);
-    }
-    hipMemPool_t pool = nullptr;
-    st = pool_of_current_device(&pool);
+    Scratch sc;
+    st = get_scratch(workspace, workspace_bytes, p.workspace_bytes, s, &sc);
     if (st != IGEMM_OK) return st;
-    void *ws = nullptr;
-    if (hipMallocFromPoolAsync(&ws, (size_t)p.workspace_bytes, pool, s) != hipSuccess ||
-        ws == nullptr) {
-        (void)hipGetLastError();
-        return IGEMM_ENOMEM;
-    }
-    st = launch_pack(es, p, m, n, k, A, lda, B, ldb, ws, stream);
-    if (st == IGEMM_OK) st = launch_multiply(es, p, m, n, k, A, lda, C, ldc, ws, stream);
-    if (hipFreeAsync(ws, s) != hipSuccess && st == IGEMM_OK) st = IGEMM_EHIP;
-    return st;
+    st = pack_both(es, p, m, n, k, A, lda, B, ldb, sc.ptr, stream);
+    if (st == IGEMM_OK) st = multiply_both(es, p, m, n, k, A, lda, C, ldc, sc.ptr, stream);
+    return put_scratch(sc, s, st);
 }
 
 // Plan of a pack-once call: the packed kernel of the operand type (kernel -1)
@@ -129,7 +162,7 @@ int run_pack(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda
     igemm_plan p;
     st = packed_plan(es, m, n, k, A, lda, B, ldb, n, kernel, workspace, workspace_bytes, &p);
     if (st != IGEMM_OK) return st;
-    return launch_pack(es, p, m, n, k, A, lda, B, ldb, workspace, stream);
+    return pack_both(es, p, m, n, k, A, lda, B, ldb, workspace, stream);
 }
 
 int run_prepacked(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
@@ -143,7 +176,49 @@ int run_prepacked(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_
     igemm_plan p;
     st = packed_plan(es, m, n, k, A, lda, fake_b, n, ldc, kernel, workspace, workspace_bytes, &p);
     if (st != IGEMM_OK) return st;
-    return launch_multiply(es, p, m, n, k, A, lda, C, ldc, workspace, stream);
+    return multiply_both(es, p, m, n, k, A, lda, C, ldc, workspace, stream);
+}
+
+// Pack B alone (the fixed operand); its layout depends on n, k and the kernel
+// only.
+int run_pack_b(int es, int64_t n, int64_t k, const void *B, int64_t ldb, int kernel,
+               void *packed_b, int64_t packed_b_bytes, void *stream) {
+    const void *fake = (const void *)(uintptr_t)4096;
+    int st = validate(es, 1, n, k, fake, k > 0 ? k : 1, B, ldb, fake, n > 0 ? n : 1);
+    if (st != IGEMM_OK) return st;
+    if (n == 0 || k == 0) return IGEMM_OK;
+    igemm_plan p;
+    st = packed_plan(es, 1, n, k, fake, k, B, ldb, n, kernel, packed_b, 0, &p);
+    if (st != IGEMM_OK && st != IGEMM_ENOMEM) return st;
+    if (packed_b_bytes < p.packed_b_bytes) return IGEMM_ENOMEM;
+    return launch_pack_b(es, p, 1, n, k, fake, k, B, ldb, packed_b, true, stream);
+}
+
+// C += A B with B packed by run_pack_b: pack A (workspace: the caller's or
+// the pool's), then multiply.
+int run_packed_b(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
+                 const void *packed_b, int64_t packed_b_bytes, int32_t *C, int64_t ldc,
+                 int kernel, void *workspace, int64_t workspace_bytes, void *stream) {
+    const void *fake = (const void *)(uintptr_t)4096;
+    int st = validate(es, m, n, k, A, lda, fake, n > 0 ? n : 1, C, ldc);
+    if (st != IGEMM_OK) return st;
+    if (m == 0 || n == 0 || k == 0) return IGEMM_OK;
+    if (workspace != nullptr && ((uintptr_t)workspace % 256 != 0 || workspace_bytes < 0))
+        return IGEMM_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    igemm_plan p;
+    st = packed_plan(es, m, n, k, A, lda, fake, n, ldc, kernel, packed_b, 0, &p);
+    if (st != IGEMM_OK && st != IGEMM_ENOMEM) return st;
+    if (packed_b_bytes < p.packed_b_bytes) return IGEMM_ENOMEM;
+    if (p.packed_a_bytes > 0 && workspace == nullptr && stream_is_capturing(s))
+        return IGEMM_EINVAL;
+    Scratch sc;
+    st = get_scratch(workspace, workspace_bytes, p.packed_a_bytes, s, &sc);
+    if (st != IGEMM_OK) return st;
+    st = launch_pack_a(es, p, m, n, k, A, lda, sc.ptr, nullptr, stream);
+    if (st == IGEMM_OK)
+        st = launch_multiply(es, p, m, n, k, A, lda, C, ldc, sc.ptr, packed_b, stream);
+    return put_scratch(sc, s, st);
 }
 
 }  // namespace
@@ -211,6 +286,30 @@ int igemm_i8_prepacked(int64_t m, int64_t n, int64_t k, const int8_t *A, int64_t
                        int64_t workspace_bytes, void *stream) {
     return igemm::run_prepacked(1, m, n, k, A, lda, C, ldc, kernel, workspace, workspace_bytes,
                                 stream);
+}
+
+int igemm_pack_b_i16(int64_t n, int64_t k, const int16_t *B, int64_t ldb, int kernel,
+                     void *packed_b, int64_t packed_b_bytes, void *stream) {
+    return igemm::run_pack_b(2, n, k, B, ldb, kernel, packed_b, packed_b_bytes, stream);
+}
+
+int igemm_pack_b_i8(int64_t n, int64_t k, const int8_t *B, int64_t ldb, int kernel,
+                    void *packed_b, int64_t packed_b_bytes, void *stream) {
+    return igemm::run_pack_b(1, n, k, B, ldb, kernel, packed_b, packed_b_bytes, stream);
+}
+
+int igemm_i16_packed_b(int64_t m, int64_t n, int64_t k, const int16_t *A, int64_t lda,
+                       const void *packed_b, int64_t packed_b_bytes, int32_t *C, int64_t ldc,
+                       int kernel, void *workspace, int64_t workspace_bytes, void *stream) {
+    return igemm::run_packed_b(2, m, n, k, A, lda, packed_b, packed_b_bytes, C, ldc, kernel,
+                               workspace, workspace_bytes, stream);
+}
+
+int igemm_i8_packed_b(int64_t m, int64_t n, int64_t k, const int8_t *A, int64_t lda,
+                      const void *packed_b, int64_t packed_b_bytes, int32_t *C, int64_t ldc,
+                      int kernel, void *workspace, int64_t workspace_bytes, void *stream) {
+    return igemm::run_packed_b(1, m, n, k, A, lda, packed_b, packed_b_bytes, C, ldc, kernel,
+                               workspace, workspace_bytes, stream);
 }
 
 int igemm_trim_workspace(void) {

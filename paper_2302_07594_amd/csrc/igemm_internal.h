@@ -41,19 +41,23 @@ constexpr int64_t kMaxKChunk = 32768;
 
 extern const KernelDesc kKernels[K_COUNT];
 
-// Workspace of the packed path (byte offsets from a 256-byte aligned base).
-// Planes are k-contiguous int8 rows of k_pad bytes, zero beyond k:
-//   A: es planes of m_pad rows (int16: high limb, then offset low limb),
-//      absent for int8 A that is already aligned and tile-shaped;
-//   B: es planes of n_pad rows (the columns of B);
-//   corr_a: m_pad row corrections, corr_b: n_pad column corrections (int16
-//   only; pack_b adds each k slice's column sums into them).
+// Workspace of the packed path, in two parts (byte offsets from 256-byte
+// aligned bases), so that B can be packed once and reused:
+//   A part (a_bytes): es planes of m_pad rows (int16: high limb, then offset
+//     low limb), absent for int8 A that is already aligned and tile-shaped,
+//     then m_pad row corrections (int16);
+//   B part (b_bytes): es planes of n_pad rows (the columns of B), then n_pad
+//     column corrections (int16; pack_b adds each k slice's column sums).
+// Planes are k-contiguous int8 rows of k_pad bytes, zero beyond k. The
+// one-call workspace is the A part followed by the B part.
 struct PackedLayout {
     int64_t m_pad, n_pad, k_pad;
     int64_t kspan;     // k rows per pack_b workgroup
     int b_slices;      // k slices of pack_b
     bool pack_a;
-    int64_t off_a, off_b, off_corr_a, off_corr_b, bytes;
+    int64_t off_a, off_corr_a, a_bytes;  // within the A part
+    int64_t off_b, off_corr_b, b_bytes;  // within the B part
+    int64_t bytes;                        // a_bytes + b_bytes
 };
 
 // Validation and planning; pure host code, no HIP calls.
@@ -72,11 +76,17 @@ void packed_layout(int es, int64_t m, int64_t n, int64_t k, int kernel, const vo
 int launch_tiled(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
                  int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
                  void *stream);
-// The packed path in two parts: pack A and B into the workspace, then run
-// the multiply (one launch per k chunk) on a packed workspace.
-int launch_pack(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
-                int64_t lda, const void *B, int64_t ldb, void *workspace, void *stream);
+// The packed path: pack A into an A part (optionally clearing the B part's
+// column corrections, which pack_b then adds into), pack B into a B part
+// (clear_corr: clear the corrections itself first), multiply (one launch per
+// k chunk) from the two parts.
+int launch_pack_a(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                  int64_t lda, void *a_part, void *b_part_to_clear, void *stream);
+int launch_pack_b(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                  int64_t lda, const void *B, int64_t ldb, void *b_part, bool clear_corr,
+                  void *stream);
 int launch_multiply(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
-                    int64_t lda, int32_t *C, int64_t ldc, const void *workspace, void *stream);
+                    int64_t lda, int32_t *C, int64_t ldc, const void *a_part, const void *b_part,
+                    void *stream);
 
 }  // namespace igemm

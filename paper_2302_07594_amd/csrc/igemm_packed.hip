@@ -44,9 +44,14 @@ __device__ __forceinline__ int wave_sum(int v) {
     return v;
 }
 
+// ---- clear n 32-bit words (a fill kernel: graph captures record no memset) --
+__global__ void __launch_bounds__(256) clear_u32(uint32_t *__restrict__ p, int n) {
+    for (int j = blockIdx.x * 256 + threadIdx.x; j < n; j += gridDim.x * 256) p[j] = 0u;
+}
+
 // ---- pack A, int16: one workgroup per padded row ---------------------------
 // Writes Ah/Al[i][0, k_pad) and corrA[i] = 32768*sum(h) + 128*sum(l) mod 2^32,
-// and zeroes corrB[0, n_pad).
+// and, if corrB is given, zeroes corrB[0, n_pad).
 template <bool VEC>
 __global__ void __launch_bounds__(256)
 pack_a_i16(const int16_t *__restrict__ A, int64_t lda, int m, int k, int k_pad,
@@ -54,7 +59,8 @@ pack_a_i16(const int16_t *__restrict__ A, int64_t lda, int m, int k, int k_pad,
            uint32_t *__restrict__ corrB, int n_pad) {
     const int i = blockIdx.x, tid = threadIdx.x;
     // Clear the column corrections that pack_b (next on the stream) adds into.
-    for (int j = i * 256 + tid; j < n_pad; j += gridDim.x * 256) corrB[j] = 0u;
+    if (corrB != nullptr)
+        for (int j = i * 256 + tid; j < n_pad; j += gridDim.x * 256) corrB[j] = 0u;
     const int len = i < m ? k : 0;
     const int16_t *arow = A + (int64_t)(i < m ? i : 0) * lda;
     int8_t *hrow = Ah + (int64_t)i * k_pad;
@@ -545,37 +551,53 @@ using namespace packed;
 // ---------------------------------------------------------------------------
 // Host side of the packed path.
 
-int launch_pack(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
-                int64_t lda, const void *B, int64_t ldb, void *workspace, void *stream_) {
+int launch_pack_a(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                  int64_t lda, void *a_part, void *b_part_to_clear, void *stream_) {
     hipStream_t stream = (hipStream_t)stream_;
     PackedLayout L;
     packed_layout(es, m, n, k, p.kernel, A, lda, &L);
-    int8_t *ws = (int8_t *)workspace;
-    const bool va = p.vec_a != 0, vb = p.vec_b != 0;
-    const int mi = (int)m, ni = (int)n, ki = (int)k, kp = (int)L.k_pad, np = (int)L.n_pad;
-    int8_t *Apk = ws + L.off_a, *Bpk = ws + L.off_b;
-    uint32_t *corrA = (uint32_t *)(ws + L.off_corr_a);
-    uint32_t *corrB = (uint32_t *)(ws + L.off_corr_b);
-    const int64_t a_plane = L.m_pad * L.k_pad, b_plane = L.n_pad * L.k_pad;
+    if (!L.pack_a) return IGEMM_OK;
+    int8_t *wa = (int8_t *)a_part;
+    const bool va = p.vec_a != 0;
+    const int mi = (int)m, ki = (int)k, kp = (int)L.k_pad, np = (int)L.n_pad;
+    int8_t *Apk = wa + L.off_a;
+    uint32_t *corrA = (uint32_t *)(wa + L.off_corr_a);
+    uint32_t *corrB = b_part_to_clear != nullptr
+                          ? (uint32_t *)((int8_t *)b_part_to_clear + L.off_corr_b)
+                          : nullptr;
+    const int64_t a_plane = L.m_pad * L.k_pad;
+    const dim3 g((unsigned)L.m_pad);
+    if (es == 2) {
+        int8_t *Al = Apk + a_plane;
+        const int16_t *A16 = (const int16_t *)A;
+        if (va)
+            pack_a_i16<true><<<g, 256, 0, stream>>>(A16, lda, mi, ki, kp, Apk, Al, corrA, corrB, np);
+        else
+            pack_a_i16<false><<<g, 256, 0, stream>>>(A16, lda, mi, ki, kp, Apk, Al, corrA, corrB, np);
+    } else {
+        const int8_t *A8 = (const int8_t *)A;
+        if (va)
+            pack_a_i8<true><<<g, 256, 0, stream>>>(A8, lda, mi, ki, kp, Apk);
+        else
+            pack_a_i8<false><<<g, 256, 0, stream>>>(A8, lda, mi, ki, kp, Apk);
+    }
+    return hipGetLastError() == hipSuccess ? IGEMM_OK : IGEMM_EHIP;
+}
 
-    if (L.pack_a) {
-        const dim3 g((unsigned)L.m_pad);
-        if (es == 2) {
-            int8_t *Al = Apk + a_plane;
-            const int16_t *A16 = (const int16_t *)A;
-            if (va)
-                pack_a_i16<true><<<g, 256, 0, stream>>>(A16, lda, mi, ki, kp, Apk, Al, corrA,
-                                                        corrB, np);
-            else
-                pack_a_i16<false><<<g, 256, 0, stream>>>(A16, lda, mi, ki, kp, Apk, Al, corrA,
-                                                         corrB, np);
-        } else {
-            const int8_t *A8 = (const int8_t *)A;
-            if (va)
-                pack_a_i8<true><<<g, 256, 0, stream>>>(A8, lda, mi, ki, kp, Apk);
-            else
-                pack_a_i8<false><<<g, 256, 0, stream>>>(A8, lda, mi, ki, kp, Apk);
-        }
+int launch_pack_b(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                  int64_t lda, const void *B, int64_t ldb, void *b_part, bool clear_corr,
+                  void *stream_) {
+    hipStream_t stream = (hipStream_t)stream_;
+    PackedLayout L;
+    packed_layout(es, m, n, k, p.kernel, A, lda, &L);
+    int8_t *wb = (int8_t *)b_part;
+    const bool vb = p.vec_b != 0;
+    const int ni = (int)n, ki = (int)k, kp = (int)L.k_pad, np = (int)L.n_pad;
+    int8_t *Bpk = wb + L.off_b;
+    uint32_t *corrB = (uint32_t *)(wb + L.off_corr_b);
+    const int64_t b_plane = L.n_pad * L.k_pad;
+    if (es == 2 && clear_corr) {
+        clear_u32<<<dim3((unsigned)((np + 255) / 256)), 256, 0, stream>>>(corrB, np);
         if (hipGetLastError() != hipSuccess) return IGEMM_EHIP;
     }
     const dim3 g((unsigned)(L.n_pad / 64), (unsigned)L.b_slices);
@@ -596,19 +618,20 @@ int launch_pack(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, co
 }
 
 int launch_multiply(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
-                    int64_t lda, int32_t *C, int64_t ldc, const void *workspace, void *stream_) {
+                    int64_t lda, int32_t *C, int64_t ldc, const void *a_part, const void *b_part,
+                    void *stream_) {
     hipStream_t stream = (hipStream_t)stream_;
     PackedLayout L;
     packed_layout(es, m, n, k, p.kernel, A, lda, &L);
-    const int8_t *ws = (const int8_t *)workspace;
+    const int8_t *wa = (const int8_t *)a_part, *wb = (const int8_t *)b_part;
     const int mi = (int)m, ni = (int)n;
-    const int8_t *Apk = ws + L.off_a, *Bpk = ws + L.off_b;
-    const uint32_t *corrA = (const uint32_t *)(ws + L.off_corr_a);
-    const uint32_t *corrB = (const uint32_t *)(ws + L.off_corr_b);
+    const int8_t *Bpk = wb + L.off_b;
+    const uint32_t *corrA = (const uint32_t *)(wa + L.off_corr_a);
+    const uint32_t *corrB = (const uint32_t *)(wb + L.off_corr_b);
     const int64_t a_plane = L.m_pad * L.k_pad, b_plane = L.n_pad * L.k_pad;
     const KernelDesc &d = kKernels[p.kernel];
     const int tm = (int)(L.m_pad / d.bm), tn = (int)(L.n_pad / d.bn);
-    const int8_t *Asrc = L.pack_a ? Apk : (const int8_t *)A;
+    const int8_t *Asrc = L.pack_a ? wa + L.off_a : (const int8_t *)A;
     const int64_t lda_p = L.pack_a ? L.k_pad : lda;
     const dim3 grid((unsigned)p.grid);
     // One launch per k chunk; the row and column corrections and the

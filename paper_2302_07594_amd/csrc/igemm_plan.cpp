@@ -92,13 +92,16 @@ void packed_layout(int es, int64_t m, int64_t n, int64_t k, int kernel, const vo
     int64_t off = 0;
     L->off_a = off;
     if (L->pack_a) off = align256(off + es * L->m_pad * L->k_pad);
-    L->off_b = off;
-    off = align256(off + es * L->n_pad * L->k_pad);
     L->off_corr_a = off;
     if (es == 2) off = align256(off + 4 * L->m_pad);
+    L->a_bytes = off;
+    off = 0;
+    L->off_b = off;
+    off = align256(off + es * L->n_pad * L->k_pad);
     L->off_corr_b = off;
     if (es == 2) off = align256(off + 4 * L->n_pad);
-    L->bytes = off;
+    L->b_bytes = off;
+    L->bytes = L->a_bytes + L->b_bytes;
 }
 
 // The packed path pays off once the product is large enough for the pack
@@ -174,6 +177,8 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
         out->vec_b = (b % 16 == 0) && ((ldb * es) % 16 == 0);
         out->packed = 1;
         out->workspace_bytes = L.bytes;
+        out->packed_a_bytes = L.a_bytes;
+        out->packed_b_bytes = L.b_bytes;
         return IGEMM_OK;
     }
     const int64_t ktiles = cdiv(k, kBK);

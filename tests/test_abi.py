@@ -27,7 +27,10 @@ def test_header_declares_entry_points():
     fns = declared_functions()
     for name in ("igemm_i16", "igemm_i8", "igemm_strerror", "igemm_i16_ex", "igemm_i8_ex",
                  "igemm_query_plan", "igemm_num_kernels", "igemm_kernel_name",
-                 "igemm_version", "igemm_i16_ws", "igemm_i8_ws", "igemm_trim_workspace"):
+                 "igemm_version", "igemm_i16_ws", "igemm_i8_ws", "igemm_trim_workspace",
+                 "igemm_pack_i16", "igemm_pack_i8", "igemm_i16_prepacked",
+                 "igemm_i8_prepacked", "igemm_pack_b_i16", "igemm_pack_b_i8",
+                 "igemm_i16_packed_b", "igemm_i8_packed_b"):
         assert name in fns
 
 
@@ -167,6 +170,27 @@ def test_packed_workspace_layout():
     assert q["split"] == 3 and q["k_chunk"] == 32768 and q["packed"] == 1
 
 
+@pytest.mark.parametrize("es", [2, 1])
+def test_packed_workspace_parts(es):
+    """The workspace is an A part then a B part; the B part (what pack_b
+    fills) depends on n, k and the kernel only, never on m or A."""
+    kid = _kid("i16_packed_128x128" if es == 2 else "i8_packed_256x256")
+    n, k = 1000, 3000
+    bparts = set()
+    for m, a in ((1, FAKE_A), (1000, FAKE_A), (4096, FAKE_A + 1), (77, FAKE_A)):
+        q = ig.igemm_query_plan(es, m, n, k, a, k, FAKE_B, n, FAKE_C, n, kernel=kid)
+        assert q["workspace_bytes"] == q["packed_a_bytes"] + q["packed_b_bytes"]
+        assert q["packed_a_bytes"] % 256 == 0 and q["packed_b_bytes"] % 256 == 0
+        bparts.add(q["packed_b_bytes"])
+    n_pad, k_pad = (1024, 3072) if es == 2 else (1024, 3072)
+    corr = 4 * n_pad if es == 2 else 0
+    assert bparts == {es * n_pad * k_pad + corr}
+    # int8 A that is aligned and tile-shaped needs no A part at all
+    if es == 1:
+        q = ig.igemm_query_plan(1, 512, n, 3072, FAKE_A, 3072, FAKE_B, n, FAKE_C, n, kernel=kid)
+        assert q["packed_a_bytes"] == 0
+
+
 def test_packed_grid_limits():
     kid = _kid("i16_packed_128x128")
     m = 1 << 25   # more padded rows than one launch can cover with pack_a
@@ -213,3 +237,35 @@ def test_pack_once_calls_reject_bad_arguments(es):
     assert mul(64, 64, 64, FAKE_A, 64, FAKE_C, 64, fused, W, 1 << 20, s) == E
     assert mul(64, 64, 64, FAKE_A, 64, FAKE_C, 64, -1, W, 256, s) == ig.IGEMM_ENOMEM
     assert mul(64, 64, 0, FAKE_A, 1, FAKE_C, 64, -1, W, 0, s) == ig.IGEMM_OK
+
+
+@pytest.mark.parametrize("es", [2, 1])
+def test_packed_b_calls_reject_bad_arguments(es):
+    """Argument, kernel and buffer checks of the pack-B-once calls come
+    before any HIP call."""
+    s = 0
+    pk = ig.igemm_pack_b_i16 if es == 2 else ig.igemm_pack_b_i8
+    mul = ig.igemm_i16_packed_b if es == 2 else ig.igemm_i8_packed_b
+    W, P = 0x40000, 0x80000
+    E = ig.IGEMM_EINVAL
+    fused = ig.kernels_for(es)[0]
+    big = 1 << 24
+    assert pk(64, 64, FAKE_B, 64, -1, 0, big, s) == E              # no buffer
+    assert pk(64, 64, FAKE_B, 64, -1, P + 64, big, s) == E         # misaligned
+    assert pk(64, 64, FAKE_B, 64, fused, P, big, s) == E           # fused kernel
+    assert pk(64, 64, FAKE_B, 63, -1, P, big, s) == E              # ldb < n
+    assert pk(64, 64, 0, 64, -1, P, big, s) == E                   # B NULL
+    assert pk(-1, 64, FAKE_B, 64, -1, P, big, s) == E
+    assert pk(64, 64, FAKE_B, 64, -1, P, 256, s) == ig.IGEMM_ENOMEM
+    assert pk(0, 64, FAKE_B, 64, -1, P, 0, s) == ig.IGEMM_OK       # no-op
+    assert pk(64, 0, 0, 64, -1, P, 0, s) == ig.IGEMM_OK
+    assert mul(64, 64, 64, FAKE_A, 64, 0, big, FAKE_C, 64, -1, W, big, s) == E      # no B
+    assert mul(64, 64, 64, FAKE_A, 64, P + 16, big, FAKE_C, 64, -1, W, big, s) == E
+    assert mul(64, 64, 64, FAKE_A, 64, P, big, FAKE_C, 64, fused, W, big, s) == E
+    assert mul(64, 64, 64, FAKE_A, 63, P, big, FAKE_C, 64, -1, W, big, s) == E      # lda < k
+    assert mul(64, 64, 64, FAKE_A, 64, P, big, 0, 64, -1, W, big, s) == E           # C NULL
+    assert mul(64, 64, 64, FAKE_A, 64, P, big, FAKE_C, 63, -1, W, big, s) == E      # ldc < n
+    assert mul(64, 64, 64, FAKE_A, 64, P, big, FAKE_C, 64, -1, W + 8, big, s) == E  # misaligned
+    assert mul(64, 64, 64, FAKE_A, 64, P, 256, FAKE_C, 64, -1, W, big, s) == ig.IGEMM_ENOMEM
+    assert mul(64, 64, 64, FAKE_A, 64, P, big, FAKE_C, 64, -1, W, 256, s) == ig.IGEMM_ENOMEM
+    assert mul(0, 64, 64, FAKE_A, 64, 0, 0, FAKE_C, 64, -1, 0, 0, s) == ig.IGEMM_OK
