@@ -127,6 +127,7 @@ int run(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, con
     st = make_plan(es, m, n, k, A, lda, B, ldb, ldc, num_cu_of_current_device(), kernel, split,
                    pool_ok, &p);
     if (st != IGEMM_OK) return st;
+    if (p.kernel == K_I8_STREAM) return launch_stream(p, m, n, k, A, lda, B, ldb, C, ldc, stream);
     if (!p.packed) return launch_tiled(es, p, m, n, k, A, lda, B, ldb, C, ldc, stream);
     Scratch sc;
     st = get_scratch(workspace, workspace_bytes, p.workspace_bytes, s, &sc);

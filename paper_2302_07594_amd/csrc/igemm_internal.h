@@ -29,6 +29,7 @@ enum KernelId {
     K_I16_16x128,
     K_I8_PACKED_256x256,
     K_I16_PACKED_128x128,
+    K_I8_STREAM,
     K_COUNT
 };
 
@@ -73,6 +74,10 @@ void packed_layout(int es, int64_t m, int64_t n, int64_t k, int kernel, const vo
 
 // Kernel launches for a validated plan (stream is a hipStream_t). The packed
 // launch needs a workspace of at least plan.workspace_bytes, 256-byte aligned.
+// The streaming kernel for few-row int8 products.
+int launch_stream(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                  int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
+                  void *stream);
 int launch_tiled(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
                  int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
                  void *stream);

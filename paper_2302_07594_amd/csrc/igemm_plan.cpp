@@ -26,6 +26,7 @@ const KernelDesc kKernels[K_COUNT] = {
     {"i16_16x128", 2, 16, 128, 16, 32, false},
     {"i8_packed_256x256", 1, 256, 256, 128, 128, true},
     {"i16_packed_128x128", 2, 128, 128, 64, 64, true},
+    {"i8_stream_32x128", 1, 32, 128, 16, 128, false},
 };
 
 // Largest grid (in workgroups) of one launch: the dispatch packet counts
@@ -117,13 +118,50 @@ static bool packed_fits(int id, int64_t ldc) {
     return (int64_t)kKernels[id].bm * ldc * 4 < INT_MAX;
 }
 
-static int auto_kernel(int es, int64_t m, int64_t n, int64_t k, int64_t lda, int64_t ldc,
-                       int num_cu, bool allow_packed) {
+// Streaming kernel: row blocks of 16 or 32 rows, column blocks of 128, and
+// workgroups of 4 or 8 waves that each take 1, 2 or 4 k-steps of 64 (4, 8,
+// 16 or 32 steps per workgroup). Returns false if its 32-bit window offsets
+// do not fit.
+struct StreamShape {
+    int bm, threads;
+    int64_t spw, slices, tiles;
+};
+static bool stream_shape(int64_t m, int64_t n, int64_t k, int64_t lda, int64_t ldb, bool va,
+                         bool vb, int split, StreamShape *out) {
+    const int bm = m <= 16 ? 16 : 32;
+    const int64_t ksteps = cdiv(k, kBK);
+    int64_t spw = 4;
+    if (va && vb) {
+        // Few slices keep the atomic adds into C cheap; enough workgroups keep
+        // the loads of B in flight. Measured on the 4096- and 11008-column
+        // shapes with k = 4096: 8 steps per workgroup (4 and 16 are up to 10%
+        // slower, 32 up to 2x).
+        const int64_t want = split > 0 ? cdiv(ksteps, split) : 8;
+        const int64_t cap = bm == 16 ? 32 : 16;
+        while (spw < want && spw < cap) spw *= 2;
+    }
+    if ((spw * kBK) * ldb + 128 >= 0x7fff0000 || (int64_t)bm * lda + spw * kBK >= 0x7fff0000)
+        return false;
+    out->bm = bm;
+    out->threads = spw == 4 ? 256 : 512;
+    out->spw = spw;
+    out->slices = cdiv(ksteps, spw);
+    out->tiles = cdiv(m, bm) * cdiv(n, 128);
+    return out->tiles * out->slices <= ((int64_t)1 << 32) / 512 - 1;
+}
+
+static int auto_kernel(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
+                       const void *B, int64_t ldb, int64_t ldc, int num_cu, bool allow_packed) {
     const int pid = es == 2 ? K_I16_PACKED_128x128 : K_I8_PACKED_256x256;
     if (allow_packed && packed_pays(es, m, n, k, num_cu) && packed_fits(pid, ldc) &&
         16 * (k > lda ? k : lda) < ((int64_t)1 << 31))
         return pid;
     if (es == 1) {
+        StreamShape ss;
+        if (m <= 32 && n >= 512 && k >= 256 && (uintptr_t)B % 8 == 0 && ldb % 8 == 0 &&
+            (uintptr_t)A % 16 == 0 && lda % 16 == 0 &&
+            stream_shape(m, n, k, lda, ldb, true, true, -1, &ss))
+            return K_I8_STREAM;
         if (m <= 16) return K_I8_16x256;
         if (m <= 32) return K_I8_32x256;
         if (tiles_of(K_I8_256x256, m, n) >= num_cu) return K_I8_256x256;
@@ -150,7 +188,7 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
         return IGEMM_OK;  // no-op: nothing is launched
     }
     if (kernel < -1 || kernel >= K_COUNT || split < -1 || split == 0) return IGEMM_EINVAL;
-    int id = kernel >= 0 ? kernel : auto_kernel(es, m, n, k, lda, ldc, num_cu, allow_packed);
+    int id = kernel >= 0 ? kernel : auto_kernel(es, m, n, k, A, lda, B, ldb, ldc, num_cu, allow_packed);
     if (kKernels[id].es != es) return IGEMM_EINVAL;
     const KernelDesc &d = kKernels[id];
     const int64_t tiles = tiles_of(id, m, n);
@@ -179,6 +217,23 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
         out->workspace_bytes = L.bytes;
         out->packed_a_bytes = L.a_bytes;
         out->packed_b_bytes = L.b_bytes;
+        return IGEMM_OK;
+    }
+    if (id == K_I8_STREAM) {
+        const bool va = a % 16 == 0 && lda % 16 == 0;
+        const bool vb = b % 8 == 0 && ldb % 8 == 0;
+        StreamShape ss;
+        if (!stream_shape(m, n, k, lda, ldb, va, vb, split, &ss)) return IGEMM_ENOTSUP;
+        out->kernel = id;
+        out->bm = ss.bm;
+        out->bn = 128;
+        out->split = (int)ss.slices;
+        out->k_chunk = ss.spw * kBK;
+        out->tiles = ss.tiles;
+        out->grid = ss.tiles * ss.slices;
+        out->threads = ss.threads;
+        out->vec_a = va;
+        out->vec_b = vb;
         return IGEMM_OK;
     }
     const int64_t ktiles = cdiv(k, kBK);

@@ -1,0 +1,272 @@
+// Streaming kernel for int8 C += A B with few rows (blocks of 16 or 32 rows
+// of A): the shapes of deep-learning inference with one large and two small
+// dimensions (Sec. 2, Sec. 4.2), where B -- the weights -- is read exactly
+// once and the time is the time to stream it from HBM.
+//
+// Such a product has too little reuse for the LDS-staged tile kernels to
+// pay: what matters is how many bytes of B are in flight. So every wave
+// streams its own 64-row steps of a 128-column block of B straight into
+// registers, with all of its loads issued before the first use, and no
+// wave ever waits for another until the end:
+//   * lane l loads 8 consecutive bytes (columns 8(l%16) .. 8(l%16)+7) of
+//     16 consecutive rows (16(l/16) .. 16(l/16)+15 of the step); sixteen
+//     lanes of one load instruction cover one whole 128-byte row segment;
+//   * 4x4 byte transposes in registers turn those 16 rows x 8 columns into
+//     eight k-contiguous 16-byte column fragments, the B operand of
+//     v_mfma_i32_16x16x64_i8 -- fragment c of lane l is column 8(l%16)+c,
+//     so MFMA c computes the columns {8j + c};
+//   * the A operand (a block of 16 or 32 rows of A) is read with one
+//     16-byte load per lane and step; it stays in L2 across workgroups
+//     (larger m is covered by more row blocks, each streaming B again);
+//   * the waves of a workgroup take interleaved steps of one k range and
+//     sum their accumulators through LDS at the end; each workgroup then
+//     adds its m x 128 result into C (32-bit atomic adds when several
+//     workgroups share a column block, else a plain read-add-write).
+// Rows of B beyond k are read through a buffer resource whose range ends at
+// B's last byte, so the hardware returns zeros for them; A's elements
+// beyond k are masked to zero, which also cancels whatever the rows of B
+// past k would contribute. Columns beyond n and rows beyond m produce
+// accumulator entries that are never written back.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "igemm.h"
+#include "igemm_device.h"
+#include "igemm_internal.h"
+
+namespace igemm {
+namespace stream {
+
+typedef unsigned int v2u __attribute__((ext_vector_type(2)));
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+
+// 8 bytes at byte offset `off`: one 8-byte load (VEC) or eight byte loads.
+template <bool VEC>
+__device__ __forceinline__ v2u load8(__amdgpu_buffer_rsrc_t rs, u32 off) {
+    if constexpr (VEC) {
+        return __builtin_bit_cast(v2u, __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, 0));
+    } else {
+        u32 w[2] = {0u, 0u};
+#pragma unroll
+        for (int b = 0; b < 8; ++b)
+            w[b >> 2] |= (u32)__builtin_amdgcn_raw_buffer_load_b8(rs, off + b, 0, 0) << (8 * (b & 3));
+        v2u r;
+        r.x = w[0];
+        r.y = w[1];
+        return r;
+    }
+}
+
+// 16 bytes at byte offset `off`: one 16-byte load (VEC) or sixteen byte loads.
+template <bool VEC>
+__device__ __forceinline__ v4u load16(__amdgpu_buffer_rsrc_t rs, u32 off) {
+    if constexpr (VEC) {
+        return __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+    } else {
+        u32 w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int b = 0; b < 16; ++b)
+            w[b >> 2] |= (u32)__builtin_amdgcn_raw_buffer_load_b8(rs, off + b, 0, 0) << (8 * (b & 3));
+        v4u r;
+        r.x = w[0];
+        r.y = w[1];
+        r.z = w[2];
+        r.w = w[3];
+        return r;
+    }
+}
+
+// MB: 16-row MFMA blocks per row block (16 * MB rows); WAVES: waves per
+// workgroup; S: 64-row steps per wave; VA / VB: 16-byte aligned A rows / 8-byte aligned B
+// rows; SPLIT: several workgroups add into one column block of C.
+template <int MB, int WAVES, int S, bool VA, bool VB, bool SPLIT>
+__global__ void __launch_bounds__(64 * WAVES)
+igemm_stream_i8(const int8_t *__restrict__ A, int64_t lda, const int8_t *__restrict__ B,
+                int64_t ldb, int32_t *__restrict__ C, int64_t ldc, int m, int n, int k,
+                int colblocks, int rowblocks) {
+    constexpr int SPW = WAVES * S;  // steps per workgroup
+    constexpr int NP = MB * 8;      // accumulator fragments per wave
+    // Two blocks of 16 rows with eight waves sum over the waves in two phases
+    // so that the LDS buffers hold half of the waves' accumulators (64 KB, two
+    // workgroups per compute unit); otherwise every wave stores its own.
+    constexpr bool TWO = MB == 2 && WAVES == 8;
+    constexpr int H = TWO ? WAVES / 2 : WAVES;  // LDS buffers
+    __shared__ v4u red[H][NP][64];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int q = lane >> 4;  // k chunk of the MFMA fragments
+    const int i = lane & 15;  // row of A / column group of B
+    // workgroup -> (column block, row block, k range), column blocks fastest
+    const unsigned t = blockIdx.x / (unsigned)colblocks;
+    const int cb = (int)(blockIdx.x - t * (unsigned)colblocks);
+    const int rb = (int)(t % (unsigned)rowblocks);
+    const int ks = (int)(t / (unsigned)rowblocks);
+    const int j0 = cb * 128;
+    const int i0 = rb * 16 * MB;
+    const int mrows = min(m - i0, 16 * MB);  // rows of this block
+    const int kbeg = ks * SPW * 64;
+
+    // Resources based at the workgroup's window, ending at each matrix's last
+    // byte (rounded up to a dword: the hardware range-checks whole dwords).
+    const int8_t *bw = B + (int64_t)kbeg * ldb + j0;
+    const int64_t b_ext = (int64_t)(k - 1 - kbeg) * ldb + (n - j0);
+    const int b_rec = (int)min((b_ext + 3) & ~(int64_t)3, (int64_t)0x7ffffff0);
+    const __amdgpu_buffer_rsrc_t Brs =
+        __builtin_amdgcn_make_buffer_rsrc((void *)bw, 0, b_rec, 0x00020000);
+    const int8_t *aw = A + (int64_t)i0 * lda + kbeg;
+    const int64_t a_ext = (int64_t)(mrows - 1) * lda + (k - kbeg);
+    const int a_rec = (int)min((a_ext + 3) & ~(int64_t)3, (int64_t)0x7ffffff0);
+    const __amdgpu_buffer_rsrc_t Ars =
+        __builtin_amdgcn_make_buffer_rsrc((void *)aw, 0, a_rec, 0x00020000);
+    const u32 ldb32 = (u32)ldb, lda32 = (u32)lda;
+
+    // ---- every load of the wave, issued up front ---------------------------
+    v2u bv[S][16];
+    v4u av[S][MB];
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        const int kl = (s * WAVES + wave) * 64;  // step's k offset in the window
+        const u32 boff = (u32)(kl + 16 * q) * ldb32 + (u32)(8 * i);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) bv[s][r] = load8<VB>(Brs, boff + (u32)r * ldb32);
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+            av[s][mb] = load16<VA>(Ars, (u32)(16 * mb + i) * lda32 + (u32)(kl + 16 * q));
+    }
+
+    // ---- transpose and multiply --------------------------------------------
+    v4i acc[MB][8];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int c = 0; c < 8; ++c) acc[mb][c] = v4i{0, 0, 0, 0};
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        // elements of A at or beyond k are zeroed
+        const int valid = k - (kbeg + (s * WAVES + wave) * 64 + 16 * q);
+        u32 amask[4];
+#pragma unroll
+        for (int d = 0; d < 4; ++d) amask[d] = byte_mask(valid - 4 * d);
+        v4i a[MB];
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+            a[mb].x = (int)(av[s][mb].x & amask[0]);
+            a[mb].y = (int)(av[s][mb].y & amask[1]);
+            a[mb].z = (int)(av[s][mb].z & amask[2]);
+            a[mb].w = (int)(av[s][mb].w & amask[3]);
+        }
+        u32 frag[8][4];
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int d = 0; d < 4; ++d)
+                transpose4x4(bv[s][4 * d][h], bv[s][4 * d + 1][h], bv[s][4 * d + 2][h],
+                             bv[s][4 * d + 3][h], frag[4 * h][d], frag[4 * h + 1][d],
+                             frag[4 * h + 2][d], frag[4 * h + 3][d]);
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            const v4i b = v4i{(int)frag[c][0], (int)frag[c][1], (int)frag[c][2], (int)frag[c][3]};
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) acc[mb][c] = Mfma<16>::mma(a[mb], b, acc[mb][c]);
+        }
+    }
+
+    // ---- sum over the waves, then into C ------------------------------------
+    // Fragment c of lane (q, i) is stored in slot 16q + (i ^ 2c) of row p of
+    // a buffer: one fragment's writes fill 64 distinct slots, and the reads
+    // below -- sixteen consecutive threads take c = 0..7 of two column groups
+    // -- hit sixteen distinct 16-byte bank groups. In two phases the upper
+    // half of the waves stores its sums first and the lower half adds its own.
+    if (!TWO || wave >= WAVES - H) {
+#pragma unroll
+        for (int p = 0; p < NP; ++p)
+            red[wave - (WAVES - H)][p][16 * q + (i ^ (2 * (p & 7)))] =
+                __builtin_bit_cast(v4u, acc[p >> 3][p & 7]);
+    }
+    __syncthreads();
+    if constexpr (TWO) {
+        if (wave < H) {
+#pragma unroll
+            for (int p = 0; p < NP; ++p) {
+                v4u &slot = red[wave][p][16 * q + (i ^ (2 * (p & 7)))];
+                slot = slot + __builtin_bit_cast(v4u, acc[p >> 3][p & 7]);
+            }
+        }
+        __syncthreads();
+    }
+    // Thread -> (fragment, lane) with the column 8i + c running fastest: each
+    // write-back instruction covers 64 consecutive columns of one row of C.
+    constexpr int NT = 64 * WAVES;
+    static_assert((NP * 64) % NT == 0, "whole passes");
+#pragma unroll
+    for (int e0 = 0; e0 < NP * 64; e0 += NT) {
+        const int e = e0 + (int)threadIdx.x;
+        const int c = e & 7, ii = (e >> 3) & 15, qq = (e >> 7) & 3, mb = e >> 9;
+        const int p = mb * 8 + c;
+        const int slot = 16 * qq + (ii ^ (2 * c));
+        v4u sum = red[0][p][slot];
+#pragma unroll
+        for (int w = 1; w < H; ++w) sum += red[w][p][slot];
+        const int col = j0 + 8 * ii + c;
+        const int row0 = 16 * mb + 4 * qq;  // output row of component 0
+        if (col < n) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                if (row0 + r < mrows) {
+                    int32_t *dst = C + (int64_t)(i0 + row0 + r) * ldc + col;
+                    if constexpr (SPLIT)
+                        atomicAdd(dst, (int)sum[r]);
+                    else
+                        *dst = (int)((u32)*dst + sum[r]);
+                }
+            }
+        }
+    }
+}
+
+template <int MB, int WAVES, int S, bool VA, bool VB>
+const void *pick_split(bool split) {
+    return split ? (const void *)igemm_stream_i8<MB, WAVES, S, VA, VB, true>
+                 : (const void *)igemm_stream_i8<MB, WAVES, S, VA, VB, false>;
+}
+
+template <int MB>
+const void *pick(int waves, int s, bool va, bool vb, bool split) {
+    if (!va || !vb) {
+        // unaligned operands: one configuration, byte loads where needed
+        if (waves != 4 || s != 1) return nullptr;
+        if (va) return pick_split<MB, 4, 1, true, false>(split);
+        if (vb) return pick_split<MB, 4, 1, false, true>(split);
+        return pick_split<MB, 4, 1, false, false>(split);
+    }
+    if (waves == 4 && s == 1) return pick_split<MB, 4, 1, true, true>(split);
+    if (waves == 8 && s == 1) return pick_split<MB, 8, 1, true, true>(split);
+    if (waves == 8 && s == 2) return pick_split<MB, 8, 2, true, true>(split);
+    if constexpr (MB == 1)
+        if (waves == 8 && s == 4) return pick_split<MB, 8, 4, true, true>(split);
+    return nullptr;
+}
+
+}  // namespace stream
+
+int launch_stream(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                  int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
+                  void *stream) {
+    const int waves = p.threads / 64;
+    const int s = (int)(p.k_chunk / kBK) / waves;
+    const bool va = p.vec_a != 0, vb = p.vec_b != 0, split = p.split > 1;
+    const void *fn = p.bm == 16 ? stream::pick<1>(waves, s, va, vb, split)
+                                : stream::pick<2>(waves, s, va, vb, split);
+    if (fn == nullptr) return IGEMM_EINVAL;
+    int mi = (int)m, ni = (int)n, ki = (int)k;
+    int cbs = (int)((n + 127) / 128), rbs = (int)((m + p.bm - 1) / p.bm);
+    void *args[] = {(void *)&A, (void *)&lda, (void *)&B, (void *)&ldb, (void *)&C,
+                    (void *)&ldc, (void *)&mi, (void *)&ni, (void *)&ki, (void *)&cbs,
+                    (void *)&rbs};
+    hipError_t e = hipLaunchKernel(fn, dim3((unsigned)p.grid), dim3((unsigned)p.threads), args, 0,
+                                   (hipStream_t)stream);
+    return e == hipSuccess ? IGEMM_OK : IGEMM_EHIP;
+}
+
+}  // namespace igemm

@@ -1,0 +1,83 @@
+"""GPU parity of the int8 streaming kernel (few rows of A, B streamed once
+into registers) against the CPU oracle, bit-exact: every workgroup shape
+(4 or 8 waves, 1, 2 or 4 k-steps each), one and two 16-row MFMA blocks,
+several row blocks, single-slice (read-add-write) and multi-slice (atomic)
+plans, k tails, misaligned operands."""
+import numpy as np
+import pytest
+
+import workloads
+from gpu_util import describe_mismatch, gpu_gemm, oracle_gemm
+
+pytestmark = pytest.mark.gpu
+
+
+def _ig():
+    import paper_2302_07594_amd as ig
+    return ig
+
+
+def _kid():
+    ig = _ig()
+    return [i for i in range(ig.igemm_num_kernels())
+            if ig.igemm_kernel_name(i) == "i8_stream_32x128"][0]
+
+
+def _check(m, n, k, split=-1, offsets=(0, 0, 0), pads=(0, 0, 0), seed=0):
+    A, B, C = workloads.random_operands("i8", m, n, k, seed=seed, lda=k + pads[0],
+                                        ldb=n + pads[1], ldc=n + pads[2])
+    _, got = gpu_gemm(A, B, C, m, n, k, kernel=_kid(), split=split, offsets=offsets)
+    want = oracle_gemm(A, B, C, m, n, k)
+    assert np.array_equal(got, want), describe_mismatch(got, want)
+    # padding columns of C are never written
+    assert np.array_equal(got[:, n:], C[:, n:])
+
+
+# k = 3000: 47 k-steps; split s asks for ceil(47 / s) steps per workgroup,
+# rounded up to 4, 8, 16 or 32 (32 only for blocks of 16 rows)
+@pytest.mark.parametrize("m", [1, 8, 16, 17, 32, 33, 70])
+@pytest.mark.parametrize("split", [1, 3, 6, 12, -1])
+def test_stream_workgroup_shapes(m, split):
+    _check(m, 1000, 3000, split=split, seed=10 * m + split + 5)
+
+
+@pytest.mark.parametrize("shape", [(5, 300, 200), (32, 129, 64), (20, 777, 17), (1, 128, 1)])
+def test_stream_single_slice(shape):
+    """k within one workgroup's range: one slice, plain read-add-write."""
+    ig = _ig()
+    m, n, k = shape
+    p = ig.igemm_query_plan(1, m, n, k, kernel=_kid())
+    assert p["split"] == 1
+    _check(m, n, k, seed=sum(shape))
+
+
+@pytest.mark.parametrize("offsets,pads", [((1, 0, 0), (0, 0, 0)), ((0, 3, 0), (0, 0, 0)),
+                                          ((0, 0, 0), (5, 3, 2)), ((2, 1, 1), (1, 7, 3))])
+def test_stream_unaligned(offsets, pads):
+    """Unaligned A rows or B rows take the byte-load variant."""
+    _check(24, 500, 700, offsets=offsets, pads=pads, seed=sum(offsets) + sum(pads))
+
+
+@pytest.mark.parametrize("value", [-128, 127])
+def test_stream_extremes_long_k(value):
+    m, n, k = 9, 300, 70000
+    A = np.full((m, k), value, np.int8)
+    B = np.full((k, n), value, np.int8)
+    C = np.zeros((m, n), np.int32)
+    _, got = gpu_gemm(A, B, C, m, n, k, kernel=_kid())
+    assert np.all(got == np.int32(value * value * k))
+
+
+@pytest.mark.parametrize("m,n", [(1, 4096), (8, 4096), (32, 4096), (1, 11008), (8, 11008),
+                                 (32, 11008)])
+def test_stream_inference_shapes(m, n):
+    """The weight-streaming shapes (k = 4096) in the launch configuration the
+    automatic plan uses."""
+    ig = _ig()
+    k = 4096
+    p = ig.igemm_query_plan(1, m, n, k)
+    assert p["kernel_name"] == "i8_stream_32x128"
+    A, B, C = workloads.random_operands("i8", m, n, k, seed=m + n)
+    _, got = gpu_gemm(A, B, C, m, n, k)
+    want = oracle_gemm(A, B, C, m, n, k)
+    assert np.array_equal(got, want), describe_mismatch(got, want)
