@@ -99,6 +99,10 @@ int igemm_i8(int64_t m, int64_t n, int64_t k,
  *            32-bit atomic adds, which are exact modulo 2^32 in any order.
  *            Values above ceil(k/64) are reduced to it. Packed kernels
  *            ignore it: they always run one launch per 32768 k elements.
+ *            The int8 streaming kernel (few rows of A, B read once) rounds
+ *            the k range of a slice up to 4, 8, 16 or 32 k-tiles of 64
+ *            (16 at most for more than 16 rows), and to 4 k-tiles for
+ *            operands whose rows are not aligned.
  * Semantics, memory and errors are those of igemm_i16 / igemm_i8.
  */
 int igemm_i16_ex(int64_t m, int64_t n, int64_t k,
@@ -125,7 +129,8 @@ typedef struct igemm_plan {
     int64_t tiles;     /* C tiles = ceil(m/bm) * ceil(n/bn)                */
     int64_t grid;      /* workgroups launched = tiles * split              */
     int threads;       /* threads per workgroup                            */
-    int vec_a, vec_b;  /* 1 if A / B rows take 16-byte vector loads        */
+    int vec_a, vec_b;  /* 1 if A / B rows take 16-byte vector loads (the  */
+                       /* streaming kernel: 8-byte loads of B)            */
     int limb_products; /* int8 MFMA products per operand pair: 4 or 1      */
     int packed;        /* 1 if operands are packed into a workspace first  */
     int64_t workspace_bytes; /* device workspace the call needs (0: none)  */
