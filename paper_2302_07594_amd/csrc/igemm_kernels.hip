@@ -42,6 +42,14 @@
 namespace igemm {
 namespace {
 
+// Value of `v` in lane (lane ^ X) within each group of 32 lanes (ds_swizzle
+// in bit-mask mode: and-mask 0x1f, or-mask 0, xor-mask X).
+template <int X>
+__device__ __forceinline__ u32 swz_xor(u32 v) {
+    static_assert(X > 0 && X < 32, "xor within 32 lanes");
+    return (u32)__builtin_amdgcn_ds_swizzle((int)v, 0x1f | (X << 10));
+}
+
 // ---------------------------------------------------------------------------
 template <int ES, int BM, int BN, int WM, int WN, int MF, bool VA, bool VB, bool SPLIT>
 __global__ void __launch_bounds__(256, 1)
@@ -70,6 +78,11 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
 
     __shared__ __attribute__((aligned(16))) char smem[NST * STAGE];
 
+    // The kernel arguments are read from memory: loaded where first used, two
+    // or three dependent round trips would open every workgroup. Naming them
+    // all here issues their loads together.
+    asm volatile("" ::"s"(Ap), "s"(lda), "s"(Bp), "s"(ldb), "s"(C), "s"(ldc), "s"(m), "s"(n),
+                 "s"(k), "s"(kchunk), "s"(tiles_m), "s"(tiles_n), "s"(gridDim.x));
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -405,44 +418,94 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     // ---- epilogue (C += result), as a function of where C comes from ----------
     // cpre: C values loaded before the k loop (short path), or none.
     int32_t cpre[SHORT ? TM : 1][SHORT ? TN : 1][SHORT ? M::REGS : 1];
+    // C is addressed through a buffer resource based at the tile's corner with
+    // 32-bit byte offsets when bm rows of C span less than 2 GiB (the usual
+    // case); elements outside m x n then get an offset beyond the resource's
+    // range, which the hardware reads as zero and does not write, so loads
+    // and stores need no branch per element. Otherwise 64-bit addresses with
+    // a branch per element.
+    const bool c_rsrc = (int64_t)BM * ldc * 4 < 0x7fff0000;
+    const __amdgpu_buffer_rsrc_t Crs =
+        __builtin_amdgcn_make_buffer_rsrc(C + (int64_t)m0 * ldc + n0, 0, 0x7fffffff, 0x00020000);
+    const int ldc32 = (int)ldc;
+    auto c_off = [&](int lr, int lc) __attribute__((always_inline)) -> u32 {
+        return (m0 + lr < m && n0 + lc < n) ? (u32)(lr * ldc32 + lc) * 4u : 0x80000000u;
+    };
     auto epilogue = [&](auto pre) __attribute__((always_inline)) {
         constexpr bool PRE = decltype(pre)::value != 0;
-        int *sRH = (int *)smem;
-        int *sRL = sRH + BM;
-        int *sKH = sRL + BM;
-        int *sKL = sKH + BN;
+        // int16 correction terms of this k range, per row and per column,
+        // parked in LDS: row i gets 32768 sum(H_A[i,:]) + 128 sum(L_A[i,:]),
+        // column j the same of B plus the constant 16384 * (k range).
+        u32 *sR = (u32 *)smem;
+        u32 *sK = sR + BM;
         if constexpr (ES == 2) {
-            for (int i = tid; i < 2 * (BM + BN); i += 256) sRH[i] = 0;
-            __syncthreads();
+            // The eight 16-byte chunks of one row of A were staged by eight
+            // consecutive lanes: a butterfly over them gives the row total.
 #pragma unroll
             for (int s = 0; s < ACT; ++s) {
-                if (!a_dup[s]) {
-                    atomicAdd(&sRH[a_row[s]], sah[s]);
-                    atomicAdd(&sRL[a_row[s]], sal[s]);
-                }
+                u32 v = 32768u * (u32)sah[s] + 128u * (u32)sal[s];
+                v += swz_xor<1>(v);
+                v += swz_xor<2>(v);
+                v += swz_xor<4>(v);
+                if (!a_dup[s] && a_q[s] == 0) sR[a_row[s]] = v;
             }
+            // Sixteen consecutive lanes staged four rows each of the same
+            // eight columns of B: a reduce-scatter over them (halving the
+            // columns held at each exchange) leaves each even lane with the
+            // total of one column.
+            const u32 kconst = 16384u * (u32)(kend - kbeg);
+            const bool h8 = (lane & 8) != 0, h4 = (lane & 4) != 0, h2 = (lane & 2) != 0;
 #pragma unroll
             for (int s = 0; s < BUT; ++s) {
-                if (!b_dup[s]) {
+                u32 v8[8], v4[4], v2[2];
 #pragma unroll
-                    for (int c = 0; c < 8; ++c) {
-                        atomicAdd(&sKH[b_cc[s] * 8 + c], sbh[s][c]);
-                        atomicAdd(&sKL[b_cc[s] * 8 + c], sbl[s][c]);
-                    }
-                }
+                for (int c = 0; c < 8; ++c) v8[c] = 32768u * (u32)sbh[s][c] + 128u * (u32)sbl[s][c];
+#pragma unroll
+                for (int c = 0; c < 4; ++c)
+                    v4[c] = (h8 ? v8[c + 4] : v8[c]) + swz_xor<8>(h8 ? v8[c] : v8[c + 4]);
+#pragma unroll
+                for (int c = 0; c < 2; ++c)
+                    v2[c] = (h4 ? v4[c + 2] : v4[c]) + swz_xor<4>(h4 ? v4[c] : v4[c + 2]);
+                u32 v1 = (h2 ? v2[1] : v2[0]) + swz_xor<2>(h2 ? v2[0] : v2[1]);
+                v1 += swz_xor<1>(v1);
+                const int c = (h8 ? 4 : 0) + (h4 ? 2 : 0) + (h2 ? 1 : 0);
+                if (!b_dup[s] && (lane & 1) == 0) sK[b_cc[s] * 8 + c] = v1 + kconst;
             }
             __syncthreads();
         }
-        const u32 kconst = 16384u * (u32)(kend - kbeg);
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
+            // row terms of this lane's REGS output rows of block i (groups of
+            // four consecutive rows)
+            u32 rowt[M::REGS];
+            if constexpr (ES == 2) {
+#pragma unroll
+                for (int r = 0; r < M::REGS; r += 4) {
+                    const uint4 q = *(const uint4 *)(sR + wm0 + MF * i + M::out_row(lane, r));
+                    rowt[r] = q.x;
+                    rowt[r + 1] = q.y;
+                    rowt[r + 2] = q.z;
+                    rowt[r + 3] = q.w;
+                }
+            }
+            int32_t cl[TN][M::REGS];
+            if constexpr (!PRE && !SPLIT) {
+                if (c_rsrc) {
+#pragma unroll
+                    for (int j = 0; j < TN; ++j) {
+                        const int lc = wn0 + MF * j + M::out_col(lane);
+#pragma unroll
+                        for (int r = 0; r < M::REGS; ++r)
+                            cl[j][r] = __builtin_amdgcn_raw_buffer_load_b32(
+                                Crs, c_off(wm0 + MF * i + M::out_row(lane, r), lc), 0, 0);
+                    }
+                }
+            }
 #pragma unroll
             for (int j = 0; j < TN; ++j) {
                 const int lc = wn0 + MF * j + M::out_col(lane);
                 const int gc = n0 + lc;
-                u32 colterm = 0;
-                if constexpr (ES == 2)
-                    colterm = 32768u * (u32)sKH[lc] + 128u * (u32)sKL[lc] + kconst;
+                const u32 colt = ES == 2 ? sK[lc] : 0u;
 #pragma unroll
                 for (int r = 0; r < M::REGS; ++r) {
                     const int lr = wm0 + MF * i + M::out_row(lane, r);
@@ -452,17 +515,18 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
                         v = (u32)acc[0][i][j][r];
                     } else {
                         v = 65536u * (u32)acc[0][i][j][r] + 256u * (u32)acc[1][i][j][r] +
-                            (u32)acc[2][i][j][r] + 32768u * (u32)sRH[lr] + 128u * (u32)sRL[lr] +
-                            colterm;
+                            (u32)acc[2][i][j][r] + rowt[r] + colt;
                     }
-                    if (gr < m && gc < n) {
+                    if constexpr (SPLIT) {
+                        if (gr < m && gc < n) atomicAdd(C + (int64_t)gr * ldc + gc, (int)v);
+                    } else if (c_rsrc) {
+                        const u32 old = PRE ? (u32)cpre[i][j][r] : (u32)cl[j][r];
+                        __builtin_amdgcn_raw_buffer_store_b32((int)(old + v), Crs, c_off(lr, lc), 0,
+                                                              0);
+                    } else if (gr < m && gc < n) {
                         int32_t *cp = C + (int64_t)gr * ldc + gc;
-                        if constexpr (SPLIT)
-                            atomicAdd(cp, (int)v);
-                        else if constexpr (PRE)
-                            *cp = (int32_t)((u32)cpre[i][j][r] + v);
-                        else
-                            *cp = (int32_t)((u32)*cp + v);
+                        const u32 old = PRE ? (u32)cpre[i][j][r] : (u32)*cp;
+                        *cp = (int32_t)(old + v);
                     }
                 }
             }
@@ -477,14 +541,11 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     // round trip per tile would dominate. Here every tile of the range is
     // loaded at once with branch-free range-checked loads (a branch per load
     // would make the compiler wait for each load before issuing the next), C
-    // is fetched at the same time (addresses clamped into the matrix), and
-    // one barrier precedes all the MFMAs.
+    // is fetched at the same time, and one barrier precedes all the MFMAs.
     if constexpr (SHORT) {
         const int nkt = (kend - kbeg + 63) >> 6;
         // Buffer resources at the corner of this workgroup's A rows and B
-        // columns (from kbeg), with 32-bit lane offsets (an element offset
-        // past the range also reads zero, so element loads of misaligned
-        // rows follow the same rule). Rows of A beyond m,
+        // columns (from kbeg), with 32-bit lane offsets. Rows of A beyond m,
         // k-tiles beyond kend and rows of B beyond kend get an offset past the
         // resource's range, which the hardware returns as zero (per dword), so
         // the loads need no branches; the range ends at the matrix's last byte
@@ -496,45 +557,37 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
             const char *b_base = (const char *)Bp + ((int64_t)kbeg * ldb + n0) * ES;
             const int64_t a_ext = ((int64_t)(m - 1 - m0) * lda + (k - kbeg)) * ES;
             const int64_t b_ext = ((int64_t)(k - 1 - kbeg) * ldb + (n - n0)) * ES;
-            const int a_rec = (int)min((a_ext + 3) & ~(int64_t)3, (int64_t)0x7ffffff0);
-            const int b_rec = (int)min((b_ext + 3) & ~(int64_t)3, (int64_t)0x7ffffff0);
+            // Rows that are not 16-byte aligned are read with dword-aligned
+            // loads from a dword-aligned resource base and shifted into place
+            // (v_alignbyte), five dwords per 16 bytes.
+            const u32 a_dl = (u32)((uintptr_t)a_base & 3), b_dl = (u32)((uintptr_t)b_base & 3);
+            const int a_rec = (int)min((a_ext + a_dl + 3) & ~(int64_t)3, (int64_t)0x7ffffff0);
+            const int b_rec = (int)min((b_ext + b_dl + 3) & ~(int64_t)3, (int64_t)0x7ffffff0);
             const __amdgpu_buffer_rsrc_t Ars =
-                __builtin_amdgcn_make_buffer_rsrc((void *)a_base, 0, a_rec, 0x00020000);
+                __builtin_amdgcn_make_buffer_rsrc((void *)(a_base - a_dl), 0, a_rec, 0x00020000);
             const __amdgpu_buffer_rsrc_t Brs =
-                __builtin_amdgcn_make_buffer_rsrc((void *)b_base, 0, b_rec, 0x00020000);
+                __builtin_amdgcn_make_buffer_rsrc((void *)(b_base - b_dl), 0, b_rec, 0x00020000);
             const int klen = kend - kbeg;
             const int lda_b = (int)(lda * ES), ldb_b = (int)(ldb * ES);
-            // 16 bytes at byte offset `off` of a resource: one vector load when
-            // rows are 16-byte aligned (VEC), else one load per element (rows
-            // of any alignment), every load unconditional.
-            auto load16_rs = [&](auto vec, __amdgpu_buffer_rsrc_t rs, u32 off)
+            // 16 bytes at byte offset `off` (from the unaligned base; dl is the
+            // base's misalignment), every load unconditional: one vector load
+            // when rows are 16-byte aligned (VEC, dl = 0), else an aligned
+            // 16-byte and 4-byte load and a byte shift. The out-of-range
+            // offset 0x80000000 stays out of range after adding dl and 16.
+            auto load16_rs = [&](auto vec, __amdgpu_buffer_rsrc_t rs, u32 off, u32 dl)
                                  __attribute__((always_inline)) -> v4i {
                 if constexpr (decltype(vec)::value != 0) {
                     return __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
                 } else {
-                    u32 w[4];
-#pragma unroll
-                    for (int d = 0; d < 4; ++d) {
-                        if constexpr (ES == 2) {
-                            const u32 lo = __builtin_amdgcn_raw_buffer_load_b16(rs, off + 4 * d, 0, 0);
-                            const u32 hi =
-                                __builtin_amdgcn_raw_buffer_load_b16(rs, off + 4 * d + 2, 0, 0);
-                            w[d] = lo | (hi << 16);
-                        } else {
-                            u32 x = 0;
-#pragma unroll
-                            for (int b = 0; b < 4; ++b)
-                                x |= (u32)__builtin_amdgcn_raw_buffer_load_b8(rs, off + 4 * d + b,
-                                                                             0, 0)
-                                     << (8 * b);
-                            w[d] = x;
-                        }
-                    }
+                    const u32 o = off + dl;
+                    const u32 oa = o & ~3u, sh = o & 3u;
+                    const v4i lo = __builtin_amdgcn_raw_buffer_load_b128(rs, oa, 0, 0);
+                    const u32 hi = (u32)__builtin_amdgcn_raw_buffer_load_b32(rs, oa + 16, 0, 0);
                     v4i v;
-                    v.x = (int)w[0];
-                    v.y = (int)w[1];
-                    v.z = (int)w[2];
-                    v.w = (int)w[3];
+                    v.x = (int)__builtin_amdgcn_alignbyte((u32)lo.y, (u32)lo.x, sh);
+                    v.y = (int)__builtin_amdgcn_alignbyte((u32)lo.z, (u32)lo.y, sh);
+                    v.z = (int)__builtin_amdgcn_alignbyte((u32)lo.w, (u32)lo.z, sh);
+                    v.w = (int)__builtin_amdgcn_alignbyte(hi, (u32)lo.w, sh);
                     return v;
                 }
             };
@@ -548,7 +601,7 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
                     const u32 off = (m0 + a_row[s] < m && valid > 0)
                                         ? (u32)(a_row[s] * lda_b + e * ES)
                                         : 0x80000000u;
-                    ra[R][s] = load16_rs(ic<VA>{}, Ars, off);
+                    ra[R][s] = load16_rs(ic<VA>{}, Ars, off, a_dl);
                 }
 #pragma unroll
                 for (int s = 0; s < BUT; ++s) {
@@ -557,7 +610,7 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
                         const int p = T * 64 + 4 * b_rg[s] + r;  // row of B, from kbeg
                         const u32 off = p < klen ? (u32)(p * ldb_b + b_cc[s] * CPU * ES)
                                                  : 0x80000000u;
-                        rb[R][s][r] = load16_rs(ic<VB>{}, Brs, off);
+                        rb[R][s][r] = load16_rs(ic<VB>{}, Brs, off, b_dl);
                     }
                 }
             };
@@ -566,18 +619,25 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
                 for (int i = 0; i < TM; ++i)
 #pragma unroll
                     for (int j = 0; j < TN; ++j) {
-                        const int gc = min(n0 + wn0 + MF * j + M::out_col(lane), n - 1);
+                        const int lc = wn0 + MF * j + M::out_col(lane);
 #pragma unroll
                         for (int r = 0; r < M::REGS; ++r) {
-                            const int gr = min(m0 + wm0 + MF * i + M::out_row(lane, r), m - 1);
-                            cpre[i][j][r] = C[(int64_t)gr * ldc + gc];
+                            const int lr = wm0 + MF * i + M::out_row(lane, r);
+                            if (c_rsrc) {
+                                cpre[i][j][r] =
+                                    __builtin_amdgcn_raw_buffer_load_b32(Crs, c_off(lr, lc), 0, 0);
+                            } else {
+                                const int gr = min(m0 + lr, m - 1), gc = min(n0 + lc, n - 1);
+                                cpre[i][j][r] = C[(int64_t)gr * ldc + gc];
+                            }
                         }
                     }
             }
+            // Only the k-tiles of the range (nkt is uniform over the workgroup).
             load_short(ic<0>{}, ic<0>{});
-            load_short(ic<1>{}, ic<1>{});
-            load_short(ic<2>{}, ic<2>{});
-            load_short(ic<3>{}, ic<3>{});
+            if (nkt > 1) load_short(ic<1>{}, ic<1>{});
+            if (nkt > 2) load_short(ic<2>{}, ic<2>{});
+            if (nkt > 3) load_short(ic<3>{}, ic<3>{});
             __builtin_amdgcn_sched_barrier(0);  // every load goes out before the first wait
             // Elements of A at or beyond kend (the next k slice) count as zero.
             auto mask_short = [&](auto par, auto tile) __attribute__((always_inline)) {
@@ -592,13 +652,19 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
                 }
             };
             mask_short(ic<0>{}, ic<0>{});
-            mask_short(ic<1>{}, ic<1>{});
-            mask_short(ic<2>{}, ic<2>{});
-            mask_short(ic<3>{}, ic<3>{});
             store_tile(ic<0>{}, ic<0>{}, ic<1>{}, kbeg);
-            store_tile(ic<1>{}, ic<1>{}, ic<1>{}, kbeg + 64);
-            store_tile(ic<2>{}, ic<2>{}, ic<1>{}, kbeg + 128);
-            store_tile(ic<3>{}, ic<3>{}, ic<1>{}, kbeg + 192);
+            if (nkt > 1) {
+                mask_short(ic<1>{}, ic<1>{});
+                store_tile(ic<1>{}, ic<1>{}, ic<1>{}, kbeg + 64);
+            }
+            if (nkt > 2) {
+                mask_short(ic<2>{}, ic<2>{});
+                store_tile(ic<2>{}, ic<2>{}, ic<1>{}, kbeg + 128);
+            }
+            if (nkt > 3) {
+                mask_short(ic<3>{}, ic<3>{});
+                store_tile(ic<3>{}, ic<3>{}, ic<1>{}, kbeg + 192);
+            }
             __syncthreads();
             auto tile_mfmas = [&](auto buf) __attribute__((always_inline)) {
                 read_frags(ic<0>{}, buf, ic<0>{});

@@ -93,6 +93,11 @@ igemm_stream_i8(const int8_t *__restrict__ A, int64_t lda, const int8_t *__restr
     constexpr int H = TWO ? WAVES / 2 : WAVES;  // LDS buffers
     __shared__ v4u red[H][NP][64];
 
+    // Fetch every kernel argument at once (each load where first used would
+    // cost a memory round trip of its own).
+    asm volatile("" ::"s"(A), "s"(lda), "s"(B), "s"(ldb), "s"(C), "s"(ldc), "s"(m), "s"(n),
+                 "s"(k), "s"(colblocks), "s"(rowblocks));
+
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int q = lane >> 4;  // k chunk of the MFMA fragments
