@@ -8,8 +8,9 @@
 namespace igemm {
 
 // One kernel family: operand size, workgroup tile of C and the tile of C
-// each of the four waves owns. Packed kernels multiply operands that a pack
-// step has first rearranged into a workspace.
+// each wave owns (four waves per workgroup; eight for i8_packed_256x256).
+// Packed kernels multiply operands that a pack step has first rearranged
+// into a workspace.
 struct KernelDesc {
     const char *name;
     int es;      // operand bytes: 2 = int16 (two int8 limb planes), 1 = int8

@@ -195,7 +195,7 @@ pack_b(const void *__restrict__ Bv, int64_t ldb, int k, int n, int k_pad, int ks
 // the number of LDS stages of the DMA ring (4, or 3 for tiles whose stage
 // is too large for four).
 template <int ES, int BM, int BN, int WM, int WN, int NST>
-__global__ void __launch_bounds__(256, 1)
+__global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64, 1)
 igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
              const int8_t *__restrict__ Bp, int64_t ldb_p, int64_t b_plane,
              const uint32_t *__restrict__ corrA, const uint32_t *__restrict__ corrB,
@@ -208,7 +208,10 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     constexpr int NACC = ES == 2 ? 3 : 1;
     constexpr int TM = WM / MF, TN = WN / MF;
     constexpr int WGN = BN / WN;
-    static_assert((BM / WM) * WGN == 4, "four waves per workgroup");
+    // Four waves (one per SIMD), or eight (two per SIMD, at most 256
+    // registers each, so that one wave's waits are covered by the other).
+    constexpr int NW = (BM / WM) * WGN;
+    static_assert(NW == 4 || NW == 8, "four or eight waves per workgroup");
     static_assert(NST == 3 || NST == 4, "three or four LDS stages");
     constexpr int APL = BM * 64, BPL = BN * 64;
     constexpr int STAGE = P * (APL + BPL);
@@ -216,8 +219,8 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     // 1 KB DMA blocks per stage: NBA hold the A planes, NBB the B planes;
     // each wave moves DPA of the A blocks and DPB of the B blocks.
     constexpr int NBA = P * BM / 16, NBB = P * BN / 16;
-    static_assert(NBA % 4 == 0 && NBB % 4 == 0, "DMA blocks per wave");
-    constexpr int DPA = NBA / 4, DPB = NBB / 4, DPW = DPA + DPB;
+    static_assert(NBA % NW == 0 && NBB % NW == 0, "DMA blocks per wave");
+    constexpr int DPA = NBA / NW, DPB = NBB / NW, DPW = DPA + DPB;
     static_assert(DPW <= 15, "outstanding DMA count fits s_waitcnt");
 
     // The LDS stages as separate objects, so that the compiler can tell the
@@ -488,8 +491,8 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     // (All workgroups of a round reach this point together; one round trip
     // per block would leave the matrix cores idle for many microseconds.)
     constexpr int NOUT = TM * TN;
-    constexpr int NB = NOUT <= 4 ? NOUT : 2;  // 2 x 2 x 16 C values in flight keeps
-                                              // the 256x256 kernel out of scratch
+    // Eight waves (256 registers each) keep one block per batch.
+    constexpr int NB = NW == 8 ? 1 : (NOUT <= 4 ? NOUT : 2);
     constexpr int NBATCH = NOUT / NB;
     static_assert(NOUT % NB == 0 && NBATCH <= 8, "epilogue batches");
     int32_t cv[2][NB][M::REGS];
@@ -647,7 +650,7 @@ int launch_multiply(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k
                 Asrc + k0, lda_p, a_plane, Bpk + k0, L.k_pad, b_plane, cA, corrB, kc16, C, ldc,
                 mi, ni, ktiles, tm, tn);
         else
-            igemm_packed<1, 256, 256, 128, 128, 4><<<grid, 256, 0, stream>>>(
+            igemm_packed<1, 256, 256, 64, 128, 4><<<grid, 512, 0, stream>>>(
                 Asrc + k0, lda_p, 0, Bpk + k0, L.k_pad, 0, nullptr, nullptr, 0u, C, ldc, mi, ni,
                 ktiles, tm, tn);
         if (hipGetLastError() != hipSuccess) return IGEMM_EHIP;

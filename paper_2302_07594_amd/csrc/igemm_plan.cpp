@@ -24,7 +24,7 @@ const KernelDesc kKernels[K_COUNT] = {
     {"i16_64x64", 2, 64, 64, 32, 32, false},
     {"i16_32x128", 2, 32, 128, 32, 32, false},
     {"i16_16x128", 2, 16, 128, 16, 32, false},
-    {"i8_packed_256x256", 1, 256, 256, 128, 128, true},
+    {"i8_packed_256x256", 1, 256, 256, 64, 128, true},
     {"i16_packed_128x128", 2, 128, 128, 64, 64, true},
     {"i8_stream_32x128", 1, 32, 128, 16, 128, false},
 };
@@ -212,6 +212,7 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
         out->kernel = id;
         out->bm = d.bm;
         out->bn = d.bn;
+        out->threads = (d.bm / d.wm) * (d.bn / d.wn) * 64;
         out->k_chunk = L.k_pad < kMaxKChunk ? L.k_pad : kMaxKChunk;
         out->split = (int)cdiv(L.k_pad, out->k_chunk);
         out->tiles = tiles;
