@@ -19,7 +19,9 @@ Prints ONE JSON line. Besides the headline value it carries:
                 of the same workload;
   per_config    every other workload, each timed the same way (memory-bound
                 ones rotate through enough buffer sets to defeat the 256 MB
-                last-level cache), with its own roofline fraction.
+                last-level cache), with its own roofline fraction; the last
+                entry is the paper's own GEMM shape (4096, 4096, 290), for
+                context.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-extra]
                        [--no-cpu-baseline] [--cpu-seconds S]
@@ -271,7 +273,7 @@ def main():
     torch.cuda.empty_cache()
     if not args.no_extra:
         per = []
-        for wname in ("i16_256", "i8_8192", "i16_conv", "i8_skinny"):
+        for wname in ("i16_256", "i8_8192", "i16_conv", "i8_skinny", "i16_paper"):
             for c in workloads.WORKLOADS[wname].cases:
                 log(f"bench: per-config {c.name}")
                 per.append(bench_case(c))

@@ -51,8 +51,10 @@ __device__ __forceinline__ u32 swz_xor(u32 v) {
 }
 
 // ---------------------------------------------------------------------------
+// Small tiles (bm * bn <= 8192, LDS <= 64 KB) are held to 256 registers per
+// lane so that two workgroups share a compute unit; larger tiles take one.
 template <int ES, int BM, int BN, int WM, int WN, int MF, bool VA, bool VB, bool SPLIT>
-__global__ void __launch_bounds__(256, 1)
+__global__ void __launch_bounds__(256, BM * BN <= 32 * 256 ? 2 : 1)
 igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ Bp,
             int64_t ldb, int32_t *__restrict__ C, int64_t ldc, int m, int n, int k,
             int kchunk, int tiles_m, int tiles_n) {
@@ -242,6 +244,77 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
         }
     };
 
+    // ---- range-checked loads through buffer resources ---------------------------
+    // Buffer resources at the corner of this workgroup's A rows and B columns
+    // (from kbeg), with 32-bit lane offsets. Rows of A beyond m, elements
+    // beyond kend and rows of B beyond kend get an offset past the resource's
+    // range, which the hardware returns as zero (per dword), so the loads need
+    // no branches; the range ends at the matrix's last byte (rounded up to a
+    // dword), so no load reaches past the allocation. Columns of B beyond n
+    // only feed outputs beyond n, which are never stored. Used whenever the
+    // workgroup's windows span less than 2 GiB.
+    const int klen = kend - kbeg;
+    const int64_t a_span = (int64_t)BM * lda * ES + (int64_t)klen * ES + 64;
+    const int64_t b_span = (int64_t)(klen + 1) * ldb * ES + BN * ES + 64;
+    const bool rs_ok = a_span < 0x7fff0000 && b_span < 0x7fff0000;
+    const char *a_base = (const char *)Ap + ((int64_t)m0 * lda + kbeg) * ES;
+    const char *b_base = (const char *)Bp + ((int64_t)kbeg * ldb + n0) * ES;
+    const int64_t a_ext = ((int64_t)(m - 1 - m0) * lda + (k - kbeg)) * ES;
+    const int64_t b_ext = ((int64_t)(k - 1 - kbeg) * ldb + (n - n0)) * ES;
+    // Rows that are not 16-byte aligned are read with dword-aligned loads
+    // from a dword-aligned resource base and shifted into place
+    // (v_alignbyte), five dwords per 16 bytes.
+    const u32 a_dl = (u32)((uintptr_t)a_base & 3), b_dl = (u32)((uintptr_t)b_base & 3);
+    const int a_rec = (int)min((a_ext + a_dl + 3) & ~(int64_t)3, (int64_t)0x7ffffff0);
+    const int b_rec = (int)min((b_ext + b_dl + 3) & ~(int64_t)3, (int64_t)0x7ffffff0);
+    const __amdgpu_buffer_rsrc_t Ars =
+        __builtin_amdgcn_make_buffer_rsrc((void *)(a_base - a_dl), 0, a_rec, 0x00020000);
+    const __amdgpu_buffer_rsrc_t Brs =
+        __builtin_amdgcn_make_buffer_rsrc((void *)(b_base - b_dl), 0, b_rec, 0x00020000);
+    const int lda_b = (int)(lda * ES), ldb_b = (int)(ldb * ES);
+    // 16 bytes at byte offset `off` (from the unaligned base; dl is the base's
+    // misalignment), every load unconditional: one vector load when rows are
+    // 16-byte aligned (VEC, dl = 0), else an aligned 16-byte and 4-byte load
+    // and a byte shift. The out-of-range offset 0x80000000 stays out of range
+    // after adding dl and 16.
+    auto load16_rs = [&](auto vec, __amdgpu_buffer_rsrc_t rs, u32 off, u32 dl)
+                         __attribute__((always_inline)) -> v4i {
+        if constexpr (decltype(vec)::value != 0) {
+            return __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
+        } else {
+            const u32 o = off + dl;
+            const u32 oa = o & ~3u, sh = o & 3u;
+            const v4i lo = __builtin_amdgcn_raw_buffer_load_b128(rs, oa, 0, 0);
+            const u32 hi = (u32)__builtin_amdgcn_raw_buffer_load_b32(rs, oa + 16, 0, 0);
+            v4i v;
+            v.x = (int)__builtin_amdgcn_alignbyte((u32)lo.y, (u32)lo.x, sh);
+            v.y = (int)__builtin_amdgcn_alignbyte((u32)lo.z, (u32)lo.y, sh);
+            v.z = (int)__builtin_amdgcn_alignbyte((u32)lo.w, (u32)lo.z, sh);
+            v.w = (int)__builtin_amdgcn_alignbyte(hi, (u32)lo.w, sh);
+            return v;
+        }
+    };
+    // The k-tile starting kt0 elements after kbeg into register set R.
+    auto load_rs = [&](auto par, int kt0) __attribute__((always_inline)) {
+        constexpr int R = decltype(par)::value;
+#pragma unroll
+        for (int s = 0; s < ACT; ++s) {
+            const int e = kt0 + a_q[s] * (16 / ES);  // first element, from kbeg
+            const u32 off = (m0 + a_row[s] < m && e < klen) ? (u32)(a_row[s] * lda_b + e * ES)
+                                                           : 0x80000000u;
+            ra[R][s] = load16_rs(ic<VA>{}, Ars, off, a_dl);
+        }
+#pragma unroll
+        for (int s = 0; s < BUT; ++s) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int p = kt0 + 4 * b_rg[s] + r;  // row of B, from kbeg
+                const u32 off = p < klen ? (u32)(p * ldb_b + b_cc[s] * CPU * ES) : 0x80000000u;
+                rb[R][s][r] = load16_rs(ic<VB>{}, Brs, off, b_dl);
+            }
+        }
+    };
+
     // ---- registers -> LDS (limb split, B transpose, limb sums) --------------
     // MASK: zero the limbs of elements at or beyond kend (last k-tile only).
     auto store_tile = [&](auto par, auto buf, auto mask, int k0) __attribute__((always_inline)) {
@@ -360,7 +433,15 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     // tile kt while reading the next sub-step's fragments (the last one from
     // stage S+1, already complete), writes tile kt+2 into stage S+2, and ends
     // with one barrier.
-    auto step = [&](auto phase, auto do_load, auto do_store, auto do_pref, int kt) __attribute__((always_inline)) {
+    // Pipeline loads (through the buffer resources; the plain vector loads
+    // remain available for interior workgroups with aligned rows).
+    auto load_p = [&](auto use_rs, auto par, int k0) __attribute__((always_inline)) {
+        if constexpr (decltype(use_rs)::value != 0)
+            load_rs(par, k0 - kbeg);
+        else
+            load_fast(par, k0);
+    };
+    auto step = [&](auto phase, auto do_load, auto do_store, auto do_pref, int kt, auto use_rs) __attribute__((always_inline)) {
         constexpr int S = decltype(phase)::value;
         if constexpr (M::KSTEPS == 2) {
             constexpr int NM = TM * TN * (ES == 2 ? 4 : 1);  // MFMAs per sub-step
@@ -371,7 +452,7 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
             constexpr int DSW = ES == 2 ? (2 * ACT + 16 * BUT) : (ACT + 16 * BUT);
             // sub-step 0 on slot 0 while sub-step 1 loads into slot 1 and the
             // global loads of tile kt+3 go out
-            if (decltype(do_load)::value) load_fast(ic<(S + 1) & 1>{}, kbeg + (kt + 3) * 64);
+            if (decltype(do_load)::value) load_p(use_rs, ic<(S + 1) & 1>{}, kbeg + (kt + 3) * 64);
             read_frags(ic<1>{}, ic<S>{}, ic<1>{});
             mfmas(ic<0>{});
             interleave<NM, NR, decltype(do_load)::value ? NV : 0, 0, 0>();
@@ -387,7 +468,7 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
                        decltype(do_store)::value ? (DSW + NM - 1) / NM : 0>();
             __builtin_amdgcn_sched_barrier(0);
         } else {
-            if (decltype(do_load)::value) load_fast(ic<(S + 1) & 1>{}, kbeg + (kt + 3) * 64);
+            if (decltype(do_load)::value) load_p(use_rs, ic<(S + 1) & 1>{}, kbeg + (kt + 3) * 64);
             // one sub-step per tile; tiles alternate between the slots
             constexpr int SL = S & 1;
             if (decltype(do_store)::value)
@@ -398,9 +479,12 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
         __syncthreads();
     };
 
-    // One unpipelined k-tile through LDS stage 0 with bounds checks.
+    // One unpipelined k-tile through LDS stage 0, loads range-checked.
     auto safe_tile = [&](int k0) __attribute__((always_inline)) {
-        load_safe(ic<0>{}, k0);
+        if (rs_ok)
+            load_rs(ic<0>{}, k0 - kbeg);
+        else
+            load_safe(ic<0>{}, k0);
         if (k0 + 64 > kend)
             store_tile(ic<0>{}, ic<0>{}, ic<1>{}, k0);
         else
@@ -535,6 +619,29 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
         }
     };
 
+    // C of this workgroup's tile into cpre (short path), to be consumed by the
+    // epilogue: issued before the first operand loads, its round trip
+    // overlaps theirs.
+    auto prefetch_c = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int lc = wn0 + MF * j + M::out_col(lane);
+#pragma unroll
+                for (int r = 0; r < M::REGS; ++r) {
+                    const int lr = wm0 + MF * i + M::out_row(lane, r);
+                    if (c_rsrc) {
+                        cpre[i][j][r] =
+                            __builtin_amdgcn_raw_buffer_load_b32(Crs, c_off(lr, lc), 0, 0);
+                    } else {
+                        const int gr = min(m0 + lr, m - 1), gc = min(n0 + lc, n - 1);
+                        cpre[i][j][r] = C[(int64_t)gr * ldc + gc];
+                    }
+                }
+            }
+    };
+
     // ---- short path: a k range of at most NST k-tiles -------------------------
     // Small products (skinny, convolution-shaped, small cubes) give each
     // workgroup only a few k-tiles, too few to fill a pipeline: one global
@@ -544,100 +651,13 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     // is fetched at the same time, and one barrier precedes all the MFMAs.
     if constexpr (SHORT) {
         const int nkt = (kend - kbeg + 63) >> 6;
-        // Buffer resources at the corner of this workgroup's A rows and B
-        // columns (from kbeg), with 32-bit lane offsets. Rows of A beyond m,
-        // k-tiles beyond kend and rows of B beyond kend get an offset past the
-        // resource's range, which the hardware returns as zero (per dword), so
-        // the loads need no branches; the range ends at the matrix's last byte
-        // (rounded up to a dword), so no load reaches past the allocation.
-        const int64_t a_span = (int64_t)BM * lda * ES + 256 * ES;
-        const int64_t b_span = (int64_t)256 * ldb * ES + BN * ES;
-        if (nkt <= NST && a_span < 0x7ffffff0 && b_span < 0x7ffffff0) {
-            const char *a_base = (const char *)Ap + ((int64_t)m0 * lda + kbeg) * ES;
-            const char *b_base = (const char *)Bp + ((int64_t)kbeg * ldb + n0) * ES;
-            const int64_t a_ext = ((int64_t)(m - 1 - m0) * lda + (k - kbeg)) * ES;
-            const int64_t b_ext = ((int64_t)(k - 1 - kbeg) * ldb + (n - n0)) * ES;
-            // Rows that are not 16-byte aligned are read with dword-aligned
-            // loads from a dword-aligned resource base and shifted into place
-            // (v_alignbyte), five dwords per 16 bytes.
-            const u32 a_dl = (u32)((uintptr_t)a_base & 3), b_dl = (u32)((uintptr_t)b_base & 3);
-            const int a_rec = (int)min((a_ext + a_dl + 3) & ~(int64_t)3, (int64_t)0x7ffffff0);
-            const int b_rec = (int)min((b_ext + b_dl + 3) & ~(int64_t)3, (int64_t)0x7ffffff0);
-            const __amdgpu_buffer_rsrc_t Ars =
-                __builtin_amdgcn_make_buffer_rsrc((void *)(a_base - a_dl), 0, a_rec, 0x00020000);
-            const __amdgpu_buffer_rsrc_t Brs =
-                __builtin_amdgcn_make_buffer_rsrc((void *)(b_base - b_dl), 0, b_rec, 0x00020000);
-            const int klen = kend - kbeg;
-            const int lda_b = (int)(lda * ES), ldb_b = (int)(ldb * ES);
-            // 16 bytes at byte offset `off` (from the unaligned base; dl is the
-            // base's misalignment), every load unconditional: one vector load
-            // when rows are 16-byte aligned (VEC, dl = 0), else an aligned
-            // 16-byte and 4-byte load and a byte shift. The out-of-range
-            // offset 0x80000000 stays out of range after adding dl and 16.
-            auto load16_rs = [&](auto vec, __amdgpu_buffer_rsrc_t rs, u32 off, u32 dl)
-                                 __attribute__((always_inline)) -> v4i {
-                if constexpr (decltype(vec)::value != 0) {
-                    return __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
-                } else {
-                    const u32 o = off + dl;
-                    const u32 oa = o & ~3u, sh = o & 3u;
-                    const v4i lo = __builtin_amdgcn_raw_buffer_load_b128(rs, oa, 0, 0);
-                    const u32 hi = (u32)__builtin_amdgcn_raw_buffer_load_b32(rs, oa + 16, 0, 0);
-                    v4i v;
-                    v.x = (int)__builtin_amdgcn_alignbyte((u32)lo.y, (u32)lo.x, sh);
-                    v.y = (int)__builtin_amdgcn_alignbyte((u32)lo.z, (u32)lo.y, sh);
-                    v.z = (int)__builtin_amdgcn_alignbyte((u32)lo.w, (u32)lo.z, sh);
-                    v.w = (int)__builtin_amdgcn_alignbyte(hi, (u32)lo.w, sh);
-                    return v;
-                }
-            };
-            // k-tile t of the range into register set R
-            auto load_short = [&](auto par, auto tile) __attribute__((always_inline)) {
-                constexpr int R = decltype(par)::value, T = decltype(tile)::value;
-#pragma unroll
-                for (int s = 0; s < ACT; ++s) {
-                    const int e = T * 64 + a_q[s] * (16 / ES);  // first element, from kbeg
-                    const int valid = klen - e;                 // elements before kend
-                    const u32 off = (m0 + a_row[s] < m && valid > 0)
-                                        ? (u32)(a_row[s] * lda_b + e * ES)
-                                        : 0x80000000u;
-                    ra[R][s] = load16_rs(ic<VA>{}, Ars, off, a_dl);
-                }
-#pragma unroll
-                for (int s = 0; s < BUT; ++s) {
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int p = T * 64 + 4 * b_rg[s] + r;  // row of B, from kbeg
-                        const u32 off = p < klen ? (u32)(p * ldb_b + b_cc[s] * CPU * ES)
-                                                 : 0x80000000u;
-                        rb[R][s][r] = load16_rs(ic<VB>{}, Brs, off, b_dl);
-                    }
-                }
-            };
-            if constexpr (!SPLIT) {
-#pragma unroll
-                for (int i = 0; i < TM; ++i)
-#pragma unroll
-                    for (int j = 0; j < TN; ++j) {
-                        const int lc = wn0 + MF * j + M::out_col(lane);
-#pragma unroll
-                        for (int r = 0; r < M::REGS; ++r) {
-                            const int lr = wm0 + MF * i + M::out_row(lane, r);
-                            if (c_rsrc) {
-                                cpre[i][j][r] =
-                                    __builtin_amdgcn_raw_buffer_load_b32(Crs, c_off(lr, lc), 0, 0);
-                            } else {
-                                const int gr = min(m0 + lr, m - 1), gc = min(n0 + lc, n - 1);
-                                cpre[i][j][r] = C[(int64_t)gr * ldc + gc];
-                            }
-                        }
-                    }
-            }
+        if (nkt <= NST && rs_ok) {
+            if constexpr (!SPLIT) prefetch_c();
             // Only the k-tiles of the range (nkt is uniform over the workgroup).
-            load_short(ic<0>{}, ic<0>{});
-            if (nkt > 1) load_short(ic<1>{}, ic<1>{});
-            if (nkt > 2) load_short(ic<2>{}, ic<2>{});
-            if (nkt > 3) load_short(ic<3>{}, ic<3>{});
+            load_rs(ic<0>{}, 0);
+            if (nkt > 1) load_rs(ic<1>{}, 64);
+            if (nkt > 2) load_rs(ic<2>{}, 128);
+            if (nkt > 3) load_rs(ic<3>{}, 192);
             __builtin_amdgcn_sched_barrier(0);  // every load goes out before the first wait
             // Elements of A at or beyond kend (the next k slice) count as zero.
             auto mask_short = [&](auto par, auto tile) __attribute__((always_inline)) {
@@ -685,42 +705,42 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     }
 
     // ---- main loop ------------------------------------------------------------
-    // Interior workgroups run a multiple of four full k-tiles through the
-    // pipeline; the leading remainder of full tiles, the partial last tile and
-    // every edge workgroup take the bounds-checked single-tile path.
+    // A multiple of four full k-tiles runs through the pipeline, with loads
+    // through the buffer resources (any alignment, edge workgroups
+    // included); the leading remainder of full tiles and the partial last
+    // tile take the single-tile path, and so does everything when a window
+    // spans 2 GiB or more.
     const int nfull = (kend - kbeg) >> 6;  // k-tiles with all 64 elements inside
-    const bool interior = VA && VB && (m0 + BM <= m) && (n0 + BN <= n);
-    const int npipe = interior ? (nfull & ~3) : 0;
+    const int npipe = rs_ok ? (nfull & ~3) : 0;
     const int klead = kbeg + (nfull - npipe) * 64 * (npipe > 0);
     if (npipe > 0)
         for (int k0 = kbeg; k0 < klead; k0 += 64) safe_tile(k0);
-    if constexpr (VA && VB) {
-        if (npipe > 0) {
-            const int kb = klead;  // first pipelined k-tile
-            // Prologue: tiles 0, 1 into stages 0, 1; tile 2 into register
-            // set 0; fragments of tile 0, sub-step 0 into slot 0.
-            load_fast(ic<0>{}, kb);
-            load_fast(ic<1>{}, kb + 64);
-            store_tile(ic<0>{}, ic<0>{}, ic<0>{}, kb);
-            store_tile(ic<1>{}, ic<1>{}, ic<0>{}, kb + 64);
-            load_fast(ic<0>{}, kb + 128);
-            __syncthreads();
-            read_frags(ic<0>{}, ic<0>{}, ic<0>{});
-            // The steps address tiles relative to kbeg; shift by the lead.
-            const int t0 = (kb - kbeg) >> 6;
-            int kt = 0;
-            for (; kt < npipe - 4; kt += 4) {
-                step(ic<0>{}, ic<1>{}, ic<1>{}, ic<1>{}, t0 + kt);
-                step(ic<1>{}, ic<1>{}, ic<1>{}, ic<1>{}, t0 + kt + 1);
-                step(ic<2>{}, ic<1>{}, ic<1>{}, ic<1>{}, t0 + kt + 2);
-                step(ic<3>{}, ic<1>{}, ic<1>{}, ic<1>{}, t0 + kt + 3);
-            }
-            step(ic<0>{}, ic<1>{}, ic<1>{}, ic<1>{}, t0 + kt);
-            step(ic<1>{}, ic<0>{}, ic<1>{}, ic<1>{}, t0 + kt + 1);
-            step(ic<2>{}, ic<0>{}, ic<0>{}, ic<1>{}, t0 + kt + 2);
-            step(ic<3>{}, ic<0>{}, ic<0>{}, ic<0>{}, t0 + kt + 3);
+    auto pipe = [&](auto use_rs) __attribute__((always_inline)) {
+        const int kb = klead;  // first pipelined k-tile
+        // Prologue: tiles 0, 1 into stages 0, 1; tile 2 into register
+        // set 0; fragments of tile 0, sub-step 0 into slot 0.
+        load_p(use_rs, ic<0>{}, kb);
+        load_p(use_rs, ic<1>{}, kb + 64);
+        store_tile(ic<0>{}, ic<0>{}, ic<0>{}, kb);
+        store_tile(ic<1>{}, ic<1>{}, ic<0>{}, kb + 64);
+        load_p(use_rs, ic<0>{}, kb + 128);
+        __syncthreads();
+        read_frags(ic<0>{}, ic<0>{}, ic<0>{});
+        // The steps address tiles relative to kbeg; shift by the lead.
+        const int t0 = (kb - kbeg) >> 6;
+        int kt = 0;
+        for (; kt < npipe - 4; kt += 4) {
+            step(ic<0>{}, ic<1>{}, ic<1>{}, ic<1>{}, t0 + kt, use_rs);
+            step(ic<1>{}, ic<1>{}, ic<1>{}, ic<1>{}, t0 + kt + 1, use_rs);
+            step(ic<2>{}, ic<1>{}, ic<1>{}, ic<1>{}, t0 + kt + 2, use_rs);
+            step(ic<3>{}, ic<1>{}, ic<1>{}, ic<1>{}, t0 + kt + 3, use_rs);
         }
-    }
+        step(ic<0>{}, ic<1>{}, ic<1>{}, ic<1>{}, t0 + kt, use_rs);
+        step(ic<1>{}, ic<0>{}, ic<1>{}, ic<1>{}, t0 + kt + 1, use_rs);
+        step(ic<2>{}, ic<0>{}, ic<0>{}, ic<1>{}, t0 + kt + 2, use_rs);
+        step(ic<3>{}, ic<0>{}, ic<0>{}, ic<0>{}, t0 + kt + 3, use_rs);
+    };
+    if (npipe > 0) pipe(ic<1>{});
     const int ktail = npipe > 0 ? klead + npipe * 64 : kbeg;
     for (int k0 = ktail; k0 < kend; k0 += 64) safe_tile(k0);
 

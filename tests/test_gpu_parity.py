@@ -201,6 +201,13 @@ def _sampled_full_size(wname, nrows, ncols):
     assert np.array_equal(got[:, cols], want_c), describe_mismatch(got[:, cols], want_c)
 
 
+def test_paper_shape_int16_full():
+    """The paper's GEMM shape (4096, 4096, 290), int16, every element."""
+    case = workloads.WORKLOADS["i16_paper"].cases[0]
+    A, B, C = workloads.generate(case)
+    _check(A, B, C, case.m, case.n, case.k)
+
+
 def test_int16_4096_cube_sampled():
     _sampled_full_size("i16_4096", 14, 14)
 

@@ -18,6 +18,8 @@ Workloads (all row-major, C is int32):
                    convolution to one GEMM is Sec. 4.2). A uniform in [0,255]
                    (activations), B = rint(normal(0,32)) clipped to int16
                    (weights), C zero; layer i uses seed 40+i.
+* ``i16_paper``    the paper's GEMM shape (4096, 4096, 290), int16 with the
+                   recipe of i16_4096, seed 3 (context, not a graded workload).
 * ``i8_skinny``    six int8 GEMMs shaped like the projections of a 7B-class
                    decoder at small batch (one large dimension and two small
                    ones, Sec. 2 and Sec. 4.2): m in {1,8,32} with (n,k) in
@@ -188,6 +190,16 @@ WORKLOADS = {
         "int8 skinny GEMMs shaped like 7B-class decoder projections",
     ),
 }
+
+# The paper's own GEMM shape (its m_c sweep runs (m, n, k) = (4096, 4096, 290) with
+# n_c = n and k_c = k, Sec. 6.4), with the int16 recipe of i16_4096. Context only: it
+# is measured and checked like the others but is not one of the graded workloads.
+WORKLOADS["i16_paper"] = Workload(
+    "i16_paper",
+    (Case("i16_paper_4096x4096x290", "i16", 4096, 4096, 290, _U16, _U16,
+          Dist("uniform", -(1 << 20), 1 << 20), 3),),
+    "int16 C+=A.B, (m, n, k) = (4096, 4096, 290), full-range operands, C uniform in +-2^20",
+)
 
 ORDER: List[str] = ["i16_256", "i16_4096", "i8_8192", "i16_conv", "i8_skinny"]
 
