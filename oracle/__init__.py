@@ -1,12 +1,15 @@
-"""CPU oracle for integer GEMM C += A.B -- TEST INFRASTRUCTURE ONLY.
+"""CPU oracle for integer GEMM C += A.B and for the convolution Y += conv(X, W)
+that the lowering of Sec. 4.2 turns into one GEMM -- TEST INFRASTRUCTURE ONLY.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package. The GPU library does not depend on it
 and must never fall back to it.
 
 The arithmetic lives in ``igemm_oracle.c`` (plain int64 triple loop, reduced
-modulo 2^32 at the end; Sec. 4.1 definition of C += A B). This module only
-marshals numpy arrays into that library with ctypes.
+modulo 2^32 at the end; Sec. 4.1 definition of C += A B; and the direct
+definition of a zero-padded, strided, dilated 2-D convolution in NHWC / filter
+row x filter column x input channel x output channel layouts). This module
+only marshals numpy arrays into that library with ctypes.
 """
 from __future__ import annotations
 
@@ -33,6 +36,12 @@ def _load():
         fn = getattr(lib, name)
         fn.argtypes = [i64, i64, i64, vp, i64, vp, i64, vp, i64]
         fn.restype = ctypes.c_int
+    for name in ("oracle_conv2d_i16", "oracle_conv2d_i8"):
+        fn = getattr(lib, name)
+        fn.argtypes = [i64] * 13 + [vp, vp, vp]
+        fn.restype = ctypes.c_int
+    lib.oracle_conv2d_out_dim.argtypes = [i64] * 5
+    lib.oracle_conv2d_out_dim.restype = i64
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
     _lib = lib
@@ -91,3 +100,39 @@ def igemm(A: np.ndarray, B: np.ndarray, C: np.ndarray) -> np.ndarray:
     if st != 0:
         raise RuntimeError(f"oracle returned {st}")
     return C
+
+
+def conv2d_out_dim(size: int, f: int, stride: int = 1, pad: int = 0, dil: int = 1) -> int:
+    """Output extent of one spatial dimension (floor rule; -1 if invalid)."""
+    return int(_load().oracle_conv2d_out_dim(size, f, stride, pad, dil))
+
+
+def conv2d(X: np.ndarray, W: np.ndarray, Y: np.ndarray, stride=(1, 1), pad=(0, 0),
+           dil=(1, 1)) -> np.ndarray:
+    """Y += conv(X, W) (mod 2^32) in place; returns Y.
+
+    X: n x h x w x c (int16 or int8), W: r x s x c x k (same type),
+    Y: n x oh x ow x k int32; all C-contiguous. Zero padding, strides and
+    dilations per (height, width).
+    """
+    if X.dtype != W.dtype or X.dtype not in (np.int16, np.int8):
+        raise TypeError("X and W must both be int16 or both int8")
+    if Y.dtype != np.int32:
+        raise TypeError("Y must be int32")
+    for a, nm in ((X, "X"), (W, "W"), (Y, "Y")):
+        if a.ndim != 4 or not a.flags.c_contiguous:
+            raise ValueError(f"{nm} must be a C-contiguous 4-D array")
+    n, h, w, c = X.shape
+    r, s, c2, k = W.shape
+    oh = conv2d_out_dim(h, r, stride[0], pad[0], dil[0])
+    ow = conv2d_out_dim(w, s, stride[1], pad[1], dil[1])
+    if c2 != c or Y.shape != (n, oh, ow, k):
+        raise ValueError(f"shape mismatch: X {X.shape} W {W.shape} Y {Y.shape}, "
+                         f"expected Y {(n, oh, ow, k)}")
+    lib = _load()
+    fn = lib.oracle_conv2d_i16 if X.dtype == np.int16 else lib.oracle_conv2d_i8
+    st = int(fn(n, h, w, c, k, r, s, stride[0], stride[1], pad[0], pad[1], dil[0], dil[1],
+                _ptr(X), _ptr(W), _ptr(Y)))
+    if st != 0:
+        raise RuntimeError(f"oracle returned {st}")
+    return Y

@@ -1,5 +1,6 @@
 /*
- * CPU oracle for integer GEMM  C += A * B  -- TEST INFRASTRUCTURE ONLY.
+ * CPU oracle for integer GEMM  C += A * B, and for the convolution that the
+ * paper lowers to it (at the end of this file) -- TEST INFRASTRUCTURE ONLY.
  *
  * Only the tests, the smoke check and the benchmark's CPU-baseline leg may
  * load this library. The GPU library never links, includes or calls it, and
@@ -129,3 +130,84 @@ int oracle_igemm_i8(int64_t m, int64_t n, int64_t k,
     }
     return err;
 }
+
+/*
+ * Convolution  Y += conv(X, W)  -- the operation that the lowering of Sec. 4.2
+ * (GEMM and DL inference) turns into one GEMM: IM2ROW rewrites the input
+ * activations as a matrix with one row per output pixel and one column per
+ * (filter row, filter column, input channel), and the filters as a matrix with
+ * one row per such triple and one column per output channel. The oracle does
+ * not build that matrix: it is the direct definition, summing over the filter
+ * window and the input channels for every output pixel and channel.
+ *
+ * Layouts (all dense, row-major in the order given):
+ *   X  n x h x w x c           input activations (NHWC)
+ *   W  r x s x c x k           filters (filter row, filter column, input
+ *                              channel, output channel)
+ *   Y  n x oh x ow x k         output activations, updated in place
+ * with oh = (h + 2 pad_h - dil_h (r - 1) - 1) / stride_h + 1 (floor; 0 when the
+ * numerator is negative) and likewise ow. Output pixel (oy, ox) reads input
+ * row oy * stride_h - pad_h + fy * dil_h and column ox * stride_w - pad_w +
+ * fx * dil_w for filter position (fy, fx); positions outside the input are
+ * zero (zero padding). Exact int64 sums, reduced modulo 2^32 once at the end.
+ */
+int64_t oracle_conv2d_out_dim(int64_t in, int64_t f, int64_t stride, int64_t pad, int64_t dil)
+{
+    if (in < 0 || f < 1 || stride < 1 || pad < 0 || dil < 1)
+        return -1;
+    const int64_t span = in + 2 * pad - dil * (f - 1) - 1;
+    return span < 0 ? 0 : span / stride + 1;
+}
+
+#define ORACLE_CONV2D(NAME, T)                                                               \
+    int NAME(int64_t n, int64_t h, int64_t w, int64_t c, int64_t k, int64_t r, int64_t s,  \
+             int64_t stride_h, int64_t stride_w, int64_t pad_h, int64_t pad_w,             \
+             int64_t dil_h, int64_t dil_w, const T *X, const T *W, int32_t *Y)             \
+    {                                                                                        \
+        if (n < 0 || c < 0 || k < 0)                                                         \
+            return -1;                                                                       \
+        const int64_t oh = oracle_conv2d_out_dim(h, r, stride_h, pad_h, dil_h);              \
+        const int64_t ow = oracle_conv2d_out_dim(w, s, stride_w, pad_w, dil_w);              \
+        if (oh < 0 || ow < 0)                                                                \
+            return -1;                                                                       \
+        int err = 0;                                                                         \
+        _Pragma("omp parallel for collapse(2) schedule(dynamic, 1)")                         \
+        for (int64_t b = 0; b < n; ++b)                                                      \
+            for (int64_t oy = 0; oy < oh; ++oy) {                                            \
+                int64_t *acc = (int64_t *)malloc((size_t)(k > 0 ? k : 1) * sizeof(int64_t)); \
+                if (!acc) {                                                                  \
+                    _Pragma("omp atomic write") err = -2;                                    \
+                    continue;                                                                \
+                }                                                                            \
+                for (int64_t ox = 0; ox < ow; ++ox) {                                        \
+                    int32_t *y = Y + ((b * oh + oy) * ow + ox) * k;                          \
+                    for (int64_t co = 0; co < k; ++co)                                       \
+                        acc[co] = (int64_t)y[co];                                            \
+                    for (int64_t fy = 0; fy < r; ++fy) {                                     \
+                        const int64_t iy = oy * stride_h - pad_h + fy * dil_h;               \
+                        if (iy < 0 || iy >= h)                                               \
+                            continue;                                                        \
+                        for (int64_t fx = 0; fx < s; ++fx) {                                 \
+                            const int64_t ix = ox * stride_w - pad_w + fx * dil_w;           \
+                            if (ix < 0 || ix >= w)                                           \
+                                continue;                                                    \
+                            const T *xp = X + ((b * h + iy) * w + ix) * c;                   \
+                            const T *wp = W + (fy * s + fx) * c * k;                         \
+                            for (int64_t ci = 0; ci < c; ++ci) {                             \
+                                const int64_t xv = (int64_t)xp[ci];                          \
+                                const T *wrow = wp + ci * k;                                 \
+                                for (int64_t co = 0; co < k; ++co)                           \
+                                    acc[co] += xv * (int64_t)wrow[co];                       \
+                            }                                                                \
+                        }                                                                    \
+                    }                                                                        \
+                    for (int64_t co = 0; co < k; ++co)                                       \
+                        y[co] = wrap_to_i32(acc[co]);                                        \
+                }                                                                            \
+                free(acc);                                                                   \
+            }                                                                                \
+        return err;                                                                          \
+    }
+
+ORACLE_CONV2D(oracle_conv2d_i16, int16_t)
+ORACLE_CONV2D(oracle_conv2d_i8, int8_t)
