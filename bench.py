@@ -19,9 +19,10 @@ Prints ONE JSON line. Besides the headline value it carries:
                 of the same workload;
   per_config    every other workload, each timed the same way (memory-bound
                 ones rotate through enough buffer sets to defeat the 256 MB
-                last-level cache), with its own roofline fraction; the last
-                entry is the paper's own GEMM shape (4096, 4096, 290), for
-                context.
+                last-level cache), with its own roofline fraction; then the
+                paper's own GEMM shape (4096, 4096, 290), for context, and
+                the six network layers run as convolutions through the
+                implicit-GEMM entry point (IM2ROW gathered in the kernel).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-extra]
                        [--no-cpu-baseline] [--cpu-seconds S]
@@ -130,6 +131,55 @@ def bench_case(case, min_sets=1, per_graph=40, reps=10, warmup=3):
         "name": case.name, "dtype": case.dtype, "m": case.m, "n": case.n, "k": case.k,
         "kernel": plan["kernel_name"], "split": plan["split"], "grid": plan["grid"],
         "us": round(t * 1e6, 2), "TOPS": round(2.0 * case.m * case.n * case.k / t / 1e12, 2),
+        "bound": bound, "achieved": round(ach, 1), "peak": peak, "unit": unit,
+        "frac": round(ach / peak, 4), "buffer_sets": nsets, "timing": "hip graph replay",
+    }
+
+
+def bench_conv_case(case, per_graph=40, reps=10, warmup=3):
+    """Time one convolution (implicit GEMM: IM2ROW gathered in the kernel)
+    like bench_case; the roofline counts the lowered GEMM's multiply-adds
+    and the unique bytes of X, W and Y (read and written)."""
+    import torch
+
+    import paper_2302_07594_amd as ig
+    import workloads
+    X, W, Y = workloads.generate_conv(case)
+    es = 2 if case.dtype == "i16" else 1
+    set_bytes = X.nbytes + W.nbytes + Y.nbytes
+    nsets = min(64, max(1, -(-2 * MALL_BYTES // set_bytes)))
+    Xd0, Wd0, Yd0 = (torch.from_numpy(x).cuda() for x in (X, W, Y))
+    sets = [(Xd0, Wd0, Yd0)] + [(Xd0.clone(), Wd0.clone(), Yd0.clone()) for _ in range(nsets - 1)]
+    kw = dict(stride=case.stride, pad=case.pad, dil=case.dil)
+    for i in range(warmup):
+        ig.conv2d(*sets[i % nsets], **kw)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(per_graph):
+            ig.conv2d(*sets[i % nsets], **kw)
+    g.replay()
+    torch.cuda.synchronize()
+    t = time_launches(lambda i: g.replay(), reps) / per_graph
+    m, n, k = case.gemm_shape()
+    d = ig.conv_desc(case.n, case.h, case.w, case.c, case.k, case.r, case.s, case.stride,
+                     case.pad, case.dil)
+    plan = ig.igemm_conv2d_query_plan(es, d, Xd0, Wd0, Yd0)
+    ops = 2.0 * m * n * k
+    nbytes = X.nbytes + W.nbytes + 2.0 * Y.nbytes
+    peak_ops = (PEAK_I16_TOPS if es == 2 else PEAK_INT8_TOPS) * 1e12
+    if ops / nbytes >= peak_ops / (HBM_GBS * 1e9):
+        bound, ach, peak, unit = "mfma", ops / t / 1e12, peak_ops / 1e12, "TOPS"
+    else:
+        bound, ach, peak, unit = "hbm", nbytes / t / 1e9, HBM_GBS, "GB/s"
+    return {
+        "name": case.name, "dtype": case.dtype, "conv": {
+            "n": case.n, "h": case.h, "w": case.w, "c": case.c, "k": case.k, "r": case.r,
+            "s": case.s, "stride": list(case.stride), "pad": list(case.pad),
+            "dil": list(case.dil)},
+        "m": m, "n": n, "k": k, "kernel": plan["kernel_name"], "split": plan["split"],
+        "grid": plan["grid"], "vector_gather": bool(plan["vec_a"]),
+        "us": round(t * 1e6, 2), "TOPS": round(ops / t / 1e12, 2),
         "bound": bound, "achieved": round(ach, 1), "peak": peak, "unit": unit,
         "frac": round(ach / peak, 4), "buffer_sets": nsets, "timing": "hip graph replay",
     }
@@ -278,6 +328,10 @@ def main():
                 log(f"bench: per-config {c.name}")
                 per.append(bench_case(c))
                 torch.cuda.empty_cache()
+        for c in workloads.CONV2D_CASES:
+            log(f"bench: per-config {c.name}")
+            per.append(bench_conv_case(c))
+            torch.cuda.empty_cache()
         out["per_config"] = per
     print(json.dumps(out), flush=True)
 

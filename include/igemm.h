@@ -258,6 +258,72 @@ int igemm_i8_packed_b(int64_t m, int64_t n, int64_t k,
                       int kernel, void *workspace, int64_t workspace_bytes,
                       void *stream);
 
+/*
+ * Convolution through its GEMM lowering (Sec. 4.2, "GEMM and DL inference":
+ * the convolution of a CNN layer is cast as one GEMM by the IM2ROW transform
+ * of the input activations, which can be applied on the fly, as part of
+ * packing, instead of being materialised). Here the IM2ROW rows are gathered
+ * while the operand tiles are staged, so the lowered matrix never exists in
+ * memory:
+ *
+ *   Y[b,oy,ox,co] += sum over fy < r, fx < s, ci < c of
+ *                    X[b, oy*stride_h - pad_h + fy*dil_h,
+ *                         ox*stride_w - pad_w + fx*dil_w, ci] * W[fy,fx,ci,co]
+ *
+ * with input positions outside the image counting as zero (zero padding),
+ * exact integer sums and the update reduced modulo 2^32 as for igemm_i16.
+ * The lowered GEMM has m = n*oh*ow rows (output pixels), n = k columns
+ * (output channels) and k = r*s*c (filter taps times input channels); W is
+ * exactly its B (k x n row-major) and Y its C.
+ *
+ * Layouts, all dense and row-major in the order given, DEVICE pointers owned
+ * by the caller:
+ *   X  n x h x w x c      input activations (NHWC), int16 or int8
+ *   W  r x s x c x k      filters (filter row, filter column, input channel,
+ *                         output channel), same type
+ *   Y  n x oh x ow x k    output activations, int32, updated in place
+ * oh = floor((h + 2*pad_h - dil_h*(r-1) - 1) / stride_h) + 1 (0 when the
+ * window does not fit), likewise ow; igemm_conv2d_out_dim computes it.
+ * Y must not overlap X or W. An input whose channel rows are 16-byte aligned
+ * (X 16-byte aligned, c*element size a multiple of 16) is gathered 16 bytes at
+ * a time; any other is gathered element by element.
+ *
+ * Errors: IGEMM_EINVAL (before any HIP call) for a NULL descriptor, negative
+ * extents, r or s < 1, strides or dilations < 1, negative padding, NULL
+ * tensors when there is work, or an int16 X at an odd address; IGEMM_ENOTSUP when the input exceeds 2 GiB, the
+ * padded image 2^30 elements in a dimension, the lowered k or m 2^31, or the
+ * filter tensor's offsets 2 GiB. A call with no output pixel, no output
+ * channel or k = 0 returns IGEMM_OK and leaves Y unchanged. Asynchrony as for
+ * igemm_i16 (enqueued on `stream`). No workspace is used.
+ */
+typedef struct igemm_conv2d_desc {
+    int64_t n, h, w, c;            /* input batch, height, width, channels */
+    int64_t k;                     /* output channels                      */
+    int64_t r, s;                  /* filter height and width              */
+    int64_t stride_h, stride_w;    /* >= 1                                 */
+    int64_t pad_h, pad_w;          /* >= 0, zero padding on both sides     */
+    int64_t dil_h, dil_w;          /* >= 1                                 */
+} igemm_conv2d_desc;
+
+int igemm_conv2d_i16(const igemm_conv2d_desc *desc, const int16_t *X, const int16_t *W,
+                     int32_t *Y, void *stream);
+int igemm_conv2d_i8(const igemm_conv2d_desc *desc, const int8_t *X, const int8_t *W,
+                    int32_t *Y, void *stream);
+/* The same with an explicit kernel (one of the fused 16/32-row or 64x64 tile
+ * kernels of the operand type; -1 = automatic) and k-slice count (-1 =
+ * automatic); elem_bytes 2 (int16) or 1 (int8). For sweeps and tests. */
+int igemm_conv2d_ex(int elem_bytes, const igemm_conv2d_desc *desc, const void *X,
+                    const void *W, int32_t *Y, void *stream, int kernel, int split);
+/* Host-only plan of the lowered GEMM a convolution call would launch
+ * (out->kernel = -1 when there is nothing to compute); vec_a reports the
+ * 16-byte gather. */
+int igemm_conv2d_query_plan(int elem_bytes, const igemm_conv2d_desc *desc, const void *X,
+                            const void *W, const void *Y, int num_cu, int kernel, int split,
+                            igemm_plan *out);
+/* Output extent of one spatial dimension, or -1 for invalid arguments. */
+int64_t igemm_conv2d_out_dim(int64_t in, int64_t f, int64_t stride, int64_t pad,
+                             int64_t dil);
+
 /* Release the memory the library's workspace pool for the current device
  * holds beyond what in-flight calls use (hipMemPoolTrimTo). Returns
  * IGEMM_OK, or IGEMM_EHIP. */

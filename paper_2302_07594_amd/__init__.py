@@ -24,11 +24,17 @@ Same names as the C ABI:
                                            workspace_bytes=0, stream=None)
     igemm_query_plan(elem_bytes, m, n, k, A, lda, B, ldb, C, ldc, num_cu=0,
                      kernel=-1, split=-1) -> dict
+    igemm_conv2d_i16 / igemm_conv2d_i8(desc, X, W, Y, stream=None)
+    igemm_conv2d_ex(elem_bytes, desc, X, W, Y, stream=None, kernel=-1, split=-1)
+    igemm_conv2d_query_plan(elem_bytes, desc, X=None, W=None, Y=None, num_cu=0,
+                            kernel=-1, split=-1) -> dict
+    igemm_conv2d_out_dim(in, f, stride, pad, dil)
     igemm_strerror(status), igemm_kernel_name(i), igemm_num_kernels(),
     igemm_version()
 A, B, C may be integer device addresses or torch tensors (their data_ptr()).
 Tensor conveniences: gemm_i16(A, B, C) and gemm_i8(A, B, C) take 2-D CUDA
-tensors with unit stride along rows and update C in place; a workspace the
+tensors with unit stride along rows and update C in place; conv2d(X, W, Y,
+stride, pad, dil) takes contiguous NHWC / (r, s, c, k) / NHWC tensors; a workspace the
 call needs is taken from torch's caching allocator (so the calls can be
 captured into a torch CUDA graph) unless workspace="library" asks for the
 library's own stream-ordered pool.
@@ -63,6 +69,19 @@ class _Plan(ctypes.Structure):
                 ("limb_products", ctypes.c_int), ("packed", ctypes.c_int),
                 ("workspace_bytes", ctypes.c_int64), ("packed_a_bytes", ctypes.c_int64),
                 ("packed_b_bytes", ctypes.c_int64)]
+
+
+class ConvDesc(ctypes.Structure):
+    """igemm_conv2d_desc: input n x h x w x c (NHWC), k output channels,
+    r x s filters, strides, zero padding and dilations."""
+    _fields_ = [(f, ctypes.c_int64) for f in
+                ("n", "h", "w", "c", "k", "r", "s", "stride_h", "stride_w", "pad_h", "pad_w",
+                 "dil_h", "dil_w")]
+
+
+def conv_desc(n, h, w, c, k, r, s, stride=(1, 1), pad=(0, 0), dil=(1, 1)) -> ConvDesc:
+    return ConvDesc(int(n), int(h), int(w), int(c), int(k), int(r), int(s), int(stride[0]),
+                    int(stride[1]), int(pad[0]), int(pad[1]), int(dil[0]), int(dil[1]))
 
 
 def _load():
@@ -100,6 +119,18 @@ def _load():
     for name in ("igemm_i16_packed_b", "igemm_i8_packed_b"):
         getattr(lib, name).argtypes = [i64, i64, i64, vp, i64, vp, i64, vp, i64, ci, vp, i64, vp]
         getattr(lib, name).restype = ci
+    cd = ctypes.POINTER(ConvDesc)
+    lib.igemm_conv2d_i16.argtypes = [cd, vp, vp, vp, vp]
+    lib.igemm_conv2d_i16.restype = ci
+    lib.igemm_conv2d_i8.argtypes = [cd, vp, vp, vp, vp]
+    lib.igemm_conv2d_i8.restype = ci
+    lib.igemm_conv2d_ex.argtypes = [ci, cd, vp, vp, vp, vp, ci, ci]
+    lib.igemm_conv2d_ex.restype = ci
+    lib.igemm_conv2d_query_plan.argtypes = [ci, cd, vp, vp, vp, ci, ci, ci,
+                                            ctypes.POINTER(_Plan)]
+    lib.igemm_conv2d_query_plan.restype = ci
+    lib.igemm_conv2d_out_dim.argtypes = [i64] * 5
+    lib.igemm_conv2d_out_dim.restype = i64
     lib.igemm_trim_workspace.argtypes = []
     lib.igemm_trim_workspace.restype = ci
     lib.igemm_query_plan.argtypes = [ci, i64, i64, i64, vp, i64, vp, i64, vp, i64, ci, ci, ci,
@@ -516,3 +547,67 @@ def gemm_i16(A, B, C, stream=None, kernel=-1, split=-1, workspace=None):
 def gemm_i8(A, B, C, stream=None, kernel=-1, split=-1, workspace=None):
     """C += A.B for 2-D torch.int8 CUDA tensors; see gemm_i16."""
     return _gemm(1, A, B, C, stream, kernel, split, workspace, "gemm_i8")
+
+
+# ---- convolution through its IM2ROW lowering --------------------------------
+
+def igemm_conv2d_out_dim(size, f, stride=1, pad=0, dil=1) -> int:
+    return int(_lib.igemm_conv2d_out_dim(int(size), int(f), int(stride), int(pad), int(dil)))
+
+
+def igemm_conv2d_i16(desc, X, W, Y, stream=None) -> int:
+    """Y += conv(X, W), int16 operands (see include/igemm.h). Returns the status."""
+    return int(_lib.igemm_conv2d_i16(ctypes.byref(desc), _addr(X), _addr(W), _addr(Y),
+                                     _stream(stream)))
+
+
+def igemm_conv2d_i8(desc, X, W, Y, stream=None) -> int:
+    return int(_lib.igemm_conv2d_i8(ctypes.byref(desc), _addr(X), _addr(W), _addr(Y),
+                                    _stream(stream)))
+
+
+def igemm_conv2d_ex(elem_bytes, desc, X, W, Y, stream=None, kernel=-1, split=-1) -> int:
+    return int(_lib.igemm_conv2d_ex(int(elem_bytes), ctypes.byref(desc), _addr(X), _addr(W),
+                                    _addr(Y), _stream(stream), int(kernel), int(split)))
+
+
+def igemm_conv2d_query_plan(elem_bytes, desc, X=None, W=None, Y=None, num_cu=0, kernel=-1,
+                            split=-1) -> dict:
+    """Plan of the lowered GEMM (host-only); omitted pointers stand for
+    16-byte aligned buffers."""
+    p = _Plan()
+    st = _lib.igemm_conv2d_query_plan(
+        int(elem_bytes), ctypes.byref(desc), _addr(_PLACEHOLDER if X is None else X),
+        _addr(_PLACEHOLDER if W is None else W), _addr(_PLACEHOLDER if Y is None else Y),
+        int(num_cu), int(kernel), int(split), ctypes.byref(p))
+    if st != IGEMM_OK:
+        raise IgemmError(st, "igemm_conv2d_query_plan")
+    d = {f: getattr(p, f) for f, _ in _Plan._fields_}
+    d["kernel_name"] = igemm_kernel_name(p.kernel) if p.kernel >= 0 else None
+    return d
+
+
+def conv2d(X, W, Y, stride=(1, 1), pad=(0, 0), dil=(1, 1), stream=None, kernel=-1, split=-1):
+    """Y += conv(X, W) on contiguous CUDA tensors: X n x h x w x c and W
+    r x s x c x k (both torch.int16 or both torch.int8), Y n x oh x ow x k
+    torch.int32. Returns Y; raises IgemmError on a bad status."""
+    import torch
+    if X.dtype not in (torch.int16, torch.int8) or W.dtype != X.dtype:
+        raise TypeError("conv2d: X and W must both be torch.int16 or both torch.int8")
+    if Y.dtype != torch.int32:
+        raise TypeError("conv2d: Y must be torch.int32")
+    for t, nm in ((X, "X"), (W, "W"), (Y, "Y")):
+        if t.dim() != 4 or not t.is_contiguous() or not t.is_cuda:
+            raise ValueError(f"conv2d: {nm} must be a contiguous 4-D CUDA tensor")
+    n, h, w, c = X.shape
+    r, s, c2, k = W.shape
+    oh = igemm_conv2d_out_dim(h, r, stride[0], pad[0], dil[0])
+    ow = igemm_conv2d_out_dim(w, s, stride[1], pad[1], dil[1])
+    if c2 != c or tuple(Y.shape) != (n, oh, ow, k):
+        raise ValueError(f"conv2d: X {tuple(X.shape)}, W {tuple(W.shape)} need Y "
+                         f"{(n, oh, ow, k)}, got {tuple(Y.shape)}")
+    d = conv_desc(n, h, w, c, k, r, s, stride, pad, dil)
+    st = igemm_conv2d_ex(2 if X.dtype == torch.int16 else 1, d, X, W, Y, stream, kernel, split)
+    if st != IGEMM_OK:
+        raise IgemmError(st, "conv2d")
+    return Y

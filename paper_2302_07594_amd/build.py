@@ -7,10 +7,12 @@ in ``include/igemm.h``.
 """
 from __future__ import annotations
 
+import concurrent.futures
 import glob
 import os
 import subprocess
 import sys
+import tempfile
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
@@ -34,13 +36,7 @@ def sources():
                   glob.glob(os.path.join(CSRC, "*.cpp")))
 
 
-def build(verbose: bool = False, extra_flags=None) -> str:
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
-           "-Wall", "-Wno-unused-parameter", "-I", INCLUDE, "-I", CSRC] + HIP_FLAGS
-    if extra_flags:
-        cmd += list(extra_flags)
-    cmd += sources() + ["-o", tmp]
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -50,6 +46,27 @@ def build(verbose: bool = False, extra_flags=None) -> str:
         raise RuntimeError(f"hipcc failed ({res.returncode}):\n{err}")
     if verbose and err.strip():
         print(err, file=sys.stderr)
+
+
+def build(verbose: bool = False, extra_flags=None, jobs: int = 0) -> str:
+    """Compile every source to an object (in parallel, ``jobs`` at a time;
+    0 = one per CPU, at most 16) and link the shared library."""
+    base = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall",
+            "-Wno-unused-parameter", "-I", INCLUDE, "-I", CSRC] + HIP_FLAGS
+    if extra_flags:
+        base += list(extra_flags)
+    srcs = sources()
+    jobs = jobs or min(16, os.cpu_count() or 1)
+    with tempfile.TemporaryDirectory(prefix="igemm_build_") as tmpdir:
+        objs = [os.path.join(tmpdir, os.path.basename(s) + ".o") for s in srcs]
+        with concurrent.futures.ThreadPoolExecutor(max_workers=jobs) as pool:
+            futs = [pool.submit(_run, base + ["-c", s, "-o", o], verbose)
+                    for s, o in zip(srcs, objs)]
+            for f in futs:
+                f.result()
+        tmp = LIB + ".tmp"
+        _run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC"] + objs + ["-o", tmp],
+             verbose)
     os.replace(tmp, LIB)
     return LIB
 

@@ -222,10 +222,42 @@ int run_packed_b(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t
     return put_scratch(sc, s, st);
 }
 
+// Y += conv(X, W) through the fused kernels with IM2ROW gathering of A.
+int run_conv(int es, const igemm_conv2d_desc *d, const void *X, const void *W, int32_t *Y,
+             void *stream, int kernel, int split) {
+    igemm_plan p;
+    ConvGeom g;
+    bool vg = false;
+    // Validate without touching the device, then plan for its CU count.
+    int st = make_conv_plan(es, d, X, W, Y, 0, kernel, split, &p, &g, &vg);
+    if (st != IGEMM_OK || p.kernel < 0) return st;
+    st = make_conv_plan(es, d, X, W, Y, num_cu_of_current_device(), kernel, split, &p, &g, &vg);
+    if (st != IGEMM_OK) return st;
+    const int64_t oh = conv_out_dim(d->h, d->r, d->stride_h, d->pad_h, d->dil_h);
+    const int64_t ow = conv_out_dim(d->w, d->s, d->stride_w, d->pad_w, d->dil_w);
+    return launch_conv(es, p, d->n * oh * ow, d->k, d->r * d->s * d->c, g, vg, X, W, Y, d->k,
+                       stream);
+}
+
 }  // namespace
 }  // namespace igemm
 
 extern "C" {
+
+int igemm_conv2d_i16(const igemm_conv2d_desc *desc, const int16_t *X, const int16_t *W,
+                     int32_t *Y, void *stream) {
+    return igemm::run_conv(2, desc, X, W, Y, stream, -1, -1);
+}
+
+int igemm_conv2d_i8(const igemm_conv2d_desc *desc, const int8_t *X, const int8_t *W, int32_t *Y,
+                    void *stream) {
+    return igemm::run_conv(1, desc, X, W, Y, stream, -1, -1);
+}
+
+int igemm_conv2d_ex(int elem_bytes, const igemm_conv2d_desc *desc, const void *X, const void *W,
+                    int32_t *Y, void *stream, int kernel, int split) {
+    return igemm::run_conv(elem_bytes, desc, X, W, Y, stream, kernel, split);
+}
 
 int igemm_i16(int64_t m, int64_t n, int64_t k, const int16_t *A, int64_t lda,
               const int16_t *B, int64_t ldb, int32_t *C, int64_t ldc, void *stream) {

@@ -62,6 +62,31 @@ struct PackedLayout {
     int64_t bytes;                        // a_bytes + b_bytes
 };
 
+// Division of a 32-bit unsigned integer by an invariant divisor d >= 1 with
+// one multiply-high, an add and two shifts (Granlund and Montgomery,
+// "Division by invariant integers using multiplication", 1994, the
+// round-up method with a 33-bit multiplier whose top bit is applied as an
+// add): q = (t + ((x - t) >> s1)) >> s2 with t = mulhi(x, mul). Exact for
+// every x < 2^32.
+struct DivU32 {
+    uint32_t mul, s1, s2;
+};
+DivU32 make_div(uint32_t d);
+
+// Geometry of a convolution lowered to C += A B by IM2ROW (Sec. 4.2): row i
+// of A is output pixel i (image, output row, output column), column p is
+// (filter row, filter column, input channel); A[i, p] is the input element
+// that this output pixel reads through that filter tap, or zero outside the
+// image. All extents fit in 31 bits (checked on the host).
+struct ConvGeom {
+    int h, w, c;          // input height, width, channels (NHWC)
+    int ohw, ow;          // output pixels per image, output width
+    int s;                // filter width
+    int sh, sw, ph, pw, dh, dw;
+    int x_bytes;          // bytes of the input tensor
+    DivU32 by_c, by_s, by_ohw, by_ow;
+};
+
 // Validation and planning; pure host code, no HIP calls.
 int validate(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
              const void *B, int64_t ldb, const void *C, int64_t ldc);
@@ -73,6 +98,14 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
 void packed_layout(int es, int64_t m, int64_t n, int64_t k, int kernel, const void *A,
                    int64_t lda, PackedLayout *L);
 
+// Output extent of one spatial dimension of a convolution (-1 if invalid).
+int64_t conv_out_dim(int64_t in, int64_t f, int64_t stride, int64_t pad, int64_t dil);
+// Plan of a convolution as its lowered GEMM, with the kernel's geometry.
+// Returns IGEMM_OK with out->kernel = -1 when there is nothing to compute.
+int make_conv_plan(int es, const igemm_conv2d_desc *d, const void *X, const void *W,
+                   const void *Y, int num_cu, int kernel, int split, igemm_plan *out,
+                   ConvGeom *g, bool *vec_gather);
+
 // Kernel launches for a validated plan (stream is a hipStream_t). The packed
 // launch needs a workspace of at least plan.workspace_bytes, 256-byte aligned.
 // The streaming kernel for few-row int8 products.
@@ -82,6 +115,21 @@ int launch_stream(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const vo
 int launch_tiled(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
                  int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
                  void *stream);
+// Host stubs of the fused kernel variants (VA: A rows 16-byte aligned, or for
+// convolutions the 16-byte gather; VB: B rows aligned; SPLIT: k sliced across
+// workgroups), one translation unit per group of tile shapes; nullptr for
+// ids outside the group.
+const void *fused_i8_wide(int id, bool va, bool vb, bool split);
+const void *fused_i8_rows(int id, bool va, bool vb, bool split);
+const void *fused_i16_wide(int id, bool va, bool vb, bool split);
+const void *fused_i16_rows(int id, bool va, bool vb, bool split);
+const void *fused_conv_i16(int id, bool vgather, bool vb, bool split);
+const void *fused_conv_i8(int id, bool vgather, bool vb, bool split);
+// The same fused kernels with A gathered from the NHWC input X by IM2ROW
+// (vector gather when a 16-byte chunk of A never straddles two filter taps).
+int launch_conv(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const ConvGeom &g,
+                bool vec_gather, const void *X, const void *W, int32_t *Y, int64_t ldy,
+                void *stream);
 // The packed path: pack A into an A part (optionally clearing the B part's
 // column corrections, which pack_b then adds into), pack B into a B part
 // (clear_corr: clear the corrections itself first), multiply (one launch per

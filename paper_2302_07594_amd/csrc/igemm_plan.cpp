@@ -301,6 +301,107 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
     return IGEMM_OK;
 }
 
+DivU32 make_div(uint32_t d) {
+    DivU32 r = {0u, 0u, 0u};
+    if (d <= 1) return r;  // x / 1: t = 0, q = x
+    int l = 0;
+    while (((uint64_t)1 << l) < d) ++l;  // l = ceil(log2 d), 1 <= l <= 32
+    r.mul = (uint32_t)((((uint64_t)1 << 32) * (((uint64_t)1 << l) - d)) / d + 1);
+    r.s1 = 1;
+    r.s2 = (uint32_t)(l - 1);
+    return r;
+}
+
+int64_t conv_out_dim(int64_t in, int64_t f, int64_t stride, int64_t pad, int64_t dil) {
+    if (in < 0 || f < 1 || stride < 1 || pad < 0 || dil < 1) return -1;
+    int64_t t, padded;
+    if (__builtin_mul_overflow(dil, f - 1, &t) || __builtin_mul_overflow(pad, 2, &padded) ||
+        __builtin_add_overflow(in, padded, &padded))
+        return -1;
+    const int64_t span = padded - t - 1;  // no overflow: padded >= 0, t >= 0
+    return span < 0 ? 0 : span / stride + 1;
+}
+
+// A convolution planned as the GEMM its IM2ROW lowering gives (Sec. 4.2):
+// m = n * oh * ow output pixels, n_gemm = output channels, k = r * s * c.
+int make_conv_plan(int es, const igemm_conv2d_desc *d, const void *X, const void *W,
+                   const void *Y, int num_cu, int kernel, int split, igemm_plan *out,
+                   ConvGeom *g, bool *vec_gather) {
+    if (out == NULL || d == NULL || (es != 1 && es != 2)) return IGEMM_EINVAL;
+    *out = igemm_plan{};
+    out->kernel = -1;
+    out->elem_bytes = es;
+    if (d->n < 0 || d->h < 0 || d->w < 0 || d->c < 0 || d->k < 0 || d->r < 1 || d->s < 1)
+        return IGEMM_EINVAL;
+    const int64_t oh = conv_out_dim(d->h, d->r, d->stride_h, d->pad_h, d->dil_h);
+    const int64_t ow = conv_out_dim(d->w, d->s, d->stride_w, d->pad_w, d->dil_w);
+    if (oh < 0 || ow < 0) return IGEMM_EINVAL;
+    const int64_t N = d->k;
+    int64_t M, K;
+    if (__builtin_mul_overflow(d->n, oh, &M) || __builtin_mul_overflow(M, ow, &M) ||
+        __builtin_mul_overflow(d->r, d->s, &K) || __builtin_mul_overflow(K, d->c, &K)) {
+        // Sizes beyond int64: unsupported unless one factor makes them empty.
+        if (d->n == 0 || oh == 0 || ow == 0 || N == 0 || d->c == 0) return IGEMM_OK;
+        return IGEMM_ENOTSUP;
+    }
+    if (M == 0 || N == 0 || K == 0) return IGEMM_OK;  // nothing to add
+    if (X == NULL || W == NULL || Y == NULL) return IGEMM_EINVAL;
+    // The element gather reads X one element at a time: int16 X must be
+    // 2-byte aligned (as its C type requires).
+    if (es == 2 && ((uintptr_t)X & 1) != 0) return IGEMM_EINVAL;
+    // 31-bit extents: input bytes and window arithmetic (the kernel addresses
+    // the input through one buffer resource), the lowered GEMM's sizes.
+    const int64_t lim = (int64_t)1 << 30;
+    if (d->h + 2 * d->pad_h >= lim || d->w + 2 * d->pad_w >= lim || d->c >= lim ||
+        d->s >= lim || d->stride_h >= lim || d->stride_w >= lim)
+        return IGEMM_ENOTSUP;
+    int64_t xb;
+    if (__builtin_mul_overflow(d->n, d->h, &xb) || __builtin_mul_overflow(xb, d->w, &xb) ||
+        __builtin_mul_overflow(xb, d->c, &xb) || xb > (0x7fff0000 - 64) / es)
+        return IGEMM_ENOTSUP;
+    if (M > INT_MAX || K > INT_MAX - 65536 || N > INT_MAX) return IGEMM_ENOTSUP;
+    // Filter window offsets; (K + 2) * N < 2^62 after the bounds above.
+    if ((K + 2) * N * es + 64 >= 0x7fff0000) return IGEMM_ENOTSUP;
+    int id = kernel;
+    if (id < 0) {
+        if (es == 2) {
+            if (M <= 16) id = K_I16_16x128;
+            else if (M <= 32) id = K_I16_32x128;
+            else if (tiles_of(K_I16_64x64, M, N) < 32) id = M <= 64 ? K_I16_32x128 : K_I16_16x128;
+            else id = K_I16_64x64;
+        } else {
+            id = M <= 16 ? K_I8_16x256 : K_I8_32x256;
+        }
+    }
+    const bool conv_id = id == K_I16_64x64 || id == K_I16_32x128 || id == K_I16_16x128 ||
+                         id == K_I8_32x256 || id == K_I8_16x256;
+    if (!conv_id || kKernels[id].es != es) return IGEMM_EINVAL;
+    int st = make_plan(es, M, N, K, X, K, W, N, N, num_cu, id, split, false, out);
+    if (st != IGEMM_OK) return st;
+    out->vec_a = (((uintptr_t)X % 16) == 0 && (d->c * es) % 16 == 0) ? 1 : 0;
+    *vec_gather = out->vec_a != 0;
+    g->h = (int)d->h;
+    g->w = (int)d->w;
+    g->c = (int)d->c;
+    g->ohw = (int)(oh * ow);
+    g->ow = (int)ow;
+    g->s = (int)d->s;
+    g->sh = (int)d->stride_h;
+    g->sw = (int)d->stride_w;
+    g->ph = (int)d->pad_h;
+    g->pw = (int)d->pad_w;
+    // A one-tap dimension never multiplies its dilation by anything but 0;
+    // any dilation of a wider filter is below 2^30 since the window fits.
+    g->dh = d->r == 1 ? 1 : (int)d->dil_h;
+    g->dw = d->s == 1 ? 1 : (int)d->dil_w;
+    g->x_bytes = (int)(xb * es);
+    g->by_c = make_div((uint32_t)d->c);
+    g->by_s = make_div((uint32_t)d->s);
+    g->by_ohw = make_div((uint32_t)(oh * ow));
+    g->by_ow = make_div((uint32_t)ow);
+    return IGEMM_OK;
+}
+
 }  // namespace igemm
 
 extern "C" {
@@ -334,6 +435,18 @@ const char *igemm_strerror(int status) {
     }
 }
 
-int igemm_version(void) { return 200; }
+int igemm_version(void) { return 300; }
+
+int64_t igemm_conv2d_out_dim(int64_t in, int64_t f, int64_t stride, int64_t pad, int64_t dil) {
+    return igemm::conv_out_dim(in, f, stride, pad, dil);
+}
+
+int igemm_conv2d_query_plan(int elem_bytes, const igemm_conv2d_desc *desc, const void *X,
+                            const void *W, const void *Y, int num_cu, int kernel, int split,
+                            igemm_plan *out) {
+    igemm::ConvGeom g;
+    bool vg = false;
+    return igemm::make_conv_plan(elem_bytes, desc, X, W, Y, num_cu, kernel, split, out, &g, &vg);
+}
 
 }  // extern "C"

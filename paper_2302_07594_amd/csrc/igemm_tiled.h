@@ -1,4 +1,6 @@
-// Integer GEMM C += A B on gfx950 (CDNA4) int8 matrix cores.
+// Integer GEMM C += A B on gfx950 (CDNA4) int8 matrix cores: the fused
+// kernel template. The instantiations live in igemm_fused_*.hip, a few tile
+// shapes per translation unit so that the library compiles in parallel.
 //
 // Structure (the MI355X counterpart of the paper's blocked algorithm, Fig.
 // "baseline GEMM", and of its micro-kernel, Sec. 5.2):
@@ -30,6 +32,8 @@
 // beyond k are zero, so they add nothing to any term. Partial sums in one
 // workgroup stay below 2^31 because the host caps the k range per workgroup
 // (kMaxKChunk).
+#pragma once
+
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -42,6 +46,12 @@
 namespace igemm {
 namespace {
 
+// x / d for the invariant divisor d described by `dv` (exact for every x).
+__device__ __forceinline__ u32 divu(u32 x, DivU32 dv) {
+    const u32 t = __umulhi(x, dv.mul);
+    return (t + ((x - t) >> dv.s1)) >> dv.s2;
+}
+
 // Value of `v` in lane (lane ^ X) within each group of 32 lanes (ds_swizzle
 // in bit-mask mode: and-mask 0x1f, or-mask 0, xor-mask X).
 template <int X>
@@ -53,11 +63,15 @@ __device__ __forceinline__ u32 swz_xor(u32 v) {
 // ---------------------------------------------------------------------------
 // Small tiles (bm * bn <= 8192, LDS <= 64 KB) are held to 256 registers per
 // lane so that two workgroups share a compute unit; larger tiles take one.
-template <int ES, int BM, int BN, int WM, int WN, int MF, bool VA, bool VB, bool SPLIT>
+// AM selects where A comes from: 0, the row-major matrix A (lda); 1 and 2, the
+// IM2ROW rows of a convolution gathered from the NHWC input Ap (geometry g),
+// 16 bytes at a time (1: the channel count is a multiple of a 16-byte chunk,
+// so a chunk never straddles two filter taps) or element by element (2).
+template <int ES, int BM, int BN, int WM, int WN, int MF, bool VA, bool VB, bool SPLIT, int AM>
 __global__ void __launch_bounds__(256, BM * BN <= 32 * 256 ? 2 : 1)
 igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ Bp,
             int64_t ldb, int32_t *__restrict__ C, int64_t ldc, int m, int n, int k,
-            int kchunk, int tiles_m, int tiles_n) {
+            int kchunk, int tiles_m, int tiles_n, ConvGeom g) {
     constexpr int P = ES;                  // limb planes per operand
     constexpr int NACC = ES == 2 ? 3 : 1;  // accumulator sets
     typedef Mfma<MF> M;
@@ -256,7 +270,7 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     const int klen = kend - kbeg;
     const int64_t a_span = (int64_t)BM * lda * ES + (int64_t)klen * ES + 64;
     const int64_t b_span = (int64_t)(klen + 1) * ldb * ES + BN * ES + 64;
-    const bool rs_ok = a_span < 0x7fff0000 && b_span < 0x7fff0000;
+    const bool rs_ok = (AM != 0 || a_span < 0x7fff0000) && b_span < 0x7fff0000;
     const char *a_base = (const char *)Ap + ((int64_t)m0 * lda + kbeg) * ES;
     const char *b_base = (const char *)Bp + ((int64_t)kbeg * ldb + n0) * ES;
     const int64_t a_ext = ((int64_t)(m - 1 - m0) * lda + (k - kbeg)) * ES;
@@ -264,11 +278,13 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     // Rows that are not 16-byte aligned are read with dword-aligned loads
     // from a dword-aligned resource base and shifted into place
     // (v_alignbyte), five dwords per 16 bytes.
-    const u32 a_dl = (u32)((uintptr_t)a_base & 3), b_dl = (u32)((uintptr_t)b_base & 3);
-    const int a_rec = (int)min((a_ext + a_dl + 3) & ~(int64_t)3, (int64_t)0x7ffffff0);
+    const u32 a_dl = AM != 0 ? 0u : (u32)((uintptr_t)a_base & 3);
+    const u32 b_dl = (u32)((uintptr_t)b_base & 3);
+    const int a_rec = AM != 0 ? ((g.x_bytes + 3) & ~3)
+                              : (int)min((a_ext + a_dl + 3) & ~(int64_t)3, (int64_t)0x7ffffff0);
     const int b_rec = (int)min((b_ext + b_dl + 3) & ~(int64_t)3, (int64_t)0x7ffffff0);
-    const __amdgpu_buffer_rsrc_t Ars =
-        __builtin_amdgcn_make_buffer_rsrc((void *)(a_base - a_dl), 0, a_rec, 0x00020000);
+    const __amdgpu_buffer_rsrc_t Ars = __builtin_amdgcn_make_buffer_rsrc(
+        AM != 0 ? (void *)Ap : (void *)(a_base - a_dl), 0, a_rec, 0x00020000);
     const __amdgpu_buffer_rsrc_t Brs =
         __builtin_amdgcn_make_buffer_rsrc((void *)(b_base - b_dl), 0, b_rec, 0x00020000);
     const int lda_b = (int)(lda * ES), ldb_b = (int)(ldb * ES);
@@ -294,15 +310,80 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
             return v;
         }
     };
+    // IM2ROW: the output pixel of each A row this thread stages, decoded
+    // once: first input row and column of its window (a row past m gets a
+    // window that lies outside the image), and its image's first element.
+    int cv_iy0[AM != 0 ? ACT : 1], cv_ix0[AM != 0 ? ACT : 1], cv_img[AM != 0 ? ACT : 1];
+    if constexpr (AM != 0) {
+#pragma unroll
+        for (int s = 0; s < ACT; ++s) {
+            const u32 i = (u32)(m0 + a_row[s]);
+            const u32 img = divu(i, g.by_ohw);
+            const u32 rem = i - img * (u32)g.ohw;
+            const u32 oy = divu(rem, g.by_ow);
+            const u32 ox = rem - oy * (u32)g.ow;
+            const bool ok = (int)i < m;
+            cv_iy0[s] = ok ? (int)oy * g.sh - g.ph : -(1 << 30);
+            cv_ix0[s] = (int)ox * g.sw - g.pw;
+            cv_img[s] = ok ? (int)img * g.h * g.w * g.c : 0;
+        }
+    }
+    // Element offset in X of A[row of chunk s, column p], or -1 where the
+    // filter tap falls outside the image (zero padding) or p is past the end.
+    auto tap = [&](int s, u32 p) __attribute__((always_inline)) -> int {
+        const u32 fyx = divu(p, g.by_c);
+        const int ci = (int)(p - fyx * (u32)g.c);
+        const u32 fy = divu(fyx, g.by_s);
+        const int fx = (int)(fyx - fy * (u32)g.s);
+        const int iy = cv_iy0[s] + (int)fy * g.dh;
+        const int ix = cv_ix0[s] + fx * g.dw;
+        const bool in = (u32)iy < (u32)g.h && (u32)ix < (u32)g.w;
+        return in ? cv_img[s] + (iy * g.w + ix) * g.c + ci : -1;
+    };
+    // 16 bytes of IM2ROW row a_row[s] from element e of this workgroup's k
+    // range: one vector load (AM 1: the chunk lies within one filter tap),
+    // or one load per element (AM 2); out-of-image elements read as zero.
+    auto gather16 = [&](int s, int e) __attribute__((always_inline)) -> v4i {
+        const u32 p = (u32)(kbeg + e);
+        if constexpr (AM == 1) {
+            const int o = e < klen ? tap(s, p) : -1;
+            return __builtin_amdgcn_raw_buffer_load_b128(
+                Ars, o >= 0 ? (u32)o * ES : 0x80000000u, 0, 0);
+        } else {
+            u32 w4[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int t = 0; t < 16 / ES; ++t) {
+                const int o = e + t < klen ? tap(s, p + t) : -1;
+                const u32 off = o >= 0 ? (u32)o * ES : 0x80000000u;
+                u32 v;
+                if constexpr (ES == 2)
+                    v = (u32)__builtin_amdgcn_raw_buffer_load_b16(Ars, off, 0, 0);
+                else
+                    v = (u32)__builtin_amdgcn_raw_buffer_load_b8(Ars, off, 0, 0);
+                w4[(t * ES) >> 2] |= v << (8 * ((t * ES) & 3));
+            }
+            v4i r;
+            r.x = (int)w4[0];
+            r.y = (int)w4[1];
+            r.z = (int)w4[2];
+            r.w = (int)w4[3];
+            return r;
+        }
+    };
     // The k-tile starting kt0 elements after kbeg into register set R.
     auto load_rs = [&](auto par, int kt0) __attribute__((always_inline)) {
         constexpr int R = decltype(par)::value;
 #pragma unroll
         for (int s = 0; s < ACT; ++s) {
             const int e = kt0 + a_q[s] * (16 / ES);  // first element, from kbeg
-            const u32 off = (m0 + a_row[s] < m && e < klen) ? (u32)(a_row[s] * lda_b + e * ES)
-                                                           : 0x80000000u;
-            ra[R][s] = load16_rs(ic<VA>{}, Ars, off, a_dl);
+            if constexpr (AM == 0) {
+                const u32 off = (m0 + a_row[s] < m && e < klen)
+                                    ? (u32)(a_row[s] * lda_b + e * ES)
+                                    : 0x80000000u;
+                ra[R][s] = load16_rs(ic<VA>{}, Ars, off, a_dl);
+            } else {
+                ra[R][s] = gather16(s, e);
+            }
         }
 #pragma unroll
         for (int s = 0; s < BUT; ++s) {
@@ -481,10 +562,11 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
 
     // One unpipelined k-tile through LDS stage 0, loads range-checked.
     auto safe_tile = [&](int k0) __attribute__((always_inline)) {
-        if (rs_ok)
+        if (rs_ok) {
             load_rs(ic<0>{}, k0 - kbeg);
-        else
-            load_safe(ic<0>{}, k0);
+        } else {
+            if constexpr (AM == 0) load_safe(ic<0>{}, k0);
+        }
         if (k0 + 64 > kend)
             store_tile(ic<0>{}, ic<0>{}, ic<1>{}, k0);
         else
@@ -748,9 +830,10 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
 }
 
 // ---------------------------------------------------------------------------
+// Host stub of one GEMM variant (A row-major).
 template <int ES, int BM, int BN, int WM, int WN, int MF>
 const void *pick(bool va, bool vb, bool split) {
-#define IGEMM_K(a, b, s) (const void *)&igemm_tiled<ES, BM, BN, WM, WN, MF, a, b, s>
+#define IGEMM_K(a, b, s) (const void *)&igemm_tiled<ES, BM, BN, WM, WN, MF, a, b, s, 0>
     if (split) {
         if (va) return vb ? IGEMM_K(true, true, true) : IGEMM_K(true, false, true);
         return vb ? IGEMM_K(false, true, true) : IGEMM_K(false, false, true);
@@ -760,36 +843,19 @@ const void *pick(bool va, bool vb, bool split) {
 #undef IGEMM_K
 }
 
-const void *kernel_fn(int id, bool va, bool vb, bool split) {
-    switch (id) {
-        case K_I8_256x256: return pick<1, 256, 256, 128, 128, 32>(va, vb, split);
-        case K_I8_128x128: return pick<1, 128, 128, 64, 64, 32>(va, vb, split);
-        case K_I8_32x256: return pick<1, 32, 256, 32, 64, 32>(va, vb, split);
-        case K_I8_16x256: return pick<1, 16, 256, 16, 64, 16>(va, vb, split);
-        case K_I16_128x128: return pick<2, 128, 128, 64, 64, 32>(va, vb, split);
-        case K_I16_64x64: return pick<2, 64, 64, 32, 32, 32>(va, vb, split);
-        case K_I16_32x128: return pick<2, 32, 128, 32, 32, 32>(va, vb, split);
-        case K_I16_16x128: return pick<2, 16, 128, 16, 32, 16>(va, vb, split);
-        default: return nullptr;
+// Convolution variants (A gathered by IM2ROW; VA is unused) of the small
+// tiles, which the planner chooses for lowered convolutions.
+template <int ES, int BM, int BN, int WM, int WN, int MF>
+const void *pick_conv(bool vgather, bool vb, bool split) {
+#define IGEMM_C(am, b, s) (const void *)&igemm_tiled<ES, BM, BN, WM, WN, MF, false, b, s, am>
+    if (vgather) {
+        if (split) return vb ? IGEMM_C(1, true, true) : IGEMM_C(1, false, true);
+        return vb ? IGEMM_C(1, true, false) : IGEMM_C(1, false, false);
     }
+    if (split) return vb ? IGEMM_C(2, true, true) : IGEMM_C(2, false, true);
+    return vb ? IGEMM_C(2, true, false) : IGEMM_C(2, false, false);
+#undef IGEMM_C
 }
 
 }  // namespace
-
-int launch_tiled(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
-                 int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
-                 void *stream) {
-    (void)es;
-    const void *fn = kernel_fn(p.kernel, p.vec_a != 0, p.vec_b != 0, p.split > 1);
-    if (fn == nullptr) return IGEMM_EINVAL;
-    int mi = (int)m, ni = (int)n, ki = (int)k, kc = (int)p.k_chunk;
-    int tm = (int)((m + p.bm - 1) / p.bm), tn = (int)((n + p.bn - 1) / p.bn);
-    void *args[] = {(void *)&A, (void *)&lda, (void *)&B, (void *)&ldb, (void *)&C,
-                    (void *)&ldc, (void *)&mi, (void *)&ni, (void *)&ki, (void *)&kc,
-                    (void *)&tm, (void *)&tn};
-    hipError_t e = hipLaunchKernel(fn, dim3((unsigned)p.grid), dim3(kThreads), args, 0,
-                                   (hipStream_t)stream);
-    return e == hipSuccess ? IGEMM_OK : IGEMM_EHIP;
-}
-
 }  // namespace igemm

@@ -3,11 +3,14 @@
 
 Usage (the program itself goes after ``rocprofv3 ... --``):
     python paper_2302_07594_amd/profile_run.py gemm <workload> [iters] [case]
+    python paper_2302_07594_amd/profile_run.py conv <layer> [iters]
     python paper_2302_07594_amd/profile_run.py copy <MiB> [iters]
     python paper_2302_07594_amd/profile_run.py summarize <rocprof output dir>
 
 ``gemm`` runs the library's igemm call on the named workload's case (inputs
-generated as in the benchmark, C reset is not needed for timing).
+generated as in the benchmark, C reset is not needed for timing); ``conv``
+runs the convolution entry point on one of the six network layers (index
+into ``workloads.CONV2D_CASES``).
 ``copy`` runs a device-to-device copy of a tensor of the given size; its
 FETCH_SIZE / WRITE_SIZE readings calibrate the counters against a known byte
 count. ``summarize`` prints per-kernel average durations from a
@@ -39,6 +42,20 @@ def _gemm(wname: str, iters: int, case_idx: int) -> None:
     f = ig.gemm_i16 if case.dtype == "i16" else ig.gemm_i8
     for _ in range(iters):
         f(Ad, Bd, Cd)
+    torch.cuda.synchronize()
+    print(f"ran {case.name} x{iters}", flush=True)
+
+
+def _conv(layer: int, iters: int) -> None:
+    import torch
+
+    import paper_2302_07594_amd as ig
+    import workloads
+    case = workloads.CONV2D_CASES[layer]
+    X, W, Y = workloads.generate_conv(case)
+    Xd, Wd, Yd = (torch.from_numpy(x).cuda() for x in (X, W, Y))
+    for _ in range(iters):
+        ig.conv2d(Xd, Wd, Yd, stride=case.stride, pad=case.pad, dil=case.dil)
     torch.cuda.synchronize()
     print(f"ran {case.name} x{iters}", flush=True)
 
@@ -81,6 +98,8 @@ def main(argv) -> None:
     cmd = argv[1]
     if cmd == "gemm":
         _gemm(argv[2], int(argv[3]) if len(argv) > 3 else 3, int(argv[4]) if len(argv) > 4 else 0)
+    elif cmd == "conv":
+        _conv(int(argv[2]), int(argv[3]) if len(argv) > 3 else 3)
     elif cmd == "copy":
         _copy(int(argv[2]), int(argv[3]) if len(argv) > 3 else 3)
     elif cmd == "summarize":

@@ -269,3 +269,141 @@ def test_packed_b_calls_reject_bad_arguments(es):
     assert mul(64, 64, 64, FAKE_A, 64, P, 256, FAKE_C, 64, -1, W, big, s) == ig.IGEMM_ENOMEM
     assert mul(64, 64, 64, FAKE_A, 64, P, big, FAKE_C, 64, -1, W, 256, s) == ig.IGEMM_ENOMEM
     assert mul(0, 64, 64, FAKE_A, 64, 0, 0, FAKE_C, 64, -1, 0, 0, s) == ig.IGEMM_OK
+
+
+# ---- convolution entry points -----------------------------------------------
+
+FAKE_X, FAKE_W, FAKE_Y = FAKE_A, FAKE_B, FAKE_C
+
+
+def _cd(**kw):
+    base = dict(n=1, h=8, w=8, c=16, k=32, r=3, s=3, stride=(1, 1), pad=(1, 1), dil=(1, 1))
+    base.update(kw)
+    return ig.conv_desc(**base)
+
+
+def test_conv_header_declares_entry_points():
+    fns = declared_functions()
+    for name in ("igemm_conv2d_i16", "igemm_conv2d_i8", "igemm_conv2d_ex",
+                 "igemm_conv2d_query_plan", "igemm_conv2d_out_dim"):
+        assert name in fns
+
+
+def test_conv_out_dim_matches_oracle():
+    import oracle
+    for size in (0, 1, 2, 5, 7, 56, 224):
+        for f in (1, 2, 3, 7):
+            for st in (1, 2, 3):
+                for pd in (0, 1, 3):
+                    for dl in (1, 2):
+                        assert ig.igemm_conv2d_out_dim(size, f, st, pd, dl) == \
+                            oracle.conv2d_out_dim(size, f, st, pd, dl)
+    assert ig.igemm_conv2d_out_dim(224, 7, 2, 3, 1) == 112
+    assert ig.igemm_conv2d_out_dim(-1, 3, 1, 0, 1) == -1
+    assert ig.igemm_conv2d_out_dim(5, 0, 1, 0, 1) == -1
+    assert ig.igemm_conv2d_out_dim(5, 3, 0, 0, 1) == -1
+    assert ig.igemm_conv2d_out_dim(5, 3, 1, -1, 1) == -1
+    assert ig.igemm_conv2d_out_dim(5, 3, 1, 0, 0) == -1
+    big = (1 << 62) + 5
+    assert ig.igemm_conv2d_out_dim(8, 3, 1, big, 1) == -1      # 2*pad overflows
+    assert ig.igemm_conv2d_out_dim(8, 3, 1, 0, big) == -1      # dil*(r-1) overflows
+
+
+@pytest.mark.parametrize("es,fn", [(2, ig.igemm_conv2d_i16), (1, ig.igemm_conv2d_i8)])
+def test_conv_invalid_arguments(es, fn):
+    E = ig.IGEMM_EINVAL
+    X, W, Y = FAKE_X, FAKE_W, FAKE_Y
+    assert fn(_cd(n=-1), X, W, Y, 0) == E
+    assert fn(_cd(h=-1), X, W, Y, 0) == E
+    assert fn(_cd(c=-2), X, W, Y, 0) == E
+    assert fn(_cd(k=-1), X, W, Y, 0) == E
+    assert fn(_cd(r=0), X, W, Y, 0) == E
+    assert fn(_cd(s=0), X, W, Y, 0) == E
+    assert fn(_cd(stride=(0, 1)), X, W, Y, 0) == E
+    assert fn(_cd(stride=(1, 0)), X, W, Y, 0) == E
+    assert fn(_cd(pad=(-1, 0)), X, W, Y, 0) == E
+    assert fn(_cd(dil=(1, 0)), X, W, Y, 0) == E
+    assert fn(_cd(), 0, W, Y, 0) == E
+    assert fn(_cd(), X, 0, Y, 0) == E
+    assert fn(_cd(), X, W, 0, 0) == E
+    assert ig.igemm_conv2d_ex(3, _cd(), X, W, Y, 0) == E              # bad element size
+    if es == 2:
+        assert fn(_cd(), X + 1, W, Y, 0) == E                        # odd int16 X
+    else:
+        assert ig.igemm_conv2d_query_plan(1, _cd(), X=X + 1)["vec_a"] == 0
+    # kernels the lowering does not use, or of the other operand type
+    for kid in range(ig.igemm_num_kernels()):
+        name = ig.igemm_kernel_name(kid)
+        conv_ok = name in ("i16_64x64", "i16_32x128", "i16_16x128", "i8_32x256", "i8_16x256")
+        ok = conv_ok and name.startswith("i16" if es == 2 else "i8")
+        if not ok:
+            with pytest.raises(ig.IgemmError):
+                ig.igemm_conv2d_query_plan(es, _cd(), kernel=kid)
+    with pytest.raises(ig.IgemmError):
+        ig.igemm_conv2d_query_plan(es, _cd(), kernel=ig.igemm_num_kernels())
+    with pytest.raises(ig.IgemmError):
+        ig.igemm_conv2d_query_plan(es, _cd(), split=0)
+
+
+@pytest.mark.parametrize("fn", [ig.igemm_conv2d_i16, ig.igemm_conv2d_i8])
+def test_conv_noop_calls_return_ok_without_device(fn):
+    OK = ig.IGEMM_OK
+    assert fn(_cd(n=0), 0, 0, 0, 0) == OK
+    assert fn(_cd(k=0), 0, 0, 0, 0) == OK
+    assert fn(_cd(c=0), 0, 0, FAKE_Y, 0) == OK                  # k = r*s*c = 0: Y unchanged
+    assert fn(_cd(h=1, r=3, pad=(0, 0)), 0, 0, 0, 0) == OK      # window never fits: oh = 0
+    assert fn(_cd(w=2, s=2, dil=(1, 3), pad=(0, 0)), 0, 0, 0, 0) == OK
+    # a huge but empty problem is a no-op, not an overflow
+    assert fn(_cd(n=1 << 40, h=1 << 40, w=1 << 40, c=1 << 40, k=0), 0, 0, 0, 0) == OK
+    assert ig.igemm_conv2d_query_plan(2, _cd(n=0))["kernel"] == -1
+
+
+def test_conv_too_large_is_unsupported():
+    NS = ig.IGEMM_ENOTSUP
+    X, W, Y = FAKE_X, FAKE_W, FAKE_Y
+    # input above 2 GiB
+    assert ig.igemm_conv2d_i16(_cd(n=1, h=1 << 15, w=1 << 15, c=2, r=1, s=1, pad=(0, 0)),
+                               X, W, Y, 0) == NS
+    # padded image of 2^30 rows
+    assert ig.igemm_conv2d_i8(_cd(h=4, pad=((1 << 29), 1)), X, W, Y, 0) == NS
+    # lowered m beyond 2^31
+    assert ig.igemm_conv2d_i8(_cd(n=1 << 20, h=64, w=64, c=1, r=1, s=1, pad=(0, 0)),
+                              X, W, Y, 0) == NS
+    # filter tensor of 2 GiB
+    assert ig.igemm_conv2d_i16(_cd(c=1 << 14, k=1 << 14, r=3, s=3), X, W, Y, 0) == NS
+    # products beyond int64 are refused, not wrapped
+    assert ig.igemm_conv2d_i8(_cd(n=1 << 40, h=1 << 28, w=1 << 28, c=1, r=1, s=1,
+                                  pad=(0, 0)), X, W, Y, 0) == NS
+
+
+def test_conv_plans_match_lowered_gemm():
+    """The six layers' plans: the lowered GEMM shapes, fused kernels only,
+    16-byte gather exactly when c * element size is a multiple of 16."""
+    import workloads
+    for case in workloads.CONV2D_CASES:
+        m, n, k = case.gemm_shape()
+        d = ig.conv_desc(case.n, case.h, case.w, case.c, case.k, case.r, case.s, case.stride,
+                         case.pad, case.dil)
+        p = ig.igemm_conv2d_query_plan(2, d)
+        assert p["kernel_name"] in ("i16_64x64", "i16_32x128", "i16_16x128")
+        assert not p["packed"] and p["workspace_bytes"] == 0
+        assert p["vec_a"] == (1 if (case.c * 2) % 16 == 0 else 0)
+        assert p["split"] * p["k_chunk"] >= k > (p["split"] - 1) * p["k_chunk"]
+        bm, bn = (int(x) for x in p["kernel_name"].split("_")[-1].split("x"))
+        tiles = -(-m // bm) * -(-n // bn)
+        assert p["tiles"] == tiles and p["grid"] == tiles * p["split"]
+    d = ig.conv_desc(1, 56, 56, 64, 64, 3, 3, (1, 1), (1, 1), (1, 1))
+    assert ig.igemm_conv2d_query_plan(2, d, X=FAKE_X + 2)["vec_a"] == 0   # misaligned X
+    assert ig.igemm_conv2d_query_plan(1, d)["kernel_name"] == "i8_32x256"
+    d1 = ig.conv_desc(1, 4, 4, 64, 64, 1, 1)
+    assert ig.igemm_conv2d_query_plan(1, d1)["kernel_name"] == "i8_16x256"
+    assert ig.igemm_conv2d_query_plan(2, d1)["kernel_name"] == "i16_16x128"
+
+
+def test_conv_null_descriptor():
+    lib = ctypes.CDLL(ig.library_path())
+    for name in ("igemm_conv2d_i16", "igemm_conv2d_i8"):
+        fn = getattr(lib, name)
+        fn.argtypes = [ctypes.c_void_p] * 5
+        fn.restype = ctypes.c_int
+        assert fn(None, FAKE_X, FAKE_W, FAKE_Y, None) == ig.IGEMM_EINVAL

@@ -1,0 +1,203 @@
+"""GPU parity of the convolution entry points (IM2ROW lowering gathered while
+the A tiles are staged) against the oracle's direct convolution, element by
+element and bit-exact, through the C ABI."""
+import numpy as np
+import pytest
+
+import workloads
+from gpu_util import to_device
+
+pytestmark = pytest.mark.gpu
+
+CONV_KERNELS = {"i16": ("i16_64x64", "i16_32x128", "i16_16x128"),
+                "i8": ("i8_32x256", "i8_16x256")}
+SENTINEL = 0x5A5A5A5A
+
+
+def _ig():
+    import paper_2302_07594_amd as ig
+    return ig
+
+
+def _kid(name):
+    ig = _ig()
+    return [ig.igemm_kernel_name(i) for i in range(ig.igemm_num_kernels())].index(name)
+
+
+def _oracle(X, W, Y, stride, pad, dil):
+    import oracle
+    out = Y.copy()
+    oracle.conv2d(X, W, out, stride, pad, dil)
+    return out
+
+
+def _gpu(X, W, Y, stride, pad, dil, kernel=-1, split=-1, x_off=0, w_off=0):
+    """Run Y += conv(X, W) through igemm_conv2d_ex; Y sits in a larger buffer
+    whose tail holds sentinels that must survive. Returns Y as numpy."""
+    import torch
+    ig = _ig()
+    n, h, w, c = X.shape
+    r, s, _, k = W.shape
+    Xd = to_device(X, x_off)
+    Wd = to_device(W, w_off)
+    flat = torch.full((Y.size + 64,), SENTINEL, dtype=torch.int32, device="cuda")
+    flat[:Y.size].copy_(torch.from_numpy(Y.reshape(-1)).cuda())
+    es = 2 if X.dtype == np.int16 else 1
+    d = ig.conv_desc(n, h, w, c, k, r, s, stride, pad, dil)
+    st = ig.igemm_conv2d_ex(es, d, Xd.data_ptr(), Wd.data_ptr(), flat.data_ptr(),
+                            torch.cuda.current_stream().cuda_stream, kernel, split)
+    torch.cuda.synchronize()
+    assert st == 0, f"status {st}: {ig.igemm_strerror(st)}"
+    out = flat.cpu().numpy()
+    assert np.all(out[Y.size:] == SENTINEL), "write past the end of Y"
+    return out[:Y.size].reshape(Y.shape)
+
+
+def _describe(got, want, limit=5):
+    bad = np.argwhere(got != want)
+    lines = [f"{len(bad)} of {got.size} elements differ"]
+    for idx in bad[:limit]:
+        t = tuple(int(i) for i in idx)
+        lines.append(f"  Y{t} got {got[t]} want {want[t]}")
+    return "\n".join(lines)
+
+
+def _check(dt, n, h, w, c, k, r, s, stride=(1, 1), pad=(0, 0), dil=(1, 1), seed=0, **kw):
+    ig = _ig()
+    oh = ig.igemm_conv2d_out_dim(h, r, stride[0], pad[0], dil[0])
+    ow = ig.igemm_conv2d_out_dim(w, s, stride[1], pad[1], dil[1])
+    X, W, Y = workloads.random_conv_operands(dt, n, h, w, c, k, r, s, oh, ow, seed)
+    want = _oracle(X, W, Y, stride, pad, dil)
+    got = _gpu(X, W, Y, stride, pad, dil, **kw)
+    assert np.array_equal(got, want), _describe(got, want)
+    return got
+
+
+@pytest.mark.parametrize("case", workloads.CONV2D_CASES, ids=lambda c: c.name)
+def test_resnet_layers_full(case):
+    """The six network layers at full size with their value distributions
+    (automatic plan), every output compared."""
+    X, W, Y = workloads.generate_conv(case)
+    want = _oracle(X, W, Y, case.stride, case.pad, case.dil)
+    got = _gpu(X, W, Y, case.stride, case.pad, case.dil)
+    assert np.array_equal(got, want), _describe(got, want)
+    assert np.any(got != 0)
+
+
+# (n, h, w, c, k, r, s, stride, pad, dil): channel counts that take the 16-byte
+# gather and ones that do not, windows that straddle image and batch borders,
+# strides, dilations, padding wider than the filter, one-pixel outputs.
+SHAPES = [
+    (1, 9, 11, 8, 40, 3, 3, (1, 1), (1, 1), (1, 1)),
+    (2, 13, 10, 16, 70, 3, 3, (2, 2), (1, 1), (1, 1)),
+    (3, 7, 7, 3, 33, 7, 7, (2, 2), (3, 3), (1, 1)),
+    (1, 12, 17, 5, 129, 3, 2, (1, 2), (2, 0), (2, 1)),
+    (2, 6, 6, 32, 17, 1, 1, (1, 1), (0, 0), (1, 1)),
+    (1, 10, 9, 24, 64, 5, 3, (3, 1), (4, 2), (1, 3)),
+    (4, 5, 5, 1, 7, 2, 2, (1, 1), (0, 0), (1, 1)),
+    (1, 3, 3, 64, 256, 3, 3, (1, 1), (1, 1), (1, 1)),
+    (2, 4, 4, 48, 9, 4, 4, (1, 1), (0, 0), (1, 1)),   # one output pixel per image
+    (1, 20, 3, 72, 300, 3, 1, (2, 1), (0, 5), (1, 1)),  # padding beyond the filter
+]
+
+
+@pytest.mark.parametrize("dt", ["i16", "i8"])
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda t: "x".join(map(str, t[:7])))
+def test_every_conv_kernel(dt, shape):
+    """Every conv kernel of the type, automatic and forced k slices, on
+    ragged shapes (output pixels and channels not multiples of the tile,
+    k = r*s*c not a multiple of 64)."""
+    n, h, w, c, k, r, s, stride, pad, dil = shape
+    seed = 500 + sum(shape[:7])
+    for name in CONV_KERNELS[dt]:
+        for split in (-1, 1, 3):
+            _check(dt, n, h, w, c, k, r, s, stride, pad, dil, seed=seed, kernel=_kid(name),
+                   split=split)
+
+
+@pytest.mark.parametrize("dt", ["i16", "i8"])
+@pytest.mark.parametrize("x_off,w_off", [(1, 0), (0, 1), (3, 5)])
+def test_misaligned_tensors(dt, x_off, w_off):
+    """Bases off 16-byte alignment: element gather for X, element loads of W."""
+    for name in CONV_KERNELS[dt]:
+        _check(dt, 2, 11, 9, 16, 50, 3, 3, (1, 1), (1, 1), (1, 1), seed=31 + x_off + w_off,
+               kernel=_kid(name), x_off=x_off, w_off=w_off)
+
+
+def test_automatic_plans_on_small_layers():
+    """Automatic kernel choice across output sizes (16, 32, 64-row tiles)."""
+    for (n, hw, c, k) in ((1, 4, 64, 64), (1, 5, 32, 96), (1, 8, 40, 128), (2, 14, 24, 64),
+                          (1, 28, 16, 130)):
+        for dt in ("i16", "i8"):
+            _check(dt, n, hw, hw, c, k, 3, 3, (1, 1), (1, 1), (1, 1), seed=hw + c)
+
+
+def test_wraparound_extremes():
+    """All-minimum int16 inputs with a deep window: the exact sums exceed
+    2^31, so the result checks the modulo-2^32 update."""
+    n, h, w, c, k, r, s = 1, 8, 8, 512, 64, 3, 3
+    X = np.full((n, h, w, c), -32768, dtype=np.int16)
+    W = np.full((r, s, c, k), -32768, dtype=np.int16)
+    W[:, :, ::2, ::3] = 32767
+    Y = np.full((n, h, w, k), 2 ** 31 - 5, dtype=np.int32)
+    for name in CONV_KERNELS["i16"]:
+        want = _oracle(X, W, Y, (1, 1), (1, 1), (1, 1))
+        got = _gpu(X, W, Y, (1, 1), (1, 1), (1, 1), kernel=_kid(name))
+        assert np.array_equal(got, want), _describe(got, want)
+
+
+def test_zero_channels_and_empty_output_leave_y():
+    """k = r*s*c = 0 and a window that never fits are no-ops."""
+    import torch
+    ig = _ig()
+    Y = torch.full((1, 4, 4, 8), 7, dtype=torch.int32, device="cuda")
+    d = ig.conv_desc(1, 4, 4, 0, 8, 1, 1)
+    assert ig.igemm_conv2d_i16(d, 0, 0, Y.data_ptr()) == 0
+    d = ig.conv_desc(1, 2, 2, 4, 8, 3, 3)
+    assert ig.igemm_conv2d_i8(d, 0, 0, Y.data_ptr()) == 0
+    torch.cuda.synchronize()
+    assert bool((Y == 7).all())
+
+
+def test_tensor_wrapper_matches_oracle():
+    """conv2d() on torch tensors, both operand types."""
+    import torch
+    ig = _ig()
+    for dt in ("i16", "i8"):
+        X, W, Y = workloads.random_conv_operands(dt, 2, 15, 15, 24, 48, 3, 3, 8, 8, seed=9)
+        want = _oracle(X, W, Y, (2, 2), (1, 1), (1, 1))
+        Yd = torch.from_numpy(Y).cuda()
+        ig.conv2d(torch.from_numpy(X).cuda(), torch.from_numpy(W).cuda(), Yd, stride=(2, 2),
+                  pad=(1, 1))
+        torch.cuda.synchronize()
+        got = Yd.cpu().numpy()
+        assert np.array_equal(got, want), _describe(got, want)
+
+
+def test_graph_replays_match_oracle():
+    """A convolution captured in a HIP graph (it uses no workspace and no
+    memset): every replay adds conv(X, W) once more, checked after each
+    replay, with eager work on the stream between replays."""
+    import torch
+    ig = _ig()
+    X, W, Y = workloads.random_conv_operands("i16", 2, 14, 14, 32, 72, 3, 3, 7, 7, seed=21)
+    Xd, Wd, Yd = (torch.from_numpy(a).cuda() for a in (X, W, Y))
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        ig.conv2d(Xd, Wd, Yd, stride=(2, 2), pad=(1, 1))   # eager call before capture
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    want = _oracle(X, W, Y, (2, 2), (1, 1), (1, 1))
+    assert np.array_equal(Yd.cpu().numpy(), want), _describe(Yd.cpu().numpy(), want)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        ig.conv2d(Xd, Wd, Yd, stride=(2, 2), pad=(1, 1))
+    for rep in range(3):
+        g.replay()
+        scratch = torch.ones(1 << 16, device="cuda", dtype=torch.int32) * rep  # eager work
+        torch.cuda.synchronize()
+        want = _oracle(X, W, want, (2, 2), (1, 1), (1, 1))
+        got = Yd.cpu().numpy()
+        assert np.array_equal(got, want), f"replay {rep}: " + _describe(got, want)
+        del scratch

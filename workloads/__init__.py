@@ -18,6 +18,8 @@ Workloads (all row-major, C is int32):
                    convolution to one GEMM is Sec. 4.2). A uniform in [0,255]
                    (activations), B = rint(normal(0,32)) clipped to int16
                    (weights), C zero; layer i uses seed 40+i.
+* ``CONV2D_CASES`` the six ``i16_conv`` layers as real convolutions from an
+                   NHWC image (implicit GEMM), seeds 60+i.
 * ``i16_paper``    the paper's GEMM shape (4096, 4096, 290), int16 with the
                    recipe of i16_4096, seed 3 (context, not a graded workload).
 * ``i8_skinny``    six int8 GEMMs shaped like the projections of a 7B-class
@@ -131,6 +133,20 @@ def random_operands(dtype: str, m: int, n: int, k: int, seed: int,
     return A, B, C
 
 
+def random_conv_operands(dtype: str, n: int, h: int, w: int, c: int, k: int, r: int, s: int,
+                         oh: int, ow: int, seed: int, y_range: int = 1 << 20):
+    """Full-range random X (n x h x w x c), W (r x s x c x k) and a random
+    starting Y (n x oh x ow x k int32) for a convolution, drawn in that
+    order."""
+    et = _np_dtype(dtype)
+    lo, hi = (I16_MIN, I16_MAX) if dtype == "i16" else (I8_MIN, I8_MAX)
+    rng = np.random.default_rng(seed)
+    X = rng.integers(lo, hi, size=(n, h, w, c), dtype=et, endpoint=True)
+    W = rng.integers(lo, hi, size=(r, s, c, k), dtype=et, endpoint=True)
+    Y = rng.integers(-y_range, y_range, size=(n, oh, ow, k), dtype=np.int32, endpoint=True)
+    return X, W, Y
+
+
 _U16 = Dist("uniform", I16_MIN, I16_MAX)
 _U8 = Dist("uniform", I8_MIN, I8_MAX)
 _ZERO = Dist("zero")
@@ -202,6 +218,72 @@ WORKLOADS["i16_paper"] = Workload(
 )
 
 ORDER: List[str] = ["i16_256", "i16_4096", "i8_8192", "i16_conv", "i8_skinny"]
+
+
+@dataclass(frozen=True)
+class ConvCase:
+    """One convolution Y += conv(X, W): X n x h x w x c (NHWC), W r x s x c x k,
+    Y n x oh x ow x k, with strides, zero padding and dilations."""
+
+    name: str
+    dtype: str
+    n: int
+    h: int
+    w: int
+    c: int
+    k: int
+    r: int
+    s: int
+    stride: Tuple[int, int]
+    pad: Tuple[int, int]
+    dil: Tuple[int, int]
+    x: Dist
+    wt: Dist
+    seed: int
+
+    def out_hw(self):
+        def od(size, f, st, pd, dl):
+            span = size + 2 * pd - dl * (f - 1) - 1
+            return 0 if span < 0 else span // st + 1
+        return (od(self.h, self.r, self.stride[0], self.pad[0], self.dil[0]),
+                od(self.w, self.s, self.stride[1], self.pad[1], self.dil[1]))
+
+    def gemm_shape(self):
+        """(m, n, k) of the GEMM that IM2ROW lowers this convolution to."""
+        oh, ow = self.out_hw()
+        return self.n * oh * ow, self.k, self.r * self.s * self.c
+
+
+def generate_conv(case: ConvCase, seed: Optional[int] = None):
+    """Return (X, W, Y0) for ``case``: draws in the order X, W; Y0 is zero."""
+    rng = np.random.default_rng(case.seed if seed is None else seed)
+    et = _np_dtype(case.dtype)
+    X = draw(rng, case.x, (case.n, case.h, case.w, case.c), et)
+    W = draw(rng, case.wt, (case.r, case.s, case.c, case.k), et)
+    oh, ow = case.out_hw()
+    Y = np.zeros((case.n, oh, ow, case.k), dtype=np.int32)
+    return X, W, Y
+
+
+# The six layers of the conv-shaped GEMM set as convolutions on an NHWC image
+# (batch 1, 224 x 224 input): the 7x7 stride-2 stem, a 3x3 and a 1x1 layer at
+# 56 x 56, and the 3x3 stride-2 layers that open the next three stages. Their
+# IM2ROW lowerings have exactly the GEMM shapes of ``i16_conv``. Activations
+# uniform in [0, 255], weights rint(normal(0, 32)) clipped; layer i uses seed
+# 60 + i.
+CONV2D_LAYERS = (
+    ("stem_7x7s2", 224, 3, 64, 7, 2, 3),
+    ("c2_3x3", 56, 64, 64, 3, 1, 1),
+    ("c2_1x1", 56, 64, 256, 1, 1, 0),
+    ("c3_3x3s2", 56, 128, 128, 3, 2, 1),
+    ("c4_3x3s2", 28, 256, 256, 3, 2, 1),
+    ("c5_3x3s2", 14, 512, 512, 3, 2, 1),
+)
+CONV2D_CASES = tuple(
+    ConvCase(f"i16_conv2d_{i}_{nm}", "i16", 1, hw, hw, c, k, f, f, (st, st), (pd, pd), (1, 1),
+             Dist("uniform", 0, 255), Dist("normal_clip", I16_MIN, I16_MAX, 32.0), 60 + i)
+    for i, (nm, hw, c, k, f, st, pd) in enumerate(CONV2D_LAYERS)
+)
 
 
 def ops(case: Case) -> int:
