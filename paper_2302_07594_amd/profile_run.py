@@ -6,6 +6,7 @@ Usage (the program itself goes after ``rocprofv3 ... --``):
     python paper_2302_07594_amd/profile_run.py conv <layer> [iters]
     python paper_2302_07594_amd/profile_run.py copy <MiB> [iters]
     python paper_2302_07594_amd/profile_run.py summarize <rocprof output dir>
+    python paper_2302_07594_amd/profile_run.py traffic <rocprof output dir> <out.json>
 
 ``gemm`` runs the library's igemm call on the named workload's case (inputs
 generated as in the benchmark, C reset is not needed for timing); ``conv``
@@ -15,7 +16,13 @@ into ``workloads.CONV2D_CASES``).
 FETCH_SIZE / WRITE_SIZE readings calibrate the counters against a known byte
 count. ``summarize`` prints per-kernel average durations from a
 ``*_kernel_stats.csv`` and per-dispatch counter values from a
-``*_counter_collection.csv`` found under the directory.
+``*_counter_collection.csv`` found under the directory. ``traffic`` reads the
+four counter runs ``gemm_FETCH_SIZE``, ``gemm_WRITE_SIZE``, ``copy_FETCH_SIZE``
+and ``copy_WRITE_SIZE`` under the directory (the int16 4096^3 workload's
+multiply kernel and a 1024 MiB copy), scales the multiply's counters by what
+they read for the copy of known size, and writes the per-launch HBM bytes with
+the SHA-256 of the multiply kernel's source, which ``bench.py`` compares
+before it reports them.
 """
 from __future__ import annotations
 
@@ -91,6 +98,57 @@ def _summarize(d: str) -> None:
             print(f"dispatch {key} | {names[key][:90]} | {vals}")
 
 
+def _counter_rows(path: str, counter: str, keep):
+    """Per-dispatch values (KiB) of one counter for the kernels whose name
+    satisfies keep(name), in dispatch order."""
+    per = defaultdict(float)
+    for f in glob.glob(os.path.join(path, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] == counter and keep(r["Kernel_Name"]):
+                per[int(r["Dispatch_Id"])] += float(r["Counter_Value"])
+    return [per[k] for k in sorted(per)]
+
+
+def _traffic(d: str, out: str) -> None:
+    import hashlib
+    import json
+    src = os.path.join(_ROOT, "paper_2302_07594_amd", "csrc", "igemm_packed.hip")
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    def mult(name):
+        return "igemm_packed<2, 128, 128" in name
+
+    def copy(name):  # the copy runs launch one fill, then the copies
+        return "fill" not in name.lower()
+    fetch = _counter_rows(os.path.join(d, "gemm_FETCH_SIZE"), "FETCH_SIZE", mult)
+    write = _counter_rows(os.path.join(d, "gemm_WRITE_SIZE"), "WRITE_SIZE", mult)
+    cf = _counter_rows(os.path.join(d, "copy_FETCH_SIZE"), "FETCH_SIZE", copy)
+    cw = _counter_rows(os.path.join(d, "copy_WRITE_SIZE"), "WRITE_SIZE", copy)
+    if not (fetch and write and cf and cw):
+        raise SystemExit(f"missing counter rows: {len(fetch)} {len(write)} {len(cf)} {len(cw)}")
+    copied = 1024 << 20
+    fs = copied / (sum(cf) / len(cf) * 1024)   # bytes read per counter byte
+    ws = copied / (sum(cw) / len(cw) * 1024)
+    fb = sum(fetch) / len(fetch) * 1024 * fs
+    wb = sum(write) / len(write) * 1024 * ws
+    n = 4096
+    t = {
+        "kernel": "igemm_packed<2, 128, 128, 64, 64, 4> (int16 multiply on packed operands)",
+        "workload": "int16 4096x4096x4096, row-major, one-call igemm_i16 (pack, pack, multiply)",
+        "kernel_source_sha256": sha,
+        "fetch_size_kib_per_dispatch": fetch,
+        "write_size_kib_per_dispatch": write,
+        "copy_calibration": {"bytes_copied": copied, "fetch_size_kib": cf, "write_size_kib": cw,
+                             "fetch_scale": round(fs, 4), "write_scale": round(ws, 4)},
+        "fetch_bytes_per_launch": int(fb), "write_bytes_per_launch": int(wb),
+        "traffic_bytes_per_launch": int(fb + wb),
+        "algorithmic_bytes_per_launch": 2 * n * n * 2 + 8 * n * n,
+    }
+    with open(out, "w") as f:
+        json.dump(t, f, indent=1)
+    print(json.dumps({k: t[k] for k in ("fetch_bytes_per_launch", "write_bytes_per_launch",
+                                        "traffic_bytes_per_launch")}))
+
+
 def main(argv) -> None:
     if len(argv) < 2:
         print(__doc__)
@@ -104,6 +162,8 @@ def main(argv) -> None:
         _copy(int(argv[2]), int(argv[3]) if len(argv) > 3 else 3)
     elif cmd == "summarize":
         _summarize(argv[2])
+    elif cmd == "traffic":
+        _traffic(argv[2], argv[3])
     else:
         print(__doc__)
         sys.exit(2)
