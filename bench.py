@@ -14,7 +14,9 @@ Prints ONE JSON line. Besides the headline value it carries:
   roofline      the dominant kernel (the multiply) timed alone with HIP events
                 on the stream it is launched on, by running it on operands
                 packed once (the library's pack-once calls), against the
-                int8 matrix-core peak divided by the four limb products;
+                int8 matrix-core peak divided by the four limb products,
+                with the matrix-core utilisation, int8 operations and clock
+                rocprofv3 counted for that kernel (committed summary);
   cpu_baseline  the CPU oracle timed on the host cores over a bounded sample
                 of the same workload;
   per_config    every other workload, each timed the same way (memory-bound
@@ -70,6 +72,35 @@ def measured_traffic():
     if t.get("kernel_source_sha256") != kernel_source_hash():
         return None
     return t.get("traffic_bytes_per_launch")
+
+
+MFMA_FILES = {
+    "i16": os.path.join(ROOT, "profiles", "mfma_i16_packed_128x128_4096cube.json"),
+    "i8": os.path.join(ROOT, "profiles", "mfma_i8_packed_256x256_8192cube.json"),
+}
+
+
+def measured_mfma(dtype):
+    """Matrix-core figures of the packed multiply from the committed
+    rocprofv3 counter summary (SQ_VALU_MFMA_BUSY_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_I8,
+    GRBM_GUI_ACTIVE with a kernel trace), if taken on the current kernel
+    source; otherwise None."""
+    try:
+        with open(MFMA_FILES[dtype]) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256") != kernel_source_hash() or not t.get("dispatches"):
+        return None
+    rows = t["dispatches"]
+    avg = lambda key: sum(r[key] for r in rows) / len(rows)
+    return {
+        "mfma_busy": round(avg("mfma_busy"), 4),
+        "int8_mfma_ops_per_launch": rows[0]["int8_mfma_ops"],
+        "clock_ghz": round(avg("clock_ghz"), 3),
+        "dispatches": len(rows),
+        "source": os.path.relpath(MFMA_FILES[dtype], ROOT),
+    }
 
 
 def roofline_for(dtype, m, n, k, seconds):
@@ -133,6 +164,9 @@ def bench_case(case, min_sets=1, per_graph=40, reps=10, warmup=3):
         "us": round(t * 1e6, 2), "TOPS": round(2.0 * case.m * case.n * case.k / t / 1e12, 2),
         "bound": bound, "achieved": round(ach, 1), "peak": peak, "unit": unit,
         "frac": round(ach / peak, 4), "buffer_sets": nsets, "timing": "hip graph replay",
+        # the int8 counter summary was taken on this very workload
+        **({"rocprof_mfma": measured_mfma("i8")}
+           if (case.dtype, case.m, case.n, case.k) == ("i8", 8192, 8192, 8192) else {}),
     }
 
 
@@ -314,6 +348,7 @@ def main():
             "kernel_us": round(mult * 1e6, 2),
             "pack_us": round(pack_t * 1e6, 2),
             "step_device_us": round(step_dev * 1e6, 2),
+            "rocprof_mfma": measured_mfma("i16"),
         },
     }
     if not args.no_cpu_baseline:
