@@ -6,10 +6,12 @@ Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 and must never fall back to it.
 
 The arithmetic lives in ``igemm_oracle.c`` (plain int64 triple loop, reduced
-modulo 2^32 at the end; Sec. 4.1 definition of C += A B; and the direct
+modulo 2^32 at the end; Sec. 4.1 definition of C += A B; the direct
 definition of a zero-padded, strided, dilated 2-D convolution in NHWC / filter
-row x filter column x input channel x output channel layouts). This module
-only marshals numpy arrays into that library with ctypes.
+row x filter column x input channel x output channel layouts; and the int16
+output of the micro-kernel of Sec. 5.2, converted per k_c block by
+shift-round-saturate and added with wraparound). This module only marshals
+numpy arrays into that library with ctypes.
 """
 from __future__ import annotations
 
@@ -39,6 +41,11 @@ def _load():
     for name in ("oracle_conv2d_i16", "oracle_conv2d_i8"):
         fn = getattr(lib, name)
         fn.argtypes = [i64] * 13 + [vp, vp, vp]
+        fn.restype = ctypes.c_int
+    for name in ("oracle_igemm_srs_i16", "oracle_igemm_srs_i8"):
+        fn = getattr(lib, name)
+        fn.argtypes = [i64, i64, i64, vp, i64, vp, i64, vp, i64, i64, ctypes.c_int,
+                       ctypes.c_int]
         fn.restype = ctypes.c_int
     lib.oracle_conv2d_out_dim.argtypes = [i64] * 5
     lib.oracle_conv2d_out_dim.restype = i64
@@ -136,3 +143,29 @@ def conv2d(X: np.ndarray, W: np.ndarray, Y: np.ndarray, stride=(1, 1), pad=(0, 0
     if st != 0:
         raise RuntimeError(f"oracle returned {st}")
     return Y
+
+
+def igemm_srs(A: np.ndarray, B: np.ndarray, C: np.ndarray, kc: int = 0, shift: int = 0,
+              round_half_up: bool = False) -> np.ndarray:
+    """int16-output update in place on numpy views; returns C.
+
+    For each block of kc consecutive k indices (kc = 0: all of k), the exact
+    partial product is shifted right by ``shift`` (floor; with round_half_up
+    2^(shift-1) is added first), saturated to int16 and added into the int16
+    C modulo 2^16. A, B int16 or int8 (same type).
+    """
+    if A.dtype != B.dtype or A.dtype not in (np.int16, np.int8):
+        raise TypeError("A and B must both be int16 or both int8")
+    if C.dtype != np.int16:
+        raise TypeError("C must be int16")
+    m, k = A.shape
+    k2, n = B.shape
+    if k2 != k or C.shape != (m, n):
+        raise ValueError("shape mismatch")
+    lib = _load()
+    fn = lib.oracle_igemm_srs_i16 if A.dtype == np.int16 else lib.oracle_igemm_srs_i8
+    st = int(fn(m, n, k, _ptr(A), _ld(A, "A"), _ptr(B), _ld(B, "B"), _ptr(C), _ld(C, "C"),
+                int(kc), int(shift), 1 if round_half_up else 0))
+    if st != 0:
+        raise RuntimeError(f"oracle returned {st}")
+    return C

@@ -1,6 +1,8 @@
 /*
- * CPU oracle for integer GEMM  C += A * B, and for the convolution that the
- * paper lowers to it (at the end of this file) -- TEST INFRASTRUCTURE ONLY.
+ * CPU oracle for integer GEMM  C += A * B, for the convolution that the
+ * paper lowers to it, and for the int16-output variant with the paper's
+ * shift-round-saturate conversion (both further down) -- TEST
+ * INFRASTRUCTURE ONLY.
  *
  * Only the tests, the smoke check and the benchmark's CPU-baseline leg may
  * load this library. The GPU library never links, includes or calls it, and
@@ -211,3 +213,81 @@ int64_t oracle_conv2d_out_dim(int64_t in, int64_t f, int64_t stride, int64_t pad
 
 ORACLE_CONV2D(oracle_conv2d_i16, int16_t)
 ORACLE_CONV2D(oracle_conv2d_i8, int8_t)
+
+/*
+ * int16-output GEMM with the conversion of the paper's micro-kernel -- the
+ * epilogue of the listing of Sec. 5.2 (Fig. "simplified version of the
+ * micro-kernel"): after the k_c loop, each accumulator is converted to int16
+ * with a shift-round-saturate step and the converted micro-tile is added to
+ * the int16 micro-tile C_r. In the blocked algorithm (Fig. "baseline GEMM")
+ * the micro-kernel runs once per k_c block of loop L2, so the conversion is
+ * applied to each block's partial product separately.
+ *
+ * The paper does not define the conversion beyond its name and shift (0 in
+ * the listing), nor the addition's overflow rule; the readings taken:
+ *   for each block q of kc consecutive k indices (ascending; the last block
+ *   may be shorter; kc = 0 means one block holding all of k):
+ *     acc   = sum over p in block q of A[i,p] * B[p,j]     (exact, int64)
+ *     t     = floor((acc + r) / 2^shift), r = 2^(shift-1) if round_half_up
+ *             and shift > 0, else 0  (floor: the rounding of an arithmetic
+ *             shift)
+ *     t     = min(max(t, -32768), 32767)                   (saturation)
+ *     C[i,j] = (C[i,j] + t) modulo 2^16, as int16          (wraparound)
+ * Storage as for the GEMM oracle above, C being int16.
+ *
+ * Returns 0, or -1 for invalid arguments (negative sizes, kc < 0, shift
+ * outside [0, 47], leading dimensions too small).
+ */
+static int64_t floor_div_pow2(int64_t v, int shift)
+{
+    const int64_t d = (int64_t)1 << shift;
+    int64_t q = v / d; /* truncates toward zero */
+    if (v % d != 0 && v < 0)
+        q -= 1;
+    return q;
+}
+
+static int16_t wrap_to_i16(int64_t v)
+{
+    uint16_t u = (uint16_t)((uint64_t)v & 0xFFFFu);
+    if (u <= 0x7FFFu)
+        return (int16_t)u;
+    return (int16_t)((int32_t)u - 65536);
+}
+
+#define ORACLE_SRS(NAME, T)                                                                   \
+    int NAME(int64_t m, int64_t n, int64_t k, const T *A, int64_t lda, const T *B, int64_t ldb, \
+             int16_t *C, int64_t ldc, int64_t kc, int shift, int round_half_up)              \
+    {                                                                                         \
+        if (m < 0 || n < 0 || k < 0 || kc < 0 || shift < 0 || shift > 47)                     \
+            return -1;                                                                        \
+        if (m == 0 || n == 0)                                                                 \
+            return 0;                                                                         \
+        if (ldc < n || (k > 0 && (lda < k || ldb < n)))                                       \
+            return -1;                                                                        \
+        const int64_t blk = kc == 0 ? k : kc;                                                 \
+        const int64_t half = (round_half_up && shift > 0) ? ((int64_t)1 << (shift - 1)) : 0;  \
+        _Pragma("omp parallel for schedule(dynamic, 1)")                                      \
+        for (int64_t i = 0; i < m; ++i) {                                                     \
+            for (int64_t j = 0; j < n; ++j) {                                                 \
+                int64_t c = (int64_t)C[i * ldc + j];                                          \
+                for (int64_t p0 = 0; p0 < k; p0 += blk) {                                     \
+                    const int64_t p1 = p0 + blk < k ? p0 + blk : k;                           \
+                    int64_t acc = 0;                                                          \
+                    for (int64_t p = p0; p < p1; ++p)                                         \
+                        acc += (int64_t)A[i * lda + p] * (int64_t)B[p * ldb + j];             \
+                    int64_t t = floor_div_pow2(acc + half, shift);                            \
+                    if (t > 32767)                                                            \
+                        t = 32767;                                                            \
+                    if (t < -32768)                                                           \
+                        t = -32768;                                                           \
+                    c = (int64_t)wrap_to_i16(c + t);                                          \
+                }                                                                             \
+                C[i * ldc + j] = (int16_t)c;                                                  \
+            }                                                                                 \
+        }                                                                                     \
+        return 0;                                                                             \
+    }
+
+ORACLE_SRS(oracle_igemm_srs_i16, int16_t)
+ORACLE_SRS(oracle_igemm_srs_i8, int8_t)
