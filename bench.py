@@ -22,8 +22,10 @@ Prints ONE JSON line. Besides the headline value it carries:
   per_config    every other workload, each timed the same way (memory-bound
                 ones rotate through enough buffer sets to defeat the 256 MB
                 last-level cache), with its own roofline fraction; then the
-                paper's own GEMM shape (4096, 4096, 290), for context, and
-                the six network layers run as convolutions through the
+                paper's own GEMM shape (4096, 4096, 290), for context, the
+                same shape through the int16-output entry point with the
+                paper's k_c = 290 and shift 0 (and 4096^3 with k_c = 256),
+                and the six network layers run as convolutions through the
                 implicit-GEMM entry point (IM2ROW gathered in the kernel).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-extra]
@@ -167,6 +169,52 @@ def bench_case(case, min_sets=1, per_graph=40, reps=10, warmup=3):
         # the int8 counter summary was taken on this very workload
         **({"rocprof_mfma": measured_mfma("i8")}
            if (case.dtype, case.m, case.n, case.k) == ("i8", 8192, 8192, 8192) else {}),
+    }
+
+
+def bench_srs_case(case, kc, shift, per_graph=40, reps=10, warmup=3):
+    """Time the int16-output update (one fused launch per k block of kc,
+    shift-round-saturate conversion, int16 C) on a workload's A and B with a
+    random int16 C, like bench_case; the algorithmic bytes are A and B once
+    and the int16 C read and written once per block."""
+    import numpy as np
+    import torch
+
+    import paper_2302_07594_amd as ig
+    import workloads
+    A, B, _ = workloads.generate(case)
+    C = np.random.default_rng(case.seed).integers(-32768, 32767, size=(case.m, case.n),
+                                                  dtype=np.int16, endpoint=True)
+    set_bytes = A.nbytes + B.nbytes + C.nbytes
+    nsets = min(64, max(1, -(-2 * MALL_BYTES // set_bytes)))
+    Ad0, Bd0, Cd0 = (torch.from_numpy(x).cuda() for x in (A, B, C))
+    sets = [(Ad0, Bd0, Cd0)] + [(Ad0.clone(), Bd0.clone(), Cd0.clone()) for _ in range(nsets - 1)]
+    for i in range(warmup):
+        ig.gemm_srs(*sets[i % nsets], kc=kc, shift=shift)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(per_graph):
+            ig.gemm_srs(*sets[i % nsets], kc=kc, shift=shift)
+    g.replay()
+    torch.cuda.synchronize()
+    t = time_launches(lambda i: g.replay(), reps) / per_graph
+    m, n, k = case.m, case.n, case.k
+    nblocks = 1 if (kc == 0 or kc >= k) else -(-k // kc)
+    ops = 2.0 * m * n * k
+    nbytes = A.nbytes + B.nbytes + 4.0 * m * n * nblocks
+    peak_ops = PEAK_I16_TOPS * 1e12
+    if ops / nbytes >= peak_ops / (HBM_GBS * 1e9):
+        bound, ach, peak, unit = "mfma", ops / t / 1e12, peak_ops / 1e12, "TOPS"
+    else:
+        bound, ach, peak, unit = "hbm", nbytes / t / 1e9, HBM_GBS, "GB/s"
+    return {
+        "name": f"{case.name}_srs_kc{kc}_shift{shift}", "dtype": case.dtype,
+        "m": m, "n": n, "k": k, "kc": kc, "shift": shift, "blocks": nblocks,
+        "epilogue": "int16 C += sat16(floor(block product / 2^shift)) modulo 2^16",
+        "us": round(t * 1e6, 2), "TOPS": round(ops / t / 1e12, 2),
+        "bound": bound, "achieved": round(ach, 1), "peak": peak, "unit": unit,
+        "frac": round(ach / peak, 4), "buffer_sets": nsets, "timing": "hip graph replay",
     }
 
 
@@ -363,6 +411,13 @@ def main():
                 log(f"bench: per-config {c.name}")
                 per.append(bench_case(c))
                 torch.cuda.empty_cache()
+        # The paper's configuration: its GEMM shape with its k_c = 290 and the
+        # listing's shift 0, int16 output; and 4096^3 with k_c = 256.
+        log("bench: per-config int16-output update")
+        per.append(bench_srs_case(workloads.WORKLOADS["i16_paper"].cases[0], 290, 0))
+        per.append(bench_srs_case(workloads.WORKLOADS["i16_4096"].cases[0], 256, 0,
+                                  per_graph=10, reps=5))
+        torch.cuda.empty_cache()
         for c in workloads.CONV2D_CASES:
             log(f"bench: per-config {c.name}")
             per.append(bench_conv_case(c))

@@ -324,6 +324,52 @@ int igemm_conv2d_query_plan(int elem_bytes, const igemm_conv2d_desc *desc, const
 int64_t igemm_conv2d_out_dim(int64_t in, int64_t f, int64_t stride, int64_t pad,
                              int64_t dil);
 
+/*
+ * int16-output update with the conversion of the paper's micro-kernel (Sec.
+ * 5.2, the listing of the micro-kernel: after its k_c loop the accumulators
+ * are converted to int16 by a shift-round-saturate step and added to the
+ * int16 micro-tile C_r; in the blocked algorithm, Fig. "baseline GEMM", the
+ * micro-kernel runs once per k_c block of loop L2, so the conversion applies
+ * to each block's partial product):
+ *
+ *   for each block of kc consecutive k indices (ascending; the last block may
+ *   be shorter; kc = 0, or kc >= k, means one block holding all of k):
+ *     acc    = sum over p in the block of A[i,p] * B[p,j]     (exact)
+ *     t      = floor((acc + r) / 2^shift), r = 2^(shift-1) when round_half_up
+ *              is 1 and shift > 0, else 0 (an arithmetic shift right)
+ *     t      = min(max(t, -32768), 32767)                    (saturation)
+ *     C[i,j] = (C[i,j] + t) modulo 2^16                        (wraparound)
+ *
+ * The paper names the conversion and its shift (0 in its listing) but not the
+ * rounding or the overflow rule of the add; floor (the plain arithmetic
+ * shift), saturation to int16 and a wrapping add are the readings taken, and
+ * round_half_up = 1 selects round-half-up instead of floor.
+ *
+ * A (m x k, lda) and B (k x n, ldb) row-major int16 (igemm_i16_srs) or int8
+ * (igemm_i8_srs); C is int16, m x n, row-major with leading dimension ldc,
+ * updated in place; DEVICE pointers owned by the caller; any alignment.
+ * shift in [0, 47] (the paper's accumulators are 48 bits wide); kc >= 0 and a
+ * block of at most 32768 elements. One kernel launch per block, enqueued in
+ * order on `stream`; no workspace.
+ *
+ * Errors: IGEMM_EINVAL (before any HIP call, nothing enqueued) as for
+ * igemm_i16 and for kc < 0, shift outside [0, 47], round_half_up not 0 or 1;
+ * IGEMM_ENOTSUP for blocks longer than 32768 (or extents beyond 2^31 as for
+ * igemm_i16). m = 0, n = 0 or k = 0: IGEMM_OK, C unchanged.
+ */
+int igemm_i16_srs(int64_t m, int64_t n, int64_t k, const int16_t *A, int64_t lda,
+                  const int16_t *B, int64_t ldb, int16_t *C, int64_t ldc, int64_t kc, int shift,
+                  int round_half_up, void *stream);
+int igemm_i8_srs(int64_t m, int64_t n, int64_t k, const int8_t *A, int64_t lda,
+                 const int8_t *B, int64_t ldb, int16_t *C, int64_t ldc, int64_t kc, int shift,
+                 int round_half_up, void *stream);
+/* The same with elem_bytes 2 (int16) or 1 (int8) and an explicit kernel (one
+ * of the fused 16/32-row, 64x64 or int16 128x128 tile kernels of the operand
+ * type; -1 = automatic). For sweeps and tests. */
+int igemm_srs_ex(int elem_bytes, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
+                 const void *B, int64_t ldb, int16_t *C, int64_t ldc, int64_t kc, int shift,
+                 int round_half_up, void *stream, int kernel);
+
 /* Release the memory the library's workspace pool for the current device
  * holds beyond what in-flight calls use (hipMemPoolTrimTo). Returns
  * IGEMM_OK, or IGEMM_EHIP. */

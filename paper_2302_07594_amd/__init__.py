@@ -29,11 +29,15 @@ Same names as the C ABI:
     igemm_conv2d_query_plan(elem_bytes, desc, X=None, W=None, Y=None, num_cu=0,
                             kernel=-1, split=-1) -> dict
     igemm_conv2d_out_dim(in, f, stride, pad, dil)
+    igemm_i16_srs / igemm_i8_srs(m, n, k, A, lda, B, ldb, C, ldc, kc=0, shift=0,
+                                 round_half_up=0, stream=None)
+    igemm_srs_ex(elem_bytes, ..., stream=None, kernel=-1)
     igemm_strerror(status), igemm_kernel_name(i), igemm_num_kernels(),
     igemm_version()
 A, B, C may be integer device addresses or torch tensors (their data_ptr()).
 Tensor conveniences: gemm_i16(A, B, C) and gemm_i8(A, B, C) take 2-D CUDA
-tensors with unit stride along rows and update C in place; conv2d(X, W, Y,
+tensors with unit stride along rows and update C in place; gemm_srs(A, B, C,
+kc, shift, round_half_up) the same with an int16 C; conv2d(X, W, Y,
 stride, pad, dil) takes contiguous NHWC / (r, s, c, k) / NHWC tensors; a workspace the
 call needs is taken from torch's caching allocator (so the calls can be
 captured into a torch CUDA graph) unless workspace="library" asks for the
@@ -129,6 +133,12 @@ def _load():
     lib.igemm_conv2d_query_plan.argtypes = [ci, cd, vp, vp, vp, ci, ci, ci,
                                             ctypes.POINTER(_Plan)]
     lib.igemm_conv2d_query_plan.restype = ci
+    for name in ("igemm_i16_srs", "igemm_i8_srs"):
+        getattr(lib, name).argtypes = [i64, i64, i64, vp, i64, vp, i64, vp, i64, i64, ci, ci, vp]
+        getattr(lib, name).restype = ci
+    lib.igemm_srs_ex.argtypes = [ci, i64, i64, i64, vp, i64, vp, i64, vp, i64, i64, ci, ci, vp,
+                                 ci]
+    lib.igemm_srs_ex.restype = ci
     lib.igemm_conv2d_out_dim.argtypes = [i64] * 5
     lib.igemm_conv2d_out_dim.restype = i64
     lib.igemm_trim_workspace.argtypes = []
@@ -547,6 +557,50 @@ def gemm_i16(A, B, C, stream=None, kernel=-1, split=-1, workspace=None):
 def gemm_i8(A, B, C, stream=None, kernel=-1, split=-1, workspace=None):
     """C += A.B for 2-D torch.int8 CUDA tensors; see gemm_i16."""
     return _gemm(1, A, B, C, stream, kernel, split, workspace, "gemm_i8")
+
+
+# ---- int16-output update (shift-round-saturate per k block) -----------------
+
+def igemm_i16_srs(m, n, k, A, lda, B, ldb, C, ldc, kc=0, shift=0, round_half_up=0,
+                  stream=None) -> int:
+    """int16 C += srs(A B) per k block (see include/igemm.h). Returns the status."""
+    return int(_lib.igemm_i16_srs(m, n, k, _addr(A), lda, _addr(B), ldb, _addr(C), ldc, kc,
+                                  int(shift), int(round_half_up), _stream(stream)))
+
+
+def igemm_i8_srs(m, n, k, A, lda, B, ldb, C, ldc, kc=0, shift=0, round_half_up=0,
+                 stream=None) -> int:
+    return int(_lib.igemm_i8_srs(m, n, k, _addr(A), lda, _addr(B), ldb, _addr(C), ldc, kc,
+                                 int(shift), int(round_half_up), _stream(stream)))
+
+
+def igemm_srs_ex(elem_bytes, m, n, k, A, lda, B, ldb, C, ldc, kc=0, shift=0, round_half_up=0,
+                 stream=None, kernel=-1) -> int:
+    return int(_lib.igemm_srs_ex(int(elem_bytes), m, n, k, _addr(A), lda, _addr(B), ldb,
+                                 _addr(C), ldc, kc, int(shift), int(round_half_up),
+                                 _stream(stream), int(kernel)))
+
+
+def gemm_srs(A, B, C, kc=0, shift=0, round_half_up=False, stream=None, kernel=-1):
+    """int16 C += srs(A B) for 2-D CUDA tensors: A (m x k) and B (k x n) both
+    torch.int16 or both torch.int8, C (m x n) torch.int16, rows with unit
+    stride. Per block of kc k indices (0: all of k) the exact product is
+    shifted right by `shift` (floor, or round-half-up), saturated to int16
+    and added to C modulo 2^16. Returns C."""
+    import torch
+    if A.dtype not in (torch.int16, torch.int8) or B.dtype != A.dtype:
+        raise TypeError("gemm_srs: A and B must both be torch.int16 or both torch.int8")
+    if C.dtype != torch.int16:
+        raise TypeError("gemm_srs: C must be torch.int16")
+    # the shared checks expect an int32 C: check a stand-in of C's shape
+    stand_in = torch.empty_strided(C.shape, C.stride(), dtype=torch.int32, device=C.device)
+    m, n, k, lda, ldb, ldc = _check_tensors(A, B, stand_in, A.dtype, "gemm_srs")
+    es = 2 if A.dtype == torch.int16 else 1
+    st = igemm_srs_ex(es, m, n, k, A, lda, B, ldb, C, ldc, kc, shift,
+                      1 if round_half_up else 0, stream, kernel)
+    if st != IGEMM_OK:
+        raise IgemmError(st, "gemm_srs")
+    return C
 
 
 # ---- convolution through its IM2ROW lowering --------------------------------

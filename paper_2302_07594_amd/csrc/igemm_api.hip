@@ -239,10 +239,65 @@ int run_conv(int es, const igemm_conv2d_desc *d, const void *X, const void *W, i
                        stream);
 }
 
+// int16-output update: one launch per k block of kc elements, in order. All
+// blocks are planned before the first launch, so an error enqueues nothing.
+int run_srs(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, const void *B,
+            int64_t ldb, int16_t *C, int64_t ldc, int64_t kc, int shift, int round_half_up,
+            void *stream, int kernel) {
+    int st = validate(es, m, n, k, A, lda, B, ldb, C, ldc);
+    if (st != IGEMM_OK) return st;
+    if (kc < 0 || shift < 0 || shift > 47 || (round_half_up != 0 && round_half_up != 1) ||
+        kernel < -1 || kernel >= K_COUNT)
+        return IGEMM_EINVAL;
+    if (m == 0 || n == 0 || k == 0) return IGEMM_OK;
+    const int64_t blk = (kc == 0 || kc > k) ? k : kc;
+    const int64_t nblocks = (k + blk - 1) / blk;
+    for (int pass = 0; pass < 2; ++pass) {
+        const int num_cu = pass == 0 ? 0 : num_cu_of_current_device();
+        for (int64_t q = 0; q < nblocks; ++q) {
+            const int64_t p0 = q * blk;
+            const int64_t kb = p0 + blk < k ? blk : k - p0;
+            const char *Aq = (const char *)A + p0 * es;
+            const char *Bq = (const char *)B + p0 * ldb * es;
+            igemm_plan p;
+            st = make_srs_plan(es, m, n, kb, Aq, lda, Bq, ldb, ldc, num_cu, kernel, &p);
+            if (st != IGEMM_OK) return st;
+            if (pass == 1) {
+                st = launch_srs(es, p, m, n, kb, Aq, lda, Bq, ldb, C, ldc, shift, round_half_up,
+                                stream);
+                if (st != IGEMM_OK) return st;
+            }
+        }
+    }
+    return IGEMM_OK;
+}
+
 }  // namespace
 }  // namespace igemm
 
 extern "C" {
+
+int igemm_i16_srs(int64_t m, int64_t n, int64_t k, const int16_t *A, int64_t lda,
+                  const int16_t *B, int64_t ldb, int16_t *C, int64_t ldc, int64_t kc, int shift,
+                  int round_half_up, void *stream) {
+    return igemm::run_srs(2, m, n, k, A, lda, B, ldb, C, ldc, kc, shift, round_half_up, stream,
+                          -1);
+}
+
+int igemm_i8_srs(int64_t m, int64_t n, int64_t k, const int8_t *A, int64_t lda,
+                 const int8_t *B, int64_t ldb, int16_t *C, int64_t ldc, int64_t kc, int shift,
+                 int round_half_up, void *stream) {
+    return igemm::run_srs(1, m, n, k, A, lda, B, ldb, C, ldc, kc, shift, round_half_up, stream,
+                          -1);
+}
+
+int igemm_srs_ex(int elem_bytes, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
+                 const void *B, int64_t ldb, int16_t *C, int64_t ldc, int64_t kc, int shift,
+                 int round_half_up, void *stream, int kernel) {
+    if (elem_bytes != 1 && elem_bytes != 2) return IGEMM_EINVAL;
+    return igemm::run_srs(elem_bytes, m, n, k, A, lda, B, ldb, C, ldc, kc, shift, round_half_up,
+                          stream, kernel);
+}
 
 int igemm_conv2d_i16(const igemm_conv2d_desc *desc, const int16_t *X, const int16_t *W,
                      int32_t *Y, void *stream) {

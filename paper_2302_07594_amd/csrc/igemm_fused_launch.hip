@@ -44,9 +44,10 @@ int launch_tiled(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, c
     int mi = (int)m, ni = (int)n, ki = (int)k, kc = (int)p.k_chunk;
     int tm = (int)((m + p.bm - 1) / p.bm), tn = (int)((n + p.bn - 1) / p.bn);
     ConvGeom g = {};
+    int epi = 0;
     void *args[] = {(void *)&A, (void *)&lda, (void *)&B, (void *)&ldb, (void *)&C,
                     (void *)&ldc, (void *)&mi, (void *)&ni, (void *)&ki, (void *)&kc,
-                    (void *)&tm, (void *)&tn, (void *)&g};
+                    (void *)&tm, (void *)&tn, (void *)&g, (void *)&epi};
     hipError_t e = hipLaunchKernel(fn, dim3((unsigned)p.grid), dim3(kThreads), args, 0,
                                    (hipStream_t)stream);
     return e == hipSuccess ? IGEMM_OK : IGEMM_EHIP;
@@ -62,9 +63,30 @@ int launch_conv(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, co
     int tm = (int)((m + p.bm - 1) / p.bm), tn = (int)((n + p.bn - 1) / p.bn);
     int64_t lda = k, ldb = n;
     ConvGeom gg = g;
+    int epi = 0;
     void *args[] = {(void *)&X, (void *)&lda, (void *)&W, (void *)&ldb, (void *)&Y,
                     (void *)&ldy, (void *)&mi, (void *)&ni, (void *)&ki, (void *)&kc,
-                    (void *)&tm, (void *)&tn, (void *)&gg};
+                    (void *)&tm, (void *)&tn, (void *)&gg, (void *)&epi};
+    hipError_t e = hipLaunchKernel(fn, dim3((unsigned)p.grid), dim3(kThreads), args, 0,
+                                   (hipStream_t)stream);
+    return e == hipSuccess ? IGEMM_OK : IGEMM_EHIP;
+}
+
+int launch_srs(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+               int64_t lda, const void *B, int64_t ldb, int16_t *C, int64_t ldc, int shift,
+               int round_half_up, void *stream) {
+    (void)es;
+    if (p.split != 1) return IGEMM_EINVAL;
+    const void *fn = fused_srs(p.kernel, p.vec_a != 0, p.vec_b != 0);
+    if (fn == nullptr) return IGEMM_EINVAL;
+    int mi = (int)m, ni = (int)n, ki = (int)k, kc = (int)p.k_chunk;
+    int tm = (int)((m + p.bm - 1) / p.bm), tn = (int)((n + p.bn - 1) / p.bn);
+    ConvGeom g = {};
+    int epi = (shift & 0xff) | (round_half_up ? 0x100 : 0);
+    int32_t *Cp = (int32_t *)C;  // the kernel reads it as int16 for this variant
+    void *args[] = {(void *)&A, (void *)&lda, (void *)&B, (void *)&ldb, (void *)&Cp,
+                    (void *)&ldc, (void *)&mi, (void *)&ni, (void *)&ki, (void *)&kc,
+                    (void *)&tm, (void *)&tn, (void *)&g, (void *)&epi};
     hipError_t e = hipLaunchKernel(fn, dim3((unsigned)p.grid), dim3(kThreads), args, 0,
                                    (hipStream_t)stream);
     return e == hipSuccess ? IGEMM_OK : IGEMM_EHIP;

@@ -98,6 +98,12 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
 void packed_layout(int es, int64_t m, int64_t n, int64_t k, int kernel, const void *A,
                    int64_t lda, PackedLayout *L);
 
+// Plan of one k block (kb <= kMaxKChunk elements) of the int16-output
+// update: a small-tile fused kernel, one workgroup per output tile.
+bool srs_kernel(int id);
+int make_srs_plan(int es, int64_t m, int64_t n, int64_t kb, const void *A, int64_t lda,
+                  const void *B, int64_t ldb, int64_t ldc, int num_cu, int kernel,
+                  igemm_plan *out);
 // Output extent of one spatial dimension of a convolution (-1 if invalid).
 int64_t conv_out_dim(int64_t in, int64_t f, int64_t stride, int64_t pad, int64_t dil);
 // Plan of a convolution as its lowered GEMM, with the kernel's geometry.
@@ -125,11 +131,17 @@ const void *fused_i16_wide(int id, bool va, bool vb, bool split);
 const void *fused_i16_rows(int id, bool va, bool vb, bool split);
 const void *fused_conv_i16(int id, bool vgather, bool vb, bool split);
 const void *fused_conv_i8(int id, bool vgather, bool vb, bool split);
+const void *fused_srs(int id, bool va, bool vb);
 // The same fused kernels with A gathered from the NHWC input X by IM2ROW
 // (vector gather when a 16-byte chunk of A never straddles two filter taps).
 int launch_conv(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const ConvGeom &g,
                 bool vec_gather, const void *X, const void *W, int32_t *Y, int64_t ldy,
                 void *stream);
+// The int16-output update of one k block (plan without k slices): C16 +=
+// srs(A B) modulo 2^16 with the given shift and rounding.
+int launch_srs(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+               int64_t lda, const void *B, int64_t ldb, int16_t *C, int64_t ldc, int shift,
+               int round_half_up, void *stream);
 // The packed path: pack A into an A part (optionally clearing the B part's
 // column corrections, which pack_b then adds into), pack B into a B part
 // (clear_corr: clear the corrections itself first), multiply (one launch per

@@ -322,6 +322,37 @@ int64_t conv_out_dim(int64_t in, int64_t f, int64_t stride, int64_t pad, int64_t
     return span < 0 ? 0 : span / stride + 1;
 }
 
+// One k block of the int16-output update (the conversion of Sec. 5.2 applies
+// per block, so a block is never sliced across workgroups): int16 128x128
+// tiles when they fill the chip, else 64x64 when there are enough of them,
+// else 32- or 16-row tiles; int8 32- or 16-row tiles.
+bool srs_kernel(int id) {
+    return id == K_I16_128x128 || id == K_I16_64x64 || id == K_I16_32x128 ||
+           id == K_I16_16x128 || id == K_I8_32x256 || id == K_I8_16x256;
+}
+
+int make_srs_plan(int es, int64_t m, int64_t n, int64_t kb, const void *A, int64_t lda,
+                  const void *B, int64_t ldb, int64_t ldc, int num_cu, int kernel,
+                  igemm_plan *out) {
+    if (kb > kMaxKChunk) return IGEMM_ENOTSUP;
+    if (num_cu <= 0) num_cu = 256;
+    int id = kernel;
+    if (id < 0) {
+        if (es == 2 && tiles_of(K_I16_128x128, m, n) >= num_cu)
+            id = K_I16_128x128;
+        else if (es == 2)
+            id = tiles_of(K_I16_64x64, m, n) >= 32 ? K_I16_64x64
+                                                    : (m <= 16 ? K_I16_16x128 : K_I16_32x128);
+        else
+            id = m <= 16 ? K_I8_16x256 : K_I8_32x256;
+    }
+    if (id >= K_COUNT || !srs_kernel(id) || kKernels[id].es != es) return IGEMM_EINVAL;
+    const int st = make_plan(es, m, n, kb, A, lda, B, ldb, ldc, num_cu, id, 1, false, out);
+    if (st != IGEMM_OK) return st;
+    if (out->kernel >= 0 && out->split != 1) return IGEMM_ENOTSUP;
+    return IGEMM_OK;
+}
+
 // A convolution planned as the GEMM its IM2ROW lowering gives (Sec. 4.2):
 // m = n * oh * ow output pixels, n_gemm = output channels, k = r * s * c.
 int make_conv_plan(int es, const igemm_conv2d_desc *d, const void *X, const void *W,

@@ -67,11 +67,16 @@ __device__ __forceinline__ u32 swz_xor(u32 v) {
 // IM2ROW rows of a convolution gathered from the NHWC input Ap (geometry g),
 // 16 bytes at a time (1: the channel count is a multiple of a 16-byte chunk,
 // so a chunk never straddles two filter taps) or element by element (2).
-template <int ES, int BM, int BN, int WM, int WN, int MF, bool VA, bool VB, bool SPLIT, int AM>
+// EPI selects the update of C: 0, int32 C += A B modulo 2^32; 1, int16 C
+// (passed through the int32 pointer) += srs(A B), the product converted to
+// int16 by an arithmetic shift right by (epi & 0xff) bits, after adding half
+// a unit when bit 8 of epi is set, and saturation, then added modulo 2^16.
+template <int ES, int BM, int BN, int WM, int WN, int MF, bool VA, bool VB, bool SPLIT, int AM,
+          int EPI = 0>
 __global__ void __launch_bounds__(256, BM * BN <= 32 * 256 ? 2 : 1)
 igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ Bp,
             int64_t ldb, int32_t *__restrict__ C, int64_t ldc, int m, int n, int k,
-            int kchunk, int tiles_m, int tiles_n, ConvGeom g) {
+            int kchunk, int tiles_m, int tiles_n, ConvGeom g, int epi) {
     constexpr int P = ES;                  // limb planes per operand
     constexpr int NACC = ES == 2 ? 3 : 1;  // accumulator sets
     typedef Mfma<MF> M;
@@ -91,6 +96,8 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     constexpr int NST = 4;  // LDS stages of the pipeline
     static_assert(NST * STAGE >= 4 * 2 * (BM + BN), "LDS reuse for the limb sums");
     static_assert(NST * STAGE <= 160 * 1024, "gfx950 LDS");
+    // The int16 conversion is not additive: one workgroup owns each output.
+    static_assert(EPI == 0 || !SPLIT, "no k slices with the int16-output update");
 
     __shared__ __attribute__((aligned(16))) char smem[NST * STAGE];
 
@@ -98,7 +105,7 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     // or three dependent round trips would open every workgroup. Naming them
     // all here issues their loads together.
     asm volatile("" ::"s"(Ap), "s"(lda), "s"(Bp), "s"(ldb), "s"(C), "s"(ldc), "s"(m), "s"(n),
-                 "s"(k), "s"(kchunk), "s"(tiles_m), "s"(tiles_n), "s"(gridDim.x));
+                 "s"(k), "s"(kchunk), "s"(tiles_m), "s"(tiles_n), "s"(gridDim.x), "s"(epi));
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -590,30 +597,65 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     // range, which the hardware reads as zero and does not write, so loads
     // and stores need no branch per element. Otherwise 64-bit addresses with
     // a branch per element.
-    const bool c_rsrc = (int64_t)BM * ldc * 4 < 0x7fff0000;
-    const __amdgpu_buffer_rsrc_t Crs =
-        __builtin_amdgcn_make_buffer_rsrc(C + (int64_t)m0 * ldc + n0, 0, 0x7fffffff, 0x00020000);
+    constexpr int CE = EPI == 1 ? 2 : 4;  // bytes per C element
+    int16_t *const C16 = (int16_t *)C;
+    const bool c_rsrc = (int64_t)BM * ldc * CE < 0x7fff0000;
+    const __amdgpu_buffer_rsrc_t Crs = __builtin_amdgcn_make_buffer_rsrc(
+        (char *)C + ((int64_t)m0 * ldc + n0) * CE, 0, 0x7fffffff, 0x00020000);
     const int ldc32 = (int)ldc;
     auto c_off = [&](int lr, int lc) __attribute__((always_inline)) -> u32 {
-        return (m0 + lr < m && n0 + lc < n) ? (u32)(lr * ldc32 + lc) * 4u : 0x80000000u;
+        return (m0 + lr < m && n0 + lc < n) ? (u32)(lr * ldc32 + lc) * (u32)CE : 0x80000000u;
+    };
+    // One element of C through the resource (int16 C sign-extended).
+    auto c_load = [&](u32 off) __attribute__((always_inline)) -> int32_t {
+        if constexpr (EPI == 1)
+            return (int32_t)(int16_t)__builtin_amdgcn_raw_buffer_load_b16(Crs, off, 0, 0);
+        else
+            return __builtin_amdgcn_raw_buffer_load_b32(Crs, off, 0, 0);
+    };
+    // The int16 conversion: shift and rounding offset.
+    const int srs_shift = epi & 0xff;
+    const int64_t srs_half =
+        ((epi >> 8) & 1) != 0 && srs_shift > 0 ? (int64_t)1 << (srs_shift - 1) : 0;
+    auto srs16 = [&](int64_t a) __attribute__((always_inline)) -> int32_t {
+        const int64_t t = (a + srs_half) >> srs_shift;  // arithmetic: floor
+        return (int32_t)(t > 32767 ? 32767 : (t < -32768 ? -32768 : t));
     };
     auto epilogue = [&](auto pre) __attribute__((always_inline)) {
         constexpr bool PRE = decltype(pre)::value != 0;
         // int16 correction terms of this k range, per row and per column,
         // parked in LDS: row i gets 32768 sum(H_A[i,:]) + 128 sum(L_A[i,:]),
         // column j the same of B plus the constant 16384 * (k range).
+        // With the int16 conversion the sums stay separate and exact (two
+        // words per row and per column): the conversion needs the product
+        // itself, not its residue modulo 2^32.
+        constexpr int RW = EPI == 1 ? 2 : 1;
         u32 *sR = (u32 *)smem;
-        u32 *sK = sR + BM;
+        u32 *sK = sR + RW * BM;
         if constexpr (ES == 2) {
             // The eight 16-byte chunks of one row of A were staged by eight
             // consecutive lanes: a butterfly over them gives the row total.
 #pragma unroll
             for (int s = 0; s < ACT; ++s) {
-                u32 v = 32768u * (u32)sah[s] + 128u * (u32)sal[s];
-                v += swz_xor<1>(v);
-                v += swz_xor<2>(v);
-                v += swz_xor<4>(v);
-                if (!a_dup[s] && a_q[s] == 0) sR[a_row[s]] = v;
+                if constexpr (EPI == 1) {
+                    u32 vh = (u32)sah[s], vl = (u32)sal[s];
+                    vh += swz_xor<1>(vh);
+                    vl += swz_xor<1>(vl);
+                    vh += swz_xor<2>(vh);
+                    vl += swz_xor<2>(vl);
+                    vh += swz_xor<4>(vh);
+                    vl += swz_xor<4>(vl);
+                    if (!a_dup[s] && a_q[s] == 0) {
+                        sR[2 * a_row[s]] = vh;
+                        sR[2 * a_row[s] + 1] = vl;
+                    }
+                } else {
+                    u32 v = 32768u * (u32)sah[s] + 128u * (u32)sal[s];
+                    v += swz_xor<1>(v);
+                    v += swz_xor<2>(v);
+                    v += swz_xor<4>(v);
+                    if (!a_dup[s] && a_q[s] == 0) sR[a_row[s]] = v;
+                }
             }
             // Sixteen consecutive lanes staged four rows each of the same
             // eight columns of B: a reduce-scatter over them (halving the
@@ -621,11 +663,8 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
             // total of one column.
             const u32 kconst = 16384u * (u32)(kend - kbeg);
             const bool h8 = (lane & 8) != 0, h4 = (lane & 4) != 0, h2 = (lane & 2) != 0;
-#pragma unroll
-            for (int s = 0; s < BUT; ++s) {
-                u32 v8[8], v4[4], v2[2];
-#pragma unroll
-                for (int c = 0; c < 8; ++c) v8[c] = 32768u * (u32)sbh[s][c] + 128u * (u32)sbl[s][c];
+            auto col_total = [&](const u32 *v8) __attribute__((always_inline)) -> u32 {
+                u32 v4[4], v2[2];
 #pragma unroll
                 for (int c = 0; c < 4; ++c)
                     v4[c] = (h8 ? v8[c + 4] : v8[c]) + swz_xor<8>(h8 ? v8[c] : v8[c + 4]);
@@ -633,9 +672,32 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
                 for (int c = 0; c < 2; ++c)
                     v2[c] = (h4 ? v4[c + 2] : v4[c]) + swz_xor<4>(h4 ? v4[c] : v4[c + 2]);
                 u32 v1 = (h2 ? v2[1] : v2[0]) + swz_xor<2>(h2 ? v2[0] : v2[1]);
-                v1 += swz_xor<1>(v1);
+                return v1 + swz_xor<1>(v1);
+            };
+#pragma unroll
+            for (int s = 0; s < BUT; ++s) {
                 const int c = (h8 ? 4 : 0) + (h4 ? 2 : 0) + (h2 ? 1 : 0);
-                if (!b_dup[s] && (lane & 1) == 0) sK[b_cc[s] * 8 + c] = v1 + kconst;
+                const bool w = !b_dup[s] && (lane & 1) == 0;
+                if constexpr (EPI == 1) {
+                    u32 vh[8], vl[8];
+#pragma unroll
+                    for (int cc = 0; cc < 8; ++cc) {
+                        vh[cc] = (u32)sbh[s][cc];
+                        vl[cc] = (u32)sbl[s][cc];
+                    }
+                    const u32 th = col_total(vh), tl = col_total(vl);
+                    if (w) {
+                        sK[2 * (b_cc[s] * 8 + c)] = th;
+                        sK[2 * (b_cc[s] * 8 + c) + 1] = tl;
+                    }
+                } else {
+                    u32 v8[8];
+#pragma unroll
+                    for (int cc = 0; cc < 8; ++cc)
+                        v8[cc] = 32768u * (u32)sbh[s][cc] + 128u * (u32)sbl[s][cc];
+                    const u32 v1 = col_total(v8);
+                    if (w) sK[b_cc[s] * 8 + c] = v1 + kconst;
+                }
             }
             __syncthreads();
         }
@@ -644,7 +706,22 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
             // row terms of this lane's REGS output rows of block i (groups of
             // four consecutive rows)
             u32 rowt[M::REGS];
-            if constexpr (ES == 2) {
+            int rowh[EPI == 1 ? M::REGS : 1], rowl[EPI == 1 ? M::REGS : 1];
+            if constexpr (ES == 2 && EPI == 1) {
+#pragma unroll
+                for (int r = 0; r < M::REGS; r += 4) {
+                    const u32 *q = sR + 2 * (wm0 + MF * i + M::out_row(lane, r));
+                    const uint4 q0 = *(const uint4 *)q, q1 = *(const uint4 *)(q + 4);
+                    rowh[r] = (int)q0.x;
+                    rowl[r] = (int)q0.y;
+                    rowh[r + 1] = (int)q0.z;
+                    rowl[r + 1] = (int)q0.w;
+                    rowh[r + 2] = (int)q1.x;
+                    rowl[r + 2] = (int)q1.y;
+                    rowh[r + 3] = (int)q1.z;
+                    rowl[r + 3] = (int)q1.w;
+                }
+            } else if constexpr (ES == 2) {
 #pragma unroll
                 for (int r = 0; r < M::REGS; r += 4) {
                     const uint4 q = *(const uint4 *)(sR + wm0 + MF * i + M::out_row(lane, r));
@@ -662,8 +739,7 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
                         const int lc = wn0 + MF * j + M::out_col(lane);
 #pragma unroll
                         for (int r = 0; r < M::REGS; ++r)
-                            cl[j][r] = __builtin_amdgcn_raw_buffer_load_b32(
-                                Crs, c_off(wm0 + MF * i + M::out_row(lane, r), lc), 0, 0);
+                            cl[j][r] = c_load(c_off(wm0 + MF * i + M::out_row(lane, r), lc));
                     }
                 }
             }
@@ -671,11 +747,42 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
             for (int j = 0; j < TN; ++j) {
                 const int lc = wn0 + MF * j + M::out_col(lane);
                 const int gc = n0 + lc;
-                const u32 colt = ES == 2 ? sK[lc] : 0u;
+                const u32 colt = ES == 2 && EPI == 0 ? sK[lc] : 0u;
+                int colh = 0, coll = 0;
+                if constexpr (ES == 2 && EPI == 1) {
+                    const uint2 q = *(const uint2 *)(sK + 2 * lc);
+                    colh = (int)q.x;
+                    coll = (int)q.y;
+                }
 #pragma unroll
                 for (int r = 0; r < M::REGS; ++r) {
                     const int lr = wm0 + MF * i + M::out_row(lane, r);
                     const int gr = m0 + lr;
+                    if constexpr (EPI == 1) {
+                        // The exact product of this k range, then the int16
+                        // conversion and the update modulo 2^16.
+                        int64_t a64;
+                        if constexpr (ES == 1) {
+                            a64 = (int64_t)acc[0][i][j][r];
+                        } else {
+                            a64 = (int64_t)acc[0][i][j][r] * 65536 +
+                                  (int64_t)acc[1][i][j][r] * 256 + (int64_t)acc[2][i][j][r] +
+                                  (int64_t)(rowh[r] + colh) * 32768 +
+                                  (int64_t)(rowl[r] + coll) * 128 +
+                                  (int64_t)(kend - kbeg) * 16384;
+                        }
+                        const int32_t tv = srs16(a64);
+                        if (c_rsrc) {
+                            const int32_t old = PRE ? cpre[i][j][r] : cl[j][r];
+                            __builtin_amdgcn_raw_buffer_store_b16(
+                                (unsigned short)(u32)(old + tv), Crs, c_off(lr, lc), 0, 0);
+                        } else if (gr < m && gc < n) {
+                            int16_t *cp = C16 + (int64_t)gr * ldc + gc;
+                            const int32_t old = PRE ? cpre[i][j][r] : (int32_t)*cp;
+                            *cp = (int16_t)(unsigned short)(u32)(old + tv);
+                        }
+                        continue;
+                    }
                     u32 v;
                     if constexpr (ES == 1) {
                         v = (u32)acc[0][i][j][r];
@@ -714,11 +821,13 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
                 for (int r = 0; r < M::REGS; ++r) {
                     const int lr = wm0 + MF * i + M::out_row(lane, r);
                     if (c_rsrc) {
-                        cpre[i][j][r] =
-                            __builtin_amdgcn_raw_buffer_load_b32(Crs, c_off(lr, lc), 0, 0);
+                        cpre[i][j][r] = c_load(c_off(lr, lc));
                     } else {
                         const int gr = min(m0 + lr, m - 1), gc = min(n0 + lc, n - 1);
-                        cpre[i][j][r] = C[(int64_t)gr * ldc + gc];
+                        if constexpr (EPI == 1)
+                            cpre[i][j][r] = C16[(int64_t)gr * ldc + gc];
+                        else
+                            cpre[i][j][r] = C[(int64_t)gr * ldc + gc];
                     }
                 }
             }
@@ -855,6 +964,16 @@ const void *pick_conv(bool vgather, bool vb, bool split) {
     if (split) return vb ? IGEMM_C(2, true, true) : IGEMM_C(2, false, true);
     return vb ? IGEMM_C(2, true, false) : IGEMM_C(2, false, false);
 #undef IGEMM_C
+}
+
+// int16-output variants (Sec. 5.2 conversion) of the small tiles: A row-major,
+// no k slices.
+template <int ES, int BM, int BN, int WM, int WN, int MF>
+const void *pick_srs(bool va, bool vb) {
+#define IGEMM_S(a, b) (const void *)&igemm_tiled<ES, BM, BN, WM, WN, MF, a, b, false, 0, 1>
+    if (va) return vb ? IGEMM_S(true, true) : IGEMM_S(true, false);
+    return vb ? IGEMM_S(false, true) : IGEMM_S(false, false);
+#undef IGEMM_S
 }
 
 }  // namespace

@@ -4,6 +4,7 @@
 Usage (the program itself goes after ``rocprofv3 ... --``):
     python paper_2302_07594_amd/profile_run.py gemm <workload> [iters] [case]
     python paper_2302_07594_amd/profile_run.py conv <layer> [iters]
+    python paper_2302_07594_amd/profile_run.py srs <workload> <kc> <shift> [iters]
     python paper_2302_07594_amd/profile_run.py copy <MiB> [iters]
     python paper_2302_07594_amd/profile_run.py summarize <rocprof output dir>
     python paper_2302_07594_amd/profile_run.py traffic <rocprof output dir> <out.json>
@@ -12,7 +13,8 @@ Usage (the program itself goes after ``rocprofv3 ... --``):
 ``gemm`` runs the library's igemm call on the named workload's case (inputs
 generated as in the benchmark, C reset is not needed for timing); ``conv``
 runs the convolution entry point on one of the six network layers (index
-into ``workloads.CONV2D_CASES``).
+into ``workloads.CONV2D_CASES``); ``srs`` runs the int16-output update on a
+workload's A and B (int16 C) with block size kc and the given shift.
 ``copy`` runs a device-to-device copy of a tensor of the given size; its
 FETCH_SIZE / WRITE_SIZE readings calibrate the counters against a known byte
 count. ``summarize`` prints per-kernel average durations from a
@@ -70,6 +72,22 @@ def _conv(layer: int, iters: int) -> None:
         ig.conv2d(Xd, Wd, Yd, stride=case.stride, pad=case.pad, dil=case.dil)
     torch.cuda.synchronize()
     print(f"ran {case.name} x{iters}", flush=True)
+
+
+def _srs(wname: str, kc: int, shift: int, iters: int) -> None:
+    import numpy as np
+    import torch
+
+    import paper_2302_07594_amd as ig
+    import workloads
+    case = workloads.WORKLOADS[wname].cases[0]
+    A, B, _ = workloads.generate(case)
+    C = np.zeros((case.m, case.n), dtype=np.int16)
+    Ad, Bd, Cd = (torch.from_numpy(x).cuda() for x in (A, B, C))
+    for _ in range(iters):
+        ig.gemm_srs(Ad, Bd, Cd, kc=kc, shift=shift)
+    torch.cuda.synchronize()
+    print(f"ran {case.name} srs kc={kc} shift={shift} x{iters}", flush=True)
 
 
 def _copy(mib: int, iters: int) -> None:
@@ -222,6 +240,8 @@ def main(argv) -> None:
         _gemm(argv[2], int(argv[3]) if len(argv) > 3 else 3, int(argv[4]) if len(argv) > 4 else 0)
     elif cmd == "conv":
         _conv(int(argv[2]), int(argv[3]) if len(argv) > 3 else 3)
+    elif cmd == "srs":
+        _srs(argv[2], int(argv[3]), int(argv[4]), int(argv[5]) if len(argv) > 5 else 3)
     elif cmd == "copy":
         _copy(int(argv[2]), int(argv[3]) if len(argv) > 3 else 3)
     elif cmd == "summarize":

@@ -407,3 +407,52 @@ def test_conv_null_descriptor():
         fn.argtypes = [ctypes.c_void_p] * 5
         fn.restype = ctypes.c_int
         assert fn(None, FAKE_X, FAKE_W, FAKE_Y, None) == ig.IGEMM_EINVAL
+
+
+# ---- int16-output (shift-round-saturate) entry points -------------------------
+
+def test_srs_header_declares_entry_points():
+    fns = declared_functions()
+    for name in ("igemm_i16_srs", "igemm_i8_srs", "igemm_srs_ex"):
+        assert name in fns
+
+
+@pytest.mark.parametrize("fn", [ig.igemm_i16_srs, ig.igemm_i8_srs])
+def test_srs_invalid_arguments(fn):
+    E = ig.IGEMM_EINVAL
+    a, b, c = FAKE_A, FAKE_B, FAKE_C
+    assert fn(-1, 4, 4, a, 4, b, 4, c, 4, 0, 0, 0, 0) == E
+    assert fn(4, 4, 4, a, 3, b, 4, c, 4, 0, 0, 0, 0) == E          # lda < k
+    assert fn(4, 4, 4, a, 4, b, 4, c, 3, 0, 0, 0, 0) == E          # ldc < n
+    assert fn(4, 4, 4, 0, 4, b, 4, c, 4, 0, 0, 0, 0) == E          # A NULL
+    assert fn(4, 4, 4, a, 4, b, 4, 0, 4, 0, 0, 0, 0) == E          # C NULL
+    assert fn(4, 4, 4, a, 4, b, 4, c, 4, -1, 0, 0, 0) == E         # kc < 0
+    assert fn(4, 4, 4, a, 4, b, 4, c, 4, 0, -1, 0, 0) == E         # shift < 0
+    assert fn(4, 4, 4, a, 4, b, 4, c, 4, 0, 48, 0, 0) == E         # shift > 47
+    assert fn(4, 4, 4, a, 4, b, 4, c, 4, 0, 3, 2, 0) == E          # round not 0/1
+
+
+def test_srs_kernel_choice_is_checked():
+    E = ig.IGEMM_EINVAL
+    a, b, c = FAKE_A, FAKE_B, FAKE_C
+    ok16 = {"i16_128x128", "i16_64x64", "i16_32x128", "i16_16x128"}
+    ok8 = {"i8_32x256", "i8_16x256"}
+    for kid in range(ig.igemm_num_kernels()):
+        name = ig.igemm_kernel_name(kid)
+        for es, ok in ((2, ok16), (1, ok8)):
+            if name not in ok:
+                assert ig.igemm_srs_ex(es, 4, 4, 4, a, 4, b, 4, c, 4, 0, 0, 0, 0, kid) == E
+    assert ig.igemm_srs_ex(3, 4, 4, 4, a, 4, b, 4, c, 4, 0, 0, 0, 0, -1) == E
+    assert ig.igemm_srs_ex(2, 4, 4, 4, a, 4, b, 4, c, 4, 0, 0, 0, 0,
+                           ig.igemm_num_kernels()) == E
+
+
+@pytest.mark.parametrize("fn", [ig.igemm_i16_srs, ig.igemm_i8_srs])
+def test_srs_noop_and_unsupported(fn):
+    assert fn(0, 4, 4, 0, 4, 0, 4, 0, 4, 0, 0, 0, 0) == ig.IGEMM_OK
+    assert fn(4, 0, 4, 0, 4, 0, 4, 0, 4, 0, 0, 0, 0) == ig.IGEMM_OK
+    assert fn(4, 4, 0, 0, 1, 0, 4, FAKE_C, 4, 5, 7, 1, 0) == ig.IGEMM_OK   # k = 0: C unchanged
+    k = 40000
+    # one block beyond 32768 elements: unsupported, nothing enqueued
+    assert fn(4, 4, k, FAKE_A, k, FAKE_B, 4, FAKE_C, 4, 0, 0, 0, 0) == ig.IGEMM_ENOTSUP
+    assert fn(4, 4, k, FAKE_A, k, FAKE_B, 4, FAKE_C, 4, 32769, 0, 0, 0) == ig.IGEMM_ENOTSUP

@@ -1,0 +1,192 @@
+"""GPU parity of the int16-output update (shift-round-saturate conversion per
+k block, the micro-kernel epilogue of the paper) against the oracle, element
+by element and bit-exact, through the C ABI."""
+import numpy as np
+import pytest
+
+import workloads
+from gpu_util import to_device
+
+pytestmark = pytest.mark.gpu
+
+SRS_KERNELS = {"i16": ("i16_128x128", "i16_64x64", "i16_32x128", "i16_16x128"),
+               "i8": ("i8_32x256", "i8_16x256")}
+NP_T = {"i16": np.int16, "i8": np.int8}
+SENTINEL = 0x5A5A
+
+
+def _ig():
+    import paper_2302_07594_amd as ig
+    return ig
+
+
+def _kid(name):
+    ig = _ig()
+    return [ig.igemm_kernel_name(i) for i in range(ig.igemm_num_kernels())].index(name)
+
+
+def _operands(dt, m, n, k, seed, lo=None, hi=None, pad=(0, 0, 0)):
+    """A (m x k+pad), B (k x n+pad), C16 (m x n+pad) with padding drawn like
+    the data, so stray reads change results and stray writes are visible."""
+    t = NP_T[dt]
+    info = np.iinfo(t)
+    lo = info.min if lo is None else lo
+    hi = info.max if hi is None else hi
+    rng = np.random.default_rng(seed)
+    A = rng.integers(lo, hi, size=(m, k + pad[0]), dtype=t, endpoint=True)
+    B = rng.integers(lo, hi, size=(k, n + pad[1]), dtype=t, endpoint=True)
+    C = rng.integers(-32768, 32767, size=(m, n + pad[2]), dtype=np.int16, endpoint=True)
+    return A, B, C
+
+
+def _oracle(A, B, C, m, n, k, kc, shift, rnd):
+    import oracle
+    out = C.copy()
+    oracle.igemm_srs(A[:m, :k], B[:k, :n], out[:m, :n], kc, shift, rnd)
+    return out
+
+
+def _gpu(A, B, C, m, n, k, kc, shift, rnd, kernel=-1, offsets=(0, 0, 0), check=True):
+    import torch
+    ig = _ig()
+    es = 2 if A.dtype == np.int16 else 1
+    Ad = to_device(A, offsets[0])
+    Bd = to_device(B, offsets[1])
+    Cd = to_device(C, offsets[2])
+    st = ig.igemm_srs_ex(es, m, n, k, Ad.data_ptr(), A.shape[1], Bd.data_ptr(), B.shape[1],
+                         Cd.data_ptr(), C.shape[1], kc, shift, 1 if rnd else 0,
+                         torch.cuda.current_stream().cuda_stream, kernel)
+    torch.cuda.synchronize()
+    if check:
+        assert st == 0, f"status {st}: {ig.igemm_strerror(st)}"
+    return st, Cd.cpu().numpy()
+
+
+def _describe(got, want, limit=5):
+    bad = np.argwhere(got != want)
+    lines = [f"{len(bad)} of {got.size} elements differ"]
+    for (i, j) in bad[:limit]:
+        lines.append(f"  [{i},{j}] got {got[i, j]} want {want[i, j]}")
+    return "\n".join(lines)
+
+
+def _check(A, B, C, m, n, k, kc, shift, rnd, **kw):
+    want = _oracle(A, B, C, m, n, k, kc, shift, rnd)
+    _, got = _gpu(A, B, C, m, n, k, kc, shift, rnd, **kw)
+    assert np.array_equal(got, want), _describe(got, want)
+    return got
+
+
+SHAPES = [(64, 64, 64), (67, 133, 200), (16, 128, 5), (1, 37, 290), (100, 1, 130),
+          (33, 257, 700)]
+CONVERSIONS = [(0, 0, False), (290, 0, False), (64, 7, True), (100, 12, False), (1, 3, True),
+               (0, 20, True), (7, 30, False)]
+
+
+@pytest.mark.parametrize("dt", ["i16", "i8"])
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_every_srs_kernel(dt, shape):
+    """Every int16-output kernel of the type on ragged shapes, for block
+    sizes that do and do not divide k (or exceed it), shifts that saturate
+    nearly everything (0) and ones that saturate little, both roundings."""
+    m, n, k = shape
+    A, B, C = _operands(dt, m, n, k, seed=300 + m + n + k)
+    for name in SRS_KERNELS[dt]:
+        for kc, shift, rnd in CONVERSIONS:
+            _check(A, B, C, m, n, k, kc, shift, rnd, kernel=_kid(name))
+
+
+@pytest.mark.parametrize("dt", ["i16", "i8"])
+def test_small_values_reduce_to_gemm(dt):
+    """Values small enough that nothing saturates: shift 0 gives C + A B
+    exactly, whatever the block size (checked against the plain product)."""
+    m, n, k = 150, 140, 200
+    A, B, C = _operands(dt, m, n, k, seed=11, lo=-6, hi=6)
+    C = (C // 4).astype(np.int16)
+    want = (C.astype(np.int64) + A.astype(np.int64) @ B.astype(np.int64)).astype(np.int16)
+    for kc in (0, 1, 64, 77, 200):
+        _, got = _gpu(A, B, C, m, n, k, kc, 0, False)
+        assert np.array_equal(got, want), _describe(got, want)
+
+
+@pytest.mark.parametrize("dt", ["i16", "i8"])
+@pytest.mark.parametrize("offsets,pad", [((1, 0, 0), (0, 0, 0)), ((0, 1, 1), (0, 0, 0)),
+                                         ((0, 0, 0), (3, 5, 7)), ((1, 1, 1), (1, 3, 2))])
+def test_alignment_and_padding(dt, offsets, pad):
+    """Misaligned bases and odd leading dimensions; padding columns of C
+    must be untouched."""
+    m, n, k = 90, 150, 300
+    A, B, C = _operands(dt, m, n, k, seed=55, pad=pad)
+    for name in SRS_KERNELS[dt]:
+        got = _check(A, B, C, m, n, k, 100, 9, True, kernel=_kid(name), offsets=offsets)
+        assert np.array_equal(got[:, n:], C[:, n:])
+
+
+def test_extreme_values_and_long_blocks():
+    """All-extreme operands: block sums up to 32768 * 2^30 (beyond 2^44),
+    exact before the shift; blocks of the maximum length, and a k of two
+    maximal blocks plus a tail."""
+    m, n = 40, 70
+    for k, kc, shift in ((32768, 0, 40), (70000, 32768, 45), (5000, 5000, 0)):
+        A = np.full((m, k), -32768, dtype=np.int16)
+        B = np.full((k, n), -32768, dtype=np.int16)
+        B[:, ::3] = 32767
+        A[::5, :] = 32767
+        C = np.random.default_rng(k).integers(-32768, 32767, size=(m, n), dtype=np.int16,
+                                              endpoint=True)
+        for rnd in (False, True):
+            _check(A, B, C, m, n, k, kc, shift, rnd)
+
+
+def test_block_beyond_limit_is_refused():
+    m, n, k = 8, 8, 40000
+    A, B, C = _operands("i16", m, n, k, seed=2)
+    st, got = _gpu(A, B, C, m, n, k, 0, 0, False, check=False)
+    assert st == _ig().IGEMM_ENOTSUP and np.array_equal(got, C)
+
+
+def test_paper_shape_sampled_rows():
+    """The paper's GEMM shape (4096, 4096, 290) with its k_c = 290 and shift
+    0, full-range int16 operands: whole rows sampled across the tiles,
+    checked against the oracle on those rows (each row of C depends on the
+    same row of A only)."""
+    case = workloads.WORKLOADS["i16_paper"].cases[0]
+    m, n, k = case.m, case.n, case.k
+    A, B, _ = workloads.generate(case)
+    C = np.random.default_rng(4).integers(-32768, 32767, size=(m, n), dtype=np.int16,
+                                          endpoint=True)
+    _, got = _gpu(A, B, C, m, n, k, 290, 0, False)
+    rows = np.r_[0:3, 63:66, 1000, 2047:2050, 4093:4096]
+    import oracle
+    want = C[rows].copy()
+    oracle.igemm_srs(np.ascontiguousarray(A[rows]), B, want, 290, 0, False)
+    assert np.array_equal(got[rows], want), _describe(got[rows], want)
+
+
+def test_tensor_wrapper_and_graph_replays():
+    """gemm_srs() on torch tensors, then captured in a HIP graph (several
+    launches, one per block; no workspace, no memset): each replay adds the
+    converted blocks once more, checked after every replay."""
+    import torch
+    ig = _ig()
+    m, n, k, kc, shift = 130, 96, 300, 128, 6
+    A, B, C = _operands("i16", m, n, k, seed=8, lo=-3000, hi=3000)
+    Ad, Bd, Cd = (torch.from_numpy(x).cuda() for x in (A, B, C))
+    ig.gemm_srs(Ad, Bd, Cd, kc=kc, shift=shift, round_half_up=True)
+    torch.cuda.synchronize()
+    want = _oracle(A, B, C, m, n, k, kc, shift, True)
+    assert np.array_equal(Cd.cpu().numpy(), want)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        ig.gemm_srs(Ad, Bd, Cd, kc=kc, shift=shift, round_half_up=True)
+    for rep in range(3):
+        g.replay()
+        filler = torch.ones(1 << 16, device="cuda", dtype=torch.int32) * rep  # eager work
+        torch.cuda.synchronize()
+        want = _oracle(A, B, want, m, n, k, kc, shift, True)
+        got = Cd.cpu().numpy()
+        assert np.array_equal(got, want), f"replay {rep}: " + _describe(got, want)
+        del filler
