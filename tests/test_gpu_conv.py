@@ -201,3 +201,44 @@ def test_graph_replays_match_oracle():
         got = Yd.cpu().numpy()
         assert np.array_equal(got, want), f"replay {rep}: " + _describe(got, want)
         del scratch
+
+
+def _fuzz_cases(n_cases=60, seed=4242):
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n_cases):
+        dt = "i16" if rng.integers(0, 3) else "i8"
+        n = int(rng.integers(1, 4))
+        r, s = int(rng.integers(1, 6)), int(rng.integers(1, 6))
+        st = (int(rng.integers(1, 4)), int(rng.integers(1, 4)))
+        dl = (int(rng.integers(1, 4)), int(rng.integers(1, 4)))
+        pd = (int(rng.integers(0, 5)), int(rng.integers(0, 5)))
+        h = int(rng.integers(1, 24))
+        w = int(rng.integers(1, 24))
+        c = int(rng.choice([1, 2, 3, 5, 8, 13, 16, 24, 32, 40, 64]))
+        k = int(rng.choice([1, 3, 17, 64, 100, 129, 256, 300]))
+        kname = str(rng.choice(list(CONV_KERNELS[dt]) + ["auto"]))
+        split = int(rng.choice([-1, -1, 1, 2, 3, 7]))
+        x_off = int(rng.choice([0, 0, 1, 3]))
+        out.append((i, dt, n, h, w, c, k, r, s, st, pd, dl, kname, split, x_off))
+    return out
+
+
+_FUZZ = _fuzz_cases()
+
+
+@pytest.mark.parametrize("case", _FUZZ, ids=[f"f{c[0]}-{c[1]}-{c[2]}x{c[3]}x{c[4]}x{c[5]}-k{c[6]}"
+                                             f"-r{c[7]}s{c[8]}" for c in _FUZZ])
+def test_fuzz_conv(case):
+    """Seeded random convolutions: batch, extents, channels, filter sizes,
+    strides, dilations and padding (windows that do not fit give empty
+    outputs), random kernel and k-slice count, misaligned X."""
+    i, dt, n, h, w, c, k, r, s, st, pd, dl, kname, split, x_off = case
+    ig = _ig()
+    oh = ig.igemm_conv2d_out_dim(h, r, st[0], pd[0], dl[0])
+    ow = ig.igemm_conv2d_out_dim(w, s, st[1], pd[1], dl[1])
+    X, W, Y = workloads.random_conv_operands(dt, n, h, w, c, k, r, s, oh, ow, seed=7000 + i)
+    want = _oracle(X, W, Y, st, pd, dl)
+    kid = -1 if kname == "auto" else _kid(kname)
+    got = _gpu(X, W, Y, st, pd, dl, kernel=kid, split=split, x_off=x_off)
+    assert np.array_equal(got, want), _describe(got, want)

@@ -30,8 +30,8 @@ def _operands(dt, m, n, k, seed, lo=None, hi=None, pad=(0, 0, 0)):
     the data, so stray reads change results and stray writes are visible."""
     t = NP_T[dt]
     info = np.iinfo(t)
-    lo = info.min if lo is None else lo
-    hi = info.max if hi is None else hi
+    lo = info.min if lo is None else max(lo, info.min)
+    hi = info.max if hi is None else min(hi, info.max)
     rng = np.random.default_rng(seed)
     A = rng.integers(lo, hi, size=(m, k + pad[0]), dtype=t, endpoint=True)
     B = rng.integers(lo, hi, size=(k, n + pad[1]), dtype=t, endpoint=True)
@@ -190,3 +190,38 @@ def test_tensor_wrapper_and_graph_replays():
         got = Cd.cpu().numpy()
         assert np.array_equal(got, want), f"replay {rep}: " + _describe(got, want)
         del filler
+
+
+def _fuzz_cases(n_cases=60, seed=777):
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n_cases):
+        dt = "i16" if rng.integers(0, 3) else "i8"
+        m = int(rng.choice([1, 2, 15, 16, 17, 31, 33, 64, 65, 127, 129, 200, 300]))
+        n = int(rng.choice([1, 3, 16, 63, 64, 100, 128, 255, 257, 300]))
+        k = int(rng.choice([1, 7, 63, 64, 65, 147, 256, 290, 513, 1000]))
+        kc = int(rng.choice([0, 0, 1, 5, 64, 100, 256, 290, 2000]))
+        shift = int(rng.choice([0, 0, 1, 4, 8, 13, 16, 24, 31, 47]))
+        rnd = bool(rng.integers(0, 2))
+        kname = str(rng.choice(list(SRS_KERNELS[dt]) + ["auto"]))
+        offs = tuple(int(x) for x in rng.integers(0, 2, 3) * rng.integers(1, 4, 3))
+        pads = tuple(int(x) for x in rng.integers(0, 2, 3) * rng.integers(1, 9, 3))
+        scale = int(rng.choice([8, 300, 0]))  # 0: full range
+        out.append((i, dt, m, n, k, kc, shift, rnd, kname, offs, pads, scale))
+    return out
+
+
+_FUZZ = _fuzz_cases()
+
+
+@pytest.mark.parametrize("case", _FUZZ, ids=[f"f{c[0]}-{c[1]}-{c[2]}x{c[3]}x{c[4]}-kc{c[5]}-s{c[6]}"
+                                             for c in _FUZZ])
+def test_fuzz_srs(case):
+    """Seeded random shapes, block sizes, shifts, roundings, kernels,
+    misaligned bases and padded leading dimensions, operand ranges from
+    small (nothing saturates) to full."""
+    i, dt, m, n, k, kc, shift, rnd, kname, offs, pads, scale = case
+    lo, hi = (None, None) if scale == 0 else (-scale, scale)
+    A, B, C = _operands(dt, m, n, k, seed=9000 + i, lo=lo, hi=hi, pad=pads)
+    kid = -1 if kname == "auto" else _kid(kname)
+    _check(A, B, C, m, n, k, kc, shift, rnd, kernel=kid, offsets=offs)
