@@ -227,15 +227,16 @@ int run_conv(int es, const igemm_conv2d_desc *d, const void *X, const void *W, i
              void *stream, int kernel, int split) {
     igemm_plan p;
     ConvGeom g;
-    bool vg = false;
+    int gather = 0;
     // Validate without touching the device, then plan for its CU count.
-    int st = make_conv_plan(es, d, X, W, Y, 0, kernel, split, &p, &g, &vg);
+    int st = make_conv_plan(es, d, X, W, Y, 0, kernel, split, &p, &g, &gather);
     if (st != IGEMM_OK || p.kernel < 0) return st;
-    st = make_conv_plan(es, d, X, W, Y, num_cu_of_current_device(), kernel, split, &p, &g, &vg);
+    st = make_conv_plan(es, d, X, W, Y, num_cu_of_current_device(), kernel, split, &p, &g,
+                        &gather);
     if (st != IGEMM_OK) return st;
     const int64_t oh = conv_out_dim(d->h, d->r, d->stride_h, d->pad_h, d->dil_h);
     const int64_t ow = conv_out_dim(d->w, d->s, d->stride_w, d->pad_w, d->dil_w);
-    return launch_conv(es, p, d->n * oh * ow, d->k, d->r * d->s * d->c, g, vg, X, W, Y, d->k,
+    return launch_conv(es, p, d->n * oh * ow, d->k, d->r * d->s * d->c, g, gather, X, W, Y, d->k,
                        stream);
 }
 

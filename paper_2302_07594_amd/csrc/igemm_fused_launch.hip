@@ -23,13 +23,13 @@ const void *gemm_kernel_fn(int id, bool va, bool vb, bool split) {
     }
 }
 
-const void *conv_kernel_fn(int id, bool vgather, bool vb, bool split) {
+const void *conv_kernel_fn(int id, int gather, bool vb, bool split) {
     switch (id) {
         case K_I8_32x256:
-        case K_I8_16x256: return fused_conv_i8(id, vgather, vb, split);
+        case K_I8_16x256: return fused_conv_i8(id, gather, vb, split);
         case K_I16_64x64:
         case K_I16_32x128:
-        case K_I16_16x128: return fused_conv_i16(id, vgather, vb, split);
+        case K_I16_16x128: return fused_conv_i16(id, gather, vb, split);
         default: return nullptr;
     }
 }
@@ -54,10 +54,10 @@ int launch_tiled(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, c
 }
 
 int launch_conv(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const ConvGeom &g,
-                bool vec_gather, const void *X, const void *W, int32_t *Y, int64_t ldy,
+                int gather, const void *X, const void *W, int32_t *Y, int64_t ldy,
                 void *stream) {
     (void)es;
-    const void *fn = conv_kernel_fn(p.kernel, vec_gather, p.vec_b != 0, p.split > 1);
+    const void *fn = conv_kernel_fn(p.kernel, gather, p.vec_b != 0, p.split > 1);
     if (fn == nullptr) return IGEMM_EINVAL;
     int mi = (int)m, ni = (int)n, ki = (int)k, kc = (int)p.k_chunk;
     int tm = (int)((m + p.bm - 1) / p.bm), tn = (int)((n + p.bn - 1) / p.bn);

@@ -84,7 +84,9 @@ struct ConvGeom {
     int s;                // filter width
     int sh, sw, ph, pw, dh, dw;
     int x_bytes;          // bytes of the input tensor
-    DivU32 by_c, by_s, by_ohw, by_ow;
+    int sc;               // s * c: elements of one filter row's window run
+    int run2;             // dh * w * c - s * c: from one filter row's run to the next
+    DivU32 by_c, by_s, by_ohw, by_ow, by_sc;
 };
 
 // Validation and planning; pure host code, no HIP calls.
@@ -108,9 +110,13 @@ int make_srs_plan(int es, int64_t m, int64_t n, int64_t kb, const void *A, int64
 int64_t conv_out_dim(int64_t in, int64_t f, int64_t stride, int64_t pad, int64_t dil);
 // Plan of a convolution as its lowered GEMM, with the kernel's geometry.
 // Returns IGEMM_OK with out->kernel = -1 when there is nothing to compute.
+// *gather: how the kernel reads the IM2ROW rows (1: 16-byte vector loads,
+// channel rows 16-byte aligned; 3: unaligned 16-byte loads of the contiguous
+// runs that a filter row covers when the horizontal dilation is 1; 2: one
+// load per element).
 int make_conv_plan(int es, const igemm_conv2d_desc *d, const void *X, const void *W,
                    const void *Y, int num_cu, int kernel, int split, igemm_plan *out,
-                   ConvGeom *g, bool *vec_gather);
+                   ConvGeom *g, int *gather);
 
 // Kernel launches for a validated plan (stream is a hipStream_t). The packed
 // launch needs a workspace of at least plan.workspace_bytes, 256-byte aligned.
@@ -129,13 +135,13 @@ const void *fused_i8_wide(int id, bool va, bool vb, bool split);
 const void *fused_i8_rows(int id, bool va, bool vb, bool split);
 const void *fused_i16_wide(int id, bool va, bool vb, bool split);
 const void *fused_i16_rows(int id, bool va, bool vb, bool split);
-const void *fused_conv_i16(int id, bool vgather, bool vb, bool split);
-const void *fused_conv_i8(int id, bool vgather, bool vb, bool split);
+const void *fused_conv_i16(int id, int gather, bool vb, bool split);
+const void *fused_conv_i8(int id, int gather, bool vb, bool split);
 const void *fused_srs(int id, bool va, bool vb);
 // The same fused kernels with A gathered from the NHWC input X by IM2ROW
-// (vector gather when a 16-byte chunk of A never straddles two filter taps).
+// (gather mode as make_conv_plan chose it).
 int launch_conv(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const ConvGeom &g,
-                bool vec_gather, const void *X, const void *W, int32_t *Y, int64_t ldy,
+                int gather, const void *X, const void *W, int32_t *Y, int64_t ldy,
                 void *stream);
 // The int16-output update of one k block (plan without k slices): C16 +=
 // srs(A B) modulo 2^16 with the given shift and rounding.

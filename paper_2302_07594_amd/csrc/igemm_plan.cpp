@@ -357,7 +357,7 @@ int make_srs_plan(int es, int64_t m, int64_t n, int64_t kb, const void *A, int64
 // m = n * oh * ow output pixels, n_gemm = output channels, k = r * s * c.
 int make_conv_plan(int es, const igemm_conv2d_desc *d, const void *X, const void *W,
                    const void *Y, int num_cu, int kernel, int split, igemm_plan *out,
-                   ConvGeom *g, bool *vec_gather) {
+                   ConvGeom *g, int *gather) {
     if (out == NULL || d == NULL || (es != 1 && es != 2)) return IGEMM_EINVAL;
     *out = igemm_plan{};
     out->kernel = -1;
@@ -410,7 +410,19 @@ int make_conv_plan(int es, const igemm_conv2d_desc *d, const void *X, const void
     int st = make_plan(es, M, N, K, X, K, W, N, N, num_cu, id, split, false, out);
     if (st != IGEMM_OK) return st;
     out->vec_a = (((uintptr_t)X % 16) == 0 && (d->c * es) % 16 == 0) ? 1 : 0;
-    *vec_gather = out->vec_a != 0;
+    // Runs: with horizontal dilation 1 the taps of one filter row are
+    // s * c consecutive input elements; the jump to the next filter row must
+    // fit in 31 bits.
+    // (dh as the kernel uses it: 1 for a one-row filter, else below 2^30.)
+    const int64_t dh = d->r == 1 ? 1 : d->dil_h;
+    const int64_t run2 = dh * d->w * d->c - d->s * d->c;
+    // A 16-byte chunk then spans at most two runs if s * c >= 16 / es - 1.
+    const bool runs = (d->s == 1 || d->dil_w == 1) && dh * d->w * d->c < ((int64_t)1 << 30) &&
+                      d->s * d->c < ((int64_t)1 << 30) && d->s * d->c >= 16 / es - 1;
+    *gather = out->vec_a != 0 ? 1 : (runs ? 3 : 2);
+    g->sc = (int)(d->s * d->c);
+    g->run2 = (int)run2;
+    g->by_sc = make_div((uint32_t)(d->s * d->c));
     g->h = (int)d->h;
     g->w = (int)d->w;
     g->c = (int)d->c;
@@ -476,8 +488,9 @@ int igemm_conv2d_query_plan(int elem_bytes, const igemm_conv2d_desc *desc, const
                             const void *W, const void *Y, int num_cu, int kernel, int split,
                             igemm_plan *out) {
     igemm::ConvGeom g;
-    bool vg = false;
-    return igemm::make_conv_plan(elem_bytes, desc, X, W, Y, num_cu, kernel, split, out, &g, &vg);
+    int gather = 0;
+    return igemm::make_conv_plan(elem_bytes, desc, X, W, Y, num_cu, kernel, split, out, &g,
+                                 &gather);
 }
 
 }  // extern "C"

@@ -63,10 +63,12 @@ __device__ __forceinline__ u32 swz_xor(u32 v) {
 // ---------------------------------------------------------------------------
 // Small tiles (bm * bn <= 8192, LDS <= 64 KB) are held to 256 registers per
 // lane so that two workgroups share a compute unit; larger tiles take one.
-// AM selects where A comes from: 0, the row-major matrix A (lda); 1 and 2, the
-// IM2ROW rows of a convolution gathered from the NHWC input Ap (geometry g),
-// 16 bytes at a time (1: the channel count is a multiple of a 16-byte chunk,
-// so a chunk never straddles two filter taps) or element by element (2).
+// AM selects where A comes from: 0, the row-major matrix A (lda); 1, 2 and 3,
+// the IM2ROW rows of a convolution gathered from the NHWC input Ap (geometry
+// g): 16 bytes at a time (1: the channel count is a multiple of a 16-byte
+// chunk, so a chunk never straddles two filter taps), element by element (2),
+// or (3, horizontal dilation 1) as the contiguous input runs that one filter
+// row covers, with at most two unaligned 16-byte loads per chunk.
 // EPI selects the update of C: 0, int32 C += A B modulo 2^32; 1, int16 C
 // (passed through the int32 pointer) += srs(A B), the product converted to
 // int16 by an arithmetic shift right by (epi & 0xff) bits, after adding half
@@ -285,13 +287,15 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     // Rows that are not 16-byte aligned are read with dword-aligned loads
     // from a dword-aligned resource base and shifted into place
     // (v_alignbyte), five dwords per 16 bytes.
-    const u32 a_dl = AM != 0 ? 0u : (u32)((uintptr_t)a_base & 3);
+    const u32 a_dl = AM == 3 ? (u32)((uintptr_t)Ap & 3)
+                             : (AM != 0 ? 0u : (u32)((uintptr_t)a_base & 3));
     const u32 b_dl = (u32)((uintptr_t)b_base & 3);
-    const int a_rec = AM != 0 ? ((g.x_bytes + 3) & ~3)
+    const int a_rec = AM != 0 ? ((g.x_bytes + (int)a_dl + 3) & ~3)
                               : (int)min((a_ext + a_dl + 3) & ~(int64_t)3, (int64_t)0x7ffffff0);
     const int b_rec = (int)min((b_ext + b_dl + 3) & ~(int64_t)3, (int64_t)0x7ffffff0);
     const __amdgpu_buffer_rsrc_t Ars = __builtin_amdgcn_make_buffer_rsrc(
-        AM != 0 ? (void *)Ap : (void *)(a_base - a_dl), 0, a_rec, 0x00020000);
+        AM != 0 ? (void *)((const char *)Ap - a_dl) : (void *)(a_base - a_dl), 0, a_rec,
+        0x00020000);
     const __amdgpu_buffer_rsrc_t Brs =
         __builtin_amdgcn_make_buffer_rsrc((void *)(b_base - b_dl), 0, b_rec, 0x00020000);
     const int lda_b = (int)(lda * ES), ldb_b = (int)(ldb * ES);
@@ -321,6 +325,9 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
     // once: first input row and column of its window (a row past m gets a
     // window that lies outside the image), and its image's first element.
     int cv_iy0[AM != 0 ? ACT : 1], cv_ix0[AM != 0 ? ACT : 1], cv_img[AM != 0 ? ACT : 1];
+    // AM 3: positions [cv_lo, cv_hi) of a filter row's run of s*c elements
+    // that fall inside the image horizontally.
+    int cv_lo[AM == 3 ? ACT : 1], cv_hi[AM == 3 ? ACT : 1];
     if constexpr (AM != 0) {
 #pragma unroll
         for (int s = 0; s < ACT; ++s) {
@@ -333,6 +340,11 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
             cv_iy0[s] = ok ? (int)oy * g.sh - g.ph : -(1 << 30);
             cv_ix0[s] = (int)ox * g.sw - g.pw;
             cv_img[s] = ok ? (int)img * g.h * g.w * g.c : 0;
+            if constexpr (AM == 3) {
+                const int x0 = cv_ix0[s];
+                cv_lo[s] = min(max(-x0, 0), g.s) * g.c;
+                cv_hi[s] = min(max(g.w - x0, 0), g.s) * g.c;
+            }
         }
     }
     // Element offset in X of A[row of chunk s, column p], or -1 where the
@@ -347,27 +359,75 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
         const bool in = (u32)iy < (u32)g.h && (u32)ix < (u32)g.w;
         return in ? cv_img[s] + (iy * g.w + ix) * g.c + ci : -1;
     };
+    // One load per element of the 16 bytes at column p (AM 2, and the rare
+    // chunks AM 3 cannot read as runs).
+    auto gather_elems = [&](int s, int e, u32 p) __attribute__((always_inline)) -> v4i {
+        u32 w4[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int t = 0; t < 16 / ES; ++t) {
+            const int o = e + t < klen ? tap(s, p + t) : -1;
+            const u32 off = o >= 0 ? (u32)o * ES + a_dl : 0x80000000u;
+            u32 v;
+            if constexpr (ES == 2)
+                v = (u32)__builtin_amdgcn_raw_buffer_load_b16(Ars, off, 0, 0);
+            else
+                v = (u32)__builtin_amdgcn_raw_buffer_load_b8(Ars, off, 0, 0);
+            w4[(t * ES) >> 2] |= v << (8 * ((t * ES) & 3));
+        }
+        v4i r;
+        r.x = (int)w4[0];
+        r.y = (int)w4[1];
+        r.z = (int)w4[2];
+        r.w = (int)w4[3];
+        return r;
+    };
     // 16 bytes of IM2ROW row a_row[s] from element e of this workgroup's k
     // range: one vector load (AM 1: the chunk lies within one filter tap),
-    // or one load per element (AM 2); out-of-image elements read as zero.
+    // one load per element (AM 2), or runs (AM 3); out-of-image elements and
+    // elements past the k range read as zero.
     auto gather16 = [&](int s, int e) __attribute__((always_inline)) -> v4i {
         const u32 p = (u32)(kbeg + e);
         if constexpr (AM == 1) {
             const int o = e < klen ? tap(s, p) : -1;
             return __builtin_amdgcn_raw_buffer_load_b128(
                 Ars, o >= 0 ? (u32)o * ES : 0x80000000u, 0, 0);
-        } else {
+        } else if constexpr (AM == 3) {
+            // With horizontal dilation 1, the s*c columns of filter row fy
+            // are consecutive input elements (one run), so the chunk is the
+            // tail of run fy and the head of run fy + 1 (s*c >= 16/ES - 1,
+            // checked on the host): element t comes from run 1 at
+            // base1 + t or from run 2 at base2 + t, and is valid inside the
+            // intervals [a1, b1) and [a2, b2).
+            constexpr int E = 16 / ES;
+            const u32 fy = divu(p, g.by_sc);
+            const int q1 = (int)(p - fy * (u32)g.sc);
+            const int iy1 = cv_iy0[s] + (int)fy * g.dh;
+            const bool r1 = (u32)iy1 < (u32)g.h, r2 = (u32)(iy1 + g.dh) < (u32)g.h;
+            // (modulo 2^32: exact for rows inside the image, unused otherwise)
+            const int base1 = (int)((u32)cv_img[s] +
+                                    ((u32)iy1 * (u32)g.w + (u32)cv_ix0[s]) * (u32)g.c + (u32)q1);
+            const int base2 = (int)((u32)base1 + (u32)g.run2);
+            const int split = g.sc - q1;  // elements of run 1 in the chunk
+            const int kmax = klen - e;    // elements before the end of the k range
+            const int a1 = max(cv_lo[s] - q1, 0);
+            const int b1 = r1 ? min(min(cv_hi[s] - q1, split), kmax) : 0;
+            const int a2 = split + cv_lo[s];
+            const int b2 = r2 ? min(split + cv_hi[s], kmax) : 0;
+            const bool need1 = a1 < b1 && a1 < E, need2 = a2 < b2 && a2 < E;
+            // A run that starts before the tensor (only at the first image's
+            // top-left corner, where leading elements are padding): elements.
+            if ((need1 && base1 < 0) || (need2 && base2 < 0)) return gather_elems(s, e, p);
+            const v4i v1 = load16_rs(ic<0>{}, Ars, need1 ? (u32)base1 * ES : 0x80000000u, a_dl);
+            const v4i v2 = load16_rs(ic<0>{}, Ars, need2 ? (u32)base2 * ES : 0x80000000u, a_dl);
+            const u32 w1[4] = {(u32)v1.x, (u32)v1.y, (u32)v1.z, (u32)v1.w};
+            const u32 w2[4] = {(u32)v2.x, (u32)v2.y, (u32)v2.z, (u32)v2.w};
             u32 w4[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
-            for (int t = 0; t < 16 / ES; ++t) {
-                const int o = e + t < klen ? tap(s, p + t) : -1;
-                const u32 off = o >= 0 ? (u32)o * ES : 0x80000000u;
-                u32 v;
-                if constexpr (ES == 2)
-                    v = (u32)__builtin_amdgcn_raw_buffer_load_b16(Ars, off, 0, 0);
-                else
-                    v = (u32)__builtin_amdgcn_raw_buffer_load_b8(Ars, off, 0, 0);
-                w4[(t * ES) >> 2] |= v << (8 * ((t * ES) & 3));
+            for (int t = 0; t < E; ++t) {
+                const int j = (t * ES) >> 2;
+                const u32 em = (ES == 2 ? 0xffffu : 0xffu) << (8 * ((t * ES) & 3));
+                const bool ok1 = t >= a1 && t < b1, ok2 = t >= a2 && t < b2;
+                w4[j] |= (ok1 ? (w1[j] & em) : 0u) | (ok2 ? (w2[j] & em) : 0u);
             }
             v4i r;
             r.x = (int)w4[0];
@@ -375,6 +435,8 @@ igemm_tiled(const void *__restrict__ Ap, int64_t lda, const void *__restrict__ B
             r.z = (int)w4[2];
             r.w = (int)w4[3];
             return r;
+        } else {
+            return gather_elems(s, e, p);
         }
     };
     // The k-tile starting kt0 elements after kbeg into register set R.
@@ -954,16 +1016,22 @@ const void *pick(bool va, bool vb, bool split) {
 
 // Convolution variants (A gathered by IM2ROW; VA is unused) of the small
 // tiles, which the planner chooses for lowered convolutions.
-template <int ES, int BM, int BN, int WM, int WN, int MF>
-const void *pick_conv(bool vgather, bool vb, bool split) {
-#define IGEMM_C(am, b, s) (const void *)&igemm_tiled<ES, BM, BN, WM, WN, MF, false, b, s, am>
-    if (vgather) {
-        if (split) return vb ? IGEMM_C(1, true, true) : IGEMM_C(1, false, true);
-        return vb ? IGEMM_C(1, true, false) : IGEMM_C(1, false, false);
-    }
-    if (split) return vb ? IGEMM_C(2, true, true) : IGEMM_C(2, false, true);
-    return vb ? IGEMM_C(2, true, false) : IGEMM_C(2, false, false);
+template <int ES, int BM, int BN, int WM, int WN, int MF, int AM>
+const void *pick_conv_am(bool vb, bool split) {
+#define IGEMM_C(b, s) (const void *)&igemm_tiled<ES, BM, BN, WM, WN, MF, false, b, s, AM>
+    if (split) return vb ? IGEMM_C(true, true) : IGEMM_C(false, true);
+    return vb ? IGEMM_C(true, false) : IGEMM_C(false, false);
 #undef IGEMM_C
+}
+
+template <int ES, int BM, int BN, int WM, int WN, int MF>
+const void *pick_conv(int gather, bool vb, bool split) {
+    switch (gather) {
+        case 1: return pick_conv_am<ES, BM, BN, WM, WN, MF, 1>(vb, split);
+        case 2: return pick_conv_am<ES, BM, BN, WM, WN, MF, 2>(vb, split);
+        case 3: return pick_conv_am<ES, BM, BN, WM, WN, MF, 3>(vb, split);
+        default: return nullptr;
+    }
 }
 
 // int16-output variants (Sec. 5.2 conversion) of the small tiles: A row-major,
