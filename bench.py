@@ -26,7 +26,8 @@ Prints ONE JSON line. Besides the headline value it carries:
                 same shape through the int16-output entry point with the
                 paper's k_c = 290 and shift 0 (and 4096^3 with k_c = 256),
                 and the six network layers run as convolutions through the
-                implicit-GEMM entry point (IM2ROW gathered in the kernel).
+                implicit-GEMM entry point (IM2ROW gathered in the kernel), at
+                batch 1 and batch 32.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-extra]
                        [--no-cpu-baseline] [--cpu-seconds S]
@@ -418,9 +419,9 @@ def main():
         per.append(bench_srs_case(workloads.WORKLOADS["i16_4096"].cases[0], 256, 0,
                                   per_graph=10, reps=5))
         torch.cuda.empty_cache()
-        for c in workloads.CONV2D_CASES:
+        for c in workloads.CONV2D_CASES + workloads.CONV2D_B32_CASES:
             log(f"bench: per-config {c.name}")
-            per.append(bench_conv_case(c))
+            per.append(bench_conv_case(c, per_graph=40 if c.n == 1 else 10))
             torch.cuda.empty_cache()
         out["per_config"] = per
     print(json.dumps(out), flush=True)

@@ -84,6 +84,19 @@ def test_resnet_layers_full(case):
     assert np.any(got != 0)
 
 
+@pytest.mark.parametrize("case", workloads.CONV2D_B32_CASES, ids=lambda c: c.name)
+def test_resnet_layers_batch32_sampled_images(case):
+    """The six layers at batch 32 in the launch configuration the benchmark
+    times; images 0, 17 and 31 compared in full with the oracle run on those
+    images alone (each output image depends on its own input image only)."""
+    X, W, Y = workloads.generate_conv(case)
+    got = _gpu(X, W, Y, case.stride, case.pad, case.dil)
+    for b in (0, 17, 31):
+        want = _oracle(np.ascontiguousarray(X[b:b + 1]), W, np.ascontiguousarray(Y[b:b + 1]),
+                       case.stride, case.pad, case.dil)
+        assert np.array_equal(got[b:b + 1], want), f"image {b}: " + _describe(got[b:b + 1], want)
+
+
 # (n, h, w, c, k, r, s, stride, pad, dil): channel counts that take the 16-byte
 # gather and ones that do not, windows that straddle image and batch borders,
 # strides, dilations, padding wider than the filter, one-pixel outputs.

@@ -19,7 +19,8 @@ Workloads (all row-major, C is int32):
                    (activations), B = rint(normal(0,32)) clipped to int16
                    (weights), C zero; layer i uses seed 40+i.
 * ``CONV2D_CASES`` the six ``i16_conv`` layers as real convolutions from an
-                   NHWC image (implicit GEMM), seeds 60+i.
+                   NHWC image (implicit GEMM), seeds 60+i; ``CONV2D_B32_CASES``
+                   the same at batch 32, seeds 70+i.
 * ``i16_paper``    the paper's GEMM shape (4096, 4096, 290), int16 with the
                    recipe of i16_4096, seed 3 (context, not a graded workload).
 * ``i8_skinny``    six int8 GEMMs shaped like the projections of a 7B-class
@@ -282,6 +283,13 @@ CONV2D_LAYERS = (
 CONV2D_CASES = tuple(
     ConvCase(f"i16_conv2d_{i}_{nm}", "i16", 1, hw, hw, c, k, f, f, (st, st), (pd, pd), (1, 1),
              Dist("uniform", 0, 255), Dist("normal_clip", I16_MIN, I16_MAX, 32.0), 60 + i)
+    for i, (nm, hw, c, k, f, st, pd) in enumerate(CONV2D_LAYERS)
+)
+# The same layers at batch 32, where the output traffic rather than the
+# launch latency bounds each layer; seeds 70 + i.
+CONV2D_B32_CASES = tuple(
+    ConvCase(f"i16_conv2d_b32_{i}_{nm}", "i16", 32, hw, hw, c, k, f, f, (st, st), (pd, pd),
+             (1, 1), Dist("uniform", 0, 255), Dist("normal_clip", I16_MIN, I16_MAX, 32.0), 70 + i)
     for i, (nm, hw, c, k, f, st, pd) in enumerate(CONV2D_LAYERS)
 )
 
