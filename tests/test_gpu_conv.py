@@ -255,3 +255,14 @@ def test_fuzz_conv(case):
     kid = -1 if kname == "auto" else _kid(kname)
     got = _gpu(X, W, Y, st, pd, dl, kernel=kid, split=split, x_off=x_off)
     assert np.array_equal(got, want), _describe(got, want)
+
+
+def test_window_deeper_than_one_workgroup_range():
+    """k = r*s*c = 3*3*4096 = 36864 exceeds the 32768 elements one
+    workgroup accumulates, so the lowered GEMM is sliced along k and the
+    slices are added atomically; full-range operands make the exact sums
+    wrap modulo 2^32. Every conv kernel of both types."""
+    for dt in ("i16", "i8"):
+        for name in CONV_KERNELS[dt]:
+            _check(dt, 1, 3, 4, 4096, 24, 3, 3, (1, 1), (1, 1), (1, 1), seed=88,
+                   kernel=_kid(name))
