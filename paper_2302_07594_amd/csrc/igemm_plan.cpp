@@ -174,8 +174,12 @@ static int auto_kernel(int es, int64_t m, int64_t n, int64_t k, const void *A, i
     if (m <= 32) return K_I16_32x128;
     // 128-column tiles on n <= 64 would multiply padding for half their
     // columns (measured on (401408, 64, 147): 205 us against 120 us with
-    // 64x64 tiles; (100352, 64, 576): 92 against 64 us).
-    if (n > 64 && tiles_of(K_I16_128x128, m, n) >= num_cu) return K_I16_128x128;
+    // 64x64 tiles; (100352, 64, 576): 92 against 64 us). Otherwise 128x128
+    // tiles pay from three quarters of a tile per compute unit: n = 128 and
+    // 256 with k = 512..2304 and 192-255 tiles ran 13-35% faster than 64x64
+    // tiles; at half a tile per unit the two were within +-20% either way.
+    if (n > 64 && 4 * tiles_of(K_I16_128x128, m, n) >= 3 * (int64_t)num_cu)
+        return K_I16_128x128;
     // Small outputs: time goes into each workgroup's latency chain (load,
     // stage, multiply, write back), so twice the workgroups of half the size
     // finish sooner (measured: 256x256x256 3.9 us against 5.6 us with 64x64
