@@ -309,9 +309,10 @@ int igemm_conv2d_i16(const igemm_conv2d_desc *desc, const int16_t *X, const int1
                      int32_t *Y, void *stream);
 int igemm_conv2d_i8(const igemm_conv2d_desc *desc, const int8_t *X, const int8_t *W,
                     int32_t *Y, void *stream);
-/* The same with an explicit kernel (one of the fused 16/32-row or 64x64 tile
- * kernels of the operand type; -1 = automatic) and k-slice count (-1 =
- * automatic); elem_bytes 2 (int16) or 1 (int8). For sweeps and tests. */
+/* The same with an explicit kernel (one of the fused 16/32-row, 64x64 or
+ * int16 128x128 tile kernels of the operand type; -1 = automatic) and k-slice
+ * count (-1 = automatic); elem_bytes 2 (int16) or 1 (int8). For sweeps and
+ * tests. */
 int igemm_conv2d_ex(int elem_bytes, const igemm_conv2d_desc *desc, const void *X,
                     const void *W, int32_t *Y, void *stream, int kernel, int split);
 /* Host-only plan of the lowered GEMM a convolution call would launch

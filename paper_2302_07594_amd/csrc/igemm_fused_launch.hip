@@ -27,6 +27,7 @@ const void *conv_kernel_fn(int id, int gather, bool vb, bool split) {
     switch (id) {
         case K_I8_32x256:
         case K_I8_16x256: return fused_conv_i8(id, gather, vb, split);
+        case K_I16_128x128:
         case K_I16_64x64:
         case K_I16_32x128:
         case K_I16_16x128: return fused_conv_i16(id, gather, vb, split);

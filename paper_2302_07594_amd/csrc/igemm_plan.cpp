@@ -178,7 +178,9 @@ static int auto_kernel(int es, int64_t m, int64_t n, int64_t k, const void *A, i
     // tiles pay from three quarters of a tile per compute unit: n = 128 and
     // 256 with k = 512..2304 and 192-255 tiles ran 13-35% faster than 64x64
     // tiles; at half a tile per unit the two were within +-20% either way.
-    if (n > 64 && 4 * tiles_of(K_I16_128x128, m, n) >= 3 * (int64_t)num_cu)
+    // Up to k = 256 the 64x64 tiles' single pass (every load at once, C
+    // fetched alongside) wins instead: (100352, 256, 64) 78 against 84 us.
+    if (n > 64 && k > 256 && 4 * tiles_of(K_I16_128x128, m, n) >= 3 * (int64_t)num_cu)
         return K_I16_128x128;
     // Small outputs: time goes into each workgroup's latency chain (load,
     // stage, multiply, write back), so twice the workgroups of half the size
@@ -402,17 +404,22 @@ int make_conv_plan(int es, const igemm_conv2d_desc *d, const void *X, const void
     if ((K + 2) * N * es + 64 >= 0x7fff0000) return IGEMM_ENOTSUP;
     int id = kernel;
     if (id < 0) {
+        // The rules of the GEMM planner's fused kernels (no packed path: the
+        // lowered matrix never exists).
+        const int64_t ncu = num_cu > 0 ? num_cu : 256;
         if (es == 2) {
             if (M <= 16) id = K_I16_16x128;
             else if (M <= 32) id = K_I16_32x128;
+            else if (N > 64 && K > 256 && 4 * tiles_of(K_I16_128x128, M, N) >= 3 * ncu)
+                id = K_I16_128x128;
             else if (tiles_of(K_I16_64x64, M, N) < 32) id = M <= 64 ? K_I16_32x128 : K_I16_16x128;
             else id = K_I16_64x64;
         } else {
             id = M <= 16 ? K_I8_16x256 : K_I8_32x256;
         }
     }
-    const bool conv_id = id == K_I16_64x64 || id == K_I16_32x128 || id == K_I16_16x128 ||
-                         id == K_I8_32x256 || id == K_I8_16x256;
+    const bool conv_id = id == K_I16_128x128 || id == K_I16_64x64 || id == K_I16_32x128 ||
+                         id == K_I16_16x128 || id == K_I8_32x256 || id == K_I8_16x256;
     if (!conv_id || kKernels[id].es != es) return IGEMM_EINVAL;
     int st = make_plan(es, M, N, K, X, K, W, N, N, num_cu, id, split, false, out);
     if (st != IGEMM_OK) return st;

@@ -334,7 +334,8 @@ def test_conv_invalid_arguments(es, fn):
     # kernels the lowering does not use, or of the other operand type
     for kid in range(ig.igemm_num_kernels()):
         name = ig.igemm_kernel_name(kid)
-        conv_ok = name in ("i16_64x64", "i16_32x128", "i16_16x128", "i8_32x256", "i8_16x256")
+        conv_ok = name in ("i16_128x128", "i16_64x64", "i16_32x128", "i16_16x128", "i8_32x256",
+                           "i8_16x256")
         ok = conv_ok and name.startswith("i16" if es == 2 else "i8")
         if not ok:
             with pytest.raises(ig.IgemmError):
@@ -385,7 +386,7 @@ def test_conv_plans_match_lowered_gemm():
         d = ig.conv_desc(case.n, case.h, case.w, case.c, case.k, case.r, case.s, case.stride,
                          case.pad, case.dil)
         p = ig.igemm_conv2d_query_plan(2, d)
-        assert p["kernel_name"] in ("i16_64x64", "i16_32x128", "i16_16x128")
+        assert p["kernel_name"] in ("i16_128x128", "i16_64x64", "i16_32x128", "i16_16x128")
         assert not p["packed"] and p["workspace_bytes"] == 0
         assert p["vec_a"] == (1 if (case.c * 2) % 16 == 0 else 0)
         assert p["split"] * p["k_chunk"] >= k > (p["split"] - 1) * p["k_chunk"]

@@ -9,7 +9,7 @@ from gpu_util import to_device
 
 pytestmark = pytest.mark.gpu
 
-CONV_KERNELS = {"i16": ("i16_64x64", "i16_32x128", "i16_16x128"),
+CONV_KERNELS = {"i16": ("i16_128x128", "i16_64x64", "i16_32x128", "i16_16x128"),
                 "i8": ("i8_32x256", "i8_16x256")}
 SENTINEL = 0x5A5A5A5A
 
