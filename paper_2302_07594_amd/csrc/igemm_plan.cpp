@@ -153,6 +153,20 @@ static bool stream_shape(int64_t m, int64_t n, int64_t k, int64_t lda, int64_t l
     return out->tiles * out->slices <= ((int64_t)1 << 32) / 512 - 1;
 }
 
+// k slices for the int16 128x128 tiles below one tile per compute unit. One
+// workgroup fits on a compute unit, so a grid beyond num_cu would run a
+// second, mostly empty round: slice up to num_cu / tiles, keeping at least
+// 512 k per slice. Measured: (1568, 512, 4608) 36 us with 4 slices (208
+// workgroups) against 45 us with 5 (260) and 46 with 2; (6272, 256, 2304)
+// 36 us with 2 slices against 46-49 us with 1, 3 or 4.
+static int64_t big_tile_split(int64_t tiles, int64_t k, int num_cu) {
+    if (tiles >= num_cu) return 1;
+    int64_t s = num_cu / tiles;
+    const int64_t cap = cdiv(k, kBK) / 8;
+    if (s > cap) s = cap;
+    return s < 1 ? 1 : s;
+}
+
 static int auto_kernel(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
                        const void *B, int64_t ldb, int64_t ldc, int num_cu, bool allow_packed) {
     const int pid = es == 2 ? K_I16_PACKED_128x128 : K_I8_PACKED_256x256;
@@ -180,8 +194,13 @@ static int auto_kernel(int es, int64_t m, int64_t n, int64_t k, const void *A, i
     // tiles; at half a tile per unit the two were within +-20% either way.
     // Up to k = 256 the 64x64 tiles' single pass (every load at once, C
     // fetched alongside) wins instead: (100352, 256, 64) 78 against 84 us.
-    if (n > 64 && k > 256 && 4 * tiles_of(K_I16_128x128, m, n) >= 3 * (int64_t)num_cu)
-        return K_I16_128x128;
+    // With k slices (big_tile_split) the same holds for fewer tiles: three
+    // quarters of the compute units busy with slices of at least 512 k.
+    if (n > 64 && k > 256) {
+        const int64_t t128 = tiles_of(K_I16_128x128, m, n);
+        if (4 * t128 * big_tile_split(t128, k, num_cu) >= 3 * (int64_t)num_cu)
+            return K_I16_128x128;
+    }
     // Small outputs: time goes into each workgroup's latency chain (load,
     // stage, multiply, write back), so twice the workgroups of half the size
     // finish sooner (measured: 256x256x256 3.9 us against 5.6 us with 64x64
@@ -261,6 +280,8 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
         s = split;
     } else if (tiles >= num_cu) {
         s = 1;
+    } else if (id == K_I16_128x128) {
+        s = big_tile_split(tiles, k, num_cu);
     } else {
         // Aim for two workgroups per compute unit, but keep at least two
         // k-tiles per slice so each slice still pipelines its loads (the
@@ -285,7 +306,8 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
     // Every k slice adds its partial tile into C with atomics; their cost
     // grows with m * n * slices (measured: past ~2^21 element updates it
     // outweighs the extra parallelism).
-    if (split <= 0) {
+    // (The 128x128 slices are long enough to carry their adds.)
+    if (split <= 0 && id != K_I16_128x128) {
         const int64_t cap = ((int64_t)1 << 21) / (m * n);
         if (s > cap) s = cap > 1 ? cap : 1;
     }
@@ -410,7 +432,10 @@ int make_conv_plan(int es, const igemm_conv2d_desc *d, const void *X, const void
         if (es == 2) {
             if (M <= 16) id = K_I16_16x128;
             else if (M <= 32) id = K_I16_32x128;
-            else if (N > 64 && K > 256 && 4 * tiles_of(K_I16_128x128, M, N) >= 3 * ncu)
+            else if (N > 64 && K > 256 &&
+                     4 * tiles_of(K_I16_128x128, M, N) *
+                             big_tile_split(tiles_of(K_I16_128x128, M, N), K, (int)ncu) >=
+                         3 * ncu)
                 id = K_I16_128x128;
             else if (tiles_of(K_I16_64x64, M, N) < 32) id = M <= 64 ? K_I16_32x128 : K_I16_16x128;
             else id = K_I16_64x64;
