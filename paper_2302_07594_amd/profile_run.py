@@ -3,7 +3,7 @@
 
 Usage (the program itself goes after ``rocprofv3 ... --``):
     python paper_2302_07594_amd/profile_run.py gemm <workload> [iters] [case]
-    python paper_2302_07594_amd/profile_run.py conv <layer> [iters]
+    python paper_2302_07594_amd/profile_run.py conv <layer> [iters] [b32]
     python paper_2302_07594_amd/profile_run.py srs <workload> <kc> <shift> [iters]
     python paper_2302_07594_amd/profile_run.py copy <MiB> [iters]
     python paper_2302_07594_amd/profile_run.py summarize <rocprof output dir>
@@ -13,7 +13,7 @@ Usage (the program itself goes after ``rocprofv3 ... --``):
 ``gemm`` runs the library's igemm call on the named workload's case (inputs
 generated as in the benchmark, C reset is not needed for timing); ``conv``
 runs the convolution entry point on one of the six network layers (index
-into ``workloads.CONV2D_CASES``); ``srs`` runs the int16-output update on a
+into ``workloads.CONV2D_CASES``, or ``CONV2D_B32_CASES`` with ``b32``); ``srs`` runs the int16-output update on a
 workload's A and B (int16 C) with block size kc and the given shift.
 ``copy`` runs a device-to-device copy of a tensor of the given size; its
 FETCH_SIZE / WRITE_SIZE readings calibrate the counters against a known byte
@@ -60,12 +60,12 @@ def _gemm(wname: str, iters: int, case_idx: int) -> None:
     print(f"ran {case.name} x{iters}", flush=True)
 
 
-def _conv(layer: int, iters: int) -> None:
+def _conv(layer: int, iters: int, batch32: bool = False) -> None:
     import torch
 
     import paper_2302_07594_amd as ig
     import workloads
-    case = workloads.CONV2D_CASES[layer]
+    case = (workloads.CONV2D_B32_CASES if batch32 else workloads.CONV2D_CASES)[layer]
     X, W, Y = workloads.generate_conv(case)
     Xd, Wd, Yd = (torch.from_numpy(x).cuda() for x in (X, W, Y))
     for _ in range(iters):
@@ -239,7 +239,8 @@ def main(argv) -> None:
     if cmd == "gemm":
         _gemm(argv[2], int(argv[3]) if len(argv) > 3 else 3, int(argv[4]) if len(argv) > 4 else 0)
     elif cmd == "conv":
-        _conv(int(argv[2]), int(argv[3]) if len(argv) > 3 else 3)
+        _conv(int(argv[2]), int(argv[3]) if len(argv) > 3 else 3,
+              len(argv) > 4 and argv[4] == "b32")
     elif cmd == "srs":
         _srs(argv[2], int(argv[3]), int(argv[4]), int(argv[5]) if len(argv) > 5 else 3)
     elif cmd == "copy":
