@@ -13,8 +13,9 @@ Usage (the program itself goes after ``rocprofv3 ... --``):
 ``gemm`` runs the library's igemm call on the named workload's case (inputs
 generated as in the benchmark, C reset is not needed for timing); ``conv``
 runs the convolution entry point on one of the six network layers (index
-into ``workloads.CONV2D_CASES``, or ``CONV2D_B32_CASES`` with ``b32``); ``srs`` runs the int16-output update on a
-workload's A and B (int16 C) with block size kc and the given shift.
+into ``workloads.CONV2D_CASES``, or ``CONV2D_B32_CASES`` with ``b32``);
+``srs`` runs the int16-output update on a workload's A and B (int16 C) with
+block size kc and the given shift.
 ``copy`` runs a device-to-device copy of a tensor of the given size; its
 FETCH_SIZE / WRITE_SIZE readings calibrate the counters against a known byte
 count. ``summarize`` prints per-kernel average durations from a
