@@ -153,12 +153,15 @@ static bool stream_shape(int64_t m, int64_t n, int64_t k, int64_t lda, int64_t l
     return out->tiles * out->slices <= ((int64_t)1 << 32) / 512 - 1;
 }
 
-// k slices for the int16 128x128 tiles below one tile per compute unit. One
-// workgroup fits on a compute unit, so a grid beyond num_cu would run a
-// second, mostly empty round: slice up to num_cu / tiles, keeping at least
-// 512 k per slice. Measured: (1568, 512, 4608) 36 us with 4 slices (208
-// workgroups) against 45 us with 5 (260) and 46 with 2; (6272, 256, 2304)
-// 36 us with 2 slices against 46-49 us with 1, 3 or 4.
+// k slices for the 128x128 tiles (int16 and int8) below one tile per compute
+// unit. One workgroup fits on a compute unit, so a grid beyond num_cu would
+// run a second, mostly empty round: slice up to num_cu / tiles, keeping at
+// least 512 k per slice. Measured, int16: (1568, 512, 4608) 36 us with 4
+// slices (208 workgroups) against 45 us with 5 (260) and 46 with 2;
+// (6272, 256, 2304) 36 us with 2 slices against 46-49 us with 1, 3 or 4.
+// int8: (1568, 512, 4608) 22.4 us with 4 slices against 26.0 with 2 and 25.0
+// with 5; (6272, 256, 2304) 24.2 us with 2 against 32.1 with 1;
+// (1024, 1024, 8192) 33.7 us with 4 against 47.8 with 2 and 41.1 with 5.
 static int64_t big_tile_split(int64_t tiles, int64_t k, int num_cu) {
     if (tiles >= num_cu) return 1;
     int64_t s = num_cu / tiles;
@@ -280,7 +283,10 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
         s = split;
     } else if (tiles >= num_cu) {
         s = 1;
-    } else if (id == K_I16_128x128) {
+    } else if ((id == K_I16_128x128 || id == K_I8_128x128) &&
+               2 * tiles * big_tile_split(tiles, k, num_cu) >= num_cu) {
+        // (Outputs too small to keep half the units busy this way keep the
+        // rule below.)
         s = big_tile_split(tiles, k, num_cu);
     } else {
         // Aim for two workgroups per compute unit, but keep at least two
@@ -306,8 +312,11 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
     // Every k slice adds its partial tile into C with atomics; their cost
     // grows with m * n * slices (measured: past ~2^21 element updates it
     // outweighs the extra parallelism).
-    // (The 128x128 slices are long enough to carry their adds.)
-    if (split <= 0 && id != K_I16_128x128) {
+    // (The 128x128 slices of the rule above are long enough to carry their
+    // adds.)
+    const bool big_slices = (id == K_I16_128x128 || id == K_I8_128x128) && tiles < num_cu &&
+                            2 * tiles * big_tile_split(tiles, k, num_cu) >= num_cu;
+    if (split <= 0 && !big_slices) {
         const int64_t cap = ((int64_t)1 << 21) / (m * n);
         if (s > cap) s = cap > 1 ? cap : 1;
     }
