@@ -286,7 +286,9 @@ int igemm_i8_packed_b(int64_t m, int64_t n, int64_t k,
  * window does not fit), likewise ow; igemm_conv2d_out_dim computes it.
  * Y must not overlap X or W. An input whose channel rows are 16-byte aligned
  * (X 16-byte aligned, c*element size a multiple of 16) is gathered 16 bytes at
- * a time; any other is gathered element by element.
+ * a time; with horizontal dilation 1 (or s = 1) and s*c at least 7 (int16)
+ * or 15 (int8), the s*c contiguous elements a filter row covers are read as
+ * runs with unaligned 16-byte loads; any other input element by element.
  *
  * Errors: IGEMM_EINVAL (before any HIP call) for a NULL descriptor, negative
  * extents, r or s < 1, strides or dilations < 1, negative padding, NULL
