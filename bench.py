@@ -19,9 +19,11 @@ Prints ONE JSON line. Besides the headline value it carries:
                 rocprofv3 counted for that kernel (committed summary);
   cpu_baseline  the CPU oracle timed on the host cores over a bounded sample
                 of the same workload;
-  per_config    every other workload, each timed the same way (memory-bound
-                ones rotate through enough buffer sets to defeat the 256 MB
-                last-level cache), with its own roofline fraction; then the
+  per_config    every other workload, each by graph replay (median of five
+                repetitions of at least 20 ms; memory-bound ones rotate
+                through enough buffer sets to defeat the 256 MB last-level
+                cache), with its own roofline fraction (memory-bound ones
+                also against a measured 1 GiB device copy); then the
                 paper's own GEMM shape (4096, 4096, 290), for context, the
                 same shape through the int16-output entry point with the
                 paper's k_c = 290 and shift 0 (and 4096^3 with k_c = 256),
@@ -117,20 +119,61 @@ def roofline_for(dtype, m, n, k, seconds):
     return "hbm", nbytes / seconds / 1e9, HBM_GBS, "GB/s"
 
 
-def time_launches(fn, iters):
-    """Average device time per launch (HIP events on the current stream)."""
+def time_graph(g, per_graph, reps=5, min_rep_ms=20.0):
+    """Device time per launch of a captured graph of per_graph launches: the
+    median over `reps` repetitions, each replaying the graph back to back for
+    at least min_rep_ms (HIP events on the current stream)."""
+    import statistics
+
     import torch
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     e0.record()
-    for i in range(iters):
-        fn(i)
+    g.replay()
     e1.record()
     torch.cuda.synchronize()
-    return e0.elapsed_time(e1) * 1e-3 / iters
+    per_replay_ms = max(e0.elapsed_time(e1), 1e-3)
+    n = max(1, -(-int(min_rep_ms * 1000) // int(per_replay_ms * 1000 + 1)))
+    times = []
+    for _ in range(reps):
+        e0.record()
+        for _ in range(n):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) * 1e-3 / (n * per_graph))
+    return statistics.median(times)
 
 
-def bench_case(case, min_sets=1, per_graph=40, reps=10, warmup=3):
+TIMING = "hip graph replay: median of 5 repetitions of >= 20 ms"
+
+
+def copy_bandwidth(nbytes=1 << 30, reps=5):
+    """Device-to-device copy rate (bytes read plus written per second) of a
+    1 GiB buffer, larger than the 256 MB last-level cache."""
+    import statistics
+
+    import torch
+    x = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(2):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    ts = []
+    for _ in range(reps):
+        e0.record()
+        y.copy_(x)
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) * 1e-3)
+    del x, y
+    torch.cuda.empty_cache()
+    return 2.0 * nbytes / statistics.median(ts)
+
+
+def bench_case(case, min_sets=1, per_graph=40, warmup=3):
     """Time one workload case on rotating device copies of its operands.
 
     The launches are captured once in a HIP graph (per_graph launches cycling
@@ -158,7 +201,7 @@ def bench_case(case, min_sets=1, per_graph=40, reps=10, warmup=3):
             f(*sets[i % nsets])
     g.replay()
     torch.cuda.synchronize()
-    t = time_launches(lambda i: g.replay(), reps) / per_graph
+    t = time_graph(g, per_graph)
     plan = ig.igemm_query_plan(es, case.m, case.n, case.k)
     bound, ach, peak, unit = roofline_for(case.dtype, case.m, case.n, case.k, t)
     return {
@@ -166,14 +209,14 @@ def bench_case(case, min_sets=1, per_graph=40, reps=10, warmup=3):
         "kernel": plan["kernel_name"], "split": plan["split"], "grid": plan["grid"],
         "us": round(t * 1e6, 2), "TOPS": round(2.0 * case.m * case.n * case.k / t / 1e12, 2),
         "bound": bound, "achieved": round(ach, 1), "peak": peak, "unit": unit,
-        "frac": round(ach / peak, 4), "buffer_sets": nsets, "timing": "hip graph replay",
+        "frac": round(ach / peak, 4), "buffer_sets": nsets, "timing": TIMING,
         # the int8 counter summary was taken on this very workload
         **({"rocprof_mfma": measured_mfma("i8")}
            if (case.dtype, case.m, case.n, case.k) == ("i8", 8192, 8192, 8192) else {}),
     }
 
 
-def bench_srs_case(case, kc, shift, per_graph=40, reps=10, warmup=3):
+def bench_srs_case(case, kc, shift, per_graph=40, warmup=3):
     """Time the int16-output update (one fused launch per k block of kc,
     shift-round-saturate conversion, int16 C) on a workload's A and B with a
     random int16 C, like bench_case; the algorithmic bytes are A and B once
@@ -199,7 +242,7 @@ def bench_srs_case(case, kc, shift, per_graph=40, reps=10, warmup=3):
             ig.gemm_srs(*sets[i % nsets], kc=kc, shift=shift)
     g.replay()
     torch.cuda.synchronize()
-    t = time_launches(lambda i: g.replay(), reps) / per_graph
+    t = time_graph(g, per_graph)
     m, n, k = case.m, case.n, case.k
     nblocks = 1 if (kc == 0 or kc >= k) else -(-k // kc)
     ops = 2.0 * m * n * k
@@ -215,11 +258,11 @@ def bench_srs_case(case, kc, shift, per_graph=40, reps=10, warmup=3):
         "epilogue": "int16 C += sat16(floor(block product / 2^shift)) modulo 2^16",
         "us": round(t * 1e6, 2), "TOPS": round(ops / t / 1e12, 2),
         "bound": bound, "achieved": round(ach, 1), "peak": peak, "unit": unit,
-        "frac": round(ach / peak, 4), "buffer_sets": nsets, "timing": "hip graph replay",
+        "frac": round(ach / peak, 4), "buffer_sets": nsets, "timing": TIMING,
     }
 
 
-def bench_conv_case(case, per_graph=40, reps=10, warmup=3):
+def bench_conv_case(case, per_graph=40, warmup=3):
     """Time one convolution (implicit GEMM: IM2ROW gathered in the kernel)
     like bench_case; the roofline counts the lowered GEMM's multiply-adds
     and the unique bytes of X, W and Y (read and written)."""
@@ -243,7 +286,7 @@ def bench_conv_case(case, per_graph=40, reps=10, warmup=3):
             ig.conv2d(*sets[i % nsets], **kw)
     g.replay()
     torch.cuda.synchronize()
-    t = time_launches(lambda i: g.replay(), reps) / per_graph
+    t = time_graph(g, per_graph)
     m, n, k = case.gemm_shape()
     d = ig.conv_desc(case.n, case.h, case.w, case.c, case.k, case.r, case.s, case.stride,
                      case.pad, case.dil)
@@ -264,7 +307,7 @@ def bench_conv_case(case, per_graph=40, reps=10, warmup=3):
         "grid": plan["grid"], "vector_gather": bool(plan["vec_a"]),
         "us": round(t * 1e6, 2), "TOPS": round(ops / t / 1e12, 2),
         "bound": bound, "achieved": round(ach, 1), "peak": peak, "unit": unit,
-        "frac": round(ach / peak, 4), "buffer_sets": nsets, "timing": "hip graph replay",
+        "frac": round(ach / peak, 4), "buffer_sets": nsets, "timing": TIMING,
     }
 
 
@@ -417,12 +460,19 @@ def main():
         log("bench: per-config int16-output update")
         per.append(bench_srs_case(workloads.WORKLOADS["i16_paper"].cases[0], 290, 0))
         per.append(bench_srs_case(workloads.WORKLOADS["i16_4096"].cases[0], 256, 0,
-                                  per_graph=10, reps=5))
+                                  per_graph=10))
         torch.cuda.empty_cache()
         for c in workloads.CONV2D_CASES + workloads.CONV2D_B32_CASES:
             log(f"bench: per-config {c.name}")
             per.append(bench_conv_case(c, per_graph=40 if c.n == 1 else 10))
             torch.cuda.empty_cache()
+        # Memory-bound entries also against a measured device copy.
+        log("bench: device-to-device copy bandwidth")
+        cbw = copy_bandwidth()
+        out["copy_bandwidth_GBs"] = round(cbw / 1e9, 1)
+        for r in per:
+            if r["bound"] == "hbm":
+                r["frac_of_copy"] = round(r["achieved"] * 1e9 / cbw, 4)
         out["per_config"] = per
     print(json.dumps(out), flush=True)
 
