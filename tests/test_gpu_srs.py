@@ -225,3 +225,20 @@ def test_fuzz_srs(case):
     A, B, C = _operands(dt, m, n, k, seed=9000 + i, lo=lo, hi=hi, pad=pads)
     kid = -1 if kname == "auto" else _kid(kname)
     _check(A, B, C, m, n, k, kc, shift, rnd, kernel=kid, offsets=offs)
+
+
+def test_4096_cube_blocks_of_256_sampled_rows():
+    """The benchmark's second int16-output configuration: 4096^3 with
+    k_c = 256 (sixteen blocks), full-range operands, random int16 C; whole
+    rows sampled across the tiles against the oracle on those rows."""
+    case = workloads.WORKLOADS["i16_4096"].cases[0]
+    m, n, k = case.m, case.n, case.k
+    A, B, _ = workloads.generate(case)
+    C = np.random.default_rng(case.seed).integers(-32768, 32767, size=(m, n), dtype=np.int16,
+                                                  endpoint=True)
+    _, got = _gpu(A, B, C, m, n, k, 256, 0, False)
+    rows = np.r_[0, 127:129, 2048, 4095]
+    import oracle
+    want = C[rows].copy()
+    oracle.igemm_srs(np.ascontiguousarray(A[rows]), B, want, 256, 0, False)
+    assert np.array_equal(got[rows], want), _describe(got[rows], want)
