@@ -352,8 +352,11 @@ int64_t igemm_conv2d_out_dim(int64_t in, int64_t f, int64_t stride, int64_t pad,
  * (igemm_i8_srs); C is int16, m x n, row-major with leading dimension ldc,
  * updated in place; DEVICE pointers owned by the caller; any alignment.
  * shift in [0, 47] (the paper's accumulators are 48 bits wide); kc >= 0 and a
- * block of at most 32768 elements. One kernel launch per block, enqueued in
- * order on `stream`; no workspace.
+ * block of at most 32768 elements. Large int16 products whose blocks are one
+ * block or multiples of 256 elements (at most 64 blocks) are packed once into
+ * a workspace from the library's pool, as igemm_i16 packs them (not while the
+ * stream is being captured); then, and otherwise, one kernel launch per
+ * block, enqueued in order on `stream`.
  *
  * Errors: IGEMM_EINVAL (before any HIP call, nothing enqueued) as for
  * igemm_i16 and for kc < 0, shift outside [0, 47], round_half_up not 0 or 1;
@@ -368,7 +371,9 @@ int igemm_i8_srs(int64_t m, int64_t n, int64_t k, const int8_t *A, int64_t lda,
                  int round_half_up, void *stream);
 /* The same with elem_bytes 2 (int16) or 1 (int8) and an explicit kernel (one
  * of the fused 16/32-row, 64x64 or int16 128x128 tile kernels of the operand
- * type; -1 = automatic). For sweeps and tests. */
+ * type, or the int16 packed kernel for one block or blocks of a multiple of
+ * 256, at most 64, outside stream capture; -1 = automatic). For sweeps and
+ * tests. */
 int igemm_srs_ex(int elem_bytes, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
                  const void *B, int64_t ldb, int16_t *C, int64_t ldc, int64_t kc, int shift,
                  int round_half_up, void *stream, int kernel);

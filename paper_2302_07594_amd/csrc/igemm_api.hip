@@ -253,6 +253,35 @@ int run_srs(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
     if (m == 0 || n == 0 || k == 0) return IGEMM_OK;
     const int64_t blk = (kc == 0 || kc > k) ? k : kc;
     const int64_t nblocks = (k + blk - 1) / blk;
+    if (blk > kMaxKChunk) return IGEMM_ENOTSUP;
+    // Large int16 products whose blocks fall on the packed k-tiles (one
+    // block, or blocks of a multiple of 256): pack once into a workspace
+    // from the pool, then one multiply launch per block. Not under stream
+    // capture (no pool).
+    const bool packed_ok = es == 2 && nblocks <= 64 && (nblocks == 1 || blk % 256 == 0);
+    if (kernel == K_I16_PACKED_128x128 && !packed_ok) return IGEMM_EINVAL;
+    if (kernel == K_I16_PACKED_128x128 || (kernel < 0 && packed_ok)) {
+        hipStream_t s = (hipStream_t)stream;
+        const bool capturing = stream_is_capturing(s);
+        if (kernel >= 0 && capturing) return IGEMM_EINVAL;
+        igemm_plan pp;
+        st = make_plan(es, m, n, k, A, lda, B, ldb, ldc, num_cu_of_current_device(),
+                       kernel < 0 ? -1 : kernel, -1, !capturing, &pp);
+        if (st != IGEMM_OK) return st;
+        if (pp.packed) {
+            const int64_t sums = srs_sums_bytes(pp, m, n, k, nblocks, A, lda);
+            Scratch sc;
+            st = get_scratch(nullptr, 0, pp.workspace_bytes + sums, s, &sc);
+            if (st != IGEMM_OK) return st;
+            st = pack_both(es, pp, m, n, k, A, lda, B, ldb, sc.ptr, stream);
+            if (st == IGEMM_OK)
+                st = launch_srs_packed(pp, m, n, k, blk, nblocks, A, lda, C, ldc, sc.ptr,
+                                       (const char *)sc.ptr + pp.packed_a_bytes,
+                                       (uint32_t *)((char *)sc.ptr + pp.workspace_bytes), shift,
+                                       round_half_up, stream);
+            return put_scratch(sc, s, st);
+        }
+    }
     for (int pass = 0; pass < 2; ++pass) {
         const int num_cu = pass == 0 ? 0 : num_cu_of_current_device();
         for (int64_t q = 0; q < nblocks; ++q) {

@@ -143,6 +143,17 @@ const void *fused_srs(int id, bool va, bool vb);
 int launch_conv(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const ConvGeom &g,
                 int gather, const void *X, const void *W, int32_t *Y, int64_t ldy,
                 void *stream);
+// The int16-output update on packed int16 operands (a packed plan whose
+// workspace the pack kernels have filled): exact per-block limb sums of the
+// packed planes into `sums` (srs_sums_bytes), then one multiply launch per
+// block. nblocks <= 64; blocks of kc elements, a multiple of 256 unless
+// there is one block.
+int64_t srs_sums_bytes(const igemm_plan &p, int64_t m, int64_t n, int64_t k, int64_t nblocks,
+                       const void *A, int64_t lda);
+int launch_srs_packed(const igemm_plan &p, int64_t m, int64_t n, int64_t k, int64_t kc,
+                      int64_t nblocks, const void *A, int64_t lda, int16_t *C, int64_t ldc,
+                      const void *a_part, const void *b_part, uint32_t *sums, int shift,
+                      int round_half_up, void *stream);
 // The int16-output update of one k block (plan without k slices): C16 +=
 // srs(A B) modulo 2^16 with the given shift and rounding.
 int launch_srs(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,

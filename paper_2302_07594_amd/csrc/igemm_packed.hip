@@ -189,18 +189,58 @@ pack_b(const void *__restrict__ Bv, int64_t ldb, int k, int n, int k_pad, int ks
     }
 }
 
+// ---- exact limb sums per k block, from packed planes ------------------------
+// For the int16-output update (each k block converted on its own): row r of
+// the plane pair (P0 = high limbs, P1 = offset low limbs), rows of k_pad
+// bytes, summed over each block of kc bytes (kc a multiple of 256; blocks
+// past k hold only the zero padding): out[(b * rows + r) * 2] = sum of the
+// high limbs of block b, out[... + 1] = sum of the low limbs (exact int32).
+// One workgroup per row; at most 64 blocks.
+__global__ void __launch_bounds__(256)
+block_sums(const int8_t *__restrict__ P0, const int8_t *__restrict__ P1, int64_t plane_ld,
+           int rows, int k_pad, int kc, int nblocks, uint32_t *__restrict__ out) {
+    __shared__ int sh[64][2];
+    const int r = blockIdx.x, tid = threadIdx.x;
+    for (int i = tid; i < 2 * 64; i += 256) (&sh[0][0])[i] = 0;
+    __syncthreads();
+    const int8_t *p0 = P0 + (int64_t)r * plane_ld;
+    const int8_t *p1 = P1 + (int64_t)r * plane_ld;
+    for (int e = tid * 16; e < k_pad; e += 256 * 16) {
+        const int b = e / kc;
+        const v4i x0 = *(const v4i *)(p0 + e), x1 = *(const v4i *)(p1 + e);
+        int s0 = sum4((u32)x0.x, 0), s1 = sum4((u32)x1.x, 0);
+        s0 = sum4((u32)x0.w, sum4((u32)x0.z, sum4((u32)x0.y, s0)));
+        s1 = sum4((u32)x1.w, sum4((u32)x1.z, sum4((u32)x1.y, s1)));
+        atomicAdd(&sh[b][0], s0);
+        atomicAdd(&sh[b][1], s1);
+    }
+    __syncthreads();
+    for (int b = tid; b < nblocks; b += 256) {
+        out[((int64_t)b * rows + r) * 2] = (u32)sh[b][0];
+        out[((int64_t)b * rows + r) * 2 + 1] = (u32)sh[b][1];
+    }
+}
+
 // ---- the packed-operand GEMM ---------------------------------------------
 // A planes: P x m_pad x k_pad (row stride lda_p, plane stride a_plane), B
-// planes: P x n_pad x k_pad. ktiles = k_pad / 64 is a multiple of 4. NST is
+// planes: P x n_pad x k_pad; ktiles k-tiles of 64 from the given origin. NST is
 // the number of LDS stages of the DMA ring (4, or 3 for tiles whose stage
 // is too large for four).
-template <int ES, int BM, int BN, int WM, int WN, int NST>
+// EPI 1 (int16 only): C is int16 (passed through the int32 pointer) and
+// gets srs(A B) of this launch's k range added modulo 2^16, the product
+// converted by an arithmetic shift right by (epi & 0xff) bits (half a unit
+// added first when bit 8 is set) and saturation; corrA / corrB then hold the
+// exact (high, low) limb sums of the range per row / column, and kconst is
+// 16384 times the range's length.
+// RAGGED: ktiles need not be a multiple of four (at least three), so that the
+// zero padding of k to a multiple of 256 is not multiplied; otherwise it is.
+template <int ES, int BM, int BN, int WM, int WN, int NST, int EPI = 0, bool RAGGED = false>
 __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64, 1)
 igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
              const int8_t *__restrict__ Bp, int64_t ldb_p, int64_t b_plane,
              const uint32_t *__restrict__ corrA, const uint32_t *__restrict__ corrB,
              uint32_t kconst, int32_t *__restrict__ C, int64_t ldc,
-             int m, int n, int ktiles, int tiles_m, int tiles_n) {
+             int m, int n, int ktiles, int tiles_m, int tiles_n, int epi) {
     constexpr int MF = 32;
     typedef Mfma<MF> M;
     typedef typename M::acc_t acc_t;
@@ -222,6 +262,7 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     static_assert(NBA % NW == 0 && NBB % NW == 0, "DMA blocks per wave");
     constexpr int DPA = NBA / NW, DPB = NBB / NW, DPW = DPA + DPB;
     static_assert(DPW <= 15, "outstanding DMA count fits s_waitcnt");
+    static_assert(EPI == 0 || ES == 2, "the int16-output update is for int16 operands");
 
     // The LDS stages as separate objects, so that the compiler can tell the
     // DMA writes of one stage from the fragment reads of another.
@@ -430,8 +471,10 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     __builtin_amdgcn_s_barrier();
     read_frags(ic<0>{}, ic<0>{}, ic<0>{});
     // Groups of NST steps in which every step starts a DMA and prefetches,
-    // then the remaining T = ktiles - kt steps (T in [NST-1, 2*NST-2]; ktiles
-    // is a multiple of 4 and at least 4).
+    // then the remaining T = ktiles - kt steps (T in [NST-1, 2*NST-2];
+    // ktiles >= NST - 1, a multiple of four unless RAGGED). The planes are
+    // zero-padded to a multiple of four k-tiles, so the prologue's loads stay
+    // inside them.
     int kt = 0;
     for (; kt <= ktiles - 2 * NST + 1; kt += NST) {
         step(ic<0>{}, kt, ic<1>{}, ic<1>{});
@@ -439,8 +482,19 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
         step(ic<2>{}, kt + 2, ic<1>{}, ic<1>{});
         if constexpr (NST == 4) step(ic<3>{}, kt + 3, ic<1>{}, ic<1>{});
     }
-    if constexpr (NST == 4) {
+    if constexpr (NST == 4 && !RAGGED) {
         tail(ic<4>{}, kt);
+    } else if constexpr (NST == 4) {
+        // T = ktiles - kt lies in [3, 6] (the host passes ktiles >= 3).
+        const int T = ktiles - kt;
+        if (T == 4)
+            tail(ic<4>{}, kt);
+        else if (T == 3)
+            tail(ic<3>{}, kt);
+        else if (T == 5)
+            tail(ic<5>{}, kt);
+        else
+            tail(ic<6>{}, kt);
     } else {
         const int T = ktiles - kt;
         if (T == 2)
@@ -460,7 +514,7 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int r = 0; r < M::REGS; ++r) rowt[i][r] = 0;
-    if constexpr (ES == 2) {
+    if constexpr (ES == 2 && EPI == 0) {
         if (corrA != nullptr) {
 #pragma unroll
             for (int j = 0; j < TN; ++j)
@@ -479,12 +533,27 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     // epilogue has no branches and the compiler can count the outstanding
     // loads exactly (with a branch per element it waits for all of them
     // before every store).
-    const __amdgpu_buffer_rsrc_t Crs =
-        __builtin_amdgcn_make_buffer_rsrc(C + (int64_t)m0 * ldc + n0, 0, 0x7fffffff, 0x00020000);
+    constexpr u32 CE = EPI == 1 ? 2u : 4u;  // bytes per C element
+    const __amdgpu_buffer_rsrc_t Crs = __builtin_amdgcn_make_buffer_rsrc(
+        (char *)C + ((int64_t)m0 * ldc + n0) * CE, 0, 0x7fffffff, 0x00020000);
     const int ldc32 = (int)ldc;
     auto c_off = [&](int lr, int lc) -> u32 {
-        return (m0 + lr < m && n0 + lc < n) ? (u32)(lr * ldc32 + lc) * 4u : 0x80000000u;
+        return (m0 + lr < m && n0 + lc < n) ? (u32)(lr * ldc32 + lc) * CE : 0x80000000u;
     };
+    // EPI 1: exact (high, low) limb sums of this lane's columns; the rows'
+    // are loaded with each batch.
+    int colh[EPI == 1 ? TN : 1], coll[EPI == 1 ? TN : 1];
+    if constexpr (EPI == 1) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const uint2 q = *(const uint2 *)(corrB + 2 * (n0 + wn0 + MF * j + M::out_col(lane)));
+            colh[j] = (int)q.x;
+            coll[j] = (int)q.y;
+        }
+    }
+    const int srs_shift = epi & 0xff;
+    const int64_t srs_half =
+        ((epi >> 8) & 1) != 0 && srs_shift > 0 ? (int64_t)1 << (srs_shift - 1) : 0;
     // C is read, added to and written back in batches of NB output blocks,
     // software-pipelined: the loads of batch b+1 are issued before batch b is
     // added and stored, so a wave keeps up to 2 * NB * REGS loads in flight.
@@ -496,6 +565,7 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     constexpr int NBATCH = NOUT / NB;
     static_assert(NOUT % NB == 0 && NBATCH <= 8, "epilogue batches");
     int32_t cv[2][NB][M::REGS];
+    uint2 rv[EPI == 1 ? 2 : 1][EPI == 1 ? NB : 1][EPI == 1 ? M::REGS : 1];
     auto load_batch = [&](auto buf, auto batch) {
         constexpr int BF = decltype(buf)::value, B0 = decltype(batch)::value * NB;
 #pragma unroll
@@ -505,7 +575,14 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
 #pragma unroll
             for (int r = 0; r < M::REGS; ++r) {
                 const int lr = wm0 + MF * i + M::out_row(lane, r);
-                cv[BF][bb][r] = __builtin_amdgcn_raw_buffer_load_b32(Crs, c_off(lr, lc), 0, 0);
+                if constexpr (EPI == 1) {
+                    cv[BF][bb][r] = (int32_t)(int16_t)__builtin_amdgcn_raw_buffer_load_b16(
+                        Crs, c_off(lr, lc), 0, 0);
+                    rv[BF][bb][r] = *(const uint2 *)(corrA + 2 * (m0 + lr));
+                } else {
+                    cv[BF][bb][r] =
+                        __builtin_amdgcn_raw_buffer_load_b32(Crs, c_off(lr, lc), 0, 0);
+                }
             }
         }
     };
@@ -518,6 +595,20 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
 #pragma unroll
             for (int r = 0; r < M::REGS; ++r) {
                 const int lr = wm0 + MF * i + M::out_row(lane, r);
+                if constexpr (EPI == 1) {
+                    // exact product of this k range, converted and added mod 2^16
+                    const int64_t a64 =
+                        (int64_t)acc[0][i][j][r] * 65536 + (int64_t)acc[1][i][j][r] * 256 +
+                        (int64_t)acc[2][i][j][r] +
+                        (int64_t)((int)rv[BF][bb][r].x + colh[j]) * 32768 +
+                        (int64_t)((int)rv[BF][bb][r].y + coll[j]) * 128 + (int64_t)kconst;
+                    int64_t t = (a64 + srs_half) >> srs_shift;
+                    t = t > 32767 ? 32767 : (t < -32768 ? -32768 : t);
+                    __builtin_amdgcn_raw_buffer_store_b16(
+                        (unsigned short)(u32)(cv[BF][bb][r] + (int32_t)t), Crs, c_off(lr, lc), 0,
+                        0);
+                    continue;
+                }
                 u32 v;
                 if constexpr (ES == 1) {
                     v = (u32)acc[0][i][j][r];
@@ -620,6 +711,57 @@ int launch_pack_b(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, 
     return hipGetLastError() == hipSuccess ? IGEMM_OK : IGEMM_EHIP;
 }
 
+int64_t srs_sums_bytes(const igemm_plan &p, int64_t m, int64_t n, int64_t k, int64_t nblocks,
+                       const void *A, int64_t lda) {
+    PackedLayout L;
+    packed_layout(2, m, n, k, p.kernel, A, lda, &L);
+    return 8 * nblocks * (L.m_pad + L.n_pad);
+}
+
+int launch_srs_packed(const igemm_plan &p, int64_t m, int64_t n, int64_t k, int64_t kc,
+                      int64_t nblocks, const void *A, int64_t lda, int16_t *C, int64_t ldc,
+                      const void *a_part, const void *b_part, uint32_t *sums, int shift,
+                      int round_half_up, void *stream_) {
+    hipStream_t stream = (hipStream_t)stream_;
+    PackedLayout L;
+    packed_layout(2, m, n, k, p.kernel, A, lda, &L);
+    if (nblocks < 1 || nblocks > 64 || (nblocks > 1 && kc % 256 != 0)) return IGEMM_EINVAL;
+    const int8_t *wa = (const int8_t *)a_part, *wb = (const int8_t *)b_part;
+    const int8_t *Apk = wa + L.off_a, *Bpk = wb + L.off_b;
+    const int64_t a_plane = L.m_pad * L.k_pad, b_plane = L.n_pad * L.k_pad;
+    const int kb = nblocks == 1 ? (int)L.k_pad : (int)kc;  // block span in the planes
+    uint32_t *sa = sums, *sb = sums + 2 * nblocks * L.m_pad;
+    block_sums<<<dim3((unsigned)L.m_pad), 256, 0, stream>>>(Apk, Apk + a_plane, L.k_pad,
+                                                            (int)L.m_pad, (int)L.k_pad, kb,
+                                                            (int)nblocks, sa);
+    block_sums<<<dim3((unsigned)L.n_pad), 256, 0, stream>>>(Bpk, Bpk + b_plane, L.k_pad,
+                                                            (int)L.n_pad, (int)L.k_pad, kb,
+                                                            (int)nblocks, sb);
+    if (hipGetLastError() != hipSuccess) return IGEMM_EHIP;
+    const KernelDesc &d = kKernels[p.kernel];
+    const int tm = (int)(L.m_pad / d.bm), tn = (int)(L.n_pad / d.bn);
+    const int mi = (int)m, ni = (int)n;
+    const int epi = (shift & 0xff) | (round_half_up ? 0x100 : 0);
+    const dim3 grid((unsigned)(tm * tn));
+    // One launch per block, in order (the update modulo 2^16 makes the order
+    // immaterial); block q spans [q kb, q kb + kb) of the planes.
+    for (int64_t q = 0; q < nblocks; ++q) {
+        const int64_t k0 = q * kb;
+        const int64_t span = L.k_pad - k0 < kb ? L.k_pad - k0 : kb;   // a multiple of 256
+        const int64_t real = (k - k0 < kb ? k - k0 : kb);              // elements inside k
+        // k-tiles holding data, at least 3 (covered by the zero padding)
+        int ktiles = (int)((real + 63) / 64);
+        if (ktiles < 3) ktiles = 3;
+        if (ktiles > (int)(span / 64)) ktiles = (int)(span / 64);
+        igemm_packed<2, 128, 128, 64, 64, 4, 1, true><<<grid, 256, 0, stream>>>(
+            Apk + k0, L.k_pad, a_plane, Bpk + k0, L.k_pad, b_plane, sa + 2 * q * L.m_pad,
+            sb + 2 * q * L.n_pad, 16384u * (uint32_t)real, (int32_t *)C, ldc, mi, ni, ktiles,
+            tm, tn, epi);
+        if (hipGetLastError() != hipSuccess) return IGEMM_EHIP;
+    }
+    return IGEMM_OK;
+}
+
 int launch_multiply(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
                     int64_t lda, int32_t *C, int64_t ldc, const void *a_part, const void *b_part,
                     void *stream_) {
@@ -641,18 +783,33 @@ int launch_multiply(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k
     // 16384 k constant are added by the first launch only.
     for (int64_t k0 = 0; k0 < L.k_pad; k0 += p.k_chunk) {
         const int64_t kc = L.k_pad - k0 < p.k_chunk ? L.k_pad - k0 : p.k_chunk;
-        const int ktiles = (int)(kc / 64);
+        // int16: only the k-tiles holding data (at least 3, which the zero
+        // padding covers), through the RAGGED variant when that is not a
+        // multiple of four; the padding of k to a multiple of 256 is then not
+        // multiplied (the paper's k = 290: 5 k-tiles instead of 8).
+        const int64_t real = k - k0 < kc ? k - k0 : kc;
+        int ktiles = (int)(kc / 64);
+        if (es == 2) {
+            int kr = (int)((real + 63) / 64);
+            if (kr < 3) kr = 3;
+            if (kr < ktiles) ktiles = kr;
+        }
+        const bool ragged = ktiles % 4 != 0;
         const bool first = k0 == 0;
         const uint32_t *cA = first ? corrA : nullptr;
         const uint32_t kc16 = first ? 16384u * (uint32_t)k : 0u;
-        if (es == 2)
+        if (es == 2 && ragged)
+            igemm_packed<2, 128, 128, 64, 64, 4, 0, true><<<grid, 256, 0, stream>>>(
+                Asrc + k0, lda_p, a_plane, Bpk + k0, L.k_pad, b_plane, cA, corrB, kc16, C, ldc,
+                mi, ni, ktiles, tm, tn, 0);
+        else if (es == 2)
             igemm_packed<2, 128, 128, 64, 64, 4><<<grid, 256, 0, stream>>>(
                 Asrc + k0, lda_p, a_plane, Bpk + k0, L.k_pad, b_plane, cA, corrB, kc16, C, ldc,
-                mi, ni, ktiles, tm, tn);
+                mi, ni, ktiles, tm, tn, 0);
         else
             igemm_packed<1, 256, 256, 64, 128, 4><<<grid, 512, 0, stream>>>(
                 Asrc + k0, lda_p, 0, Bpk + k0, L.k_pad, 0, nullptr, nullptr, 0u, C, ldc, mi, ni,
-                ktiles, tm, tn);
+                ktiles, tm, tn, 0);
         if (hipGetLastError() != hipSuccess) return IGEMM_EHIP;
     }
     return IGEMM_OK;

@@ -112,6 +112,31 @@ def test_packed_int8_extremes_multi_chunk(value):
     _check("i8", A, B, C, m, n, k)
 
 
+# int16 multiplies only the k-tiles of 64 that hold data: counts that are not
+# a multiple of four take the ragged tail, which ends with 3, 5 or 6 steps
+# (k = 1: the minimum of three tiles; 290 and 1300: 5 and 21 tiles, tail 5;
+# 330 and 1345: tail 6; 420: 7 tiles, one full group then a tail of 3).
+RAGGED_K = [1, 130, 290, 330, 420, 1300, 1345]
+
+
+@pytest.mark.parametrize("k", RAGGED_K)
+def test_packed_int16_ragged_k_tiles(k):
+    m, n = 200, 300
+    A, B, C = workloads.random_operands("i16", m, n, k, seed=800 + k)
+    _check("i16", A, B, C, m, n, k)
+
+
+@pytest.mark.parametrize("value", [-32768, 32767])
+def test_packed_int16_ragged_k_tiles_extremes(value):
+    """Every limb sum at its bound with a ragged tile count (k = 290)."""
+    m, n, k = 140, 130, 290
+    A = np.full((m, k), value, np.int16)
+    B = np.full((k, n), value, np.int16)
+    C = np.zeros((m, n), np.int32)
+    got = _check("i16", A, B, C, m, n, k)
+    assert np.all(got == got[0, 0])
+
+
 @pytest.mark.parametrize("dt", ["i16", "i8"])
 def test_packed_random_multi_chunk(dt):
     m, n, k = 130, 200, 33000

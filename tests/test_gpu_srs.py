@@ -242,3 +242,42 @@ def test_4096_cube_blocks_of_256_sampled_rows():
     want = C[rows].copy()
     oracle.igemm_srs(np.ascontiguousarray(A[rows]), B, want, 256, 0, False)
     assert np.array_equal(got[rows], want), _describe(got[rows], want)
+
+
+@pytest.mark.parametrize("shape", [(1100, 1030, 700), (128, 128, 256), (257, 300, 1024),
+                                   (64, 2000, 290)], ids=lambda s: "x".join(map(str, s)))
+def test_packed_kernel(shape):
+    """The packed int16 path (operands packed once, exact per-block limb sums
+    of the packed planes, one multiply per block): one block and blocks of
+    256 / 512, shifts and roundings, ragged shapes."""
+    m, n, k = shape
+    kid = _kid("i16_packed_128x128")
+    A, B, C = _operands("i16", m, n, k, seed=600 + m + n + k)
+    for kc, shift, rnd in ((0, 0, False), (256, 0, False), (512, 9, True), (k + 5, 20, True),
+                           (256, 31, False)):
+        _check(A, B, C, m, n, k, kc, shift, rnd, kernel=kid)
+
+
+def test_packed_kernel_alignment_padding_and_extremes():
+    kid = _kid("i16_packed_128x128")
+    m, n, k = 300, 260, 768
+    A, B, C = _operands("i16", m, n, k, seed=61, pad=(3, 5, 7))
+    got = _check(A, B, C, m, n, k, 256, 5, True, kernel=kid, offsets=(1, 1, 1))
+    assert np.array_equal(got[:, n:], C[:, n:])
+    # one block of 32768 all-extreme elements: sums beyond 2^44, exact
+    m, n, k = 130, 140, 32768
+    A = np.full((m, k), -32768, dtype=np.int16)
+    B = np.full((k, n), -32768, dtype=np.int16)
+    B[:, ::3] = 32767
+    A[::5, :] = 32767
+    C = np.random.default_rng(5).integers(-32768, 32767, size=(m, n), dtype=np.int16,
+                                          endpoint=True)
+    for shift in (0, 40, 45):
+        _check(A, B, C, m, n, k, 0, shift, shift == 45, kernel=kid)
+
+
+def test_packed_kernel_refuses_unaligned_blocks():
+    kid = _kid("i16_packed_128x128")
+    A, B, C = _operands("i16", 200, 200, 700, seed=3)
+    st, got = _gpu(A, B, C, 200, 200, 700, 100, 0, False, kernel=kid, check=False)
+    assert st == _ig().IGEMM_EINVAL and np.array_equal(got, C)
