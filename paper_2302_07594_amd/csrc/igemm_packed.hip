@@ -749,14 +749,22 @@ int launch_srs_packed(const igemm_plan &p, int64_t m, int64_t n, int64_t k, int6
         const int64_t k0 = q * kb;
         const int64_t span = L.k_pad - k0 < kb ? L.k_pad - k0 : kb;   // a multiple of 256
         const int64_t real = (k - k0 < kb ? k - k0 : kb);              // elements inside k
-        // k-tiles holding data, at least 3 (covered by the zero padding)
+        // k-tiles holding data, at least 3 (covered by the zero padding);
+        // a multiple of four takes the variant with the tail fixed at build
+        // time
         int ktiles = (int)((real + 63) / 64);
         if (ktiles < 3) ktiles = 3;
         if (ktiles > (int)(span / 64)) ktiles = (int)(span / 64);
-        igemm_packed<2, 128, 128, 64, 64, 4, 1, true><<<grid, 256, 0, stream>>>(
-            Apk + k0, L.k_pad, a_plane, Bpk + k0, L.k_pad, b_plane, sa + 2 * q * L.m_pad,
-            sb + 2 * q * L.n_pad, 16384u * (uint32_t)real, (int32_t *)C, ldc, mi, ni, ktiles,
-            tm, tn, epi);
+        if (ktiles % 4 == 0)
+            igemm_packed<2, 128, 128, 64, 64, 4, 1><<<grid, 256, 0, stream>>>(
+                Apk + k0, L.k_pad, a_plane, Bpk + k0, L.k_pad, b_plane, sa + 2 * q * L.m_pad,
+                sb + 2 * q * L.n_pad, 16384u * (uint32_t)real, (int32_t *)C, ldc, mi, ni, ktiles,
+                tm, tn, epi);
+        else
+            igemm_packed<2, 128, 128, 64, 64, 4, 1, true><<<grid, 256, 0, stream>>>(
+                Apk + k0, L.k_pad, a_plane, Bpk + k0, L.k_pad, b_plane, sa + 2 * q * L.m_pad,
+                sb + 2 * q * L.n_pad, 16384u * (uint32_t)real, (int32_t *)C, ldc, mi, ni, ktiles,
+                tm, tn, epi);
         if (hipGetLastError() != hipSuccess) return IGEMM_EHIP;
     }
     return IGEMM_OK;
@@ -783,18 +791,17 @@ int launch_multiply(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k
     // 16384 k constant are added by the first launch only.
     for (int64_t k0 = 0; k0 < L.k_pad; k0 += p.k_chunk) {
         const int64_t kc = L.k_pad - k0 < p.k_chunk ? L.k_pad - k0 : p.k_chunk;
-        // int16: only the k-tiles holding data (at least 3, which the zero
-        // padding covers), through the RAGGED variant when that is not a
-        // multiple of four; the padding of k to a multiple of 256 is then not
-        // multiplied (the paper's k = 290: 5 k-tiles instead of 8).
+        // int16: when the zero padding of k to a multiple of 256 spans three
+        // k-tiles of 64, only the tiles holding data are multiplied, through
+        // the RAGGED variant (the paper's k = 290: 5 k-tiles instead of 8).
+        // Saving one or two tiles does not pay: on m = n = 4096 the RAGGED
+        // kernel took 48.9 us for 3 tiles against 46.0 for 4, and 61.3 us
+        // for 7 against 56.6 for 8 (54.0 us for 5).
         const int64_t real = k - k0 < kc ? k - k0 : kc;
         int ktiles = (int)(kc / 64);
-        if (es == 2) {
-            int kr = (int)((real + 63) / 64);
-            if (kr < 3) kr = 3;
-            if (kr < ktiles) ktiles = kr;
-        }
-        const bool ragged = ktiles % 4 != 0;
+        const int kr = (int)((real + 63) / 64);
+        const bool ragged = es == 2 && kr % 4 == 1 && kr > 4 && kr < ktiles;
+        if (ragged) ktiles = kr;
         const bool first = k0 == 0;
         const uint32_t *cA = first ? corrA : nullptr;
         const uint32_t kc16 = first ? 16384u * (uint32_t)k : 0u;

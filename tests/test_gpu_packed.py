@@ -112,10 +112,10 @@ def test_packed_int8_extremes_multi_chunk(value):
     _check("i8", A, B, C, m, n, k)
 
 
-# int16 multiplies only the k-tiles of 64 that hold data: counts that are not
-# a multiple of four take the ragged tail, which ends with 3, 5 or 6 steps
-# (k = 1: the minimum of three tiles; 290 and 1300: 5 and 21 tiles, tail 5;
-# 330 and 1345: tail 6; 420: 7 tiles, one full group then a tail of 3).
+# k counts whose k-tiles of 64 are not a multiple of four. int16 multiplies
+# only the tiles that hold data when the padding spans three of them (290 and
+# 1300: 5 and 21 tiles, through the tail chosen at run time); the others (k =
+# 1, 130, 330, 420, 1345) multiply the zero padding up to a multiple of four.
 RAGGED_K = [1, 130, 290, 330, 420, 1300, 1345]
 
 

@@ -245,11 +245,14 @@ def test_4096_cube_blocks_of_256_sampled_rows():
 
 
 @pytest.mark.parametrize("shape", [(1100, 1030, 700), (128, 128, 256), (257, 300, 1024),
-                                   (64, 2000, 290)], ids=lambda s: "x".join(map(str, s)))
+                                   (64, 2000, 290), (200, 150, 350)],
+                         ids=lambda s: "x".join(map(str, s)))
 def test_packed_kernel(shape):
     """The packed int16 path (operands packed once, exact per-block limb sums
     of the packed planes, one multiply per block): one block and blocks of
-    256 / 512, shifts and roundings, ragged shapes."""
+    256 / 512, shifts and roundings, ragged shapes. Blocks of 3, 5, 6 and 11
+    k-tiles of 64 take the tail chosen at run time, those of 4, 8 and 16 the
+    one fixed at build time."""
     m, n, k = shape
     kid = _kid("i16_packed_128x128")
     A, B, C = _operands("i16", m, n, k, seed=600 + m + n + k)
