@@ -217,10 +217,13 @@ def bench_case(case, min_sets=1, per_graph=40, warmup=3):
 
 
 def bench_srs_case(case, kc, shift, per_graph=40, warmup=3):
-    """Time the int16-output update (one fused launch per k block of kc,
-    shift-round-saturate conversion, int16 C) on a workload's A and B with a
-    random int16 C, like bench_case; the algorithmic bytes are A and B once
-    and the int16 C read and written once per block."""
+    """Time the int16-output update (shift-round-saturate conversion per k
+    block of kc, int16 C) on a workload's A and B with a random int16 C, like
+    bench_case: gemm_srs as a caller gets it, i.e. the packed path (operands
+    packed into a workspace from torch's allocator, one multiply per block)
+    where the library chooses it, else one fused launch per block. The
+    algorithmic bytes are A and B once and the int16 C read and written once
+    per block."""
     import numpy as np
     import torch
 
@@ -245,6 +248,8 @@ def bench_srs_case(case, kc, shift, per_graph=40, warmup=3):
     t = time_graph(g, per_graph)
     m, n, k = case.m, case.n, case.k
     nblocks = 1 if (kc == 0 or kc >= k) else -(-k // kc)
+    ws_bytes = ig.igemm_srs_query(2 if case.dtype == "i16" else 1, m, n, k, Ad0, k, Bd0, n, Cd0,
+                                  n, kc, torch.cuda.get_device_properties(0).multi_processor_count)
     ops = 2.0 * m * n * k
     nbytes = A.nbytes + B.nbytes + 4.0 * m * n * nblocks
     peak_ops = PEAK_I16_TOPS * 1e12
@@ -256,6 +261,7 @@ def bench_srs_case(case, kc, shift, per_graph=40, warmup=3):
         "name": f"{case.name}_srs_kc{kc}_shift{shift}", "dtype": case.dtype,
         "m": m, "n": n, "k": k, "kc": kc, "shift": shift, "blocks": nblocks,
         "epilogue": "int16 C += sat16(floor(block product / 2^shift)) modulo 2^16",
+        "path": "packed" if ws_bytes > 0 else "fused", "workspace_bytes": ws_bytes,
         "us": round(t * 1e6, 2), "TOPS": round(ops / t / 1e12, 2),
         "bound": bound, "achieved": round(ach, 1), "peak": peak, "unit": unit,
         "frac": round(ach / peak, 4), "buffer_sets": nsets, "timing": TIMING,

@@ -378,6 +378,35 @@ int igemm_srs_ex(int elem_bytes, int64_t m, int64_t n, int64_t k, const void *A,
                  const void *B, int64_t ldb, int16_t *C, int64_t ldc, int64_t kc, int shift,
                  int round_half_up, void *stream, int kernel);
 
+/*
+ * The int16-output update with a caller-owned workspace, for callers that
+ * capture the call into a graph or manage device memory themselves (the same
+ * operation as igemm_srs_ex, same arguments and errors):
+ *   igemm_srs_query  host only (no HIP call): *workspace_bytes = the bytes
+ *                    igemm_srs_ws needs for these arguments on a device with
+ *                    num_cu compute units (the current device's count, as
+ *                    hipDeviceAttributeMultiprocessorCount reports it), 0 when
+ *                    the call takes a fused kernel (int8 operands, small
+ *                    products, or blocks that are not one block or multiples
+ *                    of 256). C and the pointers are only checked, never read.
+ *   igemm_srs_ws     workspace: device memory, 256-byte aligned
+ *                    (IGEMM_EINVAL otherwise), holding the packed operands
+ *                    and the per-block limb sums; at least the queried bytes
+ *                    when the packed path is taken (IGEMM_ENOMEM otherwise;
+ *                    nothing is enqueued). With a workspace the packed path
+ *                    is also taken while `stream` is being captured; with
+ *                    workspace NULL the call is igemm_srs_ex. The workspace
+ *                    must stay untouched until the call's kernels have run;
+ *                    calls that share one workspace must be ordered.
+ */
+int igemm_srs_query(int elem_bytes, int64_t m, int64_t n, int64_t k, const void *A,
+                    int64_t lda, const void *B, int64_t ldb, const void *C, int64_t ldc,
+                    int64_t kc, int num_cu, int kernel, int64_t *workspace_bytes);
+int igemm_srs_ws(int elem_bytes, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
+                 const void *B, int64_t ldb, int16_t *C, int64_t ldc, int64_t kc, int shift,
+                 int round_half_up, void *stream, int kernel, void *workspace,
+                 int64_t workspace_bytes);
+
 /* Release the memory the library's workspace pool for the current device
  * holds beyond what in-flight calls use (hipMemPoolTrimTo). Returns
  * IGEMM_OK, or IGEMM_EHIP. */

@@ -32,6 +32,10 @@ Same names as the C ABI:
     igemm_i16_srs / igemm_i8_srs(m, n, k, A, lda, B, ldb, C, ldc, kc=0, shift=0,
                                  round_half_up=0, stream=None)
     igemm_srs_ex(elem_bytes, ..., stream=None, kernel=-1)
+    igemm_srs_query(elem_bytes, m, n, k, A, lda, B, ldb, C, ldc, kc=0, num_cu=0,
+                    kernel=-1) -> workspace bytes
+    igemm_srs_ws(elem_bytes, ..., stream=None, kernel=-1, workspace=None,
+                 workspace_bytes=0)
     igemm_strerror(status), igemm_kernel_name(i), igemm_num_kernels(),
     igemm_version()
 A, B, C may be integer device addresses or torch tensors (their data_ptr()).
@@ -139,6 +143,12 @@ def _load():
     lib.igemm_srs_ex.argtypes = [ci, i64, i64, i64, vp, i64, vp, i64, vp, i64, i64, ci, ci, vp,
                                  ci]
     lib.igemm_srs_ex.restype = ci
+    lib.igemm_srs_query.argtypes = [ci, i64, i64, i64, vp, i64, vp, i64, vp, i64, i64, ci, ci,
+                                    ctypes.POINTER(i64)]
+    lib.igemm_srs_query.restype = ci
+    lib.igemm_srs_ws.argtypes = [ci, i64, i64, i64, vp, i64, vp, i64, vp, i64, i64, ci, ci, vp,
+                                 ci, vp, i64]
+    lib.igemm_srs_ws.restype = ci
     lib.igemm_conv2d_out_dim.argtypes = [i64] * 5
     lib.igemm_conv2d_out_dim.restype = i64
     lib.igemm_trim_workspace.argtypes = []
@@ -581,12 +591,37 @@ def igemm_srs_ex(elem_bytes, m, n, k, A, lda, B, ldb, C, ldc, kc=0, shift=0, rou
                                  _stream(stream), int(kernel)))
 
 
-def gemm_srs(A, B, C, kc=0, shift=0, round_half_up=False, stream=None, kernel=-1):
+def igemm_srs_query(elem_bytes, m, n, k, A, lda, B, ldb, C, ldc, kc=0, num_cu=0,
+                    kernel=-1) -> int:
+    """Workspace bytes igemm_srs_ws needs for these arguments (0: fused
+    path). Host only. Raises IgemmError for invalid arguments."""
+    out = ctypes.c_int64(0)
+    st = int(_lib.igemm_srs_query(int(elem_bytes), m, n, k, _addr(A), lda, _addr(B), ldb,
+                                  _addr(C), ldc, kc, int(num_cu), int(kernel), ctypes.byref(out)))
+    if st != IGEMM_OK:
+        raise IgemmError(st, "igemm_srs_query")
+    return int(out.value)
+
+
+def igemm_srs_ws(elem_bytes, m, n, k, A, lda, B, ldb, C, ldc, kc=0, shift=0, round_half_up=0,
+                 stream=None, kernel=-1, workspace=None, workspace_bytes=0) -> int:
+    return int(_lib.igemm_srs_ws(int(elem_bytes), m, n, k, _addr(A), lda, _addr(B), ldb,
+                                 _addr(C), ldc, kc, int(shift), int(round_half_up),
+                                 _stream(stream), int(kernel),
+                                 _addr(workspace) if workspace is not None else None,
+                                 int(workspace_bytes)))
+
+
+def gemm_srs(A, B, C, kc=0, shift=0, round_half_up=False, stream=None, kernel=-1,
+             workspace=None):
     """int16 C += srs(A B) for 2-D CUDA tensors: A (m x k) and B (k x n) both
     torch.int16 or both torch.int8, C (m x n) torch.int16, rows with unit
     stride. Per block of kc k indices (0: all of k) the exact product is
     shifted right by `shift` (floor, or round-half-up), saturated to int16
-    and added to C modulo 2^16. Returns C."""
+    and added to C modulo 2^16. `workspace` as for gemm_i16: None or 'torch'
+    (a workspace from torch's allocator when the packed path is taken, so the
+    call may be captured into a graph), 'library' (the library's pool, not
+    under capture) or a uint8 tensor. Returns C."""
     import torch
     if A.dtype not in (torch.int16, torch.int8) or B.dtype != A.dtype:
         raise TypeError("gemm_srs: A and B must both be torch.int16 or both torch.int8")
@@ -596,8 +631,21 @@ def gemm_srs(A, B, C, kc=0, shift=0, round_half_up=False, stream=None, kernel=-1
     stand_in = torch.empty_strided(C.shape, C.stride(), dtype=torch.int32, device=C.device)
     m, n, k, lda, ldb, ldc = _check_tensors(A, B, stand_in, A.dtype, "gemm_srs")
     es = 2 if A.dtype == torch.int16 else 1
-    st = igemm_srs_ex(es, m, n, k, A, lda, B, ldb, C, ldc, kc, shift,
-                      1 if round_half_up else 0, stream, kernel)
+    ws, ws_bytes = None, 0
+    if workspace is None or workspace == "torch":
+        if m and n and k:
+            ws_bytes = igemm_srs_query(es, m, n, k, A, lda, B, ldb, C, ldc, kc,
+                                       _num_cu(C.device), kernel)
+            if ws_bytes > 0:
+                ws = _aligned_workspace(ws_bytes, C.device, stream)
+    elif workspace == "library":
+        pass
+    elif hasattr(workspace, "data_ptr"):
+        ws, ws_bytes = workspace, workspace.numel() * workspace.element_size()
+    else:
+        raise ValueError("gemm_srs: workspace must be None, 'torch', 'library' or a tensor")
+    st = igemm_srs_ws(es, m, n, k, A, lda, B, ldb, C, ldc, kc, shift,
+                      1 if round_half_up else 0, stream, kernel, ws, ws_bytes)
     if st != IGEMM_OK:
         raise IgemmError(st, "gemm_srs")
     return C

@@ -240,38 +240,67 @@ int run_conv(int es, const igemm_conv2d_desc *d, const void *X, const void *W, i
                        stream);
 }
 
-// int16-output update: one launch per k block of kc elements, in order. All
+// int16-output update: the packed path for large int16 products whose blocks
+// fall on the packed k-tiles (one block, or blocks of a multiple of 256, at
+// most 64), else one fused launch per k block of kc elements, in order. All
 // blocks are planned before the first launch, so an error enqueues nothing.
-int run_srs(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, const void *B,
-            int64_t ldb, int16_t *C, int64_t ldc, int64_t kc, int shift, int round_half_up,
-            void *stream, int kernel) {
+int srs_check(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, const void *B,
+              int64_t ldb, const void *C, int64_t ldc, int64_t kc, int shift, int round_half_up,
+              int kernel) {
     int st = validate(es, m, n, k, A, lda, B, ldb, C, ldc);
     if (st != IGEMM_OK) return st;
     if (kc < 0 || shift < 0 || shift > 47 || (round_half_up != 0 && round_half_up != 1) ||
         kernel < -1 || kernel >= K_COUNT)
         return IGEMM_EINVAL;
-    if (m == 0 || n == 0 || k == 0) return IGEMM_OK;
-    const int64_t blk = (kc == 0 || kc > k) ? k : kc;
-    const int64_t nblocks = (k + blk - 1) / blk;
+    return IGEMM_OK;
+}
+bool srs_packed_ok(int es, int64_t k, int64_t kc, int64_t *blk, int64_t *nblocks) {
+    *blk = (kc == 0 || kc > k) ? k : kc;
+    *nblocks = (k + *blk - 1) / *blk;
+    return es == 2 && *nblocks <= 64 && (*nblocks == 1 || *blk % 256 == 0);
+}
+// Plans the packed path (pp->packed false when the fused path is taken) and
+// returns the workspace it needs in *need.
+int srs_packed_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
+                    const void *B, int64_t ldb, int64_t ldc, int64_t kc, int num_cu, int kernel,
+                    bool can_pack, igemm_plan *pp, int64_t *need) {
+    *need = 0;
+    pp->packed = 0;
+    int64_t blk, nblocks;
+    const bool packed_ok = srs_packed_ok(es, k, kc, &blk, &nblocks);
+    if (kernel == K_I16_PACKED_128x128 && (!packed_ok || !can_pack)) return IGEMM_EINVAL;
     if (blk > kMaxKChunk) return IGEMM_ENOTSUP;
-    // Large int16 products whose blocks fall on the packed k-tiles (one
-    // block, or blocks of a multiple of 256): pack once into a workspace
-    // from the pool, then one multiply launch per block. Not under stream
-    // capture (no pool).
-    const bool packed_ok = es == 2 && nblocks <= 64 && (nblocks == 1 || blk % 256 == 0);
+    if (kernel != K_I16_PACKED_128x128 && !(kernel < 0 && packed_ok)) return IGEMM_OK;
+    const int st = make_plan(es, m, n, k, A, lda, B, ldb, ldc, num_cu, kernel < 0 ? -1 : kernel,
+                             -1, can_pack, pp);
+    if (st != IGEMM_OK) return st;
+    if (pp->packed) *need = pp->workspace_bytes + srs_sums_bytes(*pp, m, n, k, nblocks, A, lda);
+    return IGEMM_OK;
+}
+int run_srs(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, const void *B,
+            int64_t ldb, int16_t *C, int64_t ldc, int64_t kc, int shift, int round_half_up,
+            void *stream, int kernel, void *workspace = nullptr, int64_t workspace_bytes = 0) {
+    int st = srs_check(es, m, n, k, A, lda, B, ldb, C, ldc, kc, shift, round_half_up, kernel);
+    if (st != IGEMM_OK) return st;
+    if (workspace != nullptr && ((uintptr_t)workspace % 256 != 0 || workspace_bytes < 0))
+        return IGEMM_EINVAL;
+    if (m == 0 || n == 0 || k == 0) return IGEMM_OK;
+    int64_t blk, nblocks;
+    const bool packed_ok = srs_packed_ok(es, k, kc, &blk, &nblocks);
+    if (blk > kMaxKChunk) return IGEMM_ENOTSUP;
     if (kernel == K_I16_PACKED_128x128 && !packed_ok) return IGEMM_EINVAL;
     if (kernel == K_I16_PACKED_128x128 || (kernel < 0 && packed_ok)) {
+        // The pool is not used under stream capture; a caller's workspace is.
         hipStream_t s = (hipStream_t)stream;
-        const bool capturing = stream_is_capturing(s);
-        if (kernel >= 0 && capturing) return IGEMM_EINVAL;
+        const bool can_pack = workspace != nullptr || !stream_is_capturing(s);
         igemm_plan pp;
-        st = make_plan(es, m, n, k, A, lda, B, ldb, ldc, num_cu_of_current_device(),
-                       kernel < 0 ? -1 : kernel, -1, !capturing, &pp);
+        int64_t need = 0;
+        st = srs_packed_plan(es, m, n, k, A, lda, B, ldb, ldc, kc, num_cu_of_current_device(),
+                             kernel, can_pack, &pp, &need);
         if (st != IGEMM_OK) return st;
         if (pp.packed) {
-            const int64_t sums = srs_sums_bytes(pp, m, n, k, nblocks, A, lda);
             Scratch sc;
-            st = get_scratch(nullptr, 0, pp.workspace_bytes + sums, s, &sc);
+            st = get_scratch(workspace, workspace_bytes, need, s, &sc);
             if (st != IGEMM_OK) return st;
             st = pack_both(es, pp, m, n, k, A, lda, B, ldb, sc.ptr, stream);
             if (st == IGEMM_OK)
@@ -327,6 +356,29 @@ int igemm_srs_ex(int elem_bytes, int64_t m, int64_t n, int64_t k, const void *A,
     if (elem_bytes != 1 && elem_bytes != 2) return IGEMM_EINVAL;
     return igemm::run_srs(elem_bytes, m, n, k, A, lda, B, ldb, C, ldc, kc, shift, round_half_up,
                           stream, kernel);
+}
+
+int igemm_srs_query(int elem_bytes, int64_t m, int64_t n, int64_t k, const void *A,
+                    int64_t lda, const void *B, int64_t ldb, const void *C, int64_t ldc,
+                    int64_t kc, int num_cu, int kernel, int64_t *workspace_bytes) {
+    if (workspace_bytes == nullptr || (elem_bytes != 1 && elem_bytes != 2) || num_cu < 0)
+        return IGEMM_EINVAL;
+    *workspace_bytes = 0;
+    int st = igemm::srs_check(elem_bytes, m, n, k, A, lda, B, ldb, C, ldc, kc, 0, 0, kernel);
+    if (st != IGEMM_OK) return st;
+    if (m == 0 || n == 0 || k == 0) return IGEMM_OK;
+    igemm_plan pp;
+    return igemm::srs_packed_plan(elem_bytes, m, n, k, A, lda, B, ldb, ldc, kc, num_cu, kernel,
+                                  true, &pp, workspace_bytes);
+}
+
+int igemm_srs_ws(int elem_bytes, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
+                 const void *B, int64_t ldb, int16_t *C, int64_t ldc, int64_t kc, int shift,
+                 int round_half_up, void *stream, int kernel, void *workspace,
+                 int64_t workspace_bytes) {
+    if (elem_bytes != 1 && elem_bytes != 2) return IGEMM_EINVAL;
+    return igemm::run_srs(elem_bytes, m, n, k, A, lda, B, ldb, C, ldc, kc, shift, round_half_up,
+                          stream, kernel, workspace, workspace_bytes);
 }
 
 int igemm_conv2d_i16(const igemm_conv2d_desc *desc, const int16_t *X, const int16_t *W,

@@ -414,8 +414,45 @@ def test_conv_null_descriptor():
 
 def test_srs_header_declares_entry_points():
     fns = declared_functions()
-    for name in ("igemm_i16_srs", "igemm_i8_srs", "igemm_srs_ex"):
+    for name in ("igemm_i16_srs", "igemm_i8_srs", "igemm_srs_ex", "igemm_srs_query",
+                 "igemm_srs_ws"):
         assert name in fns
+
+
+def test_srs_query_is_host_only_and_consistent():
+    """The workspace query needs no device: the packed path's bytes are the
+    packed operands' workspace plus two words per padded row and column and
+    block; fused choices need none; invalid arguments raise."""
+    P = 1 << 20
+    m = n = 4096
+    for k, kc, nblocks in ((290, 0, 1), (290, 290, 1), (4096, 256, 16), (1024, 512, 2)):
+        plan = ig.igemm_query_plan(2, m, n, k, P, k, P, n, P, n, 256)
+        need = ig.igemm_srs_query(2, m, n, k, P, k, P, n, P, n, kc, 256)
+        assert ig.igemm_kernel_name(plan["kernel"]) == "i16_packed_128x128"
+        assert need == plan["workspace_bytes"] + 8 * nblocks * (m + n), (k, kc)
+    # fused choices: int8 operands, a small product, blocks of 100, over 64 blocks
+    assert ig.igemm_srs_query(1, m, n, 4096, P, 4096, P, n, P, n, 256, 256) == 0
+    assert ig.igemm_srs_query(2, 256, 256, 256, P, 256, P, 256, P, 256, 0, 256) == 0
+    assert ig.igemm_srs_query(2, m, n, 1000, P, 1000, P, n, P, n, 100, 256) == 0
+    assert ig.igemm_srs_query(2, m, n, 20000, P, 20000, P, n, P, n, 256, 256) == 0
+    assert ig.igemm_srs_query(2, 0, n, 290, P, 290, P, n, P, n, 0, 256) == 0
+    with pytest.raises(ig.IgemmError):
+        ig.igemm_srs_query(2, m, n, 290, P, 290, P, n, P, n, -1, 256)
+    with pytest.raises(ig.IgemmError):
+        ig.igemm_srs_query(3, m, n, 290, P, 290, P, n, P, n, 0, 256)
+    kid = [i for i in ig.kernels_for(2) if ig.igemm_kernel_name(i) == "i16_packed_128x128"][0]
+    with pytest.raises(ig.IgemmError):   # explicit packed kernel, blocks of 100
+        ig.igemm_srs_query(2, m, n, 1000, P, 1000, P, n, P, n, 100, 256, kid)
+    assert ig.igemm_srs_query(2, 64, 64, 290, P, 290, P, 64, P, 64, 0, 256, kid) > 0
+
+
+def test_srs_ws_rejects_bad_workspace_before_any_hip_call():
+    E = ig.IGEMM_EINVAL
+    a, b, c = FAKE_A, FAKE_B, FAKE_C
+    assert ig.igemm_srs_ws(2, 4, 4, 4, a, 4, b, 4, c, 4, 0, 0, 0, 0, -1, 0x1010, 1 << 20) == E
+    assert ig.igemm_srs_ws(2, 4, 4, 4, a, 4, b, 4, c, 4, 0, 0, 0, 0, -1, 0x100000, -1) == E
+    assert ig.igemm_srs_ws(2, 4, 4, 4, a, 4, b, 4, c, 4, -1, 0, 0, 0, -1, None, 0) == E
+    assert ig.igemm_srs_ws(3, 4, 4, 4, a, 4, b, 4, c, 4, 0, 0, 0, 0, -1, None, 0) == E
 
 
 @pytest.mark.parametrize("fn", [ig.igemm_i16_srs, ig.igemm_i8_srs])

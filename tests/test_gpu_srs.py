@@ -284,3 +284,109 @@ def test_packed_kernel_refuses_unaligned_blocks():
     A, B, C = _operands("i16", 200, 200, 700, seed=3)
     st, got = _gpu(A, B, C, 200, 200, 700, 100, 0, False, kernel=kid, check=False)
     assert st == _ig().IGEMM_EINVAL and np.array_equal(got, C)
+
+
+# ---- caller-owned workspace (igemm_srs_ws / igemm_srs_query) ------------------
+
+def _ws_tensor(nbytes, fill=0x5A):
+    import torch
+    raw = torch.full((nbytes + 512,), fill, dtype=torch.uint8, device="cuda")
+    off = (-raw.data_ptr()) % 256
+    return raw, raw[off:off + nbytes]
+
+
+def _srs_ws(A, B, C, m, n, k, kc, shift, rnd, ws, ws_bytes, kernel=-1, ws_ptr=None):
+    import torch
+    ig = _ig()
+    es = 2 if A.dtype == np.int16 else 1
+    Ad, Bd, Cd = (torch.from_numpy(np.ascontiguousarray(x)).cuda() for x in (A, B, C))
+    ptr = ws_ptr if ws_ptr is not None else (ws.data_ptr() if ws is not None else None)
+    st = ig.igemm_srs_ws(es, m, n, k, Ad.data_ptr(), A.shape[1], Bd.data_ptr(), B.shape[1],
+                         Cd.data_ptr(), C.shape[1], kc, shift, 1 if rnd else 0,
+                         torch.cuda.current_stream().cuda_stream, kernel, ptr, ws_bytes)
+    torch.cuda.synchronize()
+    return st, Cd.cpu().numpy()
+
+
+def _num_cu():
+    import torch
+    return torch.cuda.get_device_properties(0).multi_processor_count
+
+
+@pytest.mark.parametrize("shape,kc", [((1100, 1030, 700), 256), ((1100, 1030, 700), 0),
+                                      ((64, 2000, 290), 0), ((2048, 1024, 1024), 512)],
+                         ids=["1100x1030x700-kc256", "1100x1030x700-kc0", "64x2000x290-kc0",
+                              "2048x1024x1024-kc512"])
+def test_ws_packed_path_matches_oracle(shape, kc):
+    """A caller's workspace (stale contents) holds the packed operands and the
+    limb sums; the result is the oracle's, bit for bit."""
+    ig = _ig()
+    m, n, k = shape
+    A, B, C = _operands("i16", m, n, k, seed=900 + m + k + kc)
+    kid = _kid("i16_packed_128x128")
+    need = ig.igemm_srs_query(2, m, n, k, 1 << 20, k, 1 << 20, n, 1 << 20, n, kc, _num_cu(), kid)
+    assert need > 0
+    _, ws = _ws_tensor(need)
+    want = _oracle(A, B, C, m, n, k, kc, 7, True)
+    st, got = _srs_ws(A, B, C, m, n, k, kc, 7, True, ws, need, kernel=kid)
+    assert st == 0 and np.array_equal(got, want), _describe(got, want)
+
+
+def test_ws_auto_choice_and_errors():
+    """Automatic choice with the queried workspace; too small a workspace is
+    ENOMEM and a misaligned one EINVAL, both with C unchanged; a fused choice
+    needs no workspace."""
+    ig = _ig()
+    m, n, k, kc = 4096, 1024, 512, 256
+    A, B, C = _operands("i16", m, n, k, seed=91)
+    need = ig.igemm_srs_query(2, m, n, k, 1 << 20, k, 1 << 20, n, 1 << 20, n, kc, _num_cu())
+    assert need > 0
+    raw, ws = _ws_tensor(need)
+    want = _oracle(A, B, C, m, n, k, kc, 0, False)
+    st, got = _srs_ws(A, B, C, m, n, k, kc, 0, False, ws, need)
+    assert st == 0 and np.array_equal(got, want), _describe(got, want)
+    st, got = _srs_ws(A, B, C, m, n, k, kc, 0, False, ws, need - 1)
+    assert st == ig.IGEMM_ENOMEM and np.array_equal(got, C)
+    st, got = _srs_ws(A, B, C, m, n, k, kc, 0, False, None, need, ws_ptr=ws.data_ptr() + 16)
+    assert st == ig.IGEMM_EINVAL and np.array_equal(got, C)
+    # int8 operands, and blocks of 100: fused, no workspace needed or touched
+    for dt, kc2 in (("i8", 256), ("i16", 100)):
+        A2, B2, C2 = _operands(dt, 300, 200, 700, seed=92)
+        es = 2 if dt == "i16" else 1
+        assert ig.igemm_srs_query(es, 300, 200, 700, 1 << 20, 700, 1 << 20, 200, 1 << 20, 200,
+                                  kc2, _num_cu()) == 0
+        want = _oracle(A2, B2, C2, 300, 200, 700, kc2, 3, False)
+        st, got = _srs_ws(A2, B2, C2, 300, 200, 700, kc2, 3, False, None, 0)
+        assert st == 0 and np.array_equal(got, want), _describe(got, want)
+
+
+def test_ws_packed_path_in_graph():
+    """gemm_srs with its default workspace (torch's allocator) captured into
+    a graph on a shape that takes the packed path: every replay, with eager
+    work between them, gives the oracle's result."""
+    import torch
+    ig = _ig()
+    m, n, k, kc, shift = 4096, 1024, 768, 256, 4
+    assert ig.igemm_srs_query(2, m, n, k, 1 << 20, k, 1 << 20, n, 1 << 20, n, kc, _num_cu()) > 0
+    A, B, C = _operands("i16", m, n, k, seed=93)
+    want = _oracle(A, B, C, m, n, k, kc, shift, False)
+    Ad, Bd, C0 = (torch.from_numpy(x).cuda() for x in (A, B, C))
+    Cd = C0.clone()
+    ig.gemm_srs(Ad, Bd, Cd, kc=kc, shift=shift)
+    torch.cuda.synchronize()
+    assert np.array_equal(Cd.cpu().numpy(), want)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        Cd.copy_(C0)
+        ig.gemm_srs(Ad, Bd, Cd, kc=kc, shift=shift)
+    for rep in range(3):
+        Cd.fill_(rep + 1)
+        g.replay()
+        filler = torch.ones(1 << 16, device="cuda", dtype=torch.int32) * rep  # eager work
+        torch.cuda.synchronize()
+        got = Cd.cpu().numpy()
+        assert np.array_equal(got, want), f"replay {rep}: " + _describe(got, want)
+        del filler
