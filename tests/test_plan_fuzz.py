@@ -92,3 +92,37 @@ def test_srs_status_only_without_device(fn):
         st = fn(max(m, 1), max(n, 1), k, 0x10000, k, 0x20000, max(n, 1), 0x30000, max(n, 1),
                 kc, shift, 0, 0)
         assert st in (ig.IGEMM_EINVAL, ig.IGEMM_ENOTSUP)
+
+
+@pytest.mark.parametrize("seed", range(2))
+def test_srs_query_invariants(seed):
+    """The int16-output workspace query: a status for any arguments; when it
+    accepts them, the bytes are those of the packed plan of the same product
+    plus two words per padded row and column and block, or 0 (fused path),
+    and never more than 0 for int8 operands or for blocks the packed path
+    cannot take."""
+    rng = np.random.default_rng(100 + seed)
+    nk = ig.igemm_num_kernels()
+    for _ in range(1500):
+        es = int(rng.choice([1, 2]))
+        m, n, k = (_pick(rng, BIG) for _ in range(3))
+        kc = int(rng.choice([0, 0, 1, 100, 256, 512, 290, 32768, 32769, -1, k + 3]))
+        kernel = int(rng.integers(-1, nk))
+        num_cu = int(rng.choice([0, 1, 80, 256, 304]))
+        try:
+            need = ig.igemm_srs_query(es, m, n, k, 0x10000, max(k, 1), 0x10000, max(n, 1),
+                                      0x10000, max(n, 1), kc, num_cu, kernel)
+        except ig.IgemmError as e:
+            assert e.status in (ig.IGEMM_EINVAL, ig.IGEMM_ENOTSUP)
+            continue
+        assert need >= 0
+        if need == 0:
+            continue
+        blk = k if kc == 0 or kc > k else kc
+        nblocks = -(-k // blk)
+        assert es == 2 and nblocks <= 64 and (nblocks == 1 or blk % 256 == 0)
+        p = ig.igemm_query_plan(es, m, n, k, 0x10000, max(k, 1), 0x10000, max(n, 1), 0x10000,
+                                max(n, 1), num_cu, kernel if kernel >= 0 else -1)
+        assert p["packed"]
+        m_pad, n_pad = -(-m // 128) * 128, -(-n // 128) * 128
+        assert need == p["workspace_bytes"] + 8 * nblocks * (m_pad + n_pad)
