@@ -209,6 +209,10 @@ static int auto_kernel(int es, int64_t m, int64_t n, int64_t k, const void *A, i
     // finish sooner (measured: 256x256x256 3.9 us against 5.6 us with 64x64
     // tiles; 784x128x1152 and 196x256x2304 13% and 9% faster).
     if (tiles_of(K_I16_64x64, m, n) < 32) return m <= 64 ? K_I16_32x128 : K_I16_16x128;
+    // A single k-tile cannot be sliced, so when the 64x64 tiles leave compute
+    // units idle only smaller tiles add workgroups: (3136, 256, 64) with
+    // 16x128 tiles 5.6 us against 6.1 us.
+    if (k <= kBK && tiles_of(K_I16_64x64, m, n) < num_cu) return K_I16_16x128;
     return K_I16_64x64;
 }
 
@@ -293,9 +297,12 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
         // k-tiles per slice so each slice still pipelines its loads (the
         // 16- and 32-row int16 tiles take short ranges in one pass, where a
         // single k-tile per slice measured fastest on small cubes).
+        // (The cap rounds up: with nine k-tiles, five slices of at most two
+        // rather than three slices of three; (3136, 64, 576) on 64x64 tiles
+        // 7.0 against 7.6 us, (12544, 64, 147) 8.3 against 8.5 us.)
         s = cdiv(2 * (int64_t)num_cu, tiles);
         const bool one_tile = id == K_I16_16x128 || id == K_I16_32x128;
-        int64_t cap = one_tile ? ktiles : (ktiles / 2 > 1 ? ktiles / 2 : 1);
+        const int64_t cap = one_tile ? ktiles : cdiv(ktiles, 2);
         if (s > cap) s = cap;
     }
     // Small-tile kernels take a k range of at most four k-tiles in one go
