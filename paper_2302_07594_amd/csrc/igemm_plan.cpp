@@ -454,6 +454,7 @@ int make_conv_plan(int es, const igemm_conv2d_desc *d, const void *X, const void
                          3 * ncu)
                 id = K_I16_128x128;
             else if (tiles_of(K_I16_64x64, M, N) < 32) id = M <= 64 ? K_I16_32x128 : K_I16_16x128;
+            else if (K <= kBK && tiles_of(K_I16_64x64, M, N) < ncu) id = K_I16_16x128;
             else id = K_I16_64x64;
         } else {
             id = M <= 16 ? K_I8_16x256 : K_I8_32x256;
