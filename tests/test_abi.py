@@ -495,3 +495,23 @@ def test_srs_noop_and_unsupported(fn):
     # one block beyond 32768 elements: unsupported, nothing enqueued
     assert fn(4, 4, k, FAKE_A, k, FAKE_B, 4, FAKE_C, 4, 0, 0, 0, 0) == ig.IGEMM_ENOTSUP
     assert fn(4, 4, k, FAKE_A, k, FAKE_B, 4, FAKE_C, 4, 32769, 0, 0, 0) == ig.IGEMM_ENOTSUP
+
+
+def test_planner_rules_for_small_int16_outputs():
+    """The measured rules for small int16 products on a 256-unit device: k
+    slices of the 64x64 tiles keep two k-tiles each with the count rounded
+    up; one k-tile outputs whose 64x64 tiles leave units idle take 16-row
+    tiles; convolutions follow the same rules."""
+    def plan(m, n, k):
+        p = ig.igemm_query_plan(2, m, n, k, num_cu=256)
+        return ig.igemm_kernel_name(p["kernel"]), p["split"], p["k_chunk"]
+    assert plan(3136, 64, 576) == ("i16_64x64", 5, 128)
+    assert plan(12544, 64, 147) == ("i16_64x64", 2, 128)
+    assert plan(3136, 256, 64)[0] == "i16_16x128"
+    assert plan(100352, 256, 64)[0] == "i16_64x64"      # enough 64x64 tiles to fill the units
+    d = ig.conv_desc(1, 56, 56, 64, 256, 1, 1)
+    p = ig.igemm_conv2d_query_plan(2, d, num_cu=256)
+    assert ig.igemm_kernel_name(p["kernel"]) == "i16_16x128"
+    d = ig.conv_desc(1, 56, 56, 64, 64, 3, 3, pad=(1, 1))
+    p = ig.igemm_conv2d_query_plan(2, d, num_cu=256)
+    assert (ig.igemm_kernel_name(p["kernel"]), p["split"]) == ("i16_64x64", 5)
