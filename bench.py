@@ -357,7 +357,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: --gpus {args.gpus} is not supported: this build measures one GPU "
+        print(f"bench.py: --gpus {args.gpus} is not supported: the benchmark measures one GPU "
               "(the kernel at one GPU's share); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
