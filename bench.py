@@ -2,44 +2,51 @@
 """Benchmark for integer GEMM C += A.B on one MI355X.
 
 A step is one call of igemm_i16 on the int16 workload m = n = k = 4096
-(A, B uniform over the full int16 range, C uniform in [-2^20, 2^20], seed 1):
-host validation and planning, the two pack kernels (A split into int8 limb
-planes with its row sums, B transposed and split with its column sums, into
-a workspace from torch's caching allocator), then the multiply kernel that
-streams the packed planes through LDS into the int8 matrix cores, applies
-the limb corrections and adds into C with int32 wraparound. Inputs are
-resident in HBM before the timed region starts.
+(A, B uniform over the full int16 range, C uniform in [-2^20, 2^20], seed 1)
+through the tensor wrapper gemm_i16: host validation and planning, the two
+pack kernels (A split into int8 limb planes with its row sums, B transposed
+and split with its column sums, into a workspace from torch's caching
+allocator), then the multiply kernel that streams the packed planes through
+LDS into the int8 matrix cores, applies the limb corrections and adds into C
+with int32 wraparound. Inputs are resident in HBM before the timed region
+starts.
 
 Prints ONE JSON line. Besides the headline value it carries:
   roofline      the dominant kernel (the multiply) timed alone with HIP events
                 on the stream it is launched on, by running it on operands
                 packed once (the library's pack-once calls), against the
-                int8 matrix-core peak divided by the four limb products,
-                with the matrix-core utilisation, int8 operations and clock
-                rocprofv3 counted for that kernel (committed summary);
-  cpu_baseline  the CPU oracle timed on the host cores over a bounded sample
-                of the same workload;
-  per_config    every other workload, each by graph replay (median of five
-                repetitions of at least 20 ms; memory-bound ones rotate
-                through enough buffer sets to defeat the 256 MB last-level
-                cache), with its own roofline fraction (memory-bound ones
-                also against a measured 1 GiB device copy); then the
-                paper's own GEMM shape (4096, 4096, 290), for context, the
-                same shape through the int16-output entry point with the
-                paper's k_c = 290 and shift 0 (and 4096^3 with k_c = 256),
-                and the six network layers run as convolutions through the
-                implicit-GEMM entry point (IM2ROW gathered in the kernel), at
-                batch 1 and batch 32.
+                int8 matrix-core peak divided by the four limb products; the
+                whole step's fraction of the same peak beside it; the HBM
+                traffic and matrix-core utilisation rocprofv3 counted for that
+                kernel (committed summaries, reported while the kernel's
+                sources and build flags hash to the value they were taken on);
+  cpu_baseline  the CPU oracle on the host cores: its rate on the whole int16
+                4096^3 workload, the seconds it took on every other workload
+                (each one's first GPU result is compared with it element by
+                element), one-thread seconds for int16 256^3, the CPU model;
+  per_config    every workload by graph replay (median of five repetitions of
+                at least 20 ms), in a compact map name -> {us, TOPS, GB/s for
+                memory-bound entries, bound, frac of that roofline, frac of a
+                measured 1 GiB device copy, kernel/split, MB cycled per graph
+                replay (memory-bound entries rotate at least 512 MB of
+                distinct buffers, twice the 256 MB last-level cache), exact =
+                the first result equals the oracle's in every element}: int16
+                256^3, int8 8192^3, the six conv-shaped int16 GEMMs, the six
+                skinny int8 GEMMs, the paper's GEMM shape (4096, 4096, 290)
+                for context, the int16-output update on that shape with the
+                paper's k_c = 290 and shift 0 and on 4096^3 with k_c = 256,
+                and the six network layers as convolutions through the
+                implicit-GEMM entry point at batch 1 and batch 32.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-extra]
-                       [--no-cpu-baseline] [--cpu-seconds S]
+                       [--no-cpu-baseline] [--details FILE]
 """
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
+import subprocess
 import sys
 import time
 
@@ -53,8 +60,13 @@ HBM_GBS = 8000.0             # HBM3E
 LIMB_PRODUCTS_I16 = 4        # int8 products per int16 multiply-add
 PEAK_I16_TOPS = PEAK_INT8_TOPS / LIMB_PRODUCTS_I16
 MALL_BYTES = 256 << 20
+MIN_CYCLED = 2 * MALL_BYTES  # bytes a memory-bound graph replay must rotate through
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_i16_packed_128x128_4096cube.json")
-KERNEL_SRC = os.path.join(ROOT, "paper_2302_07594_amd", "csrc", "igemm_packed.hip")
+CSRC = os.path.join(ROOT, "paper_2302_07594_amd", "csrc")
+# Everything the packed multiply kernel is built from.
+PACKED_SOURCES = [os.path.join(CSRC, f) for f in
+                  ("igemm_packed.hip", "igemm_device.h", "igemm_internal.h")] + \
+                 [os.path.join(ROOT, "include", "igemm.h")]
 
 
 def log(msg):
@@ -62,21 +74,26 @@ def log(msg):
 
 
 def kernel_source_hash() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    """SHA-256 over the packed kernel's source, the headers it includes and
+    the library's compile flags."""
+    from paper_2302_07594_amd import build as hip_build
+    return hip_build._hash_files(PACKED_SOURCES, hip_build.compile_flags())
+
+
+def _summary(path):
+    try:
+        with open(path) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    return t if t.get("kernel_source_sha256") == kernel_source_hash() else None
 
 
 def measured_traffic():
     """HBM bytes per launch from the committed rocprofv3 counter summary, if
-    it was taken on the current kernel source; otherwise None."""
-    try:
-        with open(TRAFFIC_FILE) as f:
-            t = json.load(f)
-    except (OSError, ValueError):
-        return None
-    if t.get("kernel_source_sha256") != kernel_source_hash():
-        return None
-    return t.get("traffic_bytes_per_launch")
+    it was taken on the current kernel sources and flags; otherwise None."""
+    t = _summary(TRAFFIC_FILE)
+    return None if t is None else t.get("traffic_bytes_per_launch")
 
 
 MFMA_FILES = {
@@ -89,13 +106,9 @@ def measured_mfma(dtype):
     """Matrix-core figures of the packed multiply from the committed
     rocprofv3 counter summary (SQ_VALU_MFMA_BUSY_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_I8,
     GRBM_GUI_ACTIVE with a kernel trace), if taken on the current kernel
-    source; otherwise None."""
-    try:
-        with open(MFMA_FILES[dtype]) as f:
-            t = json.load(f)
-    except (OSError, ValueError):
-        return None
-    if t.get("kernel_source_sha256") != kernel_source_hash() or not t.get("dispatches"):
+    sources and flags; otherwise None."""
+    t = _summary(MFMA_FILES[dtype])
+    if t is None or not t.get("dispatches"):
         return None
     rows = t["dispatches"]
     avg = lambda key: sum(r[key] for r in rows) / len(rows)
@@ -103,16 +116,12 @@ def measured_mfma(dtype):
         "mfma_busy": round(avg("mfma_busy"), 4),
         "int8_mfma_ops_per_launch": rows[0]["int8_mfma_ops"],
         "clock_ghz": round(avg("clock_ghz"), 3),
-        "dispatches": len(rows),
         "source": os.path.relpath(MFMA_FILES[dtype], ROOT),
     }
 
 
-def roofline_for(dtype, m, n, k, seconds):
-    """(bound, achieved, peak, unit) for one GEMM of this shape."""
-    es = 2 if dtype == "i16" else 1
-    ops = 2.0 * m * n * k
-    nbytes = m * k * es + k * n * es + 8.0 * m * n
+def roofline(ops, nbytes, es, seconds):
+    """(bound, achieved, peak, unit) for `ops` operations moving `nbytes`."""
     peak_ops = (PEAK_I16_TOPS if es == 2 else PEAK_INT8_TOPS) * 1e12
     if ops / nbytes >= peak_ops / (HBM_GBS * 1e9):
         return "mfma", ops / seconds / 1e12, peak_ops / 1e12, "TOPS"
@@ -145,9 +154,6 @@ def time_graph(g, per_graph, reps=5, min_rep_ms=20.0):
     return statistics.median(times)
 
 
-TIMING = "hip graph replay: median of 5 repetitions of >= 20 ms"
-
-
 def copy_bandwidth(nbytes=1 << 30, reps=5):
     """Device-to-device copy rate (bytes read plus written per second) of a
     1 GiB buffer, larger than the 256 MB last-level cache."""
@@ -173,25 +179,33 @@ def copy_bandwidth(nbytes=1 << 30, reps=5):
     return 2.0 * nbytes / statistics.median(ts)
 
 
-def bench_case(case, min_sets=1, per_graph=40, warmup=3):
-    """Time one workload case on rotating device copies of its operands.
+class OracleLog:
+    """Seconds the CPU oracle took per workload (each check is one whole
+    workload, all host threads)."""
 
-    The launches are captured once in a HIP graph (per_graph launches cycling
-    through the buffer sets) and the graph is replayed, so the figure is the
-    device time per launch without host launch overhead.
-    """
+    def __init__(self):
+        self.seconds = {}
+
+    def run(self, name, fn, *args):
+        t0 = time.perf_counter()
+        fn(*args)
+        self.seconds[name] = round(time.perf_counter() - t0, 3)
+
+
+def replay_sets(f, host_sets, set_bytes, memory_bound, min_per_graph=40, warmup=3):
+    """Capture launches of f over rotating device copies of the operands and
+    time the graph. Memory-bound workloads rotate through enough distinct
+    buffer sets that one replay touches at least MIN_CYCLED bytes, with at
+    least one launch per set, so no launch finds its operands in the
+    last-level cache from the launch before. Returns (seconds per launch,
+    number of sets, bytes cycled per replay)."""
     import torch
-
-    import paper_2302_07594_amd as ig
-    import workloads
-    A, B, C = workloads.generate(case)
-    es = 2 if case.dtype == "i16" else 1
-    set_bytes = A.nbytes + B.nbytes + C.nbytes
-    nsets = max(min_sets, -(-2 * MALL_BYTES // set_bytes))
-    nsets = min(nsets, 64)
-    Ad0, Bd0, Cd0 = (torch.from_numpy(x).cuda() for x in (A, B, C))
-    sets = [(Ad0, Bd0, Cd0)] + [(Ad0.clone(), Bd0.clone(), Cd0.clone()) for _ in range(nsets - 1)]
-    f = ig.gemm_i16 if es == 2 else ig.gemm_i8
+    nsets = -(-MIN_CYCLED // set_bytes) if memory_bound else max(1, -(-MIN_CYCLED // set_bytes))
+    if not memory_bound:
+        nsets = min(nsets, 2)
+    first = [torch.from_numpy(x).cuda() for x in host_sets]
+    sets = [first] + [[t.clone() for t in first] for _ in range(nsets - 1)]
+    per_graph = max(min_per_graph, nsets)
     for i in range(warmup):
         f(*sets[i % nsets])
     torch.cuda.synchronize()
@@ -202,149 +216,157 @@ def bench_case(case, min_sets=1, per_graph=40, warmup=3):
     g.replay()
     torch.cuda.synchronize()
     t = time_graph(g, per_graph)
-    plan = ig.igemm_query_plan(es, case.m, case.n, case.k)
-    bound, ach, peak, unit = roofline_for(case.dtype, case.m, case.n, case.k, t)
-    return {
-        "name": case.name, "dtype": case.dtype, "m": case.m, "n": case.n, "k": case.k,
-        "kernel": plan["kernel_name"], "split": plan["split"], "grid": plan["grid"],
-        "us": round(t * 1e6, 2), "TOPS": round(2.0 * case.m * case.n * case.k / t / 1e12, 2),
-        "bound": bound, "achieved": round(ach, 1), "peak": peak, "unit": unit,
-        "frac": round(ach / peak, 4), "buffer_sets": nsets, "timing": TIMING,
-        # the int8 counter summary was taken on this very workload
-        **({"rocprof_mfma": measured_mfma("i8")}
-           if (case.dtype, case.m, case.n, case.k) == ("i8", 8192, 8192, 8192) else {}),
-    }
+    del g, sets, first
+    torch.cuda.empty_cache()
+    return t, nsets, min(nsets, per_graph) * set_bytes
 
 
-def bench_srs_case(case, kc, shift, per_graph=40, warmup=3):
-    """Time the int16-output update (shift-round-saturate conversion per k
-    block of kc, int16 C) on a workload's A and B with a random int16 C, like
-    bench_case: gemm_srs as a caller gets it, i.e. the packed path (operands
-    packed into a workspace from torch's allocator, one multiply per block)
-    where the library chooses it, else one fused launch per block. The
-    algorithmic bytes are A and B once and the int16 C read and written once
-    per block."""
-    import numpy as np
+def entry(t, ops, nbytes, es, kernel, cycled, exact):
+    bound, ach, peak, _ = roofline(ops, nbytes, es, t)
+    e = {"us": round(t * 1e6, 2), "TOPS": round(ops / t / 1e12, 2)}
+    if bound == "hbm":
+        e["GBs"] = round(ach, 1)
+    e.update({"bound": bound, "frac": round(ach / peak, 4), "kern": kernel,
+              "MB": round(cycled / 1e6), "exact": exact})
+    return e
+
+
+def first_result(f, host):
+    """One call on pristine device copies; returns the host result."""
     import torch
+    dev = [torch.from_numpy(x).cuda() for x in host]
+    f(*dev)
+    torch.cuda.synchronize()
+    out = dev[-1].cpu().numpy()
+    del dev
+    return out
 
+
+def bench_gemm(case, olog, details):
+    import numpy as np
+
+    import oracle
+    import paper_2302_07594_amd as ig
+    import workloads
+    A, B, C = workloads.generate(case)
+    es = 2 if case.dtype == "i16" else 1
+    f = ig.gemm_i16 if es == 2 else ig.gemm_i8
+    got = first_result(f, (A, B, C))
+    want = C.copy()
+    olog.run(case.name, oracle.igemm, A, B, want)
+    exact = bool(np.array_equal(got, want))
+    del got, want
+    m, n, k = case.m, case.n, case.k
+    ops = 2.0 * m * n * k
+    nbytes = A.nbytes + B.nbytes + 2.0 * C.nbytes
+    memory_bound = roofline(ops, nbytes, es, 1.0)[0] == "hbm"
+    t, nsets, cycled = replay_sets(f, (A, B, C), A.nbytes + B.nbytes + C.nbytes, memory_bound)
+    plan = ig.igemm_query_plan(es, m, n, k)
+    e = entry(t, ops, nbytes, es, f"{plan['kernel_name']}/{plan['split']}", cycled, exact)
+    if (case.dtype, m, n, k) == ("i8", 8192, 8192, 8192):
+        mf = measured_mfma("i8")
+        if mf is not None:
+            e["mfma_busy"], e["clk_ghz"] = mf["mfma_busy"], mf["clock_ghz"]
+    details.append({"name": case.name, "m": m, "n": n, "k": k, "plan": plan, "sets": nsets,
+                    **e})
+    return e
+
+
+def bench_srs(case, kc, shift, olog, details):
+    """The int16-output update (shift-round-saturate conversion per k block of
+    kc, int16 C) on a workload's A and B with a random int16 C, through
+    gemm_srs (the packed path on a workspace from torch's allocator where the
+    library plans it, else one fused launch per block). Algorithmic bytes: A
+    and B once and the int16 C read and written once per block."""
+    import numpy as np
+
+    import oracle
     import paper_2302_07594_amd as ig
     import workloads
     A, B, _ = workloads.generate(case)
     C = np.random.default_rng(case.seed).integers(-32768, 32767, size=(case.m, case.n),
                                                   dtype=np.int16, endpoint=True)
-    set_bytes = A.nbytes + B.nbytes + C.nbytes
-    nsets = min(64, max(1, -(-2 * MALL_BYTES // set_bytes)))
-    Ad0, Bd0, Cd0 = (torch.from_numpy(x).cuda() for x in (A, B, C))
-    sets = [(Ad0, Bd0, Cd0)] + [(Ad0.clone(), Bd0.clone(), Cd0.clone()) for _ in range(nsets - 1)]
-    for i in range(warmup):
-        ig.gemm_srs(*sets[i % nsets], kc=kc, shift=shift)
-    torch.cuda.synchronize()
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g):
-        for i in range(per_graph):
-            ig.gemm_srs(*sets[i % nsets], kc=kc, shift=shift)
-    g.replay()
-    torch.cuda.synchronize()
-    t = time_graph(g, per_graph)
+    f = lambda a, b, c: ig.gemm_srs(a, b, c, kc=kc, shift=shift)
+    got = first_result(f, (A, B, C))
+    want = C.copy()
+    name = f"{case.name}_srs_kc{kc}_shift{shift}"
+    olog.run(name, oracle.igemm_srs, A, B, want, kc, shift, False)
+    exact = bool(np.array_equal(got, want))
+    del got, want
     m, n, k = case.m, case.n, case.k
     nblocks = 1 if (kc == 0 or kc >= k) else -(-k // kc)
-    ws_bytes = ig.igemm_srs_query(2 if case.dtype == "i16" else 1, m, n, k, Ad0, k, Bd0, n, Cd0,
-                                  n, kc, torch.cuda.get_device_properties(0).multi_processor_count)
     ops = 2.0 * m * n * k
     nbytes = A.nbytes + B.nbytes + 4.0 * m * n * nblocks
-    peak_ops = PEAK_I16_TOPS * 1e12
-    if ops / nbytes >= peak_ops / (HBM_GBS * 1e9):
-        bound, ach, peak, unit = "mfma", ops / t / 1e12, peak_ops / 1e12, "TOPS"
-    else:
-        bound, ach, peak, unit = "hbm", nbytes / t / 1e9, HBM_GBS, "GB/s"
-    return {
-        "name": f"{case.name}_srs_kc{kc}_shift{shift}", "dtype": case.dtype,
-        "m": m, "n": n, "k": k, "kc": kc, "shift": shift, "blocks": nblocks,
-        "epilogue": "int16 C += sat16(floor(block product / 2^shift)) modulo 2^16",
-        "path": "packed" if ws_bytes > 0 else "fused", "workspace_bytes": ws_bytes,
-        "us": round(t * 1e6, 2), "TOPS": round(ops / t / 1e12, 2),
-        "bound": bound, "achieved": round(ach, 1), "peak": peak, "unit": unit,
-        "frac": round(ach / peak, 4), "buffer_sets": nsets, "timing": TIMING,
-    }
-
-
-def bench_conv_case(case, per_graph=40, warmup=3):
-    """Time one convolution (implicit GEMM: IM2ROW gathered in the kernel)
-    like bench_case; the roofline counts the lowered GEMM's multiply-adds
-    and the unique bytes of X, W and Y (read and written)."""
+    memory_bound = roofline(ops, nbytes, 2, 1.0)[0] == "hbm"
+    t, nsets, cycled = replay_sets(f, (A, B, C), A.nbytes + B.nbytes + C.nbytes, memory_bound,
+                                   min_per_graph=10 if nblocks > 4 else 40)
     import torch
+    ncu = torch.cuda.get_device_properties(0).multi_processor_count
+    aligned = 1 << 12   # stands for a 16-byte aligned buffer; never dereferenced
+    ws = ig.igemm_srs_query(2, m, n, k, aligned, k, aligned, n, aligned, n, kc, ncu)
+    e = entry(t, ops, nbytes, 2, "packed" if ws > 0 else "fused", cycled, exact)
+    details.append({"name": name, "m": m, "n": n, "k": k, "kc": kc, "blocks": nblocks,
+                    "workspace_bytes": ws, "sets": nsets, **e})
+    return name, e
 
+
+def bench_conv(case, olog, details):
+    """One convolution (implicit GEMM: IM2ROW gathered in the kernel); the
+    roofline counts the lowered GEMM's multiply-adds and the unique bytes of
+    X, W and Y (read and written)."""
+    import numpy as np
+
+    import oracle
     import paper_2302_07594_amd as ig
     import workloads
     X, W, Y = workloads.generate_conv(case)
     es = 2 if case.dtype == "i16" else 1
-    set_bytes = X.nbytes + W.nbytes + Y.nbytes
-    nsets = min(64, max(1, -(-2 * MALL_BYTES // set_bytes)))
-    Xd0, Wd0, Yd0 = (torch.from_numpy(x).cuda() for x in (X, W, Y))
-    sets = [(Xd0, Wd0, Yd0)] + [(Xd0.clone(), Wd0.clone(), Yd0.clone()) for _ in range(nsets - 1)]
     kw = dict(stride=case.stride, pad=case.pad, dil=case.dil)
-    for i in range(warmup):
-        ig.conv2d(*sets[i % nsets], **kw)
-    torch.cuda.synchronize()
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g):
-        for i in range(per_graph):
-            ig.conv2d(*sets[i % nsets], **kw)
-    g.replay()
-    torch.cuda.synchronize()
-    t = time_graph(g, per_graph)
+    f = lambda x, w, y: ig.conv2d(x, w, y, **kw)
+    got = first_result(f, (X, W, Y))
+    want = Y.copy()
+    olog.run(case.name, oracle.conv2d, X, W, want, case.stride, case.pad, case.dil)
+    exact = bool(np.array_equal(got, want))
+    del got, want
     m, n, k = case.gemm_shape()
-    d = ig.conv_desc(case.n, case.h, case.w, case.c, case.k, case.r, case.s, case.stride,
-                     case.pad, case.dil)
-    plan = ig.igemm_conv2d_query_plan(es, d, Xd0, Wd0, Yd0)
     ops = 2.0 * m * n * k
     nbytes = X.nbytes + W.nbytes + 2.0 * Y.nbytes
-    peak_ops = (PEAK_I16_TOPS if es == 2 else PEAK_INT8_TOPS) * 1e12
-    if ops / nbytes >= peak_ops / (HBM_GBS * 1e9):
-        bound, ach, peak, unit = "mfma", ops / t / 1e12, peak_ops / 1e12, "TOPS"
-    else:
-        bound, ach, peak, unit = "hbm", nbytes / t / 1e9, HBM_GBS, "GB/s"
-    return {
-        "name": case.name, "dtype": case.dtype, "conv": {
-            "n": case.n, "h": case.h, "w": case.w, "c": case.c, "k": case.k, "r": case.r,
-            "s": case.s, "stride": list(case.stride), "pad": list(case.pad),
-            "dil": list(case.dil)},
-        "m": m, "n": n, "k": k, "kernel": plan["kernel_name"], "split": plan["split"],
-        "grid": plan["grid"], "vector_gather": bool(plan["vec_a"]),
-        "us": round(t * 1e6, 2), "TOPS": round(ops / t / 1e12, 2),
-        "bound": bound, "achieved": round(ach, 1), "peak": peak, "unit": unit,
-        "frac": round(ach / peak, 4), "buffer_sets": nsets, "timing": TIMING,
-    }
+    memory_bound = roofline(ops, nbytes, es, 1.0)[0] == "hbm"
+    t, nsets, cycled = replay_sets(f, (X, W, Y), X.nbytes + W.nbytes + Y.nbytes, memory_bound,
+                                   min_per_graph=40 if case.n == 1 else 10)
+    d = ig.conv_desc(case.n, case.h, case.w, case.c, case.k, case.r, case.s, case.stride,
+                     case.pad, case.dil)
+    plan = ig.igemm_conv2d_query_plan(es, d)
+    e = entry(t, ops, nbytes, es, f"{plan['kernel_name']}/{plan['split']}", cycled, exact)
+    details.append({"name": case.name, "gemm": [m, n, k], "plan": plan, "sets": nsets, **e})
+    return e
 
 
-def cpu_baseline(A, B, C_gpu_first, C0, seconds):
-    """Time the CPU oracle on whole rows of the same workload, for at most
-    about `seconds`; also confirm those rows match the GPU's first result."""
-    import numpy as np
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
-    import oracle
-    m, k = A.shape
-    n = B.shape[1]
-    block = 64
-    done = 0
-    elapsed = 0.0
-    mismatched = 0
-    while done < m and elapsed < seconds:
-        rows = slice(done, min(m, done + block))
-        Cr = np.ascontiguousarray(C0[rows])
-        t0 = time.perf_counter()
-        oracle.igemm(np.ascontiguousarray(A[rows]), B, Cr)
-        elapsed += time.perf_counter() - t0
-        mismatched += int((Cr != C_gpu_first[rows]).sum())
-        done = rows.stop
-    ops = 2.0 * done * n * k
-    return {
-        "value": round(ops / elapsed / 1e12, 6), "unit": "TOPS",
-        "cores": oracle.num_threads(), "kind": "oracle",
-        "sample": f"rows 0..{done - 1} of the {m}x{n}x{k} int16 workload "
-                  f"({done * n * k:.3g} multiply-adds, {elapsed:.1f} s)",
-        "rows_bit_exact_vs_gpu": mismatched == 0, "rows_checked": done,
-    }
+
+def oracle_one_thread_seconds():
+    """The oracle on the int16 256^3 workload with one OpenMP thread, in a
+    child process (the thread count is fixed when the runtime starts)."""
+    code = ("import time, workloads, oracle\n"
+            "A, B, C = workloads.generate(workloads.WORKLOADS['i16_256'].cases[0])\n"
+            "t = time.perf_counter(); oracle.igemm(A, B, C)\n"
+            "print(time.perf_counter() - t, oracle.num_threads())\n")
+    env = dict(os.environ, OMP_NUM_THREADS="1")
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True,
+                       text=True, timeout=300)
+    if r.returncode != 0:
+        return None
+    secs, threads = r.stdout.split()
+    return round(float(secs), 4) if int(threads) == 1 else None
 
 
 def main():
@@ -354,7 +376,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-extra", action="store_true", help="skip the per-config table")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--details", default=None, help="write every per-config record here")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: --gpus {args.gpus} is not supported: the benchmark measures one GPU "
@@ -369,19 +391,17 @@ def main():
 
     case = workloads.WORKLOADS["i16_4096"].cases[0]
     m, n, k = case.m, case.n, case.k
-    log(f"bench: generating {case.name}")
+    log("bench: int16 4096^3 step")
     A, B, C0 = workloads.generate(case)
     Ad = torch.from_numpy(A).cuda()
     Bd = torch.from_numpy(B).cuda()
     Cd = torch.from_numpy(C0).cuda()
-    # First launch on the pristine C; its result is compared with the oracle
-    # rows in the CPU-baseline leg.
+    # First launch on the pristine C; its result is compared with the oracle.
     ig.gemm_i16(Ad, Bd, Cd)
     torch.cuda.synchronize()
     C_first = Cd.cpu().numpy()
     plan = ig.igemm_query_plan(2, m, n, k, Ad, k, Bd, n, Cd, n)
 
-    log(f"bench: warmup {args.warmup}, timed steps {args.steps}")
     for _ in range(args.warmup):
         ig.gemm_i16(Ad, Bd, Cd)
     torch.cuda.synchronize()
@@ -402,7 +422,6 @@ def main():
 
     # The dominant kernel alone: the multiply on operands packed once. Its
     # launches go to the current stream, where the events are recorded.
-    log("bench: multiply kernel alone on packed operands")
     P = ig.pack(Ad, Bd)
     Cm = Cd.clone()
     for _ in range(3):
@@ -422,6 +441,7 @@ def main():
     pack_t = e0.elapsed_time(e1) * 1e-3 / args.steps
     del P, Cm
     ach = ops / mult / 1e12
+    mf = measured_mfma("i16")
 
     out = {
         "metric": "int16 GEMM C+=A.B throughput on 1 MI355X (int8 MFMA limb split), TOPS",
@@ -432,55 +452,68 @@ def main():
         "config": {
             "workload": "int16 GEMM C += A.B, m=n=k=4096, row-major, A,B uniform over the full "
                         "int16 range, C uniform in [-2^20,2^20], int32 wraparound, seed 1",
-            "m": m, "n": n, "k": k, "accumulate": "int32 modulo 2^32",
-            "kernel": plan["kernel_name"], "split": plan["split"], "grid": plan["grid"],
-            "workspace_bytes": plan["workspace_bytes"],
+            "kernel": plan["kernel_name"], "workspace_bytes": plan["workspace_bytes"],
         },
         "roofline": {
             "bound": "mfma", "achieved": round(ach, 1), "peak": PEAK_I16_TOPS, "unit": "TOPS",
             "frac": round(ach / PEAK_I16_TOPS, 4), "traffic": measured_traffic(),
-            "kernel": "igemm_packed<int16, 128x128> (multiply on packed operands)",
-            "peak_basis": "int8 MFMA dense peak 5000 TOPS / 4 int8 limb products per int16 "
-                          "multiply-add",
-            "int8_mfma_frac": round(ach * LIMB_PRODUCTS_I16 / PEAK_INT8_TOPS, 4),
-            "kernel_us": round(mult * 1e6, 2),
-            "pack_us": round(pack_t * 1e6, 2),
+            "kernel": "igemm_packed<int16,128x128> multiply, on packed operands",
+            "peak_basis": "5000 TOPS int8 MFMA / 4 limb products",
+            "kernel_us": round(mult * 1e6, 2), "pack_us": round(pack_t * 1e6, 2),
             "step_device_us": round(step_dev * 1e6, 2),
-            "rocprof_mfma": measured_mfma("i16"),
+            "step_frac": round(value / PEAK_I16_TOPS, 4),
+            **({"mfma_busy": mf["mfma_busy"], "clk_ghz": mf["clock_ghz"]} if mf else {}),
         },
     }
+    olog = OracleLog()
     if not args.no_cpu_baseline:
-        log("bench: CPU oracle baseline")
-        out["cpu_baseline"] = cpu_baseline(A, B, C_first, C0, args.cpu_seconds)
-    del Ad, Bd, Cd
+        import oracle
+        log("bench: CPU oracle on the whole int16 4096^3 workload")
+        want = C0.copy()
+        olog.run(case.name, oracle.igemm, A, B, want)
+        secs = olog.seconds[case.name]
+        out["cpu_baseline"] = {
+            "value": round(ops / secs / 1e12, 6), "unit": "TOPS",
+            "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"the whole {m}x{n}x{k} int16 workload ({m * n * k:.3g} multiply-adds, "
+                      f"{secs:.2f} s)",
+            "exact": bool(np.array_equal(C_first, want)),
+            "cpu_model": cpu_model(),
+            "i16_256_1thread_s": oracle_one_thread_seconds(),
+        }
+        del want
+    del Ad, Bd, Cd, C_first
     torch.cuda.empty_cache()
+    details = []
     if not args.no_extra:
-        per = []
+        import oracle  # noqa: F401  (per-config results are checked against it)
+        per = {}
         for wname in ("i16_256", "i8_8192", "i16_conv", "i8_skinny", "i16_paper"):
             for c in workloads.WORKLOADS[wname].cases:
-                log(f"bench: per-config {c.name}")
-                per.append(bench_case(c))
-                torch.cuda.empty_cache()
-        # The paper's configuration: its GEMM shape with its k_c = 290 and the
-        # listing's shift 0, int16 output; and 4096^3 with k_c = 256.
-        log("bench: per-config int16-output update")
-        per.append(bench_srs_case(workloads.WORKLOADS["i16_paper"].cases[0], 290, 0))
-        per.append(bench_srs_case(workloads.WORKLOADS["i16_4096"].cases[0], 256, 0,
-                                  per_graph=10))
-        torch.cuda.empty_cache()
+                log(f"bench: {c.name}")
+                per[c.name] = bench_gemm(c, olog, details)
+        for c, kc in ((workloads.WORKLOADS["i16_paper"].cases[0], 290),
+                      (workloads.WORKLOADS["i16_4096"].cases[0], 256)):
+            log(f"bench: {c.name} int16 output, kc {kc}")
+            name, e = bench_srs(c, kc, 0, olog, details)
+            per[name] = e
         for c in workloads.CONV2D_CASES + workloads.CONV2D_B32_CASES:
-            log(f"bench: per-config {c.name}")
-            per.append(bench_conv_case(c, per_graph=40 if c.n == 1 else 10))
-            torch.cuda.empty_cache()
-        # Memory-bound entries also against a measured device copy.
-        log("bench: device-to-device copy bandwidth")
+            log(f"bench: {c.name}")
+            per[c.name] = bench_conv(c, olog, details)
         cbw = copy_bandwidth()
-        out["copy_bandwidth_GBs"] = round(cbw / 1e9, 1)
-        for r in per:
-            if r["bound"] == "hbm":
-                r["frac_of_copy"] = round(r["achieved"] * 1e9 / cbw, 4)
+        out["copy_GBs"] = round(cbw / 1e9, 1)
+        for e in per.values():
+            if e["bound"] == "hbm":
+                e["fc"] = round(e["GBs"] * 1e9 / cbw, 4)
+        if "cpu_baseline" in out:
+            out["cpu_baseline"]["per_config_s"] = olog.seconds
+        out["all_exact"] = all(e["exact"] for e in per.values()) and \
+            out.get("cpu_baseline", {}).get("exact", True)
         out["per_config"] = per
-    print(json.dumps(out), flush=True)
+    if args.details:
+        with open(args.details, "w") as f:
+            json.dump({"headline": out, "per_config": details}, f, indent=1, default=str)
+    print(json.dumps(out, separators=(",", ":")), flush=True)
 
 
 if __name__ == "__main__":

@@ -25,18 +25,18 @@
  * Pointers and leading dimensions of any alignment are accepted; 16-byte
  * aligned rows take the vector-load path, others a slower element path.
  *
- * Workspace: large products take the packed path (Sec. 4.1's packing of the
+ * Memory: the library allocates no device memory and keeps no per-call
+ * state; every entry point may be called from several threads at once.
+ * Large products run fastest on the packed path (Sec. 4.1's packing of the
  * A and B panels into contiguous buffers, done once per call for the whole
  * operands): pack kernels rearrange A and B into a device workspace, then
- * the main kernel multiplies the packed copies. igemm_query_plan reports
- * the workspace a call needs (plan.workspace_bytes, 0 for the fused
- * kernels). The _ws calls take a caller-owned workspace; the other calls
- * draw it from a stream-ordered memory pool that the library owns, one per
- * device, allocated and released on `stream` around the launches (the pool
- * keeps freed memory for reuse until igemm_trim_workspace). While `stream`
- * is being captured into a graph those calls never use the pool: automatic
- * kernel choice then takes a fused kernel, and an explicit packed kernel
- * returns IGEMM_EINVAL.
+ * the main kernel multiplies the packed copies. That workspace always
+ * belongs to the caller: igemm_query_plan reports its size
+ * (plan.workspace_bytes) and the _ws, pack-once and packed-B calls take it.
+ * igemm_i16 / igemm_i8 and the _ex calls have no workspace, so their
+ * automatic choice is always one of the kernels that read A and B in place
+ * (fused tiles, or the int8 streaming kernel), and an explicit packed kernel
+ * returns IGEMM_EINVAL there.
  *
  * Asynchrony and errors: every entry point validates its arguments on the
  * host and returns IGEMM_EINVAL before making any HIP call if they are
@@ -61,8 +61,8 @@ typedef enum igemm_status {
     IGEMM_EHIP = -2,    /* a HIP runtime call or kernel launch failed      */
     IGEMM_ENOTSUP = -3, /* valid but unsupported (a size beyond 2^31 - 1,  */
                         /* or a grid beyond 2^24 workgroups)              */
-    IGEMM_ENOMEM = -4   /* workspace allocation failed, or the caller's    */
-                        /* workspace is smaller than the plan needs        */
+    IGEMM_ENOMEM = -4   /* the caller's workspace is smaller than the plan */
+                        /* needs                                           */
 } igemm_status;
 
 /*
@@ -98,7 +98,8 @@ int igemm_i8(int64_t m, int64_t n, int64_t k,
  *            cut into (>= 1); slices add their partial results into C with
  *            32-bit atomic adds, which are exact modulo 2^32 in any order.
  *            Values above ceil(k/64) are reduced to it. Packed kernels
- *            ignore it: they always run one launch per 32768 k elements.
+ *            need a workspace (the _ws calls; IGEMM_EINVAL here) and
+ *            ignore split: one launch per 32768 k elements.
  *            The int8 streaming kernel (few rows of A, B read once) rounds
  *            the k range of a slice up to 4, 8, 16 or 32 k-tiles of 64
  *            (16 at most for more than 16 rows), and to 4 k-tiles for
@@ -143,8 +144,11 @@ typedef struct igemm_plan {
  * Fill *out with the plan for a call with these arguments (pointers are only
  * inspected for alignment, never dereferenced). elem_bytes is 2 for int16,
  * 1 for int8. num_cu is the compute-unit count to plan for (0 = 256, one
- * MI355X). kernel/split as in the _ex calls. Returns IGEMM_OK, IGEMM_EINVAL
- * for invalid arguments, or IGEMM_OK with out->grid == 0 for a no-op call.
+ * MI355X). kernel/split as in the _ex calls. The plan is the one a _ws call
+ * follows when its workspace holds out->workspace_bytes (it may be a packed
+ * kernel); calls without a workspace follow the same rules restricted to the
+ * kernels that read A and B in place. Returns IGEMM_OK, IGEMM_EINVAL for
+ * invalid arguments, or IGEMM_OK with out->grid == 0 for a no-op call.
  */
 int igemm_query_plan(int elem_bytes, int64_t m, int64_t n, int64_t k,
                      const void *A, int64_t lda, const void *B, int64_t ldb,
@@ -156,8 +160,8 @@ int igemm_query_plan(int elem_bytes, int64_t m, int64_t n, int64_t k,
  * device memory themselves, e.g. a framework's caching allocator, or that
  * capture the call into a graph):
  *   workspace        device pointer, 256-byte aligned (IGEMM_EINVAL
- *                    otherwise), at least workspace_bytes long, or NULL to
- *                    use the library's pool as the calls above do.
+ *                    otherwise), at least workspace_bytes long, or NULL
+ *                    (the call is then the _ex call: no packed path).
  *   workspace_bytes  its size; IGEMM_ENOMEM (nothing enqueued) if it is
  *                    smaller than the plan's workspace_bytes.
  * The workspace is read and written by the kernels enqueued on `stream`; it
@@ -228,9 +232,9 @@ int igemm_i8_prepacked(int64_t m, int64_t n, int64_t k,
  *            the same n, k and kernel: pack A, then multiply. A's packed
  *            copy goes into `workspace` (caller-owned, 256-byte aligned, at
  *            least plan.packed_a_bytes of igemm_query_plan for (m, n, k)
- *            and that kernel; IGEMM_ENOMEM if smaller), or, with workspace
- *            NULL, into memory from the library's pool (IGEMM_EINVAL while
- *            `stream` is being captured, when A needs a packed copy).
+ *            and that kernel; IGEMM_ENOMEM if smaller). workspace may be
+ *            NULL only when that size is 0 (int8 A read in place);
+ *            otherwise NULL returns IGEMM_EINVAL.
  *   kernel   -1 = the packed kernel of the operand type, otherwise a packed
  *            kernel index of that type (IGEMM_EINVAL for fused kernels).
  *   packed_b, packed_b_bytes  device memory owned by the caller, 256-byte
@@ -352,11 +356,9 @@ int64_t igemm_conv2d_out_dim(int64_t in, int64_t f, int64_t stride, int64_t pad,
  * (igemm_i8_srs); C is int16, m x n, row-major with leading dimension ldc,
  * updated in place; DEVICE pointers owned by the caller; any alignment.
  * shift in [0, 47] (the paper's accumulators are 48 bits wide); kc >= 0 and a
- * block of at most 32768 elements. Large int16 products whose blocks are one
- * block or multiples of 256 elements (at most 64 blocks) are packed once into
- * a workspace from the library's pool, as igemm_i16 packs them (not while the
- * stream is being captured); then, and otherwise, one kernel launch per
- * block, enqueued in order on `stream`.
+ * block of at most 32768 elements. These calls have no workspace: one fused
+ * kernel launch per block, enqueued in order on `stream` (igemm_srs_ws with a
+ * caller's workspace packs large int16 products first).
  *
  * Errors: IGEMM_EINVAL (before any HIP call, nothing enqueued) as for
  * igemm_i16 and for kc < 0, shift outside [0, 47], round_half_up not 0 or 1;
@@ -371,9 +373,8 @@ int igemm_i8_srs(int64_t m, int64_t n, int64_t k, const int8_t *A, int64_t lda,
                  int round_half_up, void *stream);
 /* The same with elem_bytes 2 (int16) or 1 (int8) and an explicit kernel (one
  * of the fused 16/32-row, 64x64 or int16 128x128 tile kernels of the operand
- * type, or the int16 packed kernel for one block or blocks of a multiple of
- * 256, at most 64, outside stream capture; -1 = automatic). For sweeps and
- * tests. */
+ * type; -1 = automatic; the int16 packed kernel needs igemm_srs_ws, and is
+ * refused here with IGEMM_EINVAL). For sweeps and tests. */
 int igemm_srs_ex(int elem_bytes, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
                  const void *B, int64_t ldb, int16_t *C, int64_t ldc, int64_t kc, int shift,
                  int round_half_up, void *stream, int kernel);
@@ -393,9 +394,8 @@ int igemm_srs_ex(int elem_bytes, int64_t m, int64_t n, int64_t k, const void *A,
  *                    (IGEMM_EINVAL otherwise), holding the packed operands
  *                    and the per-block limb sums; at least the queried bytes
  *                    when the packed path is taken (IGEMM_ENOMEM otherwise;
- *                    nothing is enqueued). With a workspace the packed path
- *                    is also taken while `stream` is being captured; with
- *                    workspace NULL the call is igemm_srs_ex. The workspace
+ *                    nothing is enqueued). With workspace NULL the call is
+ *                    igemm_srs_ex (fused kernels only). The workspace
  *                    must stay untouched until the call's kernels have run;
  *                    calls that share one workspace must be ordered.
  */
@@ -406,11 +406,6 @@ int igemm_srs_ws(int elem_bytes, int64_t m, int64_t n, int64_t k, const void *A,
                  const void *B, int64_t ldb, int16_t *C, int64_t ldc, int64_t kc, int shift,
                  int round_half_up, void *stream, int kernel, void *workspace,
                  int64_t workspace_bytes);
-
-/* Release the memory the library's workspace pool for the current device
- * holds beyond what in-flight calls use (hipMemPoolTrimTo). Returns
- * IGEMM_OK, or IGEMM_EHIP. */
-int igemm_trim_workspace(void);
 
 /* Number of kernels, and a static name for index `kernel` (NULL if out of
  * range). */

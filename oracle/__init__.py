@@ -29,9 +29,12 @@ def _load():
     global _lib
     if _lib is not None:
         return _lib
-    if not os.path.exists(_build.LIB):
+    # IGEMM_ORACLE_LIB names another build of the same source (the sanitizer
+    # test loads the copy built with -fsanitize=address,undefined).
+    path = os.environ.get("IGEMM_ORACLE_LIB") or _build.LIB
+    if path == _build.LIB and not os.path.exists(path):
         _build.build()
-    lib = ctypes.CDLL(_build.LIB)
+    lib = ctypes.CDLL(path)
     i64 = ctypes.c_int64
     vp = ctypes.c_void_p
     for name in ("oracle_igemm_i16", "oracle_igemm_i8"):

@@ -12,7 +12,6 @@ Same names as the C ABI:
     igemm_i16_ex / igemm_i8_ex(..., kernel=-1, split=-1)
     igemm_i16_ws / igemm_i8_ws(..., kernel=-1, split=-1, workspace=None,
                                workspace_bytes=0)
-    igemm_trim_workspace()
     igemm_pack_i16 / igemm_pack_i8(m, n, k, A, lda, B, ldb, kernel=-1,
                                    workspace, workspace_bytes, stream=None)
     igemm_i16_prepacked / igemm_i8_prepacked(m, n, k, A, lda, C, ldc, kernel=-1,
@@ -44,8 +43,8 @@ tensors with unit stride along rows and update C in place; gemm_srs(A, B, C,
 kc, shift, round_half_up) the same with an int16 C; conv2d(X, W, Y,
 stride, pad, dil) takes contiguous NHWC / (r, s, c, k) / NHWC tensors; a workspace the
 call needs is taken from torch's caching allocator (so the calls can be
-captured into a torch CUDA graph) unless workspace="library" asks for the
-library's own stream-ordered pool.
+captured into a torch CUDA graph) and recorded on the stream the call runs
+on; the library itself allocates nothing.
 """
 from __future__ import annotations
 
@@ -151,8 +150,6 @@ def _load():
     lib.igemm_srs_ws.restype = ci
     lib.igemm_conv2d_out_dim.argtypes = [i64] * 5
     lib.igemm_conv2d_out_dim.restype = i64
-    lib.igemm_trim_workspace.argtypes = []
-    lib.igemm_trim_workspace.restype = ci
     lib.igemm_query_plan.argtypes = [ci, i64, i64, i64, vp, i64, vp, i64, vp, i64, ci, ci, ci,
                                      ctypes.POINTER(_Plan)]
     lib.igemm_query_plan.restype = ci
@@ -304,10 +301,6 @@ def igemm_i8_packed_b(m, n, k, A, lda, packed_b, packed_b_bytes, C, ldc, kernel=
                                       _stream(stream)))
 
 
-def igemm_trim_workspace() -> int:
-    return int(_lib.igemm_trim_workspace())
-
-
 _PLACEHOLDER = 1 << 12  # aligned, non-NULL; the planner never dereferences it
 
 
@@ -396,11 +389,18 @@ def _num_cu(device) -> int:
 
 def _aligned_workspace(nbytes, device, stream=None):
     """A uint8 device tensor of nbytes from torch's caching allocator,
-    256-byte aligned, recorded on `stream` if that is a torch stream."""
+    256-byte aligned. It is allocated on torch's current stream and recorded
+    on `stream` when the call runs elsewhere (a torch stream, or a raw HIP
+    stream handle, wrapped as an external stream), so that the allocator does
+    not hand its memory to other work before the call's kernels are done."""
     import torch
     ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
-    if stream is not None and hasattr(stream, "cuda_stream"):
-        ws.record_stream(stream)
+    if stream is not None:
+        if isinstance(stream, int):
+            if stream != int(torch.cuda.current_stream(device).cuda_stream):
+                ws.record_stream(torch.cuda.ExternalStream(stream, device=device))
+        elif hasattr(stream, "cuda_stream"):
+            ws.record_stream(stream)
     off = (-ws.data_ptr()) % 256
     return ws[off:off + nbytes]
 
@@ -417,12 +417,12 @@ def _gemm(es, A, B, C, stream, kernel, split, workspace, name):
             if plan["workspace_bytes"] > 0:
                 ws_bytes = plan["workspace_bytes"]
                 ws = _aligned_workspace(ws_bytes, C.device, stream)
-    elif workspace == "library":
+    elif workspace == "none":
         pass
     elif hasattr(workspace, "data_ptr"):
         ws, ws_bytes = workspace, workspace.numel() * workspace.element_size()
     else:
-        raise ValueError(f"{name}: workspace must be None, 'torch', 'library' or a tensor")
+        raise ValueError(f"{name}: workspace must be None, 'torch', 'none' or a tensor")
     st = fn(m, n, k, A, lda, B, ldb, C, ldc, stream, kernel, split, ws, ws_bytes)
     if st != IGEMM_OK:
         raise IgemmError(st, name)
@@ -559,8 +559,9 @@ def gemm_packed_b(A, PB, C, stream=None):
 def gemm_i16(A, B, C, stream=None, kernel=-1, split=-1, workspace=None):
     """C += A.B for 2-D torch.int16 CUDA tensors A (m x k), B (k x n) and a
     torch.int32 C (m x n). Returns C. Raises IgemmError on a bad status.
-    workspace: None / "torch" (torch's allocator), "library" (the library's
-    pool) or a uint8 CUDA tensor (256-byte aligned) to use as is."""
+    workspace: None / "torch" (a workspace from torch's allocator when the
+    plan packs the operands), "none" (no workspace: the in-place kernels
+    only) or a uint8 CUDA tensor (256-byte aligned) to use as is."""
     return _gemm(2, A, B, C, stream, kernel, split, workspace, "gemm_i16")
 
 
@@ -620,8 +621,8 @@ def gemm_srs(A, B, C, kc=0, shift=0, round_half_up=False, stream=None, kernel=-1
     shifted right by `shift` (floor, or round-half-up), saturated to int16
     and added to C modulo 2^16. `workspace` as for gemm_i16: None or 'torch'
     (a workspace from torch's allocator when the packed path is taken, so the
-    call may be captured into a graph), 'library' (the library's pool, not
-    under capture) or a uint8 tensor. Returns C."""
+    call may be captured into a graph), 'none' (fused kernels only) or a
+    uint8 tensor. Returns C."""
     import torch
     if A.dtype not in (torch.int16, torch.int8) or B.dtype != A.dtype:
         raise TypeError("gemm_srs: A and B must both be torch.int16 or both torch.int8")
@@ -638,12 +639,12 @@ def gemm_srs(A, B, C, kc=0, shift=0, round_half_up=False, stream=None, kernel=-1
                                        _num_cu(C.device), kernel)
             if ws_bytes > 0:
                 ws = _aligned_workspace(ws_bytes, C.device, stream)
-    elif workspace == "library":
+    elif workspace == "none":
         pass
     elif hasattr(workspace, "data_ptr"):
         ws, ws_bytes = workspace, workspace.numel() * workspace.element_size()
     else:
-        raise ValueError("gemm_srs: workspace must be None, 'torch', 'library' or a tensor")
+        raise ValueError("gemm_srs: workspace must be None, 'torch', 'none' or a tensor")
     st = igemm_srs_ws(es, m, n, k, A, lda, B, ldb, C, ldc, kc, shift,
                       1 if round_half_up else 0, stream, kernel, ws, ws_bytes)
     if st != IGEMM_OK:

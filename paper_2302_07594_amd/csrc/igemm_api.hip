@@ -1,9 +1,10 @@
-// The C entry points: validation, planning, workspace and dispatch to the
-// fused tiled kernels or to the pack-then-multiply path.
+// The C entry points: validation, planning and dispatch to the fused tiled
+// kernels, the streaming kernel or (on a caller's workspace) the
+// pack-then-multiply path. The library allocates no device memory.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include <mutex>
+#include <atomic>
 
 #include "igemm.h"
 #include "igemm_internal.h"
@@ -13,53 +14,24 @@ namespace {
 
 constexpr int kMaxDevices = 64;
 
+// Compute units per device, looked up once per device. Relaxed atomics: a
+// racing first call may query twice, and both store the same value.
+std::atomic<int> g_num_cu[kMaxDevices];
+
 int num_cu_of_current_device() {
-    static int cached[kMaxDevices] = {0};
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return 256;
-    if (dev >= 0 && dev < kMaxDevices && cached[dev] > 0) return cached[dev];
+    const bool cacheable = dev >= 0 && dev < kMaxDevices;
+    if (cacheable) {
+        const int c = g_num_cu[dev].load(std::memory_order_relaxed);
+        if (c > 0) return c;
+    }
     int cu = 0;
     if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         cu <= 0)
         cu = 256;
-    if (dev >= 0 && dev < kMaxDevices) cached[dev] = cu;
+    if (cacheable) g_num_cu[dev].store(cu, std::memory_order_relaxed);
     return cu;
-}
-
-// One stream-ordered memory pool per device for the packed path's workspace.
-// Its release threshold is unlimited, so after the first call of a given
-// size the allocations are served from memory the pool already holds.
-std::mutex g_pool_mu;
-hipMemPool_t g_pools[kMaxDevices] = {};
-
-int pool_of_current_device(hipMemPool_t *out) {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return IGEMM_EHIP;
-    std::lock_guard<std::mutex> lock(g_pool_mu);
-    if (g_pools[dev] == nullptr) {
-        hipMemPoolProps props = {};
-        props.allocType = hipMemAllocationTypePinned;
-        props.handleTypes = hipMemHandleTypeNone;
-        props.location.type = hipMemLocationTypeDevice;
-        props.location.id = dev;
-        hipMemPool_t pool = nullptr;
-        if (hipMemPoolCreate(&pool, &props) != hipSuccess) return IGEMM_EHIP;
-        uint64_t threshold = UINT64_MAX;
-        if (hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &threshold) !=
-            hipSuccess) {
-            (void)hipMemPoolDestroy(pool);
-            return IGEMM_EHIP;
-        }
-        g_pools[dev] = pool;
-    }
-    *out = g_pools[dev];
-    return IGEMM_OK;
-}
-
-bool stream_is_capturing(hipStream_t s) {
-    hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
-    if (hipStreamIsCapturing(s, &st) != hipSuccess) return false;
-    return st != hipStreamCaptureStatusNone;
 }
 
 // The one-call workspace holds the A part, then the B part.
@@ -78,36 +50,6 @@ int multiply_both(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, 
                            (const char *)ws + p.packed_a_bytes, stream);
 }
 
-// Device workspace for one call: the caller's, or one from the pool that is
-// released on the stream after the call's kernels.
-struct Scratch {
-    void *ptr = nullptr;
-    bool pooled = false;
-};
-int get_scratch(void *workspace, int64_t workspace_bytes, int64_t need, hipStream_t s,
-                Scratch *out) {
-    if (need <= 0) return IGEMM_OK;
-    if (workspace != nullptr) {
-        if (workspace_bytes < need) return IGEMM_ENOMEM;
-        out->ptr = workspace;
-        return IGEMM_OK;
-    }
-    hipMemPool_t pool = nullptr;
-    int st = pool_of_current_device(&pool);
-    if (st != IGEMM_OK) return st;
-    if (hipMallocFromPoolAsync(&out->ptr, (size_t)need, pool, s) != hipSuccess ||
-        out->ptr == nullptr) {
-        (void)hipGetLastError();
-        return IGEMM_ENOMEM;
-    }
-    out->pooled = true;
-    return IGEMM_OK;
-}
-int put_scratch(const Scratch &sc, hipStream_t s, int st) {
-    if (sc.pooled && hipFreeAsync(sc.ptr, s) != hipSuccess && st == IGEMM_OK) st = IGEMM_EHIP;
-    return st;
-}
-
 int run(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, const void *B,
         int64_t ldb, int32_t *C, int64_t ldc, void *stream, int kernel, int split,
         void *workspace, int64_t workspace_bytes) {
@@ -118,23 +60,22 @@ int run(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, con
     if (kernel >= 0 && kKernels[kernel].es != es) return IGEMM_EINVAL;
     if (workspace != nullptr && ((uintptr_t)workspace % 256 != 0 || workspace_bytes < 0))
         return IGEMM_EINVAL;
-    hipStream_t s = (hipStream_t)stream;
-    // Without a caller workspace the pool is the only source, and it is not
-    // used while the stream is being captured.
-    const bool pool_ok = workspace != nullptr || !stream_is_capturing(s);
-    if (kernel >= 0 && kKernels[kernel].packed && !pool_ok) return IGEMM_EINVAL;
+    // The library allocates nothing: the packed path runs only on a
+    // caller's workspace; without one, automatic choice keeps to the kernels
+    // that read the operands in place, and an explicit packed kernel is
+    // refused.
+    const bool have_ws = workspace != nullptr;
+    if (kernel >= 0 && kKernels[kernel].packed && !have_ws) return IGEMM_EINVAL;
     igemm_plan p;
     st = make_plan(es, m, n, k, A, lda, B, ldb, ldc, num_cu_of_current_device(), kernel, split,
-                   pool_ok, &p);
+                   have_ws, &p);
     if (st != IGEMM_OK) return st;
     if (p.kernel == K_I8_STREAM) return launch_stream(p, m, n, k, A, lda, B, ldb, C, ldc, stream);
     if (!p.packed) return launch_tiled(es, p, m, n, k, A, lda, B, ldb, C, ldc, stream);
-    Scratch sc;
-    st = get_scratch(workspace, workspace_bytes, p.workspace_bytes, s, &sc);
+    if (workspace_bytes < p.workspace_bytes) return IGEMM_ENOMEM;
+    st = pack_both(es, p, m, n, k, A, lda, B, ldb, workspace, stream);
     if (st != IGEMM_OK) return st;
-    st = pack_both(es, p, m, n, k, A, lda, B, ldb, sc.ptr, stream);
-    if (st == IGEMM_OK) st = multiply_both(es, p, m, n, k, A, lda, C, ldc, sc.ptr, stream);
-    return put_scratch(sc, s, st);
+    return multiply_both(es, p, m, n, k, A, lda, C, ldc, workspace, stream);
 }
 
 // Plan of a pack-once call: the packed kernel of the operand type (kernel -1)
@@ -195,8 +136,9 @@ int run_pack_b(int es, int64_t n, int64_t k, const void *B, int64_t ldb, int ker
     return launch_pack_b(es, p, 1, n, k, fake, k, B, ldb, packed_b, true, stream);
 }
 
-// C += A B with B packed by run_pack_b: pack A (workspace: the caller's or
-// the pool's), then multiply.
+// C += A B with B packed by run_pack_b: pack A into the caller's workspace
+// (none is needed for int8 A that the multiply reads in place), then
+// multiply.
 int run_packed_b(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
                  const void *packed_b, int64_t packed_b_bytes, int32_t *C, int64_t ldc,
                  int kernel, void *workspace, int64_t workspace_bytes, void *stream) {
@@ -206,20 +148,15 @@ int run_packed_b(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t
     if (m == 0 || n == 0 || k == 0) return IGEMM_OK;
     if (workspace != nullptr && ((uintptr_t)workspace % 256 != 0 || workspace_bytes < 0))
         return IGEMM_EINVAL;
-    hipStream_t s = (hipStream_t)stream;
     igemm_plan p;
     st = packed_plan(es, m, n, k, A, lda, fake, n, ldc, kernel, packed_b, 0, &p);
     if (st != IGEMM_OK && st != IGEMM_ENOMEM) return st;
     if (packed_b_bytes < p.packed_b_bytes) return IGEMM_ENOMEM;
-    if (p.packed_a_bytes > 0 && workspace == nullptr && stream_is_capturing(s))
-        return IGEMM_EINVAL;
-    Scratch sc;
-    st = get_scratch(workspace, workspace_bytes, p.packed_a_bytes, s, &sc);
+    if (p.packed_a_bytes > 0 && workspace == nullptr) return IGEMM_EINVAL;
+    if (workspace_bytes < p.packed_a_bytes) return IGEMM_ENOMEM;
+    st = launch_pack_a(es, p, m, n, k, A, lda, workspace, nullptr, stream);
     if (st != IGEMM_OK) return st;
-    st = launch_pack_a(es, p, m, n, k, A, lda, sc.ptr, nullptr, stream);
-    if (st == IGEMM_OK)
-        st = launch_multiply(es, p, m, n, k, A, lda, C, ldc, sc.ptr, packed_b, stream);
-    return put_scratch(sc, s, st);
+    return launch_multiply(es, p, m, n, k, A, lda, C, ldc, workspace, packed_b, stream);
 }
 
 // Y += conv(X, W) through the fused kernels with IM2ROW gathering of A.
@@ -290,25 +227,21 @@ int run_srs(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
     if (blk > kMaxKChunk) return IGEMM_ENOTSUP;
     if (kernel == K_I16_PACKED_128x128 && !packed_ok) return IGEMM_EINVAL;
     if (kernel == K_I16_PACKED_128x128 || (kernel < 0 && packed_ok)) {
-        // The pool is not used under stream capture; a caller's workspace is.
-        hipStream_t s = (hipStream_t)stream;
-        const bool can_pack = workspace != nullptr || !stream_is_capturing(s);
+        // The packed path needs the caller's workspace.
+        const bool can_pack = workspace != nullptr;
         igemm_plan pp;
         int64_t need = 0;
         st = srs_packed_plan(es, m, n, k, A, lda, B, ldb, ldc, kc, num_cu_of_current_device(),
                              kernel, can_pack, &pp, &need);
         if (st != IGEMM_OK) return st;
         if (pp.packed) {
-            Scratch sc;
-            st = get_scratch(workspace, workspace_bytes, need, s, &sc);
+            if (workspace_bytes < need) return IGEMM_ENOMEM;
+            st = pack_both(es, pp, m, n, k, A, lda, B, ldb, workspace, stream);
             if (st != IGEMM_OK) return st;
-            st = pack_both(es, pp, m, n, k, A, lda, B, ldb, sc.ptr, stream);
-            if (st == IGEMM_OK)
-                st = launch_srs_packed(pp, m, n, k, blk, nblocks, A, lda, C, ldc, sc.ptr,
-                                       (const char *)sc.ptr + pp.packed_a_bytes,
-                                       (uint32_t *)((char *)sc.ptr + pp.workspace_bytes), shift,
-                                       round_half_up, stream);
-            return put_scratch(sc, s, st);
+            return launch_srs_packed(pp, m, n, k, blk, nblocks, A, lda, C, ldc, workspace,
+                                     (const char *)workspace + pp.packed_a_bytes,
+                                     (uint32_t *)((char *)workspace + pp.workspace_bytes), shift,
+                                     round_half_up, stream);
         }
     }
     for (int pass = 0; pass < 2; ++pass) {
@@ -480,13 +413,6 @@ int igemm_i8_packed_b(int64_t m, int64_t n, int64_t k, const int8_t *A, int64_t 
                       int kernel, void *workspace, int64_t workspace_bytes, void *stream) {
     return igemm::run_packed_b(1, m, n, k, A, lda, packed_b, packed_b_bytes, C, ldc, kernel,
                                workspace, workspace_bytes, stream);
-}
-
-int igemm_trim_workspace(void) {
-    hipMemPool_t pool = nullptr;
-    int st = igemm::pool_of_current_device(&pool);
-    if (st != IGEMM_OK) return st;
-    return hipMemPoolTrimTo(pool, 0) == hipSuccess ? IGEMM_OK : IGEMM_EHIP;
 }
 
 }  // extern "C"

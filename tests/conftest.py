@@ -16,14 +16,14 @@ def pytest_configure(config):
 
 
 def _ensure_built():
-    """Build the HIP library and the oracle only if nothing is built yet."""
-    lib = os.path.join(ROOT, "paper_2302_07594_amd", "libigemm.so")
-    if not os.path.exists(lib):
-        from paper_2302_07594_amd import build as hip_build
+    """Build the HIP library and the oracle when they are missing or were
+    built from other sources than the tree's (each build stamps the SHA-256 of
+    its sources, headers and flags next to the library)."""
+    from paper_2302_07594_amd import build as hip_build
+    from oracle import build as oracle_build
+    if not hip_build.is_current():
         hip_build.build()
-    olib = os.path.join(ROOT, "oracle", "liboracle.so")
-    if not os.path.exists(olib):
-        from oracle import build as oracle_build
+    if not oracle_build.is_current():
         oracle_build.build()
 
 

@@ -22,11 +22,13 @@ def to_device(x: np.ndarray, offset_elems: int = 0):
 
 
 def gpu_gemm(A, B, C, m, n, k, kernel=-1, split=-1, offsets=(0, 0, 0), stream=None,
-             check_status=True, workspace=None):
+             check_status=True, workspace="auto"):
     """Run C += A.B on the GPU. A, B, C are full numpy arrays whose row length
     is the leading dimension; the logical shapes are m x k, k x n, m x n.
-    workspace=None calls the _ex entry point (library pool for packed plans);
-    a device tensor is passed to the _ws entry point as the workspace.
+    workspace="auto" passes a workspace of the planned size to the _ws entry
+    point when the plan (with this kernel and split) packs the operands, and
+    calls the _ex entry point otherwise; workspace=None calls the _ex entry
+    point (no workspace); a device tensor is passed to the _ws entry point.
     Returns (status, C after the call as numpy)."""
     import torch
 
@@ -37,6 +39,15 @@ def gpu_gemm(A, B, C, m, n, k, kernel=-1, split=-1, offsets=(0, 0, 0), stream=No
     Cd = to_device(C, offsets[2])
     lda, ldb, ldc = A.shape[1], B.shape[1], C.shape[1]
     s = stream if stream is not None else torch.cuda.current_stream().cuda_stream
+    if isinstance(workspace, str) and workspace == "auto":
+        workspace = None
+        if m and n and k:
+            plan = ig.igemm_query_plan(es, m, n, k, Ad, lda, Bd, ldb, Cd, ldc,
+                                       torch.cuda.get_device_properties(0).multi_processor_count,
+                                       kernel, split)
+            if plan["workspace_bytes"] > 0:
+                workspace = torch.empty(plan["workspace_bytes"], dtype=torch.uint8,
+                                        device="cuda")
     if workspace is None:
         fn = ig.igemm_i16_ex if es == 2 else ig.igemm_i8_ex
         st = fn(m, n, k, Ad.data_ptr(), lda, Bd.data_ptr(), ldb, Cd.data_ptr(), ldc, s,

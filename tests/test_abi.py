@@ -27,7 +27,7 @@ def test_header_declares_entry_points():
     fns = declared_functions()
     for name in ("igemm_i16", "igemm_i8", "igemm_strerror", "igemm_i16_ex", "igemm_i8_ex",
                  "igemm_query_plan", "igemm_num_kernels", "igemm_kernel_name",
-                 "igemm_version", "igemm_i16_ws", "igemm_i8_ws", "igemm_trim_workspace",
+                 "igemm_version", "igemm_i16_ws", "igemm_i8_ws",
                  "igemm_pack_i16", "igemm_pack_i8", "igemm_i16_prepacked",
                  "igemm_i8_prepacked", "igemm_pack_b_i16", "igemm_pack_b_i8",
                  "igemm_i16_packed_b", "igemm_i8_packed_b"):
@@ -38,6 +38,42 @@ def test_library_exports_every_declared_symbol():
     lib = ctypes.CDLL(ig.library_path())
     for name in declared_functions():
         assert hasattr(lib, name), name
+
+
+def _imported_symbols(path):
+    import shutil
+    import subprocess
+    if shutil.which("nm") is None:
+        pytest.skip("nm not available")
+    out = subprocess.run(["nm", "-D", "--undefined-only", path], capture_output=True,
+                         text=True, check=True).stdout
+    return {line.split()[-1].split("@")[0] for line in out.splitlines() if line.strip()}
+
+
+def test_library_allocates_no_device_memory():
+    """The boundary allocates nothing and keeps no pool: the library imports
+    no HIP allocation, free, pool, memset or copy routine at all, so no call
+    can reach one; its only HIP imports are the launch machinery, the device
+    query for the compute-unit count and error reporting."""
+    hip = {s for s in _imported_symbols(ig.library_path()) if "hip" in s.lower()}
+    forbidden = [s for s in hip if any(w in s for w in
+                                       ("Malloc", "Free", "MemPool", "Memset", "Memcpy",
+                                        "HostRegister", "StreamCreate", "EventCreate"))]
+    assert not forbidden, forbidden
+    allowed = {"hipLaunchKernel", "hipGetLastError", "hipGetDevice", "hipDeviceGetAttribute",
+               "hipGetSymbolAddress", "__hipPushCallConfiguration",
+               "__hipPopCallConfiguration", "__hipRegisterFatBinary", "__hipRegisterFunction",
+               "__hipUnregisterFatBinary", "__hipRegisterVar"}
+    assert hip <= allowed, sorted(hip - allowed)
+
+
+def test_build_stamp_tracks_sources():
+    """The build records the hash of the sources, headers and flags it used;
+    the test session's library is current, and any change of flags changes
+    the hash."""
+    from paper_2302_07594_amd import build as hip_build
+    assert hip_build.is_current()
+    assert hip_build.source_hash(["-DX"]) != hip_build.source_hash()
 
 
 def test_oracle_not_linked_into_library():

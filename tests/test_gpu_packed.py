@@ -1,7 +1,8 @@
 """GPU parity of the pack-then-multiply path (pack kernels into a workspace,
 then the DMA-fed matrix-core kernel) against the CPU oracle, bit-exact, and
-its workspace handling: library pool, caller workspace, too-small and
-misaligned workspaces, graph capture."""
+its workspace handling: caller workspaces (the library allocates none),
+too-small and misaligned workspaces, refusal of the packed kernels without a
+workspace, graph capture."""
 import numpy as np
 import pytest
 
@@ -47,7 +48,7 @@ SHAPES = [
 
 @pytest.mark.parametrize("dt", ["i16", "i8"])
 @pytest.mark.parametrize("shape", SHAPES, ids=["x".join(map(str, s)) for s in SHAPES])
-def test_packed_ragged_pool(dt, shape):
+def test_packed_ragged(dt, shape):
     m, n, k = shape
     A, B, C = workloads.random_operands(dt, m, n, k, seed=600 + m + 3 * n + 7 * k)
     _check(dt, A, B, C, m, n, k)
@@ -162,33 +163,59 @@ def test_tensor_wrapper_workspace_modes():
     m, n, k = 1024, 1100, 1300
     A, B, C = workloads.random_operands("i16", m, n, k, seed=51)
     want = oracle_gemm(A, B, C, m, n, k)
-    for mode in (None, "library"):
+    need = ig.igemm_query_plan(2, m, n, k, kernel=_kid("i16"))["workspace_bytes"]
+    for mode in (None, "torch", "none", _workspace(need)):
         Ad, Bd, Cd = (torch.from_numpy(x).cuda() for x in (A, B, C))
-        ig.gemm_i16(Ad, Bd, Cd, kernel=_kid("i16"), workspace=mode)
+        kid = -1 if isinstance(mode, str) and mode == "none" else _kid("i16")
+        ig.gemm_i16(Ad, Bd, Cd, kernel=kid, workspace=mode)
         torch.cuda.synchronize()
-        assert np.array_equal(Cd.cpu().numpy(), want), mode
-    assert ig.igemm_trim_workspace() == ig.IGEMM_OK
+        assert np.array_equal(Cd.cpu().numpy(), want), str(mode)[:20]
 
 
-def test_capture_refuses_pool_for_explicit_packed():
-    """Under stream capture the pool is not used: an explicit packed kernel
-    without a workspace is refused, and nothing is recorded."""
+@pytest.mark.parametrize("dt", ["i16", "i8"])
+def test_explicit_packed_needs_workspace(dt):
+    """The library allocates nothing: an explicit packed kernel without a
+    workspace is refused before anything is enqueued, eagerly and under
+    stream capture (nothing recorded), and C is left untouched."""
     import torch
     ig = _ig()
     m, n, k = 256, 256, 512
-    A, B, C = workloads.random_operands("i16", m, n, k, seed=53)
+    A, B, C = workloads.random_operands(dt, m, n, k, seed=53)
+    st, got = gpu_gemm(A, B, C, m, n, k, kernel=_kid(dt), workspace=None, check_status=False)
+    assert st == ig.IGEMM_EINVAL and np.array_equal(got, C)
     Ad, Bd, Cd = (torch.from_numpy(x).cuda() for x in (A, B, C))
+    fn = ig.igemm_i16_ex if dt == "i16" else ig.igemm_i8_ex
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     s = torch.cuda.Stream()
     with torch.cuda.stream(s):
         with torch.cuda.graph(g, stream=s):
-            st = ig.igemm_i16_ex(m, n, k, Ad, k, Bd, n, Cd, n, s.cuda_stream, _kid("i16"), -1)
+            st = fn(m, n, k, Ad, k, Bd, n, Cd, n, s.cuda_stream, _kid(dt), -1)
             Cd.add_(0)   # keep the captured graph non-empty
     assert st == ig.IGEMM_EINVAL
     g.replay()
     torch.cuda.synchronize()
     assert np.array_equal(Cd.cpu().numpy(), C)
+
+
+@pytest.mark.parametrize("dt,shape", [("i16", (2048, 2048, 1300)), ("i16", (4096, 1024, 512)),
+                                      ("i8", (4096, 4096, 768))])
+def test_plain_call_without_workspace(dt, shape):
+    """igemm_i16 / igemm_i8 (no workspace) on shapes whose _ws plan packs:
+    they run an in-place kernel, bit-exact against the oracle."""
+    import torch
+    ig = _ig()
+    m, n, k = shape
+    es = 2 if dt == "i16" else 1
+    assert ig.igemm_query_plan(es, m, n, k)["packed"] == 1
+    A, B, C = workloads.random_operands(dt, m, n, k, seed=57 + m)
+    Ad, Bd, Cd = (torch.from_numpy(x).cuda() for x in (A, B, C))
+    fn = ig.igemm_i16 if dt == "i16" else ig.igemm_i8
+    assert fn(m, n, k, Ad, k, Bd, n, Cd, n) == ig.IGEMM_OK
+    torch.cuda.synchronize()
+    want = oracle_gemm(A, B, C, m, n, k)
+    got = Cd.cpu().numpy()
+    assert np.array_equal(got, want), describe_mismatch(got, want)
 
 
 @pytest.mark.parametrize("dt,shape", [("i16", (300, 520, 1000)), ("i8", (300, 520, 1000)),
@@ -225,3 +252,30 @@ def test_prepacked_equals_one_shot_call():
     ig.gemm_prepacked(ig.pack(Ad, Bd), C2)
     torch.cuda.synchronize()
     assert torch.equal(C1, C2)
+
+
+@pytest.mark.parametrize("kind", ["raw_handle", "torch_stream"])
+def test_wrapper_workspace_on_side_stream(kind):
+    """gemm_i16 on a side stream given as a raw HIP handle (or a torch
+    stream): the workspace taken from torch's allocator on the current stream
+    is recorded on the side stream, so memory allocated and overwritten on
+    the current stream right after the call cannot reuse it while the side
+    stream's pack and multiply kernels still read it."""
+    import torch
+    ig = _ig()
+    m, n, k = 2048, 2048, 2048
+    A, B, C = workloads.random_operands("i16", m, n, k, seed=71)
+    Ad, Bd, Cd = (torch.from_numpy(x).cuda() for x in (A, B, C))
+    need = ig.igemm_query_plan(2, m, n, k)["workspace_bytes"]
+    assert need > 0
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    arg = side.cuda_stream if kind == "raw_handle" else side
+    ig.gemm_i16(Ad, Bd, Cd, stream=arg)
+    junk = [torch.full((need // 4 + 4096,), -1, dtype=torch.int32, device="cuda")
+            for _ in range(3)]
+    torch.cuda.synchronize()
+    want = oracle_gemm(A, B, C, m, n, k)
+    got = Cd.cpu().numpy()
+    assert np.array_equal(got, want), describe_mismatch(got, want)
+    del junk

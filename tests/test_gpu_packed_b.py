@@ -44,7 +44,9 @@ def _pack_b_abi(dt, B, n, k):
     return buf, nbytes
 
 
-def _mul_abi(dt, A, m, n, k, buf, nbytes, C, use_pool, a_offset=0):
+def _mul_abi(dt, A, m, n, k, buf, nbytes, C, with_ws=True, a_offset=0):
+    """igemm_*_packed_b through the C ABI. with_ws=False passes no workspace
+    (valid only when A needs no packed copy); returns (status, C)."""
     import torch
     ig = _ig()
     es, kid = ES[dt], _kid(dt)
@@ -52,20 +54,43 @@ def _mul_abi(dt, A, m, n, k, buf, nbytes, C, use_pool, a_offset=0):
     Cd = to_device(C)
     lda, ldc = A.shape[1], C.shape[1]
     ws, ws_bytes = None, 0
-    if not use_pool:
+    if with_ws:
         ws_bytes = ig.igemm_query_plan(es, m, n, k, Ad, lda, None, n, Cd, ldc,
                                        kernel=kid)["packed_a_bytes"]
         ws = _aligned(max(ws_bytes, 1)) if ws_bytes > 0 else None
     fn = ig.igemm_i16_packed_b if es == 2 else ig.igemm_i8_packed_b
     st = fn(m, n, k, Ad, lda, buf, nbytes, Cd, ldc, kid, ws, ws_bytes, None)
     torch.cuda.synchronize()
-    assert st == 0, ig.igemm_strerror(st)
-    return Cd.cpu().numpy()
+    return st, Cd.cpu().numpy()
+
+
+def _mul_ok(*args, **kw):
+    st, got = _mul_abi(*args, **kw)
+    assert st == 0, _ig().igemm_strerror(st)
+    return got
 
 
 @pytest.mark.parametrize("dt", ["i16", "i8"])
-@pytest.mark.parametrize("use_pool", [False, True], ids=["caller_ws", "pool"])
-def test_pack_b_once_many_a(dt, use_pool):
+def test_packed_b_without_workspace(dt):
+    """No workspace: refused (C untouched) when A needs a packed copy; int8 A
+    that the multiply reads in place (aligned, 256-row multiple, k a multiple
+    of 256) needs none and runs."""
+    ig = _ig()
+    n, k = 520, 768
+    B = workloads.random_operands(dt, 1, n, k, seed=1211)[1]
+    buf, nbytes = _pack_b_abi(dt, B, n, k)
+    A, _, C = workloads.random_operands(dt, 300, n, k, seed=1212)
+    st, got = _mul_abi(dt, A, 300, n, k, buf, nbytes, C, with_ws=False)
+    assert st == ig.IGEMM_EINVAL and np.array_equal(got, C)
+    if dt == "i8":
+        A, _, C = workloads.random_operands(dt, 512, n, k, seed=1213)
+        st, got = _mul_abi(dt, A, 512, n, k, buf, nbytes, C, with_ws=False)
+        want = oracle_gemm(A, B, C, 512, n, k)
+        assert st == 0 and np.array_equal(got, want), describe_mismatch(got, want)
+
+
+@pytest.mark.parametrize("dt", ["i16", "i8"])
+def test_pack_b_once_many_a(dt):
     """One packed B, then A of 1, 129, 300 and 512 rows (int8 512 rows and
     k = 768 reads A in place) and padded leading dimensions: every product
     matches the oracle."""
@@ -75,7 +100,7 @@ def test_pack_b_once_many_a(dt, use_pool):
     for i, m in enumerate((1, 129, 300, 512)):
         lda = k + (0 if m == 512 else 3)
         A, _, C = workloads.random_operands(dt, m, n, k, seed=1300 + i, lda=lda, ldc=n + 2)
-        got = _mul_abi(dt, A, m, n, k, buf, nbytes, C, use_pool)
+        got = _mul_ok(dt, A, m, n, k, buf, nbytes, C)
         want = oracle_gemm(A, B, C, m, n, k)
         assert np.array_equal(got, want), f"m={m}\n" + describe_mismatch(got, want)
 
@@ -86,7 +111,7 @@ def test_packed_b_misaligned_a(dt):
     B = workloads.random_operands(dt, 1, n, k, seed=1401)[1]
     buf, nbytes = _pack_b_abi(dt, B, n, k)
     A, _, C = workloads.random_operands(dt, 200, n, k, seed=1402)
-    got = _mul_abi(dt, A, 200, n, k, buf, nbytes, C, False, a_offset=1)
+    got = _mul_ok(dt, A, 200, n, k, buf, nbytes, C, a_offset=1)
     want = oracle_gemm(A, B, C, 200, n, k)
     assert np.array_equal(got, want), describe_mismatch(got, want)
 
@@ -100,7 +125,7 @@ def test_packed_b_int16_extremes_two_chunks(value):
     B = np.full((k, n), value, dtype=np.int16)
     C = np.zeros((m, n), dtype=np.int32)
     buf, nbytes = _pack_b_abi("i16", B, n, k)
-    got = _mul_abi("i16", A, m, n, k, buf, nbytes, C, False)
+    got = _mul_ok("i16", A, m, n, k, buf, nbytes, C)
     want = oracle_gemm(A, B, C, m, n, k)
     assert np.array_equal(got, want), describe_mismatch(got, want)
 
@@ -116,8 +141,8 @@ def test_packed_b_buffer_is_read_only(dt):
     torch.cuda.synchronize()
     before = buf.clone()
     A, _, C = workloads.random_operands(dt, 257, n, k, seed=1502)
-    r1 = _mul_abi(dt, A, 257, n, k, buf, nbytes, C, False)
-    r2 = _mul_abi(dt, A, 257, n, k, buf, nbytes, C, True)
+    r1 = _mul_ok(dt, A, 257, n, k, buf, nbytes, C)
+    r2 = _mul_ok(dt, A, 257, n, k, buf, nbytes, C)
     assert torch.equal(buf, before)
     assert np.array_equal(r1, r2)
 

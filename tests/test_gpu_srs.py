@@ -46,16 +46,31 @@ def _oracle(A, B, C, m, n, k, kc, shift, rnd):
     return out
 
 
-def _gpu(A, B, C, m, n, k, kc, shift, rnd, kernel=-1, offsets=(0, 0, 0), check=True):
+def _gpu(A, B, C, m, n, k, kc, shift, rnd, kernel=-1, offsets=(0, 0, 0), check=True,
+         workspace=True):
+    """igemm_srs_ws with a workspace of the queried size when the plan packs
+    the operands (workspace=True), else igemm_srs_ex (no workspace)."""
     import torch
     ig = _ig()
     es = 2 if A.dtype == np.int16 else 1
     Ad = to_device(A, offsets[0])
     Bd = to_device(B, offsets[1])
     Cd = to_device(C, offsets[2])
-    st = ig.igemm_srs_ex(es, m, n, k, Ad.data_ptr(), A.shape[1], Bd.data_ptr(), B.shape[1],
-                         Cd.data_ptr(), C.shape[1], kc, shift, 1 if rnd else 0,
-                         torch.cuda.current_stream().cuda_stream, kernel)
+    args = (es, m, n, k, Ad.data_ptr(), A.shape[1], Bd.data_ptr(), B.shape[1], Cd.data_ptr(),
+            C.shape[1], kc)
+    need = 0
+    if workspace:
+        try:
+            need = ig.igemm_srs_query(*args, num_cu=torch.cuda.get_device_properties(0)
+                                      .multi_processor_count, kernel=kernel)
+        except ig.IgemmError:
+            need = 0   # the call itself reports the invalid argument
+    s = torch.cuda.current_stream().cuda_stream
+    if need > 0:
+        ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+        st = ig.igemm_srs_ws(*args, shift, 1 if rnd else 0, s, kernel, ws.data_ptr(), need)
+    else:
+        st = ig.igemm_srs_ex(*args, shift, 1 if rnd else 0, s, kernel)
     torch.cuda.synchronize()
     if check:
         assert st == 0, f"status {st}: {ig.igemm_strerror(st)}"
@@ -145,22 +160,21 @@ def test_block_beyond_limit_is_refused():
     assert st == _ig().IGEMM_ENOTSUP and np.array_equal(got, C)
 
 
-def test_paper_shape_sampled_rows():
+@pytest.mark.parametrize("path", ["packed", "fused"])
+def test_paper_shape_full(path):
     """The paper's GEMM shape (4096, 4096, 290) with its k_c = 290 and shift
-    0, full-range int16 operands: whole rows sampled across the tiles,
-    checked against the oracle on those rows (each row of C depends on the
-    same row of A only)."""
+    0, full-range int16 operands and a random int16 C (the configuration the
+    benchmark times): every element against the oracle, on the packed path
+    (with a workspace, as the benchmark runs it) and on the fused path (no
+    workspace)."""
     case = workloads.WORKLOADS["i16_paper"].cases[0]
     m, n, k = case.m, case.n, case.k
     A, B, _ = workloads.generate(case)
-    C = np.random.default_rng(4).integers(-32768, 32767, size=(m, n), dtype=np.int16,
-                                          endpoint=True)
-    _, got = _gpu(A, B, C, m, n, k, 290, 0, False)
-    rows = np.r_[0:3, 63:66, 1000, 2047:2050, 4093:4096]
-    import oracle
-    want = C[rows].copy()
-    oracle.igemm_srs(np.ascontiguousarray(A[rows]), B, want, 290, 0, False)
-    assert np.array_equal(got[rows], want), _describe(got[rows], want)
+    C = np.random.default_rng(case.seed).integers(-32768, 32767, size=(m, n), dtype=np.int16,
+                                                  endpoint=True)
+    _, got = _gpu(A, B, C, m, n, k, 290, 0, False, workspace=path == "packed")
+    want = _oracle(A, B, C, m, n, k, 290, 0, False)
+    assert np.array_equal(got, want), _describe(got, want)
 
 
 def test_tensor_wrapper_and_graph_replays():
@@ -227,21 +241,18 @@ def test_fuzz_srs(case):
     _check(A, B, C, m, n, k, kc, shift, rnd, kernel=kid, offsets=offs)
 
 
-def test_4096_cube_blocks_of_256_sampled_rows():
+def test_4096_cube_blocks_of_256_full():
     """The benchmark's second int16-output configuration: 4096^3 with
-    k_c = 256 (sixteen blocks), full-range operands, random int16 C; whole
-    rows sampled across the tiles against the oracle on those rows."""
+    k_c = 256 (sixteen blocks), full-range operands, random int16 C, on the
+    packed path the benchmark times: every element against the oracle."""
     case = workloads.WORKLOADS["i16_4096"].cases[0]
     m, n, k = case.m, case.n, case.k
     A, B, _ = workloads.generate(case)
     C = np.random.default_rng(case.seed).integers(-32768, 32767, size=(m, n), dtype=np.int16,
                                                   endpoint=True)
     _, got = _gpu(A, B, C, m, n, k, 256, 0, False)
-    rows = np.r_[0, 127:129, 2048, 4095]
-    import oracle
-    want = C[rows].copy()
-    oracle.igemm_srs(np.ascontiguousarray(A[rows]), B, want, 256, 0, False)
-    assert np.array_equal(got[rows], want), _describe(got[rows], want)
+    want = _oracle(A, B, C, m, n, k, 256, 0, False)
+    assert np.array_equal(got, want), _describe(got, want)
 
 
 @pytest.mark.parametrize("shape", [(1100, 1030, 700), (128, 128, 256), (257, 300, 1024),
