@@ -61,8 +61,10 @@ typedef enum igemm_status {
     IGEMM_EHIP = -2,    /* a HIP runtime call or kernel launch failed      */
     IGEMM_ENOTSUP = -3, /* valid but unsupported (a size beyond 2^31 - 1,  */
                         /* or a grid beyond 2^24 workgroups)              */
-    IGEMM_ENOMEM = -4   /* the caller's workspace is smaller than the plan */
+    IGEMM_ENOMEM = -4,  /* the caller's workspace is smaller than the plan */
                         /* needs                                           */
+    IGEMM_ESCRATCH = -5 /* igemm_i16_noalloc: the call needs more than the */
+                        /* static scratch array holds; nothing enqueued   */
 } igemm_status;
 
 /*
@@ -178,6 +180,33 @@ int igemm_i8_ws(int64_t m, int64_t n, int64_t k,
                 const int8_t *B, int64_t ldb,
                 int32_t *C, int64_t ldc, void *stream,
                 int kernel, int split, void *workspace, int64_t workspace_bytes);
+
+/*
+ * For callers that cannot allocate device memory (code under graph capture,
+ * tight serving loops, harnesses that forbid allocation): igemm_i16_ws
+ * without a caller workspace. The packed path's workspace is a static device
+ * array inside the library, IGEMM_NOALLOC_SCRATCH_BYTES (72 MiB) on each GPU
+ * the library runs on, held from the first call on that GPU until the
+ * process ends; enough for int16 products up to 4096 x 4096 x 4096 (64.1 MiB
+ * of packed operands). Arguments, semantics and errors are those of
+ * igemm_i16_ws (kernel and split included), except:
+ *   - calls whose plan needs more scratch than the array holds return
+ *     IGEMM_ESCRATCH and enqueue nothing (pass kernel = one of the fused
+ *     int16 kernels to run such a product with no scratch at all);
+ *   - every call on one GPU uses that GPU's single array, which keeps the
+ *     last call's contents (the kernels clear what must start at zero):
+ *     calls that overlap on one GPU (concurrent streams, or threads without
+ *     ordering) RACE and give wrong results; order them on one stream.
+ * No hipMalloc, hipFree or other allocating routine is called. The first
+ * call on a device looks up the array's device address once
+ * (hipGetSymbolAddress) with that device current.
+ */
+#define IGEMM_NOALLOC_SCRATCH_BYTES ((int64_t)72 << 20)
+int igemm_i16_noalloc(int64_t m, int64_t n, int64_t k,
+                      const int16_t *A, int64_t lda,
+                      const int16_t *B, int64_t ldb,
+                      int32_t *C, int64_t ldc, void *stream,
+                      int kernel, int split);
 
 /*
  * Pack once, multiply many times. In DL inference one operand is fixed

@@ -12,6 +12,8 @@ Same names as the C ABI:
     igemm_i16_ex / igemm_i8_ex(..., kernel=-1, split=-1)
     igemm_i16_ws / igemm_i8_ws(..., kernel=-1, split=-1, workspace=None,
                                workspace_bytes=0)
+    igemm_i16_noalloc(m, n, k, A, lda, B, ldb, C, ldc, stream=None, kernel=-1,
+                      split=-1)
     igemm_pack_i16 / igemm_pack_i8(m, n, k, A, lda, B, ldb, kernel=-1,
                                    workspace, workspace_bytes, stream=None)
     igemm_i16_prepacked / igemm_i8_prepacked(m, n, k, A, lda, C, ldc, kernel=-1,
@@ -59,6 +61,8 @@ IGEMM_EINVAL = -1
 IGEMM_EHIP = -2
 IGEMM_ENOTSUP = -3
 IGEMM_ENOMEM = -4
+IGEMM_ESCRATCH = -5
+IGEMM_NOALLOC_SCRATCH_BYTES = 72 << 20
 
 
 class IgemmError(RuntimeError):
@@ -114,6 +118,8 @@ def _load():
         getattr(lib, name + "_ex").restype = ci
         getattr(lib, name + "_ws").argtypes = gemm_args + [ci, ci, vp, i64]
         getattr(lib, name + "_ws").restype = ci
+    lib.igemm_i16_noalloc.argtypes = gemm_args + [ci, ci]
+    lib.igemm_i16_noalloc.restype = ci
     for name in ("igemm_pack_i16", "igemm_pack_i8"):
         getattr(lib, name).argtypes = [i64, i64, i64, vp, i64, vp, i64, ci, vp, i64, vp]
         getattr(lib, name).restype = ci
@@ -243,6 +249,14 @@ def igemm_i8_ws(m, n, k, A, lda, B, ldb, C, ldc, stream=None, kernel=-1, split=-
                 workspace=None, workspace_bytes=0) -> int:
     return _call("igemm_i8_ws", m, n, k, A, lda, B, ldb, C, ldc, stream, int(kernel),
                  int(split), _addr(workspace), int(workspace_bytes))
+
+
+def igemm_i16_noalloc(m, n, k, A, lda, B, ldb, C, ldc, stream=None, kernel=-1,
+                      split=-1) -> int:
+    """igemm_i16_ws with the library's static scratch array as the workspace
+    (no allocation; calls that overlap on one GPU race). Returns the status."""
+    return _call("igemm_i16_noalloc", m, n, k, A, lda, B, ldb, C, ldc, stream, int(kernel),
+                 int(split))
 
 
 def igemm_pack_i16(m, n, k, A, lda, B, ldb, kernel=-1, workspace=None, workspace_bytes=0,

@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include <atomic>
+#include <mutex>
 
 #include "igemm.h"
 #include "igemm_internal.h"
@@ -32,6 +33,34 @@ int num_cu_of_current_device() {
         cu = 256;
     if (cacheable) g_num_cu[dev].store(cu, std::memory_order_relaxed);
     return cu;
+}
+
+// Scratch of igemm_i16_noalloc: one array per device, loaded with the code
+// object and kept until the process ends. In host code `scratch` names a
+// host-side stand-in, not device memory: host code uses only the device
+// address hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) unsigned char scratch[IGEMM_NOALLOC_SCRATCH_BYTES];
+
+std::mutex g_scratch_mu;                       // guards first look-ups only
+std::atomic<void *> g_scratch_ptr[kMaxDevices];
+
+// Device address of the current device's scratch array (looked up once per
+// device, with that device current), or nullptr on failure.
+void *scratch_of_current_device() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    void *p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (p != nullptr) return p;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (p == nullptr) {
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) {
+            (void)hipGetLastError();
+            return nullptr;
+        }
+        g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+    return p;
 }
 
 // The one-call workspace holds the A part, then the B part.
@@ -356,6 +385,27 @@ int igemm_i16_ws(int64_t m, int64_t n, int64_t k, const int16_t *A, int64_t lda,
                  int kernel, int split, void *workspace, int64_t workspace_bytes) {
     return igemm::run(2, m, n, k, A, lda, B, ldb, C, ldc, stream, kernel, split, workspace,
                       workspace_bytes);
+}
+
+int igemm_i16_noalloc(int64_t m, int64_t n, int64_t k, const int16_t *A, int64_t lda,
+                      const int16_t *B, int64_t ldb, int32_t *C, int64_t ldc, void *stream,
+                      int kernel, int split) {
+    // Argument errors first, before any HIP call (as igemm_i16_ws).
+    int st = igemm::validate(2, m, n, k, A, lda, B, ldb, C, ldc);
+    if (st != IGEMM_OK) return st;
+    if (m == 0 || n == 0 || k == 0) return IGEMM_OK;
+    if (kernel < -1 || kernel >= igemm::K_COUNT || split < -1 || split == 0) return IGEMM_EINVAL;
+    if (kernel >= 0 && igemm::kKernels[kernel].es != 2) return IGEMM_EINVAL;
+    igemm_plan p;
+    st = igemm::make_plan(2, m, n, k, A, lda, B, ldb, ldc, igemm::num_cu_of_current_device(),
+                          kernel, split, true, &p);
+    if (st != IGEMM_OK) return st;
+    if (p.workspace_bytes > IGEMM_NOALLOC_SCRATCH_BYTES) return IGEMM_ESCRATCH;
+    void *ws = igemm::scratch_of_current_device();
+    if (ws == nullptr) return IGEMM_EHIP;
+    // The same plan as above, with the scratch array as its workspace.
+    return igemm::run(2, m, n, k, A, lda, B, ldb, C, ldc, stream, kernel, split, ws,
+                      IGEMM_NOALLOC_SCRATCH_BYTES);
 }
 
 int igemm_i8_ws(int64_t m, int64_t n, int64_t k, const int8_t *A, int64_t lda,

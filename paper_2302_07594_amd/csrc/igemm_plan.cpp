@@ -529,7 +529,10 @@ const char *igemm_strerror(int status) {
         case IGEMM_EHIP: return "HIP runtime call or kernel launch failed";
         case IGEMM_ENOTSUP:
             return "unsupported size (a dimension exceeds 2^31 - 1 or the grid 2^24 workgroups)";
-        case IGEMM_ENOMEM: return "the workspace could not be allocated, or is too small";
+        case IGEMM_ENOMEM: return "the caller's workspace is smaller than the call needs";
+        case IGEMM_ESCRATCH:
+            return "the call needs more scratch than the library's static device array holds "
+                   "(IGEMM_NOALLOC_SCRATCH_BYTES)";
         default: return "unknown status";
     }
 }
