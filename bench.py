@@ -62,11 +62,6 @@ PEAK_I16_TOPS = PEAK_INT8_TOPS / LIMB_PRODUCTS_I16
 MALL_BYTES = 256 << 20
 MIN_CYCLED = 2 * MALL_BYTES  # bytes a memory-bound graph replay must rotate through
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_i16_packed_128x128_4096cube.json")
-CSRC = os.path.join(ROOT, "paper_2302_07594_amd", "csrc")
-# Everything the packed multiply kernel is built from.
-PACKED_SOURCES = [os.path.join(CSRC, f) for f in
-                  ("igemm_packed.hip", "igemm_device.h", "igemm_internal.h")] + \
-                 [os.path.join(ROOT, "include", "igemm.h")]
 
 
 def log(msg):
@@ -77,7 +72,7 @@ def kernel_source_hash() -> str:
     """SHA-256 over the packed kernel's source, the headers it includes and
     the library's compile flags."""
     from paper_2302_07594_amd import build as hip_build
-    return hip_build._hash_files(PACKED_SOURCES, hip_build.compile_flags())
+    return hip_build.packed_kernel_hash()
 
 
 def _summary(path):

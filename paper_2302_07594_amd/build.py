@@ -69,6 +69,19 @@ def source_hash(extra_flags=None) -> str:
     return _hash_files(sources() + headers(), compile_flags(extra_flags))
 
 
+# Everything the packed multiply kernel is built from (its source and the
+# headers it includes); with the compile flags this names one build of it.
+PACKED_KERNEL_SOURCES = [os.path.join(CSRC, f) for f in
+                         ("igemm_packed.hip", "igemm_device.h", "igemm_internal.h")] + \
+                        [os.path.join(INCLUDE, "igemm.h")]
+
+
+def packed_kernel_hash() -> str:
+    """SHA-256 of the packed kernel's sources and the compile flags: profile
+    summaries taken on one build are reported only for the same build."""
+    return _hash_files(PACKED_KERNEL_SOURCES, compile_flags())
+
+
 def is_current() -> bool:
     """True if the built library exists and was built from this tree."""
     try:

@@ -31,6 +31,8 @@ enum KernelId {
     K_I8_PACKED_256x256,
     K_I16_PACKED_128x128,
     K_I8_STREAM,
+    K_I16_DIRECT_128x128,
+    K_I8_DIRECT_256x256,
     K_COUNT
 };
 
@@ -118,6 +120,14 @@ int make_conv_plan(int es, const igemm_conv2d_desc *d, const void *X, const void
                    const void *Y, int num_cu, int kernel, int split, igemm_plan *out,
                    ConvGeom *g, int *gather);
 
+// The direct kernels (raw row-major A and B moved into LDS unchanged, no
+// workspace) apply to these arguments: 16-byte aligned operands with rows a
+// multiple of 16 bytes, k a multiple of 256 (whole groups of four k-tiles
+// per launch), n a multiple of 8 (int16) or 16 (int8) columns, and byte offsets
+// that fit the kernel's 32-bit lane offsets.
+bool direct_ok(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
+               const void *B, int64_t ldb, int64_t ldc);
+
 // Kernel launches for a validated plan (stream is a hipStream_t). The packed
 // launch needs a workspace of at least plan.workspace_bytes, 256-byte aligned.
 // The streaming kernel for few-row int8 products.
@@ -167,6 +177,10 @@ int launch_pack_a(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, 
                   int64_t lda, void *a_part, void *b_part_to_clear, void *stream);
 int launch_pack_b(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
                   int64_t lda, const void *B, int64_t ldb, void *b_part, bool clear_corr,
+                  void *stream);
+// The direct kernel: one launch per k chunk of plan.k_chunk elements.
+int launch_direct(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                  int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
                   void *stream);
 int launch_multiply(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
                     int64_t lda, int32_t *C, int64_t ldc, const void *a_part, const void *b_part,

@@ -27,6 +27,8 @@ const KernelDesc kKernels[K_COUNT] = {
     {"i8_packed_256x256", 1, 256, 256, 64, 128, true},
     {"i16_packed_128x128", 2, 128, 128, 64, 64, true},
     {"i8_stream_32x128", 1, 32, 128, 16, 128, false},
+    {"i16_direct_128x128", 2, 128, 128, 64, 64, false},
+    {"i8_direct_256x256", 1, 256, 256, 64, 128, false},
 };
 
 // Largest grid (in workgroups) of one launch: the dispatch packet counts
@@ -121,6 +123,29 @@ static bool packed_fits(int id, int64_t ldc) {
     return (int64_t)kKernels[id].bm * ldc * 4 < INT_MAX;
 }
 
+static bool is_direct(int id) { return id == K_I16_DIRECT_128x128 || id == K_I8_DIRECT_256x256; }
+
+bool direct_ok(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
+               const void *B, int64_t ldb, int64_t ldc) {
+    const int id = es == 2 ? K_I16_DIRECT_128x128 : K_I8_DIRECT_256x256;
+    const uintptr_t a = (uintptr_t)A, b = (uintptr_t)B;
+    if (a % 16 != 0 || b % 16 != 0 || (lda * es) % 16 != 0 || (ldb * es) % 16 != 0) return false;
+    // Whole groups of four k-tiles per launch (the kernel's loop has no
+    // remainder steps).
+    if (k % (4 * kBK) != 0 || n % (16 / es) != 0) return false;
+    // 32-bit lane offsets: rows of A from its base, 64 rows of B plus a column.
+    if (m * lda * es >= ((int64_t)1 << 31) || (kBK + 1) * ldb * es >= ((int64_t)1 << 31))
+        return false;
+    return packed_fits(id, ldc) && tiles_of(id, m, n) <= kMaxGrid;
+}
+
+// k elements per launch of the direct kernels: as few launches as the
+// 32768-element limit allows, split evenly in groups of four k-tiles.
+static int64_t direct_chunk(int64_t k) {
+    const int64_t launches = cdiv(k, kMaxKChunk);
+    return cdiv(k / (4 * kBK), launches) * 4 * kBK;
+}
+
 // Streaming kernel: row blocks of 16 or 32 rows, column blocks of 128, and
 // workgroups of 4 or 8 waves that each take 1, 2 or 4 k-steps of 64 (4, 8,
 // 16 or 32 steps per workgroup). Returns false if its 32-bit window offsets
@@ -173,9 +198,20 @@ static int64_t big_tile_split(int64_t tiles, int64_t k, int num_cu) {
 static int auto_kernel(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
                        const void *B, int64_t ldb, int64_t ldc, int num_cu, bool allow_packed) {
     const int pid = es == 2 ? K_I16_PACKED_128x128 : K_I8_PACKED_256x256;
-    if (allow_packed && packed_pays(es, m, n, k, num_cu) && packed_fits(pid, ldc) &&
+    // Large products: int8 takes the direct kernel whenever the operands
+    // allow it (int8 8192^3: 519 us against 566 us for pack + packed
+    // multiply, and 534 us for the packed multiply alone); int16 takes the
+    // packed path when a workspace is given (4096^3: pack 26 us + multiply
+    // 239 us against 282 us direct: the direct kernel's in-register limb
+    // split costs matrix-core issue slots) and the direct kernel otherwise
+    // (fused 128x128 tiles: 337 us).
+    const bool large = packed_pays(es, m, n, k, num_cu);
+    const bool direct = large && direct_ok(es, m, n, k, A, lda, B, ldb, ldc);
+    if (es == 1 && direct) return K_I8_DIRECT_256x256;
+    if (allow_packed && large && packed_fits(pid, ldc) &&
         16 * (k > lda ? k : lda) < ((int64_t)1 << 31))
         return pid;
+    if (direct) return K_I16_DIRECT_128x128;
     if (es == 1) {
         StreamShape ss;
         if (m <= 32 && n >= 512 && k >= 256 && (uintptr_t)B % 8 == 0 && ldb % 8 == 0 &&
@@ -236,6 +272,20 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
     const KernelDesc &d = kKernels[id];
     const int64_t tiles = tiles_of(id, m, n);
     const uintptr_t a = (uintptr_t)A, b = (uintptr_t)B;
+    if (is_direct(id)) {
+        if (!direct_ok(es, m, n, k, A, lda, B, ldb, ldc)) return IGEMM_EINVAL;
+        out->kernel = id;
+        out->bm = d.bm;
+        out->bn = d.bn;
+        out->threads = (d.bm / d.wm) * (d.bn / d.wn) * 64;
+        out->k_chunk = direct_chunk(k);
+        out->split = (int)cdiv(k, out->k_chunk);
+        out->tiles = tiles;
+        out->grid = tiles;
+        out->vec_a = 1;
+        out->vec_b = 1;
+        return IGEMM_OK;
+    }
     if (d.packed) {
         // Pack once, then one launch of the main kernel per k chunk of at most
         // kMaxKChunk elements; the launches add into C in stream order.

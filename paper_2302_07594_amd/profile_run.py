@@ -2,13 +2,14 @@
 ``rocprofv3`` can trace it, and summarize the resulting CSV files.
 
 Usage (the program itself goes after ``rocprofv3 ... --``):
-    python paper_2302_07594_amd/profile_run.py gemm <workload> [iters] [case]
+    python paper_2302_07594_amd/profile_run.py gemm <workload> [iters] [case] [kernel name]
     python paper_2302_07594_amd/profile_run.py conv <layer> [iters] [b32]
     python paper_2302_07594_amd/profile_run.py srs <workload> <kc> <shift> [iters]
     python paper_2302_07594_amd/profile_run.py copy <MiB> [iters]
     python paper_2302_07594_amd/profile_run.py summarize <rocprof output dir>
     python paper_2302_07594_amd/profile_run.py traffic <rocprof output dir> <out.json>
     python paper_2302_07594_amd/profile_run.py mfma <rocprof output dir> [out.json]
+    python paper_2302_07594_amd/profile_run.py breakdown <rocprof output dir> <kernel substring>
 
 ``gemm`` runs the library's igemm call on the named workload's case (inputs
 generated as in the benchmark, C reset is not needed for timing); ``conv``
@@ -46,7 +47,7 @@ if _ROOT not in sys.path:
     sys.path.insert(0, _ROOT)
 
 
-def _gemm(wname: str, iters: int, case_idx: int) -> None:
+def _gemm(wname: str, iters: int, case_idx: int, kernel_name: str = "") -> None:
     import torch
 
     import paper_2302_07594_amd as ig
@@ -55,8 +56,12 @@ def _gemm(wname: str, iters: int, case_idx: int) -> None:
     A, B, C = workloads.generate(case)
     Ad, Bd, Cd = (torch.from_numpy(x).cuda() for x in (A, B, C))
     f = ig.gemm_i16 if case.dtype == "i16" else ig.gemm_i8
+    kid = -1
+    if kernel_name:
+        kid = [i for i in range(ig.igemm_num_kernels())
+               if ig.igemm_kernel_name(i) == kernel_name][0]
     for _ in range(iters):
-        f(Ad, Bd, Cd)
+        f(Ad, Bd, Cd, kernel=kid)
     torch.cuda.synchronize()
     print(f"ran {case.name} x{iters}", flush=True)
 
@@ -134,10 +139,11 @@ def _counter_rows(path: str, counter: str, keep):
 
 
 def _traffic(d: str, out: str) -> None:
-    import hashlib
     import json
-    src = os.path.join(_ROOT, "paper_2302_07594_amd", "csrc", "igemm_packed.hip")
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+
+    from paper_2302_07594_amd import build as hip_build
+    sha = hip_build.packed_kernel_hash()
+
     def mult(name):
         return "igemm_packed<2, 128, 128" in name
 
@@ -224,12 +230,29 @@ def _mfma(d: str, out_json: str = "") -> None:
                          "duration_us": round(t * 1e6, 2) if t else None,
                          "clock_ghz": round(act / t / 1e9, 3) if t else None})
     if out_json:
-        import hashlib
         import json
-        src = os.path.join(_ROOT, "paper_2302_07594_amd", "csrc", "igemm_packed.hip")
+
+        from paper_2302_07594_amd import build as hip_build
         with open(out_json, "w") as f:
-            json.dump({"kernel_source_sha256": hashlib.sha256(open(src, "rb").read()).hexdigest(),
+            json.dump({"kernel_source_sha256": hip_build.packed_kernel_hash(),
                        "simds": simds, "xcc": xcc, "dispatches": rows}, f, indent=1)
+
+
+def _breakdown(d: str, match: str) -> None:
+    """Mean per dispatch of every counter found under d (any number of
+    --pmc passes, each in its own subdirectory) for the kernels whose name
+    contains `match`, summed over the GPU's blocks."""
+    per = defaultdict(lambda: defaultdict(float))
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        run = os.path.dirname(f)
+        for r in csv.DictReader(open(f)):
+            if match in r["Kernel_Name"]:
+                per[r["Counter_Name"]][(run, int(r["Dispatch_Id"]))] += float(r["Counter_Value"])
+    print(f"| counter (kernels matching `{match}`) | mean per dispatch | dispatches |")
+    print("|---|---|---|")
+    for c in sorted(per):
+        v = per[c]
+        print(f"| {c} | {sum(v.values()) / len(v):.4g} | {len(v)} |")
 
 
 def main(argv) -> None:
@@ -238,7 +261,8 @@ def main(argv) -> None:
         sys.exit(2)
     cmd = argv[1]
     if cmd == "gemm":
-        _gemm(argv[2], int(argv[3]) if len(argv) > 3 else 3, int(argv[4]) if len(argv) > 4 else 0)
+        _gemm(argv[2], int(argv[3]) if len(argv) > 3 else 3, int(argv[4]) if len(argv) > 4 else 0,
+              argv[5] if len(argv) > 5 else "")
     elif cmd == "conv":
         _conv(int(argv[2]), int(argv[3]) if len(argv) > 3 else 3,
               len(argv) > 4 and argv[4] == "b32")
@@ -250,6 +274,8 @@ def main(argv) -> None:
         _summarize(argv[2])
     elif cmd == "traffic":
         _traffic(argv[2], argv[3])
+    elif cmd == "breakdown":
+        _breakdown(argv[2], argv[3])
     elif cmd == "mfma":
         _mfma(argv[2], argv[3] if len(argv) > 3 else "")
     else:

@@ -76,3 +76,11 @@ def describe_mismatch(got, want, limit=5):
     for (i, j) in bad[:limit]:
         lines.append(f"  [{i},{j}] got {got[i, j]} want {want[i, j]}")
     return "\n".join(lines)
+
+
+def general_kernels(es):
+    """Kernel indices of the operand type that take any shape and alignment
+    (all but the direct kernels, whose preconditions have tests of their
+    own)."""
+    import paper_2302_07594_amd as ig
+    return [k for k in ig.kernels_for(es) if "direct" not in ig.igemm_kernel_name(k)]

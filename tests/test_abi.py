@@ -147,16 +147,21 @@ def test_plans_for_workloads():
             assert p["split"] >= 1 and p["k_chunk"] % 64 == 0
             assert p["split"] * p["k_chunk"] >= case.k > (p["split"] - 1) * p["k_chunk"]
             assert p["k_chunk"] <= 32768
-            if p["packed"]:
+            if p["packed"] or "direct" in p["kernel_name"]:
                 # one launch of `grid` workgroups per k chunk
-                assert p["grid"] == p["tiles"] and p["workspace_bytes"] > 0
+                assert p["grid"] == p["tiles"]
+                assert (p["workspace_bytes"] > 0) == bool(p["packed"])
             else:
                 assert p["grid"] == p["tiles"] * p["split"] and p["workspace_bytes"] == 0
             assert p["limb_products"] == (4 if es == 2 else 1)
     big = ig.igemm_query_plan(2, 4096, 4096, 4096, FAKE_A, 4096, FAKE_B, 4096, FAKE_C, 4096)
     assert big["kernel_name"] == "i16_packed_128x128" and big["split"] == 1
     big8 = ig.igemm_query_plan(1, 8192, 8192, 8192, FAKE_A, 8192, FAKE_B, 8192, FAKE_C, 8192)
-    assert big8["kernel_name"] == "i8_packed_256x256" and big8["split"] == 1
+    assert big8["kernel_name"] == "i8_direct_256x256" and big8["split"] == 1
+    assert big8["workspace_bytes"] == 0
+    # rows that are not 16-byte multiples, or k not a multiple of 256: packed
+    odd8 = ig.igemm_query_plan(1, 8192, 8192, 8200, FAKE_A, 8200, FAKE_B, 8192, FAKE_C, 8192)
+    assert odd8["kernel_name"] == "i8_packed_256x256"
     small = ig.igemm_query_plan(2, 256, 256, 256, FAKE_A, 256, FAKE_B, 256, FAKE_C, 256)
     assert not small["packed"] and small["workspace_bytes"] == 0
 

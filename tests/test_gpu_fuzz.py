@@ -15,7 +15,10 @@ def _cases(n_cases=80, seed=2024):
     import paper_2302_07594_amd as ig
     rng = np.random.default_rng(seed)
     out = []
-    kernels = list(range(ig.igemm_num_kernels()))
+    # (the direct kernels take only whole 256-element k groups and aligned
+    # operands; they have a fuzz of their own below)
+    kernels = [k for k in range(ig.igemm_num_kernels())
+               if "direct" not in ig.igemm_kernel_name(k)]
     for i in range(n_cases):
         dt = "i16" if rng.integers(0, 2) else "i8"
         es = 2 if dt == "i16" else 1
@@ -41,5 +44,39 @@ def test_fuzz_shape(case):
     A, B, C = workloads.random_operands(dt, m, n, k, seed=5000 + i, lda=k + pads[0],
                                         ldb=n + pads[1], ldc=n + pads[2])
     _, got = gpu_gemm(A, B, C, m, n, k, kernel=kid, split=split, offsets=offs)
+    want = oracle_gemm(A, B, C, m, n, k)
+    assert np.array_equal(got, want), describe_mismatch(got, want)
+
+
+def _direct_cases(n_cases=24, seed=2025):
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n_cases):
+        dt = "i16" if rng.integers(0, 2) else "i8"
+        cols = 8 if dt == "i16" else 16          # one 16-byte chunk of B or C row
+        m = int(rng.choice([1, 2, 17, 127, 128, 129, 255, 256, 257, 300, 513]))
+        n = int(rng.choice([1, 2, 7, 8, 15, 16, 17, 31, 32])) * cols
+        k = int(rng.choice([256, 512, 768, 1280, 33024]))
+        pads = tuple(int(x) for x in rng.integers(0, 3, 3) * cols)
+        out.append((i, dt, m, n, k, pads))
+    return out
+
+
+_DCASES = _direct_cases()
+
+
+@pytest.mark.parametrize("case", _DCASES, ids=[f"d{c[0]}-{c[1]}-{c[2]}x{c[3]}x{c[4]}"
+                                               for c in _DCASES])
+def test_fuzz_direct(case):
+    """The direct kernels on random m, n (whole 16-byte column chunks), k
+    (whole 256-element groups, one case beyond 32768: two launches) and
+    padded leading dimensions of whole 16-byte chunks."""
+    import paper_2302_07594_amd as ig
+    i, dt, m, n, k, pads = case
+    name = "i16_direct_128x128" if dt == "i16" else "i8_direct_256x256"
+    kid = [x for x in range(ig.igemm_num_kernels()) if ig.igemm_kernel_name(x) == name][0]
+    A, B, C = workloads.random_operands(dt, m, n, k, seed=7000 + i, lda=k + pads[0],
+                                        ldb=n + pads[1], ldc=n + pads[2])
+    _, got = gpu_gemm(A, B, C, m, n, k, kernel=kid)
     want = oracle_gemm(A, B, C, m, n, k)
     assert np.array_equal(got, want), describe_mismatch(got, want)

@@ -5,7 +5,7 @@ import numpy as np
 import pytest
 
 import workloads
-from gpu_util import describe_mismatch, gpu_gemm, oracle_gemm
+from gpu_util import describe_mismatch, general_kernels, gpu_gemm, oracle_gemm
 
 pytestmark = pytest.mark.gpu
 
@@ -33,6 +33,15 @@ def test_int16_256_cube_full():
 
 def _kernel_shapes(name):
     bm, bn = (int(x) for x in name.split("_")[-1].split("x"))
+    if "direct" in name:
+        # k a multiple of 256, n a multiple of 16 columns; m, n ragged
+        return [
+            (bm, bn, 256),                     # exactly one tile, four k-tiles
+            (bm + 3, bn + 16, 768),            # ragged m and n, several tiles
+            (2 * bm - 1, 2 * bn + 16, 512),
+            (1, bn - 16, 256),                 # one row
+            (bm - 1, 16, 1024),                # sixteen columns
+        ]
     return [
         (bm, bn, 64),                      # exactly one tile, one k-tile
         (bm + 3, bn + 5, 3 * 64 + 17),     # ragged m, n and k tails, several tiles
@@ -75,7 +84,7 @@ def test_alignment_and_padding(dt, offsets, pad):
     m, n, k = 150, 140, 200
     A, B, C = workloads.random_operands(dt, m, n, k, seed=77, lda=k + pad[0], ldb=n + pad[1],
                                         ldc=n + pad[2])
-    for kid in _ig().kernels_for(2 if dt == "i16" else 1):
+    for kid in general_kernels(2 if dt == "i16" else 1):
         got = _check(A, B, C, m, n, k, kernel=kid, offsets=offsets)
         assert np.array_equal(got[:, n:], C[:, n:])
 
@@ -203,6 +212,22 @@ def test_paper_shape_int16_full():
     case = workloads.WORKLOADS["i16_paper"].cases[0]
     A, B, C = workloads.generate(case)
     _check(A, B, C, case.m, case.n, case.k)
+
+
+@pytest.mark.parametrize("name", ["i16_direct_128x128", "i8_direct_256x256"])
+def test_direct_kernel_preconditions(name):
+    """The direct kernels take k a multiple of 256, 16-byte aligned operands
+    with rows of whole 16 bytes and n a multiple of 16 bytes of columns; an
+    explicit request outside that is refused, C untouched."""
+    ig = _ig()
+    kid = [i for i in range(ig.igemm_num_kernels()) if ig.igemm_kernel_name(i) == name][0]
+    dt = "i16" if name.startswith("i16") else "i8"
+    for (m, n, k, offs) in ((64, 64, 300, (0, 0, 0)), (64, 64, 256, (1, 0, 0)),
+                            (64, 64, 256, (0, 1, 0)), (64, 72 if dt == "i8" else 68, 256, (0, 0, 0))):
+        A, B, C = workloads.random_operands(dt, m, n, k, seed=77 + k)
+        st, got = gpu_gemm(A, B, C, m, n, k, kernel=kid, offsets=offs, check_status=False,
+                           workspace=None)
+        assert st == ig.IGEMM_EINVAL and np.array_equal(got, C), (m, n, k, offs)
 
 
 def test_int16_4096_cube_full():
