@@ -340,8 +340,12 @@ igemm_direct(const char *__restrict__ A, int64_t lda, const char *__restrict__ B
     // VALU instructions of one split: 8 v_perm_b32 and 4 xors per fragment,
     // plus 8 v_dot2 for the sums of two fragments.
     constexpr int NV = ES == 2 ? 12 * (TM + TN) + 16 : 0;
-    constexpr int VSLOTS = NM / 2;   // MFMA slots that carry the split
+    // MFMA slots that carry the split, and LDS reads per slot after them
+    // (a sweep of 8, 10, 11 and 12 split slots with 2-4 reads per slot put
+    // all within 2 % of each other on int16 4096^3; this one was fastest).
+    constexpr int VSLOTS = 12;
     constexpr int VPS = VSLOTS > 0 ? (NV + VSLOTS - 1) / VSLOTS : 0;
+    constexpr int RPS = 4;
 
     // One sub-step's MFMAs with, between them, the DMA share `dma`, the
     // split of the raw slot into operand slot NXT (int16, if SPLIT) in the
@@ -356,11 +360,17 @@ igemm_direct(const char *__restrict__ A, int64_t lda, const char *__restrict__ B
         mfmas(ic<CUR>{});
         if constexpr (SPLIT) split(ic<NXT>{}, sums_kind);
         if constexpr (READ) read_frags(ic<0>{}, rd_stage, rd_ks);
+        // Slot layout: the split runs in slots [1, 1 + VSLOTS) (slot 0 leaves
+        // the previous sub-step's reads time to land), the reads, which
+        // overwrite the raw slot the split consumes, in the slots after it,
+        // RPS per slot.
 #pragma unroll
         for (int i = 0; i < NM; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            if (SPLIT && i < VSLOTS) __builtin_amdgcn_sched_group_barrier(0x002, VPS, 0);
-            if (READ && i >= NM - NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            if (SPLIT && i >= 1 && i < 1 + VSLOTS)
+                __builtin_amdgcn_sched_group_barrier(0x002, VPS, 0);
+            if (READ && i >= 1 + VSLOTS && i < 1 + VSLOTS + (NR + RPS - 1) / RPS)
+                __builtin_amdgcn_sched_group_barrier(0x100, RPS, 0);
             if (ND > 0 && (i * ND) / NM != ((i + 1) * ND) / NM)
                 __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
         }
