@@ -232,6 +232,14 @@ block_sums(const int8_t *__restrict__ P0, const int8_t *__restrict__ P1, int64_t
 // added first when bit 8 is set) and saturation; corrA / corrB then hold the
 // exact (high, low) limb sums of the range per row / column, and kconst is
 // 16384 times the range's length.
+// EPI 2 (int16 only): the int16-output update of every k block in one launch.
+// The k range is kcb-tile blocks (kcb a multiple of 4, ktiles = nblocks kcb,
+// at most 16 blocks); corrA / corrB hold the exact (high, low) limb sums of
+// every block (block q at 2 (q m_pad + row), as block_sums writes them),
+// staged in LDS at the start; kconst is 16384 kcb 64. At the end of each
+// block the lane converts its accumulators into the block's int16
+// contribution (the conversion of EPI 1) and adds it to running sums kept in
+// registers; the accumulators restart at zero; C is read and written once.
 // RAGGED: ktiles need not be a multiple of four (at least three), so that the
 // zero padding of k to a multiple of 256 is not multiplied; otherwise it is.
 template <int ES, int BM, int BN, int WM, int WN, int NST, int EPI = 0, bool RAGGED = false>
@@ -240,7 +248,8 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
              const int8_t *__restrict__ Bp, int64_t ldb_p, int64_t b_plane,
              const uint32_t *__restrict__ corrA, const uint32_t *__restrict__ corrB,
              uint32_t kconst, int32_t *__restrict__ C, int64_t ldc,
-             int m, int n, int ktiles, int tiles_m, int tiles_n, int epi) {
+             int m, int n, int ktiles, int tiles_m, int tiles_n, int epi, int kcb = 0,
+             int m_pad = 0, int n_pad = 0) {
     constexpr int MF = 32;
     typedef Mfma<MF> M;
     typedef typename M::acc_t acc_t;
@@ -263,6 +272,8 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     constexpr int DPA = NBA / NW, DPB = NBB / NW, DPW = DPA + DPB;
     static_assert(DPW <= 15, "outstanding DMA count fits s_waitcnt");
     static_assert(EPI == 0 || ES == 2, "the int16-output update is for int16 operands");
+    static_assert(EPI != 2 || !RAGGED, "blocks of whole groups of four k-tiles");
+    constexpr int MAXB = 16;  // blocks of one EPI 2 launch
 
     // The LDS stages as separate objects, so that the compiler can tell the
     // DMA writes of one stage from the fragment reads of another.
@@ -294,6 +305,19 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     const int tm = first_m + (bid % span) % gsize;
     const int tn = (bid % span) / gsize;
     const int m0 = tm * BM, n0 = tn * BN;
+
+    // EPI 2: every block's limb sums of this tile's rows and columns, in LDS.
+    __shared__ uint2 bsA[EPI == 2 ? MAXB * BM : 1];
+    __shared__ uint2 bsB[EPI == 2 ? MAXB * BN : 1];
+    if constexpr (EPI == 2) {
+        const int nblocks = ktiles / kcb;
+        const uint2 *sa = (const uint2 *)corrA, *sb = (const uint2 *)corrB;
+        for (int x = tid; x < nblocks * BM; x += NW * 64)
+            bsA[x] = sa[(int64_t)(x / BM) * m_pad + m0 + x % BM];
+        for (int x = tid; x < nblocks * BN; x += NW * 64)
+            bsB[x] = sb[(int64_t)(x / BN) * n_pad + n0 + x % BN];
+        __syncthreads();
+    }
 
     // DMA: lane i of a 1 KB block writes LDS bytes [16i, 16i+16), i.e. row
     // r0 + i/4 of the block, physical chunk i%4, which holds logical chunk
@@ -475,15 +499,92 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     // ktiles >= NST - 1, a multiple of four unless RAGGED). The planes are
     // zero-padded to a multiple of four k-tiles, so the prologue's loads stay
     // inside them.
+    // EPI 2: this lane's running int16 sums, two per register (16-bit lanes
+    // that wrap modulo 2^16, as the update of C does), and the conversion of
+    // block q's accumulators into them.
+    typedef short s2 __attribute__((ext_vector_type(2)));
+    constexpr int RT = EPI == 2 ? TM : 1, RN = EPI == 2 ? TN : 1;
+    constexpr int RR = EPI == 2 ? M::REGS / 2 : 1;
+    s2 run16[RT][RN][RR];
+#pragma unroll
+    for (int i = 0; i < RT; ++i)
+#pragma unroll
+        for (int j = 0; j < RN; ++j)
+#pragma unroll
+            for (int r = 0; r < RR; ++r) run16[i][j][r] = s2{0, 0};
+    // The conversion runs in double precision: every term is an integer below
+    // 2^46 in magnitude (block sums below 2^30, scaled by at most 2^16), so
+    // the products by powers of two, the sums, the scaling by 2^-shift and the
+    // floor are all exact, and each double instruction costs what an int32
+    // one does on these compute units (unlike the 64-bit integer sequence).
+    auto convert = [&](int q) {
+        if constexpr (EPI == 2) {
+            const int sh = epi & 0xff;
+            const bool rnd = ((epi >> 8) & 1) != 0 && sh > 0;
+            const double scale = 1.0 / (double)((int64_t)1 << sh);
+            const double halfd = rnd ? (double)((int64_t)1 << (sh - 1)) : 0.0;
+            double cd[TN];
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const uint2 v = bsB[q * BN + wn0 + MF * j + M::out_col(lane)];
+                cd[j] = __builtin_fma((double)(int)v.x, 32768.0,
+                                      __builtin_fma((double)(int)v.y, 128.0, (double)kconst));
+            }
+            auto elems = [&](auto) {
+#pragma unroll
+                for (int i = 0; i < TM; ++i) {
+#pragma unroll
+                    for (int r2 = 0; r2 < M::REGS / 2; ++r2) {
+                        double rd[2];
+#pragma unroll
+                        for (int h = 0; h < 2; ++h) {
+                            const uint2 v =
+                                bsA[q * BM + wm0 + MF * i + M::out_row(lane, 2 * r2 + h)];
+                            rd[h] = __builtin_fma((double)(int)v.x, 32768.0,
+                                                  (double)(int)v.y * 128.0);
+                        }
+#pragma unroll
+                        for (int j = 0; j < TN; ++j) {
+                            short t16[2];
+#pragma unroll
+                            for (int h = 0; h < 2; ++h) {
+                                const int r = 2 * r2 + h;
+                                double a = (double)acc[2][i][j][r] + (rd[h] + cd[j]);
+                                a = __builtin_fma((double)acc[1][i][j][r], 256.0, a);
+                                a = __builtin_fma((double)acc[0][i][j][r], 65536.0, a);
+                                // (exact, and the identity for shift 0)
+                                a = __builtin_floor((a + halfd) * scale);
+                                a = __builtin_fmin(__builtin_fmax(a, -32768.0), 32767.0);
+                                t16[h] = (short)(int)a;
+                            }
+                            run16[i][j][r2] += s2{t16[0], t16[1]};
+                        }
+                    }
+                }
+            };
+            elems(ic<1>{});
+#pragma unroll
+            for (int a = 0; a < NACC; ++a)
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+#pragma unroll
+                        for (int r = 0; r < M::REGS; ++r) acc[a][i][j][r] = 0;
+        }
+    };
     int kt = 0;
     for (; kt <= ktiles - 2 * NST + 1; kt += NST) {
         step(ic<0>{}, kt, ic<1>{}, ic<1>{});
         step(ic<1>{}, kt + 1, ic<1>{}, ic<1>{});
         step(ic<2>{}, kt + 2, ic<1>{}, ic<1>{});
         if constexpr (NST == 4) step(ic<3>{}, kt + 3, ic<1>{}, ic<1>{});
+        if constexpr (EPI == 2)
+            if ((kt + NST) % kcb == 0) convert((kt + NST) / kcb - 1);
     }
     if constexpr (NST == 4 && !RAGGED) {
         tail(ic<4>{}, kt);
+        if constexpr (EPI == 2) convert(ktiles / kcb - 1);
     } else if constexpr (NST == 4) {
         // T = ktiles - kt lies in [3, 6] (the host passes ktiles >= 3).
         const int T = ktiles - kt;
@@ -533,7 +634,7 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     // epilogue has no branches and the compiler can count the outstanding
     // loads exactly (with a branch per element it waits for all of them
     // before every store).
-    constexpr u32 CE = EPI == 1 ? 2u : 4u;  // bytes per C element
+    constexpr u32 CE = EPI != 0 ? 2u : 4u;  // bytes per C element
     const __amdgpu_buffer_rsrc_t Crs = __builtin_amdgcn_make_buffer_rsrc(
         (char *)C + ((int64_t)m0 * ldc + n0) * CE, 0, 0x7fffffff, 0x00020000);
     const int ldc32 = (int)ldc;
@@ -579,6 +680,9 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
                     cv[BF][bb][r] = (int32_t)(int16_t)__builtin_amdgcn_raw_buffer_load_b16(
                         Crs, c_off(lr, lc), 0, 0);
                     rv[BF][bb][r] = *(const uint2 *)(corrA + 2 * (m0 + lr));
+                } else if constexpr (EPI == 2) {
+                    cv[BF][bb][r] = (int32_t)(int16_t)__builtin_amdgcn_raw_buffer_load_b16(
+                        Crs, c_off(lr, lc), 0, 0);
                 } else {
                     cv[BF][bb][r] =
                         __builtin_amdgcn_raw_buffer_load_b32(Crs, c_off(lr, lc), 0, 0);
@@ -607,6 +711,13 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
                     __builtin_amdgcn_raw_buffer_store_b16(
                         (unsigned short)(u32)(cv[BF][bb][r] + (int32_t)t), Crs, c_off(lr, lc), 0,
                         0);
+                    continue;
+                }
+                if constexpr (EPI == 2) {
+                    // the sum of every block's conversion, added modulo 2^16
+                    __builtin_amdgcn_raw_buffer_store_b16(
+                        (unsigned short)(u32)(cv[BF][bb][r] + (int)run16[i][j][r / 2][r & 1]),
+                        Crs, c_off(lr, lc), 0, 0);
                     continue;
                 }
                 u32 v;
@@ -743,8 +854,17 @@ int launch_srs_packed(const igemm_plan &p, int64_t m, int64_t n, int64_t k, int6
     const int mi = (int)m, ni = (int)n;
     const int epi = (shift & 0xff) | (round_half_up ? 0x100 : 0);
     const dim3 grid((unsigned)(tm * tn));
-    // One launch per block, in order (the update modulo 2^16 makes the order
-    // immaterial); block q spans [q kb, q kb + kb) of the planes.
+    // Two to sixteen whole blocks (k a multiple of kc): one launch that
+    // converts each block in registers and updates C once.
+    if (nblocks >= 2 && nblocks <= 16 && k % kc == 0 && L.k_pad == k) {
+        igemm_packed<2, 128, 128, 64, 64, 4, 2><<<grid, 256, 0, stream>>>(
+            Apk, L.k_pad, a_plane, Bpk, L.k_pad, b_plane, sa, sb, 16384u * (uint32_t)kc,
+            (int32_t *)C, ldc, mi, ni, (int)(k / 64), tm, tn, epi, (int)(kc / 64), (int)L.m_pad,
+            (int)L.n_pad);
+        return hipGetLastError() == hipSuccess ? IGEMM_OK : IGEMM_EHIP;
+    }
+    // Otherwise one launch per block, in order (the update modulo 2^16 makes
+    // the order immaterial); block q spans [q kb, q kb + kb) of the planes.
     for (int64_t q = 0; q < nblocks; ++q) {
         const int64_t k0 = q * kb;
         const int64_t span = L.k_pad - k0 < kb ? L.k_pad - k0 : kb;   // a multiple of 256
