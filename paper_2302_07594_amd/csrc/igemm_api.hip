@@ -102,6 +102,8 @@ int run(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, con
     if (p.kernel == K_I8_STREAM) return launch_stream(p, m, n, k, A, lda, B, ldb, C, ldc, stream);
     if (p.kernel == K_I16_DIRECT_128x128 || p.kernel == K_I8_DIRECT_256x256)
         return launch_direct(es, p, m, n, k, A, lda, B, ldb, C, ldc, stream);
+    if (p.kernel == K_I16_SMALL_64x64)
+        return launch_small(p, m, n, k, A, lda, B, ldb, C, ldc, stream);
     if (!p.packed) return launch_tiled(es, p, m, n, k, A, lda, B, ldb, C, ldc, stream);
     if (workspace_bytes < p.workspace_bytes) return IGEMM_ENOMEM;
     st = pack_both(es, p, m, n, k, A, lda, B, ldb, workspace, stream);

@@ -33,6 +33,7 @@ enum KernelId {
     K_I8_STREAM,
     K_I16_DIRECT_128x128,
     K_I8_DIRECT_256x256,
+    K_I16_SMALL_64x64,
     K_COUNT
 };
 
@@ -128,6 +129,13 @@ int make_conv_plan(int es, const igemm_conv2d_desc *d, const void *X, const void
 bool direct_ok(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
                const void *B, int64_t ldb, int64_t ldc);
 
+// The small-output int16 kernel (64 x 64 tiles, at most four k-tiles per
+// workgroup, all loads at once) applies to these arguments: 16-byte aligned
+// operands with rows a multiple of 16 bytes, k a multiple of 64, n a multiple
+// of 8, and byte offsets that fit its 32-bit lane offsets and grid.
+bool small_ok(int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, const void *B,
+              int64_t ldb, int64_t ldc);
+
 // Kernel launches for a validated plan (stream is a hipStream_t). The packed
 // launch needs a workspace of at least plan.workspace_bytes, 256-byte aligned.
 // The streaming kernel for few-row int8 products.
@@ -182,6 +190,10 @@ int launch_pack_b(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, 
 int launch_direct(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
                   int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
                   void *stream);
+// The small-output int16 kernel: one launch, k slices of plan.k_chunk.
+int launch_small(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                 int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
+                 void *stream);
 int launch_multiply(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
                     int64_t lda, int32_t *C, int64_t ldc, const void *a_part, const void *b_part,
                     void *stream);

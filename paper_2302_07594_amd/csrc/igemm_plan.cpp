@@ -29,6 +29,7 @@ const KernelDesc kKernels[K_COUNT] = {
     {"i8_stream_32x128", 1, 32, 128, 16, 128, false},
     {"i16_direct_128x128", 2, 128, 128, 64, 64, false},
     {"i8_direct_256x256", 1, 256, 256, 64, 128, false},
+    {"i16_small_64x64", 2, 64, 64, 32, 32, false},
 };
 
 // Largest grid (in workgroups) of one launch: the dispatch packet counts
@@ -139,6 +140,24 @@ bool direct_ok(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t l
     return packed_fits(id, ldc) && tiles_of(id, m, n) <= kMaxGrid;
 }
 
+// Most k-tiles one workgroup of the small-output kernel takes (its LDS holds
+// them all at once).
+static constexpr int64_t kSmallKtMax = 4;
+
+bool small_ok(int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, const void *B,
+              int64_t ldb, int64_t ldc) {
+    const uintptr_t a = (uintptr_t)A, b = (uintptr_t)B;
+    if (a % 16 != 0 || b % 16 != 0 || (lda * 2) % 16 != 0 || (ldb * 2) % 16 != 0) return false;
+    if (k % kBK != 0 || n % 8 != 0) return false;
+    // 32-bit lane offsets: rows of A from the k-tile's base, 64 rows of B plus
+    // a column, 64 rows of C; grid: column tiles, row tiles, k slices.
+    if (m * lda * 2 >= ((int64_t)1 << 31) || (kBK * ldb + n) * 2 >= ((int64_t)1 << 31) ||
+        64 * ldc * 4 >= ((int64_t)1 << 31))
+        return false;
+    return cdiv(n, 64) <= kMaxGrid && cdiv(m, 64) <= 65535 &&
+           cdiv(k / kBK, kSmallKtMax) <= 65535;
+}
+
 // k elements per launch of the direct kernels: as few launches as the
 // 32768-element limit allows, split evenly in groups of four k-tiles.
 static int64_t direct_chunk(int64_t k) {
@@ -195,6 +214,27 @@ static int64_t big_tile_split(int64_t tiles, int64_t k, int num_cu) {
     return s < 1 ? 1 : s;
 }
 
+// k-tiles per workgroup of the small-output kernel: its atomic adds into C
+// cost about as much as the extra parallelism of more k slices buys, so the
+// fewest slices that still give 128 workgroups (or one k-tile each, when
+// the product has fewer), spread evenly. Measured (us): (49, 512, 4608)
+// 5.96 with 4 k-tiles per workgroup, 6.02 with 3, 6.63 with 2, 8.92 with 1;
+// (784, 128, 1152) 5.50 / 5.63 / 6.04 / 8.01; (3136, 64, 576) 5.59 with 3
+// against 5.92 with 2; 256^3 4.17 with 1 against 4.23 with 2.
+static int64_t small_ktpw(int64_t tiles, int64_t ktiles) {
+    const int64_t want = tiles * ktiles < 128 ? tiles * ktiles : 128;
+    int64_t t = kSmallKtMax;
+    while (t > 1 && tiles * cdiv(ktiles, t) < want) --t;
+    return cdiv(ktiles, cdiv(ktiles, t));
+}
+
+// The small-output kernel takes int16 products whose whole grid, at four
+// k-tiles per workgroup, fits in two workgroups per compute unit.
+static bool small_pays(int64_t m, int64_t n, int64_t k, int num_cu) {
+    const int64_t tiles = cdiv(m, 64) * cdiv(n, 64);
+    return tiles * cdiv(cdiv(k, kBK), kSmallKtMax) <= 2 * (int64_t)num_cu;
+}
+
 static int auto_kernel(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
                        const void *B, int64_t ldb, int64_t ldc, int num_cu, bool allow_packed) {
     const int pid = es == 2 ? K_I16_PACKED_128x128 : K_I8_PACKED_256x256;
@@ -212,6 +252,9 @@ static int auto_kernel(int es, int64_t m, int64_t n, int64_t k, const void *A, i
         16 * (k > lda ? k : lda) < ((int64_t)1 << 31))
         return pid;
     if (direct) return K_I16_DIRECT_128x128;
+    if (es == 2 && !large && small_pays(m, n, k, num_cu) &&
+        small_ok(m, n, k, A, lda, B, ldb, ldc))
+        return K_I16_SMALL_64x64;
     if (es == 1) {
         StreamShape ss;
         if (m <= 32 && n >= 512 && k >= 256 && (uintptr_t)B % 8 == 0 && ldb % 8 == 0 &&
@@ -282,6 +325,26 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
         out->split = (int)cdiv(k, out->k_chunk);
         out->tiles = tiles;
         out->grid = tiles;
+        out->vec_a = 1;
+        out->vec_b = 1;
+        return IGEMM_OK;
+    }
+    if (id == K_I16_SMALL_64x64) {
+        if (!small_ok(m, n, k, A, lda, B, ldb, ldc)) return IGEMM_EINVAL;
+        // k-tiles per workgroup: an explicit split asks for that many slices
+        // (at least k / 256 of them: a workgroup takes at most four k-tiles).
+        const int64_t ktiles = k / kBK;
+        int64_t ktpw = split > 0 ? cdiv(ktiles, split) : small_ktpw(tiles, ktiles);
+        if (ktpw > kSmallKtMax) ktpw = kSmallKtMax;
+        if (ktpw < 1) ktpw = 1;
+        out->kernel = id;
+        out->bm = d.bm;
+        out->bn = d.bn;
+        out->threads = 256;
+        out->k_chunk = ktpw * kBK;
+        out->split = (int)cdiv(ktiles, ktpw);
+        out->tiles = tiles;
+        out->grid = tiles * out->split;
         out->vec_a = 1;
         out->vec_b = 1;
         return IGEMM_OK;

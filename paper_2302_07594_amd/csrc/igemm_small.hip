@@ -1,0 +1,300 @@
+// Small-output int16 kernel: C += A B for products whose output is too small
+// to occupy the chip with whole-k tiles -- the lowered convolution layers
+// with one large and two small dimensions (Sec. 2, Sec. 4.2), e.g. m = 49 to
+// 3136 output pixels, n = 64 to 512 channels, k = 64 to 4608.
+//
+// Such a product is bound neither by the matrix cores nor by HBM: a few MB
+// move and the work spreads over a few hundred workgroups, so the time is
+// the launch plus each workgroup's latency chain. This kernel keeps that
+// chain to one memory round trip in, one multiply pass and one write:
+//   * each workgroup owns a 64 x 64 tile of C and a range of at most KTMAX
+//     k-tiles of 64 (the k range is sliced across workgroups, gridDim.z);
+//   * it issues every load at once: all its k-tiles of A and B move global
+//     -> LDS unchanged by DMA (global_load_lds_dwordx4), and, when it is the
+//     only slice, its C tile into registers alongside;
+//   * after one wait it multiplies out of LDS: A fragments with
+//     ds_read_b128, B fragments with transpose reads, each int16 element
+//     split into its high and offset-low int8 limbs in registers, four
+//     v_mfma_i32_32x32x32_i8 per 32 k (wave tile 32 x 32);
+//   * the epilogue adds the limb corrections of its own k range (exact row
+//     sums of A and column sums of B, from the raw fragments) and updates C
+//     modulo 2^32: read-add-write from the prefetched values, or 32-bit
+//     atomic adds when k is sliced.
+// Exactness (Sec. 4.1 definition, int16 limb identity): with h = x >> 8 and
+// l' = (x & 255) - 128,
+//   sum_p x_p y_p = 65536 S_hh + 256 (S_hl' + S_l'h) + S_l'l'
+//                   + 128 sum_p x_p + 128 sum_p y_p - 16384 k     (mod 2^32),
+// summed per slice; the partial sums of at most 256 k never overflow.
+//
+// Preconditions (checked by the planner): A and B 16-byte aligned, rows a
+// multiple of 16 bytes, k a multiple of 64, n a multiple of 8, and 32-bit
+// byte offsets within one k-tile of each operand and within a C tile.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "igemm.h"
+#include "igemm_device.h"
+#include "igemm_internal.h"
+#include "igemm_lds.h"
+
+namespace igemm {
+namespace small {
+
+using namespace lds;
+
+constexpr int BM = 64, BN = 64;
+constexpr int RA = 128;               // LDS bytes of one A row per k-tile (64 int16)
+constexpr int RB = 128;               // LDS bytes of one B row (64 int16 columns)
+constexpr int APL = BM * RA;          // 8 KB
+constexpr int BPL = 64 * RB;          // 8 KB
+constexpr int STAGE = APL + BPL;      // one k-tile of A and B
+
+// 16-byte chunk c of LDS row r sits at c ^ swz(r). A: the fragment reads (16
+// consecutive rows at one chunk per LDS cycle) cover 16 distinct 16-byte bank
+// groups. B: a transpose read takes 4 consecutive k rows x 64 bytes for 32
+// lanes; rows 2 apart share banks, so rows with bit 1 set move to the other
+// half of their 128 bytes, and the 4 rows cover all 64 banks.
+__device__ __forceinline__ int swz_a(int row) { return (row >> 1) & 7; }
+__device__ __forceinline__ int swz_b(int row) { return 4 * ((row >> 1) & 1); }
+
+// KT: k-tiles per workgroup (the last k slice may hold fewer).
+template <int KT, bool SPLIT>
+__global__ void __launch_bounds__(256, 2)
+igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict__ B,
+                int64_t ldb, int32_t *__restrict__ C, int64_t ldc, int m, int n, int ktiles) {
+    typedef Mfma<32> M;
+    typedef M::acc_t acc_t;
+    static_assert(KT >= 1 && KT <= 4, "at most four k-tiles in LDS");
+    // One LDS array per k-tile: the compiler tells the DMA into each apart
+    // and waits only for the one a read needs.
+    __shared__ __attribute__((aligned(16))) char st0[STAGE];
+    __shared__ __attribute__((aligned(16))) char st1[KT > 1 ? STAGE : 16];
+    __shared__ __attribute__((aligned(16))) char st2[KT > 2 ? STAGE : 16];
+    __shared__ __attribute__((aligned(16))) char st3[KT > 3 ? STAGE : 16];
+    auto stage = [&](int kt) -> char * {
+        return kt == 0 ? st0 : kt == 1 ? st1 : kt == 2 ? st2 : st3;
+    };
+    __shared__ u32 sums[BM + BN];
+
+    // Every kernel argument is named up front so that their loads issue together.
+    asm volatile("" ::"s"(A), "s"(lda), "s"(B), "s"(ldb), "s"(C), "s"(ldc), "s"(m), "s"(n),
+                 "s"(ktiles));
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm0 = (wave >> 1) * 32, wn0 = (wave & 1) * 32;
+    const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
+    const int kt0 = blockIdx.z * KT;
+    const int nkt = min(ktiles - kt0, KT);  // >= 1 (planner)
+
+    // ---- every load, issued at once (below, before the multiply) -------------
+    // Per k-tile each wave moves two 1 KB blocks of A (8 rows of 128 bytes
+    // each) and two of B (8 k rows of 128 bytes). Lane i of a block writes LDS
+    // bytes [16 i, 16 i + 16): row i / 8, physical chunk i % 8, and fetches the
+    // logical chunk that the swizzle puts there. Rows of A beyond m read row
+    // m - 1 and column chunks of B beyond n read the last chunk; their
+    // products only reach outputs that are never written.
+    u32 off[4];
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+        const int b = 2 * wave + (d & 1);
+        const int row = 8 * b + lane / 8, pc = lane % 8;
+        if (d < 2) {
+            const int grow = min(m0 + row, m - 1);
+            off[d] = (u32)grow * (u32)(lda * 2) + 16u * (u32)(pc ^ swz_a(row));
+        } else {
+            const int col = min(n0 + 8 * (pc ^ swz_b(row)), n - 8);
+            off[d] = (u32)row * (u32)(ldb * 2) + 2u * (u32)col;
+        }
+    }
+    // Every one of the KT tiles is moved, a short last slice repeating its
+    // last tile (read, never multiplied), so that the waits below are fixed
+    // counts.
+    const int64_t b_step = 64 * ldb * 2;
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) {
+        const int64_t t = kt0 + min(kt, nkt - 1);
+        // Opaque scalar bases: the loads take a scalar base and a 32-bit lane
+        // offset instead of 64-bit vector addresses.
+        const char *ak = A + t * 128;
+        const char *bk = B + t * b_step;
+        asm volatile("" : "+s"(ak), "+s"(bk));
+        char *st = stage(kt);
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+            u32 o = off[d];
+            asm volatile("" : "+v"(o));
+            const int b = 2 * wave + (d & 1);
+            dma16((d < 2 ? ak : bk) + o, (lds_void *)(st + (d < 2 ? 0 : APL) + b * 1024));
+        }
+    }
+    // Nothing below moves above the loads: the address arithmetic of the
+    // rest of the kernel would otherwise delay them.
+    __builtin_amdgcn_sched_barrier(0);
+    // C tile: a buffer resource at the tile's corner; elements outside C get
+    // an offset beyond the range (loads return zero, stores are dropped).
+    // Without k slices C is prefetched right behind the DMA.
+    const __amdgpu_buffer_rsrc_t Crs = __builtin_amdgcn_make_buffer_rsrc(
+        (char *)C + ((int64_t)m0 * ldc + n0) * 4, 0, 0x7fffffff, 0x00020000);
+    const int ldc32 = (int)ldc;
+    const int ocol = wn0 + M::out_col(lane);
+    u32 coff[M::REGS];
+#pragma unroll
+    for (int r = 0; r < M::REGS; ++r) {
+        const int orow = wm0 + M::out_row(lane, r);
+        coff[r] = (m0 + orow < m && n0 + ocol < n) ? (u32)(orow * ldc32 + ocol) * 4u
+                                                    : 0x80000000u;
+    }
+    int32_t cv[SPLIT ? 1 : M::REGS];
+    if constexpr (!SPLIT) {
+#pragma unroll
+        for (int r = 0; r < M::REGS; ++r)
+            cv[r] = __builtin_amdgcn_raw_buffer_load_b32(Crs, coff[r], 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    constexpr int NC = SPLIT ? 0 : M::REGS;  // loads issued after the DMA
+
+    // ---- multiply -----------------------------------------------------------
+    // A: lane row fr = lane % 32, k chunk q = 2 ks + lane / 32 of 16 elements
+    // (32 bytes: two ds_read_b128). B: group g = lane / 16 covers columns
+    // 16 (g % 2) + [0, 16) of the wave's 32 and k chunk 2 ks + g / 2; lane
+    // u = lane % 16 addresses k row 16 q + 4 r + u / 4 at columns 4 (u % 4).
+    const int fr = lane & 31, g = lane >> 4, u = lane & 15;
+    int a_rd[2][2], b_rd[2];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+        const int q = 2 * ks + (lane >> 5);
+        const int row = wm0 + fr;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) a_rd[ks][h] = row * RA + 16 * ((2 * q + h) ^ swz_a(row));
+        const int qb = 2 * ks + (g >> 1);
+        const int col = wn0 + 16 * (g & 1) + 4 * (u & 3);
+        const int krow = 16 * qb + (u >> 2);
+        b_rd[ks] = APL + krow * RB + 16 * ((col >> 3) ^ swz_b(krow)) + 2 * (col & 7);
+    }
+    // Four accumulator sets (hh, hl', l'h, l'l'): no two consecutive matrix
+    // instructions of a sub-step depend on each other.
+    acc_t acc[4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int r = 0; r < M::REGS; ++r) acc[a][r] = 0;
+    int rsum = 0, csum = 0;  // raw sums: row fr of A, column (lane % 32) of B
+    // One k-tile from LDS: raw fragments of both sub-steps (32 k each), limb
+    // split, the four limb products, and the raw sums.
+    auto tile = [&](const char *st) {
+        u32 ra[2][8], rb[2][8];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const v4i x = *(const v4i *)(st + a_rd[ks][h]);
+                ra[ks][4 * h] = (u32)x.x;
+                ra[ks][4 * h + 1] = (u32)x.y;
+                ra[ks][4 * h + 2] = (u32)x.z;
+                ra[ks][4 * h + 3] = (u32)x.w;
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const v2i y = tr16(st + b_rd[ks] + r * 4 * RB);
+                rb[ks][2 * r] = (u32)y.x;
+                rb[ks][2 * r + 1] = (u32)y.y;
+            }
+        }
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const u32 *a = ra[ks], *b = rb[ks];
+            const v4i ah = v4(hi4(a[1], a[0]), hi4(a[3], a[2]), hi4(a[5], a[4]), hi4(a[7], a[6]));
+            const v4i al = v4(lo4(a[1], a[0]), lo4(a[3], a[2]), lo4(a[5], a[4]), lo4(a[7], a[6]));
+            const v4i bh = v4(hi4(b[1], b[0]), hi4(b[3], b[2]), hi4(b[5], b[4]), hi4(b[7], b[6]));
+            const v4i bl = v4(lo4(b[1], b[0]), lo4(b[3], b[2]), lo4(b[5], b[4]), lo4(b[7], b[6]));
+            acc[0] = M::mma(ah, bh, acc[0]);
+            acc[1] = M::mma(ah, bl, acc[1]);
+            acc[2] = M::mma(al, bh, acc[2]);
+            acc[3] = M::mma(al, bl, acc[3]);
+#pragma unroll
+            for (int x = 0; x < 8; ++x) {
+                rsum = sum2(a[x], rsum);
+                csum = sum2(b[x], csum);
+            }
+        }
+    };
+    // Loads complete in order: tile kt has landed once at most (KT - 1 - kt)
+    // DMA groups of four and the C loads remain outstanding, so each tile is
+    // multiplied as soon as every wave's share of it is in LDS.
+    auto wait_vm = [](auto cnt) {
+        constexpr int N = decltype(cnt)::value;
+        __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
+    };
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) {
+        if (kt == 0) wait_vm(ic<4 * (KT - 1) + NC>{});
+        if (kt == 1) wait_vm(ic<4 * (KT > 2 ? KT - 2 : 0) + NC>{});
+        if (kt == 2) wait_vm(ic<4 * (KT > 3 ? KT - 3 : 0) + NC>{});
+        if (kt == 3) wait_vm(ic<NC>{});
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");  // no LDS read moves above the wait
+        if (kt < nkt) tile(stage(kt));
+    }
+
+    // ---- epilogue -----------------------------------------------------------
+    // Lanes l and l + 32 hold complementary k chunks of the same row and
+    // column. The waves of wave column 0 publish the row sums of their 32
+    // rows, those of wave row 0 the column sums of their 32 columns.
+    {
+        const u32 rs = 128u * (u32)(rsum + __shfl_xor(rsum, 32));
+        const u32 cs = 128u * (u32)(csum + __shfl_xor(csum, 32));
+        if (lane < 32) {
+            if (wn0 == 0) sums[wm0 + lane] = rs;
+            if (wm0 == 0) sums[BM + wn0 + lane] = cs;
+        }
+    }
+    __syncthreads();
+    const u32 colt = (0u - 16384u * (u32)(64 * nkt)) + sums[BM + ocol];
+#pragma unroll
+    for (int r = 0; r < M::REGS; ++r) {
+        const u32 v = 65536u * (u32)acc[0][r] + 256u * ((u32)acc[1][r] + (u32)acc[2][r]) +
+                      (u32)acc[3][r] + colt + sums[wm0 + M::out_row(lane, r)];
+        if constexpr (SPLIT)
+            __builtin_amdgcn_raw_ptr_buffer_atomic_add_i32((int)v, Crs, (int)coff[r], 0, 0);
+        else
+            __builtin_amdgcn_raw_buffer_store_b32((int)((u32)cv[r] + v), Crs, coff[r], 0, 0);
+    }
+}
+
+}  // namespace small
+
+using namespace small;
+
+// One launch: grid (column tiles, row tiles, k slices of plan.k_chunk).
+template <int KT>
+static void launch_kt(dim3 grid, bool split, hipStream_t s, const char *A, int64_t lda,
+                      const char *B, int64_t ldb, int32_t *C, int64_t ldc, int m, int n,
+                      int ktiles) {
+    if (split)
+        igemm_small_i16<KT, true><<<grid, 256, 0, s>>>(A, lda, B, ldb, C, ldc, m, n, ktiles);
+    else
+        igemm_small_i16<KT, false><<<grid, 256, 0, s>>>(A, lda, B, ldb, C, ldc, m, n, ktiles);
+}
+
+int launch_small(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                 int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
+                 void *stream) {
+    const int64_t ktiles = k / 64, ktpw = p.k_chunk / 64;
+    if (k % 64 != 0 || ktpw < 1 || ktpw > 4) return IGEMM_EINVAL;  // the planner prevents it
+    const int64_t slices = (ktiles + ktpw - 1) / ktpw;
+    const dim3 grid((unsigned)((n + BN - 1) / BN), (unsigned)((m + BM - 1) / BM),
+                    (unsigned)slices);
+    const char *a = (const char *)A, *b = (const char *)B;
+    hipStream_t s = (hipStream_t)stream;
+    const bool split = slices > 1;
+    const int mi = (int)m, ni = (int)n, kti = (int)ktiles;
+    switch (ktpw) {
+        case 1: launch_kt<1>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti); break;
+        case 2: launch_kt<2>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti); break;
+        case 3: launch_kt<3>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti); break;
+        default: launch_kt<4>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti); break;
+    }
+    return hipGetLastError() == hipSuccess ? IGEMM_OK : IGEMM_EHIP;
+}
+
+}  // namespace igemm

@@ -164,6 +164,18 @@ def test_plans_for_workloads():
     assert odd8["kernel_name"] == "i8_packed_256x256"
     small = ig.igemm_query_plan(2, 256, 256, 256, FAKE_A, 256, FAKE_B, 256, FAKE_C, 256)
     assert not small["packed"] and small["workspace_bytes"] == 0
+    # small int16 outputs with aligned rows and whole k-tiles: the small-output
+    # kernel, at most four k-tiles per workgroup, slices spread evenly
+    for (m, n, k, kt) in ((3136, 64, 576, 3), (3136, 256, 64, 1), (784, 128, 1152, 4),
+                          (196, 256, 2304, 4), (49, 512, 4608, 4), (256, 256, 256, 1)):
+        p = ig.igemm_query_plan(2, m, n, k, FAKE_A, k, FAKE_B, n, FAKE_C, n)
+        assert p["kernel_name"] == "i16_small_64x64", (m, n, k)
+        assert p["k_chunk"] == 64 * kt and p["split"] == -(-k // p["k_chunk"])
+        assert p["grid"] == p["tiles"] * p["split"] and p["threads"] == 256
+    # k not a multiple of 64, or rows not whole 16 bytes: not the small kernel
+    for (k, lda) in ((147, 147), (576, 577)):
+        p = ig.igemm_query_plan(2, 3136, 64, k, FAKE_A, lda, FAKE_B, 64, FAKE_C, 64)
+        assert p["kernel_name"] != "i16_small_64x64"
 
 
 def test_plan_alignment_and_split_rules():
@@ -539,16 +551,19 @@ def test_srs_noop_and_unsupported(fn):
 
 
 def test_planner_rules_for_small_int16_outputs():
-    """The measured rules for small int16 products on a 256-unit device: k
-    slices of the 64x64 tiles keep two k-tiles each with the count rounded
-    up; one k-tile outputs whose 64x64 tiles leave units idle take 16-row
-    tiles; convolutions follow the same rules."""
-    def plan(m, n, k):
-        p = ig.igemm_query_plan(2, m, n, k, num_cu=256)
+    """The measured rules for small int16 products on a 256-unit device:
+    aligned operands with whole k-tiles take the small-output kernel; for the
+    fused kernels (here: rows of A not a whole number of 16 bytes), k slices
+    of the 64x64 tiles keep two k-tiles each with the count rounded up, and
+    one k-tile outputs whose 64x64 tiles leave units idle take 16-row tiles;
+    convolutions follow the fused rules."""
+    def plan(m, n, k, lda=None):
+        p = ig.igemm_query_plan(2, m, n, k, FAKE_A, lda or k, FAKE_B, n, FAKE_C, n, num_cu=256)
         return ig.igemm_kernel_name(p["kernel"]), p["split"], p["k_chunk"]
-    assert plan(3136, 64, 576) == ("i16_64x64", 5, 128)
+    assert plan(3136, 64, 576) == ("i16_small_64x64", 3, 192)
+    assert plan(3136, 64, 576, lda=577) == ("i16_64x64", 5, 128)
     assert plan(12544, 64, 147) == ("i16_64x64", 2, 128)
-    assert plan(3136, 256, 64)[0] == "i16_16x128"
+    assert plan(3136, 256, 64, lda=65)[0] == "i16_16x128"
     assert plan(100352, 256, 64)[0] == "i16_64x64"      # enough 64x64 tiles to fill the units
     d = ig.conv_desc(1, 56, 56, 64, 256, 1, 1)
     p = ig.igemm_conv2d_query_plan(2, d, num_cu=256)

@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 import workloads
-from gpu_util import describe_mismatch, gpu_gemm, oracle_gemm
+from gpu_util import describe_mismatch, gpu_gemm, oracle_gemm, restricted
 
 pytestmark = pytest.mark.gpu
 
@@ -15,10 +15,10 @@ def _cases(n_cases=80, seed=2024):
     import paper_2302_07594_amd as ig
     rng = np.random.default_rng(seed)
     out = []
-    # (the direct kernels take only whole 256-element k groups and aligned
-    # operands; they have a fuzz of their own below)
+    # (the direct and small-output kernels take only whole k groups and
+    # aligned operands; they have fuzzes of their own below)
     kernels = [k for k in range(ig.igemm_num_kernels())
-               if "direct" not in ig.igemm_kernel_name(k)]
+               if not restricted(ig.igemm_kernel_name(k))]
     for i in range(n_cases):
         dt = "i16" if rng.integers(0, 2) else "i8"
         es = 2 if dt == "i16" else 1
@@ -78,5 +78,40 @@ def test_fuzz_direct(case):
     A, B, C = workloads.random_operands(dt, m, n, k, seed=7000 + i, lda=k + pads[0],
                                         ldb=n + pads[1], ldc=n + pads[2])
     _, got = gpu_gemm(A, B, C, m, n, k, kernel=kid)
+    want = oracle_gemm(A, B, C, m, n, k)
+    assert np.array_equal(got, want), describe_mismatch(got, want)
+
+
+def _small_cases(n_cases=40, seed=2026):
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n_cases):
+        m = int(rng.choice([1, 2, 49, 63, 64, 65, 127, 196, 200, 300, 784]))
+        n = int(rng.choice([1, 2, 7, 8, 9, 16, 32, 64])) * 8
+        k = int(rng.choice([1, 2, 3, 4, 5, 7, 9, 18, 36, 72])) * 64
+        split = int(rng.choice([-1, -1, 1, 2, 3, 7, 100]))
+        pads = tuple(int(x) for x in rng.integers(0, 3, 3) * 8)
+        out.append((i, m, n, k, split, pads))
+    return out
+
+
+_SCASES = _small_cases()
+
+
+@pytest.mark.parametrize("case", _SCASES, ids=[f"s{c[0]}-{c[1]}x{c[2]}x{c[3]}-s{c[4]}"
+                                               for c in _SCASES])
+def test_fuzz_small(case):
+    """The small-output int16 kernel on random m, n (whole 16-byte column
+    chunks), k (whole k-tiles, 1 to 72), k slice requests (a workgroup
+    takes at most four k-tiles, so a request of too few slices gets more;
+    a short last slice repeats its last tile without multiplying it) and
+    padded leading dimensions of whole 16-byte chunks."""
+    import paper_2302_07594_amd as ig
+    i, m, n, k, split, pads = case
+    kid = [x for x in range(ig.igemm_num_kernels())
+           if ig.igemm_kernel_name(x) == "i16_small_64x64"][0]
+    A, B, C = workloads.random_operands("i16", m, n, k, seed=9000 + i, lda=k + pads[0],
+                                        ldb=n + pads[1], ldc=n + pads[2])
+    _, got = gpu_gemm(A, B, C, m, n, k, kernel=kid, split=split)
     want = oracle_gemm(A, B, C, m, n, k)
     assert np.array_equal(got, want), describe_mismatch(got, want)

@@ -33,6 +33,15 @@ def test_int16_256_cube_full():
 
 def _kernel_shapes(name):
     bm, bn = (int(x) for x in name.split("_")[-1].split("x"))
+    if "small" in name:
+        # k a multiple of 64, n a multiple of 8 columns; m, n ragged
+        return [
+            (bm, bn, 64),                      # exactly one tile, one k-tile
+            (bm + 3, bn + 8, 320),             # ragged m and n, five k-tiles
+            (2 * bm - 1, 2 * bn + 8, 1024),    # several tiles, k sliced
+            (1, bn - 8, 64 * 9),               # one row, a short last slice
+            (bm - 1, 8, 256),                  # eight columns
+        ]
     if "direct" in name:
         # k a multiple of 256, n a multiple of 16 columns; m, n ragged
         return [
@@ -214,15 +223,17 @@ def test_paper_shape_int16_full():
     _check(A, B, C, case.m, case.n, case.k)
 
 
-@pytest.mark.parametrize("name", ["i16_direct_128x128", "i8_direct_256x256"])
+@pytest.mark.parametrize("name", ["i16_direct_128x128", "i8_direct_256x256", "i16_small_64x64"])
 def test_direct_kernel_preconditions(name):
-    """The direct kernels take k a multiple of 256, 16-byte aligned operands
-    with rows of whole 16 bytes and n a multiple of 16 bytes of columns; an
-    explicit request outside that is refused, C untouched."""
+    """The direct kernels take k a multiple of 256 (the small-output kernel:
+    of 64), 16-byte aligned operands with rows of whole 16 bytes and n a
+    multiple of 16 bytes of columns; an explicit request outside that is
+    refused, C untouched."""
     ig = _ig()
     kid = [i for i in range(ig.igemm_num_kernels()) if ig.igemm_kernel_name(i) == name][0]
     dt = "i16" if name.startswith("i16") else "i8"
-    for (m, n, k, offs) in ((64, 64, 300, (0, 0, 0)), (64, 64, 256, (1, 0, 0)),
+    for (m, n, k, offs) in ((64, 64, 300 if "direct" in name else 100, (0, 0, 0)),
+                            (64, 64, 256, (1, 0, 0)),
                             (64, 64, 256, (0, 1, 0)), (64, 72 if dt == "i8" else 68, 256, (0, 0, 0))):
         A, B, C = workloads.random_operands(dt, m, n, k, seed=77 + k)
         st, got = gpu_gemm(A, B, C, m, n, k, kernel=kid, offsets=offs, check_status=False,
