@@ -61,48 +61,52 @@ LIMB_PRODUCTS_I16 = 4        # int8 products per int16 multiply-add
 PEAK_I16_TOPS = PEAK_INT8_TOPS / LIMB_PRODUCTS_I16
 MALL_BYTES = 256 << 20
 MIN_CYCLED = 2 * MALL_BYTES  # bytes a memory-bound graph replay must rotate through
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_i16_packed_128x128_4096cube.json")
+# Committed rocprofv3 counter summaries (paper_2302_07594_amd/profile_run.py
+# traffic / mfma), per kernel family: (family whose source hash they carry,
+# traffic file, matrix-core file).
+SUMMARIES = {
+    "i16": ("packed", os.path.join(ROOT, "profiles", "traffic_i16_packed_128x128_4096cube.json"),
+            os.path.join(ROOT, "profiles", "mfma_i16_packed_128x128_4096cube.json")),
+    "i8": ("direct", os.path.join(ROOT, "profiles", "traffic_i8_direct_256x256_8192cube.json"),
+           os.path.join(ROOT, "profiles", "mfma_i8_direct_256x256_8192cube.json")),
+}
 
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash() -> str:
-    """SHA-256 over the packed kernel's source, the headers it includes and
+def kernel_source_hash(family) -> str:
+    """SHA-256 over a kernel family's sources, the headers they include and
     the library's compile flags."""
     from paper_2302_07594_amd import build as hip_build
-    return hip_build.packed_kernel_hash()
+    return hip_build.kernel_hash(family)
 
 
-def _summary(path):
+def _summary(path, family):
     try:
         with open(path) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    return t if t.get("kernel_source_sha256") == kernel_source_hash() else None
+    return t if t.get("kernel_source_sha256") == kernel_source_hash(family) else None
 
 
-def measured_traffic():
+def measured_traffic(dtype):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if
     it was taken on the current kernel sources and flags; otherwise None."""
-    t = _summary(TRAFFIC_FILE)
+    family, path, _ = SUMMARIES[dtype]
+    t = _summary(path, family)
     return None if t is None else t.get("traffic_bytes_per_launch")
 
 
-MFMA_FILES = {
-    "i16": os.path.join(ROOT, "profiles", "mfma_i16_packed_128x128_4096cube.json"),
-    "i8": os.path.join(ROOT, "profiles", "mfma_i8_packed_256x256_8192cube.json"),
-}
-
-
 def measured_mfma(dtype):
-    """Matrix-core figures of the packed multiply from the committed
+    """Matrix-core figures of the multiply kernel from the committed
     rocprofv3 counter summary (SQ_VALU_MFMA_BUSY_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_I8,
     GRBM_GUI_ACTIVE with a kernel trace), if taken on the current kernel
     sources and flags; otherwise None."""
-    t = _summary(MFMA_FILES[dtype])
+    family, _, path = SUMMARIES[dtype]
+    t = _summary(path, family)
     if t is None or not t.get("dispatches"):
         return None
     rows = t["dispatches"]
@@ -111,7 +115,7 @@ def measured_mfma(dtype):
         "mfma_busy": round(avg("mfma_busy"), 4),
         "int8_mfma_ops_per_launch": rows[0]["int8_mfma_ops"],
         "clock_ghz": round(avg("clock_ghz"), 3),
-        "source": os.path.relpath(MFMA_FILES[dtype], ROOT),
+        "source": os.path.relpath(path, ROOT),
     }
 
 
@@ -262,6 +266,9 @@ def bench_gemm(case, olog, details):
         mf = measured_mfma("i8")
         if mf is not None:
             e["mfma_busy"], e["clk_ghz"] = mf["mfma_busy"], mf["clock_ghz"]
+        tr = measured_traffic("i8")
+        if tr is not None:
+            e["hbm_MB"] = round(tr / 1e6, 1)   # counter-measured bytes per launch
     details.append({"name": case.name, "m": m, "n": n, "k": k, "plan": plan, "sets": nsets,
                     **e})
     return e
@@ -451,7 +458,7 @@ def main():
         },
         "roofline": {
             "bound": "mfma", "achieved": round(ach, 1), "peak": PEAK_I16_TOPS, "unit": "TOPS",
-            "frac": round(ach / PEAK_I16_TOPS, 4), "traffic": measured_traffic(),
+            "frac": round(ach / PEAK_I16_TOPS, 4), "traffic": measured_traffic("i16"),
             "kernel": "igemm_packed<int16,128x128> multiply, on packed operands",
             "peak_basis": "5000 TOPS int8 MFMA / 4 limb products",
             "kernel_us": round(mult * 1e6, 2), "pack_us": round(pack_t * 1e6, 2),

@@ -82,6 +82,21 @@ def packed_kernel_hash() -> str:
     return _hash_files(PACKED_KERNEL_SOURCES, compile_flags())
 
 
+# The same for the direct kernels (igemm_direct.hip and its headers).
+DIRECT_KERNEL_SOURCES = [os.path.join(CSRC, f) for f in
+                         ("igemm_direct.hip", "igemm_lds.h", "igemm_device.h",
+                          "igemm_internal.h")] + [os.path.join(INCLUDE, "igemm.h")]
+
+
+def direct_kernel_hash() -> str:
+    return _hash_files(DIRECT_KERNEL_SOURCES, compile_flags())
+
+
+def kernel_hash(family: str) -> str:
+    """Hash of one kernel family's build: "packed" or "direct"."""
+    return {"packed": packed_kernel_hash, "direct": direct_kernel_hash}[family]()
+
+
 def is_current() -> bool:
     """True if the built library exists and was built from this tree."""
     try:

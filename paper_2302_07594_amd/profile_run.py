@@ -7,8 +7,8 @@ Usage (the program itself goes after ``rocprofv3 ... --``):
     python paper_2302_07594_amd/profile_run.py srs <workload> <kc> <shift> [iters]
     python paper_2302_07594_amd/profile_run.py copy <MiB> [iters]
     python paper_2302_07594_amd/profile_run.py summarize <rocprof output dir>
-    python paper_2302_07594_amd/profile_run.py traffic <rocprof output dir> <out.json>
-    python paper_2302_07594_amd/profile_run.py mfma <rocprof output dir> [out.json]
+    python paper_2302_07594_amd/profile_run.py traffic <rocprof output dir> <out.json> [family]
+    python paper_2302_07594_amd/profile_run.py mfma <rocprof output dir> [out.json] [family]
     python paper_2302_07594_amd/profile_run.py breakdown <rocprof output dir> <kernel substring>
 
 ``gemm`` runs the library's igemm call on the named workload's case (inputs
@@ -23,10 +23,11 @@ count. ``summarize`` prints per-kernel average durations from a
 ``*_kernel_stats.csv`` and per-dispatch counter values from a
 ``*_counter_collection.csv`` found under the directory. ``traffic`` reads the
 four counter runs ``gemm_FETCH_SIZE``, ``gemm_WRITE_SIZE``, ``copy_FETCH_SIZE``
-and ``copy_WRITE_SIZE`` under the directory (the int16 4096^3 workload's
-multiply kernel and a 1024 MiB copy), scales the multiply's counters by what
+and ``copy_WRITE_SIZE`` under the directory (the multiply kernel of a family in
+FAMILIES -- default the int16 4096^3 packed multiply, or ``i8_direct`` for
+int8 8192^3 -- and a 1024 MiB copy), scales the multiply's counters by what
 they read for the copy of known size, and writes the per-launch HBM bytes with
-the SHA-256 of the multiply kernel's source, which ``bench.py`` compares
+the SHA-256 of the kernel family's sources, which ``bench.py`` compares
 before it reports them. ``mfma`` reads one counter run of
 SQ_VALU_MFMA_BUSY_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_I8, SQ_BUSY_CU_CYCLES and
 GRBM_GUI_ACTIVE (with --kernel-trace) and prints, per dispatch, the
@@ -138,14 +139,30 @@ def _counter_rows(path: str, counter: str, keep):
     return [per[k] for k in sorted(per)]
 
 
-def _traffic(d: str, out: str) -> None:
+# Kernel families whose counter summaries bench.py reads: the multiply
+# kernel's name, the workload profiled, and its algorithmic bytes per launch
+# (A and B read once, C read and written once).
+FAMILIES = {
+    "i16_packed": {"family": "packed", "match": "igemm_packed<2, 128, 128",
+                   "kernel": "igemm_packed<2, 128, 128, 64, 64, 4> (int16 multiply on packed operands)",
+                   "workload": "int16 4096x4096x4096, row-major, one-call igemm_i16 (pack, pack, multiply)",
+                   "algorithmic": 2 * 4096 * 4096 * 2 + 8 * 4096 * 4096},
+    "i8_direct": {"family": "direct", "match": "igemm_direct<1, 256, 256",
+                  "kernel": "igemm_direct<1, 256, 256, 64, 128, 4> (int8 multiply, raw operands)",
+                  "workload": "int8 8192x8192x8192, row-major, one-call igemm_i8",
+                  "algorithmic": 2 * 8192 * 8192 + 8 * 8192 * 8192},
+}
+
+
+def _traffic(d: str, out: str, fam: str = "i16_packed") -> None:
     import json
 
     from paper_2302_07594_amd import build as hip_build
-    sha = hip_build.packed_kernel_hash()
+    F = FAMILIES[fam]
+    sha = hip_build.kernel_hash(F["family"])
 
     def mult(name):
-        return "igemm_packed<2, 128, 128" in name
+        return F["match"] in name
 
     def copy(name):  # the copy runs launch one fill, then the copies
         return "fill" not in name.lower()
@@ -160,10 +177,9 @@ def _traffic(d: str, out: str) -> None:
     ws = copied / (sum(cw) / len(cw) * 1024)
     fb = sum(fetch) / len(fetch) * 1024 * fs
     wb = sum(write) / len(write) * 1024 * ws
-    n = 4096
     t = {
-        "kernel": "igemm_packed<2, 128, 128, 64, 64, 4> (int16 multiply on packed operands)",
-        "workload": "int16 4096x4096x4096, row-major, one-call igemm_i16 (pack, pack, multiply)",
+        "kernel": F["kernel"],
+        "workload": F["workload"],
         "kernel_source_sha256": sha,
         "fetch_size_kib_per_dispatch": fetch,
         "write_size_kib_per_dispatch": write,
@@ -171,7 +187,7 @@ def _traffic(d: str, out: str) -> None:
                              "fetch_scale": round(fs, 4), "write_scale": round(ws, 4)},
         "fetch_bytes_per_launch": int(fb), "write_bytes_per_launch": int(wb),
         "traffic_bytes_per_launch": int(fb + wb),
-        "algorithmic_bytes_per_launch": 2 * n * n * 2 + 8 * n * n,
+        "algorithmic_bytes_per_launch": F["algorithmic"],
     }
     with open(out, "w") as f:
         json.dump(t, f, indent=1)
@@ -188,7 +204,7 @@ def _agent(d: str):
     return 1024, 8
 
 
-def _mfma(d: str, out_json: str = "") -> None:
+def _mfma(d: str, out_json: str = "", fam: str = "i16_packed") -> None:
     """Matrix-core utilisation per dispatch. GRBM_GUI_ACTIVE is summed over
     the XCCs, so active cycles per SIMD = GRBM_GUI_ACTIVE / Num_Xcc. Two
     figures: SQ_VALU_MFMA_BUSY_CYCLES over SIMD-cycles, and the int8 MFMA
@@ -234,7 +250,8 @@ def _mfma(d: str, out_json: str = "") -> None:
 
         from paper_2302_07594_amd import build as hip_build
         with open(out_json, "w") as f:
-            json.dump({"kernel_source_sha256": hip_build.packed_kernel_hash(),
+            json.dump({"kernel_source_sha256": hip_build.kernel_hash(FAMILIES[fam]["family"]),
+                       "kernel": FAMILIES[fam]["kernel"], "workload": FAMILIES[fam]["workload"],
                        "simds": simds, "xcc": xcc, "dispatches": rows}, f, indent=1)
 
 
@@ -273,11 +290,11 @@ def main(argv) -> None:
     elif cmd == "summarize":
         _summarize(argv[2])
     elif cmd == "traffic":
-        _traffic(argv[2], argv[3])
+        _traffic(argv[2], argv[3], argv[4] if len(argv) > 4 else "i16_packed")
     elif cmd == "breakdown":
         _breakdown(argv[2], argv[3])
     elif cmd == "mfma":
-        _mfma(argv[2], argv[3] if len(argv) > 3 else "")
+        _mfma(argv[2], argv[3] if len(argv) > 3 else "", argv[4] if len(argv) > 4 else "i16_packed")
     else:
         print(__doc__)
         sys.exit(2)
