@@ -55,8 +55,11 @@ def compile_flags(extra_flags=None):
 
 
 def _hash_files(paths, flags) -> str:
+    # Paths inside the repository enter relative to its root, so that the
+    # same tree hashes the same wherever it is checked out.
     h = hashlib.sha256()
-    h.update(" ".join(flags).encode())
+    h.update(" ".join(os.path.relpath(f, ROOT) if f.startswith(ROOT) else f
+                      for f in flags).encode())
     for p in paths:
         h.update(os.path.relpath(p, ROOT).encode())
         with open(p, "rb") as f:

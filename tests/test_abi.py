@@ -76,6 +76,28 @@ def test_build_stamp_tracks_sources():
     assert hip_build.source_hash(["-DX"]) != hip_build.source_hash()
 
 
+def test_source_hash_does_not_depend_on_checkout_location(tmp_path):
+    """A copy of the tree elsewhere (the GPU runs work on a copy) hashes the
+    same: the stamp and the profile summaries' hashes stay valid there."""
+    import shutil
+    import subprocess
+    import sys
+    from paper_2302_07594_amd import build as hip_build
+    root = os.path.dirname(os.path.dirname(os.path.abspath(hip_build.__file__)))
+    dst = tmp_path / "elsewhere"
+    shutil.copytree(os.path.join(root, "paper_2302_07594_amd"), dst / "paper_2302_07594_amd",
+                    ignore=shutil.ignore_patterns("*.so", "__pycache__"))
+    shutil.copytree(os.path.join(root, "include"), dst / "include")
+    code = ("from paper_2302_07594_amd import build as b; "
+            "print(b.source_hash(), b.kernel_hash('packed'), b.kernel_hash('direct'))")
+    # the copy's package stubs import nothing beyond build.py
+    out = subprocess.run([sys.executable, "-c", "import sys; sys.path.insert(0, sys.argv[1]); "
+                          + code, str(dst)], capture_output=True, text=True, check=True,
+                         cwd=str(tmp_path)).stdout.split()
+    assert out == [hip_build.source_hash(), hip_build.kernel_hash("packed"),
+                   hip_build.kernel_hash("direct")]
+
+
 def test_oracle_not_linked_into_library():
     lib = ctypes.CDLL(ig.library_path())
     assert not hasattr(lib, "oracle_igemm_i16")
