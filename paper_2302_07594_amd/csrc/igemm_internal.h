@@ -190,10 +190,13 @@ int launch_pack_b(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, 
 int launch_direct(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
                   int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
                   void *stream);
-// The small-output int16 kernel: one launch, k slices of plan.k_chunk.
+// The small-output int16 kernel: one launch, k slices of plan.k_chunk; and
+// its convolution variant (A gathered from X, channels a multiple of 64).
 int launch_small(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
                  int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
                  void *stream);
+int launch_small_conv(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const ConvGeom &g,
+                      const void *X, const void *W, int32_t *Y, int64_t ldy, void *stream);
 int launch_multiply(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
                     int64_t lda, int32_t *C, int64_t ldc, const void *a_part, const void *b_part,
                     void *stream);

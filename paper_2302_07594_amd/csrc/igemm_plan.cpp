@@ -553,12 +553,17 @@ int make_conv_plan(int es, const igemm_conv2d_desc *d, const void *X, const void
     if (M > INT_MAX || K > INT_MAX - 65536 || N > INT_MAX) return IGEMM_ENOTSUP;
     // Filter window offsets; (K + 2) * N < 2^62 after the bounds above.
     if ((K + 2) * N * es + 64 >= 0x7fff0000) return IGEMM_ENOTSUP;
+    // The small-output kernel gathers whole 64-channel k-tiles of one filter
+    // tap: channels a multiple of 64, 16-byte aligned input and weights.
+    const bool small_conv = es == 2 && d->c % 64 == 0 && (uintptr_t)X % 16 == 0 &&
+                            small_ok(M, N, K, X, K, W, N, N);
     int id = kernel;
     if (id < 0) {
         // The rules of the GEMM planner's fused kernels (no packed path: the
         // lowered matrix never exists).
         const int64_t ncu = num_cu > 0 ? num_cu : 256;
-        if (es == 2) {
+        if (es == 2 && small_conv && small_pays(M, N, K, (int)ncu)) id = K_I16_SMALL_64x64;
+        else if (es == 2) {
             if (M <= 16) id = K_I16_16x128;
             else if (M <= 32) id = K_I16_32x128;
             else if (N > 64 && K > 256 &&
@@ -574,7 +579,8 @@ int make_conv_plan(int es, const igemm_conv2d_desc *d, const void *X, const void
         }
     }
     const bool conv_id = id == K_I16_128x128 || id == K_I16_64x64 || id == K_I16_32x128 ||
-                         id == K_I16_16x128 || id == K_I8_32x256 || id == K_I8_16x256;
+                         id == K_I16_16x128 || id == K_I8_32x256 || id == K_I8_16x256 ||
+                         (id == K_I16_SMALL_64x64 && small_conv);
     if (!conv_id || kKernels[id].es != es) return IGEMM_EINVAL;
     int st = make_plan(es, M, N, K, X, K, W, N, N, num_cu, id, split, false, out);
     if (st != IGEMM_OK) return st;

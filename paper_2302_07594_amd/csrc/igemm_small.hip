@@ -28,7 +28,9 @@
 //
 // Preconditions (checked by the planner): A and B 16-byte aligned, rows a
 // multiple of 16 bytes, k a multiple of 64, n a multiple of 8, and 32-bit
-// byte offsets within one k-tile of each operand and within a C tile.
+// byte offsets within one k-tile of each operand and within a C tile. The
+// convolution variant gathers A from an NHWC input with a multiple of 64
+// channels (below 2 GB).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -57,11 +59,22 @@ constexpr int STAGE = APL + BPL;      // one k-tile of A and B
 __device__ __forceinline__ int swz_a(int row) { return (row >> 1) & 7; }
 __device__ __forceinline__ int swz_b(int row) { return 4 * ((row >> 1) & 1); }
 
-// KT: k-tiles per workgroup (the last k slice may hold fewer).
-template <int KT, bool SPLIT>
+// x / d for the invariant divisor d described by `dv` (the host's make_div).
+__device__ __forceinline__ u32 div_inv(u32 x, DivU32 dv) {
+    const u32 t = __umulhi(x, dv.mul);
+    return (t + ((x - t) >> dv.s1)) >> dv.s2;
+}
+
+// KT: k-tiles per workgroup (the last k slice may hold fewer). CONV: A is the
+// IM2ROW matrix of a convolution (Sec. 4.2) gathered from the NHWC input A
+// with geometry g, whose channel count is a multiple of 64, so that each
+// k-tile is 64 channels of one filter tap and each of its rows 128
+// contiguous bytes of one input pixel, or zeros outside the image.
+template <int KT, bool SPLIT, bool CONV>
 __global__ void __launch_bounds__(256, 2)
 igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict__ B,
-                int64_t ldb, int32_t *__restrict__ C, int64_t ldc, int m, int n, int ktiles) {
+                int64_t ldb, int32_t *__restrict__ C, int64_t ldc, int m, int n, int ktiles,
+                ConvGeom g) {
     typedef Mfma<32> M;
     typedef M::acc_t acc_t;
     static_assert(KT >= 1 && KT <= 4, "at most four k-tiles in LDS");
@@ -100,11 +113,34 @@ igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict_
         const int row = 8 * b + lane / 8, pc = lane % 8;
         if (d < 2) {
             const int grow = min(m0 + row, m - 1);
-            off[d] = (u32)grow * (u32)(lda * 2) + 16u * (u32)(pc ^ swz_a(row));
+            off[d] = CONV ? 16u * (u32)(pc ^ swz_a(row))
+                          : (u32)grow * (u32)(lda * 2) + 16u * (u32)(pc ^ swz_a(row));
         } else {
             const int col = min(n0 + 8 * (pc ^ swz_b(row)), n - 8);
             off[d] = (u32)row * (u32)(ldb * 2) + 2u * (u32)col;
         }
+    }
+    // IM2ROW: the output pixel of each of this lane's two A rows, decoded
+    // once: first input row and column of its window and its image's first
+    // pixel (a row past m gets a window outside the image). The input is
+    // read through a buffer resource, so that taps outside the image (an
+    // offset past its range) land in LDS as zeros.
+    int cv_iy0[2], cv_ix0[2], cv_pix[2];
+    __amdgpu_buffer_rsrc_t Xrs;
+    if constexpr (CONV) {
+#pragma unroll
+        for (int d = 0; d < 2; ++d) {
+            const u32 p = (u32)(m0 + 8 * (2 * wave + d) + lane / 8);
+            const bool ok = p < (u32)m;
+            const u32 img = div_inv(p, g.by_ohw);
+            const u32 rem = p - img * (u32)g.ohw;
+            const u32 oy = div_inv(rem, g.by_ow);
+            const u32 ox = rem - oy * (u32)g.ow;
+            cv_iy0[d] = ok ? (int)oy * g.sh - g.ph : -(1 << 30);
+            cv_ix0[d] = (int)ox * g.sw - g.pw;
+            cv_pix[d] = ok ? (int)img * g.h * g.w : 0;
+        }
+        Xrs = __builtin_amdgcn_make_buffer_rsrc((void *)A, 0, g.x_bytes, 0x00020000);
     }
     // Every one of the KT tiles is moved, a short last slice repeating its
     // last tile (read, never multiplied), so that the waits below are fixed
@@ -119,12 +155,32 @@ igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict_
         const char *bk = B + t * b_step;
         asm volatile("" : "+s"(ak), "+s"(bk));
         char *st = stage(kt);
+        // B first: its addresses need no decoding.
 #pragma unroll
         for (int d = 0; d < 4; ++d) {
-            u32 o = off[d];
+            const int dd = d ^ 2;   // B blocks (2, 3), then A blocks (0, 1)
+            if (CONV && dd < 2) continue;
+            u32 o = off[dd];
             asm volatile("" : "+v"(o));
-            const int b = 2 * wave + (d & 1);
-            dma16((d < 2 ? ak : bk) + o, (lds_void *)(st + (d < 2 ? 0 : APL) + b * 1024));
+            const int b = 2 * wave + (dd & 1);
+            dma16((dd < 2 ? ak : bk) + o, (lds_void *)(st + (dd < 2 ? 0 : APL) + b * 1024));
+        }
+        if constexpr (CONV) {
+            // k-tile t: channels [c0, c0 + 64) of filter tap (fy, fx)
+            const u32 tap = div_inv((u32)t * 64u, g.by_c);
+            const int c0 = (int)((u32)t * 64u - tap * (u32)g.c);
+            const u32 fy = div_inv(tap, g.by_s);
+            const int fx = (int)(tap - fy * (u32)g.s);
+#pragma unroll
+            for (int d = 0; d < 2; ++d) {
+                const int iy = cv_iy0[d] + (int)fy * g.dh, ix = cv_ix0[d] + fx * g.dw;
+                const bool in = (u32)iy < (u32)g.h && (u32)ix < (u32)g.w;
+                const u32 o = in ? (u32)((cv_pix[d] + iy * g.w + ix) * g.c + c0) * 2u + off[d]
+                                 : 0x80000000u;
+                const int b = 2 * wave + d;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(Xrs, (lds_void *)(st + b * 1024), 16,
+                                                         (int)o, 0, 0, 0);
+            }
         }
     }
     // Nothing below moves above the loads: the address arithmetic of the
@@ -158,7 +214,7 @@ igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict_
     // (32 bytes: two ds_read_b128). B: group g = lane / 16 covers columns
     // 16 (g % 2) + [0, 16) of the wave's 32 and k chunk 2 ks + g / 2; lane
     // u = lane % 16 addresses k row 16 q + 4 r + u / 4 at columns 4 (u % 4).
-    const int fr = lane & 31, g = lane >> 4, u = lane & 15;
+    const int fr = lane & 31, grp = lane >> 4, u = lane & 15;
     int a_rd[2][2], b_rd[2];
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
@@ -166,8 +222,8 @@ igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict_
         const int row = wm0 + fr;
 #pragma unroll
         for (int h = 0; h < 2; ++h) a_rd[ks][h] = row * RA + 16 * ((2 * q + h) ^ swz_a(row));
-        const int qb = 2 * ks + (g >> 1);
-        const int col = wn0 + 16 * (g & 1) + 4 * (u & 3);
+        const int qb = 2 * ks + (grp >> 1);
+        const int col = wn0 + 16 * (grp & 1) + 4 * (u & 3);
         const int krow = 16 * qb + (u >> 2);
         b_rd[ks] = APL + krow * RB + 16 * ((col >> 3) ^ swz_b(krow)) + 2 * (col & 7);
     }
@@ -266,19 +322,22 @@ igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict_
 using namespace small;
 
 // One launch: grid (column tiles, row tiles, k slices of plan.k_chunk).
-template <int KT>
+template <int KT, bool CONV>
 static void launch_kt(dim3 grid, bool split, hipStream_t s, const char *A, int64_t lda,
                       const char *B, int64_t ldb, int32_t *C, int64_t ldc, int m, int n,
-                      int ktiles) {
+                      int ktiles, const ConvGeom &g) {
     if (split)
-        igemm_small_i16<KT, true><<<grid, 256, 0, s>>>(A, lda, B, ldb, C, ldc, m, n, ktiles);
+        igemm_small_i16<KT, true, CONV><<<grid, 256, 0, s>>>(A, lda, B, ldb, C, ldc, m, n,
+                                                             ktiles, g);
     else
-        igemm_small_i16<KT, false><<<grid, 256, 0, s>>>(A, lda, B, ldb, C, ldc, m, n, ktiles);
+        igemm_small_i16<KT, false, CONV><<<grid, 256, 0, s>>>(A, lda, B, ldb, C, ldc, m, n,
+                                                              ktiles, g);
 }
 
-int launch_small(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
-                 int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
-                 void *stream) {
+template <bool CONV>
+static int launch_any(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                      int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
+                      const ConvGeom &g, void *stream) {
     const int64_t ktiles = k / 64, ktpw = p.k_chunk / 64;
     if (k % 64 != 0 || ktpw < 1 || ktpw > 4) return IGEMM_EINVAL;  // the planner prevents it
     const int64_t slices = (ktiles + ktpw - 1) / ktpw;
@@ -289,12 +348,24 @@ int launch_small(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const voi
     const bool split = slices > 1;
     const int mi = (int)m, ni = (int)n, kti = (int)ktiles;
     switch (ktpw) {
-        case 1: launch_kt<1>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti); break;
-        case 2: launch_kt<2>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti); break;
-        case 3: launch_kt<3>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti); break;
-        default: launch_kt<4>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti); break;
+        case 1: launch_kt<1, CONV>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti, g); break;
+        case 2: launch_kt<2, CONV>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti, g); break;
+        case 3: launch_kt<3, CONV>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti, g); break;
+        default: launch_kt<4, CONV>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti, g); break;
     }
     return hipGetLastError() == hipSuccess ? IGEMM_OK : IGEMM_EHIP;
+}
+
+int launch_small(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
+                 int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
+                 void *stream) {
+    const ConvGeom g = {};
+    return launch_any<false>(p, m, n, k, A, lda, B, ldb, C, ldc, g, stream);
+}
+
+int launch_small_conv(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const ConvGeom &g,
+                      const void *X, const void *W, int32_t *Y, int64_t ldy, void *stream) {
+    return launch_any<true>(p, m, n, k, X, k, W, n, Y, ldy, g, stream);
 }
 
 }  // namespace igemm

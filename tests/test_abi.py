@@ -453,15 +453,21 @@ def test_conv_too_large_is_unsupported():
 
 
 def test_conv_plans_match_lowered_gemm():
-    """The six layers' plans: the lowered GEMM shapes, fused kernels only,
-    16-byte gather exactly when c * element size is a multiple of 16."""
+    """The six layers' plans: the lowered GEMM shapes, no workspace, the
+    small-output kernel for the layers whose channels are a multiple of 64
+    (aligned tensors), else fused kernels with the 16-byte gather exactly when
+    c * element size is a multiple of 16."""
     import workloads
     for case in workloads.CONV2D_CASES:
         m, n, k = case.gemm_shape()
         d = ig.conv_desc(case.n, case.h, case.w, case.c, case.k, case.r, case.s, case.stride,
                          case.pad, case.dil)
         p = ig.igemm_conv2d_query_plan(2, d)
-        assert p["kernel_name"] in ("i16_128x128", "i16_64x64", "i16_32x128", "i16_16x128")
+        if case.c % 64 == 0:
+            assert p["kernel_name"] == "i16_small_64x64", case.name
+            assert p["k_chunk"] <= 256
+        else:
+            assert p["kernel_name"] in ("i16_128x128", "i16_64x64", "i16_32x128", "i16_16x128")
         assert not p["packed"] and p["workspace_bytes"] == 0
         assert p["vec_a"] == (1 if (case.c * 2) % 16 == 0 else 0)
         assert p["split"] * p["k_chunk"] >= k > (p["split"] - 1) * p["k_chunk"]
@@ -473,7 +479,8 @@ def test_conv_plans_match_lowered_gemm():
     assert ig.igemm_conv2d_query_plan(1, d)["kernel_name"] == "i8_32x256"
     d1 = ig.conv_desc(1, 4, 4, 64, 64, 1, 1)
     assert ig.igemm_conv2d_query_plan(1, d1)["kernel_name"] == "i8_16x256"
-    assert ig.igemm_conv2d_query_plan(2, d1)["kernel_name"] == "i16_16x128"
+    assert ig.igemm_conv2d_query_plan(2, d1)["kernel_name"] == "i16_small_64x64"
+    assert ig.igemm_conv2d_query_plan(2, d1, X=FAKE_X + 2)["kernel_name"] == "i16_16x128"
 
 
 def test_conv_null_descriptor():
@@ -587,9 +594,15 @@ def test_planner_rules_for_small_int16_outputs():
     assert plan(12544, 64, 147) == ("i16_64x64", 2, 128)
     assert plan(3136, 256, 64, lda=65)[0] == "i16_16x128"
     assert plan(100352, 256, 64)[0] == "i16_64x64"      # enough 64x64 tiles to fill the units
+    # convolutions: the small-output kernel when the channels are a multiple
+    # of 64 and X is 16-byte aligned, else the fused rules
     d = ig.conv_desc(1, 56, 56, 64, 256, 1, 1)
     p = ig.igemm_conv2d_query_plan(2, d, num_cu=256)
+    assert ig.igemm_kernel_name(p["kernel"]) == "i16_small_64x64"
+    p = ig.igemm_conv2d_query_plan(2, d, X=2, num_cu=256)
     assert ig.igemm_kernel_name(p["kernel"]) == "i16_16x128"
     d = ig.conv_desc(1, 56, 56, 64, 64, 3, 3, pad=(1, 1))
     p = ig.igemm_conv2d_query_plan(2, d, num_cu=256)
+    assert (ig.igemm_kernel_name(p["kernel"]), p["split"]) == ("i16_small_64x64", 3)
+    p = ig.igemm_conv2d_query_plan(2, d, X=2, num_cu=256)
     assert (ig.igemm_kernel_name(p["kernel"]), p["split"]) == ("i16_64x64", 5)

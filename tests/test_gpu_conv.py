@@ -128,6 +128,51 @@ def test_every_conv_kernel(dt, shape):
                    split=split)
 
 
+# Shapes for the small-output int16 kernel's gather (channels a multiple of
+# 64: each k-tile is 64 channels of one filter tap; output channels a
+# multiple of 8): padding beyond the filter, strides, dilations, several
+# images, taps of several k-tiles, one output pixel per image.
+SMALL_SHAPES = [
+    (1, 9, 11, 64, 40, 3, 3, (1, 1), (1, 1), (1, 1)),
+    (2, 13, 10, 64, 72, 3, 3, (2, 2), (1, 1), (1, 1)),
+    (1, 12, 17, 128, 136, 3, 2, (1, 2), (2, 0), (2, 1)),
+    (2, 6, 6, 64, 16, 1, 1, (1, 1), (0, 0), (1, 1)),
+    (1, 10, 9, 64, 64, 5, 3, (3, 1), (4, 2), (1, 3)),
+    (2, 4, 4, 192, 8, 4, 4, (1, 1), (0, 0), (1, 1)),
+    (1, 20, 3, 64, 304, 3, 1, (2, 1), (0, 5), (1, 1)),
+    (3, 7, 7, 128, 24, 3, 3, (1, 1), (1, 1), (1, 1)),
+]
+
+
+@pytest.mark.parametrize("shape", SMALL_SHAPES, ids=lambda t: "x".join(map(str, t[:7])))
+def test_small_kernel_gather(shape):
+    """The small-output kernel with A gathered from X (taps outside the image
+    read as zeros through the buffer resource), automatic and forced k
+    slices, including a short last slice."""
+    n, h, w, c, k, r, s, stride, pad, dil = shape
+    for split in (-1, 1, 3, 100):
+        _check("i16", n, h, w, c, k, r, s, stride, pad, dil, seed=900 + sum(shape[:7]),
+               kernel=_kid("i16_small_64x64"), split=split)
+
+
+def test_small_kernel_gather_preconditions():
+    """Channels not a multiple of 64, output channels not a multiple of 8 or
+    a misaligned input: an explicit request for the small kernel is refused
+    and Y is left alone."""
+    import torch
+    ig = _ig()
+    for (c, k, x_off) in ((48, 64, 0), (64, 20, 0), (64, 64, 1)):
+        X, W, Y = workloads.random_conv_operands("i16", 1, 6, 6, c, k, 3, 3, 6, 6, 5)
+        Xd, Wd = to_device(X, x_off), to_device(W, 0)
+        Yd = torch.from_numpy(Y).cuda()
+        d = ig.conv_desc(1, 6, 6, c, k, 3, 3, (1, 1), (1, 1), (1, 1))
+        st = ig.igemm_conv2d_ex(2, d, Xd.data_ptr(), Wd.data_ptr(), Yd.data_ptr(),
+                                torch.cuda.current_stream().cuda_stream,
+                                _kid("i16_small_64x64"), -1)
+        torch.cuda.synchronize()
+        assert st == ig.IGEMM_EINVAL and np.array_equal(Yd.cpu().numpy(), Y), (c, k, x_off)
+
+
 @pytest.mark.parametrize("dt", ["i16", "i8"])
 @pytest.mark.parametrize("x_off,w_off", [(1, 0), (0, 1), (3, 5)])
 def test_misaligned_tensors(dt, x_off, w_off):
@@ -153,7 +198,7 @@ def test_wraparound_extremes():
     W = np.full((r, s, c, k), -32768, dtype=np.int16)
     W[:, :, ::2, ::3] = 32767
     Y = np.full((n, h, w, k), 2 ** 31 - 5, dtype=np.int32)
-    for name in CONV_KERNELS["i16"]:
+    for name in CONV_KERNELS["i16"] + ("i16_small_64x64",):
         want = _oracle(X, W, Y, (1, 1), (1, 1), (1, 1))
         got = _gpu(X, W, Y, (1, 1), (1, 1), (1, 1), kernel=_kid(name))
         assert np.array_equal(got, want), _describe(got, want)
