@@ -241,8 +241,14 @@ int srs_packed_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int6
     if (kernel == K_I16_PACKED_128x128 && (!packed_ok || !can_pack)) return IGEMM_EINVAL;
     if (blk > kMaxKChunk) return IGEMM_ENOTSUP;
     if (kernel != K_I16_PACKED_128x128 && !(kernel < 0 && packed_ok)) return IGEMM_OK;
-    const int st = make_plan(es, m, n, k, A, lda, B, ldb, ldc, num_cu, kernel < 0 ? -1 : kernel,
-                             -1, can_pack, pp);
+    int st = make_plan(es, m, n, k, A, lda, B, ldb, ldc, num_cu, kernel < 0 ? -1 : kernel, -1,
+                       can_pack, pp);
+    // A large product the GEMM plan gives to the direct kernel (short k)
+    // still takes the packed path here: only the packed kernel has the
+    // in-kernel int16-output conversion.
+    if (st == IGEMM_OK && kernel < 0 && can_pack && pp->kernel == K_I16_DIRECT_128x128)
+        st = make_plan(es, m, n, k, A, lda, B, ldb, ldc, num_cu, K_I16_PACKED_128x128, -1, true,
+                       pp);
     if (st != IGEMM_OK) return st;
     if (pp->packed) *need = pp->workspace_bytes + srs_sums_bytes(*pp, m, n, k, nblocks, A, lda);
     return IGEMM_OK;

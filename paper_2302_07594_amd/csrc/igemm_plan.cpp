@@ -248,6 +248,11 @@ static int auto_kernel(int es, int64_t m, int64_t n, int64_t k, const void *A, i
     const bool large = packed_pays(es, m, n, k, num_cu);
     const bool direct = large && direct_ok(es, m, n, k, A, lda, B, ldb, ldc);
     if (es == 1 && direct) return K_I8_DIRECT_256x256;
+    // Up to k = 1024 the pack pass costs the packed path more than the
+    // direct kernel's in-register split (int16 m = n = 4096, one call, us:
+    // k = 256 61.6 packed against 57.9 direct, 512 77.9 / 74.7, 1024
+    // 106.9 / 106.0, 2048 161.8 / 164.6).
+    if (es == 2 && direct && k <= 1024) return K_I16_DIRECT_128x128;
     if (allow_packed && large && packed_fits(pid, ldc) &&
         16 * (k > lda ? k : lda) < ((int64_t)1 << 31))
         return pid;

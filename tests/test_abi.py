@@ -507,10 +507,12 @@ def test_srs_query_is_host_only_and_consistent():
     block; fused choices need none; invalid arguments raise."""
     P = 1 << 20
     m = n = 4096
+    kp = [i for i in ig.kernels_for(2) if ig.igemm_kernel_name(i) == "i16_packed_128x128"][0]
     for k, kc, nblocks in ((290, 0, 1), (290, 290, 1), (4096, 256, 16), (1024, 512, 2)):
-        plan = ig.igemm_query_plan(2, m, n, k, P, k, P, n, P, n, 256)
+        # (the int32 GEMM of k = 1024 takes the direct kernel; the int16-output
+        # update still packs)
+        plan = ig.igemm_query_plan(2, m, n, k, P, k, P, n, P, n, 256, kernel=kp)
         need = ig.igemm_srs_query(2, m, n, k, P, k, P, n, P, n, kc, 256)
-        assert ig.igemm_kernel_name(plan["kernel"]) == "i16_packed_128x128"
         assert need == plan["workspace_bytes"] + 8 * nblocks * (m + n), (k, kc)
     # fused choices: int8 operands, a small product, blocks of 100, over 64 blocks
     assert ig.igemm_srs_query(1, m, n, 4096, P, 4096, P, n, P, n, 256, 256) == 0
