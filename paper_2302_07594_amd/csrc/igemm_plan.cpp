@@ -174,8 +174,8 @@ struct StreamShape {
     int64_t spw, slices, tiles;
 };
 static bool stream_shape(int64_t m, int64_t n, int64_t k, int64_t lda, int64_t ldb, bool va,
-                         bool vb, int split, StreamShape *out) {
-    const int bm = m <= 16 ? 16 : 32;
+                         bool vb, int split, int num_cu, StreamShape *out) {
+    int bm = m <= 16 ? 16 : 32;
     const int64_t ksteps = cdiv(k, kBK);
     int64_t spw = 4;
     if (va && vb) {
@@ -183,7 +183,16 @@ static bool stream_shape(int64_t m, int64_t n, int64_t k, int64_t lda, int64_t l
         // the loads of B in flight. Measured on the 4096- and 11008-column
         // shapes with k = 4096: 8 steps per workgroup (4 and 16 are up to 10%
         // slower, 32 up to 2x).
-        const int64_t want = split > 0 ? cdiv(ksteps, split) : 8;
+        int64_t want = split > 0 ? cdiv(ksteps, split) : 8;
+        // 17 to 32 rows over few column blocks (at most one workgroup per
+        // compute unit with 32-row blocks of 8 steps): two 16-row blocks of
+        // 16 steps instead, half the adds per workgroup and no two-phase
+        // reduction (32 x 4096 x 4096: 7.1 us against 8.2 us; on 32 x 11008,
+        // where B's second pass costs bandwidth, 16.8 against 15.2 us).
+        if (bm == 32 && split <= 0 && cdiv(n, 128) * cdiv(ksteps, 8) <= num_cu) {
+            bm = 16;
+            want = 16;
+        }
         const int64_t cap = bm == 16 ? 32 : 16;
         while (spw < want && spw < cap) spw *= 2;
     }
@@ -264,7 +273,7 @@ static int auto_kernel(int es, int64_t m, int64_t n, int64_t k, const void *A, i
         StreamShape ss;
         if (m <= 32 && n >= 512 && k >= 256 && (uintptr_t)B % 8 == 0 && ldb % 8 == 0 &&
             (uintptr_t)A % 16 == 0 && lda % 16 == 0 &&
-            stream_shape(m, n, k, lda, ldb, true, true, -1, &ss))
+            stream_shape(m, n, k, lda, ldb, true, true, -1, num_cu, &ss))
             return K_I8_STREAM;
         if (m <= 16) return K_I8_16x256;
         if (m <= 32) return K_I8_32x256;
@@ -385,7 +394,7 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
         const bool va = a % 16 == 0 && lda % 16 == 0;
         const bool vb = b % 8 == 0 && ldb % 8 == 0;
         StreamShape ss;
-        if (!stream_shape(m, n, k, lda, ldb, va, vb, split, &ss)) return IGEMM_ENOTSUP;
+        if (!stream_shape(m, n, k, lda, ldb, va, vb, split, num_cu, &ss)) return IGEMM_ENOTSUP;
         out->kernel = id;
         out->bm = ss.bm;
         out->bn = 128;
