@@ -3,6 +3,8 @@
 
 Usage (the program itself goes after ``rocprofv3 ... --``):
     python paper_2302_07594_amd/profile_run.py gemm <workload> [iters] [case] [kernel name]
+    python paper_2302_07594_amd/profile_run.py cases <workload> [iters] [sets]
+    python paper_2302_07594_amd/profile_run.py traffic_cases <rocprof output dir> <workload> [iters]
     python paper_2302_07594_amd/profile_run.py conv <layer> [iters] [b32]
     python paper_2302_07594_amd/profile_run.py srs <workload> <kc> <shift> [iters]
     python paper_2302_07594_amd/profile_run.py copy <MiB> [iters]
@@ -12,7 +14,11 @@ Usage (the program itself goes after ``rocprofv3 ... --``):
     python paper_2302_07594_amd/profile_run.py breakdown <rocprof output dir> <kernel substring>
 
 ``gemm`` runs the library's igemm call on the named workload's case (inputs
-generated as in the benchmark, C reset is not needed for timing); ``conv``
+generated as in the benchmark, C reset is not needed for timing); ``cases`` runs every case of a
+workload in turn, cycling over several device copies of its operands, and
+``traffic_cases`` turns FETCH_SIZE / WRITE_SIZE runs of it (``gemm_*``
+subdirectories, with the copy calibration ``copy_*`` beside them) into
+per-case bytes against the algorithmic bytes. ``conv``
 runs the convolution entry point on one of the six network layers (index
 into ``workloads.CONV2D_CASES``, or ``CONV2D_B32_CASES`` with ``b32``);
 ``srs`` runs the int16-output update on a workload's A and B (int16 C) with
@@ -65,6 +71,26 @@ def _gemm(wname: str, iters: int, case_idx: int, kernel_name: str = "") -> None:
         f(Ad, Bd, Cd, kernel=kid)
     torch.cuda.synchronize()
     print(f"ran {case.name} x{iters}", flush=True)
+
+
+def _cases(wname: str, iters: int, sets: int) -> None:
+    """Every case of a workload in turn, `iters` one-call launches each,
+    cycling over `sets` device copies of the operands (so that a launch finds
+    its operands in no XCD's L2 from the launch before)."""
+    import torch
+
+    import paper_2302_07594_amd as ig
+    import workloads
+    for case in workloads.WORKLOADS[wname].cases:
+        host = workloads.generate(case)
+        dev = [[torch.from_numpy(x).cuda() for x in host] for _ in range(sets)]
+        f = ig.gemm_i16 if case.dtype == "i16" else ig.gemm_i8
+        torch.cuda.synchronize()
+        for i in range(iters):
+            f(*dev[i % sets])
+        torch.cuda.synchronize()
+        del dev
+        print(f"ran {case.name} x{iters}", flush=True)
 
 
 def _conv(layer: int, iters: int, batch32: bool = False) -> None:
@@ -195,6 +221,43 @@ def _traffic(d: str, out: str, fam: str = "i16_packed") -> None:
                                         "traffic_bytes_per_launch")}))
 
 
+def _traffic_cases(d: str, wname: str, iters: int) -> None:
+    """Per-case HBM traffic of a `cases` run: FETCH_SIZE and WRITE_SIZE per
+    dispatch (one dispatch per call, cases in workload order) scaled by the
+    copy calibration under the same directory, against each case's
+    algorithmic bytes (A and B read once, C read and written once)."""
+    import workloads
+    cases = workloads.WORKLOADS[wname].cases
+    def ours(name):   # the library's kernels (not the copies that set up operands)
+        return "igemm" in name
+    fetch = _counter_rows(os.path.join(d, "gemm_FETCH_SIZE"), "FETCH_SIZE", ours)
+    write = _counter_rows(os.path.join(d, "gemm_WRITE_SIZE"), "WRITE_SIZE", ours)
+    cf = _counter_rows(os.path.join(d, "copy_FETCH_SIZE"), "FETCH_SIZE",
+                       lambda n: "fill" not in n.lower())
+    cw = _counter_rows(os.path.join(d, "copy_WRITE_SIZE"), "WRITE_SIZE",
+                       lambda n: "fill" not in n.lower())
+    if len(fetch) != len(cases) * iters or len(write) != len(cases) * iters or not (cf and cw):
+        raise SystemExit(f"unexpected dispatch counts: {len(fetch)} {len(write)} "
+                         f"{len(cf)} {len(cw)}")
+    copied = 1024 << 20
+    fs = copied / (sum(cf) / len(cf) * 1024)
+    ws = copied / (sum(cw) / len(cw) * 1024)
+    print(f"copy calibration: FETCH_SIZE scale {fs:.4f}, WRITE_SIZE scale {ws:.4f}")
+    print("| case | algorithmic MB (A + B + 2 C) | C MB | fetched MB | written MB | "
+          "total / algorithmic | written / C |")
+    print("|---|---|---|---|---|---|---|")
+    for i, case in enumerate(cases):
+        es = 2 if case.dtype == "i16" else 1
+        f = fetch[i * iters:(i + 1) * iters]
+        w = write[i * iters:(i + 1) * iters]
+        fb = sum(f) / len(f) * 1024 * fs
+        wb = sum(w) / len(w) * 1024 * ws
+        cb = 4 * case.m * case.n
+        alg = es * (case.m * case.k + case.k * case.n) + 2 * cb
+        print(f"| {case.name} | {alg / 1e6:.2f} | {cb / 1e6:.2f} | {fb / 1e6:.2f} | "
+              f"{wb / 1e6:.2f} | {(fb + wb) / alg:.2f} | {wb / cb:.2f} |")
+
+
 def _agent(d: str):
     """(SIMD count, XCC count) of the GPU agent in a rocprofv3 output dir."""
     for f in glob.glob(os.path.join(d, "**", "*agent_info.csv"), recursive=True):
@@ -280,6 +343,10 @@ def main(argv) -> None:
     if cmd == "gemm":
         _gemm(argv[2], int(argv[3]) if len(argv) > 3 else 3, int(argv[4]) if len(argv) > 4 else 0,
               argv[5] if len(argv) > 5 else "")
+    elif cmd == "cases":
+        _cases(argv[2], int(argv[3]) if len(argv) > 3 else 4, int(argv[4]) if len(argv) > 4 else 8)
+    elif cmd == "traffic_cases":
+        _traffic_cases(argv[2], argv[3], int(argv[4]) if len(argv) > 4 else 4)
     elif cmd == "conv":
         _conv(int(argv[2]), int(argv[3]) if len(argv) > 3 else 3,
               len(argv) > 4 and argv[4] == "b32")
