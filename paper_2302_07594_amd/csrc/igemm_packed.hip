@@ -233,8 +233,9 @@ block_sums(const int8_t *__restrict__ P0, const int8_t *__restrict__ P1, int64_t
 // exact (high, low) limb sums of the range per row / column, and kconst is
 // 16384 times the range's length.
 // EPI 2 (int16 only): the int16-output update of every k block in one launch.
-// The k range is kcb-tile blocks (kcb a multiple of 4, ktiles = nblocks kcb,
-// at most 16 blocks); corrA / corrB hold the exact (high, low) limb sums of
+// The k range is kcb-tile blocks (kcb a multiple of 4 and at most 32, i.e.
+// k_c <= 2048; ktiles = nblocks kcb, at most 16 blocks; shift <= 16);
+// corrA / corrB hold the exact (high, low) limb sums of
 // every block (block q at 2 (q m_pad + row), as block_sums writes them),
 // staged in LDS at the start; kconst is 16384 kcb 64. At the end of each
 // block the lane converts its accumulators into the block's int16
@@ -272,7 +273,11 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     constexpr int DPA = NBA / NW, DPB = NBB / NW, DPW = DPA + DPB;
     static_assert(DPW <= 15, "outstanding DMA count fits s_waitcnt");
     static_assert(EPI == 0 || ES == 2, "the int16-output update is for int16 operands");
-    static_assert(EPI != 2 || !RAGGED, "blocks of whole groups of four k-tiles");
+    // EPI 2-4: the multi-block update; its shift range selects the form of the
+    // conversion (2: shift 0, 3: shift 1-7, 4: shift 8-16).
+    constexpr bool MULTI = EPI >= 2;
+    constexpr int SMODE = EPI - 2;
+    static_assert(!MULTI || !RAGGED, "blocks of whole groups of four k-tiles");
     constexpr int MAXB = 16;  // blocks of one EPI 2 launch
 
     // The LDS stages as separate objects, so that the compiler can tell the
@@ -307,9 +312,9 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     const int m0 = tm * BM, n0 = tn * BN;
 
     // EPI 2: every block's limb sums of this tile's rows and columns, in LDS.
-    __shared__ uint2 bsA[EPI == 2 ? MAXB * BM : 1];
-    __shared__ uint2 bsB[EPI == 2 ? MAXB * BN : 1];
-    if constexpr (EPI == 2) {
+    __shared__ uint2 bsA[MULTI ? MAXB * BM : 1];
+    __shared__ uint2 bsB[MULTI ? MAXB * BN : 1];
+    if constexpr (MULTI) {
         const int nblocks = ktiles / kcb;
         const uint2 *sa = (const uint2 *)corrA, *sb = (const uint2 *)corrB;
         for (int x = tid; x < nblocks * BM; x += NW * 64)
@@ -390,8 +395,12 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
             for (int j = 0; j < TN; ++j)
 #pragma unroll
                 for (int r = 0; r < M::REGS; ++r) acc[a][i][j][r] = 0;
-    auto mfmas = [&](auto slot) {
+    // FRESH: the first products of a k block start from zero (a zero
+    // accumulator operand) instead of adding to the accumulators.
+    auto mfmas = [&](auto slot, auto fresh) {
         constexpr int SL = decltype(slot)::value;
+        constexpr bool FRESH = decltype(fresh)::value != 0;
+        const acc_t zero = {};
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
             if constexpr (ES == 1) {
@@ -401,13 +410,16 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
             } else {
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[0][i][j] = M::mma(fa[SL][0][i], fb[SL][0][j], acc[0][i][j]);
+                    acc[0][i][j] =
+                        M::mma(fa[SL][0][i], fb[SL][0][j], FRESH ? zero : acc[0][i][j]);
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[1][i][j] = M::mma(fa[SL][0][i], fb[SL][1][j], acc[1][i][j]);
+                    acc[1][i][j] =
+                        M::mma(fa[SL][0][i], fb[SL][1][j], FRESH ? zero : acc[1][i][j]);
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[2][i][j] = M::mma(fa[SL][1][i], fb[SL][1][j], acc[2][i][j]);
+                    acc[2][i][j] =
+                        M::mma(fa[SL][1][i], fb[SL][1][j], FRESH ? zero : acc[2][i][j]);
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
                     acc[1][i][j] = M::mma(fa[SL][1][i], fb[SL][0][j], acc[1][i][j]);
@@ -436,14 +448,14 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     // MFMAs: the compiler cannot tell the DMA loads' LDS writes apart from
     // other LDS traffic, so any wait for a fragment is a full lgkmcnt(0), and
     // this order makes that wait cover only reads issued a sub-step earlier.
-    auto step = [&](auto s, int kt, auto do_dma, auto do_pref) {
+    auto step = [&](auto s, int kt, auto do_dma, auto do_pref, auto fresh) {
         constexpr int S = decltype(s)::value;
         constexpr int SD = (S + NST - 1) % NST;  // stage receiving the DMA
         constexpr bool DMA = decltype(do_dma)::value != 0;
         constexpr bool PREF = decltype(do_pref)::value != 0;
         if constexpr (DMA) dma_range(ic<SD>{}, kt + NST - 1, ic<0>{}, ic<D_SUB0>{});
         read_frags(ic<1>{}, ic<S>{}, ic<1>{});
-        mfmas(ic<0>{});
+        mfmas(ic<0>{}, fresh);
 #pragma unroll
         for (int i = 0; i < NM; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -455,7 +467,7 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
         if constexpr (DMA && D_SUB0 < DPW)
             dma_range(ic<SD>{}, kt + NST - 1, ic<D_SUB0>{}, ic<DPW>{});
         if constexpr (PREF) read_frags(ic<0>{}, ic<(S + 1) % NST>{}, ic<0>{});
-        mfmas(ic<1>{});
+        mfmas(ic<1>{}, ic<0>{});
 #pragma unroll
         for (int i = 0; i < NM; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -472,18 +484,20 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     };
     // The last T steps from a stage-0 step at kt0: step j starts a DMA only if
     // tile j+NST-1 exists and prefetches only if tile j+1 exists.
-    auto tail_step = [&](auto jc, auto tc, int kt0) {
+    // (FRESH: the first of them opens a k block.)
+    auto tail_step = [&](auto jc, auto tc, int kt0, auto fresh) {
         constexpr int J = decltype(jc)::value, T = decltype(tc)::value;
         if constexpr (J < T)
-            step(ic<J % NST>{}, kt0 + J, ic<(J + NST - 1 < T)>{}, ic<(J + 1 < T)>{});
+            step(ic<J % NST>{}, kt0 + J, ic<(J + NST - 1 < T)>{}, ic<(J + 1 < T)>{},
+                 ic<(J == 0 && decltype(fresh)::value != 0)>{});
     };
-    auto tail = [&](auto tc, int kt0) {
-        tail_step(ic<0>{}, tc, kt0);
-        tail_step(ic<1>{}, tc, kt0);
-        tail_step(ic<2>{}, tc, kt0);
-        tail_step(ic<3>{}, tc, kt0);
-        tail_step(ic<4>{}, tc, kt0);
-        tail_step(ic<5>{}, tc, kt0);
+    auto tail = [&](auto tc, int kt0, auto fresh) {
+        tail_step(ic<0>{}, tc, kt0, fresh);
+        tail_step(ic<1>{}, tc, kt0, fresh);
+        tail_step(ic<2>{}, tc, kt0, fresh);
+        tail_step(ic<3>{}, tc, kt0, fresh);
+        tail_step(ic<4>{}, tc, kt0, fresh);
+        tail_step(ic<5>{}, tc, kt0, fresh);
     };
 
     // Prologue: tiles 0 .. NST-2 into stages 0 .. NST-2; tiles 0 and 1 must
@@ -503,8 +517,8 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     // that wrap modulo 2^16, as the update of C does), and the conversion of
     // block q's accumulators into them.
     typedef short s2 __attribute__((ext_vector_type(2)));
-    constexpr int RT = EPI == 2 ? TM : 1, RN = EPI == 2 ? TN : 1;
-    constexpr int RR = EPI == 2 ? M::REGS / 2 : 1;
+    constexpr int RT = MULTI ? TM : 1, RN = MULTI ? TN : 1;
+    constexpr int RR = MULTI ? M::REGS / 2 : 1;
     s2 run16[RT][RN][RR];
 #pragma unroll
     for (int i = 0; i < RT; ++i)
@@ -512,98 +526,115 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
         for (int j = 0; j < RN; ++j)
 #pragma unroll
             for (int r = 0; r < RR; ++r) run16[i][j][r] = s2{0, 0};
-    // The conversion runs in double precision: every term is an integer below
-    // 2^46 in magnitude (block sums below 2^30, scaled by at most 2^16), so
-    // the products by powers of two, the sums, the scaling by 2^-shift and the
-    // floor are all exact, and each double instruction costs what an int32
-    // one does on these compute units (unlike the 64-bit integer sequence).
+    // The conversion runs in 32-bit integer arithmetic; the host takes this
+    // launch only for blocks of k_c <= 2048 elements and shifts <= 16. With
+    //   X = S_x + 128 (hA + hB),  L = S_ll + 128 (l'A + l'B) + 16384 k_c
+    // (hA, l'A: the row's limb sums over the block; hB, l'B: the column's),
+    // the block's exact product is v = 65536 S_hh + 256 X + L, where
+    // |S_hh| <= 2^14 k_c <= 2^25 and |X|, |L| <= 2^16 k_c <= 2^27. Then
+    //   y = floor(v / 256) = 256 S_hh + X + (L >> 8),  v = 256 y + (L & 255).
+    // S_hh is clamped to [-2^21, 2^21] first: inside, y is exact and
+    // |y| < 2^30; outside, |v| > 2^36 and the clamped y (|y| > 2^28, same
+    // sign) saturates the same way for every shift <= 16. The shift then
+    // takes one of two forms:
+    //   shift >= 8: floor((v + half) / 2^s) = (y + ((L & 255) + half) >> 8) >> (s - 8)
+    //   shift <  8: y is clamped to [-2^22, 2^22] (beyond it |v| >= 2^30 - 255
+    //               saturates for every shift < 8) and v = 256 y + (L & 255)
+    //               is formed exactly, then (v + half) >> s.
+    // Arithmetic shifts right are floors; half = 2^(s-1) with rounding, else 0.
     auto convert = [&](int q) {
-        if constexpr (EPI == 2) {
+        if constexpr (MULTI) {
             const int sh = epi & 0xff;
-            const bool rnd = ((epi >> 8) & 1) != 0 && sh > 0;
-            const double scale = 1.0 / (double)((int64_t)1 << sh);
-            const double halfd = rnd ? (double)((int64_t)1 << (sh - 1)) : 0.0;
-            double cd[TN];
+            const int half = ((epi >> 8) & 1) != 0 && sh > 0 ? 1 << (sh - 1) : 0;
+            int colM[TN], colL[TN];
 #pragma unroll
             for (int j = 0; j < TN; ++j) {
                 const uint2 v = bsB[q * BN + wn0 + MF * j + M::out_col(lane)];
-                cd[j] = __builtin_fma((double)(int)v.x, 32768.0,
-                                      __builtin_fma((double)(int)v.y, 128.0, (double)kconst));
+                colM[j] = (int)(v.x << 7);
+                colL[j] = (int)((v.y << 7) + kconst);
             }
-            auto elems = [&](auto) {
+            // One output block at a time, so that few accumulators are live
+            // outside the AGPRs (the next block's first products overwrite
+            // them: FRESH steps).
 #pragma unroll
-                for (int i = 0; i < TM; ++i) {
+            for (int i = 0; i < TM; ++i) {
+                int rowM[M::REGS], rowL[M::REGS];
+#pragma unroll
+                for (int r = 0; r < M::REGS; ++r) {
+                    const uint2 v = bsA[q * BM + wm0 + MF * i + M::out_row(lane, r)];
+                    rowM[r] = (int)(v.x << 7);
+                    rowL[r] = (int)(v.y << 7);
+                }
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
 #pragma unroll
                     for (int r2 = 0; r2 < M::REGS / 2; ++r2) {
-                        double rd[2];
+                        u32 t16[2];
 #pragma unroll
                         for (int h = 0; h < 2; ++h) {
-                            const uint2 v =
-                                bsA[q * BM + wm0 + MF * i + M::out_row(lane, 2 * r2 + h)];
-                            rd[h] = __builtin_fma((double)(int)v.x, 32768.0,
-                                                  (double)(int)v.y * 128.0);
-                        }
-#pragma unroll
-                        for (int j = 0; j < TN; ++j) {
-                            short t16[2];
-#pragma unroll
-                            for (int h = 0; h < 2; ++h) {
-                                const int r = 2 * r2 + h;
-                                double a = (double)acc[2][i][j][r] + (rd[h] + cd[j]);
-                                a = __builtin_fma((double)acc[1][i][j][r], 256.0, a);
-                                a = __builtin_fma((double)acc[0][i][j][r], 65536.0, a);
-                                // (exact, and the identity for shift 0)
-                                a = __builtin_floor((a + halfd) * scale);
-                                a = __builtin_fmin(__builtin_fmax(a, -32768.0), 32767.0);
-                                t16[h] = (short)(int)a;
+                            const int r = 2 * r2 + h;
+                            const int hh = min(max(acc[0][i][j][r], -(1 << 21)), 1 << 21);
+                            const int L = acc[2][i][j][r] + rowL[r] + colL[j];
+                            const int y = (int)((u32)hh << 8) + acc[1][i][j][r] + rowM[r] +
+                                          colM[j] + (L >> 8);
+                            int t;
+                            if constexpr (SMODE == 2) {
+                                t = (y + (((L & 255) + half) >> 8)) >> (sh - 8);
+                            } else {
+                                const int yc = min(max(y, -(1 << 22)), 1 << 22);
+                                // bytes: the lowest of L, then the lower three of yc
+                                t = (int)perm((u32)yc, (u32)L, 0x06050400u);
+                                if constexpr (SMODE == 1) t = (t + half) >> sh;
                             }
-                            run16[i][j][r2] += s2{t16[0], t16[1]};
+                            t16[h] = (u32)min(max(t, -32768), 32767);
                         }
+                        run16[i][j][r2] += s2{(short)t16[0], (short)t16[1]};
                     }
+                    __builtin_amdgcn_sched_barrier(0);
                 }
-            };
-            elems(ic<1>{});
-#pragma unroll
-            for (int a = 0; a < NACC; ++a)
-#pragma unroll
-                for (int i = 0; i < TM; ++i)
-#pragma unroll
-                    for (int j = 0; j < TN; ++j)
-#pragma unroll
-                        for (int r = 0; r < M::REGS; ++r) acc[a][i][j][r] = 0;
+            }
         }
     };
     int kt = 0;
     for (; kt <= ktiles - 2 * NST + 1; kt += NST) {
-        step(ic<0>{}, kt, ic<1>{}, ic<1>{});
-        step(ic<1>{}, kt + 1, ic<1>{}, ic<1>{});
-        step(ic<2>{}, kt + 2, ic<1>{}, ic<1>{});
-        if constexpr (NST == 4) step(ic<3>{}, kt + 3, ic<1>{}, ic<1>{});
-        if constexpr (EPI == 2)
+        // (k blocks of the multi-block update start at multiples of kcb, a
+        // multiple of NST = 4, so only the first step of a group opens one)
+        if (MULTI && kt % kcb == 0)
+            step(ic<0>{}, kt, ic<1>{}, ic<1>{}, ic<1>{});
+        else
+            step(ic<0>{}, kt, ic<1>{}, ic<1>{}, ic<0>{});
+        step(ic<1>{}, kt + 1, ic<1>{}, ic<1>{}, ic<0>{});
+        step(ic<2>{}, kt + 2, ic<1>{}, ic<1>{}, ic<0>{});
+        if constexpr (NST == 4) step(ic<3>{}, kt + 3, ic<1>{}, ic<1>{}, ic<0>{});
+        if constexpr (MULTI)
             if ((kt + NST) % kcb == 0) convert((kt + NST) / kcb - 1);
     }
     if constexpr (NST == 4 && !RAGGED) {
-        tail(ic<4>{}, kt);
-        if constexpr (EPI == 2) convert(ktiles / kcb - 1);
+        // the last group of four opens a block only when blocks are four tiles
+        if (MULTI && kcb == 4)
+            tail(ic<4>{}, kt, ic<1>{});
+        else
+            tail(ic<4>{}, kt, ic<0>{});
+        if constexpr (MULTI) convert(ktiles / kcb - 1);
     } else if constexpr (NST == 4) {
         // T = ktiles - kt lies in [3, 6] (the host passes ktiles >= 3).
         const int T = ktiles - kt;
         if (T == 4)
-            tail(ic<4>{}, kt);
+            tail(ic<4>{}, kt, ic<0>{});
         else if (T == 3)
-            tail(ic<3>{}, kt);
+            tail(ic<3>{}, kt, ic<0>{});
         else if (T == 5)
-            tail(ic<5>{}, kt);
+            tail(ic<5>{}, kt, ic<0>{});
         else
-            tail(ic<6>{}, kt);
+            tail(ic<6>{}, kt, ic<0>{});
     } else {
         const int T = ktiles - kt;
         if (T == 2)
-            tail(ic<2>{}, kt);
+            tail(ic<2>{}, kt, ic<0>{});
         else if (T == 3)
-            tail(ic<3>{}, kt);
+            tail(ic<3>{}, kt, ic<0>{});
         else
-            tail(ic<4>{}, kt);
+            tail(ic<4>{}, kt, ic<0>{});
     }
     // ---- epilogue -----------------------------------------------------------
     // int16 corrections (first k chunk only): the column term of each output
@@ -680,7 +711,7 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
                     cv[BF][bb][r] = (int32_t)(int16_t)__builtin_amdgcn_raw_buffer_load_b16(
                         Crs, c_off(lr, lc), 0, 0);
                     rv[BF][bb][r] = *(const uint2 *)(corrA + 2 * (m0 + lr));
-                } else if constexpr (EPI == 2) {
+                } else if constexpr (MULTI) {
                     cv[BF][bb][r] = (int32_t)(int16_t)__builtin_amdgcn_raw_buffer_load_b16(
                         Crs, c_off(lr, lc), 0, 0);
                 } else {
@@ -713,7 +744,7 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
                         0);
                     continue;
                 }
-                if constexpr (EPI == 2) {
+                if constexpr (MULTI) {
                     // the sum of every block's conversion, added modulo 2^16
                     __builtin_amdgcn_raw_buffer_store_b16(
                         (unsigned short)(u32)(cv[BF][bb][r] + (int)run16[i][j][r / 2][r & 1]),
@@ -854,13 +885,24 @@ int launch_srs_packed(const igemm_plan &p, int64_t m, int64_t n, int64_t k, int6
     const int mi = (int)m, ni = (int)n;
     const int epi = (shift & 0xff) | (round_half_up ? 0x100 : 0);
     const dim3 grid((unsigned)(tm * tn));
-    // Two to sixteen whole blocks (k a multiple of kc): one launch that
-    // converts each block in registers and updates C once.
-    if (nblocks >= 2 && nblocks <= 16 && k % kc == 0 && L.k_pad == k) {
-        igemm_packed<2, 128, 128, 64, 64, 4, 2><<<grid, 256, 0, stream>>>(
-            Apk, L.k_pad, a_plane, Bpk, L.k_pad, b_plane, sa, sb, 16384u * (uint32_t)kc,
-            (int32_t *)C, ldc, mi, ni, (int)(k / 64), tm, tn, epi, (int)(kc / 64), (int)L.m_pad,
-            (int)L.n_pad);
+    // Two to sixteen whole blocks (k a multiple of kc) of at most 2048, shift
+    // at most 16: one launch that converts each block in registers (32-bit
+    // integer arithmetic, exact within these bounds) and updates C once.
+    if (nblocks >= 2 && nblocks <= 16 && k % kc == 0 && L.k_pad == k && kc <= 2048 &&
+        shift <= 16) {
+        const int kcb = (int)(kc / 64), ktl = (int)(k / 64);
+        const uint32_t kcon = 16384u * (uint32_t)kc;
+#define IGEMM_SRS_MULTI(E)                                                                 \
+    igemm_packed<2, 128, 128, 64, 64, 4, E><<<grid, 256, 0, stream>>>(                    \
+        Apk, L.k_pad, a_plane, Bpk, L.k_pad, b_plane, sa, sb, kcon, (int32_t *)C, ldc, mi, \
+        ni, ktl, tm, tn, epi, kcb, (int)L.m_pad, (int)L.n_pad)
+        if (shift == 0)
+            IGEMM_SRS_MULTI(2);
+        else if (shift < 8)
+            IGEMM_SRS_MULTI(3);
+        else
+            IGEMM_SRS_MULTI(4);
+#undef IGEMM_SRS_MULTI
         return hipGetLastError() == hipSuccess ? IGEMM_OK : IGEMM_EHIP;
     }
     // Otherwise one launch per block, in order (the update modulo 2^16 makes

@@ -272,6 +272,33 @@ def test_packed_kernel(shape):
         _check(A, B, C, m, n, k, kc, shift, rnd, kernel=kid)
 
 
+@pytest.mark.parametrize("kc", [256, 512, 2048])
+def test_packed_multi_block_conversion_forms(kc):
+    """The one-launch update of 2-16 whole blocks (k_c <= 2048, shift <= 16)
+    converts each block in 32-bit integer arithmetic, in three forms (shift 0,
+    1-7, 8-16). Every form with and without rounding, on full-range operands,
+    on small operands whose block products straddle the saturation bounds at
+    each shift, and on all-extreme operands whose high-limb sums exceed the
+    clamp of the conversion (2^21), against the oracle element by element.
+    Shifts above 16 and blocks above 2048 take one launch per block."""
+    kid = _kid("i16_packed_128x128")
+    m, n = 256, 192
+    nblk = 16 if kc < 2048 else 3
+    k = nblk * kc
+    full = _operands("i16", m, n, k, seed=700 + kc)
+    small = _operands("i16", m, n, k, seed=701 + kc, lo=-300, hi=300)
+    A = np.full((m, k), -32768, dtype=np.int16)
+    B = np.full((k, n), -32768, dtype=np.int16)
+    B[:, ::3] = 32767
+    A[::5, :] = 32767
+    A[1::7, : k // 2] = 0      # blocks with zero high-limb sums next to clamped ones
+    ext = (A, B, full[2])
+    for ops in (full, small, ext):
+        for shift in (0, 1, 7, 8, 9, 15, 16, 17):
+            for rnd in ((False, True) if shift > 0 else (False,)):
+                _check(*ops, m, n, k, kc, shift, rnd, kernel=kid)
+
+
 def test_packed_kernel_alignment_padding_and_extremes():
     kid = _kid("i16_packed_128x128")
     m, n, k = 300, 260, 768
