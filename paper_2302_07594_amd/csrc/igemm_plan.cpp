@@ -158,6 +158,24 @@ bool small_ok(int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, const
            cdiv(k / kBK, kSmallKtMax) <= 65535;
 }
 
+// The ragged variant of the small-output kernel: A's rows at any element
+// alignment and any k >= 1 (A read through registers); B as for the DMA
+// variant but with rows past k read as zeros, so its k-tiles may overrun k.
+static bool small_rg_ok(int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
+                        const void *B, int64_t ldb, int64_t ldc) {
+    const uintptr_t a = (uintptr_t)A, b = (uintptr_t)B;
+    if (k < 1 || a % 2 != 0 || b % 16 != 0 || (ldb * 2) % 16 != 0 || n % 8 != 0) return false;
+    const int64_t ktiles = cdiv(k, kBK);
+    // 32-bit offsets: A's rows and k-tiles (plus a 20-byte read), B's k-tiles
+    // plus a column, 64 rows of C; the resources' ranges.
+    if ((m * lda + ktiles * kBK) * 2 + 32 >= ((int64_t)1 << 31) ||
+        ((ktiles + 1) * kBK * ldb + n) * 2 >= ((int64_t)1 << 31) ||
+        64 * ldc * 4 >= ((int64_t)1 << 31))
+        return false;
+    return cdiv(n, 64) <= kMaxGrid && cdiv(m, 64) <= 65535 &&
+           cdiv(ktiles, kSmallKtMax) <= 65535;
+}
+
 // k elements per launch of the direct kernels: as few launches as the
 // 32768-element limit allows, split evenly in groups of four k-tiles.
 static int64_t direct_chunk(int64_t k) {
@@ -267,7 +285,7 @@ static int auto_kernel(int es, int64_t m, int64_t n, int64_t k, const void *A, i
         return pid;
     if (direct) return K_I16_DIRECT_128x128;
     if (es == 2 && !large && small_pays(m, n, k, num_cu) &&
-        small_ok(m, n, k, A, lda, B, ldb, ldc))
+        (small_ok(m, n, k, A, lda, B, ldb, ldc) || small_rg_ok(m, n, k, A, lda, B, ldb, ldc)))
         return K_I16_SMALL_64x64;
     if (es == 1) {
         StreamShape ss;
@@ -344,10 +362,12 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
         return IGEMM_OK;
     }
     if (id == K_I16_SMALL_64x64) {
-        if (!small_ok(m, n, k, A, lda, B, ldb, ldc)) return IGEMM_EINVAL;
+        // vec_a = 1: A by DMA; 0: the ragged variant
+        const bool dma_a = small_ok(m, n, k, A, lda, B, ldb, ldc);
+        if (!dma_a && !small_rg_ok(m, n, k, A, lda, B, ldb, ldc)) return IGEMM_EINVAL;
         // k-tiles per workgroup: an explicit split asks for that many slices
         // (at least k / 256 of them: a workgroup takes at most four k-tiles).
-        const int64_t ktiles = k / kBK;
+        const int64_t ktiles = cdiv(k, kBK);
         int64_t ktpw = split > 0 ? cdiv(ktiles, split) : small_ktpw(tiles, ktiles);
         if (ktpw > kSmallKtMax) ktpw = kSmallKtMax;
         if (ktpw < 1) ktpw = 1;
@@ -359,7 +379,7 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
         out->split = (int)cdiv(ktiles, ktpw);
         out->tiles = tiles;
         out->grid = tiles * out->split;
-        out->vec_a = 1;
+        out->vec_a = dma_a ? 1 : 0;
         out->vec_b = 1;
         return IGEMM_OK;
     }

@@ -30,7 +30,12 @@
 // multiple of 16 bytes, k a multiple of 64, n a multiple of 8, and 32-bit
 // byte offsets within one k-tile of each operand and within a C tile. The
 // convolution variant gathers A from an NHWC input with a multiple of 64
-// channels (below 2 GB).
+// channels (below 2 GB). The ragged variant (RG) lifts the conditions on A
+// and k: A's rows may start at any element and k may end inside a k-tile
+// (the lowered 7x7 stem layer: k = 147, rows of 294 bytes); each lane then
+// moves its 16-byte chunk of A through registers instead of by DMA, and B
+// (still 16-byte aligned rows, n a multiple of 8) is read through a buffer
+// resource whose range ends at its last element.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -70,11 +75,13 @@ __device__ __forceinline__ u32 div_inv(u32 x, DivU32 dv) {
 // with geometry g, whose channel count is a multiple of 64, so that each
 // k-tile is 64 channels of one filter tap and each of its rows 128
 // contiguous bytes of one input pixel, or zeros outside the image.
-template <int KT, bool SPLIT, bool CONV>
+// RG: ragged A and k (see above); k is the true depth (ktiles = ceil(k / 64)).
+template <int KT, bool SPLIT, bool CONV, bool RG = false>
 __global__ void __launch_bounds__(256, 2)
 igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict__ B,
                 int64_t ldb, int32_t *__restrict__ C, int64_t ldc, int m, int n, int ktiles,
-                ConvGeom g) {
+                ConvGeom g, int k) {
+    static_assert(!(RG && CONV), "the ragged variant reads a row-major A");
     typedef Mfma<32> M;
     typedef M::acc_t acc_t;
     static_assert(KT >= 1 && KT <= 4, "at most four k-tiles in LDS");
@@ -91,7 +98,7 @@ igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict_
 
     // Every kernel argument is named up front so that their loads issue together.
     asm volatile("" ::"s"(A), "s"(lda), "s"(B), "s"(ldb), "s"(C), "s"(ldc), "s"(m), "s"(n),
-                 "s"(ktiles));
+                 "s"(ktiles), "s"(k));
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm0 = (wave >> 1) * 32, wn0 = (wave & 1) * 32;
@@ -142,6 +149,22 @@ igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict_
         }
         Xrs = __builtin_amdgcn_make_buffer_rsrc((void *)A, 0, g.x_bytes, 0x00020000);
     }
+    // RG: A through a resource based at the dword below A (dl: A's offset in
+    // that dword) that ends at A's last element; B through one that ends at
+    // B's last element (its rows past k read as zeros).
+    __amdgpu_buffer_rsrc_t Ars, Brs;
+    u32 a_dl = 0;
+    v4i av[RG ? KT : 1][2];
+    u32 ah[RG ? KT : 1][2];
+    if constexpr (RG) {
+        a_dl = (u32)((uintptr_t)A & 3);
+        const int64_t a_ext = ((int64_t)(m - 1) * lda + k) * 2 + a_dl;
+        const int64_t b_ext = ((int64_t)(k - 1) * ldb + n) * 2;
+        Ars = __builtin_amdgcn_make_buffer_rsrc((void *)(A - a_dl), 0, (int)((a_ext + 3) & ~3),
+                                                0x00020000);
+        Brs = __builtin_amdgcn_make_buffer_rsrc((void *)B, 0, (int)((b_ext + 3) & ~3),
+                                                0x00020000);
+    }
     // Every one of the KT tiles is moved, a short last slice repeating its
     // last tile (read, never multiplied), so that the waits below are fixed
     // counts.
@@ -159,11 +182,26 @@ igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict_
 #pragma unroll
         for (int d = 0; d < 4; ++d) {
             const int dd = d ^ 2;   // B blocks (2, 3), then A blocks (0, 1)
-            if (CONV && dd < 2) continue;
+            if ((CONV || RG) && dd < 2) continue;
             u32 o = off[dd];
             asm volatile("" : "+v"(o));
             const int b = 2 * wave + (dd & 1);
-            dma16((dd < 2 ? ak : bk) + o, (lds_void *)(st + (dd < 2 ? 0 : APL) + b * 1024));
+            if constexpr (RG)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    Brs, (lds_void *)(st + APL + b * 1024), 16, (int)((u32)t * (u32)b_step + o),
+                    0, 0, 0);
+            else
+                dma16((dd < 2 ? ak : bk) + o, (lds_void *)(st + (dd < 2 ? 0 : APL) + b * 1024));
+        }
+        if constexpr (RG) {
+            // this lane's chunk of each of its two A rows: an aligned 16-byte
+            // and 4-byte load (past A's end: zeros), shifted into place below
+#pragma unroll
+            for (int d = 0; d < 2; ++d) {
+                const u32 oa = ((u32)t * 128u + off[d] + a_dl) & ~3u;
+                av[kt][d] = __builtin_amdgcn_raw_buffer_load_b128(Ars, oa, 0, 0);
+                ah[kt][d] = (u32)__builtin_amdgcn_raw_buffer_load_b32(Ars, oa + 16, 0, 0);
+            }
         }
         if constexpr (CONV) {
             // k-tile t: channels [c0, c0 + 64) of filter tap (fy, fx)
@@ -281,15 +319,53 @@ igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict_
         constexpr int N = decltype(cnt)::value;
         __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
     };
+    if constexpr (RG) {
+        // Every A chunk and B tile has landed once only the C loads remain;
+        // each lane shifts its A chunks into place, zeroes the elements at or
+        // beyond k (their B rows are zeros or repeat nothing that counts: a
+        // zero element of A contributes nothing, and the limb identity holds
+        // element by element) and stores them where the DMA would have.
+        wait_vm(ic<NC>{});
 #pragma unroll
-    for (int kt = 0; kt < KT; ++kt) {
-        if (kt == 0) wait_vm(ic<4 * (KT - 1) + NC>{});
-        if (kt == 1) wait_vm(ic<4 * (KT > 2 ? KT - 2 : 0) + NC>{});
-        if (kt == 2) wait_vm(ic<4 * (KT > 3 ? KT - 3 : 0) + NC>{});
-        if (kt == 3) wait_vm(ic<NC>{});
+        for (int kt = 0; kt < KT; ++kt) {
+            const int t = kt0 + min(kt, nkt - 1);
+#pragma unroll
+            for (int d = 0; d < 2; ++d) {
+                const int b = 2 * wave + d;
+                const int row = 8 * b + lane / 8;
+                const u32 sh = ((u32)t * 128u + off[d] + a_dl) & 3u;
+                const v4i x = av[kt][d];
+                const int valid = k - (64 * t + 8 * ((lane % 8) ^ swz_a(row)));
+                v4i y;
+                y.x = (int)(__builtin_amdgcn_alignbyte((u32)x.y, (u32)x.x, sh) &
+                            byte_mask(2 * valid));
+                y.y = (int)(__builtin_amdgcn_alignbyte((u32)x.z, (u32)x.y, sh) &
+                            byte_mask(2 * (valid - 2)));
+                y.z = (int)(__builtin_amdgcn_alignbyte((u32)x.w, (u32)x.z, sh) &
+                            byte_mask(2 * (valid - 4)));
+                y.w = (int)(__builtin_amdgcn_alignbyte(ah[kt][d], (u32)x.w, sh) &
+                            byte_mask(2 * (valid - 6)));
+                *(v4i *)(stage(kt) + b * 1024 + lane * 16) = y;
+            }
+        }
+        // lgkmcnt(0): the stores are in LDS before the barrier
+        __builtin_amdgcn_s_waitcnt((0xf) | (0x7 << 4) | (0x3 << 14));
         __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");  // no LDS read moves above the wait
-        if (kt < nkt) tile(stage(kt));
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt)
+            if (kt < nkt) tile(stage(kt));
+    } else {
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt) {
+            if (kt == 0) wait_vm(ic<4 * (KT - 1) + NC>{});
+            if (kt == 1) wait_vm(ic<4 * (KT > 2 ? KT - 2 : 0) + NC>{});
+            if (kt == 2) wait_vm(ic<4 * (KT > 3 ? KT - 3 : 0) + NC>{});
+            if (kt == 3) wait_vm(ic<NC>{});
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");  // no LDS read moves above the wait
+            if (kt < nkt) tile(stage(kt));
+        }
     }
 
     // ---- epilogue -----------------------------------------------------------
@@ -322,36 +398,46 @@ igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict_
 using namespace small;
 
 // One launch: grid (column tiles, row tiles, k slices of plan.k_chunk).
-template <int KT, bool CONV>
+template <int KT, bool CONV, bool RG>
 static void launch_kt(dim3 grid, bool split, hipStream_t s, const char *A, int64_t lda,
                       const char *B, int64_t ldb, int32_t *C, int64_t ldc, int m, int n,
-                      int ktiles, const ConvGeom &g) {
+                      int ktiles, const ConvGeom &g, int k) {
     if (split)
-        igemm_small_i16<KT, true, CONV><<<grid, 256, 0, s>>>(A, lda, B, ldb, C, ldc, m, n,
-                                                             ktiles, g);
+        igemm_small_i16<KT, true, CONV, RG><<<grid, 256, 0, s>>>(A, lda, B, ldb, C, ldc, m, n,
+                                                                 ktiles, g, k);
     else
-        igemm_small_i16<KT, false, CONV><<<grid, 256, 0, s>>>(A, lda, B, ldb, C, ldc, m, n,
-                                                              ktiles, g);
+        igemm_small_i16<KT, false, CONV, RG><<<grid, 256, 0, s>>>(A, lda, B, ldb, C, ldc, m, n,
+                                                                  ktiles, g, k);
 }
 
-template <bool CONV>
+// RG: the ragged variant (A at any alignment, any k).
+template <bool CONV, bool RG>
 static int launch_any(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
                       int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
                       const ConvGeom &g, void *stream) {
-    const int64_t ktiles = k / 64, ktpw = p.k_chunk / 64;
-    if (k % 64 != 0 || ktpw < 1 || ktpw > 4) return IGEMM_EINVAL;  // the planner prevents it
+    const int64_t ktiles = (k + 63) / 64, ktpw = p.k_chunk / 64;
+    // (the planner prevents both)
+    if ((!RG && k % 64 != 0) || ktpw < 1 || ktpw > 4) return IGEMM_EINVAL;
     const int64_t slices = (ktiles + ktpw - 1) / ktpw;
     const dim3 grid((unsigned)((n + BN - 1) / BN), (unsigned)((m + BM - 1) / BM),
                     (unsigned)slices);
     const char *a = (const char *)A, *b = (const char *)B;
     hipStream_t s = (hipStream_t)stream;
     const bool split = slices > 1;
-    const int mi = (int)m, ni = (int)n, kti = (int)ktiles;
+    const int mi = (int)m, ni = (int)n, kti = (int)ktiles, ki = (int)k;
     switch (ktpw) {
-        case 1: launch_kt<1, CONV>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti, g); break;
-        case 2: launch_kt<2, CONV>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti, g); break;
-        case 3: launch_kt<3, CONV>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti, g); break;
-        default: launch_kt<4, CONV>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti, g); break;
+        case 1:
+            launch_kt<1, CONV, RG>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti, g, ki);
+            break;
+        case 2:
+            launch_kt<2, CONV, RG>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti, g, ki);
+            break;
+        case 3:
+            launch_kt<3, CONV, RG>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti, g, ki);
+            break;
+        default:
+            launch_kt<4, CONV, RG>(grid, split, s, a, lda, b, ldb, C, ldc, mi, ni, kti, g, ki);
+            break;
     }
     return hipGetLastError() == hipSuccess ? IGEMM_OK : IGEMM_EHIP;
 }
@@ -360,12 +446,15 @@ int launch_small(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const voi
                  int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
                  void *stream) {
     const ConvGeom g = {};
-    return launch_any<false>(p, m, n, k, A, lda, B, ldb, C, ldc, g, stream);
+    // vec_a = 0: A's rows are not whole aligned 16-byte chunks, or k ends
+    // inside a k-tile (the ragged variant)
+    if (p.vec_a == 0) return launch_any<false, true>(p, m, n, k, A, lda, B, ldb, C, ldc, g, stream);
+    return launch_any<false, false>(p, m, n, k, A, lda, B, ldb, C, ldc, g, stream);
 }
 
 int launch_small_conv(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const ConvGeom &g,
                       const void *X, const void *W, int32_t *Y, int64_t ldy, void *stream) {
-    return launch_any<true>(p, m, n, k, X, k, W, n, Y, ldy, g, stream);
+    return launch_any<true, false>(p, m, n, k, X, k, W, n, Y, ldy, g, stream);
 }
 
 }  // namespace igemm

@@ -194,9 +194,14 @@ def test_plans_for_workloads():
         assert p["kernel_name"] == "i16_small_64x64", (m, n, k)
         assert p["k_chunk"] == 64 * kt and p["split"] == -(-k // p["k_chunk"])
         assert p["grid"] == p["tiles"] * p["split"] and p["threads"] == 256
-    # k not a multiple of 64, or rows not whole 16 bytes: not the small kernel
+    # k not a multiple of 64, or rows not whole 16 bytes: the small kernel's
+    # ragged variant (A through registers, vec_a = 0); B's rows must still be
+    # whole 16-byte chunks
     for (k, lda) in ((147, 147), (576, 577)):
         p = ig.igemm_query_plan(2, 3136, 64, k, FAKE_A, lda, FAKE_B, 64, FAKE_C, 64)
+        assert p["kernel_name"] == "i16_small_64x64" and p["vec_a"] == 0
+        assert p["split"] == -(-(-(-k // 64)) // (p["k_chunk"] // 64))
+        p = ig.igemm_query_plan(2, 3136, 64, k, FAKE_A, lda, FAKE_B, 65, FAKE_C, 64)
         assert p["kernel_name"] != "i16_small_64x64"
 
 
@@ -583,18 +588,20 @@ def test_srs_noop_and_unsupported(fn):
 
 def test_planner_rules_for_small_int16_outputs():
     """The measured rules for small int16 products on a 256-unit device:
-    aligned operands with whole k-tiles take the small-output kernel; for the
-    fused kernels (here: rows of A not a whole number of 16 bytes), k slices
-    of the 64x64 tiles keep two k-tiles each with the count rounded up, and
-    one k-tile outputs whose 64x64 tiles leave units idle take 16-row tiles;
-    convolutions follow the fused rules."""
+    aligned operands with whole k-tiles take the small-output kernel, and
+    so (its ragged variant) do rows of A that are not whole 16-byte chunks
+    and k that ends inside a k-tile, while B's rows are; convolutions whose
+    input the small kernel cannot gather follow the fused rules (k slices of
+    the 64x64 tiles keep two k-tiles each with the count rounded up)."""
     def plan(m, n, k, lda=None):
         p = ig.igemm_query_plan(2, m, n, k, FAKE_A, lda or k, FAKE_B, n, FAKE_C, n, num_cu=256)
         return ig.igemm_kernel_name(p["kernel"]), p["split"], p["k_chunk"]
     assert plan(3136, 64, 576) == ("i16_small_64x64", 3, 192)
-    assert plan(3136, 64, 576, lda=577) == ("i16_64x64", 5, 128)
-    assert plan(12544, 64, 147) == ("i16_64x64", 2, 128)
-    assert plan(3136, 256, 64, lda=65)[0] == "i16_16x128"
+    # rows of A not whole 16 bytes, or k ending inside a k-tile: the ragged
+    # variant of the small-output kernel
+    assert plan(3136, 64, 576, lda=577) == ("i16_small_64x64", 3, 192)
+    assert plan(12544, 64, 147) == ("i16_small_64x64", 1, 192)
+    assert plan(3136, 256, 64, lda=65) == ("i16_small_64x64", 1, 64)
     assert plan(100352, 256, 64)[0] == "i16_64x64"      # enough 64x64 tiles to fill the units
     # convolutions: the small-output kernel when the channels are a multiple
     # of 64 and X is 16-byte aligned, else the fused rules

@@ -115,3 +115,46 @@ def test_fuzz_small(case):
     _, got = gpu_gemm(A, B, C, m, n, k, kernel=kid, split=split)
     want = oracle_gemm(A, B, C, m, n, k)
     assert np.array_equal(got, want), describe_mismatch(got, want)
+
+
+def _ragged_cases(n_cases=40, seed=2027):
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n_cases):
+        m = int(rng.choice([1, 3, 49, 63, 64, 65, 130, 196, 300, 784]))
+        n = int(rng.choice([1, 2, 8, 9, 16, 32, 64])) * 8
+        k = int(rng.choice([1, 2, 5, 63, 64, 65, 127, 147, 200, 255, 257, 576, 1000, 1153]))
+        split = int(rng.choice([-1, -1, -1, 1, 2, 3, 100]))
+        pad_a = int(rng.integers(0, 10))
+        off_a = int(rng.choice([0, 1, 2, 3, 5]))
+        pads = (pad_a, int(rng.integers(0, 3)) * 8, int(rng.integers(0, 3)))
+        extreme = bool(rng.integers(0, 4) == 0)
+        out.append((i, m, n, k, split, pads, off_a, extreme))
+    return out
+
+
+_RCASES = _ragged_cases()
+
+
+@pytest.mark.parametrize("case", _RCASES, ids=[f"r{c[0]}-{c[1]}x{c[2]}x{c[3]}-s{c[4]}-o{c[6]}"
+                                               for c in _RCASES])
+def test_fuzz_small_ragged(case):
+    """The ragged variant of the small-output int16 kernel: rows of A that
+    start at any element (base offsets of 0-5 elements, any lda) and k that
+    ends inside a k-tile (1 to 1153), with k slice requests, padded C and
+    sometimes all-extreme operands; the automatic plan of such a shape is
+    checked too."""
+    import paper_2302_07594_amd as ig
+    i, m, n, k, split, pads, off_a, extreme = case
+    kid = [x for x in range(ig.igemm_num_kernels())
+           if ig.igemm_kernel_name(x) == "i16_small_64x64"][0]
+    A, B, C = workloads.random_operands("i16", m, n, k, seed=9500 + i, lda=k + pads[0],
+                                        ldb=n + pads[1], ldc=n + pads[2])
+    if extreme:
+        A[:, :] = np.where(A < 0, -32768, 32767).astype(np.int16)
+        B[:, :] = np.where(B < 0, -32768, 32767).astype(np.int16)
+    _, got = gpu_gemm(A, B, C, m, n, k, kernel=kid, split=split, offsets=(off_a, 0, 0))
+    want = oracle_gemm(A, B, C, m, n, k)
+    assert np.array_equal(got, want), describe_mismatch(got, want)
+    _, got = gpu_gemm(A, B, C, m, n, k, offsets=(off_a, 0, 0))
+    assert np.array_equal(got, want), describe_mismatch(got, want)

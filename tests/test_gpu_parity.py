@@ -225,20 +225,26 @@ def test_paper_shape_int16_full():
 
 @pytest.mark.parametrize("name", ["i16_direct_128x128", "i8_direct_256x256", "i16_small_64x64"])
 def test_direct_kernel_preconditions(name):
-    """The direct kernels take k a multiple of 256 (the small-output kernel:
-    of 64), 16-byte aligned operands with rows of whole 16 bytes and n a
-    multiple of 16 bytes of columns; an explicit request outside that is
-    refused, C untouched."""
+    """The direct kernels take k a multiple of 256, 16-byte aligned operands
+    with rows of whole 16 bytes and n a multiple of 16 bytes of columns; an
+    explicit request outside that is refused, C untouched. The small-output
+    kernel needs this of B only: its ragged variant takes A at any alignment
+    and any k (checked against the oracle here)."""
     ig = _ig()
     kid = [i for i in range(ig.igemm_num_kernels()) if ig.igemm_kernel_name(i) == name][0]
     dt = "i16" if name.startswith("i16") else "i8"
+    small = name == "i16_small_64x64"
     for (m, n, k, offs) in ((64, 64, 300 if "direct" in name else 100, (0, 0, 0)),
                             (64, 64, 256, (1, 0, 0)),
                             (64, 64, 256, (0, 1, 0)), (64, 72 if dt == "i8" else 68, 256, (0, 0, 0))):
         A, B, C = workloads.random_operands(dt, m, n, k, seed=77 + k)
         st, got = gpu_gemm(A, B, C, m, n, k, kernel=kid, offsets=offs, check_status=False,
                            workspace=None)
-        assert st == ig.IGEMM_EINVAL and np.array_equal(got, C), (m, n, k, offs)
+        if small and offs[1] == 0 and n % 8 == 0:
+            want = oracle_gemm(A, B, C, m, n, k)
+            assert st == 0 and np.array_equal(got, want), (m, n, k, offs)
+        else:
+            assert st == ig.IGEMM_EINVAL and np.array_equal(got, C), (m, n, k, offs)
 
 
 def test_int16_4096_cube_full():
