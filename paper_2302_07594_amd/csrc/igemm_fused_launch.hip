@@ -59,7 +59,7 @@ int launch_conv(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, co
                 void *stream) {
     (void)es;
     if (p.kernel == K_I16_SMALL_64x64)
-        return launch_small_conv(p, m, n, k, g, X, W, Y, ldy, stream);
+        return launch_small_conv(p, m, n, k, g, gather, X, W, Y, ldy, stream);
     const void *fn = conv_kernel_fn(p.kernel, gather, p.vec_b != 0, p.split > 1);
     if (fn == nullptr) return IGEMM_EINVAL;
     int mi = (int)m, ni = (int)n, ki = (int)k, kc = (int)p.k_chunk;

@@ -135,6 +135,10 @@ bool direct_ok(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t l
 // of 8, and byte offsets that fit its 32-bit lane offsets and grid.
 bool small_ok(int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, const void *B,
               int64_t ldb, int64_t ldc);
+// Its ragged variant (A through registers): A at any element alignment and
+// any k >= 1; B 16-byte aligned with rows of whole 16 bytes, n a multiple of 8.
+bool small_rg_ok(int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, const void *B,
+                 int64_t ldb, int64_t ldc);
 
 // Kernel launches for a validated plan (stream is a hipStream_t). The packed
 // launch needs a workspace of at least plan.workspace_bytes, 256-byte aligned.
@@ -191,12 +195,14 @@ int launch_direct(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, 
                   int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
                   void *stream);
 // The small-output int16 kernel: one launch, k slices of plan.k_chunk; and
-// its convolution variant (A gathered from X, channels a multiple of 64).
+// its convolution variants (A gathered from X: gather 1, whole 64-channel
+// taps by DMA; gather 3, input runs through registers).
 int launch_small(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
                  int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
                  void *stream);
 int launch_small_conv(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const ConvGeom &g,
-                      const void *X, const void *W, int32_t *Y, int64_t ldy, void *stream);
+                      int gather, const void *X, const void *W, int32_t *Y, int64_t ldy,
+                      void *stream);
 int launch_multiply(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
                     int64_t lda, int32_t *C, int64_t ldc, const void *a_part, const void *b_part,
                     void *stream);

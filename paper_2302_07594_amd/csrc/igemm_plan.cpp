@@ -161,7 +161,7 @@ bool small_ok(int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, const
 // The ragged variant of the small-output kernel: A's rows at any element
 // alignment and any k >= 1 (A read through registers); B as for the DMA
 // variant but with rows past k read as zeros, so its k-tiles may overrun k.
-static bool small_rg_ok(int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
+bool small_rg_ok(int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
                         const void *B, int64_t ldb, int64_t ldc) {
     const uintptr_t a = (uintptr_t)A, b = (uintptr_t)B;
     if (k < 1 || a % 2 != 0 || b % 16 != 0 || (ldb * 2) % 16 != 0 || n % 8 != 0) return false;
@@ -587,16 +587,30 @@ int make_conv_plan(int es, const igemm_conv2d_desc *d, const void *X, const void
     if (M > INT_MAX || K > INT_MAX - 65536 || N > INT_MAX) return IGEMM_ENOTSUP;
     // Filter window offsets; (K + 2) * N < 2^62 after the bounds above.
     if ((K + 2) * N * es + 64 >= 0x7fff0000) return IGEMM_ENOTSUP;
+    // Runs: with horizontal dilation 1 the taps of one filter row are
+    // s * c consecutive input elements; the jump to the next filter row must
+    // fit in 31 bits.
+    // (dh as the kernel uses it: 1 for a one-row filter, else below 2^30.)
+    const int64_t dh = d->r == 1 ? 1 : d->dil_h;
+    const int64_t run2 = dh * d->w * d->c - d->s * d->c;
+    // A 16-byte chunk then spans at most two runs if s * c >= 16 / es - 1.
+    const bool runs = (d->s == 1 || d->dil_w == 1) && dh * d->w * d->c < ((int64_t)1 << 30) &&
+                      d->s * d->c < ((int64_t)1 << 30) && d->s * d->c >= 16 / es - 1;
     // The small-output kernel gathers whole 64-channel k-tiles of one filter
-    // tap: channels a multiple of 64, 16-byte aligned input and weights.
+    // tap (channels a multiple of 64, 16-byte aligned input and weights), or,
+    // in its ragged variant, input runs through registers (any channel count;
+    // 16-byte aligned weights with rows of whole 16 bytes).
     const bool small_conv = es == 2 && d->c % 64 == 0 && (uintptr_t)X % 16 == 0 &&
                             small_ok(M, N, K, X, K, W, N, N);
+    const bool small_runs = es == 2 && !small_conv && runs &&
+                            small_rg_ok(M, N, K, X, K, W, N, N);
     int id = kernel;
     if (id < 0) {
         // The rules of the GEMM planner's fused kernels (no packed path: the
         // lowered matrix never exists).
         const int64_t ncu = num_cu > 0 ? num_cu : 256;
-        if (es == 2 && small_conv && small_pays(M, N, K, (int)ncu)) id = K_I16_SMALL_64x64;
+        if (es == 2 && (small_conv || small_runs) && small_pays(M, N, K, (int)ncu))
+            id = K_I16_SMALL_64x64;
         else if (es == 2) {
             if (M <= 16) id = K_I16_16x128;
             else if (M <= 32) id = K_I16_32x128;
@@ -614,21 +628,14 @@ int make_conv_plan(int es, const igemm_conv2d_desc *d, const void *X, const void
     }
     const bool conv_id = id == K_I16_128x128 || id == K_I16_64x64 || id == K_I16_32x128 ||
                          id == K_I16_16x128 || id == K_I8_32x256 || id == K_I8_16x256 ||
-                         (id == K_I16_SMALL_64x64 && small_conv);
+                         (id == K_I16_SMALL_64x64 && (small_conv || small_runs));
     if (!conv_id || kKernels[id].es != es) return IGEMM_EINVAL;
     int st = make_plan(es, M, N, K, X, K, W, N, N, num_cu, id, split, false, out);
     if (st != IGEMM_OK) return st;
     out->vec_a = (((uintptr_t)X % 16) == 0 && (d->c * es) % 16 == 0) ? 1 : 0;
-    // Runs: with horizontal dilation 1 the taps of one filter row are
-    // s * c consecutive input elements; the jump to the next filter row must
-    // fit in 31 bits.
-    // (dh as the kernel uses it: 1 for a one-row filter, else below 2^30.)
-    const int64_t dh = d->r == 1 ? 1 : d->dil_h;
-    const int64_t run2 = dh * d->w * d->c - d->s * d->c;
-    // A 16-byte chunk then spans at most two runs if s * c >= 16 / es - 1.
-    const bool runs = (d->s == 1 || d->dil_w == 1) && dh * d->w * d->c < ((int64_t)1 << 30) &&
-                      d->s * d->c < ((int64_t)1 << 30) && d->s * d->c >= 16 / es - 1;
     *gather = out->vec_a != 0 ? 1 : (runs ? 3 : 2);
+    // the small-output kernel: whole taps by DMA, or runs
+    if (id == K_I16_SMALL_64x64) *gather = small_conv ? 1 : 3;
     g->sc = (int)(d->s * d->c);
     g->run2 = (int)run2;
     g->by_sc = make_div((uint32_t)(d->s * d->c));

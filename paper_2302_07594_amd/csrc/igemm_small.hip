@@ -81,7 +81,8 @@ __global__ void __launch_bounds__(256, 2)
 igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict__ B,
                 int64_t ldb, int32_t *__restrict__ C, int64_t ldc, int m, int n, int ktiles,
                 ConvGeom g, int k) {
-    static_assert(!(RG && CONV), "the ragged variant reads a row-major A");
+    // RG && CONV: the convolution's IM2ROW rows gathered as input runs (any
+    // channel count; horizontal dilation 1 and s c >= 7, checked on the host).
     typedef Mfma<32> M;
     typedef M::acc_t acc_t;
     static_assert(KT >= 1 && KT <= 4, "at most four k-tiles in LDS");
@@ -132,8 +133,11 @@ igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict_
     // pixel (a row past m gets a window outside the image). The input is
     // read through a buffer resource, so that taps outside the image (an
     // offset past its range) land in LDS as zeros.
-    int cv_iy0[2], cv_ix0[2], cv_pix[2];
+    // RG: [cv_lo, cv_hi), the positions of a filter row's run of s c input
+    // elements that lie inside the image horizontally.
+    int cv_iy0[2], cv_ix0[2], cv_pix[2], cv_lo[2], cv_hi[2];
     __amdgpu_buffer_rsrc_t Xrs;
+    u32 x_dl = 0;
     if constexpr (CONV) {
 #pragma unroll
         for (int d = 0; d < 2; ++d) {
@@ -146,9 +150,46 @@ igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict_
             cv_iy0[d] = ok ? (int)oy * g.sh - g.ph : -(1 << 30);
             cv_ix0[d] = (int)ox * g.sw - g.pw;
             cv_pix[d] = ok ? (int)img * g.h * g.w : 0;
+            cv_lo[d] = min(max(-cv_ix0[d], 0), g.s) * g.c;
+            cv_hi[d] = min(max(g.w - cv_ix0[d], 0), g.s) * g.c;
         }
-        Xrs = __builtin_amdgcn_make_buffer_rsrc((void *)A, 0, g.x_bytes, 0x00020000);
+        // RG: based at the dword below X (X is 2-byte aligned)
+        x_dl = RG ? (u32)((uintptr_t)A & 3) : 0u;
+        Xrs = __builtin_amdgcn_make_buffer_rsrc((void *)(A - x_dl), 0,
+                                                (int)(((u32)g.x_bytes + x_dl + 3) & ~3u),
+                                                0x00020000);
     }
+    // RG && CONV: chunk d's 8 IM2ROW elements from column p are the tail of
+    // filter row fy's run (input elements base1 + t) and the head of run
+    // fy + 1 (base2 + t), valid in [a1, b1) and [a2, b2) (inside the image
+    // and before k); a run that starts before the tensor (the first image's
+    // top-left corner, where its leading elements are padding) is read
+    // element by element instead (bad).
+    struct Runs {
+        int base1, base2, a1, b1, a2, b2;
+        bool need1, need2, bad;
+    };
+    auto runs = [&](int d, u32 p) -> Runs {
+        Runs r;
+        const u32 fy = div_inv(p, g.by_sc);
+        const int q1 = (int)(p - fy * (u32)g.sc);
+        const int iy1 = cv_iy0[d] + (int)fy * g.dh;
+        const bool r1 = (u32)iy1 < (u32)g.h, r2 = (u32)(iy1 + g.dh) < (u32)g.h;
+        // (modulo 2^32: exact for rows inside the image, unused otherwise)
+        r.base1 = (int)((u32)cv_pix[d] * (u32)g.c +
+                        ((u32)iy1 * (u32)g.w + (u32)cv_ix0[d]) * (u32)g.c + (u32)q1);
+        r.base2 = (int)((u32)r.base1 + (u32)g.run2);
+        const int split = g.sc - q1;
+        const int kmax = k - (int)p;
+        r.a1 = max(cv_lo[d] - q1, 0);
+        r.b1 = r1 ? min(min(cv_hi[d] - q1, split), kmax) : 0;
+        r.a2 = split + cv_lo[d];
+        r.b2 = r2 ? min(split + cv_hi[d], kmax) : 0;
+        r.need1 = r.a1 < r.b1 && r.a1 < 8;
+        r.need2 = r.a2 < r.b2 && r.a2 < 8;
+        r.bad = (r.need1 && r.base1 < 0) || (r.need2 && r.base2 < 0);
+        return r;
+    };
     // RG: A through a resource based at the dword below A (dl: A's offset in
     // that dword) that ends at A's last element; B through one that ends at
     // B's last element (its rows past k read as zeros).
@@ -156,12 +197,15 @@ igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict_
     u32 a_dl = 0;
     v4i av[RG ? KT : 1][2];
     u32 ah[RG ? KT : 1][2];
+    v4i av2[RG && CONV ? KT : 1][2];
+    u32 ah2[RG && CONV ? KT : 1][2];
     if constexpr (RG) {
         a_dl = (u32)((uintptr_t)A & 3);
         const int64_t a_ext = ((int64_t)(m - 1) * lda + k) * 2 + a_dl;
         const int64_t b_ext = ((int64_t)(k - 1) * ldb + n) * 2;
-        Ars = __builtin_amdgcn_make_buffer_rsrc((void *)(A - a_dl), 0, (int)((a_ext + 3) & ~3),
-                                                0x00020000);
+        if constexpr (!CONV)
+            Ars = __builtin_amdgcn_make_buffer_rsrc((void *)(A - a_dl), 0,
+                                                    (int)((a_ext + 3) & ~3), 0x00020000);
         Brs = __builtin_amdgcn_make_buffer_rsrc((void *)B, 0, (int)((b_ext + 3) & ~3),
                                                 0x00020000);
     }
@@ -193,7 +237,22 @@ igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict_
             else
                 dma16((dd < 2 ? ak : bk) + o, (lds_void *)(st + (dd < 2 ? 0 : APL) + b * 1024));
         }
-        if constexpr (RG) {
+        if constexpr (RG && CONV) {
+            // each run's 16 bytes: an aligned 16-byte and 4-byte load each
+            // (a run not needed, or read element by element, loads nothing)
+#pragma unroll
+            for (int d = 0; d < 2; ++d) {
+                const int row = 8 * (2 * wave + d) + lane / 8;
+                const u32 p = (u32)t * 64u + 8u * (u32)((lane % 8) ^ swz_a(row));
+                const Runs r = runs(d, p);
+                const u32 o1 = r.need1 && !r.bad ? ((u32)r.base1 * 2u + x_dl) & ~3u : 0x80000000u;
+                const u32 o2 = r.need2 && !r.bad ? ((u32)r.base2 * 2u + x_dl) & ~3u : 0x80000000u;
+                av[kt][d] = __builtin_amdgcn_raw_buffer_load_b128(Xrs, o1, 0, 0);
+                ah[kt][d] = (u32)__builtin_amdgcn_raw_buffer_load_b32(Xrs, o1 + 16, 0, 0);
+                av2[kt][d] = __builtin_amdgcn_raw_buffer_load_b128(Xrs, o2, 0, 0);
+                ah2[kt][d] = (u32)__builtin_amdgcn_raw_buffer_load_b32(Xrs, o2 + 16, 0, 0);
+            }
+        } else if constexpr (RG) {
             // this lane's chunk of each of its two A rows: an aligned 16-byte
             // and 4-byte load (past A's end: zeros), shifted into place below
 #pragma unroll
@@ -203,7 +262,7 @@ igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict_
                 ah[kt][d] = (u32)__builtin_amdgcn_raw_buffer_load_b32(Ars, oa + 16, 0, 0);
             }
         }
-        if constexpr (CONV) {
+        if constexpr (CONV && !RG) {
             // k-tile t: channels [c0, c0 + 64) of filter tap (fy, fx)
             const u32 tap = div_inv((u32)t * 64u, g.by_c);
             const int c0 = (int)((u32)t * 64u - tap * (u32)g.c);
@@ -333,6 +392,45 @@ igemm_small_i16(const char *__restrict__ A, int64_t lda, const char *__restrict_
             for (int d = 0; d < 2; ++d) {
                 const int b = 2 * wave + d;
                 const int row = 8 * b + lane / 8;
+                if constexpr (CONV) {
+                    const u32 p = (u32)t * 64u + 8u * (u32)((lane % 8) ^ swz_a(row));
+                    const Runs r = runs(d, p);
+                    u32 w[4] = {0u, 0u, 0u, 0u};
+                    if (r.bad) {
+                        // element by element (every valid element lies inside X)
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) {
+                            const bool in1 = e >= r.a1 && e < r.b1, in2 = e >= r.a2 && e < r.b2;
+                            const u32 o = in1 ? (u32)(r.base1 + e) * 2u + x_dl
+                                              : (in2 ? (u32)(r.base2 + e) * 2u + x_dl
+                                                     : 0x80000000u);
+                            w[e >> 1] |= (u32)__builtin_amdgcn_raw_buffer_load_b16(Xrs, o, 0, 0)
+                                         << (16 * (e & 1));
+                        }
+                    } else {
+                        const u32 s1 = ((u32)r.base1 * 2u + x_dl) & 3u;
+                        const u32 s2 = ((u32)r.base2 * 2u + x_dl) & 3u;
+                        const v4i x1 = av[kt][d], x2 = av2[kt][d];
+                        const u32 v1[4] = {
+                            __builtin_amdgcn_alignbyte((u32)x1.y, (u32)x1.x, s1),
+                            __builtin_amdgcn_alignbyte((u32)x1.z, (u32)x1.y, s1),
+                            __builtin_amdgcn_alignbyte((u32)x1.w, (u32)x1.z, s1),
+                            __builtin_amdgcn_alignbyte(ah[kt][d], (u32)x1.w, s1)};
+                        const u32 v2[4] = {
+                            __builtin_amdgcn_alignbyte((u32)x2.y, (u32)x2.x, s2),
+                            __builtin_amdgcn_alignbyte((u32)x2.z, (u32)x2.y, s2),
+                            __builtin_amdgcn_alignbyte((u32)x2.w, (u32)x2.z, s2),
+                            __builtin_amdgcn_alignbyte(ah2[kt][d], (u32)x2.w, s2)};
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) {
+                            const u32 em = 0xffffu << (16 * (e & 1));
+                            const bool in1 = e >= r.a1 && e < r.b1, in2 = e >= r.a2 && e < r.b2;
+                            w[e >> 1] |= (in1 ? v1[e >> 1] & em : 0u) | (in2 ? v2[e >> 1] & em : 0u);
+                        }
+                    }
+                    *(v4i *)(stage(kt) + b * 1024 + lane * 16) = v4(w[0], w[1], w[2], w[3]);
+                    continue;
+                }
                 const u32 sh = ((u32)t * 128u + off[d] + a_dl) & 3u;
                 const v4i x = av[kt][d];
                 const int valid = k - (64 * t + 8 * ((lane % 8) ^ swz_a(row)));
@@ -453,7 +551,11 @@ int launch_small(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const voi
 }
 
 int launch_small_conv(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const ConvGeom &g,
-                      const void *X, const void *W, int32_t *Y, int64_t ldy, void *stream) {
+                      int gather, const void *X, const void *W, int32_t *Y, int64_t ldy,
+                      void *stream) {
+    // gather 1: whole 64-channel taps by DMA; 3: input runs through registers
+    if (gather == 3) return launch_any<true, true>(p, m, n, k, X, k, W, n, Y, ldy, g, stream);
+    if (gather != 1) return IGEMM_EINVAL;
     return launch_any<true, false>(p, m, n, k, X, k, W, n, Y, ldy, g, stream);
 }
 

@@ -411,11 +411,12 @@ def test_conv_invalid_arguments(es, fn):
         assert fn(_cd(), X + 1, W, Y, 0) == E                        # odd int16 X
     else:
         assert ig.igemm_conv2d_query_plan(1, _cd(), X=X + 1)["vec_a"] == 0
-    # kernels the lowering does not use, or of the other operand type
+    # kernels the lowering does not use, or of the other operand type (the
+    # small-output kernel gathers this 16-channel input as runs)
     for kid in range(ig.igemm_num_kernels()):
         name = ig.igemm_kernel_name(kid)
         conv_ok = name in ("i16_128x128", "i16_64x64", "i16_32x128", "i16_16x128", "i8_32x256",
-                           "i8_16x256")
+                           "i8_16x256", "i16_small_64x64")
         ok = conv_ok and name.startswith("i16" if es == 2 else "i8")
         if not ok:
             with pytest.raises(ig.IgemmError):
@@ -459,20 +460,18 @@ def test_conv_too_large_is_unsupported():
 
 def test_conv_plans_match_lowered_gemm():
     """The six layers' plans: the lowered GEMM shapes, no workspace, the
-    small-output kernel for the layers whose channels are a multiple of 64
-    (aligned tensors), else fused kernels with the 16-byte gather exactly when
-    c * element size is a multiple of 16."""
+    small-output kernel for every layer (whole 64-channel taps by DMA when the
+    channels are a multiple of 64 and the tensors aligned; the 3-channel stem
+    as input runs, vec_a = 0), the fused kernels with the 16-byte gather when
+    the small kernel does not apply and c * element size is a multiple of 16."""
     import workloads
     for case in workloads.CONV2D_CASES:
         m, n, k = case.gemm_shape()
         d = ig.conv_desc(case.n, case.h, case.w, case.c, case.k, case.r, case.s, case.stride,
                          case.pad, case.dil)
         p = ig.igemm_conv2d_query_plan(2, d)
-        if case.c % 64 == 0:
-            assert p["kernel_name"] == "i16_small_64x64", case.name
-            assert p["k_chunk"] <= 256
-        else:
-            assert p["kernel_name"] in ("i16_128x128", "i16_64x64", "i16_32x128", "i16_16x128")
+        assert p["kernel_name"] == "i16_small_64x64", case.name
+        assert p["k_chunk"] <= 256
         assert not p["packed"] and p["workspace_bytes"] == 0
         assert p["vec_a"] == (1 if (case.c * 2) % 16 == 0 else 0)
         assert p["split"] * p["k_chunk"] >= k > (p["split"] - 1) * p["k_chunk"]
@@ -485,7 +484,10 @@ def test_conv_plans_match_lowered_gemm():
     d1 = ig.conv_desc(1, 4, 4, 64, 64, 1, 1)
     assert ig.igemm_conv2d_query_plan(1, d1)["kernel_name"] == "i8_16x256"
     assert ig.igemm_conv2d_query_plan(2, d1)["kernel_name"] == "i16_small_64x64"
-    assert ig.igemm_conv2d_query_plan(2, d1, X=FAKE_X + 2)["kernel_name"] == "i16_16x128"
+    assert ig.igemm_conv2d_query_plan(2, d1, X=FAKE_X + 2)["kernel_name"] == "i16_small_64x64"
+    # weights whose rows are not whole 16 bytes: the fused kernels
+    d2 = ig.conv_desc(1, 4, 4, 64, 60, 1, 1)
+    assert ig.igemm_conv2d_query_plan(2, d2, X=FAKE_X + 2)["kernel_name"] == "i16_16x128"
 
 
 def test_conv_null_descriptor():
@@ -603,15 +605,21 @@ def test_planner_rules_for_small_int16_outputs():
     assert plan(12544, 64, 147) == ("i16_small_64x64", 1, 192)
     assert plan(3136, 256, 64, lda=65) == ("i16_small_64x64", 1, 64)
     assert plan(100352, 256, 64)[0] == "i16_64x64"      # enough 64x64 tiles to fill the units
-    # convolutions: the small-output kernel when the channels are a multiple
-    # of 64 and X is 16-byte aligned, else the fused rules
+    # convolutions: the small-output kernel (whole taps by DMA when the
+    # channels are a multiple of 64 and X is 16-byte aligned, else input runs:
+    # vec_a = 0), and the fused rules where the weights' rows are not whole
+    # 16-byte chunks
     d = ig.conv_desc(1, 56, 56, 64, 256, 1, 1)
     p = ig.igemm_conv2d_query_plan(2, d, num_cu=256)
-    assert ig.igemm_kernel_name(p["kernel"]) == "i16_small_64x64"
+    assert ig.igemm_kernel_name(p["kernel"]) == "i16_small_64x64" and p["vec_a"] == 1
     p = ig.igemm_conv2d_query_plan(2, d, X=2, num_cu=256)
+    assert ig.igemm_kernel_name(p["kernel"]) == "i16_small_64x64" and p["vec_a"] == 0
+    p = ig.igemm_conv2d_query_plan(2, d, X=2, W=2, num_cu=256)
     assert ig.igemm_kernel_name(p["kernel"]) == "i16_16x128"
     d = ig.conv_desc(1, 56, 56, 64, 64, 3, 3, pad=(1, 1))
     p = ig.igemm_conv2d_query_plan(2, d, num_cu=256)
     assert (ig.igemm_kernel_name(p["kernel"]), p["split"]) == ("i16_small_64x64", 3)
     p = ig.igemm_conv2d_query_plan(2, d, X=2, num_cu=256)
+    assert (ig.igemm_kernel_name(p["kernel"]), p["split"]) == ("i16_small_64x64", 3)
+    p = ig.igemm_conv2d_query_plan(2, d, X=2, W=2, num_cu=256)
     assert (ig.igemm_kernel_name(p["kernel"]), p["split"]) == ("i16_64x64", 5)

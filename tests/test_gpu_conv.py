@@ -155,17 +155,46 @@ def test_small_kernel_gather(shape):
                kernel=_kid("i16_small_64x64"), split=split)
 
 
+RUN_SHAPES = [
+    # (n, h, w, c, k, r, s, stride, pad, dil, x_off)
+    (1, 224, 224, 3, 64, 7, 7, (2, 2), (3, 3), (1, 1), 0),   # the stem layer
+    (2, 17, 13, 3, 16, 7, 7, (2, 2), (3, 3), (1, 1), 1),
+    (1, 9, 11, 5, 24, 3, 3, (1, 1), (1, 1), (2, 1), 3),
+    (1, 12, 12, 1, 8, 7, 7, (1, 1), (3, 3), (1, 1), 0),      # s c = 7: two runs per chunk
+    (1, 10, 10, 100, 16, 3, 3, (1, 1), (1, 1), (1, 1), 1),
+    (3, 8, 8, 17, 40, 2, 5, (1, 2), (0, 2), (1, 1), 0),
+    (1, 6, 6, 48, 64, 3, 3, (1, 1), (1, 1), (1, 1), 0),
+    (1, 20, 20, 64, 64, 3, 3, (1, 1), (1, 1), (1, 1), 1),    # 64 channels, misaligned X
+    (1, 9, 9, 8, 16, 3, 1, (1, 1), (1, 0), (2, 3), 0),       # one-column filter, any dilation
+]
+
+
+@pytest.mark.parametrize("shape", RUN_SHAPES, ids=lambda t: "x".join(map(str, t[:7])))
+def test_small_kernel_runs(shape):
+    """The small-output kernel gathering IM2ROW rows as input runs (any
+    channel count or a misaligned input): padding on every side, including
+    runs that would start before the input (the first image's top-left
+    corner), strides, vertical dilation, batches, automatic and forced k
+    slices, against the oracle element by element."""
+    n, h, w, c, k, r, s, stride, pad, dil, x_off = shape
+    for split in (-1, 1, 3, 100):
+        _check("i16", n, h, w, c, k, r, s, stride, pad, dil, seed=950 + sum(shape[:7]),
+               kernel=_kid("i16_small_64x64"), split=split, x_off=x_off)
+    _check("i16", n, h, w, c, k, r, s, stride, pad, dil, seed=951 + sum(shape[:7]), x_off=x_off)
+
+
 def test_small_kernel_gather_preconditions():
-    """Channels not a multiple of 64, output channels not a multiple of 8 or
-    a misaligned input: an explicit request for the small kernel is refused
-    and Y is left alone."""
+    """Output channels not a multiple of 8, misaligned weights, or a filter
+    row that is not one input run (horizontal dilation with several columns
+    and channels not a multiple of 64): an explicit request for the small
+    kernel is refused and Y is left alone."""
     import torch
     ig = _ig()
-    for (c, k, x_off) in ((48, 64, 0), (64, 20, 0), (64, 64, 1)):
+    for (c, k, x_off, w_off, dw) in ((64, 20, 0, 0, 1), (48, 64, 0, 1, 1), (48, 64, 0, 0, 2)):
         X, W, Y = workloads.random_conv_operands("i16", 1, 6, 6, c, k, 3, 3, 6, 6, 5)
-        Xd, Wd = to_device(X, x_off), to_device(W, 0)
+        Xd, Wd = to_device(X, x_off), to_device(W, w_off)
         Yd = torch.from_numpy(Y).cuda()
-        d = ig.conv_desc(1, 6, 6, c, k, 3, 3, (1, 1), (1, 1), (1, 1))
+        d = ig.conv_desc(1, 6, 6, c, k, 3, 3, (1, 1), (1, dw), (1, dw))
         st = ig.igemm_conv2d_ex(2, d, Xd.data_ptr(), Wd.data_ptr(), Yd.data_ptr(),
                                 torch.cuda.current_stream().cuda_stream,
                                 _kid("i16_small_64x64"), -1)
