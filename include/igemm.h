@@ -103,9 +103,10 @@ int igemm_i8(int64_t m, int64_t n, int64_t k,
  *            need a workspace (the _ws calls; IGEMM_EINVAL here) and
  *            ignore split: one launch per 32768 k elements.
  *            The int8 streaming kernel (few rows of A, B read once) rounds
- *            the k range of a slice up to 4, 8, 16 or 32 k-tiles of 64
- *            (16 at most for more than 16 rows), and to 4 k-tiles for
- *            operands whose rows are not aligned.
+ *            the k range of a slice up to 4, 8 or 16 k-tiles of 64 when
+ *            the rows of A and B are whole 16-byte chunks; up to 4, 8, 16
+ *            or 32 (16 at most for more than 16 rows) when B's rows are
+ *            whole 8-byte chunks; and to 4 otherwise.
  * Semantics, memory and errors are those of igemm_i16 / igemm_i8.
  */
 int igemm_i16_ex(int64_t m, int64_t n, int64_t k,
@@ -132,8 +133,7 @@ typedef struct igemm_plan {
     int64_t tiles;     /* C tiles = ceil(m/bm) * ceil(n/bn)                */
     int64_t grid;      /* workgroups launched = tiles * split              */
     int threads;       /* threads per workgroup                            */
-    int vec_a, vec_b;  /* 1 if A / B rows take 16-byte vector loads (the  */
-                       /* streaming kernel: 8-byte loads of B)            */
+    int vec_a, vec_b;  /* 1 if A / B rows take 16-byte vector loads      */
     int limb_products; /* int8 MFMA products per operand pair: 4 or 1      */
     int packed;        /* 1 if operands are packed into a workspace first  */
     int64_t workspace_bytes; /* device workspace the call needs (0: none)  */

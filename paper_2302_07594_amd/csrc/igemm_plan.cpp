@@ -192,11 +192,32 @@ struct StreamShape {
     int64_t spw, slices, tiles;
 };
 static bool stream_shape(int64_t m, int64_t n, int64_t k, int64_t lda, int64_t ldb, bool va,
-                         bool vb, int split, int num_cu, StreamShape *out) {
+                         bool vb16, bool vb, int split, int num_cu, StreamShape *out) {
     int bm = m <= 16 ? 16 : 32;
     const int64_t ksteps = cdiv(k, kBK);
     int64_t spw = 4;
+    if (va && vb16) {
+        // The column-per-wave kernel (A and B rows of whole 16-byte chunks):
+        // eight waves, 4, 8 or 16 steps of 64 k per workgroup, all of them in
+        // LDS at once (up to 160 KB). 8 steps by default; measured with k =
+        // 4096 (us, 4 / 8 / 16 steps): 1 x 4096 4.76 / 4.92 / 5.82, 32 x 4096
+        // 8.98 / 7.34 / 7.79, 1 x 11008 9.94 / 10.16 / 12.79, 32 x 11008
+        // 19.07 / 14.76 / 16.63.
+        const int64_t want = split > 0 ? cdiv(ksteps, split) : 8;
+        while (spw < want && spw < 16) spw *= 2;
+        // (Two 16-row blocks instead of one of 32 rows on 32 x 4096 x 4096,
+        // twice the workgroups: 7.44 us against 7.22; not taken.)
+        if (spw * kBK * ldb + 256 >= 0x7fff0000 || 32 * lda + spw * kBK >= 0x7fff0000)
+            return false;
+        out->bm = bm;
+        out->threads = 512;
+        out->spw = spw;
+        out->slices = cdiv(ksteps, spw);
+        out->tiles = cdiv(m, bm) * cdiv(n, 128);
+        return out->tiles * out->slices <= ((int64_t)1 << 32) / 512 - 1;
+    }
     if (va && vb) {
+        // The register kernel with 8-byte loads of B.
         // Few slices keep the atomic adds into C cheap; enough workgroups keep
         // the loads of B in flight. Measured on the 4096- and 11008-column
         // shapes with k = 4096: 8 steps per workgroup (4 and 16 are up to 10%
@@ -291,7 +312,8 @@ static int auto_kernel(int es, int64_t m, int64_t n, int64_t k, const void *A, i
         StreamShape ss;
         if (m <= 32 && n >= 512 && k >= 256 && (uintptr_t)B % 8 == 0 && ldb % 8 == 0 &&
             (uintptr_t)A % 16 == 0 && lda % 16 == 0 &&
-            stream_shape(m, n, k, lda, ldb, true, true, -1, num_cu, &ss))
+            stream_shape(m, n, k, lda, ldb, true, (uintptr_t)B % 16 == 0 && ldb % 16 == 0, true,
+                         -1, num_cu, &ss))
             return K_I8_STREAM;
         if (m <= 16) return K_I8_16x256;
         if (m <= 32) return K_I8_32x256;
@@ -411,10 +433,14 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
         return IGEMM_OK;
     }
     if (id == K_I8_STREAM) {
+        // vec_b = 1: B's rows are whole 16-byte chunks (with vec_a, the
+        // column-per-wave kernel); otherwise the register kernel
         const bool va = a % 16 == 0 && lda % 16 == 0;
-        const bool vb = b % 8 == 0 && ldb % 8 == 0;
+        const bool vb = b % 16 == 0 && ldb % 16 == 0;
+        const bool vb8 = b % 8 == 0 && ldb % 8 == 0;
         StreamShape ss;
-        if (!stream_shape(m, n, k, lda, ldb, va, vb, split, num_cu, &ss)) return IGEMM_ENOTSUP;
+        if (!stream_shape(m, n, k, lda, ldb, va, vb, vb8, split, num_cu, &ss))
+            return IGEMM_ENOTSUP;
         out->kernel = id;
         out->bm = ss.bm;
         out->bn = 128;

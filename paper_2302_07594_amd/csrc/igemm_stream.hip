@@ -38,6 +38,8 @@ namespace igemm {
 namespace stream {
 
 typedef unsigned int v2u __attribute__((ext_vector_type(2)));
+typedef int v2i_t __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void lds_void;
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 
 // 8 bytes at byte offset `off`: one 8-byte load (VEC) or eight byte loads.
@@ -253,16 +255,176 @@ const void *pick(int waves, int s, bool va, bool vb, bool split) {
     return nullptr;
 }
 
+
+// ---------------------------------------------------------------------------
+// Column-per-wave variant (16-byte aligned operands with rows of whole 16
+// bytes). The register kernel above gives every wave its own k steps of the
+// whole 128-column block, so the waves' partial 16 MB x 128 results must be
+// summed through LDS at the end -- for 32 rows that sum moves more LDS bytes
+// than B itself. Here every wave owns 16 of the 128 columns for all of the
+// workgroup's k range instead, so nothing is summed across waves:
+//   * every byte of the workgroup's B window (SPW steps of 64 rows x 128
+//     columns) and of its A window (16 MB rows x SPW 64 k) moves global ->
+//     LDS by DMA (no registers), all issued at once, then one wait;
+//   * a wave's B operands (its 16 columns x 16 k per lane) come from LDS with
+//     gfx950 transpose reads (ds_read_b64_tr_b8: lane t of each 16-lane group
+//     gathers byte t % 8 of the 8-byte vectors addressed by lanes t / 8 + 2 j,
+//     j = 0..7, i.e. one column for 8 consecutive k rows), its A operands with
+//     ds_read_b128, one v_mfma_i32_16x16x64_i8 per 16-row block and step;
+//   * each wave then adds its 16 MB x 16 block into C (atomic adds when k is
+//     sliced across workgroups, else read-add-write).
+// B's rows past k lie beyond its buffer resource and read as zeros, so the
+// elements of A past k (the next row's, or zeros past A's end) meet zeros; rows
+// of A past m read as zeros and their outputs are not written; columns past
+// n are multiplied and not written.
+// LDS rows: B 128 bytes per k row, 16-byte chunk c of row r at c ^ (r & 7)
+// (the 8 rows of one transpose read hit 8 distinct bank groups); A 64 bytes
+// per row, chunk q of row r at q ^ swz(r).
+template <int MB, int SPW, bool SPLIT>
+__global__ void __launch_bounds__(512)
+igemm_stream_lds(const int8_t *__restrict__ A, int64_t lda, const int8_t *__restrict__ B,
+                 int64_t ldb, int32_t *__restrict__ C, int64_t ldc, int m, int n, int k,
+                 int colblocks, int rowblocks) {
+    constexpr int BST = 64 * 128;      // B bytes per step
+    constexpr int AST = MB * 16 * 64;  // A bytes per step
+    __shared__ __attribute__((aligned(16))) char sB[SPW * BST];
+    __shared__ __attribute__((aligned(16))) char sA[SPW * AST];
+    asm volatile("" ::"s"(A), "s"(lda), "s"(B), "s"(ldb), "s"(C), "s"(ldc), "s"(m), "s"(n),
+                 "s"(k), "s"(colblocks), "s"(rowblocks));
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const unsigned t = blockIdx.x / (unsigned)colblocks;
+    const int cb = (int)(blockIdx.x - t * (unsigned)colblocks);
+    const int rb = (int)(t % (unsigned)rowblocks);
+    const int ks = (int)(t / (unsigned)rowblocks);
+    const int j0 = cb * 128, i0 = rb * 16 * MB, kbeg = ks * SPW * 64;
+    const int mrows = min(m - i0, 16 * MB);
+
+    const int8_t *bw = B + (int64_t)kbeg * ldb + j0;
+    const int64_t b_ext = (int64_t)(k - 1 - kbeg) * ldb + (n - j0);
+    const __amdgpu_buffer_rsrc_t Brs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)bw, 0, (int)min((b_ext + 3) & ~(int64_t)3, (int64_t)0x7ffffff0), 0x00020000);
+    const int8_t *aw = A + (int64_t)i0 * lda + kbeg;
+    const int64_t a_ext = (int64_t)(mrows - 1) * lda + (k - kbeg);
+    const __amdgpu_buffer_rsrc_t Ars = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)aw, 0, (int)min((a_ext + 3) & ~(int64_t)3, (int64_t)0x7ffffff0), 0x00020000);
+
+    // ---- every load of the workgroup, by DMA -------------------------------
+    // B: wave w moves rows 8 w .. 8 w + 7 of each step (lane i: row 8 w + i / 8,
+    // physical chunk i % 8, which holds logical chunk (i % 8) ^ (row & 7)).
+    {
+        const int rr = 8 * wave + lane / 8;
+        const u32 off = (u32)rr * (u32)ldb + 16u * (u32)((lane % 8) ^ (rr & 7));
+#pragma unroll
+        for (int s = 0; s < SPW; ++s)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                Brs, (lds_void *)(sB + s * BST + wave * 1024), 16,
+                (int)(off + (u32)(64 * s) * (u32)ldb), 0, 0, 0);
+    }
+    // A: SPW * MB blocks of 16 rows x 64 bytes, dealt to the waves in turn
+    // (lane i: row i / 4, physical chunk i % 4, logical (i % 4) ^ swz(row)).
+    {
+        const int rr = lane / 4;
+        const u32 off = 16u * (u32)((lane % 4) ^ swz(rr));
+#pragma unroll
+        for (int b0 = 0; b0 < SPW * MB; b0 += 8) {
+            const int b = b0 + wave;
+            if (b < SPW * MB) {
+                const int s = b / MB, mb = b % MB;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    Ars, (lds_void *)(sA + s * AST + mb * 1024), 16,
+                    (int)((u32)(16 * mb + rr) * (u32)lda + (u32)(64 * s) + off), 0, 0, 0);
+            }
+        }
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+
+    // ---- multiply -------------------------------------------------------------
+    // B: lane u of each 16-lane group q addresses k row 16 q + 8 h + u / 2 of the
+    // step at the 8-byte half u % 2 of the wave's logical chunk; A: row
+    // lane % 16 of each 16-row block, k chunk q.
+    const int q = lane >> 4, u = lane & 15;
+    int b_rd[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int row = 16 * q + 8 * h + u / 2;
+        b_rd[h] = row * 128 + 16 * (wave ^ (row & 7)) + 8 * (u % 2);
+    }
+    const int a_rd = u * 64 + 16 * (q ^ swz(u));
+    v4i acc[MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[mb] = v4i{0, 0, 0, 0};
+#pragma unroll
+    for (int s = 0; s < SPW; ++s) {
+        const char *bs = sB + s * BST;
+        const v2i_t b0 = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+            (__attribute__((address_space(3))) v2i_t *)(lds_void *)(bs + b_rd[0]));
+        const v2i_t b1 = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+            (__attribute__((address_space(3))) v2i_t *)(lds_void *)(bs + b_rd[1]));
+        const v4i b = v4i{b0.x, b0.y, b1.x, b1.y};
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+            const v4i a = *(const v4i *)(sA + s * AST + mb * 1024 + a_rd);
+            acc[mb] = Mfma<16>::mma(a, b, acc[mb]);
+        }
+    }
+
+    // ---- into C ---------------------------------------------------------------
+    const int col = j0 + 16 * wave + Mfma<16>::out_col(lane);
+    if (col < n) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = 16 * mb + Mfma<16>::out_row(lane, r);
+                if (row < mrows) {
+                    int32_t *dst = C + (int64_t)(i0 + row) * ldc + col;
+                    if constexpr (SPLIT)
+                        atomicAdd(dst, acc[mb][r]);
+                    else
+                        *dst = (int)((u32)*dst + (u32)acc[mb][r]);
+                }
+            }
+        }
+    }
+}
+
+template <int MB, int SPW>
+const void *pick_lds(bool split) {
+    return split ? (const void *)igemm_stream_lds<MB, SPW, true>
+                 : (const void *)igemm_stream_lds<MB, SPW, false>;
+}
+
+template <int MB>
+const void *pick_lds_spw(int spw, bool split) {
+    if (spw == 4) return pick_lds<MB, 4>(split);
+    if (spw == 8) return pick_lds<MB, 8>(split);
+    if (spw == 16) return pick_lds<MB, 16>(split);
+    return nullptr;
+}
+
 }  // namespace stream
 
 int launch_stream(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
                   int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,
                   void *stream) {
     const int waves = p.threads / 64;
-    const int s = (int)(p.k_chunk / kBK) / waves;
+    const int spw = (int)(p.k_chunk / kBK);
     const bool va = p.vec_a != 0, vb = p.vec_b != 0, split = p.split > 1;
-    const void *fn = p.bm == 16 ? stream::pick<1>(waves, s, va, vb, split)
-                                : stream::pick<2>(waves, s, va, vb, split);
+    const void *fn;
+    if (va && vb) {
+        // the column-per-wave kernel (operands of whole 16-byte rows)
+        fn = p.bm == 16 ? stream::pick_lds_spw<1>(spw, split)
+                        : stream::pick_lds_spw<2>(spw, split);
+    } else {
+        // the register kernel; 8-byte loads of B where its rows allow
+        const bool vb8 = (uintptr_t)B % 8 == 0 && ldb % 8 == 0;
+        const int s = spw / waves;
+        fn = p.bm == 16 ? stream::pick<1>(waves, s, va, vb8, split)
+                        : stream::pick<2>(waves, s, va, vb8, split);
+    }
     if (fn == nullptr) return IGEMM_EINVAL;
     int mi = (int)m, ni = (int)n, ki = (int)k;
     int cbs = (int)((n + 127) / 128), rbs = (int)((m + p.bm - 1) / p.bm);

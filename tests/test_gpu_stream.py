@@ -1,6 +1,7 @@
-"""GPU parity of the int8 streaming kernel (few rows of A, B streamed once
-into registers) against the CPU oracle, bit-exact: every workgroup shape
-(4 or 8 waves, 1, 2 or 4 k-steps each), one and two 16-row MFMA blocks,
+"""GPU parity of the int8 streaming kernels (few rows of A, B streamed once)
+against the CPU oracle, bit-exact: the column-per-wave kernel (operands with
+rows of whole 16-byte chunks; 4, 8 or 16 k-steps per workgroup in LDS) and
+the register kernel (other operands), one and two 16-row MFMA blocks,
 several row blocks, single-slice (read-add-write) and multi-slice (atomic)
 plans, k tails, misaligned operands."""
 import numpy as np
@@ -39,6 +40,38 @@ def _check(m, n, k, split=-1, offsets=(0, 0, 0), pads=(0, 0, 0), seed=0):
 @pytest.mark.parametrize("split", [1, 3, 6, 12, -1])
 def test_stream_workgroup_shapes(m, split):
     _check(m, 1000, 3000, split=split, seed=10 * m + split + 5)
+
+
+# n = 1008 and lda = 3008: rows of A and B whole 16-byte chunks, the last
+# column block partial, k = 3000 ending inside a k-step: the column-per-wave kernel (4, 8 or 16 k-steps per workgroup, all in LDS)
+@pytest.mark.parametrize("m", [1, 8, 16, 17, 32, 33, 70])
+@pytest.mark.parametrize("split", [1, 3, 6, 12, -1])
+def test_stream_lds_workgroup_shapes(m, split):
+    ig = _ig()
+    p = ig.igemm_query_plan(1, m, 1008, 3000, lda=3008, ldb=1008, ldc=1008, kernel=_kid(),
+                            split=split)
+    assert p["vec_a"] == 1 and p["vec_b"] == 1 and p["threads"] == 512
+    assert p["k_chunk"] in (256, 512, 1024)
+    _check(m, 1008, 3000, split=split, pads=(8, 0, 0), seed=10 * m + split + 7)
+
+
+@pytest.mark.parametrize("shape,pads", [((5, 304, 200), (0, 0, 0)), ((32, 144, 64), (16, 16, 1)),
+                                        ((1, 128, 1), (0, 0, 0)), ((17, 2064, 4096), (48, 0, 3))])
+def test_stream_lds_single_slice_and_padding(shape, pads):
+    """The column-per-wave kernel with k inside one workgroup's range (plain
+    read-add-write), short k, padded leading dimensions of whole 16 bytes."""
+    m, n, k = shape
+    _check(m, n, k, split=1, pads=pads, seed=sum(shape) + 1)
+
+
+@pytest.mark.parametrize("value", [-128, 127])
+def test_stream_lds_extremes_long_k(value):
+    m, n, k = 9, 304, 70000
+    A = np.full((m, k), value, np.int8)
+    B = np.full((k, n), value, np.int8)
+    C = np.zeros((m, n), np.int32)
+    _, got = gpu_gemm(A, B, C, m, n, k, kernel=_kid())
+    assert np.all(got == np.int32(value * value * k))
 
 
 @pytest.mark.parametrize("shape", [(5, 300, 200), (32, 129, 64), (20, 777, 17), (1, 128, 1)])
