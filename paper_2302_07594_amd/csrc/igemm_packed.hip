@@ -191,16 +191,25 @@ pack_b(const void *__restrict__ Bv, int64_t ldb, int k, int n, int k_pad, int ks
 
 // ---- exact limb sums per k block, from packed planes ------------------------
 // For the int16-output update (each k block converted on its own): row r of
-// the plane pair (P0 = high limbs, P1 = offset low limbs), rows of k_pad
+// a plane pair (P0 = high limbs, P1 = offset low limbs), rows of k_pad
 // bytes, summed over each block of kc bytes (kc a multiple of 256; blocks
 // past k hold only the zero padding): out[(b * rows + r) * 2] = sum of the
 // high limbs of block b, out[... + 1] = sum of the low limbs (exact int32).
-// One workgroup per row; at most 64 blocks.
+// One workgroup per row, A's rows (pair 0, rows0 of them) then B's (pair 1,
+// in one launch); at most 64 blocks.
 __global__ void __launch_bounds__(256)
-block_sums(const int8_t *__restrict__ P0, const int8_t *__restrict__ P1, int64_t plane_ld,
-           int rows, int k_pad, int kc, int nblocks, uint32_t *__restrict__ out) {
+block_sums(const int8_t *__restrict__ A0, const int8_t *__restrict__ A1, int rows0,
+           uint32_t *__restrict__ out0, const int8_t *__restrict__ B0,
+           const int8_t *__restrict__ B1, int rows1, uint32_t *__restrict__ out1,
+           int64_t plane_ld, int k_pad, int kc, int nblocks) {
     __shared__ int sh[64][2];
-    const int r = blockIdx.x, tid = threadIdx.x;
+    const int tid = threadIdx.x;
+    const bool first = (int)blockIdx.x < rows0;
+    const int r = first ? (int)blockIdx.x : (int)blockIdx.x - rows0;
+    const int rows = first ? rows0 : rows1;
+    const int8_t *P0 = first ? A0 : B0;
+    const int8_t *P1 = first ? A1 : B1;
+    uint32_t *out = first ? out0 : out1;
     for (int i = tid; i < 2 * 64; i += 256) (&sh[0][0])[i] = 0;
     __syncthreads();
     const int8_t *p0 = P0 + (int64_t)r * plane_ld;
@@ -873,12 +882,9 @@ int launch_srs_packed(const igemm_plan &p, int64_t m, int64_t n, int64_t k, int6
     const int64_t a_plane = L.m_pad * L.k_pad, b_plane = L.n_pad * L.k_pad;
     const int kb = nblocks == 1 ? (int)L.k_pad : (int)kc;  // block span in the planes
     uint32_t *sa = sums, *sb = sums + 2 * nblocks * L.m_pad;
-    block_sums<<<dim3((unsigned)L.m_pad), 256, 0, stream>>>(Apk, Apk + a_plane, L.k_pad,
-                                                            (int)L.m_pad, (int)L.k_pad, kb,
-                                                            (int)nblocks, sa);
-    block_sums<<<dim3((unsigned)L.n_pad), 256, 0, stream>>>(Bpk, Bpk + b_plane, L.k_pad,
-                                                            (int)L.n_pad, (int)L.k_pad, kb,
-                                                            (int)nblocks, sb);
+    block_sums<<<dim3((unsigned)(L.m_pad + L.n_pad)), 256, 0, stream>>>(
+        Apk, Apk + a_plane, (int)L.m_pad, sa, Bpk, Bpk + b_plane, (int)L.n_pad, sb, L.k_pad,
+        (int)L.k_pad, kb, (int)nblocks);
     if (hipGetLastError() != hipSuccess) return IGEMM_EHIP;
     const KernelDesc &d = kKernels[p.kernel];
     const int tm = (int)(L.m_pad / d.bm), tn = (int)(L.n_pad / d.bn);
