@@ -190,13 +190,21 @@ static int64_t direct_chunk(int64_t k) {
 struct StreamShape {
     int bm, threads;
     int64_t spw, slices, tiles;
+    bool lds;  // the column-per-wave kernel (else the register kernel)
 };
 static bool stream_shape(int64_t m, int64_t n, int64_t k, int64_t lda, int64_t ldb, bool va,
                          bool vb16, bool vb, int split, int num_cu, StreamShape *out) {
     int bm = m <= 16 ? 16 : 32;
     const int64_t ksteps = cdiv(k, kBK);
     int64_t spw = 4;
-    if (va && vb16) {
+    // 17 to 32 rows over few column blocks (at most one workgroup per compute
+    // unit with 32-row blocks of 8 steps) take the register kernel's two
+    // 16-row blocks of 16 steps even when the column-per-wave kernel could
+    // run: 32 x 4096 x 4096 7.07-7.26 us against 7.22-7.71 us.
+    const bool two_blocks =
+        va && vb && bm == 32 && split <= 0 && cdiv(n, 128) * cdiv(ksteps, 8) <= num_cu;
+    out->lds = va && vb16 && !two_blocks;
+    if (out->lds) {
         // The column-per-wave kernel (A and B rows of whole 16-byte chunks):
         // eight waves, 4, 8 or 16 steps of 64 k per workgroup, all of them in
         // LDS at once (up to 160 KB). 8 steps by default; measured with k =
@@ -205,8 +213,7 @@ static bool stream_shape(int64_t m, int64_t n, int64_t k, int64_t lda, int64_t l
         // 19.07 / 14.76 / 16.63.
         const int64_t want = split > 0 ? cdiv(ksteps, split) : 8;
         while (spw < want && spw < 16) spw *= 2;
-        // (Two 16-row blocks instead of one of 32 rows on 32 x 4096 x 4096,
-        // twice the workgroups: 7.44 us against 7.22; not taken.)
+        // (This kernel with two 16-row blocks took 7.44 us on 32 x 4096 x 4096.)
         if (spw * kBK * ldb + 256 >= 0x7fff0000 || 32 * lda + spw * kBK >= 0x7fff0000)
             return false;
         out->bm = bm;
@@ -228,7 +235,7 @@ static bool stream_shape(int64_t m, int64_t n, int64_t k, int64_t lda, int64_t l
         // 16 steps instead, half the adds per workgroup and no two-phase
         // reduction (32 x 4096 x 4096: 7.1 us against 8.2 us; on 32 x 11008,
         // where B's second pass costs bandwidth, 16.8 against 15.2 us).
-        if (bm == 32 && split <= 0 && cdiv(n, 128) * cdiv(ksteps, 8) <= num_cu) {
+        if (two_blocks) {
             bm = 16;
             want = 16;
         }
@@ -450,7 +457,8 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
         out->grid = ss.tiles * ss.slices;
         out->threads = ss.threads;
         out->vec_a = va;
-        out->vec_b = vb;
+        // vec_b = 1: the column-per-wave kernel (B's rows whole 16-byte chunks)
+        out->vec_b = ss.lds ? 1 : 0;
         return IGEMM_OK;
     }
     const int64_t ktiles = cdiv(k, kBK);
