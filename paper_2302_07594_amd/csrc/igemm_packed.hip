@@ -550,7 +550,8 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     //   shift <  8: y is clamped to [-2^22, 2^22] (beyond it |v| >= 2^30 - 255
     //               saturates for every shift < 8) and v = 256 y + (L & 255)
     //               is formed exactly, then (v + half) >> s.
-    // Arithmetic shifts right are floors; half = 2^(s-1) with rounding, else 0.
+    // Arithmetic shifts right are floors; half = 2^(s-1) with rounding, else 0;
+    // the saturation to int16 is that of v_cvt_pk_i16_i32.
     auto convert = [&](int q) {
         if constexpr (MULTI) {
             const int sh = epi & 0xff;
@@ -578,7 +579,7 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
                 for (int j = 0; j < TN; ++j) {
 #pragma unroll
                     for (int r2 = 0; r2 < M::REGS / 2; ++r2) {
-                        u32 t16[2];
+                        int t32[2];
 #pragma unroll
                         for (int h = 0; h < 2; ++h) {
                             const int r = 2 * r2 + h;
@@ -595,9 +596,11 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
                                 t = (int)perm((u32)yc, (u32)L, 0x06050400u);
                                 if constexpr (SMODE == 1) t = (t + half) >> sh;
                             }
-                            t16[h] = (u32)min(max(t, -32768), 32767);
+                            t32[h] = t;
                         }
-                        run16[i][j][r2] += s2{(short)t16[0], (short)t16[1]};
+                        // v_cvt_pk_i16_i32 saturates each to int16 (checked on the
+                        // device); the running sums wrap modulo 2^16
+                        run16[i][j][r2] += __builtin_amdgcn_cvt_pk_i16(t32[0], t32[1]);
                     }
                     __builtin_amdgcn_sched_barrier(0);
                 }
