@@ -282,3 +282,27 @@ def test_wrapper_workspace_on_side_stream(kind):
     got = Cd.cpu().numpy()
     assert np.array_equal(got, want), describe_mismatch(got, want)
     del junk
+
+
+# Short k over many tiles: k-tile counts 1 to 9 around the boundaries (the
+# ragged tail variants and the zero padding up to a multiple of four tiles),
+# ragged m and n.
+SHORT_K = [2, 63, 64, 65, 128, 200, 256, 290, 383, 448, 511, 512, 513]
+
+
+@pytest.mark.parametrize("k", SHORT_K)
+def test_packed_int16_short_k_tiles(k):
+    m, n = 700, 650
+    A, B, C = workloads.random_operands("i16", m, n, k, seed=900 + k)
+    _check("i16", A, B, C, m, n, k)
+
+
+@pytest.mark.parametrize("value", [-32768, 32767])
+def test_packed_int16_short_k_extremes(value):
+    """Every limb sum at its bound with k = 512 and C nonzero."""
+    m, n, k = 200, 130, 512
+    A = np.full((m, k), value, np.int16)
+    B = np.full((k, n), -value if value > 0 else value, np.int16)
+    C = np.full((m, n), -7, np.int32)
+    got = _check("i16", A, B, C, m, n, k)
+    assert np.all(got == got[0, 0])
