@@ -275,12 +275,17 @@ int run_srs(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda,
         if (st != IGEMM_OK) return st;
         if (pp.packed) {
             if (workspace_bytes < need) return IGEMM_ENOMEM;
-            st = pack_both(es, pp, m, n, k, A, lda, B, ldb, workspace, stream);
+            // the pack kernels also take the per-block limb sums
+            char *wb = (char *)workspace + pp.packed_a_bytes;
+            uint32_t *sums = (uint32_t *)((char *)workspace + pp.workspace_bytes);
+            st = launch_pack_a(es, pp, m, n, k, A, lda, workspace, wb, stream, sums, blk,
+                               nblocks);
             if (st != IGEMM_OK) return st;
-            return launch_srs_packed(pp, m, n, k, blk, nblocks, A, lda, C, ldc, workspace,
-                                     (const char *)workspace + pp.packed_a_bytes,
-                                     (uint32_t *)((char *)workspace + pp.workspace_bytes), shift,
-                                     round_half_up, stream);
+            st = launch_pack_b(es, pp, m, n, k, A, lda, B, ldb, wb, false, stream, sums, blk,
+                               nblocks);
+            if (st != IGEMM_OK) return st;
+            return launch_srs_packed(pp, m, n, k, blk, nblocks, A, lda, C, ldc, workspace, wb,
+                                     sums, shift, round_half_up, stream);
         }
     }
     for (int pass = 0; pass < 2; ++pass) {

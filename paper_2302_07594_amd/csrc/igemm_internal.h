@@ -166,9 +166,9 @@ int launch_conv(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, co
                 int gather, const void *X, const void *W, int32_t *Y, int64_t ldy,
                 void *stream);
 // The int16-output update on packed int16 operands (a packed plan whose
-// workspace the pack kernels have filled): exact per-block limb sums of the
-// packed planes into `sums` (srs_sums_bytes), then one multiply launch per
-// block. nblocks <= 64; blocks of kc elements, a multiple of 256 unless
+// workspace the pack kernels have filled, with the exact per-block limb sums
+// of both operands in `sums`, srs_sums_bytes): one multiply launch, or one
+// per block. nblocks <= 64; blocks of kc elements, a multiple of 256 unless
 // there is one block.
 int64_t srs_sums_bytes(const igemm_plan &p, int64_t m, int64_t n, int64_t k, int64_t nblocks,
                        const void *A, int64_t lda);
@@ -184,12 +184,17 @@ int launch_srs(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, con
 // The packed path: pack A into an A part (optionally clearing the B part's
 // column corrections, which pack_b then adds into), pack B into a B part
 // (clear_corr: clear the corrections itself first), multiply (one launch per
-// k chunk) from the two parts.
+// k chunk) from the two parts. For the int16-output update (sums given, int16
+// only) the pack kernels also write the exact limb sums of each block of kc
+// elements (one block: all of k) into sums, A's then B's, as
+// launch_srs_packed reads them.
 int launch_pack_a(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
-                  int64_t lda, void *a_part, void *b_part_to_clear, void *stream);
+                  int64_t lda, void *a_part, void *b_part_to_clear, void *stream,
+                  uint32_t *sums = nullptr, int64_t kc = 0, int64_t nblocks = 0);
 int launch_pack_b(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
                   int64_t lda, const void *B, int64_t ldb, void *b_part, bool clear_corr,
-                  void *stream);
+                  void *stream, uint32_t *sums = nullptr, int64_t kc = 0,
+                  int64_t nblocks = 0);
 // The direct kernel: one launch per k chunk of plan.k_chunk elements.
 int launch_direct(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
                   int64_t lda, const void *B, int64_t ldb, int32_t *C, int64_t ldc,

@@ -52,15 +52,28 @@ __global__ void __launch_bounds__(256) clear_u32(uint32_t *__restrict__ p, int n
 // ---- pack A, int16: one workgroup per padded row ---------------------------
 // Writes Ah/Al[i][0, k_pad) and corrA[i] = 32768*sum(h) + 128*sum(l) mod 2^32,
 // and, if corrB is given, zeroes corrB[0, n_pad).
+// For the int16-output update (bsA given): also the exact per-block limb
+// sums of the row, block b = [b bspan, (b + 1) bspan) of the planes (bspan a
+// multiple of 256, at most 64 blocks), at bsA[2 (b m_pad + i)] (high limbs)
+// and + 1 (offset low limbs), m_pad = gridDim.x; and zeroes clr[0, nclr)
+// (B's block sums, which pack_b adds into).
 template <bool VEC>
 __global__ void __launch_bounds__(256)
 pack_a_i16(const int16_t *__restrict__ A, int64_t lda, int m, int k, int k_pad,
            int8_t *__restrict__ Ah, int8_t *__restrict__ Al, uint32_t *__restrict__ corrA,
-           uint32_t *__restrict__ corrB, int n_pad) {
+           uint32_t *__restrict__ corrB, int n_pad, uint32_t *__restrict__ bsA, int bspan,
+           int nblocks, uint32_t *__restrict__ clr, int nclr) {
     const int i = blockIdx.x, tid = threadIdx.x;
     // Clear the column corrections that pack_b (next on the stream) adds into.
     if (corrB != nullptr)
         for (int j = i * 256 + tid; j < n_pad; j += gridDim.x * 256) corrB[j] = 0u;
+    if (clr != nullptr)
+        for (int j = i * 256 + tid; j < nclr; j += gridDim.x * 256) clr[j] = 0u;
+    __shared__ int bsum[64][2];
+    if (bsA != nullptr) {
+        if (tid < 128) (&bsum[0][0])[tid] = 0;
+        __syncthreads();
+    }
     const int len = i < m ? k : 0;
     const int16_t *arow = A + (int64_t)(i < m ? i : 0) * lda;
     int8_t *hrow = Ah + (int64_t)i * k_pad;
@@ -76,8 +89,19 @@ pack_a_i16(const int16_t *__restrict__ A, int64_t lda, int m, int k, int k_pad,
         const u32 l1 = (perm(y3, y2, 0x06040200u) ^ 0x80808080u) & m1;
         sh = sum4(h1, sum4(h0, sh));
         sl = sum4(l1, sum4(l0, sl));
+        if (bsA != nullptr) {
+            atomicAdd(&bsum[e0 / bspan][0], sum4(h1, sum4(h0, 0)));
+            atomicAdd(&bsum[e0 / bspan][1], sum4(l1, sum4(l0, 0)));
+        }
         *(uint2 *)(hrow + e0) = make_uint2(h0, h1);
         *(uint2 *)(lrow + e0) = make_uint2(l0, l1);
+    }
+    if (bsA != nullptr) {
+        __syncthreads();
+        for (int b = tid; b < nblocks; b += 256) {
+            bsA[((int64_t)b * gridDim.x + i) * 2] = (u32)bsum[b][0];
+            bsA[((int64_t)b * gridDim.x + i) * 2 + 1] = (u32)bsum[b][1];
+        }
     }
     __shared__ int red[2][4];
     sh = wave_sum(sh);
@@ -113,11 +137,16 @@ pack_a_i8(const int8_t *__restrict__ A, int64_t lda, int m, int k, int k_pad,
 // bytes, transposes 4x4 byte blocks in registers (and for int16 separates the
 // limb planes), parks the per-column dwords in LDS, and the workgroup writes
 // each column's k run out contiguously. For int16 the per-column limb sums of
-// the slice are added into corrB[col] (zeroed by pack_a_i16, which runs first).
+// the slice are added into corrB[col] (zeroed by pack_a_i16, which runs first),
+// and, for the int16-output update (bsB given), the exact per-block limb sums
+// of the slice into bsB[2 (b n_pad + col)] and + 1 (zeroed by pack_a_i16;
+// blocks of bspan rows, a multiple of 128, so that each pass of 128 rows lies
+// in one block).
 template <int ES, bool VEC>
 __global__ void __launch_bounds__(256)
 pack_b(const void *__restrict__ Bv, int64_t ldb, int k, int n, int k_pad, int kspan, int n_pad,
-       int8_t *__restrict__ Bp0, int8_t *__restrict__ Bp1, uint32_t *__restrict__ corrB) {
+       int8_t *__restrict__ Bp0, int8_t *__restrict__ Bp1, uint32_t *__restrict__ corrB,
+       uint32_t *__restrict__ bsB = nullptr, int bspan = 0) {
     constexpr int P = ES;                 // output planes
     constexpr int CC = ES == 2 ? 8 : 4;   // 16-byte column chunks per workgroup (64 columns)
     constexpr int RG = 256 / CC;          // row groups of 4 rows
@@ -132,8 +161,32 @@ pack_b(const void *__restrict__ Bv, int64_t ldb, int k, int n, int k_pad, int ks
     const int kb = blockIdx.y * kspan, ke = min(k_pad, kb + kspan);
     const int nlen = n - j0;
     int shh[8] = {0, 0, 0, 0, 0, 0, 0, 0}, sll[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    // this thread's column sums of the current block (bsB)
+    int bh[8] = {0, 0, 0, 0, 0, 0, 0, 0}, bl[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    __shared__ int bcs[64][2];
+    // Adds the current block's column sums into bsB (uniform: every thread
+    // calls it at the same pass).
+    auto flush = [&](int b) {
+        if (tid < 128) (&bcs[0][0])[tid] = 0;
+        __syncthreads();
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            atomicAdd(&bcs[cc * 8 + c][0], bh[c]);
+            atomicAdd(&bcs[cc * 8 + c][1], bl[c]);
+            bh[c] = 0;
+            bl[c] = 0;
+        }
+        __syncthreads();
+        if (tid < 64) {
+            atomicAdd(&bsB[((int64_t)b * n_pad + j0 + tid) * 2], (u32)bcs[tid][0]);
+            atomicAdd(&bsB[((int64_t)b * n_pad + j0 + tid) * 2 + 1], (u32)bcs[tid][1]);
+        }
+        __syncthreads();
+    };
     if (tid < 64) cs[tid] = 0;
     for (int p0 = kb; p0 < ke; p0 += ROWS) {
+        if constexpr (ES == 2)
+            if (bsB != nullptr && p0 > kb && p0 % bspan == 0) flush(p0 / bspan - 1);
         v4i x[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -159,6 +212,10 @@ pack_b(const void *__restrict__ Bv, int64_t ldb, int k, int n, int k_pad, int ks
                     const int c = 2 * d + h;
                     shh[c] = sum4(hi, shh[c]);
                     sll[c] = sum4(lo, sll[c]);
+                    if (bsB != nullptr) {
+                        bh[c] = sum4(hi, bh[c]);
+                        bl[c] = sum4(lo, bl[c]);
+                    }
                     T[0][cc * 8 + c][rg] = hi;
                     T[1][cc * 8 + c][rg] = lo;
                 }
@@ -182,51 +239,11 @@ pack_b(const void *__restrict__ Bv, int64_t ldb, int k, int n, int k_pad, int ks
         __syncthreads();
     }
     if constexpr (ES == 2) {
+        if (bsB != nullptr && ke > kb) flush((ke - 1) / bspan);
 #pragma unroll
         for (int c = 0; c < 8; ++c) atomicAdd(&cs[cc * 8 + c], (int)(32768u * (u32)shh[c] + 128u * (u32)sll[c]));
         __syncthreads();
         if (tid < 64) atomicAdd(&corrB[j0 + tid], (u32)cs[tid]);
-    }
-}
-
-// ---- exact limb sums per k block, from packed planes ------------------------
-// For the int16-output update (each k block converted on its own): row r of
-// a plane pair (P0 = high limbs, P1 = offset low limbs), rows of k_pad
-// bytes, summed over each block of kc bytes (kc a multiple of 256; blocks
-// past k hold only the zero padding): out[(b * rows + r) * 2] = sum of the
-// high limbs of block b, out[... + 1] = sum of the low limbs (exact int32).
-// One workgroup per row, A's rows (pair 0, rows0 of them) then B's (pair 1,
-// in one launch); at most 64 blocks.
-__global__ void __launch_bounds__(256)
-block_sums(const int8_t *__restrict__ A0, const int8_t *__restrict__ A1, int rows0,
-           uint32_t *__restrict__ out0, const int8_t *__restrict__ B0,
-           const int8_t *__restrict__ B1, int rows1, uint32_t *__restrict__ out1,
-           int64_t plane_ld, int k_pad, int kc, int nblocks) {
-    __shared__ int sh[64][2];
-    const int tid = threadIdx.x;
-    const bool first = (int)blockIdx.x < rows0;
-    const int r = first ? (int)blockIdx.x : (int)blockIdx.x - rows0;
-    const int rows = first ? rows0 : rows1;
-    const int8_t *P0 = first ? A0 : B0;
-    const int8_t *P1 = first ? A1 : B1;
-    uint32_t *out = first ? out0 : out1;
-    for (int i = tid; i < 2 * 64; i += 256) (&sh[0][0])[i] = 0;
-    __syncthreads();
-    const int8_t *p0 = P0 + (int64_t)r * plane_ld;
-    const int8_t *p1 = P1 + (int64_t)r * plane_ld;
-    for (int e = tid * 16; e < k_pad; e += 256 * 16) {
-        const int b = e / kc;
-        const v4i x0 = *(const v4i *)(p0 + e), x1 = *(const v4i *)(p1 + e);
-        int s0 = sum4((u32)x0.x, 0), s1 = sum4((u32)x1.x, 0);
-        s0 = sum4((u32)x0.w, sum4((u32)x0.z, sum4((u32)x0.y, s0)));
-        s1 = sum4((u32)x1.w, sum4((u32)x1.z, sum4((u32)x1.y, s1)));
-        atomicAdd(&sh[b][0], s0);
-        atomicAdd(&sh[b][1], s1);
-    }
-    __syncthreads();
-    for (int b = tid; b < nblocks; b += 256) {
-        out[((int64_t)b * rows + r) * 2] = (u32)sh[b][0];
-        out[((int64_t)b * rows + r) * 2 + 1] = (u32)sh[b][1];
     }
 }
 
@@ -245,7 +262,7 @@ block_sums(const int8_t *__restrict__ A0, const int8_t *__restrict__ A1, int row
 // The k range is kcb-tile blocks (kcb a multiple of 4 and at most 32, i.e.
 // k_c <= 2048; ktiles = nblocks kcb, at most 16 blocks; shift <= 16);
 // corrA / corrB hold the exact (high, low) limb sums of
-// every block (block q at 2 (q m_pad + row), as block_sums writes them),
+// every block (block q at 2 (q m_pad + row), as the pack kernels write them),
 // staged in LDS at the start; kconst is 16384 kcb 64. At the end of each
 // block the lane converts its accumulators into the block's int16
 // contribution (the conversion of EPI 1) and adds it to running sums kept in
@@ -282,8 +299,9 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     constexpr int DPA = NBA / NW, DPB = NBB / NW, DPW = DPA + DPB;
     static_assert(DPW <= 15, "outstanding DMA count fits s_waitcnt");
     static_assert(EPI == 0 || ES == 2, "the int16-output update is for int16 operands");
-    // EPI 2-4: the multi-block update; its shift range selects the form of the
-    // conversion (2: shift 0, 3: shift 1-7, 4: shift 8-16).
+    // EPI 2-5: the multi-block update; its shift range selects the form of the
+    // conversion (2: shift 0, 3: shift 1-7, 4: shift 8-16, 5: shift 0 with
+    // blocks of 256).
     constexpr bool MULTI = EPI >= 2;
     constexpr int SMODE = EPI - 2;
     static_assert(!MULTI || !RAGGED, "blocks of whole groups of four k-tiles");
@@ -552,6 +570,12 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     //               is formed exactly, then (v + half) >> s.
     // Arithmetic shifts right are floors; half = 2^(s-1) with rounding, else 0;
     // the saturation to int16 is that of v_cvt_pk_i16_i32.
+    // Shift 0 (the paper's case) takes a shorter form: y is saturated to int16
+    // (a pair at a time), v' = 256 sat16(y) + (L & 255) is formed exactly from
+    // its bytes (sign-extended), and sat16(v') = sat16(v): v' = v when y fits,
+    // and otherwise both lie beyond the int16 range on the same side. With
+    // blocks of 256 (EPI 5) |S_hh| <= 2^22, so y = 256 S_hh + X + (L >> 8) fits
+    // in 32 bits (|y| < 2^30 + 2^25) without the clamp of S_hh.
     auto convert = [&](int q) {
         if constexpr (MULTI) {
             const int sh = epi & 0xff;
@@ -579,6 +603,26 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
                 for (int j = 0; j < TN; ++j) {
 #pragma unroll
                     for (int r2 = 0; r2 < M::REGS / 2; ++r2) {
+                        if constexpr (SMODE == 0 || SMODE == 3) {
+                            int y2[2], L2[2];
+#pragma unroll
+                            for (int h = 0; h < 2; ++h) {
+                                const int r = 2 * r2 + h;
+                                const int hh =
+                                    SMODE == 3 ? acc[0][i][j][r]
+                                               : min(max(acc[0][i][j][r], -(1 << 21)), 1 << 21);
+                                L2[h] = acc[2][i][j][r] + rowL[r] + colL[j];
+                                y2[h] = (int)((u32)hh << 8) + acc[1][i][j][r] + rowM[r] +
+                                        colM[j] + (L2[h] >> 8);
+                            }
+                            const u32 yp =
+                                __builtin_bit_cast(u32, __builtin_amdgcn_cvt_pk_i16(y2[0], y2[1]));
+                            // bytes: the lowest of L, the two of sat16(y), its sign
+                            const int v0 = (int)perm(yp, (u32)L2[0], 0x0A050400u);
+                            const int v1 = (int)perm(yp, (u32)L2[1], 0x0B070600u);
+                            run16[i][j][r2] += __builtin_amdgcn_cvt_pk_i16(v0, v1);
+                            continue;
+                        }
                         int t32[2];
 #pragma unroll
                         for (int h = 0; h < 2; ++h) {
@@ -800,7 +844,8 @@ using namespace packed;
 // Host side of the packed path.
 
 int launch_pack_a(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
-                  int64_t lda, void *a_part, void *b_part_to_clear, void *stream_) {
+                  int64_t lda, void *a_part, void *b_part_to_clear, void *stream_,
+                  uint32_t *sums, int64_t kc, int64_t nblocks) {
     hipStream_t stream = (hipStream_t)stream_;
     PackedLayout L;
     packed_layout(es, m, n, k, p.kernel, A, lda, &L);
@@ -818,10 +863,17 @@ int launch_pack_a(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, 
     if (es == 2) {
         int8_t *Al = Apk + a_plane;
         const int16_t *A16 = (const int16_t *)A;
+        // int16-output update: A's block sums, and B's cleared for pack_b
+        const int bspan = sums != nullptr ? (int)(nblocks == 1 ? L.k_pad : kc) : 0;
+        const int nb = sums != nullptr ? (int)nblocks : 0;
+        uint32_t *clr = sums != nullptr ? sums + 2 * nblocks * L.m_pad : nullptr;
+        const int nclr = sums != nullptr ? (int)(2 * nblocks * L.n_pad) : 0;
         if (va)
-            pack_a_i16<true><<<g, 256, 0, stream>>>(A16, lda, mi, ki, kp, Apk, Al, corrA, corrB, np);
+            pack_a_i16<true><<<g, 256, 0, stream>>>(A16, lda, mi, ki, kp, Apk, Al, corrA, corrB, np,
+                                                    sums, bspan, nb, clr, nclr);
         else
-            pack_a_i16<false><<<g, 256, 0, stream>>>(A16, lda, mi, ki, kp, Apk, Al, corrA, corrB, np);
+            pack_a_i16<false><<<g, 256, 0, stream>>>(A16, lda, mi, ki, kp, Apk, Al, corrA, corrB,
+                                                     np, sums, bspan, nb, clr, nclr);
     } else {
         const int8_t *A8 = (const int8_t *)A;
         if (va)
@@ -834,7 +886,7 @@ int launch_pack_a(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, 
 
 int launch_pack_b(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
                   int64_t lda, const void *B, int64_t ldb, void *b_part, bool clear_corr,
-                  void *stream_) {
+                  void *stream_, uint32_t *sums, int64_t kc, int64_t nblocks) {
     hipStream_t stream = (hipStream_t)stream_;
     PackedLayout L;
     packed_layout(es, m, n, k, p.kernel, A, lda, &L);
@@ -852,10 +904,15 @@ int launch_pack_b(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, 
     const int ks = (int)L.kspan;
     if (es == 2) {
         int8_t *Bl = Bpk + b_plane;
+        // int16-output update: B's block sums (after A's; cleared by pack_a_i16)
+        uint32_t *sb = sums != nullptr ? sums + 2 * nblocks * L.m_pad : nullptr;
+        const int bspan = sums != nullptr ? (int)(nblocks == 1 ? L.k_pad : kc) : 0;
         if (vb)
-            pack_b<2, true><<<g, 256, 0, stream>>>(B, ldb, ki, ni, kp, ks, np, Bpk, Bl, corrB);
+            pack_b<2, true><<<g, 256, 0, stream>>>(B, ldb, ki, ni, kp, ks, np, Bpk, Bl, corrB, sb,
+                                                   bspan);
         else
-            pack_b<2, false><<<g, 256, 0, stream>>>(B, ldb, ki, ni, kp, ks, np, Bpk, Bl, corrB);
+            pack_b<2, false><<<g, 256, 0, stream>>>(B, ldb, ki, ni, kp, ks, np, Bpk, Bl, corrB, sb,
+                                                    bspan);
     } else {
         if (vb)
             pack_b<1, true><<<g, 256, 0, stream>>>(B, ldb, ki, ni, kp, ks, np, Bpk, Bpk, corrB);
@@ -884,11 +941,8 @@ int launch_srs_packed(const igemm_plan &p, int64_t m, int64_t n, int64_t k, int6
     const int8_t *Apk = wa + L.off_a, *Bpk = wb + L.off_b;
     const int64_t a_plane = L.m_pad * L.k_pad, b_plane = L.n_pad * L.k_pad;
     const int kb = nblocks == 1 ? (int)L.k_pad : (int)kc;  // block span in the planes
+    // the block sums, written by the pack kernels
     uint32_t *sa = sums, *sb = sums + 2 * nblocks * L.m_pad;
-    block_sums<<<dim3((unsigned)(L.m_pad + L.n_pad)), 256, 0, stream>>>(
-        Apk, Apk + a_plane, (int)L.m_pad, sa, Bpk, Bpk + b_plane, (int)L.n_pad, sb, L.k_pad,
-        (int)L.k_pad, kb, (int)nblocks);
-    if (hipGetLastError() != hipSuccess) return IGEMM_EHIP;
     const KernelDesc &d = kKernels[p.kernel];
     const int tm = (int)(L.m_pad / d.bm), tn = (int)(L.n_pad / d.bn);
     const int mi = (int)m, ni = (int)n;
@@ -909,7 +963,9 @@ int launch_srs_packed(const igemm_plan &p, int64_t m, int64_t n, int64_t k, int6
     igemm_packed<2, 128, 128, 64, 32, 4, E><<<grid, 512, 0, stream>>>(                    \
         Apk, L.k_pad, a_plane, Bpk, L.k_pad, b_plane, sa, sb, kcon, (int32_t *)C, ldc, mi, \
         ni, ktl, tm, tn, epi, kcb, (int)L.m_pad, (int)L.n_pad)
-        if (shift == 0)
+        if (shift == 0 && kc == 256)
+            IGEMM_SRS_MULTI(5);
+        else if (shift == 0)
             IGEMM_SRS_MULTI(2);
         else if (shift < 8)
             IGEMM_SRS_MULTI(3);
