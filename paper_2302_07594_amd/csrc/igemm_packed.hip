@@ -338,17 +338,22 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     const int tn = (bid % span) / gsize;
     const int m0 = tm * BM, n0 = tn * BN;
 
-    // EPI 2: every block's limb sums of this tile's rows and columns, in LDS.
-    __shared__ uint2 bsA[MULTI ? MAXB * BM : 1];
-    __shared__ uint2 bsB[MULTI ? MAXB * BN : 1];
+    // EPI 2: every block's limb sums of this tile's rows and columns, in LDS,
+    // moved by DMA (1 KB per block and operand, spread over the waves) ahead
+    // of the prologue's tiles, whose wait and barrier cover them.
+    __shared__ __attribute__((aligned(16))) uint2 bsA[MULTI ? MAXB * BM : 1];
+    __shared__ __attribute__((aligned(16))) uint2 bsB[MULTI ? MAXB * BN : 1];
     if constexpr (MULTI) {
+        static_assert(BM * 8 == 1024 && BN * 8 == 1024, "one DMA block per block's sums");
         const int nblocks = ktiles / kcb;
-        const uint2 *sa = (const uint2 *)corrA, *sb = (const uint2 *)corrB;
-        for (int x = tid; x < nblocks * BM; x += NW * 64)
-            bsA[x] = sa[(int64_t)(x / BM) * m_pad + m0 + x % BM];
-        for (int x = tid; x < nblocks * BN; x += NW * 64)
-            bsB[x] = sb[(int64_t)(x / BN) * n_pad + n0 + x % BN];
-        __syncthreads();
+        for (int x = wave; x < 2 * nblocks; x += NW) {
+            const bool on_a = x < nblocks;
+            const int q = on_a ? x : x - nblocks;
+            const char *g = on_a ? (const char *)corrA + ((int64_t)q * m_pad + m0) * 8
+                                 : (const char *)corrB + ((int64_t)q * n_pad + n0) * 8;
+            char *d = on_a ? (char *)bsA + q * 1024 : (char *)bsB + q * 1024;
+            dma16(g + 16 * lane, (lds_void *)d);
+        }
     }
 
     // DMA: lane i of a 1 KB block writes LDS bytes [16i, 16i+16), i.e. row
