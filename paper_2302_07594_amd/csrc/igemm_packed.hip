@@ -90,8 +90,18 @@ pack_a_i16(const int16_t *__restrict__ A, int64_t lda, int m, int k, int k_pad,
         sh = sum4(h1, sum4(h0, sh));
         sl = sum4(l1, sum4(l0, sl));
         if (bsA != nullptr) {
-            atomicAdd(&bsum[e0 / bspan][0], sum4(h1, sum4(h0, 0)));
-            atomicAdd(&bsum[e0 / bspan][1], sum4(l1, sum4(l0, 0)));
+            // the 32 lanes of a half-wave cover 256 elements of one block:
+            // their sums, then one LDS add per half-wave
+            int bh = sum4(h1, sum4(h0, 0)), bl = sum4(l1, sum4(l0, 0));
+#pragma unroll
+            for (int o = 16; o > 0; o >>= 1) {
+                bh += __shfl_xor(bh, o);
+                bl += __shfl_xor(bl, o);
+            }
+            if ((tid & 31) == 0) {
+                atomicAdd(&bsum[e0 / bspan][0], bh);
+                atomicAdd(&bsum[e0 / bspan][1], bl);
+            }
         }
         *(uint2 *)(hrow + e0) = make_uint2(h0, h1);
         *(uint2 *)(lrow + e0) = make_uint2(l0, l1);
@@ -169,10 +179,24 @@ pack_b(const void *__restrict__ Bv, int64_t ldb, int k, int n, int k_pad, int ks
     auto flush = [&](int b) {
         if (tid < 128) (&bcs[0][0])[tid] = 0;
         __syncthreads();
+        // the 8 lanes of a wave with one chunk cc (lanes cc + 8 j) first
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
-            atomicAdd(&bcs[cc * 8 + c][0], bh[c]);
-            atomicAdd(&bcs[cc * 8 + c][1], bl[c]);
+#pragma unroll
+            for (int o = 8; o < 64; o <<= 1) {
+                bh[c] += __shfl_xor(bh[c], o);
+                bl[c] += __shfl_xor(bl[c], o);
+            }
+        }
+        if ((tid & 63) < 8) {
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                atomicAdd(&bcs[cc * 8 + c][0], bh[c]);
+                atomicAdd(&bcs[cc * 8 + c][1], bl[c]);
+            }
+        }
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
             bh[c] = 0;
             bl[c] = 0;
         }
