@@ -282,15 +282,16 @@ pack_b(const void *__restrict__ Bv, int64_t ldb, int k, int n, int k_pad, int ks
 // added first when bit 8 is set) and saturation; corrA / corrB then hold the
 // exact (high, low) limb sums of the range per row / column, and kconst is
 // 16384 times the range's length.
-// EPI 2 (int16 only): the int16-output update of every k block in one launch.
-// The k range is kcb-tile blocks (kcb a multiple of 4 and at most 32, i.e.
-// k_c <= 2048; ktiles = nblocks kcb, at most 16 blocks; shift <= 16);
-// corrA / corrB hold the exact (high, low) limb sums of
-// every block (block q at 2 (q m_pad + row), as the pack kernels write them),
-// staged in LDS at the start; kconst is 16384 kcb 64. At the end of each
-// block the lane converts its accumulators into the block's int16
-// contribution (the conversion of EPI 1) and adds it to running sums kept in
-// registers; the accumulators restart at zero; C is read and written once.
+// EPI 2-5 (int16 only): the int16-output update of every k block in one
+// launch (the form of the conversion by shift range, below). The k range is
+// kcb-tile blocks (kcb a multiple of 4 and at most 32, i.e. k_c <= 2048;
+// ktiles = nblocks kcb, at most 16 blocks; shift <= 16); corrA / corrB hold
+// the exact (high, low) limb sums of every block (block q at
+// 2 (q m_pad + row), as the pack kernels write them), staged in LDS at the
+// start; kconst is 16384 kcb 64. At the end of each block the lane converts
+// its accumulators into the block's int16 contribution (the conversion of
+// EPI 1) and adds it to running sums kept in registers; the accumulators
+// restart at zero; C is read and written once.
 // RAGGED: ktiles need not be a multiple of four (at least three), so that the
 // zero padding of k to a multiple of 256 is not multiplied; otherwise it is.
 template <int ES, int BM, int BN, int WM, int WN, int NST, int EPI = 0, bool RAGGED = false>
@@ -329,7 +330,7 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     constexpr bool MULTI = EPI >= 2;
     constexpr int SMODE = EPI - 2;
     static_assert(!MULTI || !RAGGED, "blocks of whole groups of four k-tiles");
-    constexpr int MAXB = 16;  // blocks of one EPI 2 launch
+    constexpr int MAXB = 16;  // blocks of one multi-block launch
 
     // The LDS stages as separate objects, so that the compiler can tell the
     // DMA writes of one stage from the fragment reads of another.
@@ -362,7 +363,7 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     const int tn = (bid % span) / gsize;
     const int m0 = tm * BM, n0 = tn * BN;
 
-    // EPI 2: every block's limb sums of this tile's rows and columns, in LDS,
+    // EPI 2-5: every block's limb sums of this tile's rows and columns, in LDS,
     // moved by DMA (1 KB per block and operand, spread over the waves) ahead
     // of the prologue's tiles, whose wait and barrier cover them.
     __shared__ __attribute__((aligned(16))) uint2 bsA[MULTI ? MAXB * BM : 1];
@@ -569,7 +570,7 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     // ktiles >= NST - 1, a multiple of four unless RAGGED). The planes are
     // zero-padded to a multiple of four k-tiles, so the prologue's loads stay
     // inside them.
-    // EPI 2: this lane's running int16 sums, two per register (16-bit lanes
+    // EPI 2-5: this lane's running int16 sums, two per register (16-bit lanes
     // that wrap modulo 2^16, as the update of C does), and the conversion of
     // block q's accumulators into them.
     typedef short s2 __attribute__((ext_vector_type(2)));
