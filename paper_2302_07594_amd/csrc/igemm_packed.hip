@@ -128,6 +128,64 @@ pack_a_i16(const int16_t *__restrict__ A, int64_t lda, int m, int k, int k_pad,
     }
 }
 
+// ---- pack A, int16, short rows (k_pad <= 512): one wave per padded row -----
+// The same outputs as pack_a_i16 (four rows per workgroup, so that no wave
+// idles when a row is shorter than a workgroup's 2048 elements): lane t
+// takes elements [8 t, 8 t + 8); the row's sums are wave sums; with blocks of
+// 256 each half-wave's sums are one block's.
+template <bool VEC>
+__global__ void __launch_bounds__(256)
+pack_a_i16_rows(const int16_t *__restrict__ A, int64_t lda, int m, int k, int k_pad,
+                int8_t *__restrict__ Ah, int8_t *__restrict__ Al, uint32_t *__restrict__ corrA,
+                uint32_t *__restrict__ corrB, int n_pad, uint32_t *__restrict__ bsA, int bspan,
+                int m_pad, uint32_t *__restrict__ clr, int nclr) {
+    const int tid = threadIdx.x, lane = tid & 63;
+    if (corrB != nullptr)
+        for (int j = blockIdx.x * 256 + tid; j < n_pad; j += gridDim.x * 256) corrB[j] = 0u;
+    if (clr != nullptr)
+        for (int j = blockIdx.x * 256 + tid; j < nclr; j += gridDim.x * 256) clr[j] = 0u;
+    const int i = blockIdx.x * 4 + (tid >> 6);
+    const int len = i < m ? k : 0;
+    const int16_t *arow = A + (int64_t)(i < m ? i : 0) * lda;
+    const int e0 = lane * 8;
+    u32 h0 = 0, h1 = 0, l0 = 0, l1 = 0;
+    if (e0 < k_pad) {
+        const v4i raw = load16<2, VEC>(arow, e0, len);
+        const u32 y0 = raw.x, y1 = raw.y, y2 = raw.z, y3 = raw.w;
+        const int v = len - e0;
+        const u32 m0 = byte_mask(v), m1 = byte_mask(v - 4);
+        h0 = perm(y1, y0, 0x07050301u) & m0;
+        h1 = perm(y3, y2, 0x07050301u) & m1;
+        l0 = (perm(y1, y0, 0x06040200u) ^ 0x80808080u) & m0;
+        l1 = (perm(y3, y2, 0x06040200u) ^ 0x80808080u) & m1;
+        *(uint2 *)(Ah + (int64_t)i * k_pad + e0) = make_uint2(h0, h1);
+        *(uint2 *)(Al + (int64_t)i * k_pad + e0) = make_uint2(l0, l1);
+    }
+    // half-wave sums (32 lanes, 256 elements), then the row's
+    int sh = sum4(h1, sum4(h0, 0)), sl = sum4(l1, sum4(l0, 0));
+#pragma unroll
+    for (int o = 1; o < 32; o <<= 1) {
+        sh += __shfl_xor(sh, o);
+        sl += __shfl_xor(sl, o);
+    }
+    const int th = sh + __shfl_xor(sh, 32), tl = sl + __shfl_xor(sl, 32);
+    if (bsA != nullptr) {
+        if (bspan >= 512) {
+            // the whole row is block 0
+            if (lane == 0) {
+                bsA[(int64_t)i * 2] = (u32)th;
+                bsA[(int64_t)i * 2 + 1] = (u32)tl;
+            }
+        } else if ((lane & 31) == 0 && e0 < k_pad) {
+            // bspan = 256: one block per half-wave
+            const int b = e0 / 256;
+            bsA[((int64_t)b * m_pad + i) * 2] = (u32)sh;
+            bsA[((int64_t)b * m_pad + i) * 2 + 1] = (u32)sl;
+        }
+    }
+    if (lane == 0) corrA[i] = 32768u * (u32)th + 128u * (u32)tl;
+}
+
 // ---- pack A, int8: copy into a zero-padded m_pad x k_pad buffer ------------
 template <bool VEC>
 __global__ void __launch_bounds__(256)
@@ -898,7 +956,18 @@ int launch_pack_a(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, 
         const int nb = sums != nullptr ? (int)nblocks : 0;
         uint32_t *clr = sums != nullptr ? sums + 2 * nblocks * L.m_pad : nullptr;
         const int nclr = sums != nullptr ? (int)(2 * nblocks * L.n_pad) : 0;
-        if (va)
+        const int mp = (int)L.m_pad;
+        if (kp <= 512) {
+            // short rows: one wave per row (m_pad is a multiple of 128)
+            const dim3 g4((unsigned)(L.m_pad / 4));
+            if (va)
+                pack_a_i16_rows<true><<<g4, 256, 0, stream>>>(A16, lda, mi, ki, kp, Apk, Al, corrA,
+                                                              corrB, np, sums, bspan, mp, clr, nclr);
+            else
+                pack_a_i16_rows<false><<<g4, 256, 0, stream>>>(A16, lda, mi, ki, kp, Apk, Al,
+                                                               corrA, corrB, np, sums, bspan, mp,
+                                                               clr, nclr);
+        } else if (va)
             pack_a_i16<true><<<g, 256, 0, stream>>>(A16, lda, mi, ki, kp, Apk, Al, corrA, corrB, np,
                                                     sums, bspan, nb, clr, nclr);
         else
