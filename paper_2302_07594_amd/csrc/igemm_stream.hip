@@ -287,7 +287,33 @@ igemm_stream_lds(const int8_t *__restrict__ A, int64_t lda, const int8_t *__rest
                  int colblocks, int rowblocks) {
     constexpr int BST = 64 * 128;      // B bytes per step
     constexpr int AST = MB * 16 * 64;  // A bytes per step
-    __shared__ __attribute__((aligned(16))) char sB[SPW * BST];
+    static_assert(SPW == 4 || SPW == 8 || SPW == 16, "steps per workgroup");
+    // One LDS array per step of B, so that the compiler tells the DMA into
+    // each apart and a step's reads wait only for that step's data.
+#define IGEMM_SB(i) __shared__ __attribute__((aligned(16))) char sB##i[SPW > i ? BST : 16]
+    IGEMM_SB(0); IGEMM_SB(1); IGEMM_SB(2); IGEMM_SB(3); IGEMM_SB(4); IGEMM_SB(5);
+    IGEMM_SB(6); IGEMM_SB(7); IGEMM_SB(8); IGEMM_SB(9); IGEMM_SB(10); IGEMM_SB(11);
+    IGEMM_SB(12); IGEMM_SB(13); IGEMM_SB(14); IGEMM_SB(15);
+#undef IGEMM_SB
+    auto sb = [&](auto sc) -> char * {
+        constexpr int S = decltype(sc)::value;
+        if constexpr (S == 0) return sB0;
+        else if constexpr (S == 1) return sB1;
+        else if constexpr (S == 2) return sB2;
+        else if constexpr (S == 3) return sB3;
+        else if constexpr (S == 4) return sB4;
+        else if constexpr (S == 5) return sB5;
+        else if constexpr (S == 6) return sB6;
+        else if constexpr (S == 7) return sB7;
+        else if constexpr (S == 8) return sB8;
+        else if constexpr (S == 9) return sB9;
+        else if constexpr (S == 10) return sB10;
+        else if constexpr (S == 11) return sB11;
+        else if constexpr (S == 12) return sB12;
+        else if constexpr (S == 13) return sB13;
+        else if constexpr (S == 14) return sB14;
+        else return sB15;
+    };
     __shared__ __attribute__((aligned(16))) char sA[SPW * AST];
     asm volatile("" ::"s"(A), "s"(lda), "s"(B), "s"(ldb), "s"(C), "s"(ldc), "s"(m), "s"(n),
                  "s"(k), "s"(colblocks), "s"(rowblocks));
@@ -310,17 +336,8 @@ igemm_stream_lds(const int8_t *__restrict__ A, int64_t lda, const int8_t *__rest
         (void *)aw, 0, (int)min((a_ext + 3) & ~(int64_t)3, (int64_t)0x7ffffff0), 0x00020000);
 
     // ---- every load of the workgroup, by DMA -------------------------------
-    // B: wave w moves rows 8 w .. 8 w + 7 of each step (lane i: row 8 w + i / 8,
-    // physical chunk i % 8, which holds logical chunk (i % 8) ^ (row & 7)).
-    {
-        const int rr = 8 * wave + lane / 8;
-        const u32 off = (u32)rr * (u32)ldb + 16u * (u32)((lane % 8) ^ (rr & 7));
-#pragma unroll
-        for (int s = 0; s < SPW; ++s)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                Brs, (lds_void *)(sB + s * BST + wave * 1024), 16,
-                (int)(off + (u32)(64 * s) * (u32)ldb), 0, 0, 0);
-    }
+    // A first (every step reads it), then B step by step, so that step s can
+    // start once A and B's steps up to s have landed.
     // A: SPW * MB blocks of 16 rows x 64 bytes, dealt to the waves in turn
     // (lane i: row i / 4, physical chunk i % 4, logical (i % 4) ^ swz(row)).
     {
@@ -337,9 +354,23 @@ igemm_stream_lds(const int8_t *__restrict__ A, int64_t lda, const int8_t *__rest
             }
         }
     }
-    __builtin_amdgcn_s_waitcnt(0);
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
+    // B: wave w moves rows 8 w .. 8 w + 7 of each step (lane i: row 8 w + i / 8,
+    // physical chunk i % 8, which holds logical chunk (i % 8) ^ (row & 7)).
+    {
+        const int rr = 8 * wave + lane / 8;
+        const u32 off = (u32)rr * (u32)ldb + 16u * (u32)((lane % 8) ^ (rr & 7));
+        auto dma_step = [&](auto sc) {
+            constexpr int S = decltype(sc)::value;
+            if constexpr (S < SPW)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    Brs, (lds_void *)(sb(sc) + wave * 1024), 16,
+                    (int)(off + (u32)(64 * S) * (u32)ldb), 0, 0, 0);
+        };
+        dma_step(ic<0>{}); dma_step(ic<1>{}); dma_step(ic<2>{}); dma_step(ic<3>{});
+        dma_step(ic<4>{}); dma_step(ic<5>{}); dma_step(ic<6>{}); dma_step(ic<7>{});
+        dma_step(ic<8>{}); dma_step(ic<9>{}); dma_step(ic<10>{}); dma_step(ic<11>{});
+        dma_step(ic<12>{}); dma_step(ic<13>{}); dma_step(ic<14>{}); dma_step(ic<15>{});
+    }
 
     // ---- multiply -------------------------------------------------------------
     // B: lane u of each 16-lane group q addresses k row 16 q + 8 h + u / 2 of the
@@ -356,20 +387,32 @@ igemm_stream_lds(const int8_t *__restrict__ A, int64_t lda, const int8_t *__rest
     v4i acc[MB];
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) acc[mb] = v4i{0, 0, 0, 0};
+    // Step s: wait until this wave's DMA of A and of B's steps up to s has
+    // landed (the SPW - 1 - s later steps may stay in flight), then for the
+    // other waves' (barrier), then multiply.
+    auto mul_step = [&](auto sc) {
+        constexpr int S = decltype(sc)::value;
+        if constexpr (S < SPW) {
+            // s_waitcnt: vmcnt[3:0] = SPW - 1 - S, expcnt and lgkmcnt not waited on
+            __builtin_amdgcn_s_waitcnt((SPW - 1 - S) | (0x7 << 4) | (0xf << 8));
+            __builtin_amdgcn_s_barrier();
+            const char *bs = sb(sc);
+            const v2i_t b0 = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+                (__attribute__((address_space(3))) v2i_t *)(lds_void *)(bs + b_rd[0]));
+            const v2i_t b1 = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+                (__attribute__((address_space(3))) v2i_t *)(lds_void *)(bs + b_rd[1]));
+            const v4i b = v4i{b0.x, b0.y, b1.x, b1.y};
 #pragma unroll
-    for (int s = 0; s < SPW; ++s) {
-        const char *bs = sB + s * BST;
-        const v2i_t b0 = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
-            (__attribute__((address_space(3))) v2i_t *)(lds_void *)(bs + b_rd[0]));
-        const v2i_t b1 = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
-            (__attribute__((address_space(3))) v2i_t *)(lds_void *)(bs + b_rd[1]));
-        const v4i b = v4i{b0.x, b0.y, b1.x, b1.y};
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-            const v4i a = *(const v4i *)(sA + s * AST + mb * 1024 + a_rd);
-            acc[mb] = Mfma<16>::mma(a, b, acc[mb]);
+            for (int mb = 0; mb < MB; ++mb) {
+                const v4i a = *(const v4i *)(sA + S * AST + mb * 1024 + a_rd);
+                acc[mb] = Mfma<16>::mma(a, b, acc[mb]);
+            }
         }
-    }
+    };
+    mul_step(ic<0>{}); mul_step(ic<1>{}); mul_step(ic<2>{}); mul_step(ic<3>{});
+    mul_step(ic<4>{}); mul_step(ic<5>{}); mul_step(ic<6>{}); mul_step(ic<7>{});
+    mul_step(ic<8>{}); mul_step(ic<9>{}); mul_step(ic<10>{}); mul_step(ic<11>{});
+    mul_step(ic<12>{}); mul_step(ic<13>{}); mul_step(ic<14>{}); mul_step(ic<15>{});
 
     // ---- into C ---------------------------------------------------------------
     const int col = j0 + 16 * wave + Mfma<16>::out_col(lane);
