@@ -352,7 +352,11 @@ pack_b(const void *__restrict__ Bv, int64_t ldb, int k, int n, int k_pad, int ks
 // restart at zero; C is read and written once.
 // RAGGED: ktiles need not be a multiple of four (at least three), so that the
 // zero padding of k to a multiple of 256 is not multiplied; otherwise it is.
-template <int ES, int BM, int BN, int WM, int WN, int NST, int EPI = 0, bool RAGGED = false>
+// SKIPZ (short k, one k range): kcb counts the k-tiles that hold data, and the
+// MFMAs of the zero-padding tiles past them are skipped (RAGGED's run-time
+// tail needs more registers than eight waves have).
+template <int ES, int BM, int BN, int WM, int WN, int NST, int EPI = 0, bool RAGGED = false,
+          bool SKIPZ = false>
 __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64, 1)
 igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
              const int8_t *__restrict__ Bp, int64_t ldb_p, int64_t b_plane,
@@ -388,6 +392,7 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
     constexpr bool MULTI = EPI >= 2;
     constexpr int SMODE = EPI - 2;
     static_assert(!MULTI || !RAGGED, "blocks of whole groups of four k-tiles");
+    static_assert(!SKIPZ || (!MULTI && !RAGGED), "zero tiles skipped in one k range");
     constexpr int MAXB = 16;  // blocks of one multi-block launch
 
     // The LDS stages as separate objects, so that the compiler can tell the
@@ -570,7 +575,7 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
         constexpr bool PREF = decltype(do_pref)::value != 0;
         if constexpr (DMA) dma_range(ic<SD>{}, kt + NST - 1, ic<0>{}, ic<D_SUB0>{});
         read_frags(ic<1>{}, ic<S>{}, ic<1>{});
-        mfmas(ic<0>{}, fresh);
+        if (!SKIPZ || kt < kcb) mfmas(ic<0>{}, fresh);
 #pragma unroll
         for (int i = 0; i < NM; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -582,7 +587,7 @@ igemm_packed(const int8_t *__restrict__ Ap, int64_t lda_p, int64_t a_plane,
         if constexpr (DMA && D_SUB0 < DPW)
             dma_range(ic<SD>{}, kt + NST - 1, ic<D_SUB0>{}, ic<DPW>{});
         if constexpr (PREF) read_frags(ic<0>{}, ic<(S + 1) % NST>{}, ic<0>{});
-        mfmas(ic<1>{}, ic<0>{});
+        if (!SKIPZ || kt < kcb) mfmas(ic<1>{}, ic<0>{});
 #pragma unroll
         for (int i = 0; i < NM; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -1085,7 +1090,13 @@ int launch_srs_packed(const igemm_plan &p, int64_t m, int64_t n, int64_t k, int6
         int ktiles = (int)((real + 63) / 64);
         if (ktiles < 3) ktiles = 3;
         if (ktiles > (int)(span / 64)) ktiles = (int)(span / 64);
-        if (ktiles % 4 == 0)
+        if (span <= 512) {
+            // short blocks: eight waves, the zero tiles' MFMAs skipped
+            igemm_packed<2, 128, 128, 64, 32, 4, 1, false, true><<<grid, 512, 0, stream>>>(
+                Apk + k0, L.k_pad, a_plane, Bpk + k0, L.k_pad, b_plane, sa + 2 * q * L.m_pad,
+                sb + 2 * q * L.n_pad, 16384u * (uint32_t)real, (int32_t *)C, ldc, mi, ni,
+                (int)(span / 64), tm, tn, epi, (int)((real + 63) / 64));
+        } else if (ktiles % 4 == 0)
             igemm_packed<2, 128, 128, 64, 64, 4, 1><<<grid, 256, 0, stream>>>(
                 Apk + k0, L.k_pad, a_plane, Bpk + k0, L.k_pad, b_plane, sa + 2 * q * L.m_pad,
                 sb + 2 * q * L.n_pad, 16384u * (uint32_t)real, (int32_t *)C, ldc, mi, ni, ktiles,
@@ -1117,6 +1128,17 @@ int launch_multiply(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k
     const int8_t *Asrc = L.pack_a ? wa + L.off_a : (const int8_t *)A;
     const int64_t lda_p = L.pack_a ? L.k_pad : lda;
     const dim3 grid((unsigned)p.grid);
+    if (es == 2 && L.k_pad <= 512) {
+        // Short k (one chunk of four or eight k-tiles): eight waves of 64 x 32,
+        // the MFMAs of the zero tiles skipped. (4096, 4096, k) one call, us,
+        // against four waves (RAGGED where it applied): k = 64 52.8 / 58.8,
+        // 256 58.9 / 61.9, 290 68.3 / 71.5, 512 75.0 / 77.8.
+        const int kr = (int)((k + kBK - 1) / kBK);
+        igemm_packed<2, 128, 128, 64, 32, 4, 0, false, true><<<grid, 512, 0, stream>>>(
+            Asrc, lda_p, a_plane, Bpk, L.k_pad, b_plane, corrA, corrB, 16384u * (uint32_t)k, C,
+            ldc, mi, ni, (int)(L.k_pad / kBK), tm, tn, 0, kr);
+        return hipGetLastError() == hipSuccess ? IGEMM_OK : IGEMM_EHIP;
+    }
     // One launch per k chunk; the row and column corrections and the
     // 16384 k constant are added by the first launch only.
     for (int64_t k0 = 0; k0 < L.k_pad; k0 += p.k_chunk) {
