@@ -113,10 +113,11 @@ def test_packed_int8_extremes_multi_chunk(value):
     _check("i8", A, B, C, m, n, k)
 
 
-# k counts whose k-tiles of 64 are not a multiple of four. int16 multiplies
-# only the tiles that hold data when the padding spans three of them (290 and
-# 1300: 5 and 21 tiles, through the tail chosen at run time); the others (k =
-# 1, 130, 330, 420, 1345) multiply the zero padding up to a multiple of four.
+# k counts whose k-tiles of 64 are not a multiple of four. int16 with k up to
+# 512 skips the MFMAs of the zero tiles (eight-wave kernel: k = 1, 130, 290,
+# 330, 420); beyond it, it multiplies only the tiles that hold data when the
+# padding spans three of them (1300: 21 tiles, through the tail chosen at run
+# time) and the zero padding up to a multiple of four otherwise (1345).
 RAGGED_K = [1, 130, 290, 330, 420, 1300, 1345]
 
 
