@@ -10,8 +10,8 @@
 //   * reads A fragments with ds_read_b128 and B fragments with transpose
 //     reads, and for int16 splits every element into its high and offset-low
 //     int8 limbs in registers (v_perm_b32, one xor) right before the MFMAs;
-//   * accumulates the exact row sums of A (waves 0 and 3) and column sums of
-//     B (waves 1 and 2) from the raw int16 fragments (v_dot2 with ones), so
+//   * accumulates the exact row sums of A and column sums of B from the raw
+//     int16 fragments (v_dot2 with ones; each row and column by one wave), so
 //     that the epilogue adds the limb corrections of its own k range;
 //   * updates C modulo 2^32 with the branch-free buffer-resource epilogue.
 // Exactness (Sec. 4.1 definition, int16 limb identity): for x = 256 h + l
@@ -415,13 +415,17 @@ igemm_direct(const char *__restrict__ A, int64_t lda, const char *__restrict__ B
         tail_step(ic<2>{}, ic<4>{}, kt);
         tail_step(ic<3>{}, ic<4>{}, kt);
     };
+    // Which sums this wave takes (uniform per wave, so each runs its own copy
+    // of the loop with the same barriers): four waves (2 x 2 grid of 64 x 64)
+    // -- waves 0 and 3 the row sums of their 64 rows, waves 1 and 2 the column
+    // sums of their 64 columns; eight waves (2 x 4 grid of 64 x 32) -- waves 0
+    // and 5 the rows, waves 1 to 4 the columns (every row and column once).
+    const int skind = NW == 4 ? (wave == 0 || wave == 3 ? 1 : 2)
+                              : (wave == 0 || wave == 5 ? 1 : (wave <= 4 ? 2 : 0));
     if constexpr (ES == 2) {
-        // Waves 0 and 3 own the row sums of their 64 rows, waves 1 and 2 the
-        // column sums of their 64 columns (the 2 x 2 wave grid covers each
-        // once); the choice is uniform per wave, so each runs its own copy of
-        // the loop with the same barriers.
-        if (wave == 0 || wave == 3) run(ic<1>{});
-        else run(ic<2>{});
+        if (skind == 1) run(ic<1>{});
+        else if (skind == 2) run(ic<2>{});
+        else run(ic<0>{});
     } else {
         run(ic<0>{});
     }
@@ -437,11 +441,12 @@ igemm_direct(const char *__restrict__ A, int64_t lda, const char *__restrict__ B
     if constexpr (ES == 2) {
         // Lanes l and l + 32 hold complementary k chunks of the same row or
         // column: add them, scale by 128 and publish through LDS.
-        const bool rows = wave == 0 || wave == 3;
+        const bool rows = skind == 1;
 #pragma unroll
         for (int i = 0; i < (TM > TN ? TM : TN); ++i) {
             const u32 s = 128u * (u32)(psum[i] + __shfl_xor(psum[i], 32));
-            if (lane < 32) sums[rows ? wm0 + 32 * i + lane : BM + wn0 + 32 * i + lane] = s;
+            if (lane < 32 && skind != 0 && i < (rows ? TM : TN))
+                sums[rows ? wm0 + 32 * i + lane : BM + wn0 + 32 * i + lane] = s;
         }
         __syncthreads();
         const u32 kconst = 0u - 16384u * (u32)(64 * ktiles);
@@ -535,7 +540,14 @@ int launch_direct(int es, const igemm_plan &p, int64_t m, int64_t n, int64_t k, 
         const char *Ak = (const char *)A + k0 * es;
         const char *Bk = (const char *)B + k0 * ldb * es;
         if (ktiles % 4 != 0 || ktiles < 4) return IGEMM_EINVAL;   // the planner prevents it
-        if (es == 2)
+        // int16 with at most eight k-tiles per launch: eight waves of 64 x 32
+        // (one wave's limb split beside the other's matrix-core work; 4096 x
+        // 4096 x 256 in 55.3 us against 58.7 us), else four waves of 64 x 64
+        // (k = 4096: 276.6 us against 302.2 us with eight waves).
+        if (es == 2 && ktiles <= 8)
+            igemm_direct<2, 128, 128, 64, 32, 4><<<grid, 512, 0, stream>>>(
+                Ak, lda, Bk, ldb, C, ldc, mi, ni, ktiles, tm, tn);
+        else if (es == 2)
             igemm_direct<2, 128, 128, 64, 64, 4><<<grid, 256, 0, stream>>>(
                 Ak, lda, Bk, ldb, C, ldc, mi, ni, ktiles, tm, tn);
         else

@@ -384,6 +384,8 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
         out->threads = (d.bm / d.wm) * (d.bn / d.wn) * 64;
         out->k_chunk = direct_chunk(k);
         out->split = (int)cdiv(k, out->k_chunk);
+        // int16 launches of at most eight k-tiles run eight waves of 64 x 32
+        if (es == 2 && out->k_chunk <= 8 * kBK) out->threads = 512;
         out->tiles = tiles;
         out->grid = tiles;
         out->vec_a = 1;
