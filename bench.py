@@ -490,7 +490,8 @@ def main():
     if not args.no_extra:
         import oracle  # noqa: F401  (per-config results are checked against it)
         per = {}
-        for wname in ("i16_256", "i8_8192", "i16_conv", "i8_skinny", "i16_paper"):
+        for wname in ("i16_256", "i8_8192", "i16_conv", "i8_skinny", "i16_skinny",
+                      "i16_paper"):
             for c in workloads.WORKLOADS[wname].cases:
                 log(f"bench: {c.name}")
                 per[c.name] = bench_gemm(c, olog, details)

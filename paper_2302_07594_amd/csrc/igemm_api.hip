@@ -99,7 +99,8 @@ int run(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t lda, con
     st = make_plan(es, m, n, k, A, lda, B, ldb, ldc, num_cu_of_current_device(), kernel, split,
                    have_ws, &p);
     if (st != IGEMM_OK) return st;
-    if (p.kernel == K_I8_STREAM) return launch_stream(p, m, n, k, A, lda, B, ldb, C, ldc, stream);
+    if (p.kernel == K_I8_STREAM || p.kernel == K_I16_STREAM)
+        return launch_stream(p, m, n, k, A, lda, B, ldb, C, ldc, stream);
     if (p.kernel == K_I16_DIRECT_128x128 || p.kernel == K_I8_DIRECT_256x256)
         return launch_direct(es, p, m, n, k, A, lda, B, ldb, C, ldc, stream);
     if (p.kernel == K_I16_SMALL_64x64)

@@ -34,6 +34,7 @@ enum KernelId {
     K_I16_DIRECT_128x128,
     K_I8_DIRECT_256x256,
     K_I16_SMALL_64x64,
+    K_I16_STREAM,
     K_COUNT
 };
 

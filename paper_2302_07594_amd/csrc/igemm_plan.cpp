@@ -30,6 +30,7 @@ const KernelDesc kKernels[K_COUNT] = {
     {"i16_direct_128x128", 2, 128, 128, 64, 64, false},
     {"i8_direct_256x256", 1, 256, 256, 64, 128, false},
     {"i16_small_64x64", 2, 64, 64, 32, 32, false},
+    {"i16_stream_32x64", 2, 32, 64, 16, 16, false},
 };
 
 // Largest grid (in workgroups) of one launch: the dispatch packet counts
@@ -187,6 +188,45 @@ static int64_t direct_chunk(int64_t k) {
 // workgroups of 4 or 8 waves that each take 1, 2 or 4 k-steps of 64 (4, 8,
 // 16 or 32 steps per workgroup). Returns false if its 32-bit window offsets
 // do not fit.
+// Operands the int16 column-per-wave kernel takes: A and B 16-byte aligned
+// with rows of whole 16-byte chunks, k a multiple of 64 and n of 8.
+static bool i16_stream_ok(int64_t n, int64_t k, const void *A, int64_t lda, const void *B,
+                          int64_t ldb) {
+    return (uintptr_t)A % 16 == 0 && (uintptr_t)B % 16 == 0 && lda % 8 == 0 && ldb % 8 == 0 &&
+           k % kBK == 0 && n % 8 == 0 && k <= lda && n <= ldb;
+}
+
+// The int16 column-per-wave kernel's launch: 64-column blocks of 16 or 32
+// rows, 4 k-steps of 64 per workgroup (8 when an explicit k-slice count asks
+// for longer ranges). Four steps measured faster than eight on every
+// weight-streaming shape (k = 4096, us, 4 / 8 steps): 1 x 4096 8.6 / 9.1,
+// 8 x 4096 9.4 / 9.6, 1 x 11008 17.7 / 19.6, 8 x 11008 19.1 / 20.9,
+// 32 x 11008 25.5 / 35.5 (eight steps of two 16-row blocks hold 96 KB of
+// LDS: one workgroup per compute unit).
+static int i16_stream_plan(int64_t m, int64_t n, int64_t k, int64_t lda, int64_t ldb,
+                           int split, igemm_plan *out) {
+    const int64_t ksteps = k / kBK;
+    const int64_t spw = split > 0 && cdiv(ksteps, split) > 4 ? 8 : 4;
+    const int bm = m <= 16 ? 16 : 32;
+    // (32-bit byte offsets into a workgroup's k range of B and rows of A)
+    int64_t t;
+    if (ldb >= 0x7fff0000 / (2 * spw * kBK) || lda >= 0x7fff0000 / 64 - 64 ||
+        !mul_ok(cdiv(m, bm), cdiv(n, 64), &t) || t > kMaxGrid ||
+        t * cdiv(ksteps, spw) > kMaxGrid)
+        return IGEMM_ENOTSUP;
+    out->kernel = K_I16_STREAM;
+    out->bm = bm;
+    out->bn = 64;
+    out->threads = 256;
+    out->k_chunk = spw * kBK;
+    out->split = (int)cdiv(ksteps, spw);
+    out->tiles = t;
+    out->grid = t * out->split;
+    out->vec_a = 1;
+    out->vec_b = 1;
+    return IGEMM_OK;
+}
+
 struct StreamShape {
     int bm, threads;
     int64_t spw, slices, tiles;
@@ -327,6 +367,15 @@ static int auto_kernel(int es, int64_t m, int64_t n, int64_t k, const void *A, i
         if (tiles_of(K_I8_256x256, m, n) >= num_cu) return K_I8_256x256;
         return K_I8_128x128;
     }
+    // Up to 16 rows over wide B (the weight-streaming shapes): the int16
+    // column-per-wave kernel where the operands allow it (k = 4096, us:
+    // 1 x 11008 17.7 against 26.4 on 16x128 tiles, 8 x 4096 9.4 against
+    // 12.3). With 17 to 32 rows the fused 32x128 tiles stay (32 x 11008 24.6
+    // against 25.5 us).
+    igemm_plan sp{};
+    if (m <= 16 && n >= 512 && k >= 256 && i16_stream_ok(n, k, A, lda, B, ldb) &&
+        i16_stream_plan(m, n, k, lda, ldb, -1, &sp) == IGEMM_OK)
+        return K_I16_STREAM;
     if (m <= 16) return K_I16_16x128;
     if (m <= 32) return K_I16_32x128;
     // 128-column tiles on n <= 64 would multiply padding for half their
@@ -440,6 +489,10 @@ int make_plan(int es, int64_t m, int64_t n, int64_t k, const void *A, int64_t ld
         out->packed_a_bytes = L.a_bytes;
         out->packed_b_bytes = L.b_bytes;
         return IGEMM_OK;
+    }
+    if (id == K_I16_STREAM) {
+        if (!i16_stream_ok(n, k, A, lda, B, ldb)) return IGEMM_EINVAL;
+        return i16_stream_plan(m, n, k, lda, ldb, split, out);
     }
     if (id == K_I8_STREAM) {
         // vec_b = 1: B's rows are whole 16-byte chunks (with vec_a, the

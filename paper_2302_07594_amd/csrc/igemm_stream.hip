@@ -33,6 +33,7 @@
 #include "igemm.h"
 #include "igemm_device.h"
 #include "igemm_internal.h"
+#include "igemm_lds.h"
 
 namespace igemm {
 namespace stream {
@@ -448,6 +449,225 @@ const void *pick_lds_spw(int spw, bool split) {
     return nullptr;
 }
 
+
+// ---------------------------------------------------------------------------
+// int16 column-per-wave variant (few-row int16 products whose B, the weights,
+// dominates the traffic). As in the int8 kernel above, B moves to LDS once by
+// DMA and each wave owns 16 columns for the workgroup's whole k range; here
+// four waves cover 64 int16 columns (B rows of 128 bytes: the same LDS rows
+// and swizzle), and every element is split into its high and offset-low int8
+// limbs in registers (the int16 limb identity, Sec. 4.1 definition):
+//   * A fragments (16 int16 of one row per lane) by two ds_read_b128, B
+//     fragments (16 int16 of one column per lane) by four transpose reads
+//     ds_read_b64_tr_b16, then the limb bytes by v_perm;
+//   * four v_mfma_i32_16x16x64_i8 per 16-row block and step (hh, hl', l'h,
+//     l'l') into three accumulators, and the exact row sums of A and column
+//     sums of B (v_dot2 with ones) on the raw fragments;
+//   * C += 65536 S_hh + 256 S_x + S_ll + 128 (row sum + column sum) - 16384 K
+//     modulo 2^32 over the workgroup's K = 64 (steps) elements of k (atomic
+//     adds when k is sliced).
+// Preconditions (planner): A and B 16-byte aligned with rows of whole 16
+// bytes, k a multiple of 64, n a multiple of 8. Steps past k (a short last
+// slice) are loaded (reads past the resources' ranges return zeros) and not
+// multiplied. Rows of A past m and columns past n are multiplied and not
+// written.
+template <int MB, int SPW, bool SPLIT>
+__global__ void __launch_bounds__(256)
+igemm_stream_lds16(const int16_t *__restrict__ A, int64_t lda, const int16_t *__restrict__ B,
+                   int64_t ldb, int32_t *__restrict__ C, int64_t ldc, int m, int n, int k,
+                   int colblocks, int rowblocks) {
+    using lds::hi4;
+    using lds::lo4;
+    using lds::sum2;
+    using lds::v4;
+    constexpr int BST = 64 * 128;       // B bytes per step: 64 k rows x 64 int16
+    constexpr int AST = MB * 16 * 128;  // A bytes per step: 16 MB rows x 64 int16
+    static_assert(SPW == 4 || SPW == 8, "steps per workgroup");
+#define IGEMM_SB(i) __shared__ __attribute__((aligned(16))) char sB##i[SPW > i ? BST : 16]
+    IGEMM_SB(0); IGEMM_SB(1); IGEMM_SB(2); IGEMM_SB(3);
+    IGEMM_SB(4); IGEMM_SB(5); IGEMM_SB(6); IGEMM_SB(7);
+#undef IGEMM_SB
+    auto sb = [&](auto sc) -> char * {
+        constexpr int S = decltype(sc)::value;
+        if constexpr (S == 0) return sB0;
+        else if constexpr (S == 1) return sB1;
+        else if constexpr (S == 2) return sB2;
+        else if constexpr (S == 3) return sB3;
+        else if constexpr (S == 4) return sB4;
+        else if constexpr (S == 5) return sB5;
+        else if constexpr (S == 6) return sB6;
+        else return sB7;
+    };
+    __shared__ __attribute__((aligned(16))) char sA[SPW * AST];
+    asm volatile("" ::"s"(A), "s"(lda), "s"(B), "s"(ldb), "s"(C), "s"(ldc), "s"(m), "s"(n),
+                 "s"(k), "s"(colblocks), "s"(rowblocks));
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const unsigned t = blockIdx.x / (unsigned)colblocks;
+    const int cb = (int)(blockIdx.x - t * (unsigned)colblocks);
+    const int rb = (int)(t % (unsigned)rowblocks);
+    const int ks = (int)(t / (unsigned)rowblocks);
+    const int j0 = cb * 64, i0 = rb * 16 * MB, kbeg = ks * SPW * 64;
+    const int mrows = min(m - i0, 16 * MB);
+    const int nsteps = min(SPW, (k - kbeg) / 64);  // >= 1 (grid)
+
+    const char *bw = (const char *)B + ((int64_t)kbeg * ldb + j0) * 2;
+    const int64_t b_ext = ((int64_t)(k - 1 - kbeg) * ldb + (n - j0)) * 2;
+    const __amdgpu_buffer_rsrc_t Brs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)bw, 0, (int)min((b_ext + 3) & ~(int64_t)3, (int64_t)0x7ffffff0), 0x00020000);
+    const char *aw = (const char *)A + ((int64_t)i0 * lda + kbeg) * 2;
+    const int64_t a_ext = ((int64_t)(mrows - 1) * lda + (k - kbeg)) * 2;
+    const __amdgpu_buffer_rsrc_t Ars = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)aw, 0, (int)min((a_ext + 3) & ~(int64_t)3, (int64_t)0x7ffffff0), 0x00020000);
+
+    // ---- every load, by DMA: A first, then B step by step --------------------
+    // 1 KB blocks of 8 rows x 128 bytes; lane i writes row i / 8 of its block,
+    // physical chunk i % 8, which holds logical chunk (i % 8) ^ (row & 7).
+    // A: SPW * 2 MB blocks (step s, rows 8 h .. 8 h + 7), dealt to the waves.
+    {
+        const int rr = lane / 8;
+#pragma unroll
+        for (int b0 = 0; b0 < SPW * 2 * MB; b0 += 4) {
+            const int b = b0 + wave;
+            if (b < SPW * 2 * MB) {
+                const int s = b / (2 * MB), h = b % (2 * MB);
+                const int row = 8 * h + rr;
+                const u32 off = (u32)row * (u32)lda * 2u + (u32)(128 * s) +
+                                16u * (u32)((lane % 8) ^ (row & 7));
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    Ars, (lds_void *)(sA + s * AST + h * 1024), 16, (int)off, 0, 0, 0);
+            }
+        }
+    }
+    // B: wave w moves k rows 16 w .. 16 w + 15 of each step (two blocks).
+    {
+        auto dma_step = [&](auto sc) {
+            constexpr int S = decltype(sc)::value;
+            if constexpr (S < SPW) {
+#pragma unroll
+                for (int e = 0; e < 2; ++e) {
+                    const int rr = 16 * wave + 8 * e + lane / 8;
+                    const u32 off = (u32)(64 * S + rr) * (u32)ldb * 2u +
+                                    16u * (u32)((lane % 8) ^ (rr & 7));
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                        Brs, (lds_void *)(sb(sc) + (2 * wave + e) * 1024), 16, (int)off, 0, 0,
+                        0);
+                }
+            }
+        };
+        dma_step(ic<0>{}); dma_step(ic<1>{}); dma_step(ic<2>{}); dma_step(ic<3>{});
+        dma_step(ic<4>{}); dma_step(ic<5>{}); dma_step(ic<6>{}); dma_step(ic<7>{});
+    }
+
+    // ---- multiply -------------------------------------------------------------
+    // Lane (q, u) = (lane / 16, lane % 16): A row u of each 16-row block and B
+    // column u of the wave's 16, k chunk q (16 elements) of the step.
+    const int q = lane >> 4, u = lane & 15;
+    int a_rd[2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c) a_rd[c] = u * 128 + 16 * ((2 * q + c) ^ (u & 7));
+    // transpose reads: lane u of group q addresses k row 16 q + 4 r + u / 4 at
+    // the 8-byte column group u % 4 of the wave's columns
+    int b_rd[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int row = 16 * q + 4 * r + u / 4;
+        const int byte = 32 * wave + 8 * (u % 4);
+        b_rd[r] = row * 128 + 16 * ((byte / 16) ^ (row & 7)) + (byte % 16);
+    }
+    v4i acc_hh[MB], acc_x[MB], acc_ll[MB];
+    int rsum[MB], csum = 0;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+        acc_hh[mb] = v4i{0, 0, 0, 0};
+        acc_x[mb] = v4i{0, 0, 0, 0};
+        acc_ll[mb] = v4i{0, 0, 0, 0};
+        rsum[mb] = 0;
+    }
+    // Step s: wait until this wave's A and B steps up to s have landed (two
+    // DMAs per later step may stay in flight), then for the other waves'.
+    auto mul_step = [&](auto sc) {
+        constexpr int S = decltype(sc)::value;
+        if constexpr (S < SPW) {
+            constexpr int W = 2 * (SPW - 1 - S);
+            __builtin_amdgcn_s_waitcnt((W & 0xf) | ((W >> 4) << 14) | (0x7 << 4) | (0xf << 8));
+            __builtin_amdgcn_s_barrier();
+            if (S < nsteps) {
+                const char *bs = sb(sc);
+                u32 wb[8];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const lds::v2i d = lds::tr16(bs + b_rd[r]);
+                    wb[2 * r] = (u32)d.x;
+                    wb[2 * r + 1] = (u32)d.y;
+                }
+                const v4i bh = v4(hi4(wb[1], wb[0]), hi4(wb[3], wb[2]), hi4(wb[5], wb[4]),
+                                  hi4(wb[7], wb[6]));
+                const v4i bl = v4(lo4(wb[1], wb[0]), lo4(wb[3], wb[2]), lo4(wb[5], wb[4]),
+                                  lo4(wb[7], wb[6]));
+#pragma unroll
+                for (int x = 0; x < 8; ++x) csum = sum2(wb[x], csum);
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb) {
+                    const char *as = sA + S * AST + mb * 2048;
+                    const v4i a0 = *(const v4i *)(as + a_rd[0]);
+                    const v4i a1 = *(const v4i *)(as + a_rd[1]);
+                    const u32 wa[8] = {(u32)a0.x, (u32)a0.y, (u32)a0.z, (u32)a0.w,
+                                       (u32)a1.x, (u32)a1.y, (u32)a1.z, (u32)a1.w};
+                    const v4i ah = v4(hi4(wa[1], wa[0]), hi4(wa[3], wa[2]), hi4(wa[5], wa[4]),
+                                      hi4(wa[7], wa[6]));
+                    const v4i al = v4(lo4(wa[1], wa[0]), lo4(wa[3], wa[2]), lo4(wa[5], wa[4]),
+                                      lo4(wa[7], wa[6]));
+#pragma unroll
+                    for (int x = 0; x < 8; ++x) rsum[mb] = sum2(wa[x], rsum[mb]);
+                    acc_hh[mb] = Mfma<16>::mma(ah, bh, acc_hh[mb]);
+                    acc_x[mb] = Mfma<16>::mma(ah, bl, acc_x[mb]);
+                    acc_ll[mb] = Mfma<16>::mma(al, bl, acc_ll[mb]);
+                    acc_x[mb] = Mfma<16>::mma(al, bh, acc_x[mb]);
+                }
+            }
+        }
+    };
+    mul_step(ic<0>{}); mul_step(ic<1>{}); mul_step(ic<2>{}); mul_step(ic<3>{});
+    mul_step(ic<4>{}); mul_step(ic<5>{}); mul_step(ic<6>{}); mul_step(ic<7>{});
+
+    // ---- into C ---------------------------------------------------------------
+    // Sums over the four k chunks (lanes u, u + 16, u + 32, u + 48).
+    csum += __shfl_xor(csum, 16);
+    csum += __shfl_xor(csum, 32);
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+        rsum[mb] += __shfl_xor(rsum[mb], 16);
+        rsum[mb] += __shfl_xor(rsum[mb], 32);
+    }
+    const u32 kconst = 0u - 16384u * (u32)(64 * nsteps);
+    const int col = j0 + 16 * wave + Mfma<16>::out_col(lane);
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int row = 16 * mb + Mfma<16>::out_row(lane, r);
+            // the row's sum sits in lane (row % 16)
+            const int rs = __shfl(rsum[mb], Mfma<16>::out_row(lane, r));
+            const u32 v = 65536u * (u32)acc_hh[mb][r] + 256u * (u32)acc_x[mb][r] +
+                          (u32)acc_ll[mb][r] + 128u * ((u32)rs + (u32)csum) + kconst;
+            if (col < n && row < mrows) {
+                int32_t *dst = C + (int64_t)(i0 + row) * ldc + col;
+                if constexpr (SPLIT)
+                    atomicAdd(dst, (int)v);
+                else
+                    *dst = (int)((u32)*dst + v);
+            }
+        }
+    }
+}
+
+template <int MB, int SPW>
+const void *pick_lds16(bool split) {
+    return split ? (const void *)igemm_stream_lds16<MB, SPW, true>
+                 : (const void *)igemm_stream_lds16<MB, SPW, false>;
+}
+
 }  // namespace stream
 
 int launch_stream(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const void *A,
@@ -457,6 +677,22 @@ int launch_stream(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const vo
     const int spw = (int)(p.k_chunk / kBK);
     const bool va = p.vec_a != 0, vb = p.vec_b != 0, split = p.split > 1;
     const void *fn;
+    if (p.kernel == K_I16_STREAM) {
+        // int16: 64 columns per workgroup of four waves
+        fn = p.bm == 16 ? (spw == 8 ? stream::pick_lds16<1, 8>(split)
+                                    : spw == 4 ? stream::pick_lds16<1, 4>(split) : nullptr)
+                        : (spw == 8 ? stream::pick_lds16<2, 8>(split)
+                                    : spw == 4 ? stream::pick_lds16<2, 4>(split) : nullptr);
+        if (fn == nullptr) return IGEMM_EINVAL;
+        int mi = (int)m, ni = (int)n, ki = (int)k;
+        int cbs = (int)((n + 63) / 64), rbs = (int)((m + p.bm - 1) / p.bm);
+        void *args[] = {(void *)&A, (void *)&lda, (void *)&B, (void *)&ldb, (void *)&C,
+                        (void *)&ldc, (void *)&mi, (void *)&ni, (void *)&ki, (void *)&cbs,
+                        (void *)&rbs};
+        hipError_t e = hipLaunchKernel(fn, dim3((unsigned)p.grid), dim3(256), args, 0,
+                                       (hipStream_t)stream);
+        return e == hipSuccess ? IGEMM_OK : IGEMM_EHIP;
+    }
     if (va && vb) {
         // the column-per-wave kernel (operands of whole 16-byte rows)
         fn = p.bm == 16 ? stream::pick_lds_spw<1>(spw, split)

@@ -88,4 +88,4 @@ def general_kernels(es):
 
 def restricted(name):
     """Kernels that take only aligned operands and whole k-tiles."""
-    return "direct" in name or "small" in name
+    return "direct" in name or "small" in name or "i16_stream" in name

@@ -623,3 +623,36 @@ def test_planner_rules_for_small_int16_outputs():
     assert (ig.igemm_kernel_name(p["kernel"]), p["split"]) == ("i16_small_64x64", 3)
     p = ig.igemm_conv2d_query_plan(2, d, X=2, W=2, num_cu=256)
     assert (ig.igemm_kernel_name(p["kernel"]), p["split"]) == ("i16_64x64", 5)
+
+
+def test_int16_stream_plan_and_preconditions():
+    """The int16 column-per-wave kernel: 64-column blocks, 16- or 32-row
+    blocks, slices of 8 (or 4) k-steps; operands that break its
+    preconditions are refused when the kernel is asked for."""
+    kid = _kid("i16_stream_32x64")
+    p = ig.igemm_query_plan(2, 8, 4096, 4096, FAKE_A, 4096, FAKE_B, 4096, FAKE_C, 4096,
+                            kernel=kid)
+    assert (p["bm"], p["bn"], p["threads"], p["k_chunk"], p["split"]) == (16, 64, 256, 256, 16)
+    assert p["tiles"] == 64 and p["grid"] == 1024 and p["workspace_bytes"] == 0
+    # the automatic plan takes it for up to 16 rows over wide B when the
+    # operands allow it
+    auto = ig.igemm_query_plan(2, 8, 4096, 4096, FAKE_A, 4096, FAKE_B, 4096, FAKE_C, 4096)
+    assert auto["kernel"] == kid and auto["split"] == 16
+    for (m, lda) in ((32, 4096), (8, 4100)):
+        auto = ig.igemm_query_plan(2, m, 4096, 4096, FAKE_A, lda, FAKE_B, 4096, FAKE_C, 4096)
+        assert auto["kernel"] != kid
+    p = ig.igemm_query_plan(2, 33, 1000, 3008, FAKE_A, 3008, FAKE_B, 1000, FAKE_C, 1000,
+                            kernel=kid, split=6)
+    assert (p["bm"], p["k_chunk"], p["split"], p["tiles"]) == (32, 512, 6, 2 * 16)
+    for (m, n, k, a, lda, b, ldb) in ((8, 4096, 4000, FAKE_A, 4000, FAKE_B, 4096),  # k % 64
+                                      (8, 4092, 4096, FAKE_A, 4096, FAKE_B, 4092),  # n % 8
+                                      (8, 4096, 4096, FAKE_A + 2, 4096, FAKE_B, 4096),
+                                      (8, 4096, 4096, FAKE_A, 4100, FAKE_B, 4096),  # lda % 8
+                                      (8, 4096, 4096, FAKE_A, 4096, FAKE_B + 8, 4096)):
+        with pytest.raises(ig.IgemmError) as e:
+            ig.igemm_query_plan(2, m, n, k, a, lda, b, ldb, FAKE_C, n, kernel=kid)
+        assert e.value.status == ig.IGEMM_EINVAL
+    # an int8 call may not name it
+    with pytest.raises(ig.IgemmError):
+        ig.igemm_query_plan(1, 8, 4096, 4096, FAKE_A, 4096, FAKE_B, 4096, FAKE_C, 4096,
+                            kernel=kid)

@@ -201,6 +201,13 @@ def test_skinny_int8_set(i):
     _check(A, B, C, case.m, case.n, case.k)
 
 
+@pytest.mark.parametrize("i", range(len(workloads.SKINNY_SHAPES)))
+def test_skinny_int16_set(i):
+    case = workloads.WORKLOADS["i16_skinny"].cases[i]
+    A, B, C = workloads.generate(case)
+    _check(A, B, C, case.m, case.n, case.k)
+
+
 def _full_size(wname):
     """Full-size run of a benchmark workload on both paths: with a workspace
     (the packed plan the benchmark times through the tensor wrappers) and

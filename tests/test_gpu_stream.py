@@ -117,3 +117,74 @@ def test_stream_inference_shapes(m, n):
     _, got = gpu_gemm(A, B, C, m, n, k)
     want = oracle_gemm(A, B, C, m, n, k)
     assert np.array_equal(got, want), describe_mismatch(got, want)
+
+
+# ---------------------------------------------------------------------------
+# The int16 column-per-wave kernel (64 columns per workgroup, each element
+# split into its two int8 limbs in registers): A and B 16-byte aligned with
+# rows of whole 16-byte chunks, k a multiple of 64, n a multiple of 8.
+
+def _kid16():
+    ig = _ig()
+    return [i for i in range(ig.igemm_num_kernels())
+            if ig.igemm_kernel_name(i) == "i16_stream_32x64"][0]
+
+
+def _check16(m, n, k, split=-1, pads=(0, 0, 0), seed=0):
+    A, B, C = workloads.random_operands("i16", m, n, k, seed=seed, lda=k + pads[0],
+                                        ldb=n + pads[1], ldc=n + pads[2])
+    _, got = gpu_gemm(A, B, C, m, n, k, kernel=_kid16(), split=split)
+    want = oracle_gemm(A, B, C, m, n, k)
+    assert np.array_equal(got, want), describe_mismatch(got, want)
+    assert np.array_equal(got[:, n:], C[:, n:])
+
+
+# n = 1000: the last of 16 column blocks holds 40 columns; k = 3008: 47
+# k-steps, so slices of 4 or 8 steps end with a short one; rows in one or two
+# 16-row MFMA blocks and several row blocks
+@pytest.mark.parametrize("m", [1, 5, 16, 17, 32, 33, 70])
+@pytest.mark.parametrize("split", [1, 6, 12, -1])
+def test_stream16_workgroup_shapes(m, split):
+    ig = _ig()
+    p = ig.igemm_query_plan(2, m, 1000, 3008, lda=3016, ldb=1008, ldc=1003, kernel=_kid16(),
+                            split=split)
+    assert p["k_chunk"] == (512 if split in (1, 6) else 256) and p["threads"] == 256
+    assert p["grid"] == p["tiles"] * p["split"]
+    _check16(m, 1000, 3008, split=split, pads=(8, 8, 3), seed=10 * m + split + 11)
+
+
+@pytest.mark.parametrize("shape", [(3, 64, 64), (32, 8, 128), (20, 520, 512), (9, 136, 576)])
+def test_stream16_short_k_and_narrow(shape):
+    """One k-step, one workgroup range exactly, a slice of one step, a single
+    8-column group."""
+    m, n, k = shape
+    _check16(m, n, k, seed=sum(shape) + 3)
+
+
+@pytest.mark.parametrize("va,vb", [(-32768, -32768), (-32768, 32767), (32767, 32767),
+                                   (-1, -32768), (255, 256)])
+def test_stream16_extremes(va, vb):
+    """Constant operands at the int16 range ends and at the limb boundaries:
+    C = va * vb * k modulo 2^32, over 140 slices of 512 k."""
+    m, n, k = 17, 200, 71680
+    A = np.full((m, k), va, np.int16)
+    B = np.full((k, n), vb, np.int16)
+    C = np.full((m, n), -3, np.int32)
+    _, got = gpu_gemm(A, B, C, m, n, k, kernel=_kid16())
+    want = (np.int64(va) * vb * k - 3 + (1 << 31)) % (1 << 32) - (1 << 31)
+    assert np.all(got == np.int32(want)), (got.min(), got.max(), want)
+
+
+@pytest.mark.parametrize("m,n", [(1, 4096), (8, 4096), (32, 4096), (1, 11008), (8, 11008),
+                                 (32, 11008)])
+def test_stream16_inference_shapes(m, n):
+    """The weight-streaming shapes with k = 4096, with the kernel asked for
+    and in the automatic plan (which takes it up to 16 rows)."""
+    ig = _ig()
+    k = 4096
+    assert (ig.igemm_query_plan(2, m, n, k)["kernel_name"] == "i16_stream_32x64") == (m <= 16)
+    A, B, C = workloads.random_operands("i16", m, n, k, seed=m + n + 1)
+    want = oracle_gemm(A, B, C, m, n, k)
+    for kernel in (_kid16(), -1):
+        _, got = gpu_gemm(A, B, C, m, n, k, kernel=kernel)
+        assert np.array_equal(got, want), describe_mismatch(got, want)

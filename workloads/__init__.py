@@ -29,6 +29,10 @@ Workloads (all row-major, C is int32):
                    {(4096,4096), (11008,4096)}; A uniform in [-128,127],
                    B = rint(normal(0,20)) clipped to [-128,127], C zero;
                    shape i uses seed 50+i.
+* ``i16_skinny``   the ``i8_skinny`` shapes in int16 (context, not a graded
+                   workload): A uniform in [-32768,32767], B =
+                   rint(normal(0,5120)) clipped to int16, C zero; shape i uses
+                   seed 80+i.
 
 Conventions: numpy ``default_rng(seed)`` (PCG64); draws in the order A, B, C;
 uniform integer ranges include both ends; "normal clipped" rounds with
@@ -216,6 +220,17 @@ WORKLOADS["i16_paper"] = Workload(
     (Case("i16_paper_4096x4096x290", "i16", 4096, 4096, 290, _U16, _U16,
           Dist("uniform", -(1 << 20), 1 << 20), 3),),
     "int16 C+=A.B, (m, n, k) = (4096, 4096, 290), full-range operands, C uniform in +-2^20",
+)
+
+# The same projection shapes with int16 operands (context only, like i16_paper).
+WORKLOADS["i16_skinny"] = Workload(
+    "i16_skinny",
+    tuple(
+        Case(f"i16_skinny_{i}_{m}x{n}x{k}", "i16", m, n, k, _U16,
+             Dist("normal_clip", I16_MIN, I16_MAX, 5120.0), _ZERO, 80 + i)
+        for i, (m, n, k) in enumerate(SKINNY_SHAPES)
+    ),
+    "int16 skinny GEMMs shaped like 7B-class decoder projections",
 )
 
 ORDER: List[str] = ["i16_256", "i16_4096", "i8_8192", "i16_conv", "i8_skinny"]
