@@ -251,10 +251,27 @@ static bool stream_shape(int64_t m, int64_t n, int64_t k, int64_t lda, int64_t l
         // 4096 (us, 4 / 8 / 16 steps): 1 x 4096 4.76 / 4.92 / 5.82, 32 x 4096
         // 8.98 / 7.34 / 7.79, 1 x 11008 9.94 / 10.16 / 12.79, 32 x 11008
         // 19.07 / 14.76 / 16.63.
-        const int64_t want = split > 0 ? cdiv(ksteps, split) : 8;
+        int64_t want = split > 0 ? cdiv(ksteps, split) : 8;
+        // 17 to 32 rows over 64 to 128 column blocks: as many k slices as
+        // give one workgroup per compute unit (two for 11008 columns), each a
+        // long range through the ring variant, so that C takes two atomic
+        // adds rather than eight (32 x 11008 x 4096: 12.4 us against 14.4 us
+        // with slices of 8 steps; three slices, 258 workgroups on 256 units,
+        // 17.0 us).
+        const int64_t cbs = cdiv(n, 128), per_unit = num_cu / cbs;
+        if (split <= 0 && bm == 32 && cbs >= 64 && cbs <= 128 && per_unit >= 1 &&
+            cdiv(ksteps, per_unit) > 16)
+            want = cdiv(ksteps, per_unit);
         while (spw < want && spw < 16) spw *= 2;
+        // Longer ranges (more than 16 steps) take the ring variant, which
+        // streams any number of steps through eight LDS stages (measured
+        // with k = 4096, slices of 64, 32 or 22 steps against 8: slower on
+        // the 4096-column shapes, whose 32 column blocks then leave most
+        // compute units idle, and within 5 % on 1 and 8 x 11008).
+        if (want > 16) spw = want;
         // (This kernel with two 16-row blocks took 7.44 us on 32 x 4096 x 4096.)
-        if (spw * kBK * ldb + 256 >= 0x7fff0000 || 32 * lda + spw * kBK >= 0x7fff0000)
+        if (ldb >= (0x7fff0000 - 256) / (spw * kBK) || lda >= 0x7fff0000 / 64 ||
+            32 * lda + spw * kBK >= 0x7fff0000)
             return false;
         out->bm = bm;
         out->threads = 512;

@@ -451,6 +451,186 @@ const void *pick_lds_spw(int spw, bool split) {
 
 
 // ---------------------------------------------------------------------------
+// Ring variant of the column-per-wave kernel for long k ranges per workgroup
+// (few k slices, so that C receives few atomic adds): the same LDS rows,
+// swizzles, transpose reads and per-wave columns, but B and A move through
+// a ring of R stages (one LDS array per stage, so that the compiler tells the
+// DMA into each apart) instead of all being resident at once:
+//   * R - 1 steps are in flight ahead of the one being multiplied; at step s
+//     a wave waits for its own DMA of step s, the barrier then also covers
+//     the other waves' and their reads of step s - 1, whose stage then takes
+//     step s + R - 1;
+//   * every wave moves one 1 KB block of B (8 rows) and 128 MB bytes of A
+//     (2 MB rows, 8 MB lanes) per step, both by DMA;
+//   * the workgroup's k range is `spw` steps (any count); steps past k read
+//     zeros from B as in the kernel above.
+template <int MB, int R, bool SPLIT>
+__global__ void __launch_bounds__(512)
+igemm_stream_ring(const int8_t *__restrict__ A, int64_t lda, const int8_t *__restrict__ B,
+                  int64_t ldb, int32_t *__restrict__ C, int64_t ldc, int m, int n, int k,
+                  int colblocks, int rowblocks, int spw) {
+    constexpr int BST = 64 * 128;      // B bytes per step
+    constexpr int AST = MB * 16 * 64;  // A bytes per step
+    static_assert(R == 4 || R == 8, "ring stages");
+    // (one array per stage, B then A: the compiler tracks a limited number of
+    // DMA destinations, and loses the per-stage waits beyond that)
+#define IGEMM_RS(i) __shared__ __attribute__((aligned(16))) char rS##i[R > i ? BST + AST : 16]
+    IGEMM_RS(0); IGEMM_RS(1); IGEMM_RS(2); IGEMM_RS(3);
+    IGEMM_RS(4); IGEMM_RS(5); IGEMM_RS(6); IGEMM_RS(7);
+#undef IGEMM_RS
+    auto sb = [&](auto sc) -> char * {
+        constexpr int S = decltype(sc)::value;
+        if constexpr (S == 0) return rS0;
+        else if constexpr (S == 1) return rS1;
+        else if constexpr (S == 2) return rS2;
+        else if constexpr (S == 3) return rS3;
+        else if constexpr (S == 4) return rS4;
+        else if constexpr (S == 5) return rS5;
+        else if constexpr (S == 6) return rS6;
+        else return rS7;
+    };
+    auto sa = [&](auto sc) -> char * { return sb(sc) + BST; };
+    asm volatile("" ::"s"(A), "s"(lda), "s"(B), "s"(ldb), "s"(C), "s"(ldc), "s"(m), "s"(n),
+                 "s"(k), "s"(colblocks), "s"(rowblocks), "s"(spw));
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const unsigned t = blockIdx.x / (unsigned)colblocks;
+    const int cb = (int)(blockIdx.x - t * (unsigned)colblocks);
+    const int rb = (int)(t % (unsigned)rowblocks);
+    const int ks = (int)(t / (unsigned)rowblocks);
+    const int j0 = cb * 128, i0 = rb * 16 * MB, kbeg = ks * spw * 64;
+    const int mrows = min(m - i0, 16 * MB);
+    const int nsteps = min(spw, (k - kbeg + 63) / 64);  // >= 1 (grid)
+
+    const int8_t *bw = B + (int64_t)kbeg * ldb + j0;
+    const int64_t b_ext = (int64_t)(k - 1 - kbeg) * ldb + (n - j0);
+    const __amdgpu_buffer_rsrc_t Brs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)bw, 0, (int)min((b_ext + 3) & ~(int64_t)3, (int64_t)0x7ffffff0), 0x00020000);
+    const int8_t *aw = A + (int64_t)i0 * lda + kbeg;
+    const int64_t a_ext = (int64_t)(mrows - 1) * lda + (k - kbeg);
+    const __amdgpu_buffer_rsrc_t Ars = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)aw, 0, (int)min((a_ext + 3) & ~(int64_t)3, (int64_t)0x7ffffff0), 0x00020000);
+
+    // B: wave w moves rows 8 w .. 8 w + 7 of a step (lane i: row 8 w + i / 8,
+    // physical chunk i % 8, logical (i % 8) ^ (row & 7)). A: wave w moves rows
+    // 2 MB w .. 2 MB w + 2 MB - 1 (lane i < 8 MB: row 2 MB w + i / 4, physical
+    // chunk i % 4, logical (i % 4) ^ swz(row)). Both by DMA written as inline
+    // assembly: the compiler's own wait placement does not follow loads whose
+    // data is used a loop iteration later and adds early waits before the LDS
+    // reads, so the kernel keeps the count itself -- each wave issues exactly
+    // two DMAs per step (the A one with its first 8 MB lanes active), and a
+    // step waits until at most the later steps' are outstanding. Steps past
+    // the workgroup's range are issued too, at an offset beyond both
+    // resources (zeros, no memory traffic). The kernel makes no other use of
+    // M0, which holds each DMA's LDS address.
+    const int brow = 8 * wave + lane / 8;
+    const u32 boff = (u32)brow * (u32)ldb + 16u * (u32)((lane % 8) ^ (brow & 7));
+    const int arow = 2 * MB * wave + lane / 4;
+    const u32 aoff = (u32)arow * (u32)lda + 16u * (u32)((lane % 4) ^ swz(arow));
+    auto lds_addr = [](const char *p) -> u32 {
+        return (u32)(uintptr_t)(const __attribute__((address_space(3))) char *)p;
+    };
+    auto dma = [&](auto sc, int s) {
+        const bool in = s < nsteps;
+        const u32 bo = in ? boff + (u32)(64 * s) * (u32)ldb : 0x80000000u;
+        const u32 bl = lds_addr(sb(sc) + wave * 1024);
+        const __amdgpu_buffer_rsrc_t br = Brs;
+        asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+                     ::"v"(bo), "s"(br), "s"(bl)
+                     : "memory");
+        const u32 ao = in ? aoff + (u32)(64 * s) : 0x80000000u;
+        const u32 al = lds_addr(sa(sc) + wave * 128 * MB);
+        const __amdgpu_buffer_rsrc_t ar = Ars;
+        if (lane < 8 * MB)
+            asm volatile(
+                "s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+                ::"v"(ao), "s"(ar), "s"(al)
+                : "memory");
+    };
+
+    const int q = lane >> 4, u = lane & 15;
+    int b_rd[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int row = 16 * q + 8 * h + u / 2;
+        b_rd[h] = row * 128 + 16 * (wave ^ (row & 7)) + 8 * (u % 2);
+    }
+    const int a_rd = u * 64 + 16 * (q ^ swz(u));
+    v4i acc[MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[mb] = v4i{0, 0, 0, 0};
+
+    // prologue: steps 0 .. R - 2 into stages 0 .. R - 2
+    dma(ic<0>{}, 0);
+    dma(ic<1>{}, 1);
+    dma(ic<2>{}, 2);
+    if constexpr (R == 8) {
+        dma(ic<3>{}, 3);
+        dma(ic<4>{}, 4);
+        dma(ic<5>{}, 5);
+        dma(ic<6>{}, 6);
+    }
+    // step s (stage S = s % R): the R - 2 later steps' DMAs may stay in
+    // flight; the barrier then covers every wave's DMAs of step s and their
+    // reads of step s - 1, whose stage takes step s + R - 1.
+    auto step = [&](auto sc, int s) {
+        constexpr int S = decltype(sc)::value;
+        constexpr int W = 2 * (R - 2);
+        __builtin_amdgcn_s_waitcnt((W & 0xf) | ((W >> 4) << 14) | (0x7 << 4) | (0xf << 8));
+        __builtin_amdgcn_s_barrier();
+        dma(ic<(S + R - 1) % R>{}, s + R - 1);
+        const char *bs = sb(sc);
+        const v2i_t b0 = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+            (__attribute__((address_space(3))) v2i_t *)(lds_void *)(bs + b_rd[0]));
+        const v2i_t b1 = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+            (__attribute__((address_space(3))) v2i_t *)(lds_void *)(bs + b_rd[1]));
+        const v4i b = v4i{b0.x, b0.y, b1.x, b1.y};
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+            const v4i a = *(const v4i *)(sa(sc) + mb * 1024 + a_rd);
+            acc[mb] = Mfma<16>::mma(a, b, acc[mb]);
+        }
+    };
+    for (int s0 = 0; s0 < nsteps; s0 += R) {
+        step(ic<0>{}, s0);
+        if (s0 + 1 < nsteps) step(ic<1>{}, s0 + 1);
+        if (s0 + 2 < nsteps) step(ic<2>{}, s0 + 2);
+        if (s0 + 3 < nsteps) step(ic<3>{}, s0 + 3);
+        if constexpr (R == 8) {
+            if (s0 + 4 < nsteps) step(ic<4>{}, s0 + 4);
+            if (s0 + 5 < nsteps) step(ic<5>{}, s0 + 5);
+            if (s0 + 6 < nsteps) step(ic<6>{}, s0 + 6);
+            if (s0 + 7 < nsteps) step(ic<7>{}, s0 + 7);
+        }
+    }
+
+    const int col = j0 + 16 * wave + Mfma<16>::out_col(lane);
+    if (col < n) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = 16 * mb + Mfma<16>::out_row(lane, r);
+                if (row < mrows) {
+                    int32_t *dst = C + (int64_t)(i0 + row) * ldc + col;
+                    if constexpr (SPLIT)
+                        atomicAdd(dst, acc[mb][r]);
+                    else
+                        *dst = (int)((u32)*dst + (u32)acc[mb][r]);
+                }
+            }
+        }
+    }
+}
+
+template <int MB>
+const void *pick_ring(bool split) {
+    return split ? (const void *)igemm_stream_ring<MB, 8, true>
+                 : (const void *)igemm_stream_ring<MB, 8, false>;
+}
+
+
+// ---------------------------------------------------------------------------
 // int16 column-per-wave variant (few-row int16 products whose B, the weights,
 // dominates the traffic). As in the int8 kernel above, B moves to LDS once by
 // DMA and each wave owns 16 columns for the workgroup's whole k range; here
@@ -690,6 +870,18 @@ int launch_stream(const igemm_plan &p, int64_t m, int64_t n, int64_t k, const vo
                         (void *)&ldc, (void *)&mi, (void *)&ni, (void *)&ki, (void *)&cbs,
                         (void *)&rbs};
         hipError_t e = hipLaunchKernel(fn, dim3((unsigned)p.grid), dim3(256), args, 0,
+                                       (hipStream_t)stream);
+        return e == hipSuccess ? IGEMM_OK : IGEMM_EHIP;
+    }
+    if (va && vb && spw > 16) {
+        // the column-per-wave kernel's ring variant (more than 16 steps)
+        fn = p.bm == 16 ? stream::pick_ring<1>(split) : stream::pick_ring<2>(split);
+        int mi = (int)m, ni = (int)n, ki = (int)k, si = spw;
+        int cbs = (int)((n + 127) / 128), rbs = (int)((m + p.bm - 1) / p.bm);
+        void *args[] = {(void *)&A, (void *)&lda, (void *)&B, (void *)&ldb, (void *)&C,
+                        (void *)&ldc, (void *)&mi, (void *)&ni, (void *)&ki, (void *)&cbs,
+                        (void *)&rbs, (void *)&si};
+        hipError_t e = hipLaunchKernel(fn, dim3((unsigned)p.grid), dim3(512), args, 0,
                                        (hipStream_t)stream);
         return e == hipSuccess ? IGEMM_OK : IGEMM_EHIP;
     }

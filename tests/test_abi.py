@@ -656,3 +656,21 @@ def test_int16_stream_plan_and_preconditions():
     with pytest.raises(ig.IgemmError):
         ig.igemm_query_plan(1, 8, 4096, 4096, FAKE_A, 4096, FAKE_B, 4096, FAKE_C, 4096,
                             kernel=kid)
+
+
+def test_int8_stream_ring_plans():
+    """17 to 32 int8 rows over 64 to 128 column blocks of B: one k slice per
+    compute unit's share (two for 11008 columns), each a long range through
+    the ring variant; an explicit split asking for more than 16 k-steps per
+    workgroup takes it too."""
+    for m in (17, 32):
+        p = ig.igemm_query_plan(1, m, 11008, 4096, num_cu=256)
+        assert p["kernel_name"] == "i8_stream_32x128"
+        assert (p["split"], p["k_chunk"], p["vec_b"], p["grid"]) == (2, 2048, 1, 2 * 86)
+    for (m, n) in ((8, 11008), (32, 4096), (32, 20000)):
+        p = ig.igemm_query_plan(1, m, n, 4096, num_cu=256)
+        assert p["k_chunk"] <= 1024, (m, n)
+    p = ig.igemm_query_plan(1, 5, 1008, 3000, lda=3008, kernel=_kid("i8_stream_32x128"),
+                            split=2)
+    assert (p["split"], p["k_chunk"], p["vec_b"]) == (2, 24 * 64, 1)
+

@@ -42,6 +42,15 @@ def _kernel_shapes(name):
             (1, bn - 8, 64 * 9),               # one row, a short last slice
             (bm - 1, 8, 256),                  # eight columns
         ]
+    if "i16_stream" in name:
+        # k a multiple of 64, n a multiple of 8 columns; m, n ragged
+        return [
+            (bm, bn, 64),                      # exactly one block, one k-step
+            (bm + 3, bn + 8, 320),             # ragged m and n, five k-steps
+            (2 * bm - 1, 2 * bn + 8, 1024),    # several blocks, k sliced
+            (1, bn - 8, 64 * 9),               # one row, a short last slice
+            (bm - 1, 8, 256),                  # eight columns
+        ]
     if "direct" in name:
         # k a multiple of 256, n a multiple of 16 columns; m, n ragged
         return [

@@ -54,8 +54,42 @@ def test_stream_lds_workgroup_shapes(m, split):
     # register kernel's 16-row blocks instead)
     lds = not (split == -1 and m > 16)
     assert p["vec_a"] == 1 and p["vec_b"] == (1 if lds else 0) and p["threads"] == 512
-    assert p["k_chunk"] in ((256, 512, 1024) if lds else (1024,))
+    # (one slice asks for all 47 k-steps in one workgroup: the ring variant)
+    assert p["k_chunk"] in ((256, 512, 1024, 3008) if lds else (1024,))
     _check(m, 1008, 3000, split=split, pads=(8, 0, 0), seed=10 * m + split + 7)
+
+
+# The ring variant of the column-per-wave kernel: more than 16 k-steps per
+# workgroup through eight LDS stages (47 steps in one slice, 24 + 23 in two),
+# k ending inside a step, a partial column block.
+@pytest.mark.parametrize("m", [1, 9, 16, 17, 32, 70])
+@pytest.mark.parametrize("split", [1, 2])
+def test_stream_ring_workgroup_shapes(m, split):
+    ig = _ig()
+    p = ig.igemm_query_plan(1, m, 1008, 3000, lda=3008, ldb=1008, ldc=1008, kernel=_kid(),
+                            split=split)
+    assert p["vec_b"] == 1 and p["k_chunk"] == 64 * -(-47 // split) and p["split"] == split
+    _check(m, 1008, 3000, split=split, pads=(8, 0, 0), seed=10 * m + split + 9)
+
+
+@pytest.mark.parametrize("shape,split", [((5, 128, 1088), 1), ((32, 2064, 8192), 2),
+                                         ((3, 4096, 4096), 3), ((24, 640, 1216), 1)])
+def test_stream_ring_ranges(shape, split):
+    """Step counts that are and are not multiples of the eight stages (17,
+    64, 22, 19 steps), plain read-add-write and atomic slices."""
+    m, n, k = shape
+    _check(m, n, k, split=split, seed=sum(shape) + split)
+
+
+@pytest.mark.parametrize("value", [-128, 127])
+def test_stream_ring_extremes_long_k(value):
+    """One slice of 1094 k-steps through the ring."""
+    m, n, k = 9, 304, 70000
+    A = np.full((m, k), value, np.int8)
+    B = np.full((k, n), value, np.int8)
+    C = np.zeros((m, n), np.int32)
+    _, got = gpu_gemm(A, B, C, m, n, k, kernel=_kid(), split=1)
+    assert np.all(got == np.int32(value * value * k))
 
 
 @pytest.mark.parametrize("shape,pads", [((5, 304, 200), (0, 0, 0)), ((32, 144, 64), (16, 16, 1)),
