@@ -253,14 +253,16 @@ static bool stream_shape(int64_t m, int64_t n, int64_t k, int64_t lda, int64_t l
         // 19.07 / 14.76 / 16.63.
         int64_t want = split > 0 ? cdiv(ksteps, split) : 8;
         // 17 to 32 rows over 64 to 128 column blocks: as many k slices as
-        // give one workgroup per compute unit (two for 11008 columns), each a
-        // long range through the ring variant, so that C takes two atomic
-        // adds rather than eight (32 x 11008 x 4096: 12.4 us against 14.4 us
-        // with slices of 8 steps; three slices, 258 workgroups on 256 units,
-        // 17.0 us).
+        // give one workgroup per compute unit (two for 11008 columns, four
+        // for 8192), each a long range (through the ring variant beyond 16
+        // steps), so that C takes fewer atomic adds (32 x 11008 x 4096:
+        // 12.4 us with two slices against 14.4 us with eight slices of 8
+        // steps; three slices, 258 workgroups on 256 units, 17.0 us;
+        // 32 x 8192 x 4096: 10.7 us with four slices of 16 steps against
+        // 11.5 us with eight).
         const int64_t cbs = cdiv(n, 128), per_unit = num_cu / cbs;
         if (split <= 0 && bm == 32 && cbs >= 64 && cbs <= 128 && per_unit >= 1 &&
-            cdiv(ksteps, per_unit) > 16)
+            cdiv(ksteps, per_unit) > 8)
             want = cdiv(ksteps, per_unit);
         while (spw < want && spw < 16) spw *= 2;
         // Longer ranges (more than 16 steps) take the ring variant, which

@@ -667,6 +667,9 @@ def test_int8_stream_ring_plans():
         p = ig.igemm_query_plan(1, m, 11008, 4096, num_cu=256)
         assert p["kernel_name"] == "i8_stream_32x128"
         assert (p["split"], p["k_chunk"], p["vec_b"], p["grid"]) == (2, 2048, 1, 2 * 86)
+    # 8192 columns: four slices of 16 steps (all resident, no ring)
+    p = ig.igemm_query_plan(1, 32, 8192, 4096, num_cu=256)
+    assert (p["split"], p["k_chunk"], p["vec_b"], p["grid"]) == (4, 1024, 1, 4 * 64)
     for (m, n) in ((8, 11008), (32, 4096), (32, 20000)):
         p = ig.igemm_query_plan(1, m, n, 4096, num_cu=256)
         assert p["k_chunk"] <= 1024, (m, n)
