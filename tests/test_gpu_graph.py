@@ -12,10 +12,15 @@ pytestmark = pytest.mark.gpu
 @pytest.mark.parametrize("dt,shape,split", [("i16", (130, 260, 300), -1), ("i8", (40, 300, 700), 5),
                                             ("i16", (256, 256, 256), 1),
                                             ("i16", (1100, 1030, 1200), -1),
-                                            ("i8", (1030, 1100, 1300), -1)])
+                                            ("i8", (1030, 1100, 1300), -1),
+                                            ("i8", (32, 11008, 4096), -1),
+                                            ("i16", (8, 4096, 4096), -1)])
 def test_graph_replays_match_eager(dt, shape, split):
-    """The last two shapes take the packed path; its workspace comes from
-    torch's caching allocator, which is capture-aware."""
+    """(1100, 1030, 1200) and (1030, 1100, 1300) take the packed path; its
+    workspace comes from torch's caching allocator, which is capture-aware.
+    (32, 11008, 4096) int8 takes the streaming kernel's ring variant (two
+    slices of 32 k-steps), (8, 4096, 4096) int16 the int16 streaming
+    kernel."""
     import torch
     import paper_2302_07594_amd as ig
     m, n, k = shape
