@@ -1,9 +1,11 @@
-"""GPU parity of the int8 streaming kernels (few rows of A, B streamed once)
-against the CPU oracle, bit-exact: the column-per-wave kernel (operands with
-rows of whole 16-byte chunks; 4, 8 or 16 k-steps per workgroup in LDS) and
-the register kernel (other operands), one and two 16-row MFMA blocks,
-several row blocks, single-slice (read-add-write) and multi-slice (atomic)
-plans, k tails, misaligned operands."""
+"""GPU parity of the streaming kernels (few rows of A, B streamed once)
+against the CPU oracle, bit-exact. int8: the column-per-wave kernel (operands
+with rows of whole 16-byte chunks; 4, 8 or 16 k-steps per workgroup in LDS),
+its ring variant (any number of k-steps through eight LDS stages) and the
+register kernel (other operands), one and two 16-row MFMA blocks, several row
+blocks, single-slice (read-add-write) and multi-slice (atomic) plans, k tails,
+misaligned operands. int16: the column-per-wave kernel with the limb split in
+registers (ragged columns, short last slices, range and limb extremes)."""
 import numpy as np
 import pytest
 
